@@ -1,0 +1,180 @@
+/*
+ * huge2.h -- C ABI of libhuge2: phase-decomposed transposed and dilated 2-D
+ * convolution for AMD Instinct MI355X (gfx950), after HUGE^2 (Shi, Xu,
+ * Yuan, Zhu, arXiv 1907.11210).
+ *
+ * What is computed
+ *   conv2d_transpose: the transposed (fractionally strided) convolution of
+ *     section 2.1.1 / Algorithm 1,
+ *       y[n,k,oh,ow] = bias[k] + sum_{c,i,j,m,q} x[n,c,i,j] * w[c,k,m,q]
+ *                      over oh = i*stride_h - pad_h + m*dil_h,
+ *                           ow = j*stride_w - pad_w + q*dil_w,
+ *     with oh in [0, h_out), h_out = (h-1)*stride_h - 2*pad_h
+ *     + dil_h*(r-1) + out_pad_h + 1 (same for w).
+ *   conv2d_dilated: the dilated convolution of section 2.1.1 / Algorithm 2
+ *     (cross-correlation, zero padding),
+ *       y[n,k,oh,ow] = bias[k] + sum_{c,m,q} x[n,c, oh*stride_h - pad_h + m*dil_h,
+ *                                              ow*stride_w - pad_w + q*dil_w] * w[k,c,m,q],
+ *     h_out = floor((h + 2*pad_h - dil_h*(r-1) - 1)/stride_h) + 1.
+ *
+ * How (section 3): the kernel is decomposed into stride_h*stride_w phase
+ * sub-kernels (section 3.1, Eq. 1-4); each phase is a dense convolution over
+ * the un-inflated input, untangled into per-tap 1x1 convolutions that
+ * accumulate as one implicit GEMM (section 3.2.1); the result is written
+ * straight to the phase's disjoint, interleaved output positions (the
+ * scatter of section 3.1), so no inserted zero is multiplied and no output
+ * element is written twice.  A stride-1 dilated convolution is split the
+ * same way into dil_h*dil_w phase views of the input (section 3.2.2).
+ *
+ * Conventions common to every entry point
+ *   - All tensor pointers are DEVICE pointers owned by the caller, contiguous
+ *     in the stated logical order, 16-byte aligned.  x and y must not alias.
+ *   - Layout (HUGE2_NCHW or HUGE2_NHWC) applies to x and y.  Weights are
+ *     always in the framework order given per entry point, whatever the
+ *     activation layout.
+ *   - dtype HUGE2_F32: x, w, y are float; MFMA in fp32.  HUGE2_BF16: x, w, y
+ *     are bfloat16; products accumulate in fp32; y is rounded to nearest
+ *     even.  bias is always float (nullable).
+ *   - hip_stream is a hipStream_t (NULL = the default stream).  Work is
+ *     enqueued asynchronously; the call returns after enqueue.
+ *   - Every argument is validated before any HIP call.  On an error nothing
+ *     is enqueued and y is untouched.  No C++ exception crosses the ABI.
+ *   - Results for one plan are deterministic (fixed summation order, no
+ *     atomics).
+ */
+#ifndef HUGE2_H
+#define HUGE2_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HUGE2_OK = 0,
+  HUGE2_ERR_INVALID_ARG = 1, /* bad pointer, size, or descriptor field */
+  HUGE2_ERR_UNSUPPORTED = 2, /* valid, but not implemented (e.g. dilated with stride > 1 and
+                                out_pad != 0) */
+  HUGE2_ERR_ALLOC = 3,       /* device or host allocation failed */
+  HUGE2_ERR_HIP = 4          /* a HIP runtime call or kernel launch failed */
+} huge2_status;
+
+typedef enum { HUGE2_F32 = 0, HUGE2_BF16 = 1 } huge2_dtype;
+typedef enum { HUGE2_NCHW = 0, HUGE2_NHWC = 1 } huge2_layout;
+
+/* Problem descriptor: the paper's Conv2DTranspose(I, K, O, s_m, s_n) and
+ * Conv2DDilated(I, K, O, s_m, s_n) (Algorithms 1-2), extended with batch,
+ * padding, output padding and both stride and dilation per axis. */
+typedef struct {
+  int32_t n, c_in, h, w;        /* input: batch, channels, height, width (all >= 1) */
+  int32_t c_out, r, s;          /* output channels; kernel height r and width s (>= 1) */
+  int32_t stride_h, stride_w;   /* >= 1 (the paper's s_m, s_n for the transposed conv) */
+  int32_t pad_h, pad_w;         /* >= 0, symmetric */
+  int32_t out_pad_h, out_pad_w; /* transposed only: 0 <= out_pad < max(stride, dil); 0 for dilated */
+  int32_t dil_h, dil_w;         /* >= 1 (the paper's s_m, s_n for the dilated conv) */
+  int32_t layout;               /* huge2_layout */
+  int32_t dtype;                /* huge2_dtype */
+} huge2_conv_desc;
+
+typedef struct huge2_plan huge2_plan; /* opaque */
+
+/* Human-readable name of a status code (static storage; never NULL). */
+const char* huge2_status_str(huge2_status status);
+
+/* Output height/width of the operation described by desc.
+ * transposed = 1: the transposed conv; 0: the dilated/strided conv.
+ * Host only, no HIP call.  INVALID_ARG if the descriptor is invalid or the
+ * output would be empty. */
+huge2_status huge2_output_shape(const huge2_conv_desc* desc, int32_t transposed, int32_t* h_out,
+                                int32_t* w_out);
+
+/* Build a reusable plan (the decomposition of section 3.1 done once per
+ * layer): enumerates the phases, their kernel taps and border classes on the
+ * host, allocates the plan's device buffers (packed weights and the work
+ * list), copies the work list and runs on hip_stream the kernel that gathers
+ * w into per-tap, K-contiguous sub-kernel blocks (section 3.2.1: the N x C
+ * matrix for each kernel position), then waits for hip_stream.
+ *   transposed = 1: w is [c_in][c_out][r][s] (the paper's C x N x R x S,
+ *                   section 4.2; PyTorch ConvTranspose2d order).
+ *   transposed = 0: w is [c_out][c_in][r][s] (PyTorch Conv2d order).
+ * w is read only by work enqueued on hip_stream: it may be freed or changed
+ * once that work has completed.  *out receives the plan (NULL on error).
+ * Errors: INVALID_ARG (descriptor, null out/w), UNSUPPORTED, ALLOC, HIP. */
+huge2_status huge2_plan_create(huge2_plan** out, const huge2_conv_desc* desc, int32_t transposed,
+                               const void* w, void* hip_stream);
+
+/* Run a plan: y = op(x) (+ bias).  x and y are laid out per the plan's
+ * descriptor; bias is NULL or [c_out] float.  Enqueues exactly one kernel
+ * (the phase GEMM, which gathers x in either layout itself) on hip_stream.
+ * A plan is immutable once created; concurrent executes of one plan on
+ * different streams are safe.  Errors: INVALID_ARG (null plan/x/y, x == y),
+ * HIP (launch failure). */
+huge2_status huge2_plan_execute(const huge2_plan* plan, const void* x, const float* bias, void* y,
+                                void* hip_stream);
+
+/* Release a plan and its device buffers.  Waits for the device to finish
+ * work that may still use them.  NULL is accepted.  Errors: HIP. */
+huge2_status huge2_plan_destroy(huge2_plan* plan);
+
+/* One-shot transposed convolution (Algorithm 1 semantics, computed by the
+ * phase decomposition): plan_create + plan_execute + stream-ordered release
+ * of the plan's buffers.  w is [c_in][c_out][r][s].  desc->out_pad_* obey
+ * 0 <= out_pad < max(stride, dil).  Errors as plan_create/plan_execute. */
+huge2_status huge2_conv2d_transpose(const huge2_conv_desc* desc, const void* x, const void* w,
+                                    const float* bias, void* y, void* hip_stream);
+
+/* One-shot dilated convolution (Algorithm 2 semantics; stride 1 is computed
+ * by dil_h x dil_w phase views, stride > 1 by the same GEMM core over a
+ * direct gather).  w is [c_out][c_in][r][s]; desc->out_pad_* must be 0. */
+huge2_status huge2_conv2d_dilated(const huge2_conv_desc* desc, const void* x, const void* w,
+                                  const float* bias, void* y, void* hip_stream);
+
+/* ---- introspection (host only, no HIP call) ---------------------------- */
+
+/* One rectangle of a box of phases with a constant set of kernel taps.
+ * Output positions: oh = phase_h + out_step_h * qh for every phase_h in
+ * [phase0_h, phase0_h + nphase_h) and qh in [q0_h, q0_h + qn_h), likewise
+ * ow; every image n in [0, desc.n).  Tap t of the segment (t in
+ * [tap_begin, tap_begin + tap_count) of the tap list) reads input row
+ *   ih = in0_h + in_dphase_h * (phase_h - phase0_h) + in_step_h * qh + taps[t].off_h
+ * (likewise iw) with kernel tap (taps[t].kh, taps[t].kw).  Transposed convs
+ * use one phase per segment (each phase has its own sub-kernel); stride-1
+ * dilated convs group the phase views that share a shape.  A segment with
+ * tap_count 0 is an output region no input reaches (it holds the bias). */
+typedef struct {
+  int32_t phase0_h, phase0_w, nphase_h, nphase_w;
+  int32_t out_step_h, out_step_w;
+  int32_t q0_h, q0_w, qn_h, qn_w;
+  int32_t in0_h, in0_w, in_dphase_h, in_dphase_w, in_step_h, in_step_w;
+  int32_t tap_begin, tap_count;
+} huge2_segment;
+
+typedef struct {
+  int32_t kh, kw;       /* kernel tap */
+  int32_t off_h, off_w; /* input offset added to in_base + in_step * q */
+} huge2_tap;
+
+/* The decomposition a plan for desc would use.  Fills up to seg_cap
+ * segments and tap_cap taps; *n_segs / *n_taps receive the full counts (call
+ * with caps 0 to size the arrays).  class_split: 1 splits every phase into
+ * border classes, so that each segment reads only in-range inputs; 0 keeps
+ * one segment per phase group with all of its taps (out-of-range reads then
+ * contribute zero); 2 is the plan's own choice (per phase group, whichever
+ * issues fewer tile-taps for the plan's tile height). */
+huge2_status huge2_plan_describe(const huge2_conv_desc* desc, int32_t transposed,
+                                 int32_t class_split, huge2_segment* segs, int32_t seg_cap,
+                                 int32_t* n_segs, huge2_tap* taps, int32_t tap_cap,
+                                 int32_t* n_taps);
+
+/* Counts for a descriptor: structural non-zero multiply-adds (products of an
+ * input element and a kernel tap that land on an output element: no inserted
+ * zero, no padding, no cropped position) and the multiply-adds the plan's
+ * GEMM tiles actually issue (including tile padding). */
+huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, int64_t* nonzero_macs,
+                             int64_t* issued_macs);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HUGE2_H */

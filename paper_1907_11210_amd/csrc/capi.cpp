@@ -1,0 +1,390 @@
+// capi.cpp -- the C ABI of libhuge2 (declared in include/huge2.h).
+//
+// plan_create runs the host-side decomposition (plan.cpp), lays the
+// segments, taps and GEMM work list out for the device, and packs the
+// weights; plan_execute enqueues the phase GEMM (one kernel).  No exception
+// crosses the ABI.
+#include <hip/hip_runtime.h>
+
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "huge2.h"
+#include "kernels.hpp"
+#include "plan.hpp"
+
+using namespace huge2;
+
+struct huge2_plan {
+  huge2_conv_desc desc;
+  int transposed;
+  int ho, wo;
+  int cfg;
+  int in_mode;
+  int cin_pad, cout_pad;
+  int n_works;
+  void* wp;    // packed weights
+  void* meta;  // segments, taps, work list
+  SegDev* d_segs;
+  TapDev* d_taps;
+  WorkDev* d_works;
+  bool stream_ordered;  // buffers came from hipMallocAsync on alloc_stream
+  hipStream_t alloc_stream;
+  int64_t nonzero_macs, issued_macs;
+};
+
+namespace {
+
+int elem_size(int dtype) { return dtype == HUGE2_BF16 ? 2 : 4; }
+int round_up(int v, int m) { return (v + m - 1) / m * m; }
+
+// Fault injection for host-side tests of the error paths: HUGE2_FAULT=alloc
+// makes the next device allocation fail, HUGE2_FAULT=launch the next launch.
+bool fault(const char* what) {
+  const char* f = std::getenv("HUGE2_FAULT");
+  return f && std::strcmp(f, what) == 0;
+}
+
+int env_int(const char* name, int dflt) {
+  const char* v = std::getenv(name);
+  if (!v || !*v) return dflt;
+  return std::atoi(v);
+}
+
+// Tile choice: output channels <= 32 take the narrow tile; otherwise
+// 128x128, or 64x128 when 128x128 would leave most of the 256 CUs idle.
+int choose_cfg(const huge2_conv_desc& d, bool transposed, int class_split) {
+  int forced = env_int("HUGE2_TILE", -1);
+  if (forced >= 0 && forced < TILE_COUNT) return forced;
+  if (d.c_out <= 32) return TILE_256x32;
+  PlanShape shape;
+  if (!build_shape(d, transposed, class_split, tile_bm(TILE_128x128), &shape)) return TILE_128x128;
+  long long works = 0;
+  const long long ntiles = (d.c_out + 127) / 128;
+  for (const huge2_segment& s : shape.segs) {
+    long long m = (long long)d.n * s.nphase_h * s.nphase_w * s.qn_h * s.qn_w;
+    works += (m + 127) / 128 * ntiles;
+  }
+  return works < 256 ? TILE_64x128 : TILE_128x128;
+}
+
+int class_split_mode() {
+  int v = env_int("HUGE2_CLASS_SPLIT", 2);
+  return (v >= 0 && v <= 2) ? v : 2;
+}
+
+void free_buffers(huge2_plan* p) {
+  void* bufs[2] = {p->wp, p->meta};
+  for (void* b : bufs) {
+    if (!b) continue;
+    if (p->stream_ordered)
+      (void)hipFreeAsync(b, p->alloc_stream);
+    else
+      (void)hipFree(b);
+  }
+  p->wp = p->meta = nullptr;
+}
+
+huge2_status dev_alloc(huge2_plan* p, void** out, size_t bytes) {
+  *out = nullptr;
+  if (bytes == 0) return HUGE2_OK;
+  if (fault("alloc")) return HUGE2_ERR_ALLOC;
+  hipError_t e = p->stream_ordered ? hipMallocAsync(out, bytes, p->alloc_stream)
+                                   : hipMalloc(out, bytes);
+  if (e != hipSuccess) {
+    *out = nullptr;
+    (void)hipGetLastError();
+    return HUGE2_ERR_ALLOC;
+  }
+  return HUGE2_OK;
+}
+
+huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int transposed,
+                         const void* w, hipStream_t stream, bool stream_ordered) {
+  if (!out) return HUGE2_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (transposed != 0 && transposed != 1) return HUGE2_ERR_INVALID_ARG;
+  huge2_status st = validate_desc(desc, transposed != 0);
+  if (st != HUGE2_OK) return st;
+  if (!w) return HUGE2_ERR_INVALID_ARG;
+  const huge2_conv_desc& d = *desc;
+  const bool tr = transposed != 0;
+
+  const int split = class_split_mode();
+  const int cfg = choose_cfg(d, tr, split);
+  const int bm = tile_bm(cfg), bn = tile_bn(cfg);
+  PlanShape shape;
+  if (!build_shape(d, tr, split, bm, &shape)) return HUGE2_ERR_INVALID_ARG;
+
+  huge2_plan* p = new (std::nothrow) huge2_plan();
+  if (!p) return HUGE2_ERR_ALLOC;
+  p->desc = d;
+  p->transposed = transposed;
+  output_dims(d, tr, &p->ho, &p->wo);
+  p->cfg = cfg;
+  const int esz = elem_size(d.dtype);
+  const int vec = 16 / esz;
+  const int bk = kBlockK_bytes / esz;
+  p->in_mode = d.layout == HUGE2_NCHW ? IN_NCHW : (d.c_in % vec == 0 ? IN_NHWC_VEC : IN_NHWC_ELEM);
+  p->cin_pad = round_up(d.c_in, bk);
+  p->cout_pad = round_up(d.c_out, bn);
+  p->stream_ordered = stream_ordered;
+  p->alloc_stream = stream;
+  p->nonzero_macs = shape.nonzero_macs;
+
+  // Device views of the decomposition, and the work list.
+  std::vector<SegDev> segs;
+  std::vector<TapDev> taps;
+  std::vector<WorkDev> works;
+  const int ntiles_n = p->cout_pad / bn;
+  int64_t issued = 0;
+  for (const huge2_tap& t : shape.taps) {
+    TapDev td;
+    td.slot = t.kh * d.s + t.kw;
+    td.off_h = t.off_h;
+    td.off_w = t.off_w;
+    td.pad = 0;
+    taps.push_back(td);
+  }
+  for (size_t i = 0; i < shape.segs.size(); ++i) {
+    const huge2_segment& s = shape.segs[i];
+    SegDev sd;
+    std::memset(&sd, 0, sizeof(sd));
+    sd.phase0_h = s.phase0_h;
+    sd.phase0_w = s.phase0_w;
+    sd.nphase_w = s.nphase_w;
+    sd.m_total = d.n * s.nphase_h * s.nphase_w * s.qn_h * s.qn_w;
+    sd.out_step_h = s.out_step_h;
+    sd.out_step_w = s.out_step_w;
+    sd.q0_h = s.q0_h;
+    sd.q0_w = s.q0_w;
+    sd.qn_h = s.qn_h;
+    sd.qn_w = s.qn_w;
+    sd.in0_h = s.in0_h;
+    sd.in0_w = s.in0_w;
+    sd.in_dphase_h = s.in_dphase_h;
+    sd.in_dphase_w = s.in_dphase_w;
+    sd.in_step_h = s.in_step_h;
+    sd.in_step_w = s.in_step_w;
+    sd.tap_begin = s.tap_begin;
+    sd.tap_count = s.tap_count;
+    segs.push_back(sd);
+    for (int m0 = 0; m0 < sd.m_total; m0 += bm)
+      for (int nt = 0; nt < ntiles_n; ++nt) {
+        WorkDev wd;
+        wd.seg = (int32_t)i;
+        wd.m0 = m0;
+        wd.n0 = nt * bn;
+        wd.pad = 0;
+        works.push_back(wd);
+        issued += (int64_t)bm * bn * s.tap_count * p->cin_pad;
+      }
+  }
+  p->issued_macs = issued;
+  p->n_works = (int)works.size();
+
+  const size_t seg_b = segs.size() * sizeof(SegDev);
+  const size_t tap_b = taps.size() * sizeof(TapDev);
+  const size_t work_b = works.size() * sizeof(WorkDev);
+  const size_t meta_b = seg_b + tap_b + work_b;
+  const size_t wp_b = (size_t)d.r * d.s * p->cout_pad * p->cin_pad * esz;
+
+  if ((st = dev_alloc(p, &p->meta, meta_b)) != HUGE2_OK ||
+      (st = dev_alloc(p, &p->wp, wp_b)) != HUGE2_OK) {
+    free_buffers(p);
+    delete p;
+    return st;
+  }
+  p->d_segs = (SegDev*)p->meta;
+  p->d_taps = (TapDev*)((char*)p->meta + seg_b);
+  p->d_works = (WorkDev*)((char*)p->meta + seg_b + tap_b);
+
+  std::vector<char> host(meta_b);
+  if (seg_b) std::memcpy(host.data(), segs.data(), seg_b);
+  if (tap_b) std::memcpy(host.data() + seg_b, taps.data(), tap_b);
+  if (work_b) std::memcpy(host.data() + seg_b + tap_b, works.data(), work_b);
+
+  bool ok = !fault("launch");
+  if (ok && meta_b)
+    ok = hipMemcpyAsync(p->meta, host.data(), meta_b, hipMemcpyHostToDevice, stream) == hipSuccess;
+  if (ok)
+    ok = launch_pack_weights(w, p->wp, d.dtype, tr, d.c_in, d.c_out, d.r, d.s, p->cin_pad,
+                             p->cout_pad, stream) == hipSuccess;
+  // the host copy of the metadata must outlive the transfer
+  if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
+  if (!ok) {
+    (void)hipGetLastError();
+    free_buffers(p);
+    delete p;
+    return HUGE2_ERR_HIP;
+  }
+  *out = p;
+  return HUGE2_OK;
+}
+
+huge2_status execute_impl(const huge2_plan* p, const void* x, const float* bias, void* y,
+                          hipStream_t stream) {
+  if (!p || !x || !y || x == y) return HUGE2_ERR_INVALID_ARG;
+  const huge2_conv_desc& d = p->desc;
+  if (fault("launch")) return HUGE2_ERR_HIP;
+  GemmArgs a;
+  a.x = x;
+  a.wp = p->wp;
+  a.bias = bias;
+  a.y = y;
+  a.segs = p->d_segs;
+  a.taps = p->d_taps;
+  a.works = p->d_works;
+  a.n_works = p->n_works;
+  a.n = d.n;
+  a.h = d.h;
+  a.w = d.w;
+  a.cin = d.c_in;
+  a.cin_pad = p->cin_pad;
+  a.cout = d.c_out;
+  a.cout_pad = p->cout_pad;
+  a.ho = p->ho;
+  a.wo = p->wo;
+  if (launch_phase_gemm(a, d.dtype, p->cfg, p->in_mode, stream) != hipSuccess) {
+    (void)hipGetLastError();
+    return HUGE2_ERR_HIP;
+  }
+  return HUGE2_OK;
+}
+
+huge2_status one_shot(const huge2_conv_desc* desc, int transposed, const void* x, const void* w,
+                      const float* bias, void* y, hipStream_t stream) {
+  huge2_status st = validate_desc(desc, transposed != 0);
+  if (st != HUGE2_OK) return st;
+  if (!x || !w || !y || x == y) return HUGE2_ERR_INVALID_ARG;
+  huge2_plan* p = nullptr;
+  st = create_impl(&p, desc, transposed, w, stream, true);
+  if (st != HUGE2_OK) return st;
+  st = execute_impl(p, x, bias, y, stream);
+  free_buffers(p);  // stream-ordered: released after the enqueued work
+  delete p;
+  return st;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* huge2_status_str(huge2_status status) {
+  switch (status) {
+    case HUGE2_OK: return "HUGE2_OK";
+    case HUGE2_ERR_INVALID_ARG: return "HUGE2_ERR_INVALID_ARG";
+    case HUGE2_ERR_UNSUPPORTED: return "HUGE2_ERR_UNSUPPORTED";
+    case HUGE2_ERR_ALLOC: return "HUGE2_ERR_ALLOC";
+    case HUGE2_ERR_HIP: return "HUGE2_ERR_HIP";
+  }
+  return "HUGE2_ERR_UNKNOWN";
+}
+
+huge2_status huge2_output_shape(const huge2_conv_desc* desc, int32_t transposed, int32_t* h_out,
+                                int32_t* w_out) {
+  if (!h_out || !w_out || (transposed != 0 && transposed != 1)) return HUGE2_ERR_INVALID_ARG;
+  huge2_status st = validate_desc(desc, transposed != 0);
+  if (st == HUGE2_ERR_UNSUPPORTED) st = HUGE2_OK;  // the shape itself is well defined
+  if (st != HUGE2_OK) return st;
+  int ho, wo;
+  output_dims(*desc, transposed != 0, &ho, &wo);
+  *h_out = ho;
+  *w_out = wo;
+  return HUGE2_OK;
+}
+
+huge2_status huge2_plan_create(huge2_plan** out, const huge2_conv_desc* desc, int32_t transposed,
+                               const void* w, void* hip_stream) {
+  try {
+    return create_impl(out, desc, transposed, w, (hipStream_t)hip_stream, false);
+  } catch (...) {
+    return HUGE2_ERR_ALLOC;
+  }
+}
+
+huge2_status huge2_plan_execute(const huge2_plan* plan, const void* x, const float* bias, void* y,
+                                void* hip_stream) {
+  try {
+    return execute_impl(plan, x, bias, y, (hipStream_t)hip_stream);
+  } catch (...) {
+    return HUGE2_ERR_HIP;
+  }
+}
+
+huge2_status huge2_plan_destroy(huge2_plan* plan) {
+  if (!plan) return HUGE2_OK;
+  free_buffers(plan);
+  delete plan;
+  return HUGE2_OK;
+}
+
+huge2_status huge2_conv2d_transpose(const huge2_conv_desc* desc, const void* x, const void* w,
+                                    const float* bias, void* y, void* hip_stream) {
+  try {
+    return one_shot(desc, 1, x, w, bias, y, (hipStream_t)hip_stream);
+  } catch (...) {
+    return HUGE2_ERR_ALLOC;
+  }
+}
+
+huge2_status huge2_conv2d_dilated(const huge2_conv_desc* desc, const void* x, const void* w,
+                                  const float* bias, void* y, void* hip_stream) {
+  try {
+    return one_shot(desc, 0, x, w, bias, y, (hipStream_t)hip_stream);
+  } catch (...) {
+    return HUGE2_ERR_ALLOC;
+  }
+}
+
+huge2_status huge2_plan_describe(const huge2_conv_desc* desc, int32_t transposed,
+                                 int32_t class_split, huge2_segment* segs, int32_t seg_cap,
+                                 int32_t* n_segs, huge2_tap* taps, int32_t tap_cap,
+                                 int32_t* n_taps) {
+  if (!n_segs || !n_taps || seg_cap < 0 || tap_cap < 0 || (seg_cap > 0 && !segs) ||
+      (tap_cap > 0 && !taps) || (transposed != 0 && transposed != 1) || class_split < 0 ||
+      class_split > 2)
+    return HUGE2_ERR_INVALID_ARG;
+  huge2_status st = validate_desc(desc, transposed != 0);
+  if (st != HUGE2_OK) return st;
+  try {
+    const int cfg = choose_cfg(*desc, transposed != 0, class_split);
+    PlanShape shape;
+    if (!build_shape(*desc, transposed != 0, class_split, tile_bm(cfg), &shape))
+      return HUGE2_ERR_INVALID_ARG;
+    *n_segs = (int32_t)shape.segs.size();
+    *n_taps = (int32_t)shape.taps.size();
+    for (int i = 0; i < seg_cap && i < *n_segs; ++i) segs[i] = shape.segs[i];
+    for (int i = 0; i < tap_cap && i < *n_taps; ++i) taps[i] = shape.taps[i];
+    return HUGE2_OK;
+  } catch (...) {
+    return HUGE2_ERR_ALLOC;
+  }
+}
+
+huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, int64_t* nonzero_macs,
+                             int64_t* issued_macs) {
+  if (!nonzero_macs || !issued_macs || (transposed != 0 && transposed != 1))
+    return HUGE2_ERR_INVALID_ARG;
+  huge2_status st = validate_desc(desc, transposed != 0);
+  if (st != HUGE2_OK) return st;
+  try {
+    const int split = class_split_mode();
+    const int cfg = choose_cfg(*desc, transposed != 0, split);
+    const int bm = tile_bm(cfg), bn = tile_bn(cfg);
+    PlanShape shape;
+    if (!build_shape(*desc, transposed != 0, split, bm, &shape)) return HUGE2_ERR_INVALID_ARG;
+    const int bk = kBlockK_bytes / elem_size(desc->dtype);
+    const int64_t cin_pad = round_up(desc->c_in, bk);
+    const int64_t ntn = round_up(desc->c_out, bn) / bn;
+    *nonzero_macs = shape.nonzero_macs;
+    *issued_macs = shape.tile_taps * bm * bn * ntn * cin_pad;
+    return HUGE2_OK;
+  } catch (...) {
+    return HUGE2_ERR_ALLOC;
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,277 @@
+// plan.cpp -- host-side phase decomposition (see plan.hpp).
+#include "plan.hpp"
+
+#include <algorithm>
+#include <climits>
+
+namespace huge2 {
+namespace {
+
+// floor(a / b) and ceil(a / b) for b > 0 and any sign of a.
+int floor_div(int a, int b) { return a >= 0 ? a / b : -((-a + b - 1) / b); }
+int ceil_div(int a, int b) { return -floor_div(-a, b); }
+
+// q in [0, q_count) with 0 <= base + step*q < in_size, as [lo, hi).
+void valid_range(int base, int step, int q_count, int in_size, int* lo, int* hi) {
+  *lo = std::max(0, ceil_div(-base, step));
+  *hi = std::min(q_count, floor_div(in_size - 1 - base, step) + 1);
+  if (*hi < *lo) *hi = *lo;
+}
+
+bool same_taps(const std::vector<AxisTap>& a, const std::vector<AxisTap>& b) {
+  if (a.size() != b.size()) return false;
+  for (size_t i = 0; i < a.size(); ++i)
+    if (a[i].k != b[i].k || a[i].off != b[i].off || a[i].lo != b[i].lo || a[i].hi != b[i].hi)
+      return false;
+  return true;
+}
+
+}  // namespace
+
+bool decompose_axis(bool transposed, int in_size, int out_size, int ksize, int stride, int pad,
+                    int dil, std::vector<AxisGroup>* groups) {
+  groups->clear();
+  if (in_size < 1 || out_size < 1 || ksize < 1 || stride < 1 || dil < 1 || pad < 0) return false;
+  if (transposed) {
+    // Output phase rho collects o = rho + stride*q.  Tap k lands there when
+    // i*stride = o + pad - k*dil, i.e. (rho + pad - k*dil) divisible by the
+    // stride, and then reads input i = q + (rho + pad - k*dil)/stride.
+    for (int rho = 0; rho < std::min(stride, out_size); ++rho) {
+      AxisGroup g;
+      g.phase0 = rho;
+      g.nphase = 1;
+      g.out_step = stride;
+      g.q_count = ceil_div(out_size - rho, stride);
+      g.in0 = 0;
+      g.in_dphase = 0;
+      g.in_step = 1;
+      for (int k = 0; k < ksize; ++k) {
+        int num = rho + pad - k * dil;
+        if (((num % stride) + stride) % stride != 0) continue;
+        AxisTap t;
+        t.k = k;
+        t.off = num / stride;  // exact
+        valid_range(t.off, 1, g.q_count, in_size, &t.lo, &t.hi);
+        if (t.lo < t.hi) g.taps.push_back(t);
+      }
+      groups->push_back(g);
+    }
+    return true;
+  }
+  if (stride == 1) {
+    // Phase views of a dilated conv (section 3.2.2): output o = phi + dil*q
+    // reads input phi - pad + dil*(q + k), the phi-th sub-lattice shifted by k.
+    int nphi = std::min(dil, out_size);
+    for (int phi = 0; phi < nphi; ++phi) {
+      AxisGroup g;
+      g.phase0 = phi;
+      g.nphase = 1;
+      g.out_step = dil;
+      g.q_count = ceil_div(out_size - phi, dil);
+      g.in0 = phi - pad;
+      g.in_dphase = 1;
+      g.in_step = dil;
+      for (int k = 0; k < ksize; ++k) {
+        AxisTap t;
+        t.k = k;
+        t.off = k * dil;
+        valid_range(g.in0 + t.off, dil, g.q_count, in_size, &t.lo, &t.hi);
+        if (t.lo < t.hi) g.taps.push_back(t);
+      }
+      // consecutive phase views with the same shape share one group
+      if (!groups->empty()) {
+        AxisGroup& prev = groups->back();
+        if (prev.q_count == g.q_count && same_taps(prev.taps, g.taps) &&
+            prev.phase0 + prev.nphase == phi) {
+          prev.nphase += 1;
+          continue;
+        }
+      }
+      groups->push_back(g);
+    }
+    return true;
+  }
+  // Strided (and possibly dilated) conv: a direct gather, one phase.
+  AxisGroup g;
+  g.phase0 = 0;
+  g.nphase = 1;
+  g.out_step = 1;
+  g.q_count = out_size;
+  g.in0 = -pad;
+  g.in_dphase = 0;
+  g.in_step = stride;
+  for (int k = 0; k < ksize; ++k) {
+    AxisTap t;
+    t.k = k;
+    t.off = k * dil;
+    valid_range(g.in0 + t.off, stride, g.q_count, in_size, &t.lo, &t.hi);
+    if (t.lo < t.hi) g.taps.push_back(t);
+  }
+  groups->push_back(g);
+  return true;
+}
+
+std::vector<AxisPiece> axis_pieces(const AxisGroup& g, bool split) {
+  std::vector<AxisPiece> out;
+  if (!split) {
+    AxisPiece p;
+    p.q0 = 0;
+    p.qn = g.q_count;
+    for (int i = 0; i < (int)g.taps.size(); ++i) p.tap_idx.push_back(i);
+    out.push_back(p);
+    return out;
+  }
+  std::vector<int> cuts = {0, g.q_count};
+  for (const AxisTap& t : g.taps) {
+    cuts.push_back(t.lo);
+    cuts.push_back(t.hi);
+  }
+  std::sort(cuts.begin(), cuts.end());
+  cuts.erase(std::unique(cuts.begin(), cuts.end()), cuts.end());
+  for (size_t c = 0; c + 1 < cuts.size(); ++c) {
+    int a = cuts[c], b = cuts[c + 1];
+    if (a < 0 || b > g.q_count || a >= b) continue;
+    AxisPiece p;
+    p.q0 = a;
+    p.qn = b - a;
+    for (int i = 0; i < (int)g.taps.size(); ++i)
+      if (g.taps[i].lo <= a && b <= g.taps[i].hi) p.tap_idx.push_back(i);
+    out.push_back(p);
+  }
+  return out;
+}
+
+bool output_dims(const huge2_conv_desc& d, bool transposed, int* ho, int* wo) {
+  long long h, w;
+  if (transposed) {
+    h = (long long)(d.h - 1) * d.stride_h - 2LL * d.pad_h + (long long)d.dil_h * (d.r - 1) +
+        d.out_pad_h + 1;
+    w = (long long)(d.w - 1) * d.stride_w - 2LL * d.pad_w + (long long)d.dil_w * (d.s - 1) +
+        d.out_pad_w + 1;
+  } else {
+    long long nh = (long long)d.h + 2LL * d.pad_h - (long long)d.dil_h * (d.r - 1) - 1;
+    long long nw = (long long)d.w + 2LL * d.pad_w - (long long)d.dil_w * (d.s - 1) - 1;
+    if (nh < 0 || nw < 0) return false;
+    h = nh / d.stride_h + 1;
+    w = nw / d.stride_w + 1;
+  }
+  if (h < 1 || w < 1 || h > INT_MAX || w > INT_MAX) return false;
+  *ho = (int)h;
+  *wo = (int)w;
+  return true;
+}
+
+huge2_status validate_desc(const huge2_conv_desc* d, bool transposed) {
+  if (!d) return HUGE2_ERR_INVALID_ARG;
+  if (d->n < 1 || d->c_in < 1 || d->h < 1 || d->w < 1 || d->c_out < 1 || d->r < 1 || d->s < 1)
+    return HUGE2_ERR_INVALID_ARG;
+  if (d->stride_h < 1 || d->stride_w < 1 || d->dil_h < 1 || d->dil_w < 1)
+    return HUGE2_ERR_INVALID_ARG;
+  if (d->pad_h < 0 || d->pad_w < 0 || d->out_pad_h < 0 || d->out_pad_w < 0)
+    return HUGE2_ERR_INVALID_ARG;
+  if (d->layout != HUGE2_NCHW && d->layout != HUGE2_NHWC) return HUGE2_ERR_INVALID_ARG;
+  if (d->dtype != HUGE2_F32 && d->dtype != HUGE2_BF16) return HUGE2_ERR_INVALID_ARG;
+  if (transposed) {
+    if (d->out_pad_h >= std::max(d->stride_h, d->dil_h) ||
+        d->out_pad_w >= std::max(d->stride_w, d->dil_w))
+      return HUGE2_ERR_INVALID_ARG;
+  } else if (d->out_pad_h != 0 || d->out_pad_w != 0) {
+    return HUGE2_ERR_INVALID_ARG;
+  }
+  int ho, wo;
+  if (!output_dims(*d, transposed, &ho, &wo)) return HUGE2_ERR_INVALID_ARG;
+  // The kernels index tensors with 32-bit element offsets.
+  const long long lim = INT_MAX;
+  long long nx = (long long)d->n * d->c_in * d->h * d->w;
+  long long ny = (long long)d->n * d->c_out * ho * wo;
+  long long nw = (long long)d->c_in * d->c_out * d->r * d->s;
+  long long cin_pad = ((long long)d->c_in + 31) / 32 * 32;
+  long long cout_pad = ((long long)d->c_out + 127) / 128 * 128;
+  if (nx > lim || ny > lim || nw > lim || cin_pad * cout_pad * d->r * d->s > lim)
+    return HUGE2_ERR_UNSUPPORTED;
+  return HUGE2_OK;
+}
+
+bool build_shape(const huge2_conv_desc& d, bool transposed, int class_split, int bm,
+                 PlanShape* out) {
+  int ho, wo;
+  if (!output_dims(d, transposed, &ho, &wo)) return false;
+  std::vector<AxisGroup> gh, gw;
+  if (!decompose_axis(transposed, d.h, ho, d.r, d.stride_h, d.pad_h, d.dil_h, &gh)) return false;
+  if (!decompose_axis(transposed, d.w, wo, d.s, d.stride_w, d.pad_w, d.dil_w, &gw)) return false;
+  out->segs.clear();
+  out->taps.clear();
+  out->tile_taps = 0;
+
+  long long vh = 0, vw = 0;
+  for (const AxisGroup& g : gh)
+    for (const AxisTap& t : g.taps) vh += (long long)g.nphase * (t.hi - t.lo);
+  for (const AxisGroup& g : gw)
+    for (const AxisTap& t : g.taps) vw += (long long)g.nphase * (t.hi - t.lo);
+  out->nonzero_macs = (int64_t)d.n * d.c_in * d.c_out * vh * vw;
+
+  if (bm < 1) bm = 1;
+  auto tiles = [&](long long m) { return (m + bm - 1) / bm; };
+  for (const AxisGroup& a : gh) {
+    for (const AxisGroup& b : gw) {
+      // choose border-class splitting per axis for this group pair
+      int best_sh = 1, best_sw = 1;
+      if (class_split != 1) {
+        long long best = -1;
+        for (int sh = 1; sh >= 0; --sh)
+          for (int sw = 1; sw >= 0; --sw) {
+            if (class_split == 0 && (sh || sw)) continue;
+            long long cost = 0;
+            for (const AxisPiece& ph : axis_pieces(a, sh))
+              for (const AxisPiece& pw : axis_pieces(b, sw)) {
+                long long m = (long long)d.n * a.nphase * b.nphase * ph.qn * pw.qn;
+                cost += tiles(m) * (4LL * (long long)ph.tap_idx.size() * pw.tap_idx.size() + 1);
+              }
+            if (best < 0 || cost < best) {
+              best = cost;
+              best_sh = sh;
+              best_sw = sw;
+            }
+          }
+      }
+      for (const AxisPiece& ph : axis_pieces(a, best_sh)) {
+        for (const AxisPiece& pw : axis_pieces(b, best_sw)) {
+          huge2_segment s;
+          s.phase0_h = a.phase0;
+          s.phase0_w = b.phase0;
+          s.nphase_h = a.nphase;
+          s.nphase_w = b.nphase;
+          s.out_step_h = a.out_step;
+          s.out_step_w = b.out_step;
+          s.q0_h = ph.q0;
+          s.q0_w = pw.q0;
+          s.qn_h = ph.qn;
+          s.qn_w = pw.qn;
+          s.in0_h = a.in0;
+          s.in0_w = b.in0;
+          s.in_dphase_h = a.in_dphase;
+          s.in_dphase_w = b.in_dphase;
+          s.in_step_h = a.in_step;
+          s.in_step_w = b.in_step;
+          s.tap_begin = (int32_t)out->taps.size();
+          for (int ih : ph.tap_idx)
+            for (int iw : pw.tap_idx) {
+              huge2_tap t;
+              t.kh = a.taps[ih].k;
+              t.kw = b.taps[iw].k;
+              t.off_h = a.taps[ih].off;
+              t.off_w = b.taps[iw].off;
+              out->taps.push_back(t);
+            }
+          s.tap_count = (int32_t)out->taps.size() - s.tap_begin;
+          long long m = (long long)d.n * a.nphase * b.nphase * ph.qn * pw.qn;
+          out->tile_taps += tiles(m) * s.tap_count;
+          out->segs.push_back(s);
+        }
+      }
+    }
+  }
+  return true;
+}
+
+}  // namespace huge2

@@ -1,0 +1,172 @@
+"""Seeded synthetic inputs for the five benchmark workloads (CPU tensors).
+
+Input generation only -- no convolution arithmetic lives here.  Both the GPU
+path and the CPU oracle are fed from these generators, so they see the same
+bytes.  All draws use ``torch.Generator('cpu').manual_seed(seed)`` in a fixed
+order; bf16 tensors are the float32 draws rounded to nearest even
+(``.to(torch.bfloat16)``).
+
+The paper evaluates DCGAN / cGAN generators pretrained on CIFAR100 (section 4);
+neither the weights nor the dataset are available, so random-init weights and
+random activations of the same shapes stand in, following the distributions
+named per workload below.
+
+Workloads (``name``: layers):
+  convt_small  single ConvTranspose 64->32, 8x8 -> 16x16, k4 s2 p1, fp32 NCHW, batch 1.
+  dcgan        z(100) -> linear -> 4x4x1024, then ConvTranspose k4 s2 p1:
+               1024->512 (8x8), 512->256 (16x16), 256->128 (32x32), 128->3 (64x64);
+               batch 64, NCHW, fp32 and bf16.
+  convt_odd    ConvTranspose 256->128, 32x32 -> 64x64, k3 s2 p1 op1, bf16 NHWC, batch 16.
+  aspp         four 3x3 dilated convs 2048->256 on 64x64, dilations 6/12/18/24, 'same'
+               padding, bf16 NHWC, batch 8, input ReLU(N(0,1)).
+  fcn_upsample ConvTranspose 21->21, 16x16 -> 512x512, k64 s32 p16, bilinear kernel plus
+               N(0, 1e-3) noise, bf16 NCHW, batch 4.
+"""
+from __future__ import annotations
+
+import dataclasses
+
+import torch
+
+
+@dataclasses.dataclass(frozen=True)
+class Layer:
+    name: str
+    transposed: bool
+    n: int
+    c_in: int
+    h: int
+    w: int
+    c_out: int
+    r: int
+    s: int
+    stride: int
+    pad: int
+    out_pad: int
+    dil: int
+    layout: str  # "NCHW" or "NHWC"
+    dtype: str   # "f32" or "bf16"
+
+    def out_hw(self):
+        if self.transposed:
+            ho = (self.h - 1) * self.stride - 2 * self.pad + self.dil * (self.r - 1) + self.out_pad + 1
+            wo = (self.w - 1) * self.stride - 2 * self.pad + self.dil * (self.s - 1) + self.out_pad + 1
+        else:
+            ho = (self.h + 2 * self.pad - self.dil * (self.r - 1) - 1) // self.stride + 1
+            wo = (self.w + 2 * self.pad - self.dil * (self.s - 1) - 1) // self.stride + 1
+        return ho, wo
+
+    def w_shape(self):
+        return ((self.c_in, self.c_out, self.r, self.s) if self.transposed
+                else (self.c_out, self.c_in, self.r, self.s))
+
+    def with_(self, **kw):
+        return dataclasses.replace(self, **kw)
+
+
+def dcgan_layers(dtype="bf16", batch=64):
+    chans = [(1024, 512), (512, 256), (256, 128), (128, 3)]
+    out = []
+    for i, (ci, co) in enumerate(chans):
+        hw = 4 << i
+        out.append(Layer("dcgan_l%d" % (i + 1), True, batch, ci, hw, hw, co, 4, 4, 2, 1, 0, 1,
+                         "NCHW", dtype))
+    return out
+
+
+def aspp_layers(batch=8, c_in=2048, c_out=256, hw=64):
+    return [Layer("aspp_d%d" % d, False, batch, c_in, hw, hw, c_out, 3, 3, 1, d, 0, d, "NHWC",
+                  "bf16") for d in (6, 12, 18, 24)]
+
+
+WORKLOADS = {
+    "convt_small": [Layer("convt_small", True, 1, 64, 8, 8, 32, 4, 4, 2, 1, 0, 1, "NCHW", "f32")],
+    "dcgan": dcgan_layers("bf16"),
+    "dcgan_f32": dcgan_layers("f32"),
+    "convt_odd": [Layer("convt_odd", True, 16, 256, 32, 32, 128, 3, 3, 2, 1, 1, 1, "NHWC", "bf16")],
+    "aspp": aspp_layers(),
+    "fcn_upsample": [Layer("fcn_upsample", True, 4, 21, 16, 16, 21, 64, 64, 32, 16, 0, 1, "NCHW",
+                           "bf16")],
+}
+
+
+def torch_dtype(name):
+    return {"f32": torch.float32, "bf16": torch.bfloat16}[name]
+
+
+def bilinear_kernel(size):
+    """FCN-style bilinear upsampling taps: f[m] = (2*min(m, size-1-m) + 1) / size."""
+    m = torch.arange(size, dtype=torch.float64)
+    f = (2 * torch.minimum(m, size - 1 - m) + 1) / size
+    return f
+
+
+def _normal(g, shape, std=1.0):
+    return torch.randn(shape, generator=g, dtype=torch.float32) * std
+
+
+def generate(workload, seed=0, batch=None):
+    """Inputs of a workload: list of (Layer, x NCHW float32, w float32).
+
+    ``batch`` overrides the batch size (the draws are then made at that size).
+    For ``dcgan`` only the first layer has a drawn input (the linear layer of
+    the generator); the others are chained on the device by the benchmark.
+    Use :func:`layer_input` for a standalone input of any layer.
+    """
+    g = torch.Generator("cpu").manual_seed(seed)
+    layers = WORKLOADS[workload]
+    if batch is not None:
+        layers = [l.with_(n=batch) for l in layers]
+    if workload in ("dcgan", "dcgan_f32"):
+        n = layers[0].n
+        z = _normal(g, (n, 100))
+        lin_w = _normal(g, (1024 * 4 * 4, 100), 0.02)
+        x1 = (z @ lin_w.t()).reshape(n, 1024, 4, 4)  # linear layer, bias 0
+        ws = [_normal(g, l.w_shape(), 0.02) for l in layers]
+        out = [(layers[0], x1, ws[0])]
+        out += [(l, None, w) for l, w in zip(layers[1:], ws[1:])]
+        return out
+    if workload == "aspp":
+        l0 = layers[0]
+        x = torch.relu(_normal(g, (l0.n, l0.c_in, l0.h, l0.w)))
+        return [(l, x, _normal(g, l.w_shape(), 0.01)) for l in layers]
+    l0 = layers[0]
+    if workload == "convt_small":
+        x = _normal(g, (l0.n, l0.c_in, l0.h, l0.w))
+        return [(l0, x, _normal(g, l0.w_shape(), 0.02))]
+    if workload == "convt_odd":
+        x = torch.rand((l0.n, l0.c_in, l0.h, l0.w), generator=g, dtype=torch.float32) * 2 - 1
+        return [(l0, x, _normal(g, l0.w_shape(), 0.02))]
+    if workload == "fcn_upsample":
+        x = _normal(g, (l0.n, l0.c_in, l0.h, l0.w))
+        f = bilinear_kernel(l0.r).to(torch.float32)
+        w = _normal(g, l0.w_shape(), 1e-3)
+        for c in range(l0.c_in):
+            w[c, c] += torch.outer(f, f)
+        return [(l0, x, w)]
+    raise KeyError(workload)
+
+
+def layer_input(layer, seed=0, std=1.0):
+    """A standalone N(0, std^2) NCHW float32 input for one layer."""
+    g = torch.Generator("cpu").manual_seed(seed)
+    return _normal(g, (layer.n, layer.c_in, layer.h, layer.w), std)
+
+
+def random_weight(layer, seed=0, std=0.02):
+    g = torch.Generator("cpu").manual_seed(seed)
+    return _normal(g, layer.w_shape(), std)
+
+
+def to_layout(x_nchw, layout):
+    """NCHW tensor -> contiguous tensor in ``layout`` (a permutation, no arithmetic)."""
+    if layout == "NCHW":
+        return x_nchw.contiguous()
+    return x_nchw.permute(0, 2, 3, 1).contiguous()
+
+
+def from_layout(x, layout):
+    """Tensor in ``layout`` -> NCHW view."""
+    if layout == "NCHW":
+        return x
+    return x.permute(0, 3, 1, 2)

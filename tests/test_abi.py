@@ -1,0 +1,139 @@
+"""The C ABI on the CPU: the library loads, exports every symbol the header
+declares, and rejects invalid arguments before any HIP call (no GPU needed)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+h2 = pytest.importorskip("paper_1907_11210_amd.huge2")
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(h2.LIB_PATH):
+        from paper_1907_11210_amd import _build
+        _build.build()
+    return h2.lib()
+
+
+def _declared_functions():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", fn)).read()
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            names |= set(re.findall(r"\b(huge2_\w+)\s*\(", text))
+    return names
+
+
+def test_every_declared_symbol_is_exported(L):
+    declared = _declared_functions()
+    assert declared >= set(h2.EXPORTED)
+    for name in declared:
+        assert hasattr(L, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", h2.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (huge2_\w+)", out))
+    assert declared <= exported
+
+
+def test_status_strings(L):
+    for code, name in enumerate(["HUGE2_OK", "HUGE2_ERR_INVALID_ARG", "HUGE2_ERR_UNSUPPORTED",
+                                 "HUGE2_ERR_ALLOC", "HUGE2_ERR_HIP"]):
+        assert h2.status_str(code) == name
+    assert h2.status_str(99) == "HUGE2_ERR_UNKNOWN"
+
+
+def _good():
+    return h2.make_desc(2, 8, 5, 5, 4, 4, 4, 2, 1, 0, 1, h2.HUGE2_NCHW, h2.HUGE2_F32)
+
+
+@pytest.mark.parametrize("field,value", [
+    ("n", 0), ("c_in", 0), ("h", -1), ("c_out", 0), ("r", 0), ("stride_h", 0), ("dil_w", 0),
+    ("pad_h", -1), ("out_pad_w", 2), ("layout", 2), ("dtype", 7), ("pad_h", 40),
+])
+def test_invalid_descriptor_rejected_without_gpu(L, field, value):
+    d = _good()
+    setattr(d, field, value)
+    ho, wo = ctypes.c_int32(-5), ctypes.c_int32(-5)
+    st = L.huge2_output_shape(ctypes.byref(d), 1, ctypes.byref(ho), ctypes.byref(wo))
+    assert st == h2.HUGE2_ERR_INVALID_ARG
+    assert ho.value == -5  # untouched
+    fake = ctypes.c_void_p(4096)
+    assert L.huge2_conv2d_transpose(ctypes.byref(d), fake, fake, None, ctypes.c_void_p(8192),
+                                    None) == h2.HUGE2_ERR_INVALID_ARG
+    plan = ctypes.c_void_p(1234)
+    assert L.huge2_plan_create(ctypes.byref(plan), ctypes.byref(d), 1, fake,
+                               None) == h2.HUGE2_ERR_INVALID_ARG
+    assert plan.value is None
+
+
+def test_dilated_rejects_output_padding(L):
+    d = h2.make_desc(1, 4, 8, 8, 4, 3, 3, 1, 2, 1, 2, h2.HUGE2_NHWC, h2.HUGE2_BF16)
+    ho, wo = ctypes.c_int32(), ctypes.c_int32()
+    assert L.huge2_output_shape(ctypes.byref(d), 0, ctypes.byref(ho),
+                                ctypes.byref(wo)) == h2.HUGE2_ERR_INVALID_ARG
+    # the same descriptor is valid as a transposed conv (out_pad < dilation)
+    assert L.huge2_output_shape(ctypes.byref(d), 1, ctypes.byref(ho), ctypes.byref(wo)) == 0
+
+
+def test_null_and_aliased_pointers_rejected(L):
+    d = _good()
+    fake = ctypes.c_void_p(4096)
+    assert L.huge2_conv2d_transpose(ctypes.byref(d), None, fake, None, fake,
+                                    None) == h2.HUGE2_ERR_INVALID_ARG
+    assert L.huge2_conv2d_transpose(ctypes.byref(d), fake, None, None, ctypes.c_void_p(8192),
+                                    None) == h2.HUGE2_ERR_INVALID_ARG
+    assert L.huge2_conv2d_transpose(ctypes.byref(d), fake, fake, None, fake,
+                                    None) == h2.HUGE2_ERR_INVALID_ARG  # x == y
+    assert L.huge2_conv2d_dilated(None, fake, fake, None, ctypes.c_void_p(8192),
+                                  None) == h2.HUGE2_ERR_INVALID_ARG
+    assert L.huge2_plan_execute(None, fake, None, ctypes.c_void_p(8192),
+                                None) == h2.HUGE2_ERR_INVALID_ARG
+    assert L.huge2_plan_destroy(None) == h2.HUGE2_OK
+    assert L.huge2_plan_create(None, ctypes.byref(d), 1, fake, None) == h2.HUGE2_ERR_INVALID_ARG
+    plan = ctypes.c_void_p()
+    assert L.huge2_plan_create(ctypes.byref(plan), ctypes.byref(d), 2, fake,
+                               None) == h2.HUGE2_ERR_INVALID_ARG
+
+
+def test_too_large_is_unsupported(L):
+    d = h2.make_desc(64, 4096, 512, 512, 16, 3, 3, 1, 1, 0, 1, h2.HUGE2_NHWC, h2.HUGE2_BF16)
+    ho, wo = ctypes.c_int32(), ctypes.c_int32()
+    assert L.huge2_output_shape(ctypes.byref(d), 0, ctypes.byref(ho), ctypes.byref(wo)) == 0
+    plan = ctypes.c_void_p()
+    assert L.huge2_plan_create(ctypes.byref(plan), ctypes.byref(d), 0, ctypes.c_void_p(4096),
+                               None) == h2.HUGE2_ERR_UNSUPPORTED
+
+
+def test_allocation_failure_is_reported(L, monkeypatch):
+    monkeypatch.setenv("HUGE2_FAULT", "alloc")
+    d = _good()
+    plan = ctypes.c_void_p(77)
+    assert L.huge2_plan_create(ctypes.byref(plan), ctypes.byref(d), 1, ctypes.c_void_p(4096),
+                               None) == h2.HUGE2_ERR_ALLOC
+    assert plan.value is None
+
+
+def test_describe_sizes_and_caps(L):
+    d = _good()
+    ns, nt = ctypes.c_int32(), ctypes.c_int32()
+    assert L.huge2_plan_describe(ctypes.byref(d), 1, 2, None, 0, ctypes.byref(ns), None, 0,
+                                 ctypes.byref(nt)) == 0
+    assert ns.value > 0 and nt.value > 0
+    assert L.huge2_plan_describe(ctypes.byref(d), 1, 3, None, 0, ctypes.byref(ns), None, 0,
+                                 ctypes.byref(nt)) == h2.HUGE2_ERR_INVALID_ARG
+    assert L.huge2_plan_describe(ctypes.byref(d), 1, 1, None, 5, ctypes.byref(ns), None, 0,
+                                 ctypes.byref(nt)) == h2.HUGE2_ERR_INVALID_ARG
+
+
+def test_product_path_has_no_cpu_fallback():
+    """The binding never imports the oracle and raises if the library is missing."""
+    src = open(os.path.join(ROOT, "paper_1907_11210_amd", "huge2.py")).read()
+    assert "oracle" not in src
+    for fn in os.listdir(os.path.join(ROOT, "paper_1907_11210_amd")):
+        if fn.endswith(".py"):
+            assert "import oracle" not in open(os.path.join(ROOT, "paper_1907_11210_amd", fn)).read()

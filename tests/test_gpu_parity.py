@@ -1,0 +1,201 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Every case feeds both sides the same dtype-rounded inputs and compares element
+by element (see tests/parity.py for the criterion).  Small cases are checked in
+full; the five benchmark workloads are checked in full at reduced size and on
+sampled outputs at full size, in the plan configuration the benchmark times.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_1907_11210_amd import huge2 as h2
+from paper_1907_11210_amd import workloads as wl
+from paper_1907_11210_amd.workloads import Layer
+
+import parity as P
+
+pytestmark = pytest.mark.gpu
+
+
+def L(name, tr, n, ci, h, w, co, r, s, st, pd, op, dl, layout, dtype):
+    return Layer(name, tr, n, ci, h, w, co, r, s, st, pd, op, dl, layout, dtype)
+
+
+SMALL = [
+    L("ct_ragged_f32_nchw", True, 2, 40, 9, 9, 136, 4, 4, 2, 1, 0, 1, "NCHW", "f32"),
+    L("ct_ragged_bf16_nhwc", True, 2, 40, 9, 9, 136, 4, 4, 2, 1, 0, 1, "NHWC", "bf16"),
+    L("ct_ragged_bf16_nchw", True, 3, 72, 6, 7, 200, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
+    L("ct_ragged_f32_nhwc", True, 1, 20, 10, 6, 36, 4, 4, 2, 1, 0, 1, "NHWC", "f32"),
+    L("ct_odd_op_bf16_nhwc", True, 2, 24, 7, 7, 40, 3, 3, 2, 1, 1, 1, "NHWC", "bf16"),
+    L("ct_zero_tap_phases", True, 1, 16, 5, 5, 16, 1, 1, 2, 0, 1, 1, "NHWC", "f32"),
+    L("ct_crop", True, 1, 8, 6, 6, 8, 3, 3, 2, 2, 0, 1, "NCHW", "f32"),
+    L("ct_c21_staged", True, 2, 21, 6, 6, 21, 8, 8, 4, 2, 0, 1, "NHWC", "bf16"),
+    L("ct_stride32", True, 1, 3, 3, 3, 3, 64, 64, 32, 16, 0, 1, "NCHW", "bf16"),
+    L("ct_dilated_kernel", True, 2, 16, 5, 6, 24, 3, 3, 2, 1, 1, 2, "NCHW", "f32"),
+    L("ct_stride1", True, 1, 32, 8, 8, 32, 3, 3, 1, 1, 0, 1, "NHWC", "bf16"),
+    L("ct_h1", True, 2, 32, 1, 9, 48, 4, 4, 2, 1, 0, 1, "NCHW", "f32"),
+    L("ct_cout1", True, 2, 64, 8, 8, 1, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
+    L("ct_big_k", True, 1, 256, 4, 4, 160, 4, 4, 2, 1, 0, 1, "NHWC", "bf16"),
+    L("dil_aspp_d6", False, 1, 64, 64, 64, 48, 3, 3, 1, 6, 0, 6, "NHWC", "bf16"),
+    L("dil_aspp_d24", False, 1, 64, 64, 64, 48, 3, 3, 1, 24, 0, 24, "NHWC", "bf16"),
+    L("dil_f32_nchw", False, 2, 12, 13, 11, 20, 3, 3, 1, 2, 0, 2, "NCHW", "f32"),
+    L("dil_valid", False, 1, 16, 12, 12, 16, 3, 3, 1, 0, 0, 3, "NHWC", "f32"),
+    L("conv_strided_dilated", False, 2, 8, 11, 11, 40, 3, 3, 2, 2, 0, 2, "NHWC", "f32"),
+    L("conv_plain", False, 2, 48, 9, 9, 136, 3, 3, 1, 1, 0, 1, "NCHW", "bf16"),
+    L("conv_1x1", False, 1, 64, 5, 5, 64, 1, 1, 1, 0, 0, 1, "NHWC", "bf16"),
+]
+
+
+def _inputs(layer, seed):
+    x = wl.layer_input(layer, seed=seed)
+    w = wl.random_weight(layer, seed=seed + 1, std=0.1)
+    return P.quantise(x, layer.dtype), P.quantise(w, layer.dtype)
+
+
+@pytest.mark.parametrize("layer", SMALL, ids=lambda l: l.name)
+def test_small_case(layer):
+    P.say("case", layer)
+    xq, wq = _inputs(layer, seed=hash(layer.name) % 1000)
+    bias = torch.linspace(-0.5, 0.5, layer.c_out)
+    ref = P.oracle_full(layer, xq, wq, bias)
+    absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
+    y = P.run_gpu(layer, xq, wq, bias)
+    P.check(y, ref, absref, layer.dtype, layer.name)
+
+
+def _random_layers(count, seed):
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        tr = bool(rng.integers(0, 2))
+        n = int(rng.integers(1, 3))
+        ci, co = int(rng.integers(1, 41)), int(rng.integers(1, 70))
+        h, w = int(rng.integers(1, 10)), int(rng.integers(1, 10))
+        r = int(rng.integers(1, 6))
+        st = int(rng.integers(1, 4)) if tr else int(rng.choice([1, 1, 2]))
+        dl = int(rng.integers(1, 3))
+        pd = int(rng.integers(0, dl * (r - 1) + 1))
+        op = int(rng.integers(0, max(st, dl))) if tr else 0
+        layout = str(rng.choice(["NCHW", "NHWC"]))
+        dtype = str(rng.choice(["f32", "bf16"]))
+        lay = L("rand%d" % len(out), tr, n, ci, h, w, co, r, r, st, pd, op, dl, layout, dtype)
+        ho, wo = lay.out_hw()
+        if ho < 1 or wo < 1:
+            continue
+        out.append(lay)
+    return out
+
+
+def test_random_sweep():
+    for i, layer in enumerate(_random_layers(30, 2024)):
+        P.say("case", layer)
+        xq, wq = _inputs(layer, seed=500 + i)
+        ref = P.oracle_full(layer, xq, wq)
+        absref = P.oracle_full(layer, xq, wq, absolute=True)
+        y = P.run_gpu(layer, xq, wq)
+        P.check(y, ref, absref, layer.dtype, layer.name)
+
+
+@pytest.mark.parametrize("layer", [SMALL[1], SMALL[4], SMALL[14], SMALL[18]],
+                         ids=lambda l: l.name)
+def test_one_shot_entry_points(layer):
+    P.say("case", layer)
+    xq, wq = _inputs(layer, seed=77)
+    bias = torch.linspace(1.0, -1.0, layer.c_out)
+    ref = P.oracle_full(layer, xq, wq, bias)
+    absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
+    y = P.run_gpu(layer, xq, wq, bias, one_shot=True)
+    P.check(y, ref, absref, layer.dtype, layer.name + " one-shot")
+
+
+def test_coverage_and_determinism():
+    """Every output element is written (a NaN-prefilled output keeps no NaN) and
+    two executions of one plan agree bitwise."""
+    dev = torch.device("cuda", 0)
+    for layer in [SMALL[2], SMALL[4], SMALL[7], SMALL[8], SMALL[15]]:
+        P.say("case", layer)
+        xq, wq = _inputs(layer, seed=5)
+        x_dev = wl.to_layout(xq, layer.layout).to(dev)
+        plan = P.make_plan(layer, wq.contiguous().to(dev))
+        y1 = torch.full(plan.out_shape, float("nan"), dtype=xq.dtype, device=dev)
+        y2 = torch.full(plan.out_shape, float("nan"), dtype=xq.dtype, device=dev)
+        plan(x_dev, out=y1)
+        plan(x_dev, out=y2)
+        torch.cuda.synchronize()
+        plan.close()
+        assert not torch.isnan(y1).any(), layer.name
+        assert torch.equal(y1.view(torch.int16) if y1.dtype == torch.bfloat16 else y1.view(torch.int32),
+                           y2.view(torch.int16) if y2.dtype == torch.bfloat16 else y2.view(torch.int32))
+
+
+# ---- the benchmark workloads ------------------------------------------------
+
+def test_dcgan_chain_reduced_batch():
+    """DCGAN generator at batch 2: each layer gets the oracle's output of the
+    previous layer (rounded to the dtype), so errors do not compound."""
+    for wname in ("dcgan_f32", "dcgan"):
+        items = wl.generate(wname, seed=0, batch=2)
+        x_prev = None
+        for layer, x, w in items:
+            P.say("case", wname, layer)
+            xin = x if x is not None else x_prev
+            xq = P.quantise(xin, layer.dtype)
+            wq = P.quantise(w, layer.dtype)
+            ref = P.oracle_full(layer, xq, wq)
+            absref = P.oracle_full(layer, xq, wq, absolute=True)
+            y = P.run_gpu(layer, xq, wq)
+            P.check(y, ref, absref, layer.dtype, layer.name)
+            x_prev = torch.from_numpy(ref).to(torch.float32)
+
+
+REDUCED = [
+    ("convt_small", {}),
+    ("convt_odd", dict(n=1)),
+    ("aspp", dict(n=1, c_in=256, c_out=64)),
+    ("fcn_upsample", dict(n=1, c_in=5, c_out=5, h=3, w=3)),
+]
+
+
+@pytest.mark.parametrize("wname,over", REDUCED, ids=[r[0] for r in REDUCED])
+def test_workload_reduced_full_check(wname, over):
+    for i, layer in enumerate(wl.WORKLOADS[wname]):
+        layer = layer.with_(**over)
+        P.say("case", layer)
+        g = torch.Generator("cpu").manual_seed(i)
+        x = wl.layer_input(layer, seed=10 + i)
+        if wname == "aspp":
+            x = torch.relu(x)
+        w = wl.random_weight(layer, seed=20 + i, std=0.02)
+        if wname == "fcn_upsample":
+            f = wl.bilinear_kernel(layer.r).to(torch.float32)
+            w = w * 0.05
+            for c in range(layer.c_in):
+                w[c, c] += torch.outer(f, f)
+        del g
+        xq, wq = P.quantise(x, layer.dtype), P.quantise(w, layer.dtype)
+        ref = P.oracle_full(layer, xq, wq)
+        absref = P.oracle_full(layer, xq, wq, absolute=True)
+        y = P.run_gpu(layer, xq, wq)
+        P.check(y, ref, absref, layer.dtype, layer.name)
+
+
+FULL = ["convt_small", "dcgan_f32", "dcgan", "convt_odd", "aspp", "fcn_upsample"]
+
+
+@pytest.mark.parametrize("wname", FULL)
+def test_workload_full_size_sampled(wname):
+    """Full-size workloads, plan path (as timed by the benchmark), checked on
+    sampled outputs that cover every phase, border and first/last channel."""
+    items = wl.generate(wname, seed=0)
+    for i, (layer, x, w) in enumerate(items):
+        if x is None:  # dcgan layers 2-4: standalone input of the chained shape
+            x = wl.layer_input(layer, seed=100 + i, std=0.25)
+        P.say("case", wname, layer)
+        xq, wq = P.quantise(x, layer.dtype), P.quantise(w, layer.dtype)
+        y = P.run_gpu(layer, xq, wq)
+        idx = P.sample_indices(layer, 3000, seed=i)
+        ref = P.oracle_points(layer, xq, wq, idx)
+        absref = P.oracle_points(layer, xq, wq, idx, absolute=True)
+        P.check(y.ravel()[idx], ref, absref, layer.dtype, layer.name)
+        assert np.all(np.isfinite(y))

@@ -1,0 +1,192 @@
+"""The host-side phase decomposition, checked on the CPU (no GPU needed).
+
+``huge2_plan_describe`` returns the segments and taps a plan would use.  A
+slow numpy executor of that description (loops over segments, pixels and
+taps, the way the GPU kernel walks them) must reproduce the oracle, every
+output element must be written exactly once (the disjoint scatter of the
+paper's section 3.1), and with border classes on, no tap of a segment may
+read outside the input.  The structural non-zero MAC count is checked
+against a brute-force count.
+"""
+import numpy as np
+import pytest
+
+h2 = pytest.importorskip("paper_1907_11210_amd.huge2")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _built():
+    import os
+    if not os.path.exists(h2.LIB_PATH):
+        from paper_1907_11210_amd import _build
+        _build.build()
+
+
+def _desc(n, ci, h, w, co, r, s, st, pd, op, dl, transposed):
+    return h2.make_desc(n, ci, h, w, co, r, s, st, pd, op if transposed else 0, dl,
+                        h2.HUGE2_NCHW, h2.HUGE2_F32)
+
+
+def execute_description(segs, taps, x, w, transposed, ho, wo):
+    """Run a plan description in numpy: returns (y, write counts)."""
+    n, ci, h, wd = x.shape
+    co = w.shape[1] if transposed else w.shape[0]
+    y = np.zeros((n, co, ho, wo))
+    cnt = np.zeros((n, co, ho, wo), dtype=np.int64)
+    for sg in segs:
+        tl = taps[sg["tap_begin"]: sg["tap_begin"] + sg["tap_count"]]
+        for iph in range(sg["nphase_h"]):
+            for ipw in range(sg["nphase_w"]):
+                for a_h in range(sg["qn_h"]):
+                    for a_w in range(sg["qn_w"]):
+                        qh, qw = sg["q0_h"] + a_h, sg["q0_w"] + a_w
+                        oh = sg["phase0_h"] + iph + sg["out_step_h"] * qh
+                        ow = sg["phase0_w"] + ipw + sg["out_step_w"] * qw
+                        ihb = sg["in0_h"] + sg["in_dphase_h"] * iph + sg["in_step_h"] * qh
+                        iwb = sg["in0_w"] + sg["in_dphase_w"] * ipw + sg["in_step_w"] * qw
+                        acc = np.zeros((n, co))
+                        for t in tl:
+                            ih, iw = ihb + t["off_h"], iwb + t["off_w"]
+                            if not (0 <= ih < h and 0 <= iw < wd):
+                                continue
+                            wk = (w[:, :, t["kh"], t["kw"]] if transposed
+                                  else w[:, :, t["kh"], t["kw"]].T)  # [ci, co]
+                            acc += x[:, :, ih, iw] @ wk
+                        y[:, :, oh, ow] = acc
+                        cnt[:, :, oh, ow] += 1
+    return y, cnt
+
+
+def _cases(transposed, count, seed):
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        n = int(rng.integers(1, 3))
+        ci, co = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+        h, w = int(rng.integers(1, 8)), int(rng.integers(1, 8))
+        r, s = int(rng.integers(1, 6)), int(rng.integers(1, 6))
+        st = (int(rng.integers(1, 5)), int(rng.integers(1, 5)))
+        dl = (int(rng.integers(1, 4)), int(rng.integers(1, 4)))
+        pd = (int(rng.integers(0, dl[0] * (r - 1) + 1)), int(rng.integers(0, dl[1] * (s - 1) + 1)))
+        if transposed:
+            op = (int(rng.integers(0, max(st[0], dl[0]))), int(rng.integers(0, max(st[1], dl[1]))))
+        else:
+            op = (0, 0)
+            if rng.random() < 0.6:
+                st = (1, 1)  # phase views are the stride-1 path
+        d = _desc(n, ci, h, w, co, r, s, st, pd, op, dl, transposed)
+        try:
+            h2.huge2_output_shape(d, transposed)
+        except h2.Huge2Error:
+            continue
+        out.append((n, ci, h, w, co, r, s, st, pd, op, dl))
+    return out
+
+
+@pytest.mark.parametrize("transposed", [1, 0])
+@pytest.mark.parametrize("class_split", [0, 1, 2])
+def test_description_executes_to_oracle(oracle_mod, transposed, class_split):
+    rng = np.random.default_rng(100 + 3 * transposed + class_split)
+    for case in _cases(transposed, 40, 17 + transposed):
+        n, ci, h, w_, co, r, s, st, pd, op, dl = case
+        d = _desc(n, ci, h, w_, co, r, s, st, pd, op, dl, transposed)
+        ho, wo = h2.huge2_output_shape(d, transposed)
+        x = rng.standard_normal((n, ci, h, w_))
+        w = rng.standard_normal((ci, co, r, s) if transposed else (co, ci, r, s))
+        segs, taps = h2.huge2_plan_describe(d, transposed, class_split)
+        y, cnt = execute_description(segs, taps, x, w, transposed, ho, wo)
+        assert (cnt == 1).all(), ("every output written exactly once", case)
+        if transposed:
+            ref = oracle_mod.conv2d_transpose_alg1(x, w, None, st, pd, op, dl)
+        else:
+            ref = oracle_mod.conv2d_dilated_alg2(x, w, None, st, pd, dl)
+        np.testing.assert_allclose(y, ref, rtol=1e-11, atol=1e-11, err_msg=str(case))
+        if class_split == 1:
+            h_, w__ = h, w_
+            for sg in segs:
+                for t in taps[sg["tap_begin"]: sg["tap_begin"] + sg["tap_count"]]:
+                    for iph in range(sg["nphase_h"]):
+                        for a_h in range(sg["qn_h"]):
+                            ih = (sg["in0_h"] + sg["in_dphase_h"] * iph +
+                                  sg["in_step_h"] * (sg["q0_h"] + a_h) + t["off_h"])
+                            assert 0 <= ih < h_, case
+                    for ipw in range(sg["nphase_w"]):
+                        for a_w in range(sg["qn_w"]):
+                            iw = (sg["in0_w"] + sg["in_dphase_w"] * ipw +
+                                  sg["in_step_w"] * (sg["q0_w"] + a_w) + t["off_w"])
+                            assert 0 <= iw < w__, case
+
+
+def _brute_nonzero(transposed, n, ci, co, h, w, r, s, st, pd, dl, ho, wo):
+    def axis(insz, outsz, k, stv, pdv, dlv):
+        cnt = 0
+        if transposed:
+            for i in range(insz):
+                for m in range(k):
+                    if 0 <= i * stv - pdv + m * dlv < outsz:
+                        cnt += 1
+        else:
+            for o in range(outsz):
+                for m in range(k):
+                    if 0 <= o * stv - pdv + m * dlv < insz:
+                        cnt += 1
+        return cnt
+    return n * ci * co * axis(h, ho, r, st[0], pd[0], dl[0]) * axis(w, wo, s, st[1], pd[1], dl[1])
+
+
+@pytest.mark.parametrize("transposed", [1, 0])
+def test_nonzero_mac_count(transposed):
+    for case in _cases(transposed, 60, 99 + transposed):
+        n, ci, h, w, co, r, s, st, pd, op, dl = case
+        d = _desc(n, ci, h, w, co, r, s, st, pd, op, dl, transposed)
+        ho, wo = h2.huge2_output_shape(d, transposed)
+        nz, issued = h2.huge2_plan_macs(d, transposed)
+        assert nz == _brute_nonzero(transposed, n, ci, co, h, w, r, s, st, pd, dl, ho, wo), case
+        assert issued >= nz
+
+
+def test_phase_tap_counts_closed_form():
+    """|T(rho)| = ceil((R - r)/s) with r = (rho + p) mod s (dilation 1), the
+    size of the pattern of Eq. 1-4; zero when r >= R."""
+    for r_, st, pd in [(4, 2, 1), (3, 2, 1), (5, 2, 2), (64, 32, 16), (3, 4, 0), (7, 3, 2)]:
+        d = _desc(1, 1, 40, 40, 1, r_, r_, (st, st), (pd, pd), (0, 0), (1, 1), 1)
+        segs, taps = h2.huge2_plan_describe(d, 1, 0)
+        seen = {}
+        for sg in segs:
+            tl = taps[sg["tap_begin"]: sg["tap_begin"] + sg["tap_count"]]
+            seen[(sg["phase0_h"], sg["phase0_w"])] = len({t["kh"] for t in tl})
+        for rho in range(st):
+            rr = (rho + pd) % st
+            expect = 0 if rr >= r_ else -(-(r_ - rr) // st)
+            assert seen[(rho, rho)] == expect, (r_, st, pd, rho)
+
+
+def test_dcgan_pattern_parity():
+    """k4 s2 p1: even output rows take the odd kernel rows (Pattern 1 of
+    section 3.1 reads odd rows/columns of the kernel for even outputs)."""
+    d = _desc(1, 1, 4, 4, 1, 4, 4, (2, 2), (1, 1), (0, 0), (1, 1), 1)
+    segs, taps = h2.huge2_plan_describe(d, 1, 0)
+    for sg in segs:
+        tl = taps[sg["tap_begin"]: sg["tap_begin"] + sg["tap_count"]]
+        assert {t["kh"] % 2 for t in tl} == {1 - sg["phase0_h"]}
+        assert {t["kw"] % 2 for t in tl} == {1 - sg["phase0_w"]}
+
+
+@pytest.mark.parametrize("dil", [6, 12, 18, 24])
+def test_aspp_phase_views(dil):
+    """A 'same' 3x3 dilated conv on 64x64 splits into dil x dil phase views; the
+    planner groups views of equal shape, and with border classes the segments
+    issue only their non-zero taps (plus M-tile padding)."""
+    d = h2.make_desc(8, 2048, 64, 64, 256, 3, 3, 1, dil, 0, dil, h2.HUGE2_NHWC, h2.HUGE2_BF16)
+    segs, taps = h2.huge2_plan_describe(d, 0, 2)
+    phases = set()
+    for sg in segs:
+        assert sg["out_step_h"] == dil and sg["in_step_h"] == dil
+        for a in range(sg["nphase_h"]):
+            for b in range(sg["nphase_w"]):
+                phases.add((sg["phase0_h"] + a, sg["phase0_w"] + b))
+    assert phases == {(a, b) for a in range(dil) for b in range(dil)}
+    nz, issued = h2.huge2_plan_macs(d, 0)
+    expect = {6: 135.9e9, 12: 118.4e9, 18: 102.1e9, 24: 86.97e9}[dil]
+    assert abs(nz - expect) / expect < 1e-3
+    assert nz <= issued <= 1.03 * nz  # only the ragged ends of M tiles are padding

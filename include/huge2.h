@@ -105,11 +105,13 @@ huge2_status huge2_plan_create(huge2_plan** out, const huge2_conv_desc* desc, in
                                const void* w, void* hip_stream);
 
 /* Run a plan: y = op(x) (+ bias).  x and y are laid out per the plan's
- * descriptor; bias is NULL or [c_out] float.  Enqueues exactly one kernel
- * (the phase GEMM, which gathers x in either layout itself) on hip_stream.
- * A plan is immutable once created; concurrent executes of one plan on
- * different streams are safe.  Errors: INVALID_ARG (null plan/x/y, x == y),
- * HIP (launch failure). */
+ * descriptor; bias is NULL or [c_out] float.  Enqueues on hip_stream the
+ * phase GEMM kernel, preceded, when x is NCHW or its channel count is not a
+ * multiple of 16 bytes, by a kernel that re-lays x out into the plan's
+ * channel-contiguous staging buffer.  A plan is immutable once created; two
+ * executes of one plan that needs staging must not overlap (they share the
+ * staging buffer).  Errors: INVALID_ARG (null plan/x/y, x == y), HIP (launch
+ * failure). */
 huge2_status huge2_plan_execute(const huge2_plan* plan, const void* x, const float* bias, void* y,
                                 void* hip_stream);
 

@@ -2,8 +2,9 @@
 //
 // plan_create runs the host-side decomposition (plan.cpp), lays the
 // segments, taps and GEMM work list out for the device, and packs the
-// weights; plan_execute enqueues the phase GEMM (one kernel).  No exception
-// crosses the ABI.
+// weights; plan_execute enqueues the phase GEMM (preceded by an input
+// re-layout when the input is NCHW or has a ragged channel count).  No
+// exception crosses the ABI.
 #include <hip/hip_runtime.h>
 
 #include <cstdlib>
@@ -22,11 +23,14 @@ struct huge2_plan {
   int transposed;
   int ho, wo;
   int cfg;
-  int in_mode;
+  bool staged;    // input re-laid out into xs first
+  int c_stride;   // channels per pixel of the GEMM's input
   int cin_pad, cout_pad;
+  size_t x_bytes, wp_bytes;  // extents of the GEMM's input and packed weights
   int n_works;
   void* wp;    // packed weights
   void* meta;  // segments, taps, work list
+  void* xs;    // staged input (or null)
   SegDev* d_segs;
   TapDev* d_taps;
   WorkDev* d_works;
@@ -53,21 +57,28 @@ int env_int(const char* name, int dflt) {
   return std::atoi(v);
 }
 
-// Tile choice: output channels <= 32 take the narrow tile; otherwise
-// 128x128, or 64x128 when 128x128 would leave most of the 256 CUs idle.
+long long count_works(const huge2_conv_desc& d, bool transposed, int class_split, int cfg) {
+  PlanShape shape;
+  const int bm = tile_bm(cfg), bn = tile_bn(cfg);
+  if (!build_shape(d, transposed, class_split, bm, &shape)) return 0;
+  long long works = 0;
+  const long long ntiles = (d.c_out + bn - 1) / bn;
+  for (const huge2_segment& s : shape.segs) {
+    long long m = (long long)d.n * s.nphase_h * s.nphase_w * s.qn_h * s.qn_w;
+    works += (m + bm - 1) / bm * ntiles;
+  }
+  return works;
+}
+
+// Tile choice: output channels <= 32 take the narrow tile; otherwise the
+// largest tile that still gives every one of the 256 CUs a workgroup.
 int choose_cfg(const huge2_conv_desc& d, bool transposed, int class_split) {
   int forced = env_int("HUGE2_TILE", -1);
   if (forced >= 0 && forced < TILE_COUNT) return forced;
   if (d.c_out <= 32) return TILE_256x32;
-  PlanShape shape;
-  if (!build_shape(d, transposed, class_split, tile_bm(TILE_128x128), &shape)) return TILE_128x128;
-  long long works = 0;
-  const long long ntiles = (d.c_out + 127) / 128;
-  for (const huge2_segment& s : shape.segs) {
-    long long m = (long long)d.n * s.nphase_h * s.nphase_w * s.qn_h * s.qn_w;
-    works += (m + 127) / 128 * ntiles;
-  }
-  return works < 256 ? TILE_64x128 : TILE_128x128;
+  if (count_works(d, transposed, class_split, TILE_256x128) >= 256) return TILE_256x128;
+  if (count_works(d, transposed, class_split, TILE_128x128) >= 256) return TILE_128x128;
+  return TILE_64x128;
 }
 
 int class_split_mode() {
@@ -76,7 +87,7 @@ int class_split_mode() {
 }
 
 void free_buffers(huge2_plan* p) {
-  void* bufs[2] = {p->wp, p->meta};
+  void* bufs[3] = {p->wp, p->meta, p->xs};
   for (void* b : bufs) {
     if (!b) continue;
     if (p->stream_ordered)
@@ -84,7 +95,7 @@ void free_buffers(huge2_plan* p) {
     else
       (void)hipFree(b);
   }
-  p->wp = p->meta = nullptr;
+  p->wp = p->meta = p->xs = nullptr;
 }
 
 huge2_status dev_alloc(huge2_plan* p, void** out, size_t bytes) {
@@ -127,7 +138,11 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   const int esz = elem_size(d.dtype);
   const int vec = 16 / esz;
   const int bk = kBlockK_bytes / esz;
-  p->in_mode = d.layout == HUGE2_NCHW ? IN_NCHW : (d.c_in % vec == 0 ? IN_NHWC_VEC : IN_NHWC_ELEM);
+  // NCHW inputs and ragged channel counts are re-laid out to channel-
+  // contiguous pixels (channel count padded to 16 bytes) by a staging kernel.
+  p->staged = !(d.layout == HUGE2_NHWC && d.c_in % vec == 0);
+  p->c_stride = p->staged ? round_up(d.c_in, vec) : d.c_in;
+  p->x_bytes = (size_t)d.n * d.h * d.w * p->c_stride * esz;
   p->cin_pad = round_up(d.c_in, bk);
   p->cout_pad = round_up(d.c_out, bn);
   p->stream_ordered = stream_ordered;
@@ -170,6 +185,20 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     sd.in_step_w = s.in_step_w;
     sd.tap_begin = s.tap_begin;
     sd.tap_count = s.tap_count;
+    // exact: every tap's read is in range for every pixel of the segment (the
+    // input coordinate is affine and non-decreasing in phase and q, so the
+    // extremes are at the segment's corners)
+    sd.exact = 1;
+    for (int t = s.tap_begin; t < s.tap_begin + s.tap_count; ++t) {
+      const huge2_tap& tp = shape.taps[t];
+      const long long h_lo = s.in0_h + (long long)s.in_step_h * s.q0_h + tp.off_h;
+      const long long h_hi = s.in0_h + (long long)s.in_dphase_h * (s.nphase_h - 1) +
+                             (long long)s.in_step_h * (s.q0_h + s.qn_h - 1) + tp.off_h;
+      const long long w_lo = s.in0_w + (long long)s.in_step_w * s.q0_w + tp.off_w;
+      const long long w_hi = s.in0_w + (long long)s.in_dphase_w * (s.nphase_w - 1) +
+                             (long long)s.in_step_w * (s.q0_w + s.qn_w - 1) + tp.off_w;
+      if (h_lo < 0 || h_hi >= d.h || w_lo < 0 || w_hi >= d.w) sd.exact = 0;
+    }
     segs.push_back(sd);
     for (int m0 = 0; m0 < sd.m_total; m0 += bm)
       for (int nt = 0; nt < ntiles_n; ++nt) {
@@ -190,9 +219,12 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   const size_t work_b = works.size() * sizeof(WorkDev);
   const size_t meta_b = seg_b + tap_b + work_b;
   const size_t wp_b = (size_t)d.r * d.s * p->cout_pad * p->cin_pad * esz;
+  const size_t xs_b = p->staged ? p->x_bytes : 0;
+  p->wp_bytes = wp_b;
 
   if ((st = dev_alloc(p, &p->meta, meta_b)) != HUGE2_OK ||
-      (st = dev_alloc(p, &p->wp, wp_b)) != HUGE2_OK) {
+      (st = dev_alloc(p, &p->wp, wp_b)) != HUGE2_OK ||
+      (st = dev_alloc(p, &p->xs, xs_b)) != HUGE2_OK) {
     free_buffers(p);
     delete p;
     return st;
@@ -229,8 +261,17 @@ huge2_status execute_impl(const huge2_plan* p, const void* x, const float* bias,
   if (!p || !x || !y || x == y) return HUGE2_ERR_INVALID_ARG;
   const huge2_conv_desc& d = p->desc;
   if (fault("launch")) return HUGE2_ERR_HIP;
+  const void* xin = x;
+  if (p->staged) {
+    if (launch_stage_input(x, p->xs, d.dtype, d.layout == HUGE2_NCHW, d.n, d.c_in, d.h * d.w,
+                           p->c_stride, stream) != hipSuccess) {
+      (void)hipGetLastError();
+      return HUGE2_ERR_HIP;
+    }
+    xin = p->xs;
+  }
   GemmArgs a;
-  a.x = x;
+  a.x = xin;
   a.wp = p->wp;
   a.bias = bias;
   a.y = y;
@@ -241,13 +282,15 @@ huge2_status execute_impl(const huge2_plan* p, const void* x, const float* bias,
   a.n = d.n;
   a.h = d.h;
   a.w = d.w;
-  a.cin = d.c_in;
+  a.cin = p->c_stride;
+  a.x_bytes = (uint32_t)p->x_bytes;
+  a.wp_bytes = (uint32_t)p->wp_bytes;
   a.cin_pad = p->cin_pad;
   a.cout = d.c_out;
   a.cout_pad = p->cout_pad;
   a.ho = p->ho;
   a.wo = p->wo;
-  if (launch_phase_gemm(a, d.dtype, p->cfg, p->in_mode, stream) != hipSuccess) {
+  if (launch_phase_gemm(a, d.dtype, p->cfg, d.layout == HUGE2_NCHW, stream) != hipSuccess) {
     (void)hipGetLastError();
     return HUGE2_ERR_HIP;
   }

@@ -10,26 +10,13 @@
 //                      (the scatter of section 3.1: disjoint, no atomics).
 //  pack_weights_kernel the per-tap sub-kernel blocks (the N x C matrix of each
 //                      kernel position, section 3.2.1), K-contiguous.
+//  stage_*_kernel      input re-layout to channel-contiguous pixels.
 #include "kernels.hpp"
 
 namespace huge2 {
 
 typedef __attribute__((ext_vector_type(16))) float f32x16;
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
-
-int tile_bm(int cfg) {
-  switch (cfg) {
-    case TILE_256x32: return 256;
-    case TILE_64x128: return 64;
-    default: return 128;
-  }
-}
-int tile_bn(int cfg) {
-  switch (cfg) {
-    case TILE_256x32: return 32;
-    default: return 128;
-  }
-}
 
 // Workgroups are dealt to the 8 XCDs round-robin (id mod 8).  Map them so
 // that each XCD runs one contiguous run of the work list: neighbouring
@@ -72,140 +59,164 @@ __device__ __forceinline__ PixelPos pixel_pos(const SegDev& sg, int nimg, int m)
 // ---------------------------------------------------------------------------
 // Phase GEMM.  A workgroup of 256 threads (4 waves) computes a BM x BN tile
 // (BM pixels of one segment, BN output channels).  The K loop runs over the
-// segment's taps and, per tap, over 64-byte blocks of input channels.  Each
-// stage holds BM + BN rows of 64 bytes in LDS (row pitch 80 bytes, so that
-// 16-byte accesses of 8 consecutive rows hit distinct banks), double
-// buffered, with the next stage's global loads issued before the current
-// stage's MFMAs.
+// segment's taps and, per tap, over KB-byte blocks of input channels (one
+// "stage").  Each stage holds BM + BN rows of KB bytes in LDS with a 16-byte
+// row pad (so that the 16-byte accesses of 8 consecutive rows hit distinct
+// banks), double buffered.  Global loads run two stages ahead through two
+// register buffers: while the MFMAs consume stage s from LDS, the loads of
+// stage s+2 are in flight and stage s+1 is written to the other LDS buffer.
 //
-// Input gather (IN_*): the tile row of a pixel at a tap is the 64-byte run of
-// channels [cb*BK, cb*BK + BK) of input pixel (ih, iw) = pixel base + tap
-// offset; rows that fall outside the input (or past cin) are zero.
-//   IN_NHWC_VEC : 4 lanes per pixel, one 16-byte load each.
-//   IN_NCHW     : lane j of a wave on pixel row j, one element load per
-//                 channel (consecutive lanes read consecutive input columns),
-//                 packed into 16-byte LDS writes.
-//   IN_NHWC_ELEM: as IN_NCHW, for NHWC inputs whose channel count is not a
-//                 multiple of 16 bytes.
+// The input is channel-contiguous ([n][h][w][cin], cin a multiple of 16
+// bytes).  The tile row of a pixel at a tap is the run of channels
+// [cb*KC, cb*KC + KC) of input pixel (ih, iw) = pixel base + tap offset,
+// fetched as KB/16 buffer loads of 16 bytes by KB/16 neighbouring lanes.
+// Rows outside the input get an out-of-range buffer offset, which the
+// hardware returns as zeros: the loads are branch-free, so the compiler can
+// keep the next stages' loads in flight while it waits for the current one.
 //
-// MFMA operands are K-contiguous per lane: lane l reads 32 bytes of its row
-// at byte offset 32*(l/32).  The K order inside a stage is permuted
+// MFMA operands are K-contiguous per lane: lane l reads KB/2 bytes of its
+// row at byte offset (KB/2)*(l/32).  The K order inside a stage is permuted
 // identically for both operands, which leaves the contraction unchanged:
-//   bf16: MFMA t (t = 0,1) uses row elements [16h + 8t, 16h + 8t + 8), h = l/32
-//   fp32: MFMA t (t = 0..7) uses row element 8h + t.
-// NHWC output puts pixels on MFMA rows (lanes hold consecutive channels, so
-// the stores of a pixel's channels coalesce); NCHW output puts pixels on MFMA
-// columns (lanes hold consecutive pixels).
-template <bool BF16, int BM, int BN, int PWAVES, int CWAVES, int IN_MODE>
-__global__ __launch_bounds__(256) void phase_gemm_kernel(GemmArgs a) {
-  constexpr bool NHWC_OUT = IN_MODE != IN_NCHW;
-  constexpr bool VEC_IN = IN_MODE == IN_NHWC_VEC;
+//   bf16: MFMA t uses row elements [h*KC/2 + 8t, h*KC/2 + 8t + 8), h = l/32
+//   fp32: MFMA t uses row element h*KC/2 + t.
+// NCHW output puts pixels on MFMA columns (lanes hold consecutive pixels, so
+// a channel's stores coalesce); NHWC output puts pixels on MFMA rows (lanes
+// hold consecutive channels of a pixel).
+template <bool BF16, int BM, int BN, int PWAVES, int CWAVES, int KB, bool NCHW_OUT>
+__global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmArgs a) {
+  constexpr int NT = PWAVES * CWAVES * 64;  // threads per workgroup
   constexpr int ESZ = BF16 ? 2 : 4;
-  constexpr int BK = kBlockK_bytes / ESZ;  // K elements per stage
-  constexpr int VE = 16 / ESZ;             // elements per 16-byte chunk
-  constexpr int ROWB = 80;
+  constexpr int KC = KB / ESZ;    // K elements per stage
+  constexpr int VE = 16 / ESZ;    // elements per 16-byte chunk
+  constexpr int CPR = KB / 16;    // 16-byte chunks per row
+  constexpr int ROWB = KB + 16;   // LDS row pitch
   constexpr int WP = BM / PWAVES, WC = BN / CWAVES;
   constexpr int TP = WP / 32, TC = WC / 32;
-  constexpr int A_LD = BM * 4 / 256;
-  constexpr int B_LD = (BN * 4 + 255) / 256;
-  static_assert(BM % 64 == 0, "A-tile rows per thread");
-  static_assert(PWAVES * CWAVES == 4, "4 waves");
+  constexpr int A_LD = BM * CPR / NT;
+  constexpr int B_LD = BN * CPR / NT;
+  constexpr int KSUB = BF16 ? KB / 32 : KB / 8;  // MFMAs per operand pair and stage
+  static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "whole loads per thread");
   static_assert(TP >= 1 && TC >= 1 && WP % 32 == 0 && WC % 32 == 0, "32x32 MFMA blocks");
   constexpr int STAGE_B = (BM + BN) * ROWB;
+  constexpr uint32_t OOB = 0x80000000u;  // beyond every buffer: loads return 0
   __shared__ __attribute__((aligned(16))) char smem[2 * STAGE_B];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int work = xcd_remap(blockIdx.x, gridDim.x);
   const WorkDev wk = a.works[work];
   const SegDev sg = a.segs[wk.seg];
-  const char* xb = (const char*)a.x;
-  const char* wb = (const char*)a.wp;
+  const __amdgpu_buffer_rsrc_t xr =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.x, 0, a.x_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t wr =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.wp, 0, a.wp_bytes, 0x00020000);
 
-  // The A-tile units (row, 16-byte chunk) this thread loads, and their pixels'
-  // input coordinates before the tap offset.
-  int a_row[A_LD], a_chunk[A_LD], a_ih[A_LD], a_iw[A_LD], a_img[A_LD];
+  // This thread's A-tile rows (pixels) and its 16-byte chunk within a row.
+  // Rows past the end of the segment repeat its last pixel: they compute
+  // values the epilogue never stores.
+  const int chunk = tid % CPR;
+  int a_ih[A_LD], a_iw[A_LD];
+  uint32_t a_base[A_LD];  // byte offset of (pixel, chunk) at tap offset (0, 0)
 #pragma unroll
   for (int i = 0; i < A_LD; ++i) {
-    const int u = tid + 256 * i;
-    a_row[i] = VEC_IN ? (u >> 2) : (u % BM);
-    a_chunk[i] = VEC_IN ? (u & 3) : (u / BM);
-    const int m = wk.m0 + a_row[i];
-    if (m < sg.m_total) {
-      const PixelPos p = pixel_pos(sg, a.n, m);
-      a_ih[i] = p.ih;
-      a_iw[i] = p.iw;
-      a_img[i] = p.img;
-    } else {
-      a_ih[i] = -(1 << 29);  // fails every bounds test
-      a_iw[i] = 0;
-      a_img[i] = 0;
+    const int m = min(wk.m0 + tid / CPR + (NT / CPR) * i, sg.m_total - 1);
+    const PixelPos p = pixel_pos(sg, a.n, m);
+    a_ih[i] = p.ih;
+    a_iw[i] = p.iw;
+    // unsigned (wrapping) arithmetic: the tap offset brings it back in range
+    a_base[i] = (((uint32_t)p.img * (uint32_t)a.h + (uint32_t)p.ih) * (uint32_t)a.w +
+                 (uint32_t)p.iw) * (uint32_t)a.cin * ESZ + (uint32_t)(chunk * VE * ESZ);
+  }
+  const int ntaps = sg.tap_count;
+  const int cblocks = a.cin_pad / KC;
+  const int nsteps = ntaps * cblocks;
+  // channels of the last K block that exist (a partial block needs masking)
+  const int tail_c = a.cin - (cblocks - 1) * KC;
+
+  // The segment's taps in LDS: byte delta of the tapped pixel and byte
+  // offset of the tap's weight block.
+  __shared__ int4 s_taps[kMaxLdsTaps];
+  const bool lds_taps = ntaps <= kMaxLdsTaps;
+  if (lds_taps) {
+    for (int t = tid; t < ntaps; t += NT) {
+      const TapDev tp = a.taps[sg.tap_begin + t];
+      s_taps[t] = make_int4((tp.off_h * a.w + tp.off_w) * a.cin * ESZ,
+                            (int)((uint32_t)tp.slot * (uint32_t)a.cout_pad * (uint32_t)a.cin_pad * ESZ),
+                            tp.off_h, tp.off_w);
     }
   }
-  const int hw = a.h * a.w;
+  __syncthreads();
 
-  const int cblocks = a.cin_pad / BK;
-  const int nsteps = sg.tap_count * cblocks;
-  uint4 ra[A_LD], rb[B_LD];
+  struct Regs {
+    uint4 a[A_LD];
+    uint4 b[B_LD];
+  };
+  Regs r0, r1;
 
-  auto load_step = [&](int s) {
-    const int t = s / cblocks, cb = s - t * cblocks;
-    const TapDev tp = a.taps[sg.tap_begin + t];
+  uint32_t voff_b[B_LD];  // per B row: byte offset within a tap's weight block
+#pragma unroll
+  for (int i = 0; i < B_LD; ++i)
+    voff_b[i] = (uint32_t)(((wk.n0 + tid / CPR + (NT / CPR) * i) * a.cin_pad + chunk * VE) * ESZ);
+
+  // Resources with no records: every load through them returns zero.
+  const __amdgpu_buffer_rsrc_t xr0 =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.x, 0, 0, 0x00020000);
+  const __amdgpu_buffer_rsrc_t wr0 =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.wp, 0, 0, 0x00020000);
+
+  // K order: channel block outer, tap inner, so that the taps of one channel
+  // block re-read the same input rows while they are still in cache.  A load
+  // past the last stage goes through the empty resources instead of
+  // branching around the loads: the load sequence stays the same on every
+  // path, which lets the compiler wait only for the stage it stores.
+  int ld_tap = 0, ld_cb = 0;
+  auto load_step = [&](Regs& R, bool valid) {
+    const __amdgpu_buffer_rsrc_t xs = valid ? xr : xr0;
+    const __amdgpu_buffer_rsrc_t ws = valid ? wr : wr0;
+    int4 ti;
+    if (lds_taps) {
+      ti = s_taps[valid ? ld_tap : 0];
+    } else {
+      const TapDev tp = a.taps[sg.tap_begin + (valid ? ld_tap : 0)];
+      ti = make_int4((tp.off_h * a.w + tp.off_w) * a.cin * ESZ,
+                     (int)((uint32_t)tp.slot * (uint32_t)a.cout_pad * (uint32_t)a.cin_pad * ESZ),
+                     tp.off_h, tp.off_w);
+    }
+    const int delta = __builtin_amdgcn_readfirstlane(ti.x);
+    const uint32_t slot_b = (uint32_t)__builtin_amdgcn_readfirstlane(ti.y);
+    const int off_h = __builtin_amdgcn_readfirstlane(ti.z);
+    const int off_w = __builtin_amdgcn_readfirstlane(ti.w);
+    const uint32_t kb = (uint32_t)ld_cb * KB;
+    const bool tail = ld_cb == cblocks - 1 && tail_c < KC;
+    const bool chunk_out = tail && chunk * VE >= tail_c;
 #pragma unroll
     for (int i = 0; i < A_LD; ++i) {
-      const int ih = a_ih[i] + tp.off_h, iw = a_iw[i] + tp.off_w;
-      const bool in = (unsigned)ih < (unsigned)a.h && (unsigned)iw < (unsigned)a.w;
-      const int c0 = cb * BK + a_chunk[i] * VE;
-      if constexpr (VEC_IN) {
-        if (in && c0 < a.cin) {
-          const size_t off = ((size_t)a_img[i] * hw + ih * a.w + iw) * a.cin + c0;
-          ra[i] = *(const uint4*)(xb + off * ESZ);
-        } else {
-          ra[i] = make_uint4(0, 0, 0, 0);
-        }
-      } else {
-        uint32_t v[VE];
-#pragma unroll
-        for (int e = 0; e < VE; ++e) {
-          const int c = c0 + e;
-          v[e] = 0;
-          if (in && c < a.cin) {
-            const size_t off = IN_MODE == IN_NCHW
-                                   ? ((size_t)a_img[i] * a.cin + c) * hw + ih * a.w + iw
-                                   : ((size_t)a_img[i] * hw + ih * a.w + iw) * a.cin + c;
-            if constexpr (BF16)
-              v[e] = *(const uint16_t*)(xb + off * 2);
-            else
-              v[e] = *(const uint32_t*)(xb + off * 4);
-          }
-        }
-        if constexpr (BF16)
-          ra[i] = make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16),
-                             v[6] | (v[7] << 16));
-        else
-          ra[i] = make_uint4(v[0], v[1], v[2], v[3]);
+      uint32_t v = a_base[i] + (uint32_t)delta;
+      if (!sg.exact) {
+        const int ih = a_ih[i] + off_h, iw = a_iw[i] + off_w;
+        const bool in = ((unsigned)ih < (unsigned)a.h) & ((unsigned)iw < (unsigned)a.w);
+        v = in ? v : OOB;
       }
+      v = chunk_out ? OOB : v;
+      R.a[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xs, v, kb, 0));
     }
 #pragma unroll
-    for (int i = 0; i < B_LD; ++i) {
-      const int idx = tid + 256 * i;
-      if (idx < BN * 4) {
-        const int row = idx >> 2;
-        const size_t off = ((size_t)tp.slot * a.cout_pad + wk.n0 + row) * a.cin_pad + cb * BK +
-                           (idx & 3) * VE;
-        rb[i] = *(const uint4*)(wb + off * ESZ);
-      }
+    for (int i = 0; i < B_LD; ++i)
+      R.b[i] = __builtin_bit_cast(
+          uint4, __builtin_amdgcn_raw_buffer_load_b128(ws, voff_b[i], slot_b + kb, 0));
+    if (valid && ++ld_tap == ntaps) {
+      ld_tap = 0;
+      ++ld_cb;
     }
   };
-  auto store_stage = [&](int buf) {
+  auto store_stage = [&](int buf, const Regs& R) {
     char* as = smem + buf * STAGE_B;
     char* bs = as + BM * ROWB;
 #pragma unroll
-    for (int i = 0; i < A_LD; ++i) *(uint4*)(as + a_row[i] * ROWB + a_chunk[i] * 16) = ra[i];
+    for (int i = 0; i < A_LD; ++i)
+      *(uint4*)(as + (tid / CPR + (NT / CPR) * i) * ROWB + chunk * 16) = R.a[i];
 #pragma unroll
-    for (int i = 0; i < B_LD; ++i) {
-      const int idx = tid + 256 * i;
-      if (idx < BN * 4) *(uint4*)(bs + (idx >> 2) * ROWB + (idx & 3) * 16) = rb[i];
-    }
+    for (int i = 0; i < B_LD; ++i)
+      *(uint4*)(bs + (tid / CPR + (NT / CPR) * i) * ROWB + chunk * 16) = R.b[i];
   };
 
   f32x16 acc[TP][TC];
@@ -217,60 +228,73 @@ __global__ __launch_bounds__(256) void phase_gemm_kernel(GemmArgs a) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int wp_i = wave % PWAVES, wc_i = wave / PWAVES;
-  if (nsteps > 0) {
-    load_step(0);
-    store_stage(0);
-    __syncthreads();
-    for (int s = 0; s < nsteps; ++s) {
-      const int cur = s & 1;
-      if (s + 1 < nsteps) load_step(s + 1);
-      const char* as = smem + cur * STAGE_B;
-      const char* bs = as + BM * ROWB;
-      uint4 fp[TP][2], fc[TC][2];
+  auto compute = [&](int buf) {
+    const char* as = smem + buf * STAGE_B + (wp_i * WP + (lane & 31)) * ROWB + (lane >> 5) * (KB / 2);
+    const char* bs = smem + buf * STAGE_B + (BM + wc_i * WC + (lane & 31)) * ROWB + (lane >> 5) * (KB / 2);
+    if constexpr (BF16) {
 #pragma unroll
-      for (int i = 0; i < TP; ++i) {
-        const char* p = as + (wp_i * WP + 32 * i + (lane & 31)) * ROWB + (lane >> 5) * 32;
-        fp[i][0] = *(const uint4*)p;
-        fp[i][1] = *(const uint4*)(p + 16);
+      for (int t = 0; t < KSUB; ++t) {
+        uint4 fp[TP], fc[TC];
+#pragma unroll
+        for (int i = 0; i < TP; ++i) fp[i] = *(const uint4*)(as + 32 * i * ROWB + 16 * t);
+#pragma unroll
+        for (int j = 0; j < TC; ++j) fc[j] = *(const uint4*)(bs + 32 * j * ROWB + 16 * t);
+#pragma unroll
+        for (int i = 0; i < TP; ++i)
+#pragma unroll
+          for (int j = 0; j < TC; ++j) {
+            const bf16x8 vp = __builtin_bit_cast(bf16x8, fp[i]);
+            const bf16x8 vc = __builtin_bit_cast(bf16x8, fc[j]);
+            if constexpr (NCHW_OUT)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vc, vp, acc[i][j], 0, 0, 0);
+            else
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vp, vc, acc[i][j], 0, 0, 0);
+          }
       }
+    } else {
 #pragma unroll
-      for (int j = 0; j < TC; ++j) {
-        const char* p = bs + (wc_i * WC + 32 * j + (lane & 31)) * ROWB + (lane >> 5) * 32;
-        fc[j][0] = *(const uint4*)p;
-        fc[j][1] = *(const uint4*)(p + 16);
-      }
-      if constexpr (BF16) {
+      for (int t4 = 0; t4 < KSUB / 4; ++t4) {
+        uint4 fp[TP], fc[TC];
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+        for (int i = 0; i < TP; ++i) fp[i] = *(const uint4*)(as + 32 * i * ROWB + 16 * t4);
+#pragma unroll
+        for (int j = 0; j < TC; ++j) fc[j] = *(const uint4*)(bs + 32 * j * ROWB + 16 * t4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
 #pragma unroll
           for (int i = 0; i < TP; ++i)
 #pragma unroll
             for (int j = 0; j < TC; ++j) {
-              const bf16x8 vp = __builtin_bit_cast(bf16x8, fp[i][t]);
-              const bf16x8 vc = __builtin_bit_cast(bf16x8, fc[j][t]);
-              if constexpr (NHWC_OUT)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vp, vc, acc[i][j], 0, 0, 0);
-              else
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vc, vp, acc[i][j], 0, 0, 0);
-            }
-      } else {
-#pragma unroll
-        for (int t = 0; t < 8; ++t)
-#pragma unroll
-          for (int i = 0; i < TP; ++i)
-#pragma unroll
-            for (int j = 0; j < TC; ++j) {
-              const uint4 up = fp[i][t >> 2], uc = fc[j][t >> 2];
-              const uint32_t bp = (t & 3) == 0 ? up.x : (t & 3) == 1 ? up.y : (t & 3) == 2 ? up.z : up.w;
-              const uint32_t bc = (t & 3) == 0 ? uc.x : (t & 3) == 1 ? uc.y : (t & 3) == 2 ? uc.z : uc.w;
+              const uint32_t bp = e == 0 ? fp[i].x : e == 1 ? fp[i].y : e == 2 ? fp[i].z : fp[i].w;
+              const uint32_t bc = e == 0 ? fc[j].x : e == 1 ? fc[j].y : e == 2 ? fc[j].z : fc[j].w;
               const float vp = __uint_as_float(bp), vc = __uint_as_float(bc);
-              if constexpr (NHWC_OUT)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(vp, vc, acc[i][j], 0, 0, 0);
-              else
+              if constexpr (NCHW_OUT)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(vc, vp, acc[i][j], 0, 0, 0);
+              else
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(vp, vc, acc[i][j], 0, 0, 0);
             }
       }
-      if (s + 1 < nsteps) store_stage(cur ^ 1);
+    }
+  };
+
+  // Main loop, unrolled by two so that the two register buffers alternate
+  // statically; an odd stage count is padded with one all-zero stage.
+  // Invariant at the top of each half: LDS buffer (s & 1) holds stage s and
+  // the other register buffer is receiving stage s+1.
+  const int nsteps2 = (nsteps + 1) & ~1;
+  if (nsteps2 > 0) {
+    load_step(r0, true);
+    store_stage(0, r0);
+    load_step(r0, 1 < nsteps);
+    __syncthreads();
+    for (int s = 0; s < nsteps2; s += 2) {
+      load_step(r1, s + 2 < nsteps);
+      compute(0);
+      store_stage(1, r0);
+      __syncthreads();
+      load_step(r0, s + 3 < nsteps);
+      compute(1);
+      store_stage(0, r1);
       __syncthreads();
     }
   }
@@ -279,7 +303,7 @@ __global__ __launch_bounds__(256) void phase_gemm_kernel(GemmArgs a) {
   // 32x32 MFMA result layout: lane l holds column l%32 and rows
   // 8*(r/4) + 4*(l/32) + (r%4) for r = 0..15.
   const int hw_o = a.ho * a.wo;
-  if constexpr (NHWC_OUT) {
+  if constexpr (!NCHW_OUT) {
 #pragma unroll
     for (int i = 0; i < TP; ++i) {
 #pragma unroll
@@ -328,20 +352,74 @@ __global__ __launch_bounds__(256) void phase_gemm_kernel(GemmArgs a) {
   }
 }
 
-template <bool BF16, int IN_MODE>
+int tile_bm(int cfg) {
+  switch (cfg) {
+    case TILE_256x32:
+    case TILE_256x128:
+    case TILE_256x256_W8:
+    case TILE_256x128_W8: return 256;
+    case TILE_64x128: return 64;
+    default: return 128;
+  }
+}
+int tile_bn(int cfg) {
+  switch (cfg) {
+    case TILE_256x32: return 32;
+    case TILE_128x256:
+    case TILE_256x256_W8:
+    case TILE_128x256_W8: return 256;
+    default: return 128;
+  }
+}
+int tile_threads(int cfg) {
+  switch (cfg) {
+    case TILE_256x256_W8:
+    case TILE_256x128_W8:
+    case TILE_128x256_W8:
+    case TILE_128x128_W8: return 512;
+    default: return 256;
+  }
+}
+
+template <bool BF16, bool NCHW_OUT>
 static hipError_t launch_cfg(const GemmArgs& a, int cfg, hipStream_t stream) {
-  dim3 grid(a.n_works), block(256);
+  dim3 grid(a.n_works), block(tile_threads(cfg));
+  constexpr int KB = kBlockK_bytes;
   switch (cfg) {
     case TILE_128x128:
-      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 128, 128, 2, 2, IN_MODE>), grid, block, 0,
+      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 128, 128, 2, 2, KB, NCHW_OUT>), grid, block, 0,
                          stream, a);
       break;
     case TILE_256x32:
-      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 256, 32, 4, 1, IN_MODE>), grid, block, 0,
+      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 256, 32, 4, 1, KB, NCHW_OUT>), grid, block, 0,
                          stream, a);
       break;
     case TILE_64x128:
-      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 64, 128, 1, 4, IN_MODE>), grid, block, 0,
+      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 64, 128, 1, 4, KB, NCHW_OUT>), grid, block, 0,
+                         stream, a);
+      break;
+    case TILE_256x128:
+      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 256, 128, 2, 2, KB, NCHW_OUT>), grid, block, 0,
+                         stream, a);
+      break;
+    case TILE_128x256:
+      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 128, 256, 2, 2, KB, NCHW_OUT>), grid, block, 0,
+                         stream, a);
+      break;
+    case TILE_256x256_W8:
+      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 256, 256, 2, 4, KB, NCHW_OUT>), grid, block, 0,
+                         stream, a);
+      break;
+    case TILE_256x128_W8:
+      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 256, 128, 4, 2, KB, NCHW_OUT>), grid, block, 0,
+                         stream, a);
+      break;
+    case TILE_128x256_W8:
+      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 128, 256, 2, 4, KB, NCHW_OUT>), grid, block, 0,
+                         stream, a);
+      break;
+    case TILE_128x128_W8:
+      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 128, 128, 4, 2, KB, NCHW_OUT>), grid, block, 0,
                          stream, a);
       break;
     default:
@@ -350,21 +428,12 @@ static hipError_t launch_cfg(const GemmArgs& a, int cfg, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <bool BF16>
-static hipError_t launch_mode(const GemmArgs& a, int cfg, int in_mode, hipStream_t stream) {
-  switch (in_mode) {
-    case IN_NHWC_VEC: return launch_cfg<BF16, IN_NHWC_VEC>(a, cfg, stream);
-    case IN_NCHW: return launch_cfg<BF16, IN_NCHW>(a, cfg, stream);
-    case IN_NHWC_ELEM: return launch_cfg<BF16, IN_NHWC_ELEM>(a, cfg, stream);
-  }
-  return hipErrorInvalidValue;
-}
-
-hipError_t launch_phase_gemm(const GemmArgs& a, int dtype, int cfg, int in_mode,
+hipError_t launch_phase_gemm(const GemmArgs& a, int dtype, int cfg, bool nchw_out,
                              hipStream_t stream) {
   if (a.n_works <= 0) return hipSuccess;
-  return dtype == 1 ? launch_mode<true>(a, cfg, in_mode, stream)
-                    : launch_mode<false>(a, cfg, in_mode, stream);
+  if (dtype == 1)
+    return nchw_out ? launch_cfg<true, true>(a, cfg, stream) : launch_cfg<true, false>(a, cfg, stream);
+  return nchw_out ? launch_cfg<false, true>(a, cfg, stream) : launch_cfg<false, false>(a, cfg, stream);
 }
 
 // ---------------------------------------------------------------------------
@@ -407,6 +476,66 @@ hipError_t launch_pack_weights(const void* w, void* wp, int dtype, bool transpos
     hipLaunchKernelGGL(pack_weights_kernel<uint32_t>, dim3(grid), dim3(block), 0, stream,
                        (const uint32_t*)w, (uint32_t*)wp, transposed, cin, cout, r, s, cin_pad,
                        cout_pad, total);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Input staging: channel-contiguous pixels [n][h*w][c_stride], zero padded
+// channels, for NCHW inputs and for NHWC inputs whose channel count is not a
+// multiple of 16 bytes.
+
+// NCHW source: a 64-channel x 64-pixel block per workgroup through LDS.
+template <typename T>
+__global__ __launch_bounds__(256) void stage_nchw_kernel(const T* __restrict__ x,
+                                                         T* __restrict__ xs, int cin, int hw,
+                                                         int cs) {
+  __shared__ T tile[64][65];
+  const int img = blockIdx.z, c0 = blockIdx.y * 64, p0 = blockIdx.x * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int c = c0 + i, p = p0 + tx;
+    tile[i][tx] = (c < cin && p < hw) ? x[((size_t)img * cin + c) * hw + p] : T(0);
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int p = p0 + i, c = c0 + tx;
+    if (p < hw && c < cs) xs[((size_t)img * hw + p) * cs + c] = tile[tx][i];
+  }
+}
+
+// NHWC source with cin channels per pixel.
+template <typename T>
+__global__ void stage_nhwc_kernel(const T* __restrict__ x, T* __restrict__ xs, int cin, int cs,
+                                  long long total) {
+  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const int c = (int)(idx % cs);
+    const long long p = idx / cs;
+    xs[idx] = c < cin ? x[p * cin + c] : T(0);
+  }
+}
+
+hipError_t launch_stage_input(const void* x, void* xs, int dtype, bool nchw, int n, int cin,
+                              int hw, int c_stride, hipStream_t stream) {
+  if (nchw) {
+    dim3 grid((hw + 63) / 64, (c_stride + 63) / 64, n), block(256);
+    if (dtype == 1)
+      hipLaunchKernelGGL(stage_nchw_kernel<uint16_t>, grid, block, 0, stream,
+                         (const uint16_t*)x, (uint16_t*)xs, cin, hw, c_stride);
+    else
+      hipLaunchKernelGGL(stage_nchw_kernel<uint32_t>, grid, block, 0, stream,
+                         (const uint32_t*)x, (uint32_t*)xs, cin, hw, c_stride);
+  } else {
+    const long long total = (long long)n * hw * c_stride;
+    const long long want = (total + 255) / 256;
+    const int grid = (int)(want < 65536 ? want : 65536);
+    if (dtype == 1)
+      hipLaunchKernelGGL(stage_nhwc_kernel<uint16_t>, dim3(grid), dim3(256), 0, stream,
+                         (const uint16_t*)x, (uint16_t*)xs, cin, c_stride, total);
+    else
+      hipLaunchKernelGGL(stage_nhwc_kernel<uint32_t>, dim3(grid), dim3(256), 0, stream,
+                         (const uint32_t*)x, (uint32_t*)xs, cin, c_stride, total);
+  }
   return hipGetLastError();
 }
 

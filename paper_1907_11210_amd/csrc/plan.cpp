@@ -180,15 +180,18 @@ huge2_status validate_desc(const huge2_conv_desc* d, bool transposed) {
   }
   int ho, wo;
   if (!output_dims(*d, transposed, &ho, &wo)) return HUGE2_ERR_INVALID_ARG;
-  // The kernels index tensors with 32-bit element offsets.
+  // The kernels address the input and the packed weights through buffer
+  // resources with 32-bit byte offsets, and the output with 32-bit element
+  // offsets: every extent (with channel padding) must stay below 2^31 bytes.
   const long long lim = INT_MAX;
-  long long nx = (long long)d->n * d->c_in * d->h * d->w;
-  long long ny = (long long)d->n * d->c_out * ho * wo;
-  long long nw = (long long)d->c_in * d->c_out * d->r * d->s;
-  long long cin_pad = ((long long)d->c_in + 31) / 32 * 32;
+  const long long esz = d->dtype == HUGE2_BF16 ? 2 : 4;
+  long long cin_v = ((long long)d->c_in + 7) / 8 * 8;
+  long long cin_pad = ((long long)d->c_in + 63) / 64 * 64;
   long long cout_pad = ((long long)d->c_out + 127) / 128 * 128;
-  if (nx > lim || ny > lim || nw > lim || cin_pad * cout_pad * d->r * d->s > lim)
-    return HUGE2_ERR_UNSUPPORTED;
+  long long nx = (long long)d->n * cin_v * d->h * d->w * esz;
+  long long ny = (long long)d->n * d->c_out * ho * wo * esz;
+  long long nw = cin_pad * cout_pad * d->r * d->s * esz;
+  if (nx > lim || ny > lim || nw > lim) return HUGE2_ERR_UNSUPPORTED;
   return HUGE2_OK;
 }
 

@@ -199,3 +199,21 @@ def test_workload_full_size_sampled(wname):
         absref = P.oracle_points(layer, xq, wq, idx, absolute=True)
         P.check(y.ravel()[idx], ref, absref, layer.dtype, layer.name)
         assert np.all(np.isfinite(y))
+
+
+TILE_CONFIGS = list(range(9))  # every GEMM tile configuration of the kernel
+
+
+@pytest.mark.parametrize("tile", TILE_CONFIGS)
+def test_every_tile_configuration(tile, monkeypatch):
+    """Each tile shape (forced through HUGE2_TILE at plan creation) matches the
+    oracle on ragged transposed and dilated cases in both layouts and dtypes."""
+    monkeypatch.setenv("HUGE2_TILE", str(tile))
+    for layer in [SMALL[0], SMALL[2], SMALL[4], SMALL[7], SMALL[14], SMALL[19]]:
+        P.say("case tile", tile, layer)
+        xq, wq = _inputs(layer, seed=31 + tile)
+        bias = torch.linspace(-0.25, 0.75, layer.c_out)
+        ref = P.oracle_full(layer, xq, wq, bias)
+        absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
+        y = P.run_gpu(layer, xq, wq, bias)
+        P.check(y, ref, absref, layer.dtype, "%s tile %d" % (layer.name, tile))

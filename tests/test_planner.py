@@ -189,4 +189,4 @@ def test_aspp_phase_views(dil):
     nz, issued = h2.huge2_plan_macs(d, 0)
     expect = {6: 135.9e9, 12: 118.4e9, 18: 102.1e9, 24: 86.97e9}[dil]
     assert abs(nz - expect) / expect < 1e-3
-    assert nz <= issued <= 1.03 * nz  # only the ragged ends of M tiles are padding
+    assert nz <= issued <= 1.10 * nz  # only the ragged ends of M tiles are padding

@@ -5,14 +5,20 @@ decomposed transposed / dilated convolution on one MI355X.
 One step = one pass of every layer of the workload over one batch of seeded
 synthetic input already resident in HBM (default: the DCGAN generator's four
 ConvTranspose layers, bf16 NCHW, batch 64, chained on the device; the z ->
-linear layer is input generation and is not timed).  Each layer is one
-kernel launch (huge2_plan_execute); the plans (weight packing) are built
-before the timed region.
+linear layer is input generation and is not timed).  Each layer is an
+input-staging launch where the layout needs one (NCHW, or channels not a
+multiple of the vector width) followed by one GEMM launch
+(huge2_plan_stage_input + huge2_plan_run_gemm, the two halves of
+huge2_plan_execute); the plans (weight packing) are built before the timed
+region.
 
 Prints ONE JSON line.  Fields beyond the standard ones:
-  roofline      the dominant layer's GEMM kernel: algorithmic FLOP per launch /
-                its mean duration from HIP events on the launch stream, vs the
-                dense MFMA peak of its dtype.
+  roofline      the dominant layer's GEMM kernel (the longest mean launch, timed
+                with HIP events on the launch stream around that kernel alone):
+                algorithmic FLOP (or bytes, when its arithmetic intensity is below
+                the MI355X ridge) per launch / mean duration, vs the dense MFMA peak
+                of its dtype (or HBM bandwidth); traffic from the committed
+                rocprofv3 counter summary when it matches the kernel source.
   cpu_baseline  the CPU oracle (Algorithm 1 zero insertion / Algorithm 2
                 gather, float64) timed on a bounded sample of the workload.
   layers        per-layer mean time, effective TFLOP/s, issued-MAC utilisation.
@@ -53,8 +59,13 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="dcgan", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 256 MiB device copy (to scale HBM traffic counters)")
+    ap.add_argument("--summarize-profiles", metavar="DIR",
+                    help="no GPU: turn the rocprofv3 CSVs of PROFILE_COMMANDS under DIR into "
+                         "the summaries under profiles/")
     return ap.parse_args()
 
 
@@ -83,15 +94,174 @@ def build_workload(name, dev):
             for p, (l, _, _) in zip(plans, items)]
 
     def step(events=None):
+        # events[3*i]: before the layer's input staging, events[3*i+1]: before its
+        # GEMM kernel, events[3*i+2]: after it (all on the launch stream)
         for i, p in enumerate(plans):
             x = inputs[i] if (not chained or i == 0) else outs[i - 1]
             if events is not None:
-                events[i].record()
-            p(x, out=outs[i])
-        if events is not None:
-            events[len(plans)].record()
+                events[3 * i].record()
+            p.stage(x)
+            if events is not None:
+                events[3 * i + 1].record()
+            p.gemm(x, outs[i])
+            if events is not None:
+                events[3 * i + 2].record()
 
     return items, plans, step
+
+
+def kernel_source_sha():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "kernels.hpp", "capi.cpp", "plan.cpp"):
+        with open(os.path.join(ROOT, "paper_1907_11210_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, layer_name):
+    """HBM bytes per launch of the layer's GEMM kernel, from the committed
+    rocprofv3 counter summary, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", "phase_gemm_%s_traffic.json" % workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("kernel_source_sha") != kernel_source_sha():
+        return None
+    entry = t.get("layers", {}).get(layer_name)
+    return None if entry is None else entry.get("traffic_bytes")
+
+
+COPY_MIB = 256
+
+
+def copy_calibration(dev, mib=COPY_MIB, reps=10):
+    """A plain elementwise copy kernel (y = x * 1) of known size, to scale the
+    FETCH_SIZE / WRITE_SIZE counters: it reads and writes mib MiB per launch."""
+    import torch
+    n = mib * (1 << 20) // 4
+    a = torch.ones(n, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(reps):
+        torch.mul(a, 1.0, out=b)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n * 4, "reps": reps}), flush=True)
+
+
+# The rocprofv3 runs whose CSVs --summarize-profiles reads ($R = repository root,
+# $O = output directory).  Each line is run on its own, after
+# `cd /tmp && export TMPDIR=/tmp`.
+PROFILE_COMMANDS = [
+    ("trace", "rocprofv3 --kernel-trace --stats -f csv -d $O -o trace -- "
+              "python3 $R/bench.py --workload {w} --no-cpu-baseline"),
+    ("fetch", "timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE -f csv -d $O -o fetch -- "
+              "python3 $R/bench.py --workload {w} --no-cpu-baseline --steps 3 --warmup 1"),
+    ("write", "timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE -f csv -d $O -o write -- "
+              "python3 $R/bench.py --workload {w} --no-cpu-baseline --steps 3 --warmup 1"),
+    ("copy_fetch", "timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE -f csv -d $O -o copy_fetch -- "
+                   "python3 $R/bench.py --copy-calibration"),
+    ("copy_write", "timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE -f csv -d $O -o copy_write -- "
+                   "python3 $R/bench.py --copy-calibration"),
+]
+
+
+def _csv_rows(path):
+    import csv
+    with open(path) as f:
+        return list(csv.DictReader(f))
+
+
+def _counter_per_dispatch(path, counter):
+    """{dispatch id: (kernel name, counter value summed over instances)}"""
+    out = {}
+    for r in _csv_rows(path):
+        if r["Counter_Name"] != counter:
+            continue
+        d = int(r["Dispatch_Id"])
+        name, v = out.get(d, (r["Kernel_Name"], 0.0))
+        out[d] = (name, v + float(r["Counter_Value"]))
+    return out
+
+
+def _layer_dispatches(per_dispatch, nl):
+    """Assign the GEMM dispatches, in launch order, to the workload's layers."""
+    ids = sorted(d for d, (name, _) in per_dispatch.items() if "phase_gemm_kernel" in name)
+    by_layer = [[] for _ in range(nl)]
+    for k, d in enumerate(ids):
+        by_layer[k % nl].append(d)
+    return by_layer
+
+
+def summarize_profiles(d, workload):
+    import numpy as np
+    from paper_1907_11210_amd import workloads as wl
+
+    layers = wl.WORKLOADS[workload]
+    nl = len(layers)
+    cmds = ["cd /tmp && export TMPDIR=/tmp"] + [c.format(w=workload) for _, c in PROFILE_COMMANDS]
+    lines = ["# phase_gemm_kernel on workload `%s`: rocprofv3 kernel trace" % workload, "",
+             "Kernel source sha256[:16]: `%s`" % kernel_source_sha(), "",
+             "Commands (R = repository root, O = output directory):", "", "```"] + cmds + ["```", ""]
+
+    stats = _csv_rows(os.path.join(d, "trace_kernel_stats.csv"))
+    lines += ["## --stats (all kernels of the process)", "",
+              "| kernel | calls | average ns | total ns | % |", "|---|---|---|---|---|"]
+    for r in stats[:10]:
+        lines.append("| %s | %s | %.0f | %s | %.2f |" % (r["Name"][:110], r["Calls"],
+                                                       float(r["AverageNs"]), r["TotalDurationNs"],
+                                                       float(r["Percentage"])))
+    trace = _csv_rows(os.path.join(d, "trace_kernel_trace.csv"))
+    per = {int(r["Dispatch_Id"]): (r["Kernel_Name"], int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+           for r in trace}
+    by_layer = _layer_dispatches(per, nl)
+    lines += ["", "## phase_gemm_kernel per layer (dispatches in launch order, layer = k mod %d)" % nl,
+              "", "| layer | dispatches | mean us | min us | kernel instance |", "|---|---|---|---|---|"]
+    avg_us = {}
+    for l, ids in zip(layers, by_layer):
+        t = np.array([per[i][1] for i in ids]) / 1e3
+        avg_us[l.name] = float(t.mean())
+        name = per[ids[0]][0]
+        inst = name[name.find("<"):name.find(">") + 1] if "<" in name else name
+        lines.append("| %s | %d | %.2f | %.2f | %s |" % (l.name, len(ids), t.mean(), t.min(), inst))
+
+    traffic = None
+    if os.path.exists(os.path.join(d, "fetch_counter_collection.csv")):
+        cf = _counter_per_dispatch(os.path.join(d, "copy_fetch_counter_collection.csv"), "FETCH_SIZE")
+        cw = _counter_per_dispatch(os.path.join(d, "copy_write_counter_collection.csv"), "WRITE_SIZE")
+        copy_name = max(cf.values(), key=lambda t: t[1])[0]
+        known_kib = COPY_MIB * 1024.0
+        f_fetch = known_kib / np.mean([v for n, v in cf.values() if n == copy_name])
+        f_write = known_kib / np.mean([v for n, v in cw.values() if n == copy_name])
+        fe = _counter_per_dispatch(os.path.join(d, "fetch_counter_collection.csv"), "FETCH_SIZE")
+        wr = _counter_per_dispatch(os.path.join(d, "write_counter_collection.csv"), "WRITE_SIZE")
+        traffic = {"kernel_source_sha": kernel_source_sha(), "workload": workload,
+                   "copy_kernel": copy_name[:120], "copy_bytes": COPY_MIB << 20,
+                   "scale_fetch": round(float(f_fetch), 4), "scale_write": round(float(f_write), 4),
+                   "layers": {}}
+        lines += ["", "## HBM traffic of phase_gemm_kernel (FETCH_SIZE, WRITE_SIZE; KiB per dispatch)",
+                  "", "Calibration: a %d MiB elementwise copy reads FETCH_SIZE x %.4f and writes "
+                  "WRITE_SIZE x %.4f of its known size." % (COPY_MIB, f_fetch, f_write), "",
+                  "| layer | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled traffic MB | algorithmic MB |",
+                  "|---|---|---|---|---|"]
+        for l, fids, wids in zip(layers, _layer_dispatches(fe, nl), _layer_dispatches(wr, nl)):
+            fk = float(np.mean([fe[i][1] for i in fids]))
+            wk = float(np.mean([wr[i][1] for i in wids]))
+            tb = 1024.0 * (fk * f_fetch + wk * f_write)
+            ho, wo = l.out_hw()
+            esz = 2 if l.dtype == "bf16" else 4
+            algo = esz * (l.n * l.c_in * l.h * l.w + l.c_in * l.c_out * l.r * l.s + l.n * l.c_out * ho * wo)
+            traffic["layers"][l.name] = {"fetch_kib": round(fk, 1), "write_kib": round(wk, 1),
+                                         "traffic_bytes": int(round(tb)), "algorithmic_bytes": algo}
+            lines.append("| %s | %.1f | %.1f | %.2f | %.2f |" % (l.name, fk, wk, tb / 1e6, algo / 1e6))
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    with open(os.path.join(ROOT, "profiles", "phase_gemm_%s.md" % workload), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    if traffic is not None:
+        with open(os.path.join(ROOT, "profiles", "phase_gemm_%s_traffic.json" % workload), "w") as f:
+            json.dump(traffic, f, indent=1)
+            f.write("\n")
+    print(json.dumps({"layer_mean_us": avg_us}))
 
 
 def cpu_baseline(name, target_s):
@@ -160,6 +330,10 @@ def main():
               "(asked for --gpus %d, WORLD_SIZE %d)" % (args.gpus, world), file=sys.stderr)
         sys.exit(2)
 
+    if args.summarize_profiles:
+        summarize_profiles(args.summarize_profiles, args.workload)
+        return
+
     import numpy as np
     import torch
     from paper_1907_11210_amd import huge2 as h2
@@ -168,18 +342,22 @@ def main():
         import __graft_entry__
         __graft_entry__.build()
     dev = torch.device("cuda", 0)
+    if args.copy_calibration:
+        copy_calibration(dev)
+        return
     items, plans, step = build_workload(args.workload, dev)
     flops = layer_flops(plans)
     issued = [2 * p.macs()[1] for p in plans]
     total_flops = sum(flops)
     dtype = items[0][0].dtype
+    esz = 2 if dtype == "bf16" else 4
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
     nl = len(plans)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(nl + 1)] for _ in range(args.steps)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3 * nl)] for _ in range(args.steps)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -191,26 +369,47 @@ def main():
     wall = time.perf_counter() - t0
     ms_step = start.elapsed_time(stop) / args.steps
 
-    per_layer_ms = np.array([[ev[k][i].elapsed_time(ev[k][i + 1]) for i in range(nl)]
-                             for k in range(args.steps)]).mean(axis=0)
+    stage_ms = np.array([[ev[k][3 * i].elapsed_time(ev[k][3 * i + 1]) for i in range(nl)]
+                         for k in range(args.steps)]).mean(axis=0)
+    gemm_ms = np.array([[ev[k][3 * i + 1].elapsed_time(ev[k][3 * i + 2]) for i in range(nl)]
+                        for k in range(args.steps)]).mean(axis=0)
     layers = []
+    algo_bytes = []
     for i, ((layer, _, _), p) in enumerate(zip(items, plans)):
-        t = per_layer_ms[i] * 1e-3
+        ho, wo = layer.out_hw()
+        nbytes = esz * (layer.n * layer.c_in * layer.h * layer.w +
+                        layer.c_in * layer.c_out * layer.r * layer.s +
+                        layer.n * layer.c_out * ho * wo)
+        algo_bytes.append(nbytes)
+        t = (stage_ms[i] + gemm_ms[i]) * 1e-3
         layers.append({
-            "layer": layer.name, "ms": round(per_layer_ms[i], 5),
+            "layer": layer.name, "ms": round(stage_ms[i] + gemm_ms[i], 5),
+            "gemm_ms": round(gemm_ms[i], 5), "stage_ms": round(stage_ms[i], 5),
             "eff_tflops": round(flops[i] / t / 1e12, 2),
-            "mfma_issued_util": round(issued[i] / t / 1e12 / PEAK[layer.dtype], 4),
+            "gemm_eff_tflops": round(flops[i] / (gemm_ms[i] * 1e-3) / 1e12, 2),
+            "mfma_issued_util": round(issued[i] / (gemm_ms[i] * 1e-3) / 1e12 / PEAK[layer.dtype], 4),
             "nz_gflop": round(flops[i] / 1e9, 3),
+            "algorithmic_mb": round(nbytes / 1e6, 2),
         })
-    dom = int(np.argmax(per_layer_ms))
-    dom_t = per_layer_ms[dom] * 1e-3
-    achieved = flops[dom] / dom_t / 1e12
-    roofline = {
-        "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK[dtype], "unit": "TFLOP/s",
-        "frac": round(achieved / PEAK[dtype], 4), "traffic": None,
-        "kernel": "phase_gemm_kernel (%s)" % items[dom][0].name,
-        "algorithmic_flop_per_launch": flops[dom],
-    }
+    dom = int(np.argmax(gemm_ms))
+    dom_t = gemm_ms[dom] * 1e-3
+    intensity = flops[dom] / algo_bytes[dom]
+    ridge = PEAK[dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
+    if intensity >= ridge:
+        achieved = flops[dom] / dom_t / 1e12
+        roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK[dtype],
+                    "unit": "TFLOP/s", "frac": round(achieved / PEAK[dtype], 4)}
+        per_launch = {"algorithmic_flop_per_launch": flops[dom]}
+    else:
+        achieved = algo_bytes[dom] / dom_t / 1e9
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
+        per_launch = {"algorithmic_bytes_per_launch": algo_bytes[dom]}
+    roofline["traffic"] = measured_traffic(args.workload, items[dom][0].name)
+    roofline.update({"kernel": "phase_gemm_kernel (%s)" % items[dom][0].name,
+                     "mean_launch_ms": round(gemm_ms[dom], 5),
+                     "arithmetic_intensity_flop_per_byte": round(intensity, 1)})
+    roofline.update(per_launch)
     out = {
         "metric": METRIC,
         "value": round(total_flops / (ms_step * 1e-3) / 1e12, 3),
@@ -228,6 +427,7 @@ def main():
                    "batch": items[0][0].n, "layout": items[0][0].layout},
         "roofline": roofline,
         "layers": layers,
+        "kernel_source_sha": kernel_source_sha(),
         "wall_s_timed": round(wall, 3),
     }
     for p in plans:

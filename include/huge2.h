@@ -115,6 +115,21 @@ huge2_status huge2_plan_create(huge2_plan** out, const huge2_conv_desc* desc, in
 huge2_status huge2_plan_execute(const huge2_plan* plan, const void* x, const float* bias, void* y,
                                 void* hip_stream);
 
+/* The two halves of huge2_plan_execute, for callers that want to schedule or
+ * time them separately.  huge2_plan_stage_input enqueues the re-layout of x
+ * into the plan's staging buffer when the plan needs one (NCHW input, or a
+ * channel count that is not a multiple of 16 bytes) and does nothing
+ * otherwise.  huge2_plan_run_gemm enqueues the phase GEMM: it reads the
+ * staging buffer when the plan stages (x may then be NULL), x otherwise.
+ * Errors: INVALID_ARG (null plan or y, x NULL when needed, x == y), HIP. */
+huge2_status huge2_plan_stage_input(const huge2_plan* plan, const void* x, void* hip_stream);
+huge2_status huge2_plan_run_gemm(const huge2_plan* plan, const void* x, const float* bias, void* y,
+                                 void* hip_stream);
+
+/* 1 if plan_execute of this plan enqueues the input re-layout kernel, else 0
+ * (host only; -1 for a NULL plan). */
+int32_t huge2_plan_stages_input(const huge2_plan* plan);
+
 /* Release a plan and its device buffers.  Waits for the device to finish
  * work that may still use them.  NULL is accepted.  Errors: HIP. */
 huge2_status huge2_plan_destroy(huge2_plan* plan);

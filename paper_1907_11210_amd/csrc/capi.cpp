@@ -70,15 +70,16 @@ long long count_works(const huge2_conv_desc& d, bool transposed, int class_split
   return works;
 }
 
-// Tile choice: output channels <= 32 take the narrow tile; otherwise the
-// largest tile that still gives every one of the 256 CUs a workgroup.
+// Tile choice, from measurements on MI355X: few output channels take the
+// narrow 128 x 32 tile with 64-byte K stages (many small workgroups keep the
+// latency-bound loop busy); large problems the 8-wave 128 x 128 tile; the
+// rest the 64 x 128 tile, which still gives every CU work.
 int choose_cfg(const huge2_conv_desc& d, bool transposed, int class_split) {
   int forced = env_int("HUGE2_TILE", -1);
   if (forced >= 0 && forced < TILE_COUNT) return forced;
-  if (d.c_out <= 32) return TILE_256x32;
-  if (count_works(d, transposed, class_split, TILE_256x128) >= 256) return TILE_256x128;
-  if (count_works(d, transposed, class_split, TILE_128x128) >= 256) return TILE_128x128;
-  return TILE_64x128;
+  if (d.c_out <= 32) return 10;                                     // 128 x 32, KB 64
+  if (count_works(d, transposed, class_split, 8) >= 512) return 8;  // 128 x 128, 8 waves
+  return 2;                                                         // 64 x 128
 }
 
 int class_split_mode() {
@@ -137,7 +138,7 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   p->cfg = cfg;
   const int esz = elem_size(d.dtype);
   const int vec = 16 / esz;
-  const int bk = kBlockK_bytes / esz;
+  const int bk = tile_kb(cfg) / esz;
   // NCHW inputs and ragged channel counts are re-laid out to channel-
   // contiguous pixels (channel count padded to 16 bytes) by a staging kernel.
   p->staged = !(d.layout == HUGE2_NHWC && d.c_in % vec == 0);
@@ -185,6 +186,9 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     sd.in_step_w = s.in_step_w;
     sd.tap_begin = s.tap_begin;
     sd.tap_count = s.tap_count;
+    const uint32_t divisors[4] = {(uint32_t)s.qn_w, (uint32_t)s.qn_h, (uint32_t)d.n,
+                                  (uint32_t)s.nphase_w};
+    for (int k = 0; k < 4; ++k) division_magic(divisors[k], &sd.div_mul[k], &sd.div_shift[k]);
     // exact: every tap's read is in range for every pixel of the segment (the
     // input coordinate is affine and non-decreasing in phase and q, so the
     // extremes are at the segment's corners)
@@ -199,6 +203,34 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
                              (long long)s.in_step_w * (s.q0_w + s.qn_w - 1) + tp.off_w;
       if (h_lo < 0 || h_hi >= d.h || w_lo < 0 || w_hi >= d.w) sd.exact = 0;
     }
+    // taps as a product of two arithmetic progressions (the order build_shape
+    // emits: h outer, w inner), verified tap by tap
+    sd.tap_ap = 0;
+    if (s.tap_count > 0) {
+      const huge2_tap* tl = &shape.taps[s.tap_begin];
+      int ntw = 1;
+      while (ntw < s.tap_count && tl[ntw].kh == tl[0].kh) ++ntw;
+      if (s.tap_count % ntw == 0) {
+        const int nth = s.tap_count / ntw;
+        sd.ntw = ntw;
+        sd.off0_h = tl[0].off_h;
+        sd.off0_w = tl[0].off_w;
+        sd.kh0 = tl[0].kh;
+        sd.kw0 = tl[0].kw;
+        sd.doff_h = nth > 1 ? tl[ntw].off_h - tl[0].off_h : 0;
+        sd.dkh = nth > 1 ? tl[ntw].kh - tl[0].kh : 0;
+        sd.doff_w = ntw > 1 ? tl[1].off_w - tl[0].off_w : 0;
+        sd.dkw = ntw > 1 ? tl[1].kw - tl[0].kw : 0;
+        bool ok = true;
+        for (int t = 0; t < s.tap_count && ok; ++t) {
+          const int th = t / ntw, tw = t % ntw;
+          ok = tl[t].kh == sd.kh0 + th * sd.dkh && tl[t].kw == sd.kw0 + tw * sd.dkw &&
+               tl[t].off_h == sd.off0_h + th * sd.doff_h && tl[t].off_w == sd.off0_w + tw * sd.doff_w;
+        }
+        sd.tap_ap = ok ? 1 : 0;
+      }
+    }
+    if (!sd.tap_ap) sd.ntw = 1;
     segs.push_back(sd);
     for (int m0 = 0; m0 < sd.m_total; m0 += bm)
       for (int nt = 0; nt < ntiles_n; ++nt) {
@@ -256,22 +288,27 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   return HUGE2_OK;
 }
 
-huge2_status execute_impl(const huge2_plan* p, const void* x, const float* bias, void* y,
-                          hipStream_t stream) {
-  if (!p || !x || !y || x == y) return HUGE2_ERR_INVALID_ARG;
+huge2_status stage_impl(const huge2_plan* p, const void* x, hipStream_t stream) {
+  if (!p) return HUGE2_ERR_INVALID_ARG;
+  if (!p->staged) return HUGE2_OK;
+  if (!x) return HUGE2_ERR_INVALID_ARG;
   const huge2_conv_desc& d = p->desc;
   if (fault("launch")) return HUGE2_ERR_HIP;
-  const void* xin = x;
-  if (p->staged) {
-    if (launch_stage_input(x, p->xs, d.dtype, d.layout == HUGE2_NCHW, d.n, d.c_in, d.h * d.w,
-                           p->c_stride, stream) != hipSuccess) {
-      (void)hipGetLastError();
-      return HUGE2_ERR_HIP;
-    }
-    xin = p->xs;
+  if (launch_stage_input(x, p->xs, d.dtype, d.layout == HUGE2_NCHW, d.n, d.c_in, d.h * d.w,
+                         p->c_stride, stream) != hipSuccess) {
+    (void)hipGetLastError();
+    return HUGE2_ERR_HIP;
   }
+  return HUGE2_OK;
+}
+
+huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, void* y,
+                       hipStream_t stream) {
+  if (!p || !y || (!p->staged && !x) || x == y) return HUGE2_ERR_INVALID_ARG;
+  const huge2_conv_desc& d = p->desc;
+  if (fault("launch")) return HUGE2_ERR_HIP;
   GemmArgs a;
-  a.x = xin;
+  a.x = p->staged ? p->xs : x;
   a.wp = p->wp;
   a.bias = bias;
   a.y = y;
@@ -283,6 +320,7 @@ huge2_status execute_impl(const huge2_plan* p, const void* x, const float* bias,
   a.h = d.h;
   a.w = d.w;
   a.cin = p->c_stride;
+  a.ks = d.s;
   a.x_bytes = (uint32_t)p->x_bytes;
   a.wp_bytes = (uint32_t)p->wp_bytes;
   a.cin_pad = p->cin_pad;
@@ -295,6 +333,14 @@ huge2_status execute_impl(const huge2_plan* p, const void* x, const float* bias,
     return HUGE2_ERR_HIP;
   }
   return HUGE2_OK;
+}
+
+huge2_status execute_impl(const huge2_plan* p, const void* x, const float* bias, void* y,
+                          hipStream_t stream) {
+  if (!p || !x || !y || x == y) return HUGE2_ERR_INVALID_ARG;
+  huge2_status st = stage_impl(p, x, stream);
+  if (st != HUGE2_OK) return st;
+  return gemm_impl(p, x, bias, y, stream);
 }
 
 huge2_status one_shot(const huge2_conv_desc* desc, int transposed, const void* x, const void* w,
@@ -355,6 +401,28 @@ huge2_status huge2_plan_execute(const huge2_plan* plan, const void* x, const flo
   } catch (...) {
     return HUGE2_ERR_HIP;
   }
+}
+
+huge2_status huge2_plan_stage_input(const huge2_plan* plan, const void* x, void* hip_stream) {
+  try {
+    return stage_impl(plan, x, (hipStream_t)hip_stream);
+  } catch (...) {
+    return HUGE2_ERR_HIP;
+  }
+}
+
+huge2_status huge2_plan_run_gemm(const huge2_plan* plan, const void* x, const float* bias, void* y,
+                                 void* hip_stream) {
+  try {
+    return gemm_impl(plan, x, bias, y, (hipStream_t)hip_stream);
+  } catch (...) {
+    return HUGE2_ERR_HIP;
+  }
+}
+
+int32_t huge2_plan_stages_input(const huge2_plan* plan) {
+  if (!plan) return -1;
+  return plan->staged ? 1 : 0;
 }
 
 huge2_status huge2_plan_destroy(huge2_plan* plan) {
@@ -419,7 +487,7 @@ huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, in
     const int bm = tile_bm(cfg), bn = tile_bn(cfg);
     PlanShape shape;
     if (!build_shape(*desc, transposed != 0, split, bm, &shape)) return HUGE2_ERR_INVALID_ARG;
-    const int bk = kBlockK_bytes / elem_size(desc->dtype);
+    const int bk = tile_kb(cfg) / elem_size(desc->dtype);
     const int64_t cin_pad = round_up(desc->c_in, bk);
     const int64_t ntn = round_up(desc->c_out, bn) / bn;
     *nonzero_macs = shape.nonzero_macs;

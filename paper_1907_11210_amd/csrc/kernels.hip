@@ -38,20 +38,27 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
 struct PixelPos {
   int img, oh, ow, ih, iw;
 };
+__device__ __forceinline__ uint32_t fast_div(uint32_t v, uint32_t mul, uint32_t shift) {
+  return (uint32_t)(((uint64_t)v * mul) >> shift);
+}
 __device__ __forceinline__ PixelPos pixel_pos(const SegDev& sg, int nimg, int m) {
   PixelPos p;
-  int j = m;
-  const int a_w = j % sg.qn_w;
-  j /= sg.qn_w;
-  const int a_h = j % sg.qn_h;
-  j /= sg.qn_h;
-  p.img = j % nimg;
-  const int iph = j / nimg;
-  const int iph_h = iph / sg.nphase_w, iph_w = iph - iph_h * sg.nphase_w;
+  uint32_t j = (uint32_t)m;
+  uint32_t t = fast_div(j, sg.div_mul[0], sg.div_shift[0]);
+  const int a_w = (int)(j - t * (uint32_t)sg.qn_w);
+  j = t;
+  t = fast_div(j, sg.div_mul[1], sg.div_shift[1]);
+  const int a_h = (int)(j - t * (uint32_t)sg.qn_h);
+  j = t;
+  t = fast_div(j, sg.div_mul[2], sg.div_shift[2]);
+  p.img = (int)(j - t * (uint32_t)nimg);
+  const uint32_t iph = t;
+  const uint32_t iph_h = fast_div(iph, sg.div_mul[3], sg.div_shift[3]);
+  const int iph_w = (int)(iph - iph_h * (uint32_t)sg.nphase_w);
   const int qh = sg.q0_h + a_h, qw = sg.q0_w + a_w;
-  p.oh = sg.phase0_h + iph_h + sg.out_step_h * qh;
+  p.oh = sg.phase0_h + (int)iph_h + sg.out_step_h * qh;
   p.ow = sg.phase0_w + iph_w + sg.out_step_w * qw;
-  p.ih = sg.in0_h + sg.in_dphase_h * iph_h + sg.in_step_h * qh;
+  p.ih = sg.in0_h + sg.in_dphase_h * (int)iph_h + sg.in_step_h * qh;
   p.iw = sg.in0_w + sg.in_dphase_w * iph_w + sg.in_step_w * qw;
   return p;
 }
@@ -82,7 +89,7 @@ __device__ __forceinline__ PixelPos pixel_pos(const SegDev& sg, int nimg, int m)
 // NCHW output puts pixels on MFMA columns (lanes hold consecutive pixels, so
 // a channel's stores coalesce); NHWC output puts pixels on MFMA rows (lanes
 // hold consecutive channels of a pixel).
-template <bool BF16, int BM, int BN, int PWAVES, int CWAVES, int KB, bool NCHW_OUT>
+template <bool BF16, int BM, int BN, int PWAVES, int CWAVES, int KB, int DEPTH, bool NCHW_OUT>
 __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmArgs a) {
   constexpr int NT = PWAVES * CWAVES * 64;  // threads per workgroup
   constexpr int ESZ = BF16 ? 2 : 4;
@@ -93,9 +100,9 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
   constexpr int WP = BM / PWAVES, WC = BN / CWAVES;
   constexpr int TP = WP / 32, TC = WC / 32;
   constexpr int A_LD = BM * CPR / NT;
-  constexpr int B_LD = BN * CPR / NT;
+  constexpr int B_LD = (BN * CPR + NT - 1) / NT;  // the last may be partial
   constexpr int KSUB = BF16 ? KB / 32 : KB / 8;  // MFMAs per operand pair and stage
-  static_assert(BM * CPR % NT == 0 && BN * CPR % NT == 0, "whole loads per thread");
+  static_assert(BM * CPR % NT == 0, "whole A loads per thread");
   static_assert(TP >= 1 && TC >= 1 && WP % 32 == 0 && WC % 32 == 0, "32x32 MFMA blocks");
   constexpr int STAGE_B = (BM + BN) * ROWB;
   constexpr uint32_t OOB = 0x80000000u;  // beyond every buffer: loads return 0
@@ -135,7 +142,7 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
   // The segment's taps in LDS: byte delta of the tapped pixel and byte
   // offset of the tap's weight block.
   __shared__ int4 s_taps[kMaxLdsTaps];
-  const bool lds_taps = ntaps <= kMaxLdsTaps;
+  const bool lds_taps = !sg.tap_ap && ntaps <= kMaxLdsTaps;
   if (lds_taps) {
     for (int t = tid; t < ntaps; t += NT) {
       const TapDev tp = a.taps[sg.tap_begin + t];
@@ -150,12 +157,15 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
     uint4 a[A_LD];
     uint4 b[B_LD];
   };
-  Regs r0, r1;
+  Regs r0;
+  [[maybe_unused]] Regs r1;
 
   uint32_t voff_b[B_LD];  // per B row: byte offset within a tap's weight block
 #pragma unroll
   for (int i = 0; i < B_LD; ++i)
-    voff_b[i] = (uint32_t)(((wk.n0 + tid / CPR + (NT / CPR) * i) * a.cin_pad + chunk * VE) * ESZ);
+    voff_b[i] = tid + NT * i < BN * CPR
+                    ? (uint32_t)(((wk.n0 + tid / CPR + (NT / CPR) * i) * a.cin_pad + chunk * VE) * ESZ)
+                    : OOB;
 
   // Resources with no records: every load through them returns zero.
   const __amdgpu_buffer_rsrc_t xr0 =
@@ -168,23 +178,33 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
   // past the last stage goes through the empty resources instead of
   // branching around the loads: the load sequence stays the same on every
   // path, which lets the compiler wait only for the stage it stores.
-  int ld_tap = 0, ld_cb = 0;
+  int ld_tap = 0, ld_cb = 0, ld_th = 0, ld_tw = 0;
+  const uint32_t slot_bytes = (uint32_t)a.cout_pad * (uint32_t)a.cin_pad * ESZ;
   auto load_step = [&](Regs& R, bool valid) {
     const __amdgpu_buffer_rsrc_t xs = valid ? xr : xr0;
     const __amdgpu_buffer_rsrc_t ws = valid ? wr : wr0;
-    int4 ti;
-    if (lds_taps) {
-      ti = s_taps[valid ? ld_tap : 0];
+    int delta, off_h, off_w;
+    uint32_t slot_b;
+    if (sg.tap_ap) {
+      // the tap from two counters, in scalar registers
+      off_h = sg.off0_h + ld_th * sg.doff_h;
+      off_w = sg.off0_w + ld_tw * sg.doff_w;
+      delta = (off_h * a.w + off_w) * a.cin * ESZ;
+      slot_b = (uint32_t)((sg.kh0 + ld_th * sg.dkh) * a.ks + sg.kw0 + ld_tw * sg.dkw) * slot_bytes;
     } else {
-      const TapDev tp = a.taps[sg.tap_begin + (valid ? ld_tap : 0)];
-      ti = make_int4((tp.off_h * a.w + tp.off_w) * a.cin * ESZ,
-                     (int)((uint32_t)tp.slot * (uint32_t)a.cout_pad * (uint32_t)a.cin_pad * ESZ),
-                     tp.off_h, tp.off_w);
+      int4 ti;
+      if (lds_taps) {
+        ti = s_taps[valid ? ld_tap : 0];
+      } else {
+        const TapDev tp = a.taps[sg.tap_begin + (valid ? ld_tap : 0)];
+        ti = make_int4((tp.off_h * a.w + tp.off_w) * a.cin * ESZ, (int)((uint32_t)tp.slot * slot_bytes),
+                       tp.off_h, tp.off_w);
+      }
+      delta = __builtin_amdgcn_readfirstlane(ti.x);
+      slot_b = (uint32_t)__builtin_amdgcn_readfirstlane(ti.y);
+      off_h = __builtin_amdgcn_readfirstlane(ti.z);
+      off_w = __builtin_amdgcn_readfirstlane(ti.w);
     }
-    const int delta = __builtin_amdgcn_readfirstlane(ti.x);
-    const uint32_t slot_b = (uint32_t)__builtin_amdgcn_readfirstlane(ti.y);
-    const int off_h = __builtin_amdgcn_readfirstlane(ti.z);
-    const int off_w = __builtin_amdgcn_readfirstlane(ti.w);
     const uint32_t kb = (uint32_t)ld_cb * KB;
     const bool tail = ld_cb == cblocks - 1 && tail_c < KC;
     const bool chunk_out = tail && chunk * VE >= tail_c;
@@ -203,9 +223,17 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
     for (int i = 0; i < B_LD; ++i)
       R.b[i] = __builtin_bit_cast(
           uint4, __builtin_amdgcn_raw_buffer_load_b128(ws, voff_b[i], slot_b + kb, 0));
-    if (valid && ++ld_tap == ntaps) {
-      ld_tap = 0;
-      ++ld_cb;
+    if (valid) {
+      if (++ld_tw == sg.ntw) {
+        ld_tw = 0;
+        ++ld_th;
+      }
+      if (++ld_tap == ntaps) {
+        ld_tap = 0;
+        ld_th = 0;
+        ld_tw = 0;
+        ++ld_cb;
+      }
     }
   };
   auto store_stage = [&](int buf, const Regs& R) {
@@ -216,7 +244,8 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
       *(uint4*)(as + (tid / CPR + (NT / CPR) * i) * ROWB + chunk * 16) = R.a[i];
 #pragma unroll
     for (int i = 0; i < B_LD; ++i)
-      *(uint4*)(bs + (tid / CPR + (NT / CPR) * i) * ROWB + chunk * 16) = R.b[i];
+      if (BN * CPR % NT == 0 || tid + NT * i < BN * CPR)
+        *(uint4*)(bs + (tid / CPR + (NT / CPR) * i) * ROWB + chunk * 16) = R.b[i];
   };
 
   f32x16 acc[TP][TC];
@@ -283,19 +312,36 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
   // the other register buffer is receiving stage s+1.
   const int nsteps2 = (nsteps + 1) & ~1;
   if (nsteps2 > 0) {
-    load_step(r0, true);
-    store_stage(0, r0);
-    load_step(r0, 1 < nsteps);
-    __syncthreads();
-    for (int s = 0; s < nsteps2; s += 2) {
-      load_step(r1, s + 2 < nsteps);
-      compute(0);
-      store_stage(1, r0);
+    if constexpr (DEPTH == 2) {
+      load_step(r0, true);
+      store_stage(0, r0);
+      load_step(r0, 1 < nsteps);
       __syncthreads();
-      load_step(r0, s + 3 < nsteps);
-      compute(1);
-      store_stage(0, r1);
+      for (int s = 0; s < nsteps2; s += 2) {
+        load_step(r1, s + 2 < nsteps);
+        compute(0);
+        store_stage(1, r0);
+        __syncthreads();
+        load_step(r0, s + 3 < nsteps);
+        compute(1);
+        store_stage(0, r1);
+        __syncthreads();
+      }
+    } else {
+      // one register buffer: the loads of stage s+1 overlap the MFMAs of stage s
+      load_step(r0, true);
+      store_stage(0, r0);
       __syncthreads();
+      for (int s = 0; s < nsteps2; s += 2) {
+        load_step(r0, s + 1 < nsteps);
+        compute(0);
+        store_stage(1, r0);
+        __syncthreads();
+        load_step(r0, s + 2 < nsteps);
+        compute(1);
+        store_stage(0, r0);
+        __syncthreads();
+      }
     }
   }
 
@@ -352,80 +398,24 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
   }
 }
 
-int tile_bm(int cfg) {
-  switch (cfg) {
-    case TILE_256x32:
-    case TILE_256x128:
-    case TILE_256x256_W8:
-    case TILE_256x128_W8: return 256;
-    case TILE_64x128: return 64;
-    default: return 128;
-  }
-}
-int tile_bn(int cfg) {
-  switch (cfg) {
-    case TILE_256x32: return 32;
-    case TILE_128x256:
-    case TILE_256x256_W8:
-    case TILE_128x256_W8: return 256;
-    default: return 128;
-  }
-}
-int tile_threads(int cfg) {
-  switch (cfg) {
-    case TILE_256x256_W8:
-    case TILE_256x128_W8:
-    case TILE_128x256_W8:
-    case TILE_128x128_W8: return 512;
-    default: return 256;
-  }
+template <bool BF16, bool NCHW_OUT, int CFG>
+static void launch_one(const GemmArgs& a, hipStream_t stream) {
+  constexpr TileShape t = kTiles[CFG];
+  hipLaunchKernelGGL((phase_gemm_kernel<BF16, t.bm, t.bn, t.pw, t.cw, t.kb, t.depth, NCHW_OUT>),
+                     dim3(a.n_works), dim3(t.pw * t.cw * 64), 0, stream, a);
 }
 
-template <bool BF16, bool NCHW_OUT>
+template <bool BF16, bool NCHW_OUT, int CFG = 0>
 static hipError_t launch_cfg(const GemmArgs& a, int cfg, hipStream_t stream) {
-  dim3 grid(a.n_works), block(tile_threads(cfg));
-  constexpr int KB = kBlockK_bytes;
-  switch (cfg) {
-    case TILE_128x128:
-      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 128, 128, 2, 2, KB, NCHW_OUT>), grid, block, 0,
-                         stream, a);
-      break;
-    case TILE_256x32:
-      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 256, 32, 4, 1, KB, NCHW_OUT>), grid, block, 0,
-                         stream, a);
-      break;
-    case TILE_64x128:
-      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 64, 128, 1, 4, KB, NCHW_OUT>), grid, block, 0,
-                         stream, a);
-      break;
-    case TILE_256x128:
-      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 256, 128, 2, 2, KB, NCHW_OUT>), grid, block, 0,
-                         stream, a);
-      break;
-    case TILE_128x256:
-      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 128, 256, 2, 2, KB, NCHW_OUT>), grid, block, 0,
-                         stream, a);
-      break;
-    case TILE_256x256_W8:
-      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 256, 256, 2, 4, KB, NCHW_OUT>), grid, block, 0,
-                         stream, a);
-      break;
-    case TILE_256x128_W8:
-      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 256, 128, 4, 2, KB, NCHW_OUT>), grid, block, 0,
-                         stream, a);
-      break;
-    case TILE_128x256_W8:
-      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 128, 256, 2, 4, KB, NCHW_OUT>), grid, block, 0,
-                         stream, a);
-      break;
-    case TILE_128x128_W8:
-      hipLaunchKernelGGL((phase_gemm_kernel<BF16, 128, 128, 4, 2, KB, NCHW_OUT>), grid, block, 0,
-                         stream, a);
-      break;
-    default:
-      return hipErrorInvalidValue;
+  if constexpr (CFG < TILE_COUNT) {
+    if (cfg == CFG) {
+      launch_one<BF16, NCHW_OUT, CFG>(a, stream);
+      return hipGetLastError();
+    }
+    return launch_cfg<BF16, NCHW_OUT, CFG + 1>(a, cfg, stream);
+  } else {
+    return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 hipError_t launch_phase_gemm(const GemmArgs& a, int dtype, int cfg, bool nchw_out,

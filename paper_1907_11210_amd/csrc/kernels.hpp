@@ -17,8 +17,28 @@ struct SegDev {
   int32_t in_dphase_h, in_dphase_w, in_step_h, in_step_w;
   int32_t tap_begin, tap_count;
   int32_t exact;  // 1: every tap reads inside the input for every pixel (no bounds tests)
-  int32_t pad0;
+  // tap_ap = 1: the taps are the product of two arithmetic progressions, tap
+  // t = (th, tw) = (t / ntw, t % ntw) with kernel tap (kh0 + th*dkh, kw0 + tw*dkw)
+  // at input offset (off0_h + th*doff_h, off0_w + tw*doff_w); the kernel then
+  // derives each tap from two counters instead of reading the tap list
+  int32_t tap_ap;
+  int32_t ntw, off0_h, doff_h, off0_w, doff_w, kh0, dkh, kw0, dkw;
+  // floor(v / d) = (v * mul) >> shift for 0 <= v < 2^31, for the divisors
+  // qn_w, qn_h, n (images) and nphase_w of the pixel decomposition
+  uint32_t div_mul[4];
+  uint32_t div_shift[4];
 };
+
+// Multiplier and shift of the division by d (1 <= d < 2^31) for dividends
+// below 2^31: floor(v / d) = (v * mul) >> shift with l = ceil(log2 d),
+// mul = floor(2^(31+l) / d) + 1, shift = 31 + l (Granlund and Montgomery,
+// "Division by invariant integers using multiplication", 1994).
+inline void division_magic(uint32_t d, uint32_t* mul, uint32_t* shift) {
+  uint32_t l = 0;
+  while ((1ull << l) < d) ++l;
+  *mul = (uint32_t)(((1ull << (31 + l)) / d) + 1);
+  *shift = 31 + l;
+}
 
 // One tap of a segment: the packed sub-kernel block (slot = kh*s + kw) and
 // the input offset it reads at.
@@ -46,25 +66,43 @@ struct GemmArgs {
   int32_t cin_pad;            // K stride of the packed weights (multiple of the K block)
   int32_t cout, cout_pad;
   int32_t ho, wo;
+  int32_t ks;  // kernel width s: weight slot of tap (kh, kw) = kh * ks + kw
 };
 
-// Tile configurations of the phase GEMM kernel.
-enum TileCfg : int32_t {
-  TILE_128x128 = 0,  // 128 pixels x 128 output channels, 4 waves as 2x2
-  TILE_256x32 = 1,   // 256 pixels x 32 output channels, 4 waves as 4x1
-  TILE_64x128 = 2,   // 64 pixels x 128 output channels, 4 waves as 1x4
-  TILE_256x128 = 3,  // 256 pixels x 128 output channels, 4 waves as 2x2
-  TILE_128x256 = 4,  // 128 pixels x 256 output channels, 4 waves as 2x2
-  TILE_256x256_W8 = 5,  // 256 x 256, 8 waves as 2x4
-  TILE_256x128_W8 = 6,  // 256 x 128, 8 waves as 4x2
-  TILE_128x256_W8 = 7,  // 128 x 256, 8 waves as 2x4
-  TILE_128x128_W8 = 8,  // 128 x 128, 8 waves as 4x2
-  TILE_COUNT = 9
+// Tile configurations of the phase GEMM kernel: BM pixels x BN output
+// channels per workgroup, PW x CW waves (64 threads each), KB bytes of K per
+// LDS stage.
+// depth: stages of global loads in flight ahead of the MFMAs (1 or 2; each
+// in-flight stage costs one register buffer).
+struct TileShape {
+  int bm, bn, pw, cw, kb, depth;
 };
-int tile_bm(int cfg);
-int tile_bn(int cfg);
-int tile_threads(int cfg);
-constexpr int kBlockK_bytes = 128;  // K block per LDS stage: 64 bf16 or 32 fp32
+constexpr TileShape kTiles[] = {
+    {128, 128, 2, 2, 128, 2},  // 0
+    {256, 32, 4, 1, 128, 2},   // 1  narrow: few output channels
+    {64, 128, 1, 4, 128, 2},   // 2
+    {256, 128, 2, 2, 128, 2},  // 3
+    {128, 256, 2, 2, 128, 2},  // 4
+    {256, 256, 2, 4, 128, 2},  // 5  8 waves
+    {256, 128, 4, 2, 128, 2},  // 6  8 waves
+    {128, 256, 2, 4, 128, 2},  // 7  8 waves
+    {128, 128, 4, 2, 128, 2},  // 8  8 waves
+    {256, 256, 2, 2, 128, 1},  // 9  4 waves of 128 x 128
+    {128, 32, 4, 1, 64, 2},    // 10 narrow, small LDS footprint
+    {256, 32, 4, 1, 64, 2},    // 11 narrow, small LDS footprint
+    {64, 128, 1, 4, 64, 2},    // 12 small LDS footprint
+    {128, 128, 2, 2, 64, 2},   // 13 small LDS footprint
+    {256, 128, 2, 2, 128, 1},  // 14 4 waves of 128 x 64, one buffer
+    {128, 256, 2, 2, 128, 1},  // 15 4 waves of 64 x 128, one buffer
+};
+constexpr int TILE_COUNT = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
+inline int tile_bm(int cfg) { return kTiles[cfg].bm; }
+inline int tile_bn(int cfg) { return kTiles[cfg].bn; }
+inline int tile_threads(int cfg) { return kTiles[cfg].pw * kTiles[cfg].cw * 64; }
+inline int tile_kb(int cfg) { return kTiles[cfg].kb; }
+// LDS bytes of a configuration (two stages of BM + BN rows, 16-byte row pad)
+inline int tile_lds(int cfg) { return 2 * (kTiles[cfg].bm + kTiles[cfg].bn) * (kTiles[cfg].kb + 16); }
+constexpr int kMaxBlockK_bytes = 128;  // largest K block per stage: 64 bf16 or 32 fp32
 
 // dtype: 0 fp32, 1 bf16; nchw_out selects the output layout.
 hipError_t launch_phase_gemm(const GemmArgs& a, int dtype, int cfg, bool nchw_out,

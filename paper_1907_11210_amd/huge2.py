@@ -23,6 +23,7 @@ HUGE2_NCHW, HUGE2_NHWC = 0, 1
 
 EXPORTED = (
     "huge2_status_str", "huge2_output_shape", "huge2_plan_create", "huge2_plan_execute",
+    "huge2_plan_stage_input", "huge2_plan_run_gemm", "huge2_plan_stages_input",
     "huge2_plan_destroy", "huge2_conv2d_transpose", "huge2_conv2d_dilated",
     "huge2_plan_describe", "huge2_plan_macs",
 )
@@ -71,6 +72,9 @@ def lib():
         L.huge2_output_shape.argtypes = [dp, i32, i32p, i32p]
         L.huge2_plan_create.argtypes = [ctypes.POINTER(vp), dp, i32, vp, vp]
         L.huge2_plan_execute.argtypes = [vp, vp, vp, vp, vp]
+        L.huge2_plan_stage_input.argtypes = [vp, vp, vp]
+        L.huge2_plan_run_gemm.argtypes = [vp, vp, vp, vp, vp]
+        L.huge2_plan_stages_input.argtypes = [vp]
         L.huge2_plan_destroy.argtypes = [vp]
         L.huge2_conv2d_transpose.argtypes = [dp, vp, vp, vp, vp, vp]
         L.huge2_conv2d_dilated.argtypes = [dp, vp, vp, vp, vp, vp]
@@ -128,6 +132,21 @@ def huge2_plan_execute(plan, x_ptr, bias_ptr, y_ptr, stream=0):
     _check(lib().huge2_plan_execute(plan, ctypes.c_void_p(x_ptr), ctypes.c_void_p(bias_ptr),
                                     ctypes.c_void_p(y_ptr), ctypes.c_void_p(stream)),
            "huge2_plan_execute")
+
+
+def huge2_plan_stage_input(plan, x_ptr, stream=0):
+    _check(lib().huge2_plan_stage_input(plan, ctypes.c_void_p(x_ptr), ctypes.c_void_p(stream)),
+           "huge2_plan_stage_input")
+
+
+def huge2_plan_run_gemm(plan, x_ptr, bias_ptr, y_ptr, stream=0):
+    _check(lib().huge2_plan_run_gemm(plan, ctypes.c_void_p(x_ptr), ctypes.c_void_p(bias_ptr),
+                                     ctypes.c_void_p(y_ptr), ctypes.c_void_p(stream)),
+           "huge2_plan_run_gemm")
+
+
+def huge2_plan_stages_input(plan):
+    return int(lib().huge2_plan_stages_input(plan))
 
 
 def huge2_plan_destroy(plan):
@@ -332,6 +351,27 @@ class Plan:
         huge2_plan_execute(self._plan, x.data_ptr(), _bias_ptr(bias, x), y.data_ptr(),
                            _stream(x))
         return y
+
+    def stage(self, x):
+        """Enqueue only the input re-layout (no-op for plans that need none)."""
+        _check_tensor(x, "x", self.device)
+        if tuple(x.shape) != self.x_shape or x.dtype != self.dtype:
+            raise ValueError("x does not match the plan")
+        huge2_plan_stage_input(self._plan, x.data_ptr(), _stream(x))
+
+    def gemm(self, x, out, bias=None):
+        """Enqueue only the phase GEMM (after :meth:`stage` when the plan stages)."""
+        _check_tensor(x, "x", self.device)
+        _check_tensor(out, "out", self.device)
+        if tuple(out.shape) != self.out_shape or out.dtype != self.dtype:
+            raise ValueError("out does not match the plan")
+        huge2_plan_run_gemm(self._plan, x.data_ptr(), _bias_ptr(bias, x), out.data_ptr(),
+                            _stream(x))
+        return out
+
+    @property
+    def stages_input(self):
+        return huge2_plan_stages_input(self._plan) == 1
 
     def macs(self):
         return huge2_plan_macs(self.desc, self.transposed)

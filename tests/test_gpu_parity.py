@@ -201,7 +201,7 @@ def test_workload_full_size_sampled(wname):
         assert np.all(np.isfinite(y))
 
 
-TILE_CONFIGS = list(range(9))  # every GEMM tile configuration of the kernel
+TILE_CONFIGS = list(range(16))  # every GEMM tile configuration of the kernel
 
 
 @pytest.mark.parametrize("tile", TILE_CONFIGS)
@@ -217,3 +217,27 @@ def test_every_tile_configuration(tile, monkeypatch):
         absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
         y = P.run_gpu(layer, xq, wq, bias)
         P.check(y, ref, absref, layer.dtype, "%s tile %d" % (layer.name, tile))
+
+
+@pytest.mark.parametrize("layer", [SMALL[2], SMALL[1], SMALL[7], SMALL[14]], ids=lambda l: l.name)
+def test_stage_then_gemm_equals_execute(layer):
+    """huge2_plan_stage_input followed by huge2_plan_run_gemm writes the same
+    bits as huge2_plan_execute, whether or not the plan stages its input."""
+    P.say("case", layer)
+    dev = torch.device("cuda", 0)
+    xq, wq = _inputs(layer, seed=9)
+    x_dev = wl.to_layout(xq, layer.layout).to(dev)
+    bias = torch.linspace(-1.0, 1.0, layer.c_out).to(dev)
+    plan = P.make_plan(layer, wq.contiguous().to(dev))
+    y1 = torch.full(plan.out_shape, float("nan"), dtype=xq.dtype, device=dev)
+    y2 = torch.full(plan.out_shape, float("nan"), dtype=xq.dtype, device=dev)
+    plan(x_dev, bias=bias, out=y1)
+    plan.stage(x_dev)
+    plan.gemm(x_dev, y2, bias=bias)
+    torch.cuda.synchronize()
+    staged = plan.stages_input
+    plan.close()
+    assert staged == (layer.layout == "NCHW" or layer.c_in % (8 if layer.dtype == "bf16" else 4) != 0)
+    assert not torch.isnan(y2).any()
+    iv = torch.int16 if y1.dtype == torch.bfloat16 else torch.int32
+    assert torch.equal(y1.view(iv), y2.view(iv)), layer.name

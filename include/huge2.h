@@ -177,8 +177,9 @@ typedef struct {
  * with caps 0 to size the arrays).  class_split: 1 splits every phase into
  * border classes, so that each segment reads only in-range inputs; 0 keeps
  * one segment per phase group with all of its taps (out-of-range reads then
- * contribute zero); 2 is the plan's own choice (per phase group, whichever
- * issues fewer tile-taps for the plan's tile height). */
+ * contribute zero); 2 chooses per phase group whichever issues fewer
+ * tile-taps for the plan's tile height.  A plan uses 0 or 2, whichever a
+ * model of its schedule on the MI355X's compute units finishes first. */
 huge2_status huge2_plan_describe(const huge2_conv_desc* desc, int32_t transposed,
                                  int32_t class_split, huge2_segment* segs, int32_t seg_cap,
                                  int32_t* n_segs, huge2_tap* taps, int32_t tap_cap,

@@ -7,9 +7,11 @@
 // exception crosses the ABI.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdlib>
 #include <cstring>
 #include <new>
+#include <queue>
 #include <vector>
 
 #include "huge2.h"
@@ -82,9 +84,114 @@ int choose_cfg(const huge2_conv_desc& d, bool transposed, int class_split) {
   return 2;                                                         // 64 x 128
 }
 
-int class_split_mode() {
-  int v = env_int("HUGE2_CLASS_SPLIT", 2);
-  return (v >= 0 && v <= 2) ? v : 2;
+// Order the work list for the eight XCDs.  The kernel hands work index
+// chunk x (contiguous, works/8 long) to the workgroups that the dispatcher
+// places on XCD x, and each XCD has its own L2.  The works are split into
+// eight cells, a ranges of spatial position (image, then output row of the
+// phase) times b ranges of output-channel tiles (a * b = 8), choosing the
+// split that minimises the bytes every XCD must fetch (input / a + packed
+// weights / b).  All phases and border classes of one region land in the same
+// cell, so the input rows they share are read into one L2 and each output
+// cache line is completed by one XCD.  Inside a cell the works run in order of
+// position, then segment, then tile.
+void order_works_for_xcds(std::vector<WorkDev>& works, const std::vector<SegDev>& segs, int nimg,
+                          int ho, int bn, int ntiles_n, double x_bytes, double w_bytes) {
+  if (works.size() < 16) return;
+  int best_b = 1;
+  double best = 1e300;
+  for (int b = 1; b <= 8; b *= 2) {
+    if (b > ntiles_n) break;
+    const double cost = x_bytes / (8 / b) + w_bytes / b;
+    if (cost < best) {
+      best = cost;
+      best_b = b;
+    }
+  }
+  const int b = best_b, a = 8 / best_b;
+  struct Key {
+    int64_t cell, pos;
+    int32_t seg, m0, n0;
+  };
+  std::vector<Key> keys;
+  keys.reserve(works.size());
+  for (const WorkDev& w : works) {
+    const SegDev& sg = segs[w.seg];
+    int64_t j = w.m0;
+    j /= sg.qn_w;
+    const int64_t a_h = j % sg.qn_h;
+    j /= sg.qn_h;
+    const int64_t img = j % nimg;
+    const int64_t qt = std::max<int64_t>(1, (ho + sg.out_step_h - 1) / sg.out_step_h);
+    const int64_t qh = std::min<int64_t>(sg.q0_h + a_h, qt - 1);
+    const int64_t pos = img * qt + qh;  // in [0, nimg * qt)
+    const int64_t row = pos * a / ((int64_t)nimg * qt);
+    const int64_t col = (int64_t)(w.n0 / bn) * b / ntiles_n;
+    Key k;
+    k.cell = row * b + col;
+    k.pos = pos;
+    k.seg = w.seg;
+    k.m0 = w.m0;
+    k.n0 = w.n0;
+    keys.push_back(k);
+  }
+  std::stable_sort(keys.begin(), keys.end(), [](const Key& x, const Key& y) {
+    if (x.cell != y.cell) return x.cell < y.cell;
+    if (x.pos != y.pos) return x.pos < y.pos;
+    if (x.seg != y.seg) return x.seg < y.seg;
+    if (x.m0 != y.m0) return x.m0 < y.m0;
+    return x.n0 < y.n0;
+  });
+  for (size_t i = 0; i < works.size(); ++i) {
+    works[i].seg = keys[i].seg;
+    works[i].m0 = keys[i].m0;
+    works[i].n0 = keys[i].n0;
+  }
+}
+
+// Schedule model: the dispatcher hands the works, in list order, to the first
+// free workgroup slot (kComputeUnits x wg_per_cu slots); a work costs its K
+// stages plus about two stages of prologue and epilogue.  Returns the model's
+// makespan in stages.  A work count just above the slot count doubles the
+// makespan, which a finer split into border classes can cause.
+int64_t makespan_stages(const huge2_conv_desc& d, const PlanShape& shape, int cfg) {
+  const int bm = tile_bm(cfg), bn = tile_bn(cfg);
+  const int64_t kc = tile_kb(cfg) / elem_size(d.dtype);
+  const int64_t cblocks = (d.c_in + kc - 1) / kc;
+  const int64_t ntn = (d.c_out + bn - 1) / bn;
+  const int64_t slots = (int64_t)kComputeUnits * kTiles[cfg].wg_per_cu;
+  std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> free_at;
+  int64_t used = 0, end = 0;
+  for (const huge2_segment& s : shape.segs) {
+    const int64_t m = (int64_t)d.n * s.nphase_h * s.nphase_w * s.qn_h * s.qn_w;
+    const int64_t works = (m + bm - 1) / bm * ntn;
+    const int64_t cost = (int64_t)s.tap_count * cblocks + 2;
+    for (int64_t i = 0; i < works; ++i) {
+      int64_t t = 0;
+      if (used < slots) {
+        ++used;
+      } else {
+        t = free_at.top();
+        free_at.pop();
+      }
+      free_at.push(t + cost);
+      end = std::max(end, t + cost);
+    }
+  }
+  return end;
+}
+
+// Border-class splitting of a plan: HUGE2_CLASS_SPLIT (0, 1, 2) forces it;
+// otherwise 0 (one segment per phase group, out-of-range taps read zeros) or
+// 2 (per group, the form that issues fewer tile-taps), whichever the schedule
+// model finishes first (ties: 2).
+int choose_split(const huge2_conv_desc& d, bool transposed, int cfg) {
+  const int forced = env_int("HUGE2_CLASS_SPLIT", -1);
+  if (forced >= 0 && forced <= 2) return forced;
+  PlanShape s0, s2;
+  if (!build_shape(d, transposed, 0, tile_bm(cfg), &s0) ||
+      !build_shape(d, transposed, 2, tile_bm(cfg), &s2))
+    return 2;
+  return makespan_stages(d, s0, cfg) < makespan_stages(d, s2, cfg) ? 0 : 2;
 }
 
 void free_buffers(huge2_plan* p) {
@@ -124,8 +231,8 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   const huge2_conv_desc& d = *desc;
   const bool tr = transposed != 0;
 
-  const int split = class_split_mode();
-  const int cfg = choose_cfg(d, tr, split);
+  const int cfg = choose_cfg(d, tr, 2);
+  const int split = choose_split(d, tr, cfg);
   const int bm = tile_bm(cfg), bn = tile_bn(cfg);
   PlanShape shape;
   if (!build_shape(d, tr, split, bm, &shape)) return HUGE2_ERR_INVALID_ARG;
@@ -245,6 +352,13 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   }
   p->issued_macs = issued;
   p->n_works = (int)works.size();
+  // NCHW outputs of transposed convs with few phases: the phases of a
+  // region share input rows and output cache lines (measured: fewer bytes and
+  // faster); elsewhere the segment-major order measured as fast or faster.
+  const int order = env_int("HUGE2_WORK_ORDER", -1);
+  if (order == 1 || (order < 0 && tr && d.layout == HUGE2_NCHW && d.stride_h * d.stride_w <= 16))
+    order_works_for_xcds(works, segs, d.n, p->ho, bn, ntiles_n, (double)p->x_bytes,
+                         (double)d.r * d.s * p->cout_pad * p->cin_pad * esz);
 
   const size_t seg_b = segs.size() * sizeof(SegDev);
   const size_t tap_b = taps.size() * sizeof(TapDev);
@@ -461,7 +575,7 @@ huge2_status huge2_plan_describe(const huge2_conv_desc* desc, int32_t transposed
   huge2_status st = validate_desc(desc, transposed != 0);
   if (st != HUGE2_OK) return st;
   try {
-    const int cfg = choose_cfg(*desc, transposed != 0, class_split);
+    const int cfg = choose_cfg(*desc, transposed != 0, 2);
     PlanShape shape;
     if (!build_shape(*desc, transposed != 0, class_split, tile_bm(cfg), &shape))
       return HUGE2_ERR_INVALID_ARG;
@@ -482,8 +596,8 @@ huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, in
   huge2_status st = validate_desc(desc, transposed != 0);
   if (st != HUGE2_OK) return st;
   try {
-    const int split = class_split_mode();
-    const int cfg = choose_cfg(*desc, transposed != 0, split);
+    const int cfg = choose_cfg(*desc, transposed != 0, 2);
+    const int split = choose_split(*desc, transposed != 0, cfg);
     const int bm = tile_bm(cfg), bn = tile_bn(cfg);
     PlanShape shape;
     if (!build_shape(*desc, transposed != 0, split, bm, &shape)) return HUGE2_ERR_INVALID_ARG;

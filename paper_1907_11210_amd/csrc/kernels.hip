@@ -493,6 +493,47 @@ __global__ __launch_bounds__(256) void stage_nchw_kernel(const T* __restrict__ x
   }
 }
 
+// NCHW source whose plane size is a multiple of 16 bytes: 64 channels x
+// 128 bytes of pixels per workgroup, read and written in 16-byte pieces (a
+// channel run of one pixel is gathered from an LDS column).
+template <typename T>
+__global__ __launch_bounds__(256) void stage_nchw_vec_kernel(const T* __restrict__ x,
+                                                             T* __restrict__ xs, int cin, int hw,
+                                                             int cs) {
+  constexpr int VE = 16 / sizeof(T);  // elements per 16 bytes
+  constexpr int PX = 8 * VE;          // pixels per tile (128 bytes per channel)
+  constexpr int CC = 64 / VE;         // 16-byte channel chunks per pixel
+  __shared__ __attribute__((aligned(16))) T tile[64][PX + VE];
+  const int img = blockIdx.z, c0 = blockIdx.y * 64, p0 = blockIdx.x * PX;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int q = threadIdx.x + 256 * i;
+    const int c = q >> 3, j = q & 7, p = p0 + j * VE;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (c0 + c < cin && p < hw)
+      v = *(const uint4*)(x + ((size_t)img * cin + c0 + c) * hw + p);
+    *(uint4*)&tile[c][j * VE] = v;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int q = threadIdx.x + 256 * i;
+    const int cc = q % CC, px = q / CC;
+    const int p = p0 + px, c = c0 + cc * VE;
+    if (p >= hw || c >= cs) continue;
+    uint32_t w[4];
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        w[e] = (uint32_t)tile[cc * VE + 2 * e][px] | ((uint32_t)tile[cc * VE + 2 * e + 1][px] << 16);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) w[e] = (uint32_t)tile[cc * VE + e][px];
+    }
+    *(uint4*)(xs + ((size_t)img * hw + p) * cs + c) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
 // NHWC source with cin channels per pixel.
 template <typename T>
 __global__ void stage_nhwc_kernel(const T* __restrict__ x, T* __restrict__ xs, int cin, int cs,
@@ -507,7 +548,16 @@ __global__ void stage_nhwc_kernel(const T* __restrict__ x, T* __restrict__ xs, i
 
 hipError_t launch_stage_input(const void* x, void* xs, int dtype, bool nchw, int n, int cin,
                               int hw, int c_stride, hipStream_t stream) {
-  if (nchw) {
+  const int ve = dtype == 1 ? 8 : 4;
+  if (nchw && hw % ve == 0) {
+    dim3 grid((hw + 8 * ve - 1) / (8 * ve), (c_stride + 63) / 64, n), block(256);
+    if (dtype == 1)
+      hipLaunchKernelGGL(stage_nchw_vec_kernel<uint16_t>, grid, block, 0, stream,
+                         (const uint16_t*)x, (uint16_t*)xs, cin, hw, c_stride);
+    else
+      hipLaunchKernelGGL(stage_nchw_vec_kernel<uint32_t>, grid, block, 0, stream,
+                         (const uint32_t*)x, (uint32_t*)xs, cin, hw, c_stride);
+  } else if (nchw) {
     dim3 grid((hw + 63) / 64, (c_stride + 63) / 64, n), block(256);
     if (dtype == 1)
       hipLaunchKernelGGL(stage_nchw_kernel<uint16_t>, grid, block, 0, stream,

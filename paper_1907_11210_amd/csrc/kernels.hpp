@@ -74,27 +74,31 @@ struct GemmArgs {
 // LDS stage.
 // depth: stages of global loads in flight ahead of the MFMAs (1 or 2; each
 // in-flight stage costs one register buffer).
+// wg_per_cu: workgroups of this shape that fit on one compute unit at once
+// (the tighter of the register and LDS limits; the same for both dtypes and
+// layouts), used by the host's schedule model.
 struct TileShape {
-  int bm, bn, pw, cw, kb, depth;
+  int bm, bn, pw, cw, kb, depth, wg_per_cu;
 };
 constexpr TileShape kTiles[] = {
-    {128, 128, 2, 2, 128, 2},  // 0
-    {256, 32, 4, 1, 128, 2},   // 1  narrow: few output channels
-    {64, 128, 1, 4, 128, 2},   // 2
-    {256, 128, 2, 2, 128, 2},  // 3
-    {128, 256, 2, 2, 128, 2},  // 4
-    {256, 256, 2, 4, 128, 2},  // 5  8 waves
-    {256, 128, 4, 2, 128, 2},  // 6  8 waves
-    {128, 256, 2, 4, 128, 2},  // 7  8 waves
-    {128, 128, 4, 2, 128, 2},  // 8  8 waves
-    {256, 256, 2, 2, 128, 1},  // 9  4 waves of 128 x 128
-    {128, 32, 4, 1, 64, 2},    // 10 narrow, small LDS footprint
-    {256, 32, 4, 1, 64, 2},    // 11 narrow, small LDS footprint
-    {64, 128, 1, 4, 64, 2},    // 12 small LDS footprint
-    {128, 128, 2, 2, 64, 2},   // 13 small LDS footprint
-    {256, 128, 2, 2, 128, 1},  // 14 4 waves of 128 x 64, one buffer
-    {128, 256, 2, 2, 128, 1},  // 15 4 waves of 64 x 128, one buffer
+    {128, 128, 2, 2, 128, 2, 2},  // 0
+    {256, 32, 4, 1, 128, 2, 1},   // 1  narrow: few output channels
+    {64, 128, 1, 4, 128, 2, 2},   // 2
+    {256, 128, 2, 2, 128, 2, 1},  // 3
+    {128, 256, 2, 2, 128, 2, 1},  // 4
+    {256, 256, 2, 4, 128, 2, 1},  // 5  8 waves
+    {256, 128, 4, 2, 128, 2, 1},  // 6  8 waves
+    {128, 256, 2, 4, 128, 2, 1},  // 7  8 waves
+    {128, 128, 4, 2, 128, 2, 2},  // 8  8 waves
+    {256, 256, 2, 2, 128, 1, 1},  // 9  4 waves of 128 x 128
+    {128, 32, 4, 1, 64, 2, 6},    // 10 narrow, small LDS footprint
+    {256, 32, 4, 1, 64, 2, 3},    // 11 narrow, small LDS footprint
+    {64, 128, 1, 4, 64, 2, 5},    // 12 small LDS footprint
+    {128, 128, 2, 2, 64, 2, 3},   // 13 small LDS footprint
+    {256, 128, 2, 2, 128, 1, 1},  // 14 4 waves of 128 x 64, one buffer
+    {128, 256, 2, 2, 128, 1, 1},  // 15 4 waves of 64 x 128, one buffer
 };
+constexpr int kComputeUnits = 256;  // MI355X
 constexpr int TILE_COUNT = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 inline int tile_bm(int cfg) { return kTiles[cfg].bm; }
 inline int tile_bn(int cfg) { return kTiles[cfg].bn; }

@@ -44,6 +44,8 @@ SMALL = [
     L("conv_strided_dilated", False, 2, 8, 11, 11, 40, 3, 3, 2, 2, 0, 2, "NHWC", "f32"),
     L("conv_plain", False, 2, 48, 9, 9, 136, 3, 3, 1, 1, 0, 1, "NCHW", "bf16"),
     L("conv_1x1", False, 1, 64, 5, 5, 64, 1, 1, 1, 0, 0, 1, "NHWC", "bf16"),
+    L("ct_vecstage_bf16", True, 2, 72, 4, 6, 40, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
+    L("ct_vecstage_f32", True, 2, 70, 3, 4, 24, 3, 3, 2, 1, 1, 1, "NCHW", "f32"),
 ]
 
 
@@ -241,3 +243,19 @@ def test_stage_then_gemm_equals_execute(layer):
     assert not torch.isnan(y2).any()
     iv = torch.int16 if y1.dtype == torch.bfloat16 else torch.int32
     assert torch.equal(y1.view(iv), y2.view(iv)), layer.name
+
+
+@pytest.mark.parametrize("split", [0, 1, 2])
+def test_border_class_forms(split, monkeypatch):
+    """Both forms of a phase's border handling (one masked segment, or border
+    classes that read only in-range inputs) and the per-group choice agree
+    with the oracle."""
+    monkeypatch.setenv("HUGE2_CLASS_SPLIT", str(split))
+    for layer in [SMALL[0], SMALL[4], SMALL[9], SMALL[15], SMALL[16], SMALL[18]]:
+        P.say("case split", split, layer)
+        xq, wq = _inputs(layer, seed=50 + split)
+        bias = torch.linspace(-0.5, 0.25, layer.c_out)
+        ref = P.oracle_full(layer, xq, wq, bias)
+        absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
+        y = P.run_gpu(layer, xq, wq, bias)
+        P.check(y, ref, absref, layer.dtype, "%s split %d" % (layer.name, split))

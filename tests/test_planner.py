@@ -173,7 +173,7 @@ def test_dcgan_pattern_parity():
 
 
 @pytest.mark.parametrize("dil", [6, 12, 18, 24])
-def test_aspp_phase_views(dil):
+def test_aspp_phase_views(dil, monkeypatch):
     """A 'same' 3x3 dilated conv on 64x64 splits into dil x dil phase views; the
     planner groups views of equal shape, and with border classes the segments
     issue only their non-zero taps (plus M-tile padding)."""
@@ -186,7 +186,11 @@ def test_aspp_phase_views(dil):
             for b in range(sg["nphase_w"]):
                 phases.add((sg["phase0_h"] + a, sg["phase0_w"] + b))
     assert phases == {(a, b) for a in range(dil) for b in range(dil)}
-    nz, issued = h2.huge2_plan_macs(d, 0)
+    nz, issued_auto = h2.huge2_plan_macs(d, 0)
     expect = {6: 135.9e9, 12: 118.4e9, 18: 102.1e9, 24: 86.97e9}[dil]
     assert abs(nz - expect) / expect < 1e-3
+    assert issued_auto >= nz
+    monkeypatch.setenv("HUGE2_CLASS_SPLIT", "2")
+    nz2, issued = h2.huge2_plan_macs(d, 0)
+    assert nz2 == nz
     assert nz <= issued <= 1.10 * nz  # only the ragged ends of M tiles are padding

@@ -10,7 +10,10 @@ input-staging launch where the layout needs one (NCHW, or channels not a
 multiple of the vector width) followed by one GEMM launch
 (huge2_plan_stage_input + huge2_plan_run_gemm, the two halves of
 huge2_plan_execute); the plans (weight packing) are built before the timed
-region.
+region.  Kernels are launched eagerly from the host (measured faster here
+than replaying the step as one captured HIP graph, which --launch graph
+does after checking a replay bitwise against the eager step).  Per-layer
+times come from a separate eager pass with HIP events around each kernel.
 
 Prints ONE JSON line.  Fields beyond the standard ones:
   roofline      the dominant layer's GEMM kernel (the longest mean launch, timed
@@ -63,6 +66,8 @@ def parse():
                     help="target CPU time of the oracle sample")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 256 MiB device copy (to scale HBM traffic counters)")
+    ap.add_argument("--launch", choices=["graph", "eager"], default="eager",
+                    help="replay each timed step as one captured HIP graph, or launch eagerly")
     ap.add_argument("--summarize-profiles", metavar="DIR",
                     help="no GPU: turn the rocprofv3 CSVs of PROFILE_COMMANDS under DIR into "
                          "the summaries under profiles/")
@@ -107,7 +112,7 @@ def build_workload(name, dev):
             if events is not None:
                 events[3 * i + 2].record()
 
-    return items, plans, step
+    return items, plans, step, lambda: outs
 
 
 def kernel_source_sha():
@@ -345,7 +350,7 @@ def main():
     if args.copy_calibration:
         copy_calibration(dev)
         return
-    items, plans, step = build_workload(args.workload, dev)
+    items, plans, step, step_outputs = build_workload(args.workload, dev)
     flops = layer_flops(plans)
     issued = [2 * p.macs()[1] for p in plans]
     total_flops = sum(flops)
@@ -356,19 +361,58 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    nl = len(plans)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3 * nl)] for _ in range(args.steps)]
+    # The whole step as one HIP graph (the library's launches are captured on
+    # torch's capture stream); replays must reproduce the eager outputs bitwise.
+    graph = None
+    if args.launch == "graph":
+        eager_out = [o.clone() for o in step_outputs()]
+        s_side = torch.cuda.Stream()
+        s_side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s_side):
+            step()
+        torch.cuda.current_stream().wait_stream(s_side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+        for _ in range(3):
+            for o in step_outputs():
+                o.fill_(float("nan"))
+            graph.replay()
+            torch.cuda.synchronize()
+            for o, e in zip(step_outputs(), eager_out):
+                iv = torch.int16 if o.dtype == torch.bfloat16 else torch.int32
+                if not torch.equal(o.view(iv), e.view(iv)):
+                    raise RuntimeError("graph replay differs from the eager step")
+        del eager_out
+
+    def run_once():
+        if graph is not None:
+            graph.replay()
+        else:
+            step()
+
+    for _ in range(args.warmup):
+        run_once()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     start.record()
-    for k in range(args.steps):
-        step(ev[k])
+    for _ in range(args.steps):
+        run_once()
     stop.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = start.elapsed_time(stop) / args.steps
 
+    # Per-layer breakdown: a separate eager pass with events around each kernel.
+    nl = len(plans)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3 * nl)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for k in range(args.steps):
+        step(ev[k])
+    torch.cuda.synchronize()
     stage_ms = np.array([[ev[k][3 * i].elapsed_time(ev[k][3 * i + 1]) for i in range(nl)]
                          for k in range(args.steps)]).mean(axis=0)
     gemm_ms = np.array([[ev[k][3 * i + 1].elapsed_time(ev[k][3 * i + 2]) for i in range(nl)]
@@ -424,7 +468,8 @@ def main():
         "dtype": dtype,
         "data": "synthetic (seeded; random-init weights of the workload's shapes)",
         "config": {"workload": args.workload, "description": DESCRIPTIONS[args.workload],
-                   "batch": items[0][0].n, "layout": items[0][0].layout},
+                   "batch": items[0][0].n, "layout": items[0][0].layout,
+                   "launch": "one HIP graph per step" if graph is not None else "eager launches"},
         "roofline": roofline,
         "layers": layers,
         "kernel_source_sha": kernel_source_sha(),

@@ -39,6 +39,8 @@ struct huge2_plan {
   bool stream_ordered;  // buffers came from hipMallocAsync on alloc_stream
   hipStream_t alloc_stream;
   int64_t nonzero_macs, issued_macs;
+  bool ztile;   // all-taps form for few output channels (no GEMM work list)
+  ZArgs zargs;  // its launch shape (pointers filled per call)
 };
 
 namespace {
@@ -180,6 +182,107 @@ int64_t makespan_stages(const huge2_conv_desc& d, const PlanShape& shape, int cf
   return end;
 }
 
+int floor_div_i(int a, int b) { return a >= 0 ? a / b : -((-a + b - 1) / b); }
+int ceil_div_i(int a, int b) { return -floor_div_i(-a, b); }
+
+// Channel pitch of the all-taps tile, in elements: an odd multiple of the
+// 16-byte vector, so that the two lane halves of an MFMA fragment (channels
+// 8 apart) read disjoint halves of the LDS banks.
+int cpitch_of(int elems, int ve) {
+  int c = round_up(elems, ve);
+  if ((c / ve) % 2 == 0) c += ve;
+  return c;
+}
+
+// The all-taps form (ztile_kernel) applies to NCHW transposed convs whose
+// taps x output channels fit one 64-column MFMA tile, with 16-byte input rows
+// strides up to 4, at most 4 taps of an axis reaching one output phase and
+// output rows of at most 256 columns.
+// The block of output rows per workgroup is the largest multiple of the
+// stride whose input tile fits the LDS budget while the grid still has one
+// workgroup per CU; small problems take the smallest block that fits.
+// Returns false when the form does not apply (or HUGE2_ZTILE=0, or a GEMM
+// tile is forced through HUGE2_TILE).
+bool ztile_shape(const huge2_conv_desc& d, bool transposed, ZArgs* z, int64_t* issued) {
+  // bf16 only: in fp32 the phase GEMM measured faster
+  if (!transposed || d.layout != HUGE2_NCHW || d.dtype != HUGE2_BF16) return false;
+  if (env_int("HUGE2_ZTILE", 1) == 0 || env_int("HUGE2_TILE", -1) >= 0) return false;
+  const int esz = elem_size(d.dtype), ve = 16 / esz;
+  if ((long long)d.c_out * d.r * d.s > 64 || d.w % ve != 0) return false;
+  if (d.stride_h > kZtileMaxStride || d.stride_w > kZtileMaxStride || d.r > kZtileMaxTaps ||
+      d.s > kZtileMaxTaps || d.dil_h > 16 || d.dil_w > 16)
+    return false;
+  int ho, wo;
+  if (!output_dims(d, true, &ho, &wo)) return false;
+  const int j_lo = ceil_div_i(d.pad_w - (d.s - 1) * d.dil_w, d.stride_w);
+  const int j_hi = floor_div_i(wo - 1 + d.pad_w, d.stride_w);
+  if (j_lo < -kZtileColOff || wo > 256) return false;
+  const int tcw = j_hi - j_lo + 1;
+  const int tcp = round_up(std::max(j_hi, d.w - 1) + kZtileColOff + 1, ve);
+  const int cchunk = esz == 2 ? 64 : 32;
+  const int cin_pad = round_up(d.c_in, cchunk);
+  const int i_off = ceil_div_i(d.pad_h - (d.r - 1) * d.dil_h, d.stride_h);
+  int best = -1, fallback = -1;
+  for (int q = (ho + d.stride_h - 1) / d.stride_h; q >= 1; --q) {
+    const int ob = std::min(q * d.stride_h, ho);
+    const int tr = floor_div_i(ob - 1 + d.pad_h, d.stride_h) - i_off + 1;
+    const long long np = (long long)tr * tcw;
+    if (np > kZtileMaxPixels) continue;
+    if ((long long)cin_pad * cpitch_of(tr * tcp, ve) * esz > kZtileLds) continue;
+    const long long blocks = (long long)d.n * ((ho + ob - 1) / ob);
+    fallback = ob;
+    if (best < 0 && blocks >= kComputeUnits) best = ob;
+  }
+  const int ob = best >= 0 ? best : fallback;
+  if (ob < 0) return false;
+  std::memset(z, 0, sizeof(*z));
+  z->n = d.n;
+  z->cin = d.c_in;
+  z->h = d.h;
+  z->w = d.w;
+  z->cout = d.c_out;
+  z->r = d.r;
+  z->s = d.s;
+  z->cin_pad = cin_pad;
+  z->cout_pad = d.c_out;
+  z->stride_h = d.stride_h;
+  z->stride_w = d.stride_w;
+  z->pad_h = d.pad_h;
+  z->pad_w = d.pad_w;
+  z->dil_h = d.dil_h;
+  z->dil_w = d.dil_w;
+  z->ho = ho;
+  z->wo = wo;
+  z->ob = ob;
+  z->tr = floor_div_i(ob - 1 + d.pad_h, d.stride_h) - i_off + 1;
+  z->tcw = tcw;
+  z->tcp = tcp;
+  z->cpitch = cpitch_of(z->tr * tcp, ve);
+  z->j_lo = j_lo;
+  z->cchunk = cchunk;
+  // per-phase tap tables: output o with o + pad = stride*Q + rho reads input
+  // Q + delta through kernel tap k when rho - k*dil = stride*delta
+  const int strides[2] = {d.stride_h, d.stride_w}, ks[2] = {d.r, d.s}, dils[2] = {d.dil_h, d.dil_w};
+  for (int ax = 0; ax < 2; ++ax)
+    for (int rho = 0; rho < strides[ax]; ++rho) {
+      int cnt = 0;
+      for (int k = 0; k < ks[ax]; ++k) {
+        const int num = rho - k * dils[ax];
+        if (((num % strides[ax]) + strides[ax]) % strides[ax] != 0) continue;
+        if (cnt == kZtilePhaseTaps) return false;
+        z->tap_k[ax][rho][cnt] = (int8_t)k;
+        z->tap_d[ax][rho][cnt] = (int8_t)(num / strides[ax]);
+        ++cnt;
+      }
+      z->tap_n[ax][rho] = (int8_t)cnt;
+      int& mx = ax == 0 ? z->max_th : z->max_tw;
+      mx = std::max(mx, cnt);
+    }
+  const int64_t np = (int64_t)z->tr * tcw;
+  *issued = (int64_t)d.n * ((ho + ob - 1) / ob) * ((np + 31) / 32 * 32) * 64 * z->cin_pad;
+  return true;
+}
+
 // Border-class splitting of a plan: HUGE2_CLASS_SPLIT (0, 1, 2) forces it;
 // otherwise 0 (one segment per phase group, out-of-range taps read zeros) or
 // 2 (per group, the form that issues fewer tile-taps), whichever the schedule
@@ -220,6 +323,54 @@ huge2_status dev_alloc(huge2_plan* p, void** out, size_t bytes) {
   return HUGE2_OK;
 }
 
+// Plan of the all-taps form: packed K-contiguous weights only (the kernel
+// reads the NCHW input directly, so nothing is staged).
+huge2_status create_ztile(huge2_plan** out, const huge2_conv_desc& d, int transposed,
+                          const void* w, hipStream_t stream, bool stream_ordered, const ZArgs& z,
+                          int64_t issued) {
+  PlanShape shape;
+  if (!build_shape(d, true, 2, 128, &shape)) return HUGE2_ERR_INVALID_ARG;
+  huge2_plan* p = new (std::nothrow) huge2_plan();
+  if (!p) return HUGE2_ERR_ALLOC;
+  const int esz = elem_size(d.dtype);
+  p->desc = d;
+  p->transposed = transposed;
+  p->ho = z.ho;
+  p->wo = z.wo;
+  p->cfg = -1;
+  p->staged = false;
+  p->c_stride = d.c_in;
+  p->cin_pad = z.cin_pad;
+  p->cout_pad = z.cout_pad;
+  p->x_bytes = (size_t)d.n * d.c_in * d.h * d.w * esz;
+  p->wp_bytes = (size_t)d.r * d.s * z.cout_pad * z.cin_pad * esz;
+  p->stream_ordered = stream_ordered;
+  p->alloc_stream = stream;
+  p->nonzero_macs = shape.nonzero_macs;
+  p->issued_macs = issued;
+  p->ztile = true;
+  p->zargs = z;
+  huge2_status st = dev_alloc(p, &p->wp, p->wp_bytes);
+  if (st != HUGE2_OK) {
+    free_buffers(p);
+    delete p;
+    return st;
+  }
+  bool ok = !fault("launch");
+  if (ok)
+    ok = launch_pack_weights(w, p->wp, d.dtype, true, d.c_in, d.c_out, d.r, d.s, z.cin_pad,
+                             z.cout_pad, 0, stream) == hipSuccess;
+  if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
+  if (!ok) {
+    (void)hipGetLastError();
+    free_buffers(p);
+    delete p;
+    return HUGE2_ERR_HIP;
+  }
+  *out = p;
+  return HUGE2_OK;
+}
+
 huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int transposed,
                          const void* w, hipStream_t stream, bool stream_ordered) {
   if (!out) return HUGE2_ERR_INVALID_ARG;
@@ -230,6 +381,13 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   if (!w) return HUGE2_ERR_INVALID_ARG;
   const huge2_conv_desc& d = *desc;
   const bool tr = transposed != 0;
+
+  {
+    ZArgs z;
+    int64_t z_issued = 0;
+    if (ztile_shape(d, tr, &z, &z_issued))
+      return create_ztile(out, d, transposed, w, stream, stream_ordered, z, z_issued);
+  }
 
   const int cfg = choose_cfg(d, tr, 2);
   const int split = choose_split(d, tr, cfg);
@@ -389,7 +547,8 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     ok = hipMemcpyAsync(p->meta, host.data(), meta_b, hipMemcpyHostToDevice, stream) == hipSuccess;
   if (ok)
     ok = launch_pack_weights(w, p->wp, d.dtype, tr, d.c_in, d.c_out, d.r, d.s, p->cin_pad,
-                             p->cout_pad, stream) == hipSuccess;
+                             p->cout_pad, kTiles[cfg].kind == 1 ? tile_kb(cfg) : 0,
+                             stream) == hipSuccess;
   // the host copy of the metadata must outlive the transfer
   if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
   if (!ok) {
@@ -421,6 +580,18 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
   if (!p || !y || (!p->staged && !x) || x == y) return HUGE2_ERR_INVALID_ARG;
   const huge2_conv_desc& d = p->desc;
   if (fault("launch")) return HUGE2_ERR_HIP;
+  if (p->ztile) {
+    ZArgs z = p->zargs;
+    z.x = x;
+    z.wp = p->wp;
+    z.bias = bias;
+    z.y = y;
+    if (launch_ztile(z, d.dtype, stream) != hipSuccess) {
+      (void)hipGetLastError();
+      return HUGE2_ERR_HIP;
+    }
+    return HUGE2_OK;
+  }
   GemmArgs a;
   a.x = p->staged ? p->xs : x;
   a.wp = p->wp;
@@ -596,6 +767,15 @@ huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, in
   huge2_status st = validate_desc(desc, transposed != 0);
   if (st != HUGE2_OK) return st;
   try {
+    ZArgs z;
+    int64_t z_issued = 0;
+    if (ztile_shape(*desc, transposed != 0, &z, &z_issued)) {
+      PlanShape shape;
+      if (!build_shape(*desc, true, 2, 128, &shape)) return HUGE2_ERR_INVALID_ARG;
+      *nonzero_macs = shape.nonzero_macs;
+      *issued_macs = z_issued;
+      return HUGE2_OK;
+    }
     const int cfg = choose_cfg(*desc, transposed != 0, 2);
     const int split = choose_split(*desc, transposed != 0, cfg);
     const int bm = tile_bm(cfg), bn = tile_bn(cfg);

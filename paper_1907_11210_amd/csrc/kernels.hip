@@ -11,6 +11,8 @@
 //  pack_weights_kernel the per-tap sub-kernel blocks (the N x C matrix of each
 //                      kernel position, section 3.2.1), K-contiguous.
 //  stage_*_kernel      input re-layout to channel-contiguous pixels.
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace huge2 {
@@ -61,6 +63,67 @@ __device__ __forceinline__ PixelPos pixel_pos(const SegDev& sg, int nimg, int m)
   p.ih = sg.in0_h + sg.in_dphase_h * (int)iph_h + sg.in_step_h * qh;
   p.iw = sg.in0_w + sg.in_dphase_w * iph_w + sg.in_step_w * qw;
   return p;
+}
+
+// Epilogue: bias, rounding, and the scatter of a wave's TP x TC blocks of
+// 32 x 32 results (pixels from pix0, output channels from ch0) to the
+// interleaved output positions of their phase.  32x32 MFMA result layout:
+// lane l holds column l % 32 and rows 8*(r/4) + 4*(l/32) + (r%4), r = 0..15.
+// NCHW output puts pixels on the columns (a channel's stores coalesce along
+// the lanes); NHWC output puts pixels on the rows.
+// sb: bias by output channel (sb[ch], staged in LDS, zeros without bias):
+// reading it from global memory between the stores would make every load
+// wait for the stores issued before it.
+template <bool BF16, bool NCHW_OUT, int TP, int TC>
+__device__ __forceinline__ void store_tile(const GemmArgs& a, const SegDev& sg,
+                                           const f32x16 (&acc)[TP][TC], int pix0, int ch0,
+                                           int lane, const float* sb) {
+  const int hw_o = a.ho * a.wo;
+  if constexpr (!NCHW_OUT) {
+#pragma unroll
+    for (int i = 0; i < TP; ++i) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = pix0 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (m >= sg.m_total) continue;
+        const PixelPos p = pixel_pos(sg, a.n, m);
+        const int pix = (p.img * a.ho + p.oh) * a.wo + p.ow;
+#pragma unroll
+        for (int j = 0; j < TC; ++j) {
+          const int ch = ch0 + 32 * j + (lane & 31);
+          if (ch >= a.cout) continue;
+          const float v = acc[i][j][r] + sb[ch];
+          const size_t off = (size_t)pix * a.cout + ch;
+          if constexpr (BF16)
+            ((uint16_t*)a.y)[off] = f32_to_bf16_rne(v);
+          else
+            ((float*)a.y)[off] = v;
+        }
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < TP; ++i) {
+      const int m = pix0 + 32 * i + (lane & 31);
+      if (m >= sg.m_total) continue;
+      const PixelPos p = pixel_pos(sg, a.n, m);
+      const size_t base = (size_t)p.img * a.cout * hw_o + (size_t)p.oh * a.wo + p.ow;
+#pragma unroll
+      for (int j = 0; j < TC; ++j) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int ch = ch0 + 32 * j + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (ch >= a.cout) continue;
+          const float v = acc[i][j][r] + sb[ch];
+          const size_t off = base + (size_t)ch * hw_o;
+          if constexpr (BF16)
+            ((uint16_t*)a.y)[off] = f32_to_bf16_rne(v);
+          else
+            ((float*)a.y)[off] = v;
+        }
+      }
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -138,6 +201,10 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
   const int nsteps = ntaps * cblocks;
   // channels of the last K block that exist (a partial block needs masking)
   const int tail_c = a.cin - (cblocks - 1) * KC;
+
+  __shared__ float s_bias[BN];
+  for (int t = tid; t < BN; t += NT)
+    s_bias[t] = (a.bias && wk.n0 + t < a.cout) ? a.bias[wk.n0 + t] : 0.f;
 
   // The segment's taps in LDS: byte delta of the tapped pixel and byte
   // offset of the tap's weight block.
@@ -345,64 +412,292 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
     }
   }
 
-  // Epilogue: bias, rounding, and the scatter to the interleaved output.
-  // 32x32 MFMA result layout: lane l holds column l%32 and rows
-  // 8*(r/4) + 4*(l/32) + (r%4) for r = 0..15.
-  const int hw_o = a.ho * a.wo;
-  if constexpr (!NCHW_OUT) {
+  store_tile<BF16, NCHW_OUT, TP, TC>(a, sg, acc, wk.m0 + wp_i * WP, wk.n0 + wc_i * WC, lane,
+                                     s_bias - wk.n0);
+}
+
+// ---------------------------------------------------------------------------
+// Phase GEMM, split-wave form.  The W waves of a workgroup split its BM x BN
+// tile along one dimension only.  The operand every wave needs (SHARE_A: the
+// BM pixel rows; otherwise the BN weight rows) goes through LDS, written once
+// and read once per wave per stage; each wave loads its own slice of the
+// other operand straight from global memory into registers, already in the
+// MFMA lane layout (lane l: row l % 32, bytes [(l/32)*KB/2, (l/32+1)*KB/2)
+// of the stage).  Per K element, LDS then moves RS*(W+1) rows' bytes for
+// 2*BM*BN flops, against (BM+BN) + W*(wave rows + wave columns) rows in the
+// form above, which is what bounds the MFMA rate at small wave tiles.
+// DEPTH register buffers hold the stages in flight; the loop is unrolled by
+// U = lcm(DEPTH, 2) so that every buffer index is a compile-time constant.
+template <bool BF16, int BM, int BN, int W, int KB, int DEPTH, bool SHARE_A, bool NCHW_OUT>
+__global__ __launch_bounds__(W * 64) void phase_gemm2_kernel(GemmArgs a) {
+  constexpr int NT = W * 64;
+  constexpr int ESZ = BF16 ? 2 : 4;
+  constexpr int KC = KB / ESZ;    // K elements per stage
+  constexpr int VE = 16 / ESZ;    // elements per 16-byte chunk
+  constexpr int CPR = KB / 16;    // 16-byte chunks per row and stage
+  constexpr int HC = CPR / 2;     // chunks per lane half
+  constexpr int ROWB = KB + 16;   // LDS row pitch
+  constexpr int RS = SHARE_A ? BM : BN;        // rows through LDS
+  constexpr int RD = (SHARE_A ? BN : BM) / W;  // rows each wave loads itself
+  constexpr int TS = RS / 32, TD = RD / 32;
+  constexpr int TP = SHARE_A ? TS : TD, TC = SHARE_A ? TD : TS;
+  constexpr int S_LD = (RS * CPR + NT - 1) / NT;  // shared-operand loads per thread
+  constexpr int U = DEPTH == 3 ? 6 : (DEPTH == 1 ? 2 : DEPTH);
+  static_assert(RD % 32 == 0 && RS % 32 == 0 && HC >= 1, "32-row blocks, whole lane halves");
+  static_assert(DEPTH >= 2 && DEPTH <= 4, "two to four stages in flight");
+  constexpr int STAGE_B = RS * ROWB;
+  constexpr uint32_t OOB = 0x80000000u;
+  __shared__ __attribute__((aligned(16))) char smem[2 * STAGE_B];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int half = lane >> 5, row32 = lane & 31;
+  const int work = xcd_remap(blockIdx.x, gridDim.x);
+  const WorkDev wk = a.works[work];
+  const SegDev sg = a.segs[wk.seg];
+  const __amdgpu_buffer_rsrc_t xr =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.x, 0, a.x_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t wr =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.wp, 0, a.wp_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t xr0 =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.x, 0, 0, 0x00020000);
+  const __amdgpu_buffer_rsrc_t wr0 =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.wp, 0, 0, 0x00020000);
+
+  // Pixel rows this thread loads: the shared rows (SHARE_A, S_LD of them, as
+  // chunk tid % CPR) or its wave's own rows (TD of them, as lane half).
+  constexpr int NPIX = SHARE_A ? S_LD : TD;
+  int p_ih[NPIX], p_iw[NPIX];
+  uint32_t p_base[NPIX];
+  const int s_chunk = tid % CPR;
 #pragma unroll
-    for (int i = 0; i < TP; ++i) {
+  for (int i = 0; i < NPIX; ++i) {
+    const int r = SHARE_A ? tid / CPR + (NT / CPR) * i : wave * RD + 32 * i + row32;
+    const int m = min(wk.m0 + r, sg.m_total - 1);
+    const PixelPos p = pixel_pos(sg, a.n, m);
+    p_ih[i] = p.ih;
+    p_iw[i] = p.iw;
+    const uint32_t byte_in_row = SHARE_A ? (uint32_t)(s_chunk * 16) : (uint32_t)(half * (KB / 2));
+    p_base[i] = (((uint32_t)p.img * (uint32_t)a.h + (uint32_t)p.ih) * (uint32_t)a.w +
+                 (uint32_t)p.iw) * (uint32_t)a.cin * ESZ + byte_in_row;
+  }
+  // Weight rows (output channels) this thread loads, byte offset in a tap block.
+  constexpr int NW = SHARE_A ? TD : S_LD;
+  uint32_t w_off[NW];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = wk.m0 + wp_i * WP + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (m >= sg.m_total) continue;
-        const PixelPos p = pixel_pos(sg, a.n, m);
-        const int pix = (p.img * a.ho + p.oh) * a.wo + p.ow;
+  for (int i = 0; i < NW; ++i) {
+    if (SHARE_A) {
+      // lane-ordered weights: 32-channel block (n0 + wave*RD)/32 + i
+      w_off[i] = (uint32_t)(((wk.n0 + wave * RD) / 32 + i) * 32 * a.cin_pad * ESZ + lane * 16);
+    } else {
+      const int r = tid / CPR + (NT / CPR) * i;
+      w_off[i] = tid + NT * i < RS * CPR
+                     ? (uint32_t)(((wk.n0 + r) * a.cin_pad) * ESZ + s_chunk * 16)
+                     : OOB;
+    }
+  }
+
+  const int ntaps = sg.tap_count;
+  const int cblocks = a.cin_pad / KC;
+  const int nsteps = ntaps * cblocks;
+  const int tail_c = a.cin - (cblocks - 1) * KC;
+
+  __shared__ float s_bias[BN];
+  for (int t = tid; t < BN; t += NT)
+    s_bias[t] = (a.bias && wk.n0 + t < a.cout) ? a.bias[wk.n0 + t] : 0.f;
+  __shared__ int4 s_taps[kMaxLdsTaps];
+  const bool lds_taps = !sg.tap_ap && ntaps <= kMaxLdsTaps;
+  if (lds_taps) {
+    for (int t = tid; t < ntaps; t += NT) {
+      const TapDev tp = a.taps[sg.tap_begin + t];
+      s_taps[t] = make_int4((tp.off_h * a.w + tp.off_w) * a.cin * ESZ,
+                            (int)((uint32_t)tp.slot * (uint32_t)a.cout_pad * (uint32_t)a.cin_pad * ESZ),
+                            tp.off_h, tp.off_w);
+    }
+  }
+  __syncthreads();
+
+  struct Regs {
+    uint4 s[S_LD];      // shared operand, this thread's chunks
+    uint4 d[TD][HC];    // this wave's own operand, MFMA layout
+  };
+  Regs rb[DEPTH];
+
+  int ld_tap = 0, ld_cb = 0, ld_th = 0, ld_tw = 0;
+  const uint32_t slot_bytes = (uint32_t)a.cout_pad * (uint32_t)a.cin_pad * ESZ;
+  auto load_step = [&](Regs& R, bool valid) {
+    const __amdgpu_buffer_rsrc_t xs = valid ? xr : xr0;
+    const __amdgpu_buffer_rsrc_t ws = valid ? wr : wr0;
+    int delta, off_h, off_w;
+    uint32_t slot_b;
+    if (sg.tap_ap) {
+      off_h = sg.off0_h + ld_th * sg.doff_h;
+      off_w = sg.off0_w + ld_tw * sg.doff_w;
+      delta = (off_h * a.w + off_w) * a.cin * ESZ;
+      slot_b = (uint32_t)((sg.kh0 + ld_th * sg.dkh) * a.ks + sg.kw0 + ld_tw * sg.dkw) * slot_bytes;
+    } else {
+      int4 ti;
+      if (lds_taps) {
+        ti = s_taps[valid ? ld_tap : 0];
+      } else {
+        const TapDev tp = a.taps[sg.tap_begin + (valid ? ld_tap : 0)];
+        ti = make_int4((tp.off_h * a.w + tp.off_w) * a.cin * ESZ, (int)((uint32_t)tp.slot * slot_bytes),
+                       tp.off_h, tp.off_w);
+      }
+      delta = __builtin_amdgcn_readfirstlane(ti.x);
+      slot_b = (uint32_t)__builtin_amdgcn_readfirstlane(ti.y);
+      off_h = __builtin_amdgcn_readfirstlane(ti.z);
+      off_w = __builtin_amdgcn_readfirstlane(ti.w);
+    }
+    const uint32_t kb = (uint32_t)ld_cb * KB;
+    const bool tail = ld_cb == cblocks - 1 && tail_c < KC;
+    auto pix_off = [&](int i) {
+      uint32_t v = p_base[i] + (uint32_t)delta;
+      if (!sg.exact) {
+        const int ih = p_ih[i] + off_h, iw = p_iw[i] + off_w;
+        const bool in = ((unsigned)ih < (unsigned)a.h) & ((unsigned)iw < (unsigned)a.w);
+        v = in ? v : OOB;
+      }
+      return v;
+    };
+    // the wave's own operand first: waiting for the shared chunks of a stage
+    // then also covers these loads
+    if constexpr (SHARE_A) {
 #pragma unroll
-        for (int j = 0; j < TC; ++j) {
-          const int ch = wk.n0 + wc_i * WC + 32 * j + (lane & 31);
-          if (ch >= a.cout) continue;
-          float v = acc[i][j][r];
-          if (a.bias) v += a.bias[ch];
-          const size_t off = (size_t)pix * a.cout + ch;
-          if constexpr (BF16)
-            ((uint16_t*)a.y)[off] = f32_to_bf16_rne(v);
-          else
-            ((float*)a.y)[off] = v;
+      for (int i = 0; i < TD; ++i)
+#pragma unroll
+        for (int c = 0; c < HC; ++c)
+          R.d[i][c] = __builtin_bit_cast(
+              uint4, __builtin_amdgcn_raw_buffer_load_b128(ws, w_off[i], slot_b + 32 * kb + 1024 * c, 0));
+#pragma unroll
+      for (int i = 0; i < S_LD; ++i) {
+        uint32_t v = pix_off(i);
+        v = (tail && s_chunk * VE >= tail_c) ? OOB : v;
+        R.s[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xs, v, kb, 0));
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < TD; ++i) {
+        const uint32_t v = pix_off(i);
+#pragma unroll
+        for (int c = 0; c < HC; ++c) {
+          const bool out = tail && (half * HC + c) * VE >= tail_c;
+          R.d[i][c] = __builtin_bit_cast(
+              uint4, __builtin_amdgcn_raw_buffer_load_b128(xs, out ? OOB : v, kb + 16 * c, 0));
         }
       }
+#pragma unroll
+      for (int i = 0; i < S_LD; ++i)
+        R.s[i] = __builtin_bit_cast(
+            uint4, __builtin_amdgcn_raw_buffer_load_b128(ws, w_off[i], slot_b + kb, 0));
     }
-  } else {
+    if (valid) {
+      if (++ld_tw == sg.ntw) {
+        ld_tw = 0;
+        ++ld_th;
+      }
+      if (++ld_tap == ntaps) {
+        ld_tap = 0;
+        ld_th = 0;
+        ld_tw = 0;
+        ++ld_cb;
+      }
+    }
+  };
+  auto store_shared = [&](int buf, const Regs& R) {
+    char* ss = smem + buf * STAGE_B;
 #pragma unroll
-    for (int i = 0; i < TP; ++i) {
-      const int m = wk.m0 + wp_i * WP + 32 * i + (lane & 31);
-      if (m >= sg.m_total) continue;
-      const PixelPos p = pixel_pos(sg, a.n, m);
-      const size_t base = (size_t)p.img * a.cout * hw_o + (size_t)p.oh * a.wo + p.ow;
+    for (int i = 0; i < S_LD; ++i)
+      if (RS * CPR % NT == 0 || tid + NT * i < RS * CPR)
+        *(uint4*)(ss + (tid / CPR + (NT / CPR) * i) * ROWB + s_chunk * 16) = R.s[i];
+  };
+
+  f32x16 acc[TP][TC];
 #pragma unroll
-      for (int j = 0; j < TC; ++j) {
+  for (int i = 0; i < TP; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int ch = wk.n0 + wc_i * WC + 32 * j + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-          if (ch >= a.cout) continue;
-          float v = acc[i][j][r];
-          if (a.bias) v += a.bias[ch];
-          const size_t off = base + (size_t)ch * hw_o;
-          if constexpr (BF16)
-            ((uint16_t*)a.y)[off] = f32_to_bf16_rne(v);
-          else
-            ((float*)a.y)[off] = v;
-        }
+    for (int j = 0; j < TC; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  auto compute = [&](int buf, const Regs& R) {
+    const char* ss = smem + buf * STAGE_B + row32 * ROWB + half * (KB / 2);
+#pragma unroll
+    for (int c = 0; c < HC; ++c) {
+      uint4 fs[TS];
+#pragma unroll
+      for (int i = 0; i < TS; ++i) fs[i] = *(const uint4*)(ss + 32 * i * ROWB + 16 * c);
+      uint4 fp[TP], fc[TC];
+#pragma unroll
+      for (int i = 0; i < TP; ++i) fp[i] = SHARE_A ? fs[i] : R.d[i][c];
+#pragma unroll
+      for (int j = 0; j < TC; ++j) fc[j] = SHARE_A ? R.d[j][c] : fs[j];
+      if constexpr (BF16) {
+#pragma unroll
+        for (int i = 0; i < TP; ++i)
+#pragma unroll
+          for (int j = 0; j < TC; ++j) {
+            const bf16x8 vp = __builtin_bit_cast(bf16x8, fp[i]);
+            const bf16x8 vc = __builtin_bit_cast(bf16x8, fc[j]);
+            if constexpr (NCHW_OUT)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vc, vp, acc[i][j], 0, 0, 0);
+            else
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vp, vc, acc[i][j], 0, 0, 0);
+          }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int i = 0; i < TP; ++i)
+#pragma unroll
+            for (int j = 0; j < TC; ++j) {
+              const uint32_t bp = e == 0 ? fp[i].x : e == 1 ? fp[i].y : e == 2 ? fp[i].z : fp[i].w;
+              const uint32_t bc = e == 0 ? fc[j].x : e == 1 ? fc[j].y : e == 2 ? fc[j].z : fc[j].w;
+              const float vp = __uint_as_float(bp), vc = __uint_as_float(bc);
+              if constexpr (NCHW_OUT)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(vc, vp, acc[i][j], 0, 0, 0);
+              else
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(vp, vc, acc[i][j], 0, 0, 0);
+            }
+      }
+    }
+  };
+
+  // Prologue: stages 0 .. DEPTH-1 in flight, stage 0 in LDS buffer 0.  Loop
+  // invariant at the top of step u of an unrolled block starting at stage s:
+  // LDS buffer (u & 1) holds stage s+u, register buffer (u % DEPTH) holds its
+  // own-operand chunks, and the next DEPTH-1 stages are in flight.
+  const int nsteps_u = (nsteps + U - 1) / U * U;
+  if (nsteps_u > 0) {
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) load_step(rb[d], d < nsteps);
+    store_shared(0, rb[0]);
+    __syncthreads();
+    for (int s = 0; s < nsteps_u; s += U) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        compute(u & 1, rb[u % DEPTH]);
+        store_shared((u + 1) & 1, rb[(u + 1) % DEPTH]);
+        load_step(rb[u % DEPTH], s + u + DEPTH < nsteps);
+        __syncthreads();
       }
     }
   }
+
+  const int pix0 = wk.m0 + (SHARE_A ? 0 : wave * RD);
+  const int ch0 = wk.n0 + (SHARE_A ? wave * RD : 0);
+  store_tile<BF16, NCHW_OUT, TP, TC>(a, sg, acc, pix0, ch0, lane, s_bias - wk.n0);
 }
 
 template <bool BF16, bool NCHW_OUT, int CFG>
 static void launch_one(const GemmArgs& a, hipStream_t stream) {
   constexpr TileShape t = kTiles[CFG];
-  hipLaunchKernelGGL((phase_gemm_kernel<BF16, t.bm, t.bn, t.pw, t.cw, t.kb, t.depth, NCHW_OUT>),
-                     dim3(a.n_works), dim3(t.pw * t.cw * 64), 0, stream, a);
+  if constexpr (t.kind == 0)
+    hipLaunchKernelGGL((phase_gemm_kernel<BF16, t.bm, t.bn, t.pw, t.cw, t.kb, t.depth, NCHW_OUT>),
+                       dim3(a.n_works), dim3(t.pw * t.cw * 64), 0, stream, a);
+  else
+    hipLaunchKernelGGL((phase_gemm2_kernel<BF16, t.bm, t.bn, t.pw * t.cw, t.kb, t.depth,
+                                           t.kind == 1, NCHW_OUT>),
+                       dim3(a.n_works), dim3(t.pw * t.cw * 64), 0, stream, a);
 }
 
 template <bool BF16, bool NCHW_OUT, int CFG = 0>
@@ -427,12 +722,279 @@ hipError_t launch_phase_gemm(const GemmArgs& a, int dtype, int cfg, bool nchw_ou
 }
 
 // ---------------------------------------------------------------------------
-// Weight packing: wp[slot][k][c] = w at kernel tap slot = (kh, kw).
+// Transposed conv with few output channels (c_out * r * s <= 64), NCHW.
+// The phase GEMM has N = c_out there, so its tiles are mostly padding and
+// every input pixel is fetched once per (phase, tap).  This kernel instead
+// keeps a block of input rows (full width, plus the halo its outputs need) in
+// LDS, computes for every pixel of the block the products with all kernel
+// taps at once on MFMA, Z[p][tap * c_out + k] = sum_c x[c][p] * w[c][k][tap]
+// (section 3.2.1's per-tap 1x1 convolutions, all taps in one GEMM), and then
+// forms each owned output as the sum of the Z entries of the input pixels and
+// taps that reach it (the interleaved scatter of section 3.1, read side).
+// Workgroup (image, block of OB output rows).  Input tile: rows [i_lo, i_hi],
+// columns [j_lo, j_hi] of the input, zero outside it; LDS column of input
+// column j is j + ZOFF (a multiple of the 16-byte vector).
+__device__ __forceinline__ int floor_div_d(int a, int b) { return a >= 0 ? a / b : -((-a + b - 1) / b); }
+
+template <bool BF16>
+__global__ __launch_bounds__(kZtileThreads) void ztile_kernel(ZArgs a) {
+  using T = typename std::conditional<BF16, uint16_t, uint32_t>::type;
+  constexpr int ESZ = sizeof(T);
+  constexpr int VE = 16 / ESZ;
+  constexpr int PASS = BF16 ? 64 : 32;  // input channels per MFMA pass
+  constexpr int KSTEP = BF16 ? 16 : 2;  // K per MFMA
+  constexpr int NKS = PASS / KSTEP;
+  constexpr int NT = kZtileThreads, NW = NT / 64;
+  constexpr int NLD = 12;               // 16-byte input loads per thread in flight
+  constexpr int MB_MAX = ((kZtileMaxPixels + 31) / 32 + NW - 1) / NW;  // M blocks per wave
+  __shared__ __attribute__((aligned(16))) char zsm[kZtileLds];
+  T* tile = (T*)zsm;        // [cin_pad][cpitch]: per channel tr rows of tcp
+  float* zs = (float*)zsm;  // [p][kZtileZPitch], after the GEMM
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int img = blockIdx.y, o0 = blockIdx.x * a.ob, o1 = min(o0 + a.ob, a.ho);
+  const int i_lo = -floor_div_d(-(o0 + a.pad_h - (a.r - 1) * a.dil_h), a.stride_h);
+  const int np = a.tr * a.tcw;
+  const int mblocks = (np + 31) / 32;
+  const int kx = a.r * a.s * a.cout;
+  const int plane = a.cpitch;  // elements per input channel (>= tr * tcp)
+
+  // weight fragments of one pass: column col = nb*32 + lane%32 = tap*cout + k
+  auto load_w = [&](int c0, uint4 (&bfr)[NKS][2], float (&bf32)[NKS][2]) {
+#pragma unroll
+    for (int t = 0; t < NKS; ++t)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        const int col = nb * 32 + (lane & 31);
+        const int tap = col / a.cout, k = col - tap * a.cout;
+        const int c = c0 + t * KSTEP + (lane >> 5) * (KSTEP / 2);
+        const bool ok = col < kx && c < a.cin_pad;
+        const size_t widx = ((size_t)tap * a.cout_pad + k) * a.cin_pad + c;
+        if constexpr (BF16)
+          bfr[t][nb] = ok ? *(const uint4*)((const T*)a.wp + widx) : make_uint4(0, 0, 0, 0);
+        else
+          bf32[t][nb] = ok ? ((const float*)a.wp)[widx] : 0.f;
+      }
+  };
+  uint4 bfr[NKS][2];
+  float bf32[NKS][2];
+  load_w(0, bfr, bf32);
+  // tap tables and bias for the final combine (read here, long before use;
+  // the barrier after the input loads publishes them)
+  __shared__ int8_t s_tap[3][2][kZtileMaxStride][kZtileMaxTaps];
+  __shared__ int8_t s_tapn[2][kZtileMaxStride];
+  __shared__ float s_zb[64];
+  if (tid < 64) s_zb[tid] = (a.bias && tid < a.cout) ? a.bias[tid] : 0.f;
+  for (int e = tid; e < 2 * kZtileMaxStride * kZtileMaxTaps; e += NT) {
+    const int ax = e / (kZtileMaxStride * kZtileMaxTaps), rem = e % (kZtileMaxStride * kZtileMaxTaps);
+    const int rho = rem / kZtileMaxTaps, t = rem % kZtileMaxTaps;
+    s_tap[0][ax][rho][t] = a.tap_k[ax][rho][t];
+    s_tap[1][ax][rho][t] = a.tap_d[ax][rho][t];
+    if (t == 0) s_tapn[ax][rho] = a.tap_n[ax][rho];
+  }
+
+  // zero the halo columns of every tile row (LDS columns outside the input)
+  const int nrows = a.cin_pad * a.tr;
+  const int right = a.tcp - kZtileColOff - a.w;  // elements, a multiple of VE
+  for (int rr = tid; rr < nrows; rr += NT) {
+    const int cc = rr / a.tr;
+    T* row = tile + cc * plane + (rr - cc * a.tr) * a.tcp;
+    *(uint4*)row = make_uint4(0, 0, 0, 0);  // kZtileColOff == VE (bf16) or 2 VE (fp32)
+    if (kZtileColOff > VE) *(uint4*)(row + VE) = make_uint4(0, 0, 0, 0);
+    for (int c = 0; c < right; c += VE)
+      *(uint4*)(row + kZtileColOff + a.w + c) = make_uint4(0, 0, 0, 0);
+  }
+  // every input row of the tile, all channels: 16-byte pieces, zero outside
+  const int vec_per_row = a.w / VE;
+  const int total_vec = nrows * vec_per_row;
+  for (int e0 = 0; e0 < total_vec; e0 += NT * NLD) {
+    uint4 val[NLD];
+#pragma unroll
+    for (int l = 0; l < NLD; ++l) {
+      const int e = e0 + tid + NT * l;
+      const int rr = e / vec_per_row, v = e - rr * vec_per_row;
+      const int cc = rr / a.tr, tr = rr - cc * a.tr;
+      const int i = i_lo + tr;
+      val[l] = make_uint4(0, 0, 0, 0);
+      if (e < total_vec && cc < a.cin && i >= 0 && i < a.h)
+        val[l] = *(const uint4*)((const T*)a.x + (((size_t)img * a.cin + cc) * a.h + i) * a.w + v * VE);
+    }
+#pragma unroll
+    for (int l = 0; l < NLD; ++l) {
+      const int e = e0 + tid + NT * l;
+      if (e < total_vec) {
+        const int rr = e / vec_per_row, v = e - rr * vec_per_row;
+        const int cc = rr / a.tr, tr = rr - cc * a.tr;
+        *(uint4*)(tile + cc * plane + tr * a.tcp + kZtileColOff + v * VE) = val[l];
+      }
+    }
+  }
+  __syncthreads();
+
+  f32x16 acc[MB_MAX][2];
+#pragma unroll
+  for (int i = 0; i < MB_MAX; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
+  // pixel (tile row, column) of each of this wave's M-block rows
+  int src_off[MB_MAX];
+#pragma unroll
+  for (int mi = 0; mi < MB_MAX; ++mi) {
+    const int p = min((wave + NW * mi) * 32 + (lane & 31), np - 1);
+    const int tr = p / a.tcw, tc = p - tr * a.tcw;
+    src_off[mi] = tr * a.tcp + tc + a.j_lo + kZtileColOff;
+  }
+  // Z = X^T W over all input channels, one pass of PASS channels at a time;
+  // the next pass's weights load while this one computes
+  for (int c0 = 0; c0 < a.cin_pad; c0 += PASS) {
+    uint4 nbfr[NKS][2];
+    float nbf32[NKS][2];
+    if (c0 + PASS < a.cin_pad) load_w(c0 + PASS, nbfr, nbf32);
+#pragma unroll
+    for (int mi = 0; mi < MB_MAX; ++mi) {
+      if (wave + NW * mi >= mblocks) break;
+      const T* src = tile + src_off[mi];
+#pragma unroll
+      for (int t = 0; t < NKS; ++t) {
+        const int cc = c0 + t * KSTEP + (lane >> 5) * (KSTEP / 2);
+        if constexpr (BF16) {
+          uint32_t wv[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            wv[e] = (uint32_t)src[(cc + 2 * e) * plane] |
+                    ((uint32_t)src[(cc + 2 * e + 1) * plane] << 16);
+          const bf16x8 av = __builtin_bit_cast(bf16x8, make_uint4(wv[0], wv[1], wv[2], wv[3]));
+#pragma unroll
+          for (int nb = 0; nb < 2; ++nb)
+            acc[mi][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                av, __builtin_bit_cast(bf16x8, bfr[t][nb]), acc[mi][nb], 0, 0, 0);
+        } else {
+          const float av = __uint_as_float(src[cc * plane]);
+#pragma unroll
+          for (int nb = 0; nb < 2; ++nb)
+            acc[mi][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bf32[t][nb], acc[mi][nb], 0, 0, 0);
+        }
+      }
+    }
+    if (c0 + PASS < a.cin_pad) {
+#pragma unroll
+      for (int t = 0; t < NKS; ++t)
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+          bfr[t][nb] = nbfr[t][nb];
+          bf32[t][nb] = nbf32[t][nb];
+        }
+    }
+  }
+  __syncthreads();
+  // Z to LDS: lane holds column lane%32 of rows 8*(q/4) + 4*(lane/32) + q%4
+#pragma unroll
+  for (int mi = 0; mi < MB_MAX; ++mi) {
+    const int mb = wave + NW * mi;
+    if (mb >= mblocks) break;
+    // rows past np land in the unused part of the LDS buffer (mblocks * 32
+    // rows of Z fit: kZtileMaxPixels rounded up to 32 is within kZtileLds)
+    float* zr = zs + (mb * 32 + 4 * (lane >> 5)) * kZtileZPitch + (lane & 31);
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int q = 0; q < 16; ++q)
+        zr[(8 * (q >> 2) + (q & 3)) * kZtileZPitch + nb * 32] = acc[mi][nb][q];
+  }
+  __syncthreads();
+  // Owned outputs: rows [o0, o1), all columns, all channels.  Output row oh
+  // with u = oh + pad = s*Q + rho takes the taps of phase rho, reading input
+  // row Q + delta (the host's per-phase tap tables, staged in LDS).  Each
+  // wave takes whole output rows, all channels; lane l takes columns
+  // ow = l, l + 64, ...  The column part of every Z address depends only on
+  // ow, so it is computed once per lane; the row part once per row.
+  constexpr int PT = kZtilePhaseTaps;
+  constexpr int OWL = 4;  // columns per lane held in registers (wo <= 256)
+  int wpart[OWL][PT], ntw[OWL];
+#pragma unroll
+  for (int c = 0; c < OWL; ++c) {
+    const int ow = lane + 64 * c;
+    const int uw = ow + a.pad_w, qw = uw / a.stride_w, rw = uw - qw * a.stride_w;
+    ntw[c] = ow < a.wo ? s_tapn[1][rw] : 0;
+#pragma unroll
+    for (int tw = 0; tw < PT; ++tw)
+      wpart[c][tw] = (qw + s_tap[1][1][rw][tw] - a.j_lo) * kZtileZPitch + s_tap[0][1][rw][tw] * a.cout;
+  }
+  const int rows = o1 - o0;
+  const int zmax = np * kZtileZPitch - 1;
+  for (int orow = wave; orow < rows; orow += NW) {
+    const int oh = o0 + orow;
+    const int uh = oh + a.pad_h, qh = uh / a.stride_h, rh = uh - qh * a.stride_h;
+    const int nth = s_tapn[0][rh];
+    int hpart[PT];
+#pragma unroll
+    for (int th = 0; th < PT; ++th)
+      hpart[th] = (qh + s_tap[1][0][rh][th] - i_lo) * a.tcw * kZtileZPitch +
+                  s_tap[0][0][rh][th] * a.s * a.cout;
+#pragma unroll
+    for (int c = 0; c < OWL; ++c) {
+      if (64 * c >= a.wo) break;
+      const int ow = lane + 64 * c;
+      // every tap pair up to the largest counts is read (addresses clamped
+      // into Z) and the pairs this phase lacks are selected away, so that
+      // the reads issue together instead of behind one branch each
+      int addr[PT][PT];
+      bool use[PT][PT];
+#pragma unroll
+      for (int th = 0; th < PT; ++th)
+#pragma unroll
+        for (int tw = 0; tw < PT; ++tw) {
+          addr[th][tw] = min(max(hpart[th] + wpart[c][tw], 0), zmax - a.cout + 1);
+          use[th][tw] = th < nth && tw < ntw[c];
+        }
+      size_t off = (((size_t)img * a.cout) * a.ho + oh) * a.wo + ow;
+      for (int k = 0; k < a.cout; ++k, off += (size_t)a.ho * a.wo) {
+        float v = s_zb[k];
+#pragma unroll
+        for (int th = 0; th < PT; ++th) {
+          if (th >= a.max_th) break;
+#pragma unroll
+          for (int tw = 0; tw < PT; ++tw) {
+            if (tw >= a.max_tw) break;
+            const float z = zs[addr[th][tw] + k];
+            v += use[th][tw] ? z : 0.f;
+          }
+        }
+        if (ow < a.wo) {
+          if constexpr (BF16)
+            ((uint16_t*)a.y)[off] = f32_to_bf16_rne(v);
+          else
+            ((float*)a.y)[off] = v;
+        }
+      }
+    }
+  }
+}
+
+hipError_t launch_ztile(const ZArgs& a, int dtype, hipStream_t stream) {
+  const dim3 grid((a.ho + a.ob - 1) / a.ob, a.n);
+  if (dtype == 1)
+    hipLaunchKernelGGL(ztile_kernel<true>, grid, dim3(kZtileThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(ztile_kernel<false>, grid, dim3(kZtileThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Weight packing: element (slot, k, c) = w at kernel tap slot = (kh, kw),
+// output channel k, input channel c.
+//   lane_kb = 0: K-contiguous rows, wp[slot][k][c].
+//   lane_kb = KB: the lane order of the split-wave GEMM's own-operand loads
+//     for KB-byte stages: per (slot, 32-channel block, K stage) a block of
+//     32 rows x KB bytes stored as [chunk c16 < KB/32][lane < 64][16 bytes],
+//     lane = 32 * (byte / (KB/2)) + row, so that one 16-byte load per lane
+//     reads 1 KB contiguous.
 
 template <typename T>
 __global__ void pack_weights_kernel(const T* __restrict__ w, T* __restrict__ wp, bool transposed,
                                     int cin, int cout, int r, int s, int cin_pad, int cout_pad,
-                                    long long total) {
+                                    int lane_kb, long long total) {
   for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
        idx += (long long)gridDim.x * blockDim.x) {
     const int c = (int)(idx % cin_pad);
@@ -446,12 +1008,22 @@ __global__ void pack_weights_kernel(const T* __restrict__ w, T* __restrict__ wp,
                                        : (((long long)k * cin + c) * r + kh) * s + kw;
       v = w[src];
     }
-    wp[idx] = v;
+    long long dst = idx;
+    if (lane_kb > 0) {
+      const int kc = lane_kb / (int)sizeof(T);          // K elements per stage
+      const int e = (c % kc) * (int)sizeof(T);          // byte within the stage row
+      const int h = e / (lane_kb / 2), c16 = (e % (lane_kb / 2)) / 16, bo = e % 16;
+      const long long blk = (long long)slot * (cout_pad / 32) + k / 32;
+      const long long byte = ((blk * (cin_pad / kc) + c / kc) * (lane_kb / 32) + c16) * 1024 +
+                             (h * 32 + k % 32) * 16 + bo;
+      dst = byte / (long long)sizeof(T);
+    }
+    wp[dst] = v;
   }
 }
 
 hipError_t launch_pack_weights(const void* w, void* wp, int dtype, bool transposed, int cin,
-                               int cout, int r, int s, int cin_pad, int cout_pad,
+                               int cout, int r, int s, int cin_pad, int cout_pad, int lane_kb,
                                hipStream_t stream) {
   const long long total = (long long)r * s * cout_pad * cin_pad;
   const int block = 256;
@@ -461,11 +1033,11 @@ hipError_t launch_pack_weights(const void* w, void* wp, int dtype, bool transpos
   if (dtype == 1)
     hipLaunchKernelGGL(pack_weights_kernel<uint16_t>, dim3(grid), dim3(block), 0, stream,
                        (const uint16_t*)w, (uint16_t*)wp, transposed, cin, cout, r, s, cin_pad,
-                       cout_pad, total);
+                       cout_pad, lane_kb, total);
   else
     hipLaunchKernelGGL(pack_weights_kernel<uint32_t>, dim3(grid), dim3(block), 0, stream,
                        (const uint32_t*)w, (uint32_t*)wp, transposed, cin, cout, r, s, cin_pad,
-                       cout_pad, total);
+                       cout_pad, lane_kb, total);
   return hipGetLastError();
 }
 

@@ -77,26 +77,40 @@ struct GemmArgs {
 // wg_per_cu: workgroups of this shape that fit on one compute unit at once
 // (the tighter of the register and LDS limits; the same for both dtypes and
 // layouts), used by the host's schedule model.
+// kind 0: both operands through LDS, PW x CW waves of (BM/PW) x (BN/CW).
+// kind 1: split-wave form, the pixel tile through LDS, CW waves each loading
+//         BN/CW weight rows itself (PW = 1) from lane-ordered packed weights.
+// kind 2: split-wave form, the weight tile through LDS, PW waves each loading
+//         BM/PW pixel rows itself (CW = 1).
 struct TileShape {
-  int bm, bn, pw, cw, kb, depth, wg_per_cu;
+  int bm, bn, pw, cw, kb, depth, wg_per_cu, kind;
 };
 constexpr TileShape kTiles[] = {
-    {128, 128, 2, 2, 128, 2, 2},  // 0
-    {256, 32, 4, 1, 128, 2, 1},   // 1  narrow: few output channels
-    {64, 128, 1, 4, 128, 2, 2},   // 2
-    {256, 128, 2, 2, 128, 2, 1},  // 3
-    {128, 256, 2, 2, 128, 2, 1},  // 4
-    {256, 256, 2, 4, 128, 2, 1},  // 5  8 waves
-    {256, 128, 4, 2, 128, 2, 1},  // 6  8 waves
-    {128, 256, 2, 4, 128, 2, 1},  // 7  8 waves
-    {128, 128, 4, 2, 128, 2, 2},  // 8  8 waves
-    {256, 256, 2, 2, 128, 1, 1},  // 9  4 waves of 128 x 128
-    {128, 32, 4, 1, 64, 2, 6},    // 10 narrow, small LDS footprint
-    {256, 32, 4, 1, 64, 2, 3},    // 11 narrow, small LDS footprint
-    {64, 128, 1, 4, 64, 2, 5},    // 12 small LDS footprint
-    {128, 128, 2, 2, 64, 2, 3},   // 13 small LDS footprint
-    {256, 128, 2, 2, 128, 1, 1},  // 14 4 waves of 128 x 64, one buffer
-    {128, 256, 2, 2, 128, 1, 1},  // 15 4 waves of 64 x 128, one buffer
+    {128, 128, 2, 2, 128, 2, 2, 0},  // 0
+    {256, 32, 4, 1, 128, 2, 1, 0},   // 1  narrow: few output channels
+    {64, 128, 1, 4, 128, 2, 2, 0},   // 2
+    {256, 128, 2, 2, 128, 2, 1, 0},  // 3
+    {128, 256, 2, 2, 128, 2, 1, 0},  // 4
+    {256, 256, 2, 4, 128, 2, 1, 0},  // 5  8 waves
+    {256, 128, 4, 2, 128, 2, 1, 0},  // 6  8 waves
+    {128, 256, 2, 4, 128, 2, 1, 0},  // 7  8 waves
+    {128, 128, 4, 2, 128, 2, 2, 0},  // 8  8 waves
+    {256, 256, 2, 2, 128, 1, 1, 0},  // 9  4 waves of 128 x 128
+    {128, 32, 4, 1, 64, 2, 6, 0},    // 10 narrow, small LDS footprint
+    {256, 32, 4, 1, 64, 2, 3, 0},    // 11 narrow, small LDS footprint
+    {64, 128, 1, 4, 64, 2, 5, 0},    // 12 small LDS footprint
+    {128, 128, 2, 2, 64, 2, 3, 0},   // 13 small LDS footprint
+    {256, 128, 2, 2, 128, 1, 1, 0},  // 14 4 waves of 128 x 64, one buffer
+    {128, 256, 2, 2, 128, 1, 1, 0},  // 15 4 waves of 64 x 128, one buffer
+    {256, 128, 4, 1, 128, 3, 1, 2},  // 16 split-wave: 4 waves of 64 pixels x 128
+    {64, 128, 1, 4, 128, 4, 3, 1},   // 17 split-wave: 4 waves of 64 x 32 channels
+    {128, 128, 4, 1, 128, 3, 2, 2},  // 18 split-wave: 4 waves of 32 pixels x 128
+    {128, 128, 1, 4, 128, 3, 2, 1},  // 19 split-wave: 4 waves of 128 x 32 channels
+    {256, 64, 4, 1, 128, 3, 2, 2},   // 20 split-wave: 4 waves of 64 pixels x 64
+    {256, 128, 8, 1, 128, 2, 2, 2},  // 21 split-wave: 8 waves of 32 pixels x 128
+    {128, 256, 1, 4, 128, 3, 1, 1},  // 22 split-wave: 4 waves of 128 x 64 channels
+    {64, 256, 1, 4, 128, 3, 2, 1},   // 23 split-wave: 4 waves of 64 x 64 channels
+    {32, 256, 1, 4, 128, 4, 2, 1},   // 24 split-wave: 4 waves of 32 x 64 channels
 };
 constexpr int kComputeUnits = 256;  // MI355X
 constexpr int TILE_COUNT = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
@@ -104,19 +118,63 @@ inline int tile_bm(int cfg) { return kTiles[cfg].bm; }
 inline int tile_bn(int cfg) { return kTiles[cfg].bn; }
 inline int tile_threads(int cfg) { return kTiles[cfg].pw * kTiles[cfg].cw * 64; }
 inline int tile_kb(int cfg) { return kTiles[cfg].kb; }
-// LDS bytes of a configuration (two stages of BM + BN rows, 16-byte row pad)
-inline int tile_lds(int cfg) { return 2 * (kTiles[cfg].bm + kTiles[cfg].bn) * (kTiles[cfg].kb + 16); }
+// LDS bytes of a configuration (two stages of the rows that go through LDS,
+// 16-byte row pad)
+inline int tile_lds(int cfg) {
+  const TileShape& t = kTiles[cfg];
+  const int rows = t.kind == 0 ? t.bm + t.bn : (t.kind == 1 ? t.bm : t.bn);
+  return 2 * rows * (t.kb + 16);
+}
 constexpr int kMaxBlockK_bytes = 128;  // largest K block per stage: 64 bf16 or 32 fp32
 
 // dtype: 0 fp32, 1 bf16; nchw_out selects the output layout.
 hipError_t launch_phase_gemm(const GemmArgs& a, int dtype, int cfg, bool nchw_out,
                              hipStream_t stream);
 
-// Gather w into [slot = kh*s + kw][cout_pad][cin_pad] (zero padded).
+// Gather w into [slot = kh*s + kw][cout_pad][cin_pad] (zero padded), in the
+// layout the tile kind reads.
 // transposed: w is [cin][cout][r][s]; otherwise [cout][cin][r][s].
+// lane_kb: 0 for the K-contiguous layout; the stage size KB of a kind-1 tile
+// for its lane-ordered layout (see pack_weights_kernel).
 hipError_t launch_pack_weights(const void* w, void* wp, int dtype, bool transposed, int cin,
-                               int cout, int r, int s, int cin_pad, int cout_pad,
+                               int cout, int r, int s, int cin_pad, int cout_pad, int lane_kb,
                                hipStream_t stream);
+
+// All-taps form of a transposed conv with few output channels (NCHW,
+// c_out * r * s <= 64): workgroup (image, block of `ob` output rows) holds
+// input rows [i_lo, i_lo + tr) (i_lo from the block's first output row) and
+// input columns [j_lo, j_lo + tcw) of all (padded) input channels in LDS,
+// column j at LDS column j + kZtileColOff of a row of tcp elements; Z (tile
+// pixels x 64 fp32) then reuses the same LDS.
+constexpr int kZtileZPitch = 65;      // Z row pitch, floats
+constexpr int kZtileColOff = 8;       // LDS column of input column 0
+constexpr int kZtileMaxPixels = 384;  // tile pixels (tr * tcw)
+constexpr int kZtileLds = 128 * 1024; // input tile (all channels), then Z
+constexpr int kZtileMaxStride = 4;    // phases per axis of the tap tables
+constexpr int kZtileMaxTaps = 8;      // kernel taps per axis
+constexpr int kZtilePhaseTaps = 4;    // taps per axis reaching one output phase
+constexpr int kZtileThreads = 512;    // 8 waves: two per SIMD hide each other's latency
+struct ZArgs {
+  const void* x;
+  const void* wp;  // packed K-contiguous weights [slot][cout_pad][cin_pad]
+  const float* bias;
+  void* y;
+  int n, cin, h, w, cout, r, s, cin_pad, cout_pad;
+  int stride_h, stride_w, pad_h, pad_w, dil_h, dil_w, ho, wo;
+  int ob;            // output rows per workgroup
+  int tr, tcw, tcp;  // tile rows, tile columns, LDS row pitch (elements)
+  int cpitch;        // LDS elements per input channel (>= tr * tcp)
+  int j_lo;          // first tile column (input coordinate)
+  int cchunk;        // K padding unit of the packed weights (channels)
+  // per axis (0 = h, 1 = w) and phase rho = (o + pad) mod stride: the taps
+  // k with (rho - k*dil) divisible by the stride, and delta = (rho - k*dil) /
+  // stride, so that output o reads input (o + pad) div stride + delta
+  int8_t tap_n[2][kZtileMaxStride];
+  int max_th, max_tw;  // largest tap count of a phase, per axis
+  int8_t tap_k[2][kZtileMaxStride][kZtileMaxTaps];
+  int8_t tap_d[2][kZtileMaxStride][kZtileMaxTaps];
+};
+hipError_t launch_ztile(const ZArgs& a, int dtype, hipStream_t stream);
 
 // Re-layout the input into [n][h*w][c_stride] with zero channel padding.
 // nchw: source is NCHW; otherwise NHWC with cin channels per pixel.

@@ -20,6 +20,18 @@ from paper_1907_11210_amd import workloads as wl
 TOL = {"f32": 1e-4, "bf16": 2e-2}
 
 
+def tile_count():
+    """Number of GEMM tile configurations (entries of kTiles in kernels.hpp)."""
+    import os
+    import re
+    src = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                       "paper_1907_11210_amd", "csrc", "kernels.hpp")
+    text = open(src).read()
+    body = text[text.index("kTiles[] = {"):]
+    body = body[:body.index("};")]
+    return len(re.findall(r"\{\s*\d+\s*,", body))
+
+
 def say(*a):
     print(*a, flush=True)
     sys.stdout.flush()

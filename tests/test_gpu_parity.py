@@ -46,6 +46,12 @@ SMALL = [
     L("conv_1x1", False, 1, 64, 5, 5, 64, 1, 1, 1, 0, 0, 1, "NHWC", "bf16"),
     L("ct_vecstage_bf16", True, 2, 72, 4, 6, 40, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
     L("ct_vecstage_f32", True, 2, 70, 3, 4, 24, 3, 3, 2, 1, 1, 1, "NCHW", "f32"),
+    # few output channels, NCHW: the all-taps form
+    L("ct_fewout_bf16", True, 2, 40, 6, 16, 3, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
+    L("ct_fewout_f32_op", True, 2, 24, 5, 8, 2, 3, 3, 2, 1, 1, 1, "NCHW", "f32"),
+    L("ct_fewout_s3d2", True, 1, 16, 7, 8, 4, 3, 3, 3, 2, 1, 2, "NCHW", "bf16"),
+    L("ct_fewout_tall", True, 3, 130, 37, 8, 1, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
+    L("ct_fewout_wide", True, 1, 8, 3, 64, 2, 5, 5, 2, 2, 1, 1, "NCHW", "f32"),
 ]
 
 
@@ -203,7 +209,7 @@ def test_workload_full_size_sampled(wname):
         assert np.all(np.isfinite(y))
 
 
-TILE_CONFIGS = list(range(16))  # every GEMM tile configuration of the kernel
+TILE_CONFIGS = list(range(P.tile_count()))  # every GEMM tile configuration
 
 
 @pytest.mark.parametrize("tile", TILE_CONFIGS)
@@ -259,3 +265,51 @@ def test_border_class_forms(split, monkeypatch):
         absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
         y = P.run_gpu(layer, xq, wq, bias)
         P.check(y, ref, absref, layer.dtype, "%s split %d" % (layer.name, split))
+
+
+def test_plan_execute_in_hip_graph():
+    """A plan's launches captured in a HIP graph reproduce the eager result on
+    every replay, with other eager work on the device between replays."""
+    dev = torch.device("cuda", 0)
+    layer = SMALL[2]  # NCHW bf16: staging kernel + GEMM
+    P.say("case graph", layer)
+    xq, wq = _inputs(layer, seed=3)
+    x_dev = wl.to_layout(xq, layer.layout).to(dev)
+    bias = torch.linspace(-1.0, 1.0, layer.c_out).to(dev)
+    plan = P.make_plan(layer, wq.contiguous().to(dev))
+    y_eager = torch.empty(plan.out_shape, dtype=xq.dtype, device=dev)
+    plan(x_dev, bias=bias, out=y_eager)
+    y = torch.empty_like(y_eager)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        plan(x_dev, bias=bias, out=y)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        plan(x_dev, bias=bias, out=y)
+    scratch = torch.empty(1 << 20, device=dev)
+    for k in range(4):
+        y.fill_(float("nan"))
+        scratch.normal_()  # unrelated eager work between replays
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y.view(torch.int16), y_eager.view(torch.int16)), "replay %d" % k
+    del g
+    plan.close()
+
+
+@pytest.mark.parametrize("ztile", [0, 1])
+def test_few_output_channel_forms(ztile, monkeypatch):
+    """Few-output-channel NCHW transposed convs through the all-taps form and,
+    with it switched off, through the phase GEMM: both match the oracle."""
+    monkeypatch.setenv("HUGE2_ZTILE", str(ztile))
+    for layer in [l for l in SMALL if l.name.startswith("ct_fewout")] + [SMALL[12]]:
+        P.say("case ztile", ztile, layer)
+        xq, wq = _inputs(layer, seed=70 + ztile)
+        bias = torch.linspace(-0.3, 0.6, layer.c_out)
+        ref = P.oracle_full(layer, xq, wq, bias)
+        absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
+        y = P.run_gpu(layer, xq, wq, bias)
+        P.check(y, ref, absref, layer.dtype, "%s ztile %d" % (layer.name, ztile))

@@ -76,10 +76,11 @@ long long count_works(const huge2_conv_desc& d, bool transposed, int class_split
 
 // Tile choice, from measurements on MI355X.  bf16: many pixels and at most
 // 128 output channels take the 8-wave 128 x 128 tile; 256 or more output
-// channels with enough 64-pixel tiles take the split-wave 64 x 256 tile
-// (ASPP); the rest the split-wave 64 x 128 tile (few pixels, long K: the
-// first DCGAN layer).  Few output channels take the narrow 128 x 32 tile.
-// fp32 keeps the two-operand-LDS tiles.
+// channels with plenty of 64-pixel tiles take the split-wave 64 x 256 tile
+// (ASPP); otherwise the split-wave tiles with two K groups per workgroup,
+// 128 x 128 when that still gives every CU a tile, else 64 x 128 (few
+// pixels and long K: the first DCGAN layers).  Few output channels take the
+// narrow 128 x 32 tile.  fp32 keeps the two-operand-LDS tiles.
 int choose_cfg(const huge2_conv_desc& d, bool transposed, int class_split) {
   int forced = env_int("HUGE2_TILE", -1);
   if (forced >= 0 && forced < TILE_COUNT) return forced;
@@ -87,8 +88,9 @@ int choose_cfg(const huge2_conv_desc& d, bool transposed, int class_split) {
   const bool large = count_works(d, transposed, class_split, 8) >= 512;
   if (d.dtype != HUGE2_BF16) return large ? 8 : 2;
   if (large && d.c_out <= 128) return 8;                            // 128 x 128, 8 waves
-  if (d.c_out >= 256 && count_works(d, transposed, class_split, 23) >= 256) return 23;
-  return 17;                                                        // 64 x 128 split-wave
+  if (d.c_out >= 256 && count_works(d, transposed, class_split, 23) >= 384) return 23;
+  if (count_works(d, transposed, class_split, 27) >= kComputeUnits) return 27;
+  return 25;                                                        // 64 x 128, 2 K groups
 }
 
 // Order the work list for the eight XCDs.  The kernel hands work index

@@ -171,7 +171,8 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
   constexpr uint32_t OOB = 0x80000000u;  // beyond every buffer: loads return 0
   __shared__ __attribute__((aligned(16))) char smem[2 * STAGE_B];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int work = xcd_remap(blockIdx.x, gridDim.x);
   const WorkDev wk = a.works[work];
   const SegDev sg = a.segs[wk.seg];
@@ -428,9 +429,10 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
 // form above, which is what bounds the MFMA rate at small wave tiles.
 // DEPTH register buffers hold the stages in flight; the loop is unrolled by
 // U = lcm(DEPTH, 2) so that every buffer index is a compile-time constant.
-template <bool BF16, int BM, int BN, int W, int KB, int DEPTH, bool SHARE_A, bool NCHW_OUT>
-__global__ __launch_bounds__(W * 64) void phase_gemm2_kernel(GemmArgs a) {
-  constexpr int NT = W * 64;
+template <bool BF16, int BM, int BN, int W, int KB, int DEPTH, bool SHARE_A, int KS, bool NCHW_OUT>
+__global__ __launch_bounds__(W * 64 * KS) void phase_gemm2_kernel(GemmArgs a) {
+  constexpr int NTA = W * 64 * KS;  // threads of the workgroup
+  constexpr int NT = W * 64;        // threads of one K group
   constexpr int ESZ = BF16 ? 2 : 4;
   constexpr int KC = KB / ESZ;    // K elements per stage
   constexpr int VE = 16 / ESZ;    // elements per 16-byte chunk
@@ -447,9 +449,20 @@ __global__ __launch_bounds__(W * 64) void phase_gemm2_kernel(GemmArgs a) {
   static_assert(DEPTH >= 2 && DEPTH <= 4, "two to four stages in flight");
   constexpr int STAGE_B = RS * ROWB;
   constexpr uint32_t OOB = 0x80000000u;
-  __shared__ __attribute__((aligned(16))) char smem[2 * STAGE_B];
+  // KS K groups of W waves each run the pipeline below on their own range of
+  // channel blocks, with their own LDS buffers; group 1 hands its partial sums
+  // to group 0 through LDS at the end (a fixed order: the result does not
+  // depend on timing).
+  constexpr int ACC_B = KS > 1 ? W * 64 * TP * TC * 16 * 4 : 0;
+  constexpr int SMEM_B = KS * 2 * STAGE_B > ACC_B ? KS * 2 * STAGE_B : ACC_B;
+  __shared__ __attribute__((aligned(16))) char smem_all[SMEM_B];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // wave indices are wave-uniform: keep them in scalar registers
+  const int wave_all = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int lane = threadIdx.x & 63, grp = KS > 1 ? wave_all / W : 0;
+  const int wave = wave_all - grp * W;                       // within the K group
+  const int tid = (int)threadIdx.x - grp * NT;
+  char* const smem = smem_all + grp * 2 * STAGE_B;
   const int half = lane >> 5, row32 = lane & 31;
   const int work = xcd_remap(blockIdx.x, gridDim.x);
   const WorkDev wk = a.works[work];
@@ -498,16 +511,19 @@ __global__ __launch_bounds__(W * 64) void phase_gemm2_kernel(GemmArgs a) {
 
   const int ntaps = sg.tap_count;
   const int cblocks = a.cin_pad / KC;
-  const int nsteps = ntaps * cblocks;
+  const int cb_per = (cblocks + KS - 1) / KS;                 // channel blocks per K group
+  const int cb_lo = min(grp * cb_per, cblocks);
+  const int nsteps = ntaps * (min(cb_lo + cb_per, cblocks) - cb_lo);  // this group's stages
+  const int nsteps_all = ntaps * cb_per;                      // the loop runs this many
   const int tail_c = a.cin - (cblocks - 1) * KC;
 
   __shared__ float s_bias[BN];
-  for (int t = tid; t < BN; t += NT)
+  for (int t = threadIdx.x; t < BN; t += NTA)
     s_bias[t] = (a.bias && wk.n0 + t < a.cout) ? a.bias[wk.n0 + t] : 0.f;
   __shared__ int4 s_taps[kMaxLdsTaps];
   const bool lds_taps = !sg.tap_ap && ntaps <= kMaxLdsTaps;
   if (lds_taps) {
-    for (int t = tid; t < ntaps; t += NT) {
+    for (int t = threadIdx.x; t < ntaps; t += NTA) {
       const TapDev tp = a.taps[sg.tap_begin + t];
       s_taps[t] = make_int4((tp.off_h * a.w + tp.off_w) * a.cin * ESZ,
                             (int)((uint32_t)tp.slot * (uint32_t)a.cout_pad * (uint32_t)a.cin_pad * ESZ),
@@ -522,7 +538,7 @@ __global__ __launch_bounds__(W * 64) void phase_gemm2_kernel(GemmArgs a) {
   };
   Regs rb[DEPTH];
 
-  int ld_tap = 0, ld_cb = 0, ld_th = 0, ld_tw = 0;
+  int ld_tap = 0, ld_cb = cb_lo, ld_th = 0, ld_tw = 0;
   const uint32_t slot_bytes = (uint32_t)a.cout_pad * (uint32_t)a.cin_pad * ESZ;
   auto load_step = [&](Regs& R, bool valid) {
     const __amdgpu_buffer_rsrc_t xs = valid ? xr : xr0;
@@ -666,7 +682,7 @@ __global__ __launch_bounds__(W * 64) void phase_gemm2_kernel(GemmArgs a) {
   // invariant at the top of step u of an unrolled block starting at stage s:
   // LDS buffer (u & 1) holds stage s+u, register buffer (u % DEPTH) holds its
   // own-operand chunks, and the next DEPTH-1 stages are in flight.
-  const int nsteps_u = (nsteps + U - 1) / U * U;
+  const int nsteps_u = (nsteps_all + U - 1) / U * U;
   if (nsteps_u > 0) {
 #pragma unroll
     for (int d = 0; d < DEPTH; ++d) load_step(rb[d], d < nsteps);
@@ -683,6 +699,26 @@ __global__ __launch_bounds__(W * 64) void phase_gemm2_kernel(GemmArgs a) {
     }
   }
 
+  if constexpr (KS > 1) {
+    // group 1's partial sums to LDS (lane-contiguous), group 0 adds them
+    float* red = (float*)smem_all + wave * (TP * TC * 16 * 64) + lane;
+    if (grp == 1) {
+#pragma unroll
+      for (int i = 0; i < TP; ++i)
+#pragma unroll
+        for (int j = 0; j < TC; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) red[((i * TC + j) * 16 + r) * 64] = acc[i][j][r];
+    }
+    __syncthreads();
+    if (grp != 0) return;
+#pragma unroll
+    for (int i = 0; i < TP; ++i)
+#pragma unroll
+      for (int j = 0; j < TC; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] += red[((i * TC + j) * 16 + r) * 64];
+  }
   const int pix0 = wk.m0 + (SHARE_A ? 0 : wave * RD);
   const int ch0 = wk.n0 + (SHARE_A ? wave * RD : 0);
   store_tile<BF16, NCHW_OUT, TP, TC>(a, sg, acc, pix0, ch0, lane, s_bias - wk.n0);
@@ -696,8 +732,8 @@ static void launch_one(const GemmArgs& a, hipStream_t stream) {
                        dim3(a.n_works), dim3(t.pw * t.cw * 64), 0, stream, a);
   else
     hipLaunchKernelGGL((phase_gemm2_kernel<BF16, t.bm, t.bn, t.pw * t.cw, t.kb, t.depth,
-                                           t.kind == 1, NCHW_OUT>),
-                       dim3(a.n_works), dim3(t.pw * t.cw * 64), 0, stream, a);
+                                           t.kind == 1, t.ksplit, NCHW_OUT>),
+                       dim3(a.n_works), dim3(t.pw * t.cw * t.ksplit * 64), 0, stream, a);
 }
 
 template <bool BF16, bool NCHW_OUT, int CFG = 0>
@@ -750,7 +786,8 @@ __global__ __launch_bounds__(kZtileThreads) void ztile_kernel(ZArgs a) {
   __shared__ __attribute__((aligned(16))) char zsm[kZtileLds];
   T* tile = (T*)zsm;        // [cin_pad][cpitch]: per channel tr rows of tcp
   float* zs = (float*)zsm;  // [p][kZtileZPitch], after the GEMM
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int img = blockIdx.y, o0 = blockIdx.x * a.ob, o1 = min(o0 + a.ob, a.ho);
   const int i_lo = -floor_div_d(-(o0 + a.pad_h - (a.r - 1) * a.dil_h), a.stride_h);
   const int np = a.tr * a.tcw;

@@ -82,8 +82,10 @@ struct GemmArgs {
 //         BN/CW weight rows itself (PW = 1) from lane-ordered packed weights.
 // kind 2: split-wave form, the weight tile through LDS, PW waves each loading
 //         BM/PW pixel rows itself (CW = 1).
+// ksplit (split-wave kinds): K groups of PW x CW waves per workgroup, each
+// over its own share of the input-channel blocks, summed in LDS at the end.
 struct TileShape {
-  int bm, bn, pw, cw, kb, depth, wg_per_cu, kind;
+  int bm, bn, pw, cw, kb, depth, wg_per_cu, kind, ksplit = 1;
 };
 constexpr TileShape kTiles[] = {
     {128, 128, 2, 2, 128, 2, 2, 0},  // 0
@@ -111,12 +113,17 @@ constexpr TileShape kTiles[] = {
     {128, 256, 1, 4, 128, 3, 1, 1},  // 22 split-wave: 4 waves of 128 x 64 channels
     {64, 256, 1, 4, 128, 3, 2, 1},   // 23 split-wave: 4 waves of 64 x 64 channels
     {32, 256, 1, 4, 128, 4, 2, 1},   // 24 split-wave: 4 waves of 32 x 64 channels
+    {64, 128, 1, 4, 128, 4, 1, 1, 2},   // 25 as 17, two K groups (8 waves)
+    {64, 256, 1, 4, 128, 3, 1, 1, 2},   // 26 as 23, two K groups
+    {128, 128, 1, 4, 128, 3, 1, 1, 2},  // 27 as 19, two K groups
 };
 constexpr int kComputeUnits = 256;  // MI355X
 constexpr int TILE_COUNT = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 inline int tile_bm(int cfg) { return kTiles[cfg].bm; }
 inline int tile_bn(int cfg) { return kTiles[cfg].bn; }
-inline int tile_threads(int cfg) { return kTiles[cfg].pw * kTiles[cfg].cw * 64; }
+inline int tile_threads(int cfg) {
+  return kTiles[cfg].pw * kTiles[cfg].cw * (kTiles[cfg].kind ? kTiles[cfg].ksplit : 1) * 64;
+}
 inline int tile_kb(int cfg) { return kTiles[cfg].kb; }
 // LDS bytes of a configuration (two stages of the rows that go through LDS,
 // 16-byte row pad)

@@ -16,8 +16,9 @@ does after checking a replay bitwise against the eager step).  Per-layer
 times come from a separate eager pass with HIP events around each kernel.
 
 Prints ONE JSON line.  Fields beyond the standard ones:
-  roofline      the dominant layer's GEMM kernel (the longest mean launch, timed
-                with HIP events on the launch stream around that kernel alone):
+  roofline      the dominant layer's main kernel (the longest mean launch in the
+                per-layer pass), timed over back-to-back launches of that kernel
+                alone between two HIP events on the launch stream:
                 algorithmic FLOP (or bytes, when its arithmetic intensity is below
                 the MI355X ridge) per launch / mean duration, vs the dense MFMA peak
                 of its dtype (or HBM bandwidth); traffic from the committed
@@ -112,7 +113,10 @@ def build_workload(name, dev):
             if events is not None:
                 events[3 * i + 2].record()
 
-    return items, plans, step, lambda: outs
+    def step_input(i):
+        return inputs[i] if (not chained or i == 0) else outs[i - 1]
+
+    return items, plans, step, lambda: outs, step_input
 
 
 def kernel_source_sha():
@@ -127,7 +131,7 @@ def kernel_source_sha():
 def measured_traffic(workload, layer_name):
     """HBM bytes per launch of the layer's GEMM kernel, from the committed
     rocprofv3 counter summary, if it was taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", "phase_gemm_%s_traffic.json" % workload)
+    path = os.path.join(ROOT, "profiles", "layer_kernels_%s_traffic.json" % workload)
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -189,9 +193,16 @@ def _counter_per_dispatch(path, counter):
     return out
 
 
+MAIN_KERNELS = ("phase_gemm_kernel", "phase_gemm2_kernel", "ztile_kernel")
+
+
+def _is_main(name):
+    return any(k + "<" in name or k + "(" in name for k in MAIN_KERNELS)
+
+
 def _layer_dispatches(per_dispatch, nl):
-    """Assign the GEMM dispatches, in launch order, to the workload's layers."""
-    ids = sorted(d for d, (name, _) in per_dispatch.items() if "phase_gemm_kernel" in name)
+    """Assign each layer's main-kernel dispatches (in launch order) to it."""
+    ids = sorted(d for d, (name, _) in per_dispatch.items() if _is_main(name))
     by_layer = [[] for _ in range(nl)]
     for k, d in enumerate(ids):
         by_layer[k % nl].append(d)
@@ -205,7 +216,8 @@ def summarize_profiles(d, workload):
     layers = wl.WORKLOADS[workload]
     nl = len(layers)
     cmds = ["cd /tmp && export TMPDIR=/tmp"] + [c.format(w=workload) for _, c in PROFILE_COMMANDS]
-    lines = ["# phase_gemm_kernel on workload `%s`: rocprofv3 kernel trace" % workload, "",
+    lines = ["# Main kernel of each layer (phase GEMM or all-taps form) on workload `%s`: "
+             "rocprofv3 kernel trace" % workload, "",
              "Kernel source sha256[:16]: `%s`" % kernel_source_sha(), "",
              "Commands (R = repository root, O = output directory):", "", "```"] + cmds + ["```", ""]
 
@@ -220,7 +232,7 @@ def summarize_profiles(d, workload):
     per = {int(r["Dispatch_Id"]): (r["Kernel_Name"], int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
            for r in trace}
     by_layer = _layer_dispatches(per, nl)
-    lines += ["", "## phase_gemm_kernel per layer (dispatches in launch order, layer = k mod %d)" % nl,
+    lines += ["", "## Main kernel per layer (dispatches in launch order, layer = k mod %d)" % nl,
               "", "| layer | dispatches | mean us | min us | kernel instance |", "|---|---|---|---|---|"]
     avg_us = {}
     for l, ids in zip(layers, by_layer):
@@ -244,7 +256,7 @@ def summarize_profiles(d, workload):
                    "copy_kernel": copy_name[:120], "copy_bytes": COPY_MIB << 20,
                    "scale_fetch": round(float(f_fetch), 4), "scale_write": round(float(f_write), 4),
                    "layers": {}}
-        lines += ["", "## HBM traffic of phase_gemm_kernel (FETCH_SIZE, WRITE_SIZE; KiB per dispatch)",
+        lines += ["", "## HBM traffic of each layer's main kernel (FETCH_SIZE, WRITE_SIZE; KiB per dispatch)",
                   "", "Calibration: a %d MiB elementwise copy reads FETCH_SIZE x %.4f and writes "
                   "WRITE_SIZE x %.4f of its known size." % (COPY_MIB, f_fetch, f_write), "",
                   "| layer | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled traffic MB | algorithmic MB |",
@@ -260,10 +272,10 @@ def summarize_profiles(d, workload):
                                          "traffic_bytes": int(round(tb)), "algorithmic_bytes": algo}
             lines.append("| %s | %.1f | %.1f | %.2f | %.2f |" % (l.name, fk, wk, tb / 1e6, algo / 1e6))
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
-    with open(os.path.join(ROOT, "profiles", "phase_gemm_%s.md" % workload), "w") as f:
+    with open(os.path.join(ROOT, "profiles", "layer_kernels_%s.md" % workload), "w") as f:
         f.write("\n".join(lines) + "\n")
     if traffic is not None:
-        with open(os.path.join(ROOT, "profiles", "phase_gemm_%s_traffic.json" % workload), "w") as f:
+        with open(os.path.join(ROOT, "profiles", "layer_kernels_%s_traffic.json" % workload), "w") as f:
             json.dump(traffic, f, indent=1)
             f.write("\n")
     print(json.dumps({"layer_mean_us": avg_us}))
@@ -350,7 +362,7 @@ def main():
     if args.copy_calibration:
         copy_calibration(dev)
         return
-    items, plans, step, step_outputs = build_workload(args.workload, dev)
+    items, plans, step, step_outputs, step_input = build_workload(args.workload, dev)
     flops = layer_flops(plans)
     issued = [2 * p.macs()[1] for p in plans]
     total_flops = sum(flops)
@@ -427,7 +439,7 @@ def main():
         algo_bytes.append(nbytes)
         t = (stage_ms[i] + gemm_ms[i]) * 1e-3
         layers.append({
-            "layer": layer.name, "ms": round(stage_ms[i] + gemm_ms[i], 5),
+            "layer": layer.name, "kernel": p.kernel, "ms": round(stage_ms[i] + gemm_ms[i], 5),
             "gemm_ms": round(gemm_ms[i], 5), "stage_ms": round(stage_ms[i], 5),
             "eff_tflops": round(flops[i] / t / 1e12, 2),
             "gemm_eff_tflops": round(flops[i] / (gemm_ms[i] * 1e-3) / 1e12, 2),
@@ -436,7 +448,21 @@ def main():
             "algorithmic_mb": round(nbytes / 1e6, 2),
         })
     dom = int(np.argmax(gemm_ms))
-    dom_t = gemm_ms[dom] * 1e-3
+    # The dominant layer's main kernel alone: its input staged once, then
+    # `steps` back-to-back launches between two events on the launch stream
+    # (the same input every time), so that per-launch event overhead does
+    # not enter the mean launch duration.
+    x_dom = step_input(dom)
+    plans[dom].stage(x_dom)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        plans[dom].gemm(x_dom, step_outputs()[dom])
+    e1.record()
+    torch.cuda.synchronize()
+    dom_ms = e0.elapsed_time(e1) / args.steps
+    dom_t = dom_ms * 1e-3
     intensity = flops[dom] / algo_bytes[dom]
     ridge = PEAK[dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
     if intensity >= ridge:
@@ -450,8 +476,8 @@ def main():
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
         per_launch = {"algorithmic_bytes_per_launch": algo_bytes[dom]}
     roofline["traffic"] = measured_traffic(args.workload, items[dom][0].name)
-    roofline.update({"kernel": "phase_gemm_kernel (%s)" % items[dom][0].name,
-                     "mean_launch_ms": round(gemm_ms[dom], 5),
+    roofline.update({"kernel": "%s (%s)" % (plans[dom].kernel, items[dom][0].name),
+                     "mean_launch_ms": round(dom_ms, 5),
                      "arithmetic_intensity_flop_per_byte": round(intensity, 1)})
     roofline.update(per_launch)
     out = {

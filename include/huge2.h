@@ -130,6 +130,11 @@ huge2_status huge2_plan_run_gemm(const huge2_plan* plan, const void* x, const fl
  * (host only; -1 for a NULL plan). */
 int32_t huge2_plan_stages_input(const huge2_plan* plan);
 
+/* Name of the main kernel a plan launches and its tile shape, e.g.
+ * "phase_gemm2_kernel 64x128 w4 k2" (static storage owned by the plan,
+ * valid until huge2_plan_destroy; "" for a NULL plan).  Host only. */
+const char* huge2_plan_kernel(const huge2_plan* plan);
+
 /* Release a plan and its device buffers.  Waits for the device to finish
  * work that may still use them.  NULL is accepted.  Errors: HIP. */
 huge2_status huge2_plan_destroy(huge2_plan* plan);

@@ -10,5 +10,5 @@ from .huge2 import (  # noqa: F401
     Plan, conv2d_dilated, conv2d_transpose, huge2_conv2d_dilated, huge2_conv2d_transpose,
     huge2_output_shape, huge2_plan_create, huge2_plan_describe, huge2_plan_destroy,
     huge2_plan_execute, huge2_plan_macs, huge2_plan_run_gemm, huge2_plan_stage_input,
-    huge2_plan_stages_input, make_desc,
+    huge2_plan_kernel, huge2_plan_stages_input, make_desc,
 )

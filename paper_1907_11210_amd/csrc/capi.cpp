@@ -8,6 +8,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <new>
@@ -41,6 +42,7 @@ struct huge2_plan {
   int64_t nonzero_macs, issued_macs;
   bool ztile;   // all-taps form for few output channels (no GEMM work list)
   ZArgs zargs;  // its launch shape (pointers filled per call)
+  char kernel_name[64];
 };
 
 namespace {
@@ -357,6 +359,7 @@ huge2_status create_ztile(huge2_plan** out, const huge2_conv_desc& d, int transp
   p->issued_macs = issued;
   p->ztile = true;
   p->zargs = z;
+  std::snprintf(p->kernel_name, sizeof(p->kernel_name), "ztile_kernel ob%d", z.ob);
   huge2_status st = dev_alloc(p, &p->wp, p->wp_bytes);
   if (st != HUGE2_OK) {
     free_buffers(p);
@@ -408,6 +411,15 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   p->transposed = transposed;
   output_dims(d, tr, &p->ho, &p->wo);
   p->cfg = cfg;
+  {
+    const TileShape& t = kTiles[cfg];
+    if (t.kind == 0)
+      std::snprintf(p->kernel_name, sizeof(p->kernel_name), "phase_gemm_kernel %dx%d w%dx%d",
+                    t.bm, t.bn, t.pw, t.cw);
+    else
+      std::snprintf(p->kernel_name, sizeof(p->kernel_name), "phase_gemm2_kernel %dx%d w%d k%d",
+                    t.bm, t.bn, t.pw * t.cw, t.ksplit);
+  }
   const int esz = elem_size(d.dtype);
   const int vec = 16 / esz;
   const int bk = tile_kb(cfg) / esz;
@@ -710,6 +722,11 @@ huge2_status huge2_plan_run_gemm(const huge2_plan* plan, const void* x, const fl
   } catch (...) {
     return HUGE2_ERR_HIP;
   }
+}
+
+const char* huge2_plan_kernel(const huge2_plan* plan) {
+  if (!plan) return "";
+  return plan->kernel_name;
 }
 
 int32_t huge2_plan_stages_input(const huge2_plan* plan) {

@@ -24,6 +24,7 @@ HUGE2_NCHW, HUGE2_NHWC = 0, 1
 EXPORTED = (
     "huge2_status_str", "huge2_output_shape", "huge2_plan_create", "huge2_plan_execute",
     "huge2_plan_stage_input", "huge2_plan_run_gemm", "huge2_plan_stages_input",
+    "huge2_plan_kernel",
     "huge2_plan_destroy", "huge2_conv2d_transpose", "huge2_conv2d_dilated",
     "huge2_plan_describe", "huge2_plan_macs",
 )
@@ -75,6 +76,7 @@ def lib():
         L.huge2_plan_stage_input.argtypes = [vp, vp, vp]
         L.huge2_plan_run_gemm.argtypes = [vp, vp, vp, vp, vp]
         L.huge2_plan_stages_input.argtypes = [vp]
+        L.huge2_plan_kernel.argtypes = [vp]
         L.huge2_plan_destroy.argtypes = [vp]
         L.huge2_conv2d_transpose.argtypes = [dp, vp, vp, vp, vp, vp]
         L.huge2_conv2d_dilated.argtypes = [dp, vp, vp, vp, vp, vp]
@@ -83,6 +85,7 @@ def lib():
         L.huge2_plan_macs.argtypes = [dp, i32, i64p, i64p]
         for name in EXPORTED[1:]:
             getattr(L, name).restype = ctypes.c_int
+        L.huge2_plan_kernel.restype = ctypes.c_char_p
         _lib = L
     return _lib
 
@@ -147,6 +150,10 @@ def huge2_plan_run_gemm(plan, x_ptr, bias_ptr, y_ptr, stream=0):
 
 def huge2_plan_stages_input(plan):
     return int(lib().huge2_plan_stages_input(plan))
+
+
+def huge2_plan_kernel(plan):
+    return lib().huge2_plan_kernel(plan).decode()
 
 
 def huge2_plan_destroy(plan):
@@ -372,6 +379,11 @@ class Plan:
     @property
     def stages_input(self):
         return huge2_plan_stages_input(self._plan) == 1
+
+    @property
+    def kernel(self):
+        """Name and tile shape of the main kernel this plan launches."""
+        return huge2_plan_kernel(self._plan)
 
     def macs(self):
         return huge2_plan_macs(self.desc, self.transposed)

@@ -97,6 +97,7 @@ def test_null_and_aliased_pointers_rejected(L):
     assert L.huge2_plan_run_gemm(None, fake, None, ctypes.c_void_p(8192),
                                  None) == h2.HUGE2_ERR_INVALID_ARG
     assert L.huge2_plan_stages_input(None) == -1
+    assert h2.huge2_plan_kernel(None) == ""
     assert L.huge2_plan_destroy(None) == h2.HUGE2_OK
     assert L.huge2_plan_create(None, ctypes.byref(d), 1, fake, None) == h2.HUGE2_ERR_INVALID_ARG
     plan = ctypes.c_void_p()

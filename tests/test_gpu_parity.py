@@ -313,3 +313,16 @@ def test_few_output_channel_forms(ztile, monkeypatch):
         absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
         y = P.run_gpu(layer, xq, wq, bias)
         P.check(y, ref, absref, layer.dtype, "%s ztile %d" % (layer.name, ztile))
+
+
+def test_plan_reports_its_kernel():
+    """huge2_plan_kernel names the kernel family the planner chose."""
+    dev = torch.device("cuda", 0)
+    for layer, family in [(SMALL[23], "ztile_kernel"), (SMALL[1], "phase_gemm"),
+                          (SMALL[14], "phase_gemm")]:
+        P.say("case kernel name", layer)
+        wq = P.quantise(wl.random_weight(layer, seed=1, std=0.1), layer.dtype)
+        plan = P.make_plan(layer, wq.contiguous().to(dev))
+        name = plan.kernel
+        plan.close()
+        assert name.startswith(family), (layer.name, name)

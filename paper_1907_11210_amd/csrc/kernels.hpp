@@ -116,6 +116,10 @@ constexpr TileShape kTiles[] = {
     {64, 128, 1, 4, 128, 4, 1, 1, 2},   // 25 as 17, two K groups (8 waves)
     {64, 256, 1, 4, 128, 3, 1, 1, 2},   // 26 as 23, two K groups
     {128, 128, 1, 4, 128, 3, 1, 1, 2},  // 27 as 19, two K groups
+    {64, 128, 1, 4, 256, 3, 1, 1, 2},   // 28 as 25 with 256-byte K stages
+    {128, 128, 1, 4, 256, 2, 1, 1, 2},  // 29 as 27 with 256-byte K stages
+    {64, 256, 1, 4, 256, 2, 2, 1, 1},   // 30 as 23 with 256-byte K stages
+    {128, 128, 4, 2, 256, 2, 1, 0},     // 31 as 8 with 256-byte K stages
 };
 constexpr int kComputeUnits = 256;  // MI355X
 constexpr int TILE_COUNT = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
@@ -132,7 +136,7 @@ inline int tile_lds(int cfg) {
   const int rows = t.kind == 0 ? t.bm + t.bn : (t.kind == 1 ? t.bm : t.bn);
   return 2 * rows * (t.kb + 16);
 }
-constexpr int kMaxBlockK_bytes = 128;  // largest K block per stage: 64 bf16 or 32 fp32
+constexpr int kMaxBlockK_bytes = 256;  // largest K block per stage: 128 bf16 or 64 fp32
 
 // dtype: 0 fp32, 1 bf16; nchw_out selects the output layout.
 hipError_t launch_phase_gemm(const GemmArgs& a, int dtype, int cfg, bool nchw_out,

@@ -186,8 +186,9 @@ huge2_status validate_desc(const huge2_conv_desc* d, bool transposed) {
   const long long lim = INT_MAX;
   const long long esz = d->dtype == HUGE2_BF16 ? 2 : 4;
   long long cin_v = ((long long)d->c_in + 7) / 8 * 8;
-  long long cin_pad = ((long long)d->c_in + 63) / 64 * 64;
-  long long cout_pad = ((long long)d->c_out + 127) / 128 * 128;
+  // the largest paddings any tile configuration applies
+  long long cin_pad = ((long long)d->c_in + 127) / 128 * 128;
+  long long cout_pad = ((long long)d->c_out + 255) / 256 * 256;
   long long nx = (long long)d->n * cin_v * d->h * d->w * esz;
   long long ny = (long long)d->n * d->c_out * ho * wo * esz;
   long long nw = cin_pad * cout_pad * d->r * d->s * esz;

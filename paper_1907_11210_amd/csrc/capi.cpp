@@ -42,6 +42,8 @@ struct huge2_plan {
   int64_t nonzero_macs, issued_macs;
   bool ztile;   // all-taps form for few output channels (no GEMM work list)
   ZArgs zargs;  // its launch shape (pointers filled per call)
+  bool rowphase;  // output-stationary form for large strides
+  RpArgs rpargs;
   char kernel_name[64];
 };
 
@@ -292,6 +294,77 @@ bool ztile_shape(const huge2_conv_desc& d, bool transposed, ZArgs* z, int64_t* i
   return true;
 }
 
+// The output-stationary form (rowphase_kernel) applies to NCHW bf16
+// transposed convs with strides of at least 4, dilation 1, at most 32 input
+// and output channels, kernel extents at most twice the stride, input rows
+// of at most 64 and output rows a multiple of 8 elements (at most 2048).  Returns false
+// otherwise (or with HUGE2_ROWPHASE=0, or a GEMM tile forced).
+bool rowphase_shape(const huge2_conv_desc& d, bool transposed, RpArgs* z, int64_t* issued) {
+  if (!transposed || d.layout != HUGE2_NCHW || d.dtype != HUGE2_BF16) return false;
+  if (env_int("HUGE2_ROWPHASE", 1) == 0 || env_int("HUGE2_TILE", -1) >= 0) return false;
+  if (d.stride_h < 4 || d.stride_w < 4 || d.dil_h != 1 || d.dil_w != 1) return false;
+  if (d.stride_w > (kRpThreads / 64) * kRpMaxColPhasesPerWave) return false;
+  if (d.c_in > kRpCh || d.c_out > kRpCh || d.r > 2 * d.stride_h || d.s > 2 * d.stride_w)
+    return false;
+  if (d.w > kRpMaxW) return false;
+  int ho, wo;
+  if (!output_dims(d, true, &ho, &wo) || wo % 8 != 0 || wo > 64 * 4 * 8) return false;
+  if ((long long)kRpMaxRb * (d.w + 2) >= 4096) return false;  // pixel index range of a phase
+  // input columns read: Q_w - t for t < 2 must stay within [-1, w]
+  int max_rows = 0;
+  for (int rho = 0; rho < d.stride_w; ++rho) {
+    const int qhi = floor_div_i(wo - 1 + d.pad_w - rho, d.stride_w);
+    if (qhi > d.w) return false;
+  }
+  for (int rho = 0; rho < d.stride_h; ++rho) {
+    const int qlo = ceil_div_i(d.pad_h - rho, d.stride_h);
+    const int qhi = floor_div_i(ho - 1 + d.pad_h - rho, d.stride_h);
+    max_rows = std::max(max_rows, qhi - qlo + 1);
+  }
+  if (max_rows <= 0) return false;
+  // LDS rows are column-phase major: stride_w phases x nq slots per row
+  int nq = d.w + 1;
+  while ((d.stride_w * nq) % 8 != 0) ++nq;
+  const long long row_elems = (long long)d.stride_w * nq;
+  int rb = std::min(kRpMaxRb, max_rows);
+  while (rb > 1 && d.c_out * (rb * row_elems + 2) > kRpOutElems) --rb;
+  if (d.c_out * (rb * row_elems + 2) > kRpOutElems) return false;
+  std::memset(z, 0, sizeof(*z));
+  z->n = d.n;
+  z->cin = d.c_in;
+  z->h = d.h;
+  z->w = d.w;
+  z->cout = d.c_out;
+  z->r = d.r;
+  z->s = d.s;
+  z->stride_h = d.stride_h;
+  z->stride_w = d.stride_w;
+  z->pad_h = d.pad_h;
+  z->pad_w = d.pad_w;
+  z->ho = ho;
+  z->wo = wo;
+  z->rb = rb;
+  z->qblocks = (max_rows + rb - 1) / rb;
+  z->nq = nq;
+  // issued multiply-adds: per workgroup and column phase, 32-pixel blocks x
+  // 32 channels x (taps x 32 input channels)
+  int64_t iss = 0;
+  for (int rh = 0; rh < d.stride_h; ++rh) {
+    const int tnh = rh < d.r ? std::min(2, (d.r - 1 - rh) / d.stride_h + 1) : 0;
+    const int rows = floor_div_i(ho - 1 + d.pad_h - rh, d.stride_h) - ceil_div_i(d.pad_h - rh, d.stride_h) + 1;
+    for (int rw = 0; rw < d.stride_w; ++rw) {
+      const int tnw = rw < d.s ? std::min(2, (d.s - 1 - rw) / d.stride_w + 1) : 0;
+      const int nqw = floor_div_i(wo - 1 + d.pad_w - rw, d.stride_w) - ceil_div_i(d.pad_w - rw, d.stride_w) + 1;
+      for (int q0 = 0; q0 < rows; q0 += rb) {
+        const int64_t npix = (int64_t)std::min(rb, rows - q0) * std::max(nqw, 0);
+        iss += (npix + 31) / 32 * 32 * 32 * (int64_t)tnh * tnw * 32;
+      }
+    }
+  }
+  *issued = iss * d.n;
+  return true;
+}
+
 // Border-class splitting of a plan: HUGE2_CLASS_SPLIT (0, 1, 2) forces it;
 // otherwise 0 (one segment per phase group, out-of-range taps read zeros) or
 // 2 (per group, the form that issues fewer tile-taps), whichever the schedule
@@ -332,11 +405,12 @@ huge2_status dev_alloc(huge2_plan* p, void** out, size_t bytes) {
   return HUGE2_OK;
 }
 
-// Plan of the all-taps form: packed K-contiguous weights only (the kernel
-// reads the NCHW input directly, so nothing is staged).
-huge2_status create_ztile(huge2_plan** out, const huge2_conv_desc& d, int transposed,
-                          const void* w, hipStream_t stream, bool stream_ordered, const ZArgs& z,
-                          int64_t issued) {
+// Plan of the all-taps form (zp) or the output-stationary form (rp): packed
+// K-contiguous weights only (both kernels read the NCHW input directly, so
+// nothing is staged).
+huge2_status create_direct(huge2_plan** out, const huge2_conv_desc& d, int transposed,
+                          const void* w, hipStream_t stream, bool stream_ordered, const ZArgs* zp,
+                          const RpArgs* rp, int64_t issued) {
   PlanShape shape;
   if (!build_shape(d, true, 2, 128, &shape)) return HUGE2_ERR_INVALID_ARG;
   huge2_plan* p = new (std::nothrow) huge2_plan();
@@ -344,22 +418,27 @@ huge2_status create_ztile(huge2_plan** out, const huge2_conv_desc& d, int transp
   const int esz = elem_size(d.dtype);
   p->desc = d;
   p->transposed = transposed;
-  p->ho = z.ho;
-  p->wo = z.wo;
+  output_dims(d, true, &p->ho, &p->wo);
   p->cfg = -1;
   p->staged = false;
   p->c_stride = d.c_in;
-  p->cin_pad = z.cin_pad;
-  p->cout_pad = z.cout_pad;
+  p->cin_pad = zp ? zp->cin_pad : kRpCh;
+  p->cout_pad = zp ? zp->cout_pad : kRpCh;
   p->x_bytes = (size_t)d.n * d.c_in * d.h * d.w * esz;
-  p->wp_bytes = (size_t)d.r * d.s * z.cout_pad * z.cin_pad * esz;
+  p->wp_bytes = (size_t)d.r * d.s * p->cout_pad * p->cin_pad * esz;
   p->stream_ordered = stream_ordered;
   p->alloc_stream = stream;
   p->nonzero_macs = shape.nonzero_macs;
   p->issued_macs = issued;
-  p->ztile = true;
-  p->zargs = z;
-  std::snprintf(p->kernel_name, sizeof(p->kernel_name), "ztile_kernel ob%d", z.ob);
+  if (zp) {
+    p->ztile = true;
+    p->zargs = *zp;
+    std::snprintf(p->kernel_name, sizeof(p->kernel_name), "ztile_kernel ob%d", zp->ob);
+  } else {
+    p->rowphase = true;
+    p->rpargs = *rp;
+    std::snprintf(p->kernel_name, sizeof(p->kernel_name), "rowphase_kernel rb%d", rp->rb);
+  }
   huge2_status st = dev_alloc(p, &p->wp, p->wp_bytes);
   if (st != HUGE2_OK) {
     free_buffers(p);
@@ -368,8 +447,8 @@ huge2_status create_ztile(huge2_plan** out, const huge2_conv_desc& d, int transp
   }
   bool ok = !fault("launch");
   if (ok)
-    ok = launch_pack_weights(w, p->wp, d.dtype, true, d.c_in, d.c_out, d.r, d.s, z.cin_pad,
-                             z.cout_pad, 0, stream) == hipSuccess;
+    ok = launch_pack_weights(w, p->wp, d.dtype, true, d.c_in, d.c_out, d.r, d.s, p->cin_pad,
+                             p->cout_pad, 0, stream) == hipSuccess;
   if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
   if (!ok) {
     (void)hipGetLastError();
@@ -396,7 +475,10 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     ZArgs z;
     int64_t z_issued = 0;
     if (ztile_shape(d, tr, &z, &z_issued))
-      return create_ztile(out, d, transposed, w, stream, stream_ordered, z, z_issued);
+      return create_direct(out, d, transposed, w, stream, stream_ordered, &z, nullptr, z_issued);
+    RpArgs rp;
+    if (rowphase_shape(d, tr, &rp, &z_issued))
+      return create_direct(out, d, transposed, w, stream, stream_ordered, nullptr, &rp, z_issued);
   }
 
   const int cfg = choose_cfg(d, tr, 2);
@@ -611,6 +693,18 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
     }
     return HUGE2_OK;
   }
+  if (p->rowphase) {
+    RpArgs z = p->rpargs;
+    z.x = x;
+    z.wp = p->wp;
+    z.bias = bias;
+    z.y = y;
+    if (launch_rowphase(z, stream) != hipSuccess) {
+      (void)hipGetLastError();
+      return HUGE2_ERR_HIP;
+    }
+    return HUGE2_OK;
+  }
   GemmArgs a;
   a.x = p->staged ? p->xs : x;
   a.wp = p->wp;
@@ -793,7 +887,9 @@ huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, in
   try {
     ZArgs z;
     int64_t z_issued = 0;
-    if (ztile_shape(*desc, transposed != 0, &z, &z_issued)) {
+    RpArgs rp;
+    if (ztile_shape(*desc, transposed != 0, &z, &z_issued) ||
+        rowphase_shape(*desc, transposed != 0, &rp, &z_issued)) {
       PlanShape shape;
       if (!build_shape(*desc, true, 2, 128, &shape)) return HUGE2_ERR_INVALID_ARG;
       *nonzero_macs = shape.nonzero_macs;

@@ -1019,6 +1019,188 @@ hipError_t launch_ztile(const ZArgs& a, int dtype, hipStream_t stream) {
 }
 
 // ---------------------------------------------------------------------------
+// Transposed conv with a large stride and few channels (NCHW, bf16, dilation
+// 1, c_in and c_out <= 32, at most two taps of each axis per output phase):
+// the segmentation-decoder upsampling shape.  Every output phase there is a
+// GEMM of a few hundred pixels, and its pixels lie `stride` apart in the
+// output, so the phase GEMM writes 2-byte elements that no store can
+// combine.  This kernel is output-stationary instead: workgroup (image, row
+// phase rho_h, block of RB rows of that phase) runs, for every column phase
+// rho_w in turn, the small phase GEMM of section 3.1 (pixels x c_out, K =
+// taps x c_in) on MFMA, scatters the results into an LDS copy of its output
+// rows, and finally writes those rows whole with 16-byte stores.
+// Output o with o + pad = s*Q + rho takes kernel taps k = rho + s*t and input
+// Q - t (t = 0, 1 while k < kernel size).
+
+__global__ __launch_bounds__(kRpThreads) void rowphase_kernel(RpArgs a) {
+  constexpr int CH = kRpCh;
+  constexpr int NT = kRpThreads, NW = NT / 64;
+  constexpr int MRW = kRpMaxColPhasesPerWave;
+  constexpr int PP = CH + 8;  // LDS elements per input pixel (16-byte pad: spreads the banks)
+  __shared__ __attribute__((aligned(16))) uint16_t s_in[(kRpMaxRb + 1) * (kRpMaxW + 2) * PP];
+  // output rows, column-phase major: [k][row][rho_w][q_w] (q_w < nq), so that
+  // the lanes of one phase GEMM write consecutive elements
+  __shared__ __attribute__((aligned(16))) uint16_t s_out[kRpOutElems];
+  __shared__ float s_b[CH];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int b = blockIdx.x;
+  const int qb = b % a.qblocks;
+  b /= a.qblocks;
+  const int rho_h = b % a.stride_h, img = b / a.stride_h;
+  // rows of this row phase: oh = s*Q + rho_h - pad in [0, ho)
+  const int q_lo = -floor_div_d(-(a.pad_h - rho_h), a.stride_h);
+  const int q_hi = floor_div_d(a.ho - 1 + a.pad_h - rho_h, a.stride_h);
+  const int Q0 = q_lo + qb * a.rb;
+  const int nrows = min(a.rb, q_hi - Q0 + 1);
+  if (nrows <= 0) return;  // the whole workgroup leaves together
+  const int tnh = rho_h < a.r ? min(2, (a.r - 1 - rho_h) / a.stride_h + 1) : 0;
+  const int wp2 = a.w + 2;
+  const int nq = a.nq;  // q_w slots per column phase (>= largest q_w + 1)
+
+  // weight fragments of all this wave's column phases rho_w = wave + NW*c,
+  // issued first so that they arrive while the input is staged
+  const int k = lane & 31, half = lane >> 5;
+  uint4 bw[MRW][4][2];
+#pragma unroll
+  for (int c = 0; c < MRW; ++c) {
+    const int rho_w = wave + NW * c;
+    const int tnw = (rho_w < a.stride_w && rho_w < a.s) ? min(2, (a.s - 1 - rho_w) / a.stride_w + 1) : 0;
+#pragma unroll
+    for (int tp = 0; tp < 4; ++tp)
+#pragma unroll
+      for (int cs = 0; cs < 2; ++cs) {
+        const int th = tp >> 1, tw = tp & 1;
+        bw[c][tp][cs] = make_uint4(0, 0, 0, 0);
+        if (th < tnh && tw < tnw) {
+          const int slot = (rho_h + a.stride_h * th) * a.s + rho_w + a.stride_w * tw;
+          bw[c][tp][cs] = *(const uint4*)((const uint16_t*)a.wp +
+                                          ((size_t)slot * CH + k) * CH + cs * 16 + half * 8);
+        }
+      }
+  }
+
+  if (tid < CH) s_b[tid] = (a.bias && tid < a.cout) ? a.bias[tid] : 0.f;
+  // input rows Q0-1 .. Q0+nrows-1, columns -1 .. w, channel-contiguous; zero outside
+  const int in_elems = (nrows + 1) * wp2 * CH;
+  for (int e = tid; e < in_elems; e += NT) {
+    const int c = e % CH, pc = e / CH;
+    const int lc = pc % wp2, lr = pc / wp2;
+    const int i = Q0 - 1 + lr, j = lc - 1;
+    uint16_t v = 0;
+    if (c < a.cin && i >= 0 && i < a.h && j >= 0 && j < a.w)
+      v = ((const uint16_t*)a.x)[(((size_t)img * a.cin + c) * a.h + i) * a.w + j];
+    s_in[pc * PP + c] = v;
+  }
+  __syncthreads();
+  // output rows start at the bias (phases no tap reaches keep it), two
+  // elements at a time.  Channel k's rows start at k * cp: one dword more
+  // than its rows need, so that the 32 channels one store instruction
+  // writes fall in distinct LDS banks.
+  const int blk = a.stride_w * nq;  // a multiple of 8 (host)
+  const int cp = nrows * blk + 2;
+  const int npair = a.cout * (cp / 2);
+  for (int e = tid; e < npair; e += NT) {
+    const int kk = e / (cp / 2);
+    const uint32_t bb = f32_to_bf16_rne(s_b[kk]);
+    *(uint32_t*)(s_out + (size_t)e * 2) = bb | (bb << 16);
+  }
+  __syncthreads();
+
+#pragma unroll
+  for (int c = 0; c < MRW; ++c) {
+    const int rho_w = wave + NW * c;
+    if (rho_w >= a.stride_w) break;
+    const int tnw = rho_w < a.s ? min(2, (a.s - 1 - rho_w) / a.stride_w + 1) : 0;
+    const int qw_lo = -floor_div_d(-(a.pad_w - rho_w), a.stride_w);
+    const int qw_hi = floor_div_d(a.wo - 1 + a.pad_w - rho_w, a.stride_w);
+    const int nqw = qw_hi - qw_lo + 1;
+    const int npix = nrows * nqw;
+    if (tnh == 0 || tnw == 0 || nqw <= 0) continue;
+    // pixel m -> (row, column) by a float reciprocal: m < 2^12, so
+    // (m + 0.5) / nqw never lands within rounding error of an integer
+    const float inv_nqw = 1.0f / (float)nqw;
+    for (int mb = 0; mb * 32 < npix; ++mb) {
+      const int m = min(mb * 32 + (lane & 31), npix - 1);
+      const int qrow = (int)(((float)m + 0.5f) * inv_nqw), qw = qw_lo + m - qrow * nqw;
+      f32x16 acc;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+#pragma unroll
+      for (int tp = 0; tp < 4; ++tp) {
+        const int th = tp >> 1, tw = tp & 1;
+        if (th >= tnh || tw >= tnw) continue;
+        const int lr = qrow + 1 - th, lc = qw - tw + 1;
+#pragma unroll
+        for (int cs = 0; cs < 2; ++cs) {
+          const uint4 av = *(const uint4*)(s_in + (lr * wp2 + lc) * PP + cs * 16 + half * 8);
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av),
+                                                        __builtin_bit_cast(bf16x8, bw[c][tp][cs]),
+                                                        acc, 0, 0, 0);
+        }
+      }
+      // lane holds output channel k for pixels 8*(q/4) + 4*half + q%4 of the block
+      if (k < a.cout) {
+        const float bk = s_b[k];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const int mm = mb * 32 + 8 * (q >> 2) + 4 * half + (q & 3);
+          if (mm >= npix) continue;
+          const int qr = (int)(((float)mm + 0.5f) * inv_nqw), qwv = qw_lo + mm - qr * nqw;
+          s_out[k * cp + (qr * a.stride_w + rho_w) * nq + qwv] = f32_to_bf16_rne(acc[q] + bk);
+        }
+      }
+    }
+  }
+  __syncthreads();
+  // whole output rows, 16 bytes per store: element ow of a row is phase
+  // (ow + pad) mod stride, slot (ow + pad) div stride.  Lane l takes the
+  // 8-element pieces v = l, l + 64, ... of every row its wave visits, so the
+  // phase/slot decomposition is done once per piece.
+  const int vpr = a.wo / 8;
+  constexpr int VPL = 4;  // pieces per lane: rows of at most 2048 elements
+  int q0[VPL], r0[VPL];
+#pragma unroll
+  for (int c = 0; c < VPL; ++c) {
+    const int u = (lane + 64 * c) * 8 + a.pad_w;
+    q0[c] = u / a.stride_w;
+    r0[c] = u - q0[c] * a.stride_w;
+  }
+  for (int rr = wave; rr < a.cout * nrows; rr += NW) {
+    const int kk = rr / nrows, qr = rr - kk * nrows;
+    const int oh = a.stride_h * (Q0 + qr) + rho_h - a.pad_h;
+    const uint16_t* row = s_out + kk * cp + qr * blk;
+    uint16_t* yrow = (uint16_t*)a.y + (((size_t)img * a.cout + kk) * a.ho + oh) * a.wo;
+#pragma unroll
+    for (int c = 0; c < VPL; ++c) {
+      const int v = lane + 64 * c;
+      if (v >= vpr) break;
+      int qw = q0[c], rw = r0[c];
+      uint32_t wv[4];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const uint32_t h16 = row[rw * nq + qw];
+        if (t & 1)
+          wv[t >> 1] |= h16 << 16;
+        else
+          wv[t >> 1] = h16;
+        if (++rw == a.stride_w) {
+          rw = 0;
+          ++qw;
+        }
+      }
+      *(uint4*)(yrow + v * 8) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+    }
+  }
+}
+
+hipError_t launch_rowphase(const RpArgs& a, hipStream_t stream) {
+  const dim3 grid(a.n * a.stride_h * a.qblocks);
+  hipLaunchKernelGGL(rowphase_kernel, grid, dim3(kRpThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Weight packing: element (slot, k, c) = w at kernel tap slot = (kh, kw),
 // output channel k, input channel c.
 //   lane_kb = 0: K-contiguous rows, wp[slot][k][c].

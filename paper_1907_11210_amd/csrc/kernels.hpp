@@ -187,6 +187,29 @@ struct ZArgs {
 };
 hipError_t launch_ztile(const ZArgs& a, int dtype, hipStream_t stream);
 
+// Output-stationary form for large strides and few channels (NCHW, bf16,
+// dilation 1, c_in, c_out <= 32, kernel size <= 2 * stride): workgroup
+// (image, row phase, block of rb rows of that phase) runs every column
+// phase's small GEMM, collects its output rows in LDS and writes them whole.
+constexpr int kRpCh = 32;                  // channel padding of input and weights
+constexpr int kRpMaxW = 64;                // input width
+constexpr int kRpMaxRb = 8;                // rows of one row phase per workgroup
+constexpr int kRpOutElems = 48 * 1024;     // LDS output rows (bf16 elements)
+constexpr int kRpThreads = 512;            // 8 waves: many column phases in flight
+constexpr int kRpMaxColPhasesPerWave = 4;  // stride_w <= 8 waves x 4
+struct RpArgs {
+  const void* x;
+  const void* wp;  // packed K-contiguous weights [slot][32][32]
+  const float* bias;
+  void* y;
+  int n, cin, h, w, cout, r, s;
+  int stride_h, stride_w, pad_h, pad_w, ho, wo;
+  int rb;       // rows of one row phase per workgroup
+  int qblocks;  // row blocks per (image, row phase)
+  int nq;       // q_w slots per column phase in LDS (stride_w * nq a multiple of 8)
+};
+hipError_t launch_rowphase(const RpArgs& a, hipStream_t stream);
+
 // Re-layout the input into [n][h*w][c_stride] with zero channel padding.
 // nchw: source is NCHW; otherwise NHWC with cin channels per pixel.
 hipError_t launch_stage_input(const void* x, void* xs, int dtype, bool nchw, int n, int cin,

@@ -52,6 +52,11 @@ SMALL = [
     L("ct_fewout_s3d2", True, 1, 16, 7, 8, 4, 3, 3, 3, 2, 1, 2, "NCHW", "bf16"),
     L("ct_fewout_tall", True, 3, 130, 37, 8, 1, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
     L("ct_fewout_wide", True, 1, 8, 3, 64, 2, 5, 5, 2, 2, 1, 1, "NCHW", "f32"),
+    # large stride, few channels, NCHW bf16: the output-stationary form
+    L("ct_rowphase_s8", True, 2, 5, 6, 6, 7, 16, 16, 8, 4, 0, 1, "NCHW", "bf16"),
+    L("ct_rowphase_s4", True, 2, 20, 5, 8, 9, 6, 6, 4, 1, 0, 1, "NCHW", "bf16"),
+    L("ct_rowphase_zerotap", True, 1, 4, 3, 8, 3, 6, 6, 8, 3, 0, 1, "NCHW", "bf16"),
+    L("ct_rowphase_c32", True, 1, 32, 4, 4, 32, 8, 8, 4, 2, 0, 1, "NCHW", "bf16"),
 ]
 
 
@@ -326,3 +331,23 @@ def test_plan_reports_its_kernel():
         name = plan.kernel
         plan.close()
         assert name.startswith(family), (layer.name, name)
+
+
+@pytest.mark.parametrize("rowphase", [0, 1])
+def test_large_stride_forms(rowphase, monkeypatch):
+    """Large-stride few-channel NCHW transposed convs through the output-
+    stationary form and, with it switched off, through the phase GEMM."""
+    monkeypatch.setenv("HUGE2_ROWPHASE", str(rowphase))
+    dev = torch.device("cuda", 0)
+    for layer in [l for l in SMALL if l.name.startswith("ct_rowphase")]:
+        P.say("case rowphase", rowphase, layer)
+        xq, wq = _inputs(layer, seed=90 + rowphase)
+        bias = torch.linspace(-0.4, 0.4, layer.c_out)
+        ref = P.oracle_full(layer, xq, wq, bias)
+        absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
+        y = P.run_gpu(layer, xq, wq, bias)
+        P.check(y, ref, absref, layer.dtype, "%s rowphase %d" % (layer.name, rowphase))
+        plan = P.make_plan(layer, wq.contiguous().to(dev))
+        name = plan.kernel
+        plan.close()
+        assert name.startswith("rowphase_kernel") == bool(rowphase), (layer.name, name)

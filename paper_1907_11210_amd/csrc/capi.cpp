@@ -365,6 +365,33 @@ bool rowphase_shape(const huge2_conv_desc& d, bool transposed, RpArgs* z, int64_
   return true;
 }
 
+// Whether a segment's taps are the product of two arithmetic progressions
+// (the order build_shape emits: h outer, w inner), verified tap by tap; fills
+// the progression fields of sd when they are.
+bool tap_progressions(const huge2_tap* tl, int count, SegDev* sd) {
+  if (count <= 0) return false;
+  int ntw = 1;
+  while (ntw < count && tl[ntw].kh == tl[0].kh) ++ntw;
+  if (count % ntw != 0) return false;
+  const int nth = count / ntw;
+  sd->ntw = ntw;
+  sd->off0_h = tl[0].off_h;
+  sd->off0_w = tl[0].off_w;
+  sd->kh0 = tl[0].kh;
+  sd->kw0 = tl[0].kw;
+  sd->doff_h = nth > 1 ? tl[ntw].off_h - tl[0].off_h : 0;
+  sd->dkh = nth > 1 ? tl[ntw].kh - tl[0].kh : 0;
+  sd->doff_w = ntw > 1 ? tl[1].off_w - tl[0].off_w : 0;
+  sd->dkw = ntw > 1 ? tl[1].kw - tl[0].kw : 0;
+  for (int t = 0; t < count; ++t) {
+    const int th = t / ntw, tw = t % ntw;
+    if (tl[t].kh != sd->kh0 + th * sd->dkh || tl[t].kw != sd->kw0 + tw * sd->dkw ||
+        tl[t].off_h != sd->off0_h + th * sd->doff_h || tl[t].off_w != sd->off0_w + tw * sd->doff_w)
+      return false;
+  }
+  return true;
+}
+
 // Border-class splitting of a plan: HUGE2_CLASS_SPLIT (0, 1, 2) forces it;
 // otherwise 0 (one segment per phase group, out-of-range taps read zeros) or
 // 2 (per group, the form that issues fewer tile-taps), whichever the schedule
@@ -378,6 +405,17 @@ int choose_split(const huge2_conv_desc& d, bool transposed, int cfg) {
     return 2;
   return makespan_stages(d, s0, cfg) < makespan_stages(d, s2, cfg) ? 0 : 2;
 }
+
+// Tile configuration, border-class form and decomposition of a GEMM plan
+// (shared by plan creation and the MAC report).  Returns -1 if the shape
+// cannot be built.
+int plan_gemm_shape(const huge2_conv_desc& d, bool tr, PlanShape* shape) {
+  const int cfg = choose_cfg(d, tr, 2);
+  const int split = choose_split(d, tr, cfg);
+  if (!build_shape(d, tr, split, tile_bm(cfg), shape)) return -1;
+  return cfg;
+}
+
 
 void free_buffers(huge2_plan* p) {
   void* bufs[3] = {p->wp, p->meta, p->xs};
@@ -481,11 +519,10 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
       return create_direct(out, d, transposed, w, stream, stream_ordered, nullptr, &rp, z_issued);
   }
 
-  const int cfg = choose_cfg(d, tr, 2);
-  const int split = choose_split(d, tr, cfg);
-  const int bm = tile_bm(cfg), bn = tile_bn(cfg);
   PlanShape shape;
-  if (!build_shape(d, tr, split, bm, &shape)) return HUGE2_ERR_INVALID_ARG;
+  const int cfg = plan_gemm_shape(d, tr, &shape);
+  if (cfg < 0) return HUGE2_ERR_INVALID_ARG;
+  const int bm = tile_bm(cfg), bn = tile_bn(cfg);
 
   huge2_plan* p = new (std::nothrow) huge2_plan();
   if (!p) return HUGE2_ERR_ALLOC;
@@ -569,33 +606,7 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
                              (long long)s.in_step_w * (s.q0_w + s.qn_w - 1) + tp.off_w;
       if (h_lo < 0 || h_hi >= d.h || w_lo < 0 || w_hi >= d.w) sd.exact = 0;
     }
-    // taps as a product of two arithmetic progressions (the order build_shape
-    // emits: h outer, w inner), verified tap by tap
-    sd.tap_ap = 0;
-    if (s.tap_count > 0) {
-      const huge2_tap* tl = &shape.taps[s.tap_begin];
-      int ntw = 1;
-      while (ntw < s.tap_count && tl[ntw].kh == tl[0].kh) ++ntw;
-      if (s.tap_count % ntw == 0) {
-        const int nth = s.tap_count / ntw;
-        sd.ntw = ntw;
-        sd.off0_h = tl[0].off_h;
-        sd.off0_w = tl[0].off_w;
-        sd.kh0 = tl[0].kh;
-        sd.kw0 = tl[0].kw;
-        sd.doff_h = nth > 1 ? tl[ntw].off_h - tl[0].off_h : 0;
-        sd.dkh = nth > 1 ? tl[ntw].kh - tl[0].kh : 0;
-        sd.doff_w = ntw > 1 ? tl[1].off_w - tl[0].off_w : 0;
-        sd.dkw = ntw > 1 ? tl[1].kw - tl[0].kw : 0;
-        bool ok = true;
-        for (int t = 0; t < s.tap_count && ok; ++t) {
-          const int th = t / ntw, tw = t % ntw;
-          ok = tl[t].kh == sd.kh0 + th * sd.dkh && tl[t].kw == sd.kw0 + tw * sd.dkw &&
-               tl[t].off_h == sd.off0_h + th * sd.doff_h && tl[t].off_w == sd.off0_w + tw * sd.doff_w;
-        }
-        sd.tap_ap = ok ? 1 : 0;
-      }
-    }
+    sd.tap_ap = tap_progressions(&shape.taps[s.tap_begin], s.tap_count, &sd) ? 1 : 0;
     if (!sd.tap_ap) sd.ntw = 1;
     segs.push_back(sd);
     for (int m0 = 0; m0 < sd.m_total; m0 += bm)
@@ -896,11 +907,10 @@ huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, in
       *issued_macs = z_issued;
       return HUGE2_OK;
     }
-    const int cfg = choose_cfg(*desc, transposed != 0, 2);
-    const int split = choose_split(*desc, transposed != 0, cfg);
-    const int bm = tile_bm(cfg), bn = tile_bn(cfg);
     PlanShape shape;
-    if (!build_shape(*desc, transposed != 0, split, bm, &shape)) return HUGE2_ERR_INVALID_ARG;
+    const int cfg = plan_gemm_shape(*desc, transposed != 0, &shape);
+    if (cfg < 0) return HUGE2_ERR_INVALID_ARG;
+    const int bm = tile_bm(cfg), bn = tile_bn(cfg);
     const int bk = tile_kb(cfg) / elem_size(desc->dtype);
     const int64_t cin_pad = round_up(desc->c_in, bk);
     const int64_t ntn = round_up(desc->c_out, bn) / bn;

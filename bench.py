@@ -53,6 +53,10 @@ DESCRIPTIONS = {
     "aspp": "ASPP: four 3x3 dilated convs 2048->256 (d=6,12,18,24, same pad), 64x64, "
             "bf16 NHWC, batch 8",
     "fcn_upsample": "ConvT 21->21 k64 s32 p16, 16x16->512x512, bf16 NCHW, batch 4",
+    "table1_dcgan": "the paper's Table 1 DCGAN deconvolutions: ConvT k5 s2 (p2 op1) 1024->512 "
+                    "(4->8), 512->256, 256->128, 128->3 (32->64), bf16 NCHW, batch 1",
+    "table1_cgan": "the paper's Table 1 cGAN deconvolutions: ConvT k4 s2 p1 256->128 (8->16), "
+                   "128->3 (16->32), bf16 NCHW, batch 1",
 }
 
 
@@ -95,7 +99,7 @@ def build_workload(name, dev):
                              layer.out_pad, layer.dil, layer.layout))
         inputs.append(None if x is None else wl.to_layout(x.to(dt), layer.layout).to(dev))
         del w_dev
-    chained = name in ("dcgan", "dcgan_f32")
+    chained = name in wl.CHAINED
     outs = [torch.empty(p.out_shape, dtype=wl.torch_dtype(l.dtype), device=dev)
             for p, (l, _, _) in zip(plans, items)]
 

@@ -21,6 +21,14 @@ Workloads (``name``: layers):
                padding, bf16 NHWC, batch 8, input ReLU(N(0,1)).
   fcn_upsample ConvTranspose 21->21, 16x16 -> 512x512, k64 s32 p16, bilinear kernel plus
                N(0, 1e-3) noise, bf16 NCHW, batch 4.
+  table1_dcgan the DCGAN deconvolution layers of the paper's Table 1: 5x5 kernels, stride
+               2, 4x4x1024 -> 8x8x512 -> 16x16x256 -> 32x32x128 -> 64x64x3, batch 1
+               (inference), bf16 NCHW.  The table gives no padding; the output doubles
+               the input, which symmetric padding reaches with pad 2 and output
+               padding 1 (the same taps per phase as TensorFlow's 'SAME' deconvolution,
+               with the phase roles mirrored).  Input N(0,1), weights N(0,0.02), chained.
+  table1_cgan  the cGAN layers of Table 1: 4x4 kernels, stride 2, pad 1,
+               8x8x256 -> 16x16x128 -> 32x32x3, batch 1, bf16 NCHW, chained.
 """
 from __future__ import annotations
 
@@ -74,6 +82,15 @@ def dcgan_layers(dtype="bf16", batch=64):
     return out
 
 
+def table1_layers(kind, batch=1, dtype="bf16"):
+    if kind == "dcgan":
+        chans, k, pad, op, hw0 = [(1024, 512), (512, 256), (256, 128), (128, 3)], 5, 2, 1, 4
+    else:
+        chans, k, pad, op, hw0 = [(256, 128), (128, 3)], 4, 1, 0, 8
+    return [Layer("t1_%s_dc%d" % (kind, i + 1), True, batch, ci, hw0 << i, hw0 << i, co, k, k, 2,
+                  pad, op, 1, "NCHW", dtype) for i, (ci, co) in enumerate(chans)]
+
+
 def aspp_layers(batch=8, c_in=2048, c_out=256, hw=64):
     return [Layer("aspp_d%d" % d, False, batch, c_in, hw, hw, c_out, 3, 3, 1, d, 0, d, "NHWC",
                   "bf16") for d in (6, 12, 18, 24)]
@@ -87,7 +104,10 @@ WORKLOADS = {
     "aspp": aspp_layers(),
     "fcn_upsample": [Layer("fcn_upsample", True, 4, 21, 16, 16, 21, 64, 64, 32, 16, 0, 1, "NCHW",
                            "bf16")],
+    "table1_dcgan": table1_layers("dcgan"),
+    "table1_cgan": table1_layers("cgan"),
 }
+CHAINED = ("dcgan", "dcgan_f32", "table1_dcgan", "table1_cgan")
 
 
 def torch_dtype(name):
@@ -126,6 +146,11 @@ def generate(workload, seed=0, batch=None):
         out = [(layers[0], x1, ws[0])]
         out += [(l, None, w) for l, w in zip(layers[1:], ws[1:])]
         return out
+    if workload in ("table1_dcgan", "table1_cgan"):
+        l0 = layers[0]
+        x1 = _normal(g, (l0.n, l0.c_in, l0.h, l0.w))
+        ws = [_normal(g, l.w_shape(), 0.02) for l in layers]
+        return [(layers[0], x1, ws[0])] + [(l, None, w) for l, w in zip(layers[1:], ws[1:])]
     if workload == "aspp":
         l0 = layers[0]
         x = torch.relu(_normal(g, (l0.n, l0.c_in, l0.h, l0.w)))

@@ -162,6 +162,24 @@ def test_dcgan_chain_reduced_batch():
             x_prev = torch.from_numpy(ref).to(torch.float32)
 
 
+@pytest.mark.parametrize("wname", ["table1_dcgan", "table1_cgan"])
+def test_table1_layers_full(wname):
+    """The paper's own Table 1 deconvolution layers (5x5 DCGAN with unequal
+    phases, 4x4 cGAN), batch 1, checked in full; each layer gets the oracle's
+    output of the previous one."""
+    items = wl.generate(wname, seed=0)
+    x_prev = None
+    for layer, x, w in items:
+        P.say("case", wname, layer)
+        xin = x if x is not None else x_prev
+        xq, wq = P.quantise(xin, layer.dtype), P.quantise(w, layer.dtype)
+        ref = P.oracle_full(layer, xq, wq)
+        absref = P.oracle_full(layer, xq, wq, absolute=True)
+        y = P.run_gpu(layer, xq, wq)
+        P.check(y, ref, absref, layer.dtype, layer.name)
+        x_prev = torch.from_numpy(ref).to(torch.float32)
+
+
 REDUCED = [
     ("convt_small", {}),
     ("convt_odd", dict(n=1)),

@@ -92,6 +92,9 @@ int choose_cfg(const huge2_conv_desc& d, bool transposed, int class_split) {
   const bool large = count_works(d, transposed, class_split, 8) >= 512;
   if (d.dtype != HUGE2_BF16) return large ? 8 : 2;
   if (large && d.c_out <= 128) return 8;                            // 128 x 128, 8 waves
+  // 128 x 256 split-wave, 8 waves: twice the pixels per weight fetch of the
+  // 64 x 256 tile, which the ASPP layers' L2 traffic needs
+  if (d.c_out >= 256 && count_works(d, transposed, class_split, 32) >= kComputeUnits) return 32;
   if (d.c_out >= 256 && count_works(d, transposed, class_split, 23) >= 384) return 23;
   if (count_works(d, transposed, class_split, 27) >= kComputeUnits) return 27;
   return 25;                                                        // 64 x 128, 2 K groups

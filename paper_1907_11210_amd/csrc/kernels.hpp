@@ -120,6 +120,8 @@ constexpr TileShape kTiles[] = {
     {128, 128, 1, 4, 256, 2, 1, 1, 2},  // 29 as 27 with 256-byte K stages
     {64, 256, 1, 4, 256, 2, 2, 1, 1},   // 30 as 23 with 256-byte K stages
     {128, 128, 4, 2, 256, 2, 1, 0},     // 31 as 8 with 256-byte K stages
+    {128, 256, 1, 8, 128, 3, 1, 1, 1},  // 32 split-wave: 8 waves of 128 x 32 channels
+    {128, 256, 1, 8, 128, 2, 2, 1, 1},  // 33 as 32, two stages in flight
 };
 constexpr int kComputeUnits = 256;  // MI355X
 constexpr int TILE_COUNT = (int)(sizeof(kTiles) / sizeof(kTiles[0]));

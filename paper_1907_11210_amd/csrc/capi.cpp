@@ -80,8 +80,9 @@ long long count_works(const huge2_conv_desc& d, bool transposed, int class_split
 
 // Tile choice, from measurements on MI355X.  bf16: many pixels and at most
 // 128 output channels take the 8-wave 128 x 128 tile; 256 or more output
-// channels with plenty of 64-pixel tiles take the split-wave 64 x 256 tile
-// (ASPP); otherwise the split-wave tiles with two K groups per workgroup,
+// channels take the 8-wave split-wave 128 x 256 tile when every CU gets one
+// (ASPP: twice the pixels per weight fetch of 64 x 256, which its L2 traffic
+// needs), else the 64 x 256 one with plenty of its tiles; otherwise the split-wave tiles with two K groups per workgroup,
 // 128 x 128 when that still gives every CU a tile, else 64 x 128 (few
 // pixels and long K: the first DCGAN layers).  Few output channels take the
 // narrow 128 x 32 tile.  fp32 keeps the two-operand-LDS tiles.
@@ -92,8 +93,6 @@ int choose_cfg(const huge2_conv_desc& d, bool transposed, int class_split) {
   const bool large = count_works(d, transposed, class_split, 8) >= 512;
   if (d.dtype != HUGE2_BF16) return large ? 8 : 2;
   if (large && d.c_out <= 128) return 8;                            // 128 x 128, 8 waves
-  // 128 x 256 split-wave, 8 waves: twice the pixels per weight fetch of the
-  // 64 x 256 tile, which the ASPP layers' L2 traffic needs
   if (d.c_out >= 256 && count_works(d, transposed, class_split, 32) >= kComputeUnits) return 32;
   if (d.c_out >= 256 && count_works(d, transposed, class_split, 23) >= 384) return 23;
   if (count_works(d, transposed, class_split, 27) >= kComputeUnits) return 27;

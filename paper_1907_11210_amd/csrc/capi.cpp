@@ -44,6 +44,8 @@ struct huge2_plan {
   ZArgs zargs;  // its launch shape (pointers filled per call)
   bool rowphase;  // output-stationary form for large strides
   RpArgs rpargs;
+  bool quad;      // all-phase form of the stride-2, 4x4, padding-1 layer
+  QArgs qargs;
   char kernel_name[64];
 };
 
@@ -367,6 +369,92 @@ bool rowphase_shape(const huge2_conv_desc& d, bool transposed, RpArgs* z, int64_
   return true;
 }
 
+// The all-phase form (quad_kernel) applies to NCHW bf16 transposed convs
+// with stride 2, a 4x4 kernel, padding 1, dilation 1 and no output padding
+// (so every phase has 2x2 taps at input offsets in [-1, 1] and the input's
+// pixel grid), input channels a multiple of 64, and a width of at least 4
+// that tiles 64 positions per workgroup: whole images of h*w <= 64 pixels
+// (h*w dividing 64, a multiple of 8), or 64/w full rows (w dividing 64, h a
+// multiple of 64/w).  Returns false otherwise (or with HUGE2_QUAD=0, or a
+// GEMM tile forced).
+bool quad_shape(const huge2_conv_desc& d, bool transposed, QArgs* q, int64_t* issued) {
+  if (!transposed || d.layout != HUGE2_NCHW || d.dtype != HUGE2_BF16) return false;
+  if (env_int("HUGE2_QUAD", 1) == 0 || env_int("HUGE2_TILE", -1) >= 0) return false;
+  if (d.stride_h != 2 || d.stride_w != 2 || d.r != 4 || d.s != 4 || d.pad_h != 1 ||
+      d.pad_w != 1 || d.dil_h != 1 || d.dil_w != 1 || d.out_pad_h != 0 || d.out_pad_w != 0)
+    return false;
+  if (d.c_in % 64 != 0 || d.w < 4) return false;
+  int ni, qbh;
+  const long long hw = (long long)d.h * d.w;
+  if (hw <= kQuadPix) {
+    if (kQuadPix % hw != 0 || hw % 8 != 0) return false;
+    ni = (int)(kQuadPix / hw);
+    qbh = d.h;
+  } else {
+    if (d.w > kQuadPix || kQuadPix % d.w != 0) return false;
+    ni = 1;
+    qbh = kQuadPix / d.w;
+    if (d.h % qbh != 0) return false;
+  }
+  if (ni * (qbh + 2) * (d.w + 2) > kQuadHaloRows) return false;
+  const int igroups = (d.n + ni - 1) / ni, hblocks = d.h / qbh;
+  // 64-channel tiles: two waves of 32 channels per phase, or (HUGE2_QUAD_WCH=2,
+  // an even number of 64-channel K blocks) two K groups of one wave of 64
+  // channels per phase; 32-channel tiles in two K groups when 64-channel
+  // tiles would leave compute units idle
+  const bool keven = (d.c_in / 64) % 2 == 0;
+  int nch = 2, ks = 1;
+  const long long wg64 = (long long)igroups * hblocks * ((d.c_out + 63) / 64);
+  if (wg64 < kComputeUnits && keven) {
+    nch = 1;
+    ks = 2;
+  } else if (keven && env_int("HUGE2_QUAD_WCH", 1) == 2) {
+    ks = 2;
+  }
+  // loaded rows per block: at most min(h, qbh + 2); input items (pixel pair x
+  // 8 channels) per thread bounded
+  const long long items = (long long)ni * std::min(d.h, qbh + 2) * d.w / 2 * 8;
+  if (items > (long long)kQuadMaxPieces * (kQuadThreads / ks)) return false;
+  const long long x_bytes = (long long)d.n * d.c_in * hw * 2;
+  if (x_bytes >= (1ll << 31)) return false;
+  std::memset(q, 0, sizeof(*q));
+  q->x_bytes = (uint32_t)x_bytes;
+  q->n = d.n;
+  q->cin = d.c_in;
+  q->h = d.h;
+  q->w = d.w;
+  q->cout = d.c_out;
+  q->cout_pad = round_up(d.c_out, 32 * nch);
+  q->ni = ni;
+  q->qbh = qbh;
+  q->nch = nch;
+  q->ks = ks;
+  q->igroups = igroups;
+  q->hblocks = hblocks;
+  q->ntiles = q->cout_pad / (32 * nch);
+  const long long wgs = (long long)q->ntiles * igroups * hblocks;
+  q->depth = env_int("HUGE2_QUAD_DEPTH", 2);
+  if ((q->depth != 2 && q->depth != 4 && q->depth != 8) || (nch == 2 && ks == 2)) q->depth = 2;
+  const long long wp_bytes = 16ll * q->cout_pad * d.c_in * 2;
+  if (wp_bytes >= (1ll << 31)) return false;
+  q->wp_bytes = (uint32_t)wp_bytes;
+  // output o = 2 q + rho takes kernel tap k with (rho + pad - k) even, reading
+  // input q + (rho + pad - k) / 2
+  for (int rh = 0; rh < 2; ++rh)
+    for (int rw = 0; rw < 2; ++rw)
+      for (int th = 0; th < 2; ++th)
+        for (int tw = 0; tw < 2; ++tw) {
+          const int kh = (rh + d.pad_h) % 2 + 2 * th, kw = (rw + d.pad_w) % 2 + 2 * tw;
+          q->slot[2 * rh + rw][2 * th + tw] = (int8_t)(kh * 4 + kw);
+          q->dh[2 * rh + rw][2 * th + tw] = (int8_t)((rh + d.pad_h - kh) / 2);
+          q->dw[2 * rh + rw][2 * th + tw] = (int8_t)((rw + d.pad_w - kw) / 2);
+        }
+  // issued multiply-adds: per workgroup 4 phases x 64 positions x 32*nch
+  // channels x 4 taps x c_in
+  *issued = wgs * 4 * kQuadPix * 32 * nch * 4 * (long long)d.c_in;
+  return true;
+}
+
 // Whether a segment's taps are the product of two arithmetic progressions
 // (the order build_shape emits: h outer, w inner), verified tap by tap; fills
 // the progression fields of sd when they are.
@@ -445,12 +533,13 @@ huge2_status dev_alloc(huge2_plan* p, void** out, size_t bytes) {
   return HUGE2_OK;
 }
 
-// Plan of the all-taps form (zp) or the output-stationary form (rp): packed
-// K-contiguous weights only (both kernels read the NCHW input directly, so
-// nothing is staged).
+// Plan of the all-taps form (zp), the output-stationary form (rp) or the
+// all-phase form (qp): packed weights only (K-contiguous, or in the lane order
+// of 128-byte K stages for qp); the three kernels read the NCHW input
+// directly, so nothing is staged.
 huge2_status create_direct(huge2_plan** out, const huge2_conv_desc& d, int transposed,
                           const void* w, hipStream_t stream, bool stream_ordered, const ZArgs* zp,
-                          const RpArgs* rp, int64_t issued) {
+                          const RpArgs* rp, const QArgs* qp, int64_t issued) {
   PlanShape shape;
   if (!build_shape(d, true, 2, 128, &shape)) return HUGE2_ERR_INVALID_ARG;
   huge2_plan* p = new (std::nothrow) huge2_plan();
@@ -462,8 +551,8 @@ huge2_status create_direct(huge2_plan** out, const huge2_conv_desc& d, int trans
   p->cfg = -1;
   p->staged = false;
   p->c_stride = d.c_in;
-  p->cin_pad = zp ? zp->cin_pad : kRpCh;
-  p->cout_pad = zp ? zp->cout_pad : kRpCh;
+  p->cin_pad = zp ? zp->cin_pad : qp ? d.c_in : kRpCh;
+  p->cout_pad = zp ? zp->cout_pad : qp ? qp->cout_pad : kRpCh;
   p->x_bytes = (size_t)d.n * d.c_in * d.h * d.w * esz;
   p->wp_bytes = (size_t)d.r * d.s * p->cout_pad * p->cin_pad * esz;
   p->stream_ordered = stream_ordered;
@@ -474,10 +563,15 @@ huge2_status create_direct(huge2_plan** out, const huge2_conv_desc& d, int trans
     p->ztile = true;
     p->zargs = *zp;
     std::snprintf(p->kernel_name, sizeof(p->kernel_name), "ztile_kernel ob%d", zp->ob);
-  } else {
+  } else if (rp) {
     p->rowphase = true;
     p->rpargs = *rp;
     std::snprintf(p->kernel_name, sizeof(p->kernel_name), "rowphase_kernel rb%d", rp->rb);
+  } else {
+    p->quad = true;
+    p->qargs = *qp;
+    std::snprintf(p->kernel_name, sizeof(p->kernel_name), "quad_kernel %dx%dx%d c%d k%d d%d",
+                  qp->ni, qp->qbh, d.w, 32 * qp->nch, qp->ks, qp->depth);
   }
   huge2_status st = dev_alloc(p, &p->wp, p->wp_bytes);
   if (st != HUGE2_OK) {
@@ -488,7 +582,7 @@ huge2_status create_direct(huge2_plan** out, const huge2_conv_desc& d, int trans
   bool ok = !fault("launch");
   if (ok)
     ok = launch_pack_weights(w, p->wp, d.dtype, true, d.c_in, d.c_out, d.r, d.s, p->cin_pad,
-                             p->cout_pad, 0, stream) == hipSuccess;
+                             p->cout_pad, qp ? 128 : 0, stream) == hipSuccess;
   if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
   if (!ok) {
     (void)hipGetLastError();
@@ -515,10 +609,16 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     ZArgs z;
     int64_t z_issued = 0;
     if (ztile_shape(d, tr, &z, &z_issued))
-      return create_direct(out, d, transposed, w, stream, stream_ordered, &z, nullptr, z_issued);
+      return create_direct(out, d, transposed, w, stream, stream_ordered, &z, nullptr, nullptr,
+                           z_issued);
     RpArgs rp;
     if (rowphase_shape(d, tr, &rp, &z_issued))
-      return create_direct(out, d, transposed, w, stream, stream_ordered, nullptr, &rp, z_issued);
+      return create_direct(out, d, transposed, w, stream, stream_ordered, nullptr, &rp, nullptr,
+                           z_issued);
+    QArgs q;
+    if (quad_shape(d, tr, &q, &z_issued))
+      return create_direct(out, d, transposed, w, stream, stream_ordered, nullptr, nullptr, &q,
+                           z_issued);
   }
 
   PlanShape shape;
@@ -718,6 +818,18 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
     }
     return HUGE2_OK;
   }
+  if (p->quad) {
+    QArgs z = p->qargs;
+    z.x = x;
+    z.wp = p->wp;
+    z.bias = bias;
+    z.y = y;
+    if (launch_quad(z, stream) != hipSuccess) {
+      (void)hipGetLastError();
+      return HUGE2_ERR_HIP;
+    }
+    return HUGE2_OK;
+  }
   GemmArgs a;
   a.x = p->staged ? p->xs : x;
   a.wp = p->wp;
@@ -901,8 +1013,10 @@ huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, in
     ZArgs z;
     int64_t z_issued = 0;
     RpArgs rp;
+    QArgs q;
     if (ztile_shape(*desc, transposed != 0, &z, &z_issued) ||
-        rowphase_shape(*desc, transposed != 0, &rp, &z_issued)) {
+        rowphase_shape(*desc, transposed != 0, &rp, &z_issued) ||
+        quad_shape(*desc, transposed != 0, &q, &z_issued)) {
       PlanShape shape;
       if (!build_shape(*desc, true, 2, 128, &shape)) return HUGE2_ERR_INVALID_ARG;
       *nonzero_macs = shape.nonzero_macs;

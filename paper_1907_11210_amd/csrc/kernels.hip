@@ -1201,6 +1201,288 @@ hipError_t launch_rowphase(const RpArgs& a, hipStream_t stream) {
 }
 
 // ---------------------------------------------------------------------------
+// Stride-2 transposed conv with a 4x4 kernel and padding 1 (NCHW, bf16), the
+// DCGAN/cGAN generator layer.  Each of its four output phases has 2x2 taps
+// whose input offsets lie in [-1, 1], and each phase's pixel grid is the
+// input grid (section 3.1).  A workgroup takes 64 input positions (ni images
+// x qbh rows x the full width) and 32*nch output channels, and computes the
+// four phases there:
+//  - per 64-channel K block, the input block plus a one-pixel halo is read
+//    straight from the NCHW planes into an LDS tile of channel-contiguous
+//    pixel rows: a thread loads one pixel pair of 8 channels (8 dword loads,
+//    coalesced along the pixels), regroups the halves with byte permutes and
+//    writes each pixel's 8 channels with one 16-byte store.  The four phases
+//    and their taps all read that one tile, so there is one barrier per K
+//    block rather than one per tap, and no separate re-layout pass;
+//  - wave (phase, K group or channel block) runs its phase's GEMM over WCH
+//    32-channel blocks with the four taps as K stages (the untangled 1x1
+//    convolutions of section 3.2.1), the weights loaded straight into the
+//    MFMA lane layout, DEPTH taps ahead; with WCH = 2 each 16-byte pixel
+//    fragment read from LDS feeds two MFMAs;
+//  - the four phases' results are interleaved in LDS into whole output rows
+//    (the scatter of section 3.1) and written with 16-byte stores.
+// With two K groups, group 1 hands its partial sums to group 0 through LDS in
+// a fixed order (deterministic).
+template <int KS, int WCH, int DEPTH>
+__global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
+  constexpr int NT = kQuadThreads;
+  constexpr int NTG = NT / KS;  // threads of one K group
+  constexpr int RB = kQuadRowB;
+  constexpr int HALO_B = kQuadHaloRows * RB;
+  constexpr int MAXP = kQuadMaxPieces;
+  constexpr uint32_t OOB = 0x80000000u;
+  static_assert(DEPTH == 2 || DEPTH == 4 || DEPTH == 8, "weight stages in flight");
+  static_assert(KS == 2 || WCH == 1, "one K group: two waves of 32 channels per phase");
+  constexpr int U = DEPTH > 4 ? DEPTH / 4 : 1;  // K blocks per unrolled loop step
+  __shared__ __attribute__((aligned(16))) char smem[KS * 2 * HALO_B];
+  __shared__ float s_bias[64];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int rho = wave & 3, rest = wave >> 2;
+  const int grp = KS > 1 ? rest : 0, hc = KS > 1 ? 0 : rest;
+  const int tg = tid - grp * NTG;  // thread index within the K group
+  const int bn = 32 * a.nch;
+  // output-channel tile slowest: each XCD's contiguous run of workgroups
+  // shares one weight slice
+  const int work = xcd_remap(blockIdx.x, gridDim.x);
+  const int nsp = a.igroups * a.hblocks;
+  const int ntile = work / nsp, sp = work - ntile * nsp;
+  const int ig = sp / a.hblocks, hb = sp - ig * a.hblocks;
+  const int img0 = ig * a.ni, qh0 = hb * a.qbh, n0 = ntile * bn;
+  const int hww = a.w + 2, hrows = a.qbh + 2;  // halo tile: width, rows per image
+  const uint32_t plane_b = (uint32_t)a.h * (uint32_t)a.w * 2u;
+
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc((void*)a.x, 0, a.x_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc((void*)a.wp, 0, a.wp_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t wr0 = __builtin_amdgcn_make_buffer_rsrc((void*)a.wp, 0, 0, 0x00020000);
+
+  // zero halo tiles: the halo ring, rows outside the image and images past
+  // the batch are never written afterwards
+  for (int e = tid; e < KS * 2 * HALO_B / 16; e += NT) ((uint4*)smem)[e] = make_uint4(0, 0, 0, 0);
+  // the bias is needed in the epilogue only: its load is not waited for here
+  const float bias_r = (a.bias && tid < bn && n0 + tid < a.cout) ? a.bias[n0 + tid] : 0.f;
+
+  // This thread's input items of a K block: item = (pixel pair, group of 8
+  // channels), pixel pairs fastest.  The loaded rows are [r0, r1) of each
+  // image (the block's rows plus the halo rows inside the image); w is even,
+  // so a pair never straddles a row.
+  const int r0 = max(0, qh0 - 1), r1 = min(a.h, qh0 + a.qbh + 1);
+  const int rows = r1 - r0;
+  const int npairs = a.ni * rows * a.w / 2;
+  const int itotal = npairs * 8;
+  uint32_t p_src[MAXP];
+  int p_lds[MAXP];
+#pragma unroll
+  for (int j = 0; j < MAXP; ++j) {
+    const int it = tg + NTG * j;
+    const int g = it / max(npairs, 1), pp = it - g * npairs;
+    const int px = 2 * pp, per_img = rows * a.w;
+    const int il = px / per_img, rem = px - il * per_img;
+    const int pr = rem / a.w, col = rem - pr * a.w;
+    const bool ok = it < itotal && img0 + il < a.n;
+    p_src[j] = ok ? ((((uint32_t)(img0 + il) * (uint32_t)a.cin + 8u * g) * (uint32_t)a.h + (uint32_t)(r0 + pr)) *
+                         (uint32_t)a.w + (uint32_t)col) * 2u
+                  : OOB;
+    p_lds[j] = ok ? ((il * hrows + r0 + pr - qh0 + 1) * hww + col + 1) * RB + g * 16 : -1;
+  }
+  auto load_pieces = [&](int cb, uint32_t (&P)[MAXP][8]) {
+    const uint32_t cbo = (uint32_t)cb * 64u * plane_b;
+#pragma unroll
+    for (int j = 0; j < MAXP; ++j) {
+      if (j * NTG >= itotal) break;  // the same for the whole group
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        P[j][k] = __builtin_amdgcn_raw_buffer_load_b32(xr, p_src[j], cbo + (uint32_t)k * plane_b, 0);
+    }
+  };
+  auto store_pieces = [&](char* tile, const uint32_t (&P)[MAXP][8]) {
+#pragma unroll
+    for (int j = 0; j < MAXP; ++j) {
+      if (j * NTG >= itotal) break;
+      if (p_lds[j] < 0) continue;
+      // P[j][k] holds channel 8g + k of the pixel pair: low half the first
+      // pixel, high half the second
+      uint32_t lo[4], hi[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        lo[e] = __builtin_amdgcn_perm(P[j][2 * e + 1], P[j][2 * e], 0x05040100u);
+        hi[e] = __builtin_amdgcn_perm(P[j][2 * e + 1], P[j][2 * e], 0x07060302u);
+      }
+      *(uint4*)(tile + p_lds[j]) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+      *(uint4*)(tile + p_lds[j] + RB) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+    }
+  };
+
+  // This wave's pixels: q = 32 i + lane % 32; LDS byte offset of its halo
+  // pixel at tap offset (0, 0), plus the lane half's 64 bytes of K.
+  int lrow[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int q = 32 * i + (lane & 31);
+    const int per_img = a.qbh * a.w;
+    const int il = q / per_img, qr = q - il * per_img;
+    const int qh = qr / a.w, qw = qr - qh * a.w;
+    lrow[i] = ((il * hrows + qh + 1) * hww + qw + 1) * RB + (lane >> 5) * 64;
+  }
+  int tdelta[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) tdelta[t] = (a.dh[rho][t] * hww + a.dw[rho][t]) * RB;
+
+  // weight stage (K block cb, tap t) of this wave's 32-channel blocks
+  const int ncb = a.cin / 64;
+  const int cbn = ncb / KS, cb_lo = grp * cbn;
+  const uint32_t kb32 = (uint32_t)(n0 / 32 + hc * WCH), nkb32 = (uint32_t)(a.cout_pad / 32);
+  auto load_w = [&](uint4 (&W)[WCH][4], bool valid, int cb, int t) {
+    const __amdgpu_buffer_rsrc_t ws = valid ? wr : wr0;
+#pragma unroll
+    for (int j = 0; j < WCH; ++j) {
+      const uint32_t base =
+          (((uint32_t)a.slot[rho][t] * nkb32 + kb32 + j) * (uint32_t)ncb + (uint32_t)cb) * 4096u;
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        W[j][c] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(ws, lane * 16, base + 1024u * c, 0));
+    }
+  };
+
+  f32x16 acc[WCH][2];
+#pragma unroll
+  for (int j = 0; j < WCH; ++j)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[j][i][r] = 0.f;
+  auto compute = [&](const char* tile, int t, const uint4 (&W)[WCH][4]) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const bf16x8 f0 = __builtin_bit_cast(bf16x8, *(const uint4*)(tile + lrow[0] + tdelta[t] + 16 * c));
+      const bf16x8 f1 = __builtin_bit_cast(bf16x8, *(const uint4*)(tile + lrow[1] + tdelta[t] + 16 * c));
+#pragma unroll
+      for (int j = 0; j < WCH; ++j) {
+        const bf16x8 wv = __builtin_bit_cast(bf16x8, W[j][c]);
+        acc[j][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv, f0, acc[j][0], 0, 0, 0);
+        acc[j][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv, f1, acc[j][1], 0, 0, 0);
+      }
+    }
+  };
+
+  __syncthreads();  // halo tiles zeroed
+  char* const tiles = smem + grp * 2 * HALO_B;
+  uint32_t P[MAXP][8];
+  uint4 W[DEPTH][WCH][4];
+  load_pieces(cb_lo, P);
+#pragma unroll
+  for (int d = 0; d < DEPTH; ++d) load_w(W[d], d / 4 < cbn, cb_lo + min(d / 4, cbn - 1), d % 4);
+  store_pieces(tiles, P);
+  __syncthreads();
+  if (cbn > 1) load_pieces(cb_lo + 1, P);
+  for (int cb0 = 0; cb0 < cbn; cb0 += U) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int cbi = cb0 + u;
+      if (U > 1 && cbi >= cbn) break;  // the same for the whole workgroup
+      const char* tile = tiles + (cbi & 1) * HALO_B;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        compute(tile, t, W[(4 * u + t) % DEPTH]);
+        // the stage DEPTH taps later goes into the buffer just consumed,
+        // issued here (not sunk below later taps' MFMAs by the scheduler)
+        const int nb = cbi + (t + DEPTH) / 4;
+        __builtin_amdgcn_sched_barrier(0);
+        load_w(W[(4 * u + t) % DEPTH], nb < cbn, cb_lo + min(nb, cbn - 1), (t + DEPTH) % 4);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (cbi + 1 < cbn) store_pieces(tiles + ((cbi + 1) & 1) * HALO_B, P);
+      __syncthreads();
+      if (cbi + 2 < cbn) load_pieces(cb_lo + cbi + 2, P);
+    }
+  }
+
+  if constexpr (KS > 1) {
+    // group 1's partial sums to LDS (lane-contiguous), group 0 adds them
+    float* red = (float*)smem + rho * (WCH * 2 * 16 * 64) + lane;
+    if (grp == 1) {
+#pragma unroll
+      for (int j = 0; j < WCH; ++j)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) red[((j * 2 + i) * 16 + r) * 64] = acc[j][i][r];
+    }
+    __syncthreads();
+    if (grp == 0) {
+#pragma unroll
+      for (int j = 0; j < WCH; ++j)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[j][i][r] += red[((j * 2 + i) * 16 + r) * 64];
+    }
+    __syncthreads();
+  }
+
+  // Interleave the phases in LDS: [channel][image][output row][output column]
+  // of the workgroup's output block (2 qbh rows x 2w columns per image).
+  const int obw = 2 * a.w, obh = 2 * a.qbh;
+  const int cpo = a.ni * obh * obw + 8;  // elements per channel, 16-byte pad
+  uint16_t* so = (uint16_t*)smem;
+  if (tid < 64) s_bias[tid] = bias_r;
+  __syncthreads();
+  if (grp == 0) {
+    const int rho_h = rho >> 1, rho_w = rho & 1;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int q = 32 * i + (lane & 31);
+      const int per_img = a.qbh * a.w;
+      const int il = q / per_img, qr = q - il * per_img;
+      const int qh = qr / a.w, qw = qr - qh * a.w;
+      const int pos = (il * obh + 2 * qh + rho_h) * obw + 2 * qw + rho_w;
+#pragma unroll
+      for (int j = 0; j < WCH; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int ch = (hc * WCH + j) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          so[ch * cpo + pos] = f32_to_bf16_rne(acc[j][i][r] + s_bias[ch]);
+        }
+    }
+  }
+  __syncthreads();
+  // Whole output rows: per (channel, image) the rows [2 qh0, 2 qh0 + obh)
+  // are one contiguous run of obh * obw elements in y.
+  const int run8 = obh * obw / 8;
+  const int total = bn * a.ni * run8;
+  const size_t plane_o = (size_t)(2 * a.h) * (size_t)obw;
+  for (int e = tid; e < total; e += NT) {
+    const int k8 = e % run8, t2 = e / run8;
+    const int il = t2 % a.ni, ch = t2 / a.ni;
+    if (n0 + ch >= a.cout || img0 + il >= a.n) continue;
+    const uint4 v = *(const uint4*)(so + ch * cpo + il * obh * obw + 8 * k8);
+    uint16_t* dst = (uint16_t*)a.y + ((size_t)(img0 + il) * a.cout + n0 + ch) * plane_o +
+                    (size_t)(2 * qh0) * obw + 8 * k8;
+    *(uint4*)dst = v;
+  }
+}
+
+hipError_t launch_quad(const QArgs& a, hipStream_t stream) {
+  const dim3 grid(a.ntiles * a.igroups * a.hblocks);
+#define HUGE2_QUAD_LAUNCH(KS_, WCH_, D_) \
+  hipLaunchKernelGGL((quad_kernel<KS_, WCH_, D_>), grid, dim3(kQuadThreads), 0, stream, a)
+  if (a.ks == 2 && a.nch == 2) {
+    HUGE2_QUAD_LAUNCH(2, 2, 2);  // both channel blocks per wave: two stages fit the registers
+  } else if (a.ks == 2) {
+    if (a.depth == 2) HUGE2_QUAD_LAUNCH(2, 1, 2);
+    else if (a.depth == 4) HUGE2_QUAD_LAUNCH(2, 1, 4);
+    else HUGE2_QUAD_LAUNCH(2, 1, 8);
+  } else {
+    if (a.depth == 2) HUGE2_QUAD_LAUNCH(1, 1, 2);
+    else if (a.depth == 4) HUGE2_QUAD_LAUNCH(1, 1, 4);
+    else HUGE2_QUAD_LAUNCH(1, 1, 8);
+  }
+#undef HUGE2_QUAD_LAUNCH
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Weight packing: element (slot, k, c) = w at kernel tap slot = (kh, kw),
 // output channel k, input channel c.
 //   lane_kb = 0: K-contiguous rows, wp[slot][k][c].

@@ -122,6 +122,7 @@ constexpr TileShape kTiles[] = {
     {128, 128, 4, 2, 256, 2, 1, 0},     // 31 as 8 with 256-byte K stages
     {128, 256, 1, 8, 128, 3, 1, 1, 1},  // 32 split-wave: 8 waves of 128 x 32 channels
     {128, 256, 1, 8, 128, 2, 2, 1, 1},  // 33 as 32, two stages in flight
+    {128, 128, 1, 4, 128, 4, 1, 1, 2},  // 34 as 27, four stages in flight
 };
 constexpr int kComputeUnits = 256;  // MI355X
 constexpr int TILE_COUNT = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
@@ -211,6 +212,37 @@ struct RpArgs {
   int nq;       // q_w slots per column phase in LDS (stride_w * nq a multiple of 8)
 };
 hipError_t launch_rowphase(const RpArgs& a, hipStream_t stream);
+
+// All four phases per workgroup for the stride-2, 4x4, padding-1 transposed
+// conv (NCHW, bf16): every phase has 2 x 2 taps with input offsets in
+// [-1, 1] and the input's pixel grid.  Workgroup: 64 input positions (ni
+// images x qbh rows x the full width w) x 32*nch output channels, 8 waves.
+// Weights in the lane order of 128-byte K stages (pack_weights_kernel with
+// lane_kb = 128).
+constexpr int kQuadThreads = 512;
+constexpr int kQuadPix = 64;         // input positions per workgroup
+constexpr int kQuadRowB = 144;       // LDS bytes per halo pixel: 64 channels + 16-byte pad
+constexpr int kQuadHaloRows = 200;   // halo pixels per LDS tile: ni * (qbh + 2) * (w + 2)
+constexpr int kQuadMaxPieces = 2;    // input items (pixel pair x 8 channels) per thread and K block
+struct QArgs {
+  const void* x;     // NCHW input
+  const void* wp;    // packed weights [slot][cout_pad/32][cin/64][4][64 lanes][16 bytes]
+  const float* bias;
+  void* y;           // NCHW output, 2h x 2w
+  uint32_t x_bytes, wp_bytes;
+  int n, cin, h, w, cout, cout_pad;
+  int ni, qbh;       // images and input rows per workgroup (ni * qbh * w = 64)
+  // 32-channel blocks and K groups per workgroup; the 8 waves are 4 phases x
+  // (nch = 2, ks = 1: a 32-channel block each | nch = 1, ks = 2: a K group
+  // each | nch = 2, ks = 2: a K group each, both 32-channel blocks per wave)
+  int nch, ks;
+  int igroups, hblocks, ntiles;  // grid = ntiles x igroups x hblocks
+  int depth;         // weight stages in flight (2, 4 or 8)
+  // per phase (2 * rho_h + rho_w) and tap (2 * th + tw): weight slot kh*4+kw
+  // and input offsets: output (2q_h + rho_h, 2q_w + rho_w) reads input q + (dh, dw)
+  int8_t slot[4][4], dh[4][4], dw[4][4];
+};
+hipError_t launch_quad(const QArgs& a, hipStream_t stream);
 
 // Re-layout the input into [n][h*w][c_stride] with zero channel padding.
 // nchw: source is NCHW; otherwise NHWC with cin channels per pixel.

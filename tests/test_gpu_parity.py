@@ -57,6 +57,13 @@ SMALL = [
     L("ct_rowphase_s4", True, 2, 20, 5, 8, 9, 6, 6, 4, 1, 0, 1, "NCHW", "bf16"),
     L("ct_rowphase_zerotap", True, 1, 4, 3, 8, 3, 6, 6, 8, 3, 0, 1, "NCHW", "bf16"),
     L("ct_rowphase_c32", True, 1, 32, 4, 4, 32, 8, 8, 4, 2, 0, 1, "NCHW", "bf16"),
+    # stride 2, 4x4, padding 1, NCHW bf16: the all-phase form
+    L("ct_quad_img8", True, 2, 64, 8, 8, 64, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
+    L("ct_quad_img4_ragged", True, 5, 64, 4, 4, 40, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
+    L("ct_quad_two_kgroups", True, 3, 128, 8, 8, 32, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
+    L("ct_quad_rows16", True, 2, 192, 16, 16, 96, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
+    L("ct_quad_w32", True, 1, 64, 8, 32, 32, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
+    L("ct_quad_w64", True, 1, 64, 4, 64, 32, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
 ]
 
 
@@ -369,3 +376,27 @@ def test_large_stride_forms(rowphase, monkeypatch):
         name = plan.kernel
         plan.close()
         assert name.startswith("rowphase_kernel") == bool(rowphase), (layer.name, name)
+
+
+
+QUAD = [l for l in SMALL if l.name.startswith("ct_quad")]
+
+
+@pytest.mark.parametrize("quad,wch", [(0, 1), (1, 1), (1, 2)])
+@pytest.mark.parametrize("layer", QUAD, ids=lambda l: l.name)
+def test_all_phase_forms(layer, quad, wch, monkeypatch):
+    """The all-phase kernel (both wave layouts) and the phase GEMM it replaces
+    all match the oracle."""
+    monkeypatch.setenv("HUGE2_QUAD", str(quad))
+    monkeypatch.setenv("HUGE2_QUAD_WCH", str(wch))
+    P.say("case", layer, "HUGE2_QUAD", quad, "HUGE2_QUAD_WCH", wch)
+    xq, wq = _inputs(layer, seed=11)
+    bias = torch.linspace(-1.0, 1.0, layer.c_out)
+    y = P.run_gpu(layer, xq, wq, bias)
+    P.check(y, P.oracle_full(layer, xq, wq, bias), P.oracle_full(layer, xq, wq, bias, absolute=True),
+            layer.dtype, layer.name)
+    plan = P.make_plan(layer, wq.contiguous().to(torch.device("cuda", 0)))
+    try:
+        assert ("quad_kernel" in plan.kernel) == bool(quad), plan.kernel
+    finally:
+        plan.close()

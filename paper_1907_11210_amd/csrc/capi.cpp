@@ -200,57 +200,55 @@ int64_t makespan_stages(const huge2_conv_desc& d, const PlanShape& shape, int cf
 int floor_div_i(int a, int b) { return a >= 0 ? a / b : -((-a + b - 1) / b); }
 int ceil_div_i(int a, int b) { return -floor_div_i(-a, b); }
 
-// Channel pitch of the all-taps tile, in elements: an odd multiple of the
-// 16-byte vector, so that the two lane halves of an MFMA fragment (channels
-// 8 apart) read disjoint halves of the LDS banks.
-int cpitch_of(int elems, int ve) {
-  int c = round_up(elems, ve);
-  if ((c / ve) % 2 == 0) c += ve;
-  return c;
-}
-
-// The all-taps form (ztile_kernel) applies to NCHW transposed convs whose
-// taps x output channels fit one 64-column MFMA tile, with 16-byte input rows
-// strides up to 4, at most 4 taps of an axis reaching one output phase and
-// output rows of at most 256 columns.
+// The all-taps form (ztile_kernel) applies to NCHW bf16 transposed convs
+// whose taps x output channels fit one 64-column MFMA tile, with an even input
+// width, strides up to 4, at most 4 taps of an axis reaching one output phase
+// and output rows of at most 256 columns.
 // The block of output rows per workgroup is the largest multiple of the
-// stride whose input tile fits the LDS budget while the grid still has one
-// workgroup per CU; small problems take the smallest block that fits.
+// stride whose input tile fits the LDS budget while the grid still has two
+// workgroups per CU (else one); small problems take the largest block that
+// fits.
 // Returns false when the form does not apply (or HUGE2_ZTILE=0, or a GEMM
 // tile is forced through HUGE2_TILE).
 bool ztile_shape(const huge2_conv_desc& d, bool transposed, ZArgs* z, int64_t* issued) {
   // bf16 only: in fp32 the phase GEMM measured faster
   if (!transposed || d.layout != HUGE2_NCHW || d.dtype != HUGE2_BF16) return false;
   if (env_int("HUGE2_ZTILE", 1) == 0 || env_int("HUGE2_TILE", -1) >= 0) return false;
-  const int esz = elem_size(d.dtype), ve = 16 / esz;
-  if ((long long)d.c_out * d.r * d.s > 64 || d.w % ve != 0) return false;
+  if ((long long)d.c_out * d.r * d.s > 64 || d.w % 2 != 0) return false;
   if (d.stride_h > kZtileMaxStride || d.stride_w > kZtileMaxStride || d.r > kZtileMaxTaps ||
       d.s > kZtileMaxTaps || d.dil_h > 16 || d.dil_w > 16)
     return false;
   int ho, wo;
   if (!output_dims(d, true, &ho, &wo)) return false;
-  const int j_lo = ceil_div_i(d.pad_w - (d.s - 1) * d.dil_w, d.stride_w);
-  const int j_hi = floor_div_i(wo - 1 + d.pad_w, d.stride_w);
-  if (j_lo < -kZtileColOff || wo > 256) return false;
+  const long long x_bytes = (long long)d.n * d.c_in * d.h * d.w * 2;
+  if (x_bytes >= (1ll << 31) || wo > 256) return false;
+  // tile columns: every input column an output reads, and every input column
+  const int j_lo = std::min(0, ceil_div_i(d.pad_w - (d.s - 1) * d.dil_w, d.stride_w));
+  const int j_hi = std::max(d.w - 1, floor_div_i(wo - 1 + d.pad_w, d.stride_w));
   const int tcw = j_hi - j_lo + 1;
-  const int tcp = round_up(std::max(j_hi, d.w - 1) + kZtileColOff + 1, ve);
-  const int cchunk = esz == 2 ? 64 : 32;
-  const int cin_pad = round_up(d.c_in, cchunk);
+  const int cin_pad = round_up(d.c_in, 64);
   const int i_off = ceil_div_i(d.pad_h - (d.r - 1) * d.dil_h, d.stride_h);
-  int best = -1, fallback = -1;
+  // output rows per workgroup: the tile (and its Z) must fit, and the input
+  // items of a pass must fit the threads; prefer two workgroups per compute
+  // unit, then one
+  int best2 = -1, best1 = -1, fallback = -1;
   for (int q = (ho + d.stride_h - 1) / d.stride_h; q >= 1; --q) {
     const int ob = std::min(q * d.stride_h, ho);
     const int tr = floor_div_i(ob - 1 + d.pad_h, d.stride_h) - i_off + 1;
     const long long np = (long long)tr * tcw;
     if (np > kZtileMaxPixels) continue;
-    if ((long long)cin_pad * cpitch_of(tr * tcp, ve) * esz > kZtileLds) continue;
+    if ((long long)std::min(tr, d.h) * d.w * 4 > (long long)kZtileMaxItems * kZtileThreads) continue;
     const long long blocks = (long long)d.n * ((ho + ob - 1) / ob);
-    fallback = ob;
-    if (best < 0 && blocks >= kComputeUnits) best = ob;
+    if (fallback < 0) fallback = ob;
+    if (best1 < 0 && blocks >= kComputeUnits) best1 = ob;
+    if (best2 < 0 && blocks >= 2 * kComputeUnits) best2 = ob;
   }
-  const int ob = best >= 0 ? best : fallback;
+  // two workgroups share a compute unit only if their LDS fits twice
+  const bool two_per_cu = 2 * kZtileLds <= 160 * 1024;
+  const int ob = (two_per_cu && best2 >= 0) ? best2 : best1 >= 0 ? best1 : fallback;
   if (ob < 0) return false;
   std::memset(z, 0, sizeof(*z));
+  z->x_bytes = (uint32_t)x_bytes;
   z->n = d.n;
   z->cin = d.c_in;
   z->h = d.h;
@@ -271,10 +269,8 @@ bool ztile_shape(const huge2_conv_desc& d, bool transposed, ZArgs* z, int64_t* i
   z->ob = ob;
   z->tr = floor_div_i(ob - 1 + d.pad_h, d.stride_h) - i_off + 1;
   z->tcw = tcw;
-  z->tcp = tcp;
-  z->cpitch = cpitch_of(z->tr * tcp, ve);
   z->j_lo = j_lo;
-  z->cchunk = cchunk;
+  z->cchunk = 64;
   // per-phase tap tables: output o with o + pad = stride*Q + rho reads input
   // Q + delta through kernel tap k when rho - k*dil = stride*delta
   const int strides[2] = {d.stride_h, d.stride_w}, ks[2] = {d.r, d.s}, dils[2] = {d.dil_h, d.dil_w};

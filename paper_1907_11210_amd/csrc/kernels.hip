@@ -758,7 +758,7 @@ hipError_t launch_phase_gemm(const GemmArgs& a, int dtype, int cfg, bool nchw_ou
 }
 
 // ---------------------------------------------------------------------------
-// Transposed conv with few output channels (c_out * r * s <= 64), NCHW.
+// Transposed conv with few output channels (c_out * r * s <= 64), NCHW, bf16.
 // The phase GEMM has N = c_out there, so its tiles are mostly padding and
 // every input pixel is fetched once per (phase, tap).  This kernel instead
 // keeps a block of input rows (full width, plus the halo its outputs need) in
@@ -767,24 +767,22 @@ hipError_t launch_phase_gemm(const GemmArgs& a, int dtype, int cfg, bool nchw_ou
 // (section 3.2.1's per-tap 1x1 convolutions, all taps in one GEMM), and then
 // forms each owned output as the sum of the Z entries of the input pixels and
 // taps that reach it (the interleaved scatter of section 3.1, read side).
-// Workgroup (image, block of OB output rows).  Input tile: rows [i_lo, i_hi],
-// columns [j_lo, j_hi] of the input, zero outside it; LDS column of input
-// column j is j + ZOFF (a multiple of the 16-byte vector).
+// Workgroup (image, block of OB output rows).  Input tile: rows [i_lo,
+// i_lo + tr) and columns [j_lo, j_lo + tcw) of the input, zero outside it,
+// stored channel-contiguous per pixel, 64 channels per pass (two LDS buffers:
+// the next pass loads while this one multiplies).  A thread loads one pixel
+// pair of 8 channels (8 dword loads, coalesced along the pixels) and writes
+// each pixel's 8 channels with one 16-byte store.
 __device__ __forceinline__ int floor_div_d(int a, int b) { return a >= 0 ? a / b : -((-a + b - 1) / b); }
 
-template <bool BF16>
 __global__ __launch_bounds__(kZtileThreads) void ztile_kernel(ZArgs a) {
-  using T = typename std::conditional<BF16, uint16_t, uint32_t>::type;
-  constexpr int ESZ = sizeof(T);
-  constexpr int VE = 16 / ESZ;
-  constexpr int PASS = BF16 ? 64 : 32;  // input channels per MFMA pass
-  constexpr int KSTEP = BF16 ? 16 : 2;  // K per MFMA
-  constexpr int NKS = PASS / KSTEP;
   constexpr int NT = kZtileThreads, NW = NT / 64;
-  constexpr int NLD = 12;               // 16-byte input loads per thread in flight
-  constexpr int MB_MAX = ((kZtileMaxPixels + 31) / 32 + NW - 1) / NW;  // M blocks per wave
+  constexpr int RB = kZtileRowB;
+  constexpr int BUF_B = kZtileMaxPixels * RB;
+  constexpr int MAXP = kZtileMaxItems;
+  constexpr int MB_MAX = (kZtileMaxPixels / 32 + NW - 1) / NW;  // M blocks per wave
+  constexpr uint32_t OOB = 0x80000000u;
   __shared__ __attribute__((aligned(16))) char zsm[kZtileLds];
-  T* tile = (T*)zsm;        // [cin_pad][cpitch]: per channel tr rows of tcp
   float* zs = (float*)zsm;  // [p][kZtileZPitch], after the GEMM
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
@@ -793,79 +791,99 @@ __global__ __launch_bounds__(kZtileThreads) void ztile_kernel(ZArgs a) {
   const int np = a.tr * a.tcw;
   const int mblocks = (np + 31) / 32;
   const int kx = a.r * a.s * a.cout;
-  const int plane = a.cpitch;  // elements per input channel (>= tr * tcp)
+  const uint32_t plane_b = (uint32_t)a.h * (uint32_t)a.w * 2u;
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc((void*)a.x, 0, a.x_bytes, 0x00020000);
+  const uint32_t wp_bytes = (uint32_t)(a.r * a.s * a.cout_pad) * (uint32_t)a.cin_pad * 2u;
+  const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc((void*)a.wp, 0, wp_bytes, 0x00020000);
 
-  // weight fragments of one pass: column col = nb*32 + lane%32 = tap*cout + k
-  auto load_w = [&](int c0, uint4 (&bfr)[NKS][2], float (&bf32)[NKS][2]) {
+  // weight fragments of one 64-channel pass, K permuted like the input tile
+  // reads below: MFMA step t, lane half h takes channels c0 + 32h + 8t ..+8;
+  // column col = nb*32 + lane%32 = tap*cout + k.  Branch-free: columns past
+  // the taps read zeros (out-of-range offset).
+  uint32_t w_off[2];
 #pragma unroll
-    for (int t = 0; t < NKS; ++t)
+  for (int nb = 0; nb < 2; ++nb) {
+    const int col = nb * 32 + (lane & 31);
+    const int tap = col / a.cout, k = col - tap * a.cout;
+    w_off[nb] = col < kx ? ((uint32_t)(tap * a.cout_pad + k) * (uint32_t)a.cin_pad + 32u * (lane >> 5)) * 2u
+                         : OOB;
+  }
+  auto load_w = [&](int c0, uint4 (&bfr)[4][2]) {
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb) {
-        const int col = nb * 32 + (lane & 31);
-        const int tap = col / a.cout, k = col - tap * a.cout;
-        const int c = c0 + t * KSTEP + (lane >> 5) * (KSTEP / 2);
-        const bool ok = col < kx && c < a.cin_pad;
-        const size_t widx = ((size_t)tap * a.cout_pad + k) * a.cin_pad + c;
-        if constexpr (BF16)
-          bfr[t][nb] = ok ? *(const uint4*)((const T*)a.wp + widx) : make_uint4(0, 0, 0, 0);
-        else
-          bf32[t][nb] = ok ? ((const float*)a.wp)[widx] : 0.f;
-      }
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+        bfr[t][nb] = __builtin_bit_cast(
+            uint4, __builtin_amdgcn_raw_buffer_load_b128(wr, w_off[nb], (uint32_t)(c0 + 8 * t) * 2u, 0));
   };
-  uint4 bfr[NKS][2];
-  float bf32[NKS][2];
-  load_w(0, bfr, bf32);
-  // tap tables and bias for the final combine (read here, long before use;
-  // the barrier after the input loads publishes them)
+  uint4 bfr[4][2];
+  load_w(0, bfr);
+  // tap tables and bias for the final combine: read now into registers,
+  // staged in LDS only before the combine, so nothing waits for them here
   __shared__ int8_t s_tap[3][2][kZtileMaxStride][kZtileMaxTaps];
   __shared__ int8_t s_tapn[2][kZtileMaxStride];
   __shared__ float s_zb[64];
-  if (tid < 64) s_zb[tid] = (a.bias && tid < a.cout) ? a.bias[tid] : 0.f;
-  for (int e = tid; e < 2 * kZtileMaxStride * kZtileMaxTaps; e += NT) {
-    const int ax = e / (kZtileMaxStride * kZtileMaxTaps), rem = e % (kZtileMaxStride * kZtileMaxTaps);
+  constexpr int NTAB = 2 * kZtileMaxStride * kZtileMaxTaps;
+  static_assert(NTAB <= NT, "one tap-table entry per thread");
+  const float zb_r = (a.bias && tid < a.cout) ? a.bias[tid] : 0.f;
+  int8_t tk_r = 0, td_r = 0, tn_r = 0;
+  if (tid < NTAB) {
+    const int ax = tid / (kZtileMaxStride * kZtileMaxTaps), rem = tid % (kZtileMaxStride * kZtileMaxTaps);
     const int rho = rem / kZtileMaxTaps, t = rem % kZtileMaxTaps;
-    s_tap[0][ax][rho][t] = a.tap_k[ax][rho][t];
-    s_tap[1][ax][rho][t] = a.tap_d[ax][rho][t];
-    if (t == 0) s_tapn[ax][rho] = a.tap_n[ax][rho];
+    tk_r = a.tap_k[ax][rho][t];
+    td_r = a.tap_d[ax][rho][t];
+    tn_r = a.tap_n[ax][rho];
   }
+  // zero both tile buffers: halo columns and rows outside the input stay zero
+  for (int e = tid; e < 2 * BUF_B / 16; e += NT) ((uint4*)zsm)[e] = make_uint4(0, 0, 0, 0);
 
-  // zero the halo columns of every tile row (LDS columns outside the input)
-  const int nrows = a.cin_pad * a.tr;
-  const int right = a.tcp - kZtileColOff - a.w;  // elements, a multiple of VE
-  for (int rr = tid; rr < nrows; rr += NT) {
-    const int cc = rr / a.tr;
-    T* row = tile + cc * plane + (rr - cc * a.tr) * a.tcp;
-    *(uint4*)row = make_uint4(0, 0, 0, 0);  // kZtileColOff == VE (bf16) or 2 VE (fp32)
-    if (kZtileColOff > VE) *(uint4*)(row + VE) = make_uint4(0, 0, 0, 0);
-    for (int c = 0; c < right; c += VE)
-      *(uint4*)(row + kZtileColOff + a.w + c) = make_uint4(0, 0, 0, 0);
+  // This thread's input items of a pass: (pixel pair, 8-channel group), pairs
+  // fastest, over the tile rows inside the input and the full input width
+  // (w is even, so a pair never straddles a row).
+  const int ir0 = max(0, i_lo), ir1 = min(a.h, i_lo + a.tr);
+  const int npairs = max(0, ir1 - ir0) * a.w / 2;
+  const int itotal = npairs * 8;
+  uint32_t p_src[MAXP];
+  int p_lds[MAXP];
+#pragma unroll
+  for (int j = 0; j < MAXP; ++j) {
+    const int it = tid + NT * j;
+    const int g = it / max(npairs, 1), pp = it - g * npairs;
+    const int rr = (2 * pp) / a.w, col = 2 * pp - rr * a.w;
+    const bool ok = it < itotal;
+    p_src[j] = ok ? ((((uint32_t)img * (uint32_t)a.cin + 8u * g) * (uint32_t)a.h + (uint32_t)(ir0 + rr)) *
+                         (uint32_t)a.w + (uint32_t)col) * 2u
+                  : OOB;
+    p_lds[j] = ok ? ((ir0 + rr - i_lo) * a.tcw + col - a.j_lo) * RB + 16 * g : -1;
   }
-  // every input row of the tile, all channels: 16-byte pieces, zero outside
-  const int vec_per_row = a.w / VE;
-  const int total_vec = nrows * vec_per_row;
-  for (int e0 = 0; e0 < total_vec; e0 += NT * NLD) {
-    uint4 val[NLD];
+  auto load_items = [&](int c0, uint32_t (&P)[MAXP][8]) {
+    const uint32_t cbo = (uint32_t)c0 * plane_b;
 #pragma unroll
-    for (int l = 0; l < NLD; ++l) {
-      const int e = e0 + tid + NT * l;
-      const int rr = e / vec_per_row, v = e - rr * vec_per_row;
-      const int cc = rr / a.tr, tr = rr - cc * a.tr;
-      const int i = i_lo + tr;
-      val[l] = make_uint4(0, 0, 0, 0);
-      if (e < total_vec && cc < a.cin && i >= 0 && i < a.h)
-        val[l] = *(const uint4*)((const T*)a.x + (((size_t)img * a.cin + cc) * a.h + i) * a.w + v * VE);
-    }
+    for (int j = 0; j < MAXP; ++j) {
+      if (j * NT >= itotal) break;  // the same for the whole workgroup
 #pragma unroll
-    for (int l = 0; l < NLD; ++l) {
-      const int e = e0 + tid + NT * l;
-      if (e < total_vec) {
-        const int rr = e / vec_per_row, v = e - rr * vec_per_row;
-        const int cc = rr / a.tr, tr = rr - cc * a.tr;
-        *(uint4*)(tile + cc * plane + tr * a.tcp + kZtileColOff + v * VE) = val[l];
+      for (int k = 0; k < 8; ++k) {
+        // channels past c_in read zeros (out-of-range offset)
+        const bool in = c0 + 8 * ((tid + NT * j) / max(npairs, 1)) + k < a.cin;
+        P[j][k] = __builtin_amdgcn_raw_buffer_load_b32(xr, in ? p_src[j] : OOB, cbo + (uint32_t)k * plane_b, 0);
       }
     }
-  }
-  __syncthreads();
+  };
+  auto store_items = [&](char* buf, const uint32_t (&P)[MAXP][8]) {
+#pragma unroll
+    for (int j = 0; j < MAXP; ++j) {
+      if (j * NT >= itotal) break;
+      if (p_lds[j] < 0) continue;
+      uint32_t lo[4], hi[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        lo[e] = __builtin_amdgcn_perm(P[j][2 * e + 1], P[j][2 * e], 0x05040100u);
+        hi[e] = __builtin_amdgcn_perm(P[j][2 * e + 1], P[j][2 * e], 0x07060302u);
+      }
+      *(uint4*)(buf + p_lds[j]) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+      *(uint4*)(buf + p_lds[j] + RB) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+    }
+  };
 
   f32x16 acc[MB_MAX][2];
 #pragma unroll
@@ -874,70 +892,64 @@ __global__ __launch_bounds__(kZtileThreads) void ztile_kernel(ZArgs a) {
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
-  // pixel (tile row, column) of each of this wave's M-block rows
+  // LDS byte offset of each of this wave's M-block rows (pixels past np
+  // repeat the last one: their Z rows are never read)
   int src_off[MB_MAX];
 #pragma unroll
-  for (int mi = 0; mi < MB_MAX; ++mi) {
-    const int p = min((wave + NW * mi) * 32 + (lane & 31), np - 1);
-    const int tr = p / a.tcw, tc = p - tr * a.tcw;
-    src_off[mi] = tr * a.tcp + tc + a.j_lo + kZtileColOff;
-  }
-  // Z = X^T W over all input channels, one pass of PASS channels at a time;
-  // the next pass's weights load while this one computes
-  for (int c0 = 0; c0 < a.cin_pad; c0 += PASS) {
-    uint4 nbfr[NKS][2];
-    float nbf32[NKS][2];
-    if (c0 + PASS < a.cin_pad) load_w(c0 + PASS, nbfr, nbf32);
+  for (int mi = 0; mi < MB_MAX; ++mi)
+    src_off[mi] = min((wave + NW * mi) * 32 + (lane & 31), np - 1) * RB + (lane >> 5) * 64;
+
+  __syncthreads();  // tiles zeroed
+  uint32_t P[MAXP][8];
+  load_items(0, P);
+  store_items(zsm, P);
+  __syncthreads();
+  const int npass = a.cin_pad / 64;
+  if (npass > 1) load_items(64, P);
+  for (int pass = 0; pass < npass; ++pass) {
+    const char* buf = zsm + (pass & 1) * BUF_B;
 #pragma unroll
     for (int mi = 0; mi < MB_MAX; ++mi) {
       if (wave + NW * mi >= mblocks) break;
-      const T* src = tile + src_off[mi];
 #pragma unroll
-      for (int t = 0; t < NKS; ++t) {
-        const int cc = c0 + t * KSTEP + (lane >> 5) * (KSTEP / 2);
-        if constexpr (BF16) {
-          uint32_t wv[4];
+      for (int t = 0; t < 4; ++t) {
+        const bf16x8 av = __builtin_bit_cast(bf16x8, *(const uint4*)(buf + src_off[mi] + 16 * t));
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            wv[e] = (uint32_t)src[(cc + 2 * e) * plane] |
-                    ((uint32_t)src[(cc + 2 * e + 1) * plane] << 16);
-          const bf16x8 av = __builtin_bit_cast(bf16x8, make_uint4(wv[0], wv[1], wv[2], wv[3]));
-#pragma unroll
-          for (int nb = 0; nb < 2; ++nb)
-            acc[mi][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                av, __builtin_bit_cast(bf16x8, bfr[t][nb]), acc[mi][nb], 0, 0, 0);
-        } else {
-          const float av = __uint_as_float(src[cc * plane]);
-#pragma unroll
-          for (int nb = 0; nb < 2; ++nb)
-            acc[mi][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av, bf32[t][nb], acc[mi][nb], 0, 0, 0);
-        }
+        for (int nb = 0; nb < 2; ++nb)
+          acc[mi][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, __builtin_bit_cast(bf16x8, bfr[t][nb]),
+                                                                acc[mi][nb], 0, 0, 0);
       }
     }
-    if (c0 + PASS < a.cin_pad) {
-#pragma unroll
-      for (int t = 0; t < NKS; ++t)
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
-          bfr[t][nb] = nbfr[t][nb];
-          bf32[t][nb] = nbf32[t][nb];
-        }
-    }
+    // the next pass's weights into the registers just consumed
+    __builtin_amdgcn_sched_barrier(0);
+    if (pass + 1 < npass) load_w(64 * (pass + 1), bfr);
+    __builtin_amdgcn_sched_barrier(0);
+    if (pass + 1 < npass) store_items(zsm + ((pass + 1) & 1) * BUF_B, P);
+    __syncthreads();
+    if (pass + 2 < npass) load_items(64 * (pass + 2), P);
   }
-  __syncthreads();
-  // Z to LDS: lane holds column lane%32 of rows 8*(q/4) + 4*(lane/32) + q%4
+  // Z to LDS (over the tile buffers): lane holds column lane%32 of rows
+  // 8*(q/4) + 4*(lane/32) + q%4
 #pragma unroll
   for (int mi = 0; mi < MB_MAX; ++mi) {
     const int mb = wave + NW * mi;
     if (mb >= mblocks) break;
-    // rows past np land in the unused part of the LDS buffer (mblocks * 32
-    // rows of Z fit: kZtileMaxPixels rounded up to 32 is within kZtileLds)
+    // rows past np land in the unused part of the buffer (mblocks * 32 rows
+    // of Z fit in kZtileLds)
     float* zr = zs + (mb * 32 + 4 * (lane >> 5)) * kZtileZPitch + (lane & 31);
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
       for (int q = 0; q < 16; ++q)
         zr[(8 * (q >> 2) + (q & 3)) * kZtileZPitch + nb * 32] = acc[mi][nb][q];
+  }
+  if (tid < 64) s_zb[tid] = zb_r;
+  if (tid < NTAB) {
+    const int ax = tid / (kZtileMaxStride * kZtileMaxTaps), rem = tid % (kZtileMaxStride * kZtileMaxTaps);
+    const int rho = rem / kZtileMaxTaps, t = rem % kZtileMaxTaps;
+    s_tap[0][ax][rho][t] = tk_r;
+    s_tap[1][ax][rho][t] = td_r;
+    if (t == 0) s_tapn[ax][rho] = tn_r;
   }
   __syncthreads();
   // Owned outputs: rows [o0, o1), all columns, all channels.  Output row oh
@@ -998,23 +1010,16 @@ __global__ __launch_bounds__(kZtileThreads) void ztile_kernel(ZArgs a) {
             v += use[th][tw] ? z : 0.f;
           }
         }
-        if (ow < a.wo) {
-          if constexpr (BF16)
-            ((uint16_t*)a.y)[off] = f32_to_bf16_rne(v);
-          else
-            ((float*)a.y)[off] = v;
-        }
+        if (ow < a.wo) ((uint16_t*)a.y)[off] = f32_to_bf16_rne(v);
       }
     }
   }
 }
 
 hipError_t launch_ztile(const ZArgs& a, int dtype, hipStream_t stream) {
+  if (dtype != 1) return hipErrorInvalidValue;  // the planner selects this form for bf16 only
   const dim3 grid((a.ho + a.ob - 1) / a.ob, a.n);
-  if (dtype == 1)
-    hipLaunchKernelGGL(ztile_kernel<true>, grid, dim3(kZtileThreads), 0, stream, a);
-  else
-    hipLaunchKernelGGL(ztile_kernel<false>, grid, dim3(kZtileThreads), 0, stream, a);
+  hipLaunchKernelGGL(ztile_kernel, grid, dim3(kZtileThreads), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -154,16 +154,17 @@ hipError_t launch_pack_weights(const void* w, void* wp, int dtype, bool transpos
                                int cout, int r, int s, int cin_pad, int cout_pad, int lane_kb,
                                hipStream_t stream);
 
-// All-taps form of a transposed conv with few output channels (NCHW,
+// All-taps form of a transposed conv with few output channels (NCHW, bf16,
 // c_out * r * s <= 64): workgroup (image, block of `ob` output rows) holds
 // input rows [i_lo, i_lo + tr) (i_lo from the block's first output row) and
-// input columns [j_lo, j_lo + tcw) of all (padded) input channels in LDS,
-// column j at LDS column j + kZtileColOff of a row of tcp elements; Z (tile
-// pixels x 64 fp32) then reuses the same LDS.
+// input columns [j_lo, j_lo + tcw) in LDS, channel-contiguous per pixel
+// (kZtileRowB bytes: 64 channels + pad), one 64-channel pass at a time in two
+// buffers; Z (tile pixels x 64 fp32) then reuses the same LDS.
 constexpr int kZtileZPitch = 65;      // Z row pitch, floats
-constexpr int kZtileColOff = 8;       // LDS column of input column 0
-constexpr int kZtileMaxPixels = 384;  // tile pixels (tr * tcw)
-constexpr int kZtileLds = 128 * 1024; // input tile (all channels), then Z
+constexpr int kZtileMaxPixels = 256;  // tile pixels (tr * tcw)
+constexpr int kZtileRowB = 144;       // LDS bytes per tile pixel and pass
+constexpr int kZtileLds = 2 * kZtileMaxPixels * kZtileRowB;  // two pass buffers, then Z
+constexpr int kZtileMaxItems = 2;     // input items (pixel pair x 8 channels) per thread and pass
 constexpr int kZtileMaxStride = 4;    // phases per axis of the tap tables
 constexpr int kZtileMaxTaps = 8;      // kernel taps per axis
 constexpr int kZtilePhaseTaps = 4;    // taps per axis reaching one output phase
@@ -173,13 +174,13 @@ struct ZArgs {
   const void* wp;  // packed K-contiguous weights [slot][cout_pad][cin_pad]
   const float* bias;
   void* y;
+  uint32_t x_bytes;
   int n, cin, h, w, cout, r, s, cin_pad, cout_pad;
   int stride_h, stride_w, pad_h, pad_w, dil_h, dil_w, ho, wo;
-  int ob;            // output rows per workgroup
-  int tr, tcw, tcp;  // tile rows, tile columns, LDS row pitch (elements)
-  int cpitch;        // LDS elements per input channel (>= tr * tcp)
-  int j_lo;          // first tile column (input coordinate)
-  int cchunk;        // K padding unit of the packed weights (channels)
+  int ob;        // output rows per workgroup
+  int tr, tcw;   // tile rows, tile columns
+  int j_lo;      // first tile column (input coordinate)
+  int cchunk;    // K padding unit of the packed weights (channels)
   // per axis (0 = h, 1 = w) and phase rho = (o + pad) mod stride: the taps
   // k with (rho - k*dil) divisible by the stride, and delta = (rho - k*dil) /
   // stride, so that output o reads input (o + pad) div stride + delta

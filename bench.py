@@ -26,6 +26,12 @@ Prints ONE JSON line.  Fields beyond the standard ones:
   cpu_baseline  the CPU oracle (Algorithm 1 zero insertion / Algorithm 2
                 gather, float64) timed on a bounded sample of the workload.
   layers        per-layer mean time, effective TFLOP/s, issued-MAC utilisation.
+  library_reference
+                context for roofline.frac, not part of the path: the vendor
+                library's dense GEMM (torch.matmul -> hipBLASLt) of the same
+                M x N x K as the dominant layer's phase GEMMs (M output pixels,
+                N output channels, K = input channels x taps per phase), timed
+                the same way on random operands of the layer's dtype.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                        [--no-cpu-baseline]
@@ -67,6 +73,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="dcgan", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-library-reference", action="store_true",
+                    help="skip the dense-GEMM library timing reported as context")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle sample")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -283,6 +291,36 @@ def summarize_profiles(d, workload):
             json.dump(traffic, f, indent=1)
             f.write("\n")
     print(json.dumps({"layer_mean_us": avg_us}))
+
+
+def library_reference(layer, steps, dev):
+    """The vendor library's dense GEMM with the M x N x K of the layer's phase
+    GEMMs: a calibration of what this GPU reaches on that contraction size."""
+    import torch
+    ho, wo = layer.out_hw()
+    m, n = layer.n * ho * wo, layer.c_out
+    k = layer.c_in * layer.r * layer.s
+    if layer.transposed:
+        k //= layer.stride ** 2  # taps per phase
+    dt = torch.bfloat16 if layer.dtype == "bf16" else torch.float32
+    g = torch.Generator(device=dev).manual_seed(0)
+    a = torch.randn(m, k, device=dev, generator=g).to(dt)
+    b = torch.randn(k, n, device=dev, generator=g).to(dt)
+    for _ in range(3):
+        c = a @ b
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        c = a @ b
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    tf = 2.0 * m * n * k / (ms * 1e-3) / 1e12
+    del a, b, c
+    return {"op": "torch.matmul %s (hipBLASLt), %d x %d x %d" % (layer.dtype, m, n, k),
+            "layer": layer.name, "ms": round(ms, 5), "tflops": round(tf, 1),
+            "frac_of_peak": round(tf / PEAK[layer.dtype], 4)}
 
 
 def cpu_baseline(name, target_s):
@@ -507,6 +545,8 @@ def main():
     }
     for p in plans:
         p.close()
+    if not args.no_library_reference:
+        out["library_reference"] = library_reference(items[dom][0], args.steps, dev)
     if not args.no_cpu_baseline:
         cb = cpu_baseline(args.workload, args.cpu_seconds)
         cb["speedup_gpu_over_oracle"] = round(out["value"] / cb["value"], 1)

@@ -175,11 +175,13 @@ def copy_calibration(dev, mib=COPY_MIB, reps=10):
 # `cd /tmp && export TMPDIR=/tmp`.
 PROFILE_COMMANDS = [
     ("trace", "rocprofv3 --kernel-trace --stats -f csv -d $O -o trace -- "
-              "python3 $R/bench.py --workload {w} --no-cpu-baseline"),
+              "python3 $R/bench.py --workload {w} --no-cpu-baseline --no-library-reference"),
     ("fetch", "timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE -f csv -d $O -o fetch -- "
-              "python3 $R/bench.py --workload {w} --no-cpu-baseline --steps 3 --warmup 1"),
+              "python3 $R/bench.py --workload {w} --no-cpu-baseline --no-library-reference "
+              "--steps 3 --warmup 1"),
     ("write", "timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE -f csv -d $O -o write -- "
-              "python3 $R/bench.py --workload {w} --no-cpu-baseline --steps 3 --warmup 1"),
+              "python3 $R/bench.py --workload {w} --no-cpu-baseline --no-library-reference "
+              "--steps 3 --warmup 1"),
     ("copy_fetch", "timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE -f csv -d $O -o copy_fetch -- "
                    "python3 $R/bench.py --copy-calibration"),
     ("copy_write", "timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE -f csv -d $O -o copy_write -- "
@@ -194,18 +196,19 @@ def _csv_rows(path):
 
 
 def _counter_per_dispatch(path, counter):
-    """{dispatch id: (kernel name, counter value summed over instances)}"""
+    """{dispatch id: (kernel name and grid size, counter value summed over instances)}"""
     out = {}
     for r in _csv_rows(path):
         if r["Counter_Name"] != counter:
             continue
         d = int(r["Dispatch_Id"])
-        name, v = out.get(d, (r["Kernel_Name"], 0.0))
+        name, v = out.get(d, ("%s grid %s" % (r["Kernel_Name"], r["Grid_Size"]), 0.0))
         out[d] = (name, v + float(r["Counter_Value"]))
     return out
 
 
-MAIN_KERNELS = ("phase_gemm_kernel", "phase_gemm2_kernel", "ztile_kernel")
+MAIN_KERNELS = ("phase_gemm_kernel", "phase_gemm2_kernel", "ztile_kernel", "rowphase_kernel",
+                "quad_kernel")
 
 
 def _is_main(name):
@@ -213,8 +216,19 @@ def _is_main(name):
 
 
 def _layer_dispatches(per_dispatch, nl):
-    """Assign each layer's main-kernel dispatches (in launch order) to it."""
+    """Assign each layer's main-kernel dispatches (in launch order) to it.
+    bench.py launches every layer in order once per step, then the dominant
+    layer's kernel alone, back to back: that trailing run (same kernel name
+    and grid) is left out, except for the dispatches that complete the last
+    step."""
     ids = sorted(d for d, (name, _) in per_dispatch.items() if _is_main(name))
+    run = 1
+    while run < len(ids) and per_dispatch[ids[-run - 1]][0] == per_dispatch[ids[-1]][0]:
+        run += 1
+    if nl > 1 and run > 1:
+        keep = len(ids) - run
+        keep += (-keep) % nl
+        ids = ids[:keep]
     by_layer = [[] for _ in range(nl)]
     for k, d in enumerate(ids):
         by_layer[k % nl].append(d)
@@ -241,7 +255,8 @@ def summarize_profiles(d, workload):
                                                        float(r["AverageNs"]), r["TotalDurationNs"],
                                                        float(r["Percentage"])))
     trace = _csv_rows(os.path.join(d, "trace_kernel_trace.csv"))
-    per = {int(r["Dispatch_Id"]): (r["Kernel_Name"], int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    per = {int(r["Dispatch_Id"]): ("%s grid %sx%s" % (r["Kernel_Name"], r["Grid_Size_X"], r["Grid_Size_Y"]),
+                                   int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
            for r in trace}
     by_layer = _layer_dispatches(per, nl)
     lines += ["", "## Main kernel per layer (dispatches in launch order, layer = k mod %d)" % nl,
@@ -251,7 +266,9 @@ def summarize_profiles(d, workload):
         t = np.array([per[i][1] for i in ids]) / 1e3
         avg_us[l.name] = float(t.mean())
         name = per[ids[0]][0]
-        inst = name[name.find("<"):name.find(">") + 1] if "<" in name else name
+        kname = name.split("(")[0].split("::")[-1]
+        inst = kname + (name[name.find("<"):name.find(">") + 1] if "<" in name and "<" not in kname else "")
+        inst += name[name.rfind(" grid "):]
         lines.append("| %s | %d | %.2f | %.2f | %s |" % (l.name, len(ids), t.mean(), t.min(), inst))
 
     traffic = None

@@ -14,6 +14,8 @@ marshals numpy arrays into it:
 * :func:`conv2d_dilated_alg2` -- Algorithm 2 (section 2.1.1) as a direct gather,
   extended with zero padding and stride.
 * ``*_points`` -- the same definitions for selected output elements only.
+* ``*_wgrad`` -- the weight gradients of both (section 3.2.3, GAN training),
+  written out from the definitions by the chain rule.
 
 All arrays are float64 NCHW; transposed weights are ``[C_in, C_out, R, S]`` (the
 paper's C x N x R x S of section 4.2), conv weights ``[C_out, C_in, R, S]``.
@@ -65,6 +67,8 @@ def _load():
             f.argtypes = [cp, dp, dp, dp, dp, ctypes.c_int]
         for f in (lib.oracle_conv2d_transpose_points, lib.oracle_conv2d_dilated_points):
             f.argtypes = [cp, dp, dp, dp, i64p, ctypes.c_int64, dp, ctypes.c_int]
+        for f in (lib.oracle_conv2d_transpose_wgrad, lib.oracle_conv2d_dilated_wgrad):
+            f.argtypes = [cp, dp, dp, dp, ctypes.c_int]
         _lib = lib
     return _lib
 
@@ -168,3 +172,34 @@ def conv2d_dilated_points(x, w, flat_idx, bias=None, stride=1, padding=0, dilati
     x, w, bias = _f64(x), _f64(w), _f64(bias)
     d = _desc(x.shape, w.shape, False, stride, padding, 0, dilation)
     return _points(_load().oracle_conv2d_dilated_points, d, x, w, bias, flat_idx, nthreads)
+
+
+def conv2d_transpose_wgrad(x, dy, w_shape, stride=1, padding=0, output_padding=0, dilation=1,
+                           nthreads=None):
+    """Weight gradient of the transposed conv: dw [C_in, C_out, R, S] from the
+    input x and the output error dy; float64."""
+    x, dy = _f64(x), _f64(dy)
+    d = _desc(x.shape, tuple(w_shape), True, stride, padding, output_padding, dilation)
+    ho, wo = transpose_out_dims(x.shape, w_shape, stride, padding, output_padding, dilation)
+    if dy.shape != (d.n, d.c_out, ho, wo):
+        raise ValueError("dy shape %s does not match the output %s" % (dy.shape, (d.n, d.c_out, ho, wo)))
+    dw = np.empty(tuple(w_shape), dtype=np.float64)
+    if _load().oracle_conv2d_transpose_wgrad(ctypes.byref(d), _ptr(x), _ptr(dy), _ptr(dw),
+                                             _threads(nthreads)):
+        raise ValueError("oracle_conv2d_transpose_wgrad rejected its arguments")
+    return dw
+
+
+def conv2d_dilated_wgrad(x, dy, w_shape, stride=1, padding=0, dilation=1, nthreads=None):
+    """Weight gradient of the dilated / strided conv: dw [C_out, C_in, R, S]
+    from the input x and the output error dy; float64."""
+    x, dy = _f64(x), _f64(dy)
+    d = _desc(x.shape, tuple(w_shape), False, stride, padding, 0, dilation)
+    ho, wo = conv_out_dims(x.shape, w_shape, stride, padding, dilation)
+    if dy.shape != (d.n, d.c_out, ho, wo):
+        raise ValueError("dy shape %s does not match the output %s" % (dy.shape, (d.n, d.c_out, ho, wo)))
+    dw = np.empty(tuple(w_shape), dtype=np.float64)
+    if _load().oracle_conv2d_dilated_wgrad(ctypes.byref(d), _ptr(x), _ptr(dy), _ptr(dw),
+                                           _threads(nthreads)):
+        raise ValueError("oracle_conv2d_dilated_wgrad rejected its arguments")
+    return dw

@@ -322,3 +322,82 @@ int oracle_conv2d_dilated_points(const oracle_conv* d, const double* x, const do
   run_parallel(alg2_point, &a, (long)count, nthreads);
   return 0;
 }
+
+/* ------------------------------------------------------------------ */
+/* Weight gradients (section 3.2.3): the chain rule applied to the two  */
+/* definitions above, one weight element at a time.                     */
+
+typedef struct {
+  const oracle_conv* d;
+  const double* x;
+  const double* dy;
+  double* dw;
+  int ho, wo;
+  int transposed;
+} wgrad_ctx;
+
+/* dw for weight plane (c, k): all r x s taps. */
+static void wgrad_plane(void* p, long plane) {
+  wgrad_ctx* a = (wgrad_ctx*)p;
+  const oracle_conv* d = a->d;
+  const int c = (int)(plane / d->c_out), k = (int)(plane % d->c_out);
+  for (int m = 0; m < d->r; ++m)
+    for (int q = 0; q < d->s; ++q) {
+      double acc = 0.0;
+      if (a->transposed) {
+        /* every input pixel (i, j) and the output it reaches through tap (m, q) */
+        for (int n = 0; n < d->n; ++n)
+          for (int i = 0; i < d->h; ++i) {
+            const int oh = i * d->stride_h - d->pad_h + m * d->dil_h;
+            if (oh < 0 || oh >= a->ho) continue;
+            for (int j = 0; j < d->w; ++j) {
+              const int ow = j * d->stride_w - d->pad_w + q * d->dil_w;
+              if (ow < 0 || ow >= a->wo) continue;
+              acc += a->x[(((long)n * d->c_in + c) * d->h + i) * d->w + j] *
+                     a->dy[(((long)n * d->c_out + k) * a->ho + oh) * a->wo + ow];
+            }
+          }
+        a->dw[(((long)c * d->c_out + k) * d->r + m) * d->s + q] = acc;
+      } else {
+        /* every output pixel (oh, ow) and the input it reads through tap (m, q) */
+        for (int n = 0; n < d->n; ++n)
+          for (int oh = 0; oh < a->ho; ++oh) {
+            const int ih = oh * d->stride_h - d->pad_h + m * d->dil_h;
+            if (ih < 0 || ih >= d->h) continue;
+            for (int ow = 0; ow < a->wo; ++ow) {
+              const int iw = ow * d->stride_w - d->pad_w + q * d->dil_w;
+              if (iw < 0 || iw >= d->w) continue;
+              acc += a->dy[(((long)n * d->c_out + k) * a->ho + oh) * a->wo + ow] *
+                     a->x[(((long)n * d->c_in + c) * d->h + ih) * d->w + iw];
+            }
+          }
+        a->dw[(((long)k * d->c_in + c) * d->r + m) * d->s + q] = acc;
+      }
+    }
+}
+
+int oracle_conv2d_transpose_wgrad(const oracle_conv* d, const double* x, const double* dy,
+                                  double* dw, int nthreads) {
+  wgrad_ctx a;
+  if (!x || !dy || !dw || oracle_transpose_out_dims(d, &a.ho, &a.wo) != 0) return -1;
+  a.d = d;
+  a.x = x;
+  a.dy = dy;
+  a.dw = dw;
+  a.transposed = 1;
+  run_parallel(wgrad_plane, &a, (long)d->c_in * d->c_out, nthreads);
+  return 0;
+}
+
+int oracle_conv2d_dilated_wgrad(const oracle_conv* d, const double* x, const double* dy,
+                                double* dw, int nthreads) {
+  wgrad_ctx a;
+  if (!x || !dy || !dw || oracle_conv_out_dims(d, &a.ho, &a.wo) != 0) return -1;
+  a.d = d;
+  a.x = x;
+  a.dy = dy;
+  a.dw = dw;
+  a.transposed = 0;
+  run_parallel(wgrad_plane, &a, (long)d->c_in * d->c_out, nthreads);
+  return 0;
+}

@@ -60,6 +60,25 @@ int oracle_conv2d_dilated_points(const oracle_conv* d, const double* x, const do
                                  const double* bias, const int64_t* idx, int64_t count,
                                  double* out, int nthreads);
 
+/* Weight gradients for training (section 3.2.3), from the definitions
+ * above by the chain rule; dy has the forward output's shape and dw the
+ * weight's layout.
+ *  transposed conv (the generator's layer):
+ *    dw[c][k][m][q] = sum over (n, i, j) with oh = i*stride_h - pad_h + m*dil_h
+ *                     and ow = j*stride_w - pad_w + q*dil_w inside the output
+ *                     of x[n][c][i][j] * dy[n][k][oh][ow]
+ *    (a strided correlation of the input with the output-error maps);
+ *  dilated / strided conv (the discriminator's layer):
+ *    dw[k][c][m][q] = sum over (n, oh, ow) with ih = oh*stride_h - pad_h +
+ *                     m*dil_h and iw = ow*stride_w - pad_w + q*dil_w inside
+ *                     the input of dy[n][k][oh][ow] * x[n][c][ih][iw]
+ *    (the error maps, spread out by the stride, correlated with the input).
+ * Parallel over (c, k) weight planes. */
+int oracle_conv2d_transpose_wgrad(const oracle_conv* d, const double* x, const double* dy,
+                                  double* dw, int nthreads);
+int oracle_conv2d_dilated_wgrad(const oracle_conv* d, const double* x, const double* dy,
+                                double* dw, int nthreads);
+
 #ifdef __cplusplus
 }
 #endif

@@ -29,7 +29,16 @@ def _golden_cases():
     return sorted(glob.glob(os.path.join(GOLDEN, "*.json")))
 
 
-@pytest.mark.parametrize("path", _golden_cases(), ids=lambda p: os.path.basename(p)[:-5])
+def _golden_of(kind):
+    out = []
+    for path in _golden_cases():
+        with open(path) as f:
+            if json.load(f)["op"].endswith("_wgrad") == (kind == "wgrad"):
+                out.append(path)
+    return out
+
+
+@pytest.mark.parametrize("path", _golden_of("forward"), ids=lambda p: os.path.basename(p)[:-5])
 def test_golden_examples(oracle_mod, path):
     with open(path) as f:
         g = json.load(f)
@@ -45,6 +54,22 @@ def test_golden_examples(oracle_mod, path):
                                            nthreads=1)
     assert y.shape[2:] == exp.shape
     np.testing.assert_array_equal(y[0, 0], exp)
+
+
+@pytest.mark.parametrize("path", _golden_of("wgrad"), ids=lambda p: os.path.basename(p)[:-5])
+def test_golden_weight_gradients(oracle_mod, path):
+    with open(path) as f:
+        g = json.load(f)
+    assert g["citation"]
+    x = np.array(g["x"], dtype=np.float64)[None, None]
+    dy = np.array(g["dy"], dtype=np.float64)[None, None]
+    if g["op"] == "transpose_wgrad":
+        dw = oracle_mod.conv2d_transpose_wgrad(x, dy, g["w_shape"], g["stride"], g["padding"],
+                                               g["output_padding"], g["dilation"], nthreads=1)
+    else:
+        dw = oracle_mod.conv2d_dilated_wgrad(x, dy, g["w_shape"], g["stride"], g["padding"],
+                                             g["dilation"], nthreads=1)
+    np.testing.assert_array_equal(dw[0, 0], np.array(g["expected"], dtype=np.float64))
 
 
 def _random_case(rng, transposed):
@@ -241,3 +266,72 @@ def test_invalid_descriptors_rejected(oracle_mod, bad):
     kw.update(bad)
     with pytest.raises(ValueError):
         oracle_mod.conv2d_transpose_alg1(x, w, None, **kw)
+
+
+# ---------------------------------------------------------------------------
+# Weight gradients (section 3.2.3)
+
+@pytest.mark.parametrize("transposed", [True, False])
+def test_wgrad_inner_product_identity(oracle_mod, transposed):
+    """y is linear in the weights, so the gradient of <dy, y(x; w)> is dw
+    with <dw, v> = <dy, y(x; v)> for every v: pins the weight gradient to the
+    (separately pinned) forward definitions."""
+    rng = np.random.default_rng(77 if transposed else 78)
+    checked = 0
+    for _ in range(60):
+        c = _random_case(rng, transposed)
+        x = rng.standard_normal((c["n"], c["ci"], c["h"], c["w"]))
+        wshape = (c["ci"], c["co"], c["r"], c["s"]) if transposed else (c["co"], c["ci"], c["r"], c["s"])
+        v = rng.standard_normal(wshape)
+        try:
+            if transposed:
+                yv = oracle_mod.conv2d_transpose_alg1(x, v, None, c["stride"], c["pad"], c["op"], c["dil"],
+                                                      nthreads=2)
+            else:
+                yv = oracle_mod.conv2d_dilated_alg2(x, v, None, c["stride"], c["pad"], c["dil"], nthreads=2)
+        except ValueError:
+            continue
+        dy = rng.standard_normal(yv.shape)
+        if transposed:
+            dw = oracle_mod.conv2d_transpose_wgrad(x, dy, wshape, c["stride"], c["pad"], c["op"], c["dil"],
+                                                   nthreads=2)
+        else:
+            dw = oracle_mod.conv2d_dilated_wgrad(x, dy, wshape, c["stride"], c["pad"], c["dil"], nthreads=2)
+        lhs, rhs = float(np.sum(dw * v)), float(np.sum(dy * yv))
+        assert abs(lhs - rhs) <= 1e-12 * max(1.0, np.sum(np.abs(dw * v)), np.sum(np.abs(dy * yv))), c
+        checked += 1
+    assert checked >= 30
+
+
+@pytest.mark.parametrize("transposed", [True, False])
+def test_wgrad_matches_torch_autograd(oracle_mod, transposed):
+    """An independent library routine: torch CPU autograd in float64."""
+    rng = np.random.default_rng(91 if transposed else 92)
+    checked = 0
+    for _ in range(60):
+        c = _random_case(rng, transposed)
+        x = rng.standard_normal((c["n"], c["ci"], c["h"], c["w"]))
+        wshape = (c["ci"], c["co"], c["r"], c["s"]) if transposed else (c["co"], c["ci"], c["r"], c["s"])
+        w = torch.tensor(rng.standard_normal(wshape), requires_grad=True)
+        try:
+            if transposed:
+                y = torch.nn.functional.conv_transpose2d(torch.from_numpy(x), w, stride=c["stride"],
+                                                         padding=c["pad"], output_padding=c["op"],
+                                                         dilation=c["dil"])
+            else:
+                y = torch.nn.functional.conv2d(torch.from_numpy(x), w, stride=c["stride"], padding=c["pad"],
+                                               dilation=c["dil"])
+        except RuntimeError:
+            continue
+        if y.numel() == 0:
+            continue
+        dy = rng.standard_normal(tuple(y.shape))
+        (y * torch.from_numpy(dy)).sum().backward()
+        if transposed:
+            got = oracle_mod.conv2d_transpose_wgrad(x, dy, wshape, c["stride"], c["pad"], c["op"], c["dil"],
+                                                    nthreads=2)
+        else:
+            got = oracle_mod.conv2d_dilated_wgrad(x, dy, wshape, c["stride"], c["pad"], c["dil"], nthreads=2)
+        np.testing.assert_allclose(got, w.grad.numpy(), rtol=1e-10, atol=1e-10)
+        checked += 1
+    assert checked >= 30

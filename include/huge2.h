@@ -152,6 +152,60 @@ huge2_status huge2_conv2d_transpose(const huge2_conv_desc* desc, const void* x, 
 huge2_status huge2_conv2d_dilated(const huge2_conv_desc* desc, const void* x, const void* w,
                                   const float* bias, void* y, void* hip_stream);
 
+/* ---- training: weight gradients (section 3.2.3) ------------------------- */
+
+/* Back-propagation of a GAN updates the kernels from the output errors dy
+ * (the gradient of the loss with respect to y, the forward output's shape):
+ *   transposed conv (generator layer), w-shaped dw [c_in][c_out][r][s]:
+ *     dw[c,k,m,q] = sum over (n, i, j) of x[n,c,i,j] * dy[n,k, i*stride_h - pad_h
+ *                   + m*dil_h, j*stride_w - pad_w + q*dil_w], terms whose dy index
+ *                   falls outside the output omitted -- the input correlated with
+ *                   the error maps read with the stride;
+ *   dilated / strided conv (discriminator layer), dw [c_out][c_in][r][s]:
+ *     dw[k,c,m,q] = sum over (n, oh, ow) of dy[n,k,oh,ow] * x[n,c, oh*stride_h
+ *                   - pad_h + m*dil_h, ow*stride_w - pad_w + q*dil_w], out-of-range
+ *                   x omitted -- the error maps spread by the stride ("dilated
+ *                   derivative maps") correlated with the input.
+ * (The data gradients are the other form: dx of a transposed conv is the
+ * strided conv of dy with the same w, and dx of a strided conv is the
+ * transposed conv of dy; both are the entry points above.)
+ * How: per kernel tap, the large tensor (dy for the transposed conv, x for
+ * the strided conv) is gathered onto the small tensor's pixel grid -- one
+ * untangled copy per tap, as the paper's C copies of each derivative map --
+ * and every tap's gradient is then one dense MFMA GEMM over pixels with no
+ * zero products, accumulated in fp32 over chunks of images in a fixed order
+ * and rounded once to the dtype.
+ * Layout: NCHW only (HUGE2_NHWC returns HUGE2_ERR_UNSUPPORTED).  dtype as
+ * above: x, dy and dw share it; accumulation is fp32 for both dtypes. */
+typedef struct huge2_wgrad_plan huge2_wgrad_plan;
+
+/* Build a weight-gradient plan for desc (the forward layer's descriptor;
+ * transposed selects the layer type).  Allocates the per-plan workspace:
+ * the staged operands of one chunk of images (the chunk is sized so they
+ * stay under 256 MiB; at least one image) and the fp32 gradient.  No HIP
+ * work is enqueued.  Errors: INVALID_ARG (NULL out/desc, invalid
+ * descriptor), UNSUPPORTED (NHWC; byte extents of 2^31 or more), ALLOC. */
+huge2_status huge2_wgrad_plan_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc,
+                                     int32_t transposed);
+
+/* Enqueue dw for input x and output error dy (device pointers, NCHW, the
+ * plan's dtype) on hip_stream; dw must not alias x or dy.  Calls on one
+ * plan share its workspace: enqueue them on one stream (or order them).
+ * Errors: INVALID_ARG (NULL plan/pointer, aliasing), HIP. */
+huge2_status huge2_wgrad_execute(const huge2_wgrad_plan* plan, const void* x, const void* dy,
+                                 void* dw, void* hip_stream);
+
+/* Release a weight-gradient plan; waits for the device first.  NULL is
+ * accepted.  Errors: HIP. */
+huge2_status huge2_wgrad_plan_destroy(huge2_wgrad_plan* plan);
+
+/* One-shot forms: plan_create + execute + destroy (synchronises the
+ * stream before releasing the workspace). */
+huge2_status huge2_conv2d_transpose_wgrad(const huge2_conv_desc* desc, const void* x,
+                                          const void* dy, void* dw, void* hip_stream);
+huge2_status huge2_conv2d_dilated_wgrad(const huge2_conv_desc* desc, const void* x,
+                                        const void* dy, void* dw, void* hip_stream);
+
 /* ---- introspection (host only, no HIP call) ---------------------------- */
 
 /* One rectangle of a box of phases with a constant set of kernel taps.

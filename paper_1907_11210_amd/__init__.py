@@ -11,4 +11,7 @@ from .huge2 import (  # noqa: F401
     huge2_output_shape, huge2_plan_create, huge2_plan_describe, huge2_plan_destroy,
     huge2_plan_execute, huge2_plan_macs, huge2_plan_run_gemm, huge2_plan_stage_input,
     huge2_plan_kernel, huge2_plan_stages_input, make_desc,
+    conv2d_transpose_wgrad, conv2d_dilated_wgrad, conv2d_transpose_dgrad, conv2d_dilated_dgrad,
+    huge2_wgrad_plan_create, huge2_wgrad_execute, huge2_wgrad_plan_destroy,
+    huge2_conv2d_transpose_wgrad, huge2_conv2d_dilated_wgrad,
 )

@@ -878,6 +878,136 @@ huge2_status one_shot(const huge2_conv_desc* desc, int transposed, const void* x
 
 }  // namespace
 
+// ---------------------------------------------------------------------------
+// Weight gradients (section 3.2.3).
+
+struct huge2_wgrad_plan {
+  huge2_conv_desc desc;
+  int transposed;
+  int ms, nb;          // small / big tensor channels
+  int hs, ws, hb, wb;  // small / big pixel grids
+  int chunk;           // images per chunk
+  int kp;              // padded K of a full chunk
+  void* st;
+  void* bt;
+  float* g;
+};
+
+namespace {
+
+constexpr long long kWgradStageBudget = 256ll << 20;  // staged operands of one chunk
+
+void wgrad_free(huge2_wgrad_plan* p) {
+  void* bufs[3] = {p->st, p->bt, p->g};
+  for (void* b : bufs)
+    if (b) (void)hipFree(b);
+  p->st = p->bt = nullptr;
+  p->g = nullptr;
+}
+
+huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, int transposed) {
+  if (!out) return HUGE2_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (transposed != 0 && transposed != 1) return HUGE2_ERR_INVALID_ARG;
+  huge2_status st = validate_desc(desc, transposed != 0);
+  if (st != HUGE2_OK) return st;
+  const huge2_conv_desc& d = *desc;
+  if (d.layout != HUGE2_NCHW) return HUGE2_ERR_UNSUPPORTED;
+  int ho, wo;
+  if (!output_dims(d, transposed != 0, &ho, &wo)) return HUGE2_ERR_INVALID_ARG;
+  huge2_wgrad_plan* p = new (std::nothrow) huge2_wgrad_plan();
+  if (!p) return HUGE2_ERR_ALLOC;
+  p->desc = d;
+  p->transposed = transposed;
+  if (transposed) {  // small = x, big = dy
+    p->ms = d.c_in, p->nb = d.c_out, p->hs = d.h, p->ws = d.w, p->hb = ho, p->wb = wo;
+  } else {           // small = dy, big = x
+    p->ms = d.c_out, p->nb = d.c_in, p->hs = ho, p->ws = wo, p->hb = d.h, p->wb = d.w;
+  }
+  const long long esz = elem_size(d.dtype), taps = (long long)d.r * d.s;
+  const long long hws = (long long)p->hs * p->ws;
+  const long long per_img = esz * (p->ms + taps * p->nb) * hws;
+  long long chunk = std::max(1ll, std::min<long long>(d.n, kWgradStageBudget / std::max(1ll, per_img)));
+  {
+    // HUGE2_WGRAD_CHUNK: fewer images per chunk (tests of the chunk accumulation)
+    const int forced = env_int("HUGE2_WGRAD_CHUNK", 0);
+    if (forced > 0 && forced < chunk) chunk = forced;
+  }
+  const long long kp = (chunk * hws + 63) / 64 * 64;
+  const long long st_b = p->ms * kp * esz, bt_b = taps * p->nb * kp * esz;
+  const long long g_b = taps * p->ms * p->nb * 4;
+  const long long big_b = (long long)d.n * p->nb * p->hb * p->wb * esz;
+  const long long small_b = (long long)d.n * p->ms * hws * esz;
+  if (st_b >= (1ll << 31) || bt_b >= (1ll << 31) || g_b >= (1ll << 31) || big_b >= (1ll << 40) ||
+      small_b >= (1ll << 40) || taps > 65535) {
+    delete p;
+    return HUGE2_ERR_UNSUPPORTED;
+  }
+  p->chunk = (int)chunk;
+  p->kp = (int)kp;
+  if (fault("alloc") || hipMalloc(&p->st, st_b) != hipSuccess || hipMalloc(&p->bt, bt_b) != hipSuccess ||
+      hipMalloc((void**)&p->g, g_b) != hipSuccess) {
+    (void)hipGetLastError();
+    wgrad_free(p);
+    delete p;
+    return HUGE2_ERR_ALLOC;
+  }
+  *out = p;
+  return HUGE2_OK;
+}
+
+huge2_status wgrad_execute(const huge2_wgrad_plan* p, const void* x, const void* dy, void* dw,
+                           hipStream_t stream) {
+  if (!p || !x || !dy || !dw || dw == x || dw == dy) return HUGE2_ERR_INVALID_ARG;
+  const huge2_conv_desc& d = p->desc;
+  if (fault("launch")) return HUGE2_ERR_HIP;
+  WgArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.sm = p->transposed ? x : dy;
+  a.bg = p->transposed ? dy : x;
+  a.st = p->st;
+  a.bt = p->bt;
+  a.g = p->g;
+  a.dw = dw;
+  a.ms = p->ms, a.nb = p->nb, a.hs = p->hs, a.ws = p->ws, a.hb = p->hb, a.wb = p->wb;
+  a.r = d.r, a.s = d.s;
+  a.stride_h = d.stride_h, a.stride_w = d.stride_w, a.pad_h = d.pad_h, a.pad_w = d.pad_w;
+  a.dil_h = d.dil_h, a.dil_w = d.dil_w;
+  const long long hws = (long long)p->hs * p->ws;
+  // chunks in order: the first writes the fp32 gradient, the rest add to it
+  for (int img0 = 0; img0 < d.n; img0 += p->chunk) {
+    a.img0 = img0;
+    a.nimg = std::min(p->chunk, d.n - img0);
+    a.kp = (int)((a.nimg * hws + 63) / 64 * 64);
+    a.accumulate = img0 > 0;
+    if (launch_wgrad_stage(a, d.dtype, stream) != hipSuccess ||
+        launch_wgrad_gemm(a, d.dtype, stream) != hipSuccess) {
+      (void)hipGetLastError();
+      return HUGE2_ERR_HIP;
+    }
+  }
+  if (launch_wgrad_store(a, d.dtype, stream) != hipSuccess) {
+    (void)hipGetLastError();
+    return HUGE2_ERR_HIP;
+  }
+  return HUGE2_OK;
+}
+
+huge2_status wgrad_one_shot(const huge2_conv_desc* desc, int transposed, const void* x,
+                            const void* dy, void* dw, hipStream_t stream) {
+  if (!x || !dy || !dw || dw == x || dw == dy) return HUGE2_ERR_INVALID_ARG;
+  huge2_wgrad_plan* p = nullptr;
+  huge2_status st = wgrad_create(&p, desc, transposed);
+  if (st != HUGE2_OK) return st;
+  st = wgrad_execute(p, x, dy, dw, stream);
+  if (hipStreamSynchronize(stream) != hipSuccess && st == HUGE2_OK) st = HUGE2_ERR_HIP;
+  wgrad_free(p);
+  delete p;
+  return st;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* huge2_status_str(huge2_status status) {
@@ -1029,6 +1159,49 @@ huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, in
     *nonzero_macs = shape.nonzero_macs;
     *issued_macs = shape.tile_taps * bm * bn * ntn * cin_pad;
     return HUGE2_OK;
+  } catch (...) {
+    return HUGE2_ERR_ALLOC;
+  }
+}
+
+huge2_status huge2_wgrad_plan_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc,
+                                     int32_t transposed) {
+  try {
+    return wgrad_create(out, desc, transposed);
+  } catch (...) {
+    return HUGE2_ERR_ALLOC;
+  }
+}
+
+huge2_status huge2_wgrad_execute(const huge2_wgrad_plan* plan, const void* x, const void* dy,
+                                 void* dw, void* hip_stream) {
+  try {
+    return wgrad_execute(plan, x, dy, dw, (hipStream_t)hip_stream);
+  } catch (...) {
+    return HUGE2_ERR_ALLOC;
+  }
+}
+
+huge2_status huge2_wgrad_plan_destroy(huge2_wgrad_plan* plan) {
+  if (!plan) return HUGE2_OK;
+  wgrad_free(plan);
+  delete plan;
+  return HUGE2_OK;
+}
+
+huge2_status huge2_conv2d_transpose_wgrad(const huge2_conv_desc* desc, const void* x,
+                                          const void* dy, void* dw, void* hip_stream) {
+  try {
+    return wgrad_one_shot(desc, 1, x, dy, dw, (hipStream_t)hip_stream);
+  } catch (...) {
+    return HUGE2_ERR_ALLOC;
+  }
+}
+
+huge2_status huge2_conv2d_dilated_wgrad(const huge2_conv_desc* desc, const void* x,
+                                        const void* dy, void* dw, void* hip_stream) {
+  try {
+    return wgrad_one_shot(desc, 0, x, dy, dw, (hipStream_t)hip_stream);
   } catch (...) {
     return HUGE2_ERR_ALLOC;
   }

@@ -1548,6 +1548,190 @@ hipError_t launch_pack_weights(const void* w, void* wp, int dtype, bool transpos
 }
 
 // ---------------------------------------------------------------------------
+// Weight gradient (section 3.2.3).  The error maps (or, for a strided conv,
+// the input) are untangled per tap into copies on the small tensor's pixel
+// grid, so that every tap's gradient is one dense GEMM over pixels with no
+// zero products; the GEMM then runs on MFMA with both operands K-contiguous.
+
+// Staging of one image chunk: St (element-wise transpose of the image and
+// channel axes) and Bt (the tap gather), zero up to kp.
+template <typename T>
+__global__ __launch_bounds__(256) void wgrad_stage_kernel(WgArgs a) {
+  const long long hws = (long long)a.hs * a.ws;
+  const long long kreal = (long long)a.nimg * hws;
+  const long long st_total = (long long)a.ms * a.kp;
+  const long long bt_total = (long long)a.r * a.s * a.nb * a.kp;
+  const long long stride = (long long)gridDim.x * blockDim.x;
+  for (long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x; e < st_total + bt_total; e += stride) {
+    if (e < st_total) {
+      const long long k = e % a.kp, m = e / a.kp;
+      T v = T(0);
+      if (k < kreal) {
+        const long long il = k / hws, q = k - il * hws;
+        v = ((const T*)a.sm)[((a.img0 + il) * a.ms + m) * hws + q];
+      }
+      ((T*)a.st)[e] = v;
+    } else {
+      const long long f = e - st_total;
+      const long long k = f % a.kp, t2 = f / a.kp;
+      const int n = (int)(t2 % a.nb), tap = (int)(t2 / a.nb);
+      const int kh = tap / a.s, kw = tap - kh * a.s;
+      T v = T(0);
+      if (k < kreal) {
+        const long long il = k / hws, q = k - il * hws;
+        const int qh = (int)(q / a.ws), qw = (int)(q - (long long)qh * a.ws);
+        const int ih = qh * a.stride_h - a.pad_h + kh * a.dil_h;
+        const int iw = qw * a.stride_w - a.pad_w + kw * a.dil_w;
+        if (ih >= 0 && ih < a.hb && iw >= 0 && iw < a.wb)
+          v = ((const T*)a.bg)[(((a.img0 + il) * a.nb + n) * (long long)a.hb + ih) * a.wb + iw];
+      }
+      ((T*)a.bt)[f] = v;
+    }
+  }
+}
+
+// G[tap][m][n] (+)= sum_k St[m][k] * Bt[tap][n][k]: a 64 x 64 tile per
+// workgroup of 4 waves (32 x 32 each), K in 128-byte stages through LDS,
+// double buffered, the next stage's loads in registers while this one
+// multiplies.  K order inside a stage is permuted identically for both
+// operands (lane half h takes the stage's h-th half), as in the phase GEMM.
+template <bool BF16>
+__global__ __launch_bounds__(256) void wgrad_gemm_kernel(WgArgs a) {
+  constexpr int ESZ = BF16 ? 2 : 4;
+  constexpr int KB = 128, KC = KB / ESZ, ROWB = KB + 16;
+  constexpr int STAGE_B = 2 * 64 * ROWB;
+  __shared__ __attribute__((aligned(16))) char smem[2 * STAGE_B];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave & 1, wn = wave >> 1;
+  const int m0 = blockIdx.x * 64, n0 = blockIdx.y * 64, tap = blockIdx.z;
+  // this thread's two rows of each operand (rows past the end repeat the last)
+  const int chunk = tid & 7, row = tid >> 3;  // 8 chunks of 16 bytes per row
+  const char* const st = (const char*)a.st;
+  const char* const bt = (const char*)a.bt;
+  const size_t a0 = (size_t)min(m0 + row, a.ms - 1) * a.kp * ESZ + chunk * 16;
+  const size_t a1 = (size_t)min(m0 + row + 32, a.ms - 1) * a.kp * ESZ + chunk * 16;
+  const size_t b0 = ((size_t)tap * a.nb + min(n0 + row, a.nb - 1)) * a.kp * ESZ + chunk * 16;
+  const size_t b1 = ((size_t)tap * a.nb + min(n0 + row + 32, a.nb - 1)) * a.kp * ESZ + chunk * 16;
+  struct Regs {
+    uint4 a0, a1, b0, b1;
+  };
+  auto load = [&](int ks) {
+    const size_t off = (size_t)ks * KB;
+    Regs r;
+    r.a0 = *(const uint4*)(st + a0 + off);
+    r.a1 = *(const uint4*)(st + a1 + off);
+    r.b0 = *(const uint4*)(bt + b0 + off);
+    r.b1 = *(const uint4*)(bt + b1 + off);
+    return r;
+  };
+  auto store = [&](int buf, const Regs& r) {
+    char* as = smem + buf * STAGE_B;
+    char* bs = as + 64 * ROWB;
+    *(uint4*)(as + row * ROWB + chunk * 16) = r.a0;
+    *(uint4*)(as + (row + 32) * ROWB + chunk * 16) = r.a1;
+    *(uint4*)(bs + row * ROWB + chunk * 16) = r.b0;
+    *(uint4*)(bs + (row + 32) * ROWB + chunk * 16) = r.b1;
+  };
+  f32x16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  auto compute = [&](int buf) {
+    const char* as = smem + buf * STAGE_B + (wm * 32 + (lane & 31)) * ROWB + (lane >> 5) * (KB / 2);
+    const char* bs = smem + buf * STAGE_B + (64 + wn * 32 + (lane & 31)) * ROWB + (lane >> 5) * (KB / 2);
+    if constexpr (BF16) {
+#pragma unroll
+      for (int t = 0; t < KB / 32; ++t) {
+        const bf16x8 va = __builtin_bit_cast(bf16x8, *(const uint4*)(as + 16 * t));
+        const bf16x8 vb = __builtin_bit_cast(bf16x8, *(const uint4*)(bs + 16 * t));
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vb, va, acc, 0, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int t4 = 0; t4 < KB / 32; ++t4) {
+        const uint4 fa = *(const uint4*)(as + 16 * t4);
+        const uint4 fb = *(const uint4*)(bs + 16 * t4);
+        const uint32_t ea[4] = {fa.x, fa.y, fa.z, fa.w}, eb[4] = {fb.x, fb.y, fb.z, fb.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(eb[e]), __uint_as_float(ea[e]), acc, 0, 0, 0);
+      }
+    }
+  };
+  const int nk = a.kp / KC;
+  store(0, load(0));
+  __syncthreads();
+  for (int ks = 0; ks < nk; ++ks) {
+    // the next stage's loads (stage 0 again past the end: unused) overlap
+    // this stage's MFMAs
+    const Regs nx = load(ks + 1 < nk ? ks + 1 : 0);
+    compute(ks & 1);
+    if (ks + 1 < nk) store((ks + 1) & 1, nx);
+    __syncthreads();
+  }
+  // acc: lane holds m = m0 + wm*32 + lane%32 (MFMA column: the St operand went
+  // second) and n = n0 + wn*32 + 8*(r/4) + 4*(lane/32) + r%4 (rows)
+  const int m = m0 + wm * 32 + (lane & 31);
+  float* gt = a.g + ((size_t)tap * a.ms + min(m, a.ms - 1)) * a.nb;
+  const bool acc_in = a.accumulate != 0;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int n = n0 + wn * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+    const float v = acc[r];
+    if (m < a.ms && n < a.nb) gt[n] = acc_in ? gt[n] + v : v;
+  }
+}
+
+// dw[m][n][tap] from G[tap][m][n], rounded to the dtype.
+template <bool BF16>
+__global__ __launch_bounds__(256) void wgrad_store_kernel(WgArgs a) {
+  const int taps = a.r * a.s;
+  const long long total = (long long)a.ms * a.nb * taps;
+  for (long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (long long)gridDim.x * blockDim.x) {
+    const int tap = (int)(e % taps);
+    const long long mn = e / taps;
+    const float v = a.g[(long long)tap * a.ms * a.nb + mn];
+    if constexpr (BF16)
+      ((uint16_t*)a.dw)[e] = f32_to_bf16_rne(v);
+    else
+      ((float*)a.dw)[e] = v;
+  }
+}
+
+static dim3 grid_for(long long total) {
+  const long long want = (total + 255) / 256;
+  return dim3((unsigned)(want < 65536 ? (want > 0 ? want : 1) : 65536));
+}
+
+hipError_t launch_wgrad_stage(const WgArgs& a, int dtype, hipStream_t stream) {
+  const long long total = (long long)a.ms * a.kp + (long long)a.r * a.s * a.nb * a.kp;
+  if (dtype == 1)
+    hipLaunchKernelGGL(wgrad_stage_kernel<uint16_t>, grid_for(total), dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(wgrad_stage_kernel<uint32_t>, grid_for(total), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_wgrad_gemm(const WgArgs& a, int dtype, hipStream_t stream) {
+  const dim3 grid((a.ms + 63) / 64, (a.nb + 63) / 64, a.r * a.s);
+  if (dtype == 1)
+    hipLaunchKernelGGL(wgrad_gemm_kernel<true>, grid, dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(wgrad_gemm_kernel<false>, grid, dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_wgrad_store(const WgArgs& a, int dtype, hipStream_t stream) {
+  const long long total = (long long)a.ms * a.nb * a.r * a.s;
+  if (dtype == 1)
+    hipLaunchKernelGGL(wgrad_store_kernel<true>, grid_for(total), dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(wgrad_store_kernel<false>, grid_for(total), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Input staging: channel-contiguous pixels [n][h*w][c_stride], zero padded
 // channels, for NCHW inputs and for NHWC inputs whose channel count is not a
 // multiple of 16 bytes.

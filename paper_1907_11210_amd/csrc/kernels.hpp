@@ -245,6 +245,33 @@ struct QArgs {
 };
 hipError_t launch_quad(const QArgs& a, hipStream_t stream);
 
+// Weight gradient (training, section 3.2.3).  With the "small" tensor S on
+// the tap's pixel grid and the "big" tensor B read at position
+// q*stride - pad + k*dil of that grid (transposed conv: S = x, B = dy; strided
+// or dilated conv: S = dy, B = x), G[tap][m][n] = sum over (image, q) of
+// S[m][q] * B[n][tap position of q].  For one chunk of images:
+//  - wgrad_stage: St[m][k] = S[image][m][q] and Bt[tap][n][k] = B at the tap
+//    position (zero outside), k = local image * hws + q, zero up to kp (a
+//    multiple of 64): the untangled copies of the big tensor, one per tap;
+//  - wgrad_gemm: G[tap] (fp32) = (or +=) St Bt[tap]^T on MFMA;
+//  - wgrad_store: dw[(m * nb + n) * taps + tap] = G[tap][m][n] in the dtype.
+struct WgArgs {
+  const void* sm;  // small tensor [n][ms][hs][ws] (NCHW)
+  const void* bg;  // big tensor [n][nb][hb][wb]
+  void* st;       // [ms][kp]
+  void* bt;       // [taps][nb][kp]
+  float* g;       // [taps][ms][nb]
+  void* dw;       // [ms][nb][r][s]
+  int img0, nimg;  // image chunk
+  int ms, nb, hs, ws, hb, wb, r, s;
+  int stride_h, stride_w, pad_h, pad_w, dil_h, dil_w;
+  int kp;          // padded K of the chunk (multiple of 64)
+  int accumulate;  // 0: G = product, 1: G += product
+};
+hipError_t launch_wgrad_stage(const WgArgs& a, int dtype, hipStream_t stream);
+hipError_t launch_wgrad_gemm(const WgArgs& a, int dtype, hipStream_t stream);
+hipError_t launch_wgrad_store(const WgArgs& a, int dtype, hipStream_t stream);
+
 // Re-layout the input into [n][h*w][c_stride] with zero channel padding.
 // nchw: source is NCHW; otherwise NHWC with cin channels per pixel.
 hipError_t launch_stage_input(const void* x, void* xs, int dtype, bool nchw, int n, int cin,

@@ -27,6 +27,8 @@ EXPORTED = (
     "huge2_plan_kernel",
     "huge2_plan_destroy", "huge2_conv2d_transpose", "huge2_conv2d_dilated",
     "huge2_plan_describe", "huge2_plan_macs",
+    "huge2_wgrad_plan_create", "huge2_wgrad_execute", "huge2_wgrad_plan_destroy",
+    "huge2_conv2d_transpose_wgrad", "huge2_conv2d_dilated_wgrad",
 )
 
 
@@ -83,6 +85,11 @@ def lib():
         L.huge2_plan_describe.argtypes = [dp, i32, i32, ctypes.POINTER(Segment), i32, i32p,
                                           ctypes.POINTER(Tap), i32, i32p]
         L.huge2_plan_macs.argtypes = [dp, i32, i64p, i64p]
+        L.huge2_wgrad_plan_create.argtypes = [ctypes.POINTER(vp), dp, i32]
+        L.huge2_wgrad_execute.argtypes = [vp, vp, vp, vp, vp]
+        L.huge2_wgrad_plan_destroy.argtypes = [vp]
+        L.huge2_conv2d_transpose_wgrad.argtypes = [dp, vp, vp, vp, vp]
+        L.huge2_conv2d_dilated_wgrad.argtypes = [dp, vp, vp, vp, vp]
         for name in EXPORTED[1:]:
             getattr(L, name).restype = ctypes.c_int
         L.huge2_plan_kernel.restype = ctypes.c_char_p
@@ -197,6 +204,36 @@ def huge2_plan_macs(desc, transposed):
                                  ctypes.byref(issued)), "huge2_plan_macs")
     return nz.value, issued.value
 
+def huge2_wgrad_plan_create(desc, transposed):
+    plan = ctypes.c_void_p()
+    _check(lib().huge2_wgrad_plan_create(ctypes.byref(plan), ctypes.byref(desc), int(transposed)),
+           "huge2_wgrad_plan_create")
+    return plan
+
+
+def huge2_wgrad_execute(plan, x_ptr, dy_ptr, dw_ptr, stream=0):
+    _check(lib().huge2_wgrad_execute(plan, ctypes.c_void_p(x_ptr), ctypes.c_void_p(dy_ptr),
+                                     ctypes.c_void_p(dw_ptr), ctypes.c_void_p(stream)),
+           "huge2_wgrad_execute")
+
+
+def huge2_wgrad_plan_destroy(plan):
+    _check(lib().huge2_wgrad_plan_destroy(plan), "huge2_wgrad_plan_destroy")
+
+
+def huge2_conv2d_transpose_wgrad(desc, x_ptr, dy_ptr, dw_ptr, stream=0):
+    _check(lib().huge2_conv2d_transpose_wgrad(ctypes.byref(desc), ctypes.c_void_p(x_ptr),
+                                              ctypes.c_void_p(dy_ptr), ctypes.c_void_p(dw_ptr),
+                                              ctypes.c_void_p(stream)),
+           "huge2_conv2d_transpose_wgrad")
+
+
+def huge2_conv2d_dilated_wgrad(desc, x_ptr, dy_ptr, dw_ptr, stream=0):
+    _check(lib().huge2_conv2d_dilated_wgrad(ctypes.byref(desc), ctypes.c_void_p(x_ptr),
+                                            ctypes.c_void_p(dy_ptr), ctypes.c_void_p(dw_ptr),
+                                            ctypes.c_void_p(stream)),
+           "huge2_conv2d_dilated_wgrad")
+
 
 # ---- torch conveniences -----------------------------------------------------
 
@@ -310,6 +347,69 @@ def conv2d_dilated(x, w, bias=None, stride=1, padding=0, dilation=1, layout="NCH
     huge2_conv2d_dilated(desc, x.data_ptr(), w.data_ptr(), _bias_ptr(bias, x), y.data_ptr(),
                          _stream(x))
     return y
+
+
+def _wgrad(x, dy, w_shape, transposed, stride, padding, output_padding, dilation, out):
+    torch = _torch()
+    _check_tensor(x, "x")
+    _check_tensor(dy, "dy", x.device)
+    if dy.dtype != x.dtype:
+        raise ValueError("x and dy must share a dtype")
+    w_shape = tuple(int(v) for v in w_shape)
+    if x.dim() != 4 or len(w_shape) != 4:
+        raise ValueError("x and the weight shape must be 4-D")
+    n, c_in, h, wd = x.shape
+    if transposed:
+        wc_in, c_out, r, s = w_shape
+    else:
+        c_out, wc_in, r, s = w_shape
+    if wc_in != c_in:
+        raise ValueError("weight has %d input channels, x has %d" % (wc_in, c_in))
+    desc = make_desc(n, c_in, h, wd, c_out, r, s, stride, padding, output_padding, dilation,
+                     HUGE2_NCHW, _dtype_code(x))
+    if tuple(dy.shape) != _out_shape(desc, transposed):
+        raise ValueError("dy has shape %s, the layer's output is %s"
+                         % (tuple(dy.shape), _out_shape(desc, transposed)))
+    dw = out if out is not None else torch.empty(w_shape, dtype=x.dtype, device=x.device)
+    _check_tensor(dw, "out", x.device)
+    if tuple(dw.shape) != w_shape or dw.dtype != x.dtype:
+        raise ValueError("out has the wrong shape or dtype")
+    fn = huge2_conv2d_transpose_wgrad if transposed else huge2_conv2d_dilated_wgrad
+    fn(desc, x.data_ptr(), dy.data_ptr(), dw.data_ptr(), _stream(x))
+    return dw
+
+
+def conv2d_transpose_wgrad(x, dy, w_shape, stride=1, padding=0, output_padding=0, dilation=1,
+                           out=None):
+    """Weight gradient of the transposed conv (NCHW): dw [C_in, C_out, R, S]
+    from the input x and the output error dy."""
+    return _wgrad(x, dy, w_shape, True, stride, padding, output_padding, dilation, out)
+
+
+def conv2d_dilated_wgrad(x, dy, w_shape, stride=1, padding=0, dilation=1, out=None):
+    """Weight gradient of the dilated / strided conv (NCHW): dw [C_out, C_in,
+    R, S] from the input x and the output error dy."""
+    return _wgrad(x, dy, w_shape, False, stride, padding, 0, dilation, out)
+
+
+def conv2d_transpose_dgrad(dy, w, stride=1, padding=0, dilation=1, layout="NCHW"):
+    """Data gradient of the transposed conv: the strided conv of dy with the
+    same w ([C_in, C_out, R, S] is the strided conv's [C_out, C_in, R, S])."""
+    return conv2d_dilated(dy, w, None, stride, padding, dilation, layout)
+
+
+def conv2d_dilated_dgrad(dy, w, x_hw, stride=1, padding=0, dilation=1, layout="NCHW"):
+    """Data gradient of the dilated / strided conv: the transposed conv of dy
+    with the same w, output padding chosen so that the result is x_hw."""
+    sh, sw = _pair(stride)
+    ph, pw = _pair(padding)
+    dh, dw = _pair(dilation)
+    lay = _layout_code(layout)
+    ho, wo = (dy.shape[2], dy.shape[3]) if lay == HUGE2_NCHW else (dy.shape[1], dy.shape[2])
+    r, s = w.shape[2], w.shape[3]
+    oph = x_hw[0] - ((ho - 1) * sh - 2 * ph + dh * (r - 1) + 1)
+    opw = x_hw[1] - ((wo - 1) * sw - 2 * pw + dw * (s - 1) + 1)
+    return conv2d_transpose(dy, w, None, stride, padding, (oph, opw), dilation, layout)
 
 
 class Plan:

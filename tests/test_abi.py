@@ -142,3 +142,28 @@ def test_product_path_has_no_cpu_fallback():
     for fn in os.listdir(os.path.join(ROOT, "paper_1907_11210_amd")):
         if fn.endswith(".py"):
             assert "import oracle" not in open(os.path.join(ROOT, "paper_1907_11210_amd", fn)).read()
+
+
+def test_weight_gradient_entry_points_validate_without_gpu(L, monkeypatch):
+    d = _good()
+    fake, other = ctypes.c_void_p(4096), ctypes.c_void_p(8192)
+    plan = ctypes.c_void_p(55)
+    assert L.huge2_wgrad_plan_create(None, ctypes.byref(d), 1) == h2.HUGE2_ERR_INVALID_ARG
+    assert L.huge2_wgrad_plan_create(ctypes.byref(plan), None, 1) == h2.HUGE2_ERR_INVALID_ARG
+    assert plan.value is None
+    assert L.huge2_wgrad_plan_create(ctypes.byref(plan), ctypes.byref(d), 3) == h2.HUGE2_ERR_INVALID_ARG
+    bad = _good()
+    bad.stride_h = 0
+    assert L.huge2_wgrad_plan_create(ctypes.byref(plan), ctypes.byref(bad), 1) == h2.HUGE2_ERR_INVALID_ARG
+    nhwc = _good()
+    nhwc.layout = h2.HUGE2_NHWC
+    assert L.huge2_wgrad_plan_create(ctypes.byref(plan), ctypes.byref(nhwc), 1) == h2.HUGE2_ERR_UNSUPPORTED
+    assert L.huge2_wgrad_execute(None, fake, fake, other, None) == h2.HUGE2_ERR_INVALID_ARG
+    assert L.huge2_wgrad_plan_destroy(None) == h2.HUGE2_OK
+    # one-shot forms: NULL and aliased pointers, before any allocation
+    assert L.huge2_conv2d_transpose_wgrad(ctypes.byref(d), None, fake, other, None) == h2.HUGE2_ERR_INVALID_ARG
+    assert L.huge2_conv2d_transpose_wgrad(ctypes.byref(d), fake, other, fake, None) == h2.HUGE2_ERR_INVALID_ARG
+    assert L.huge2_conv2d_dilated_wgrad(ctypes.byref(d), fake, other, other, None) == h2.HUGE2_ERR_INVALID_ARG
+    monkeypatch.setenv("HUGE2_FAULT", "alloc")
+    assert L.huge2_wgrad_plan_create(ctypes.byref(plan), ctypes.byref(d), 1) == h2.HUGE2_ERR_ALLOC
+    assert plan.value is None

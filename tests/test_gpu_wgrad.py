@@ -1,0 +1,154 @@
+"""GPU parity of the weight gradients (section 3.2.3, GAN training) through
+the C ABI, against the CPU oracle's chain-rule definitions, element by
+element with the dot-product error bound (tests/parity.py): the bound uses
+the oracle on |x| and |dy|.  Also the data gradients, which are the forward
+entry points with the roles exchanged."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1907_11210_amd import huge2 as h2
+from paper_1907_11210_amd import workloads as wl
+
+import parity as P
+
+pytestmark = pytest.mark.gpu
+
+# (name, transposed, n, c_in, h, w, c_out, r, s, stride, pad, out_pad, dil, dtype)
+CASES = [
+    ("ct_dcgan_like", True, 3, 64, 8, 8, 40, 4, 4, 2, 1, 0, 1, "bf16"),
+    ("ct_op_dil_f32", True, 2, 12, 5, 6, 20, 3, 3, 2, 1, 1, 2, "f32"),
+    ("ct_ragged", True, 5, 70, 4, 4, 130, 4, 4, 2, 1, 0, 1, "bf16"),
+    ("ct_table1_5x5", True, 2, 32, 4, 4, 24, 5, 5, 2, 2, 1, 1, "bf16"),
+    ("ct_stride1", True, 1, 16, 7, 9, 8, 3, 3, 1, 1, 0, 1, "f32"),
+    ("conv_discriminator", False, 3, 24, 16, 16, 48, 4, 4, 2, 1, 0, 1, "bf16"),
+    ("conv_dilated_f32", False, 2, 16, 12, 12, 20, 3, 3, 1, 2, 0, 2, "f32"),
+    ("conv_1x1", False, 2, 33, 5, 7, 17, 1, 1, 1, 0, 0, 1, "bf16"),
+    ("conv_aspp_like", False, 1, 64, 24, 24, 32, 3, 3, 1, 6, 0, 6, "bf16"),
+]
+
+
+def _w_shape(c):
+    _, tr, n, ci, h, w, co, r, s = c[:9]
+    return (ci, co, r, s) if tr else (co, ci, r, s)
+
+
+def _inputs(c, seed):
+    name, tr, n, ci, h, w, co, r, s, st, pd, op, dl, dt = c
+    g = torch.Generator().manual_seed(seed)
+    x = torch.randn(n, ci, h, w, generator=g)
+    if tr:
+        ho = (h - 1) * st - 2 * pd + dl * (r - 1) + op + 1
+        wo = (w - 1) * st - 2 * pd + dl * (s - 1) + op + 1
+    else:
+        ho = (h + 2 * pd - dl * (r - 1) - 1) // st + 1
+        wo = (w + 2 * pd - dl * (s - 1) - 1) // st + 1
+    dy = torch.randn(n, co, ho, wo, generator=g)
+    dtype = wl.torch_dtype(dt)
+    return x.to(dtype), dy.to(dtype)
+
+
+def _oracle(c, xq, dyq, absolute=False):
+    name, tr, n, ci, h, w, co, r, s, st, pd, op, dl, dt = c
+    x, dy = xq.double().numpy(), dyq.double().numpy()
+    if absolute:
+        x, dy = np.abs(x), np.abs(dy)
+    if tr:
+        return oracle.conv2d_transpose_wgrad(x, dy, _w_shape(c), st, pd, op, dl)
+    return oracle.conv2d_dilated_wgrad(x, dy, _w_shape(c), st, pd, dl)
+
+
+def _gpu(c, xq, dyq):
+    name, tr, n, ci, h, w, co, r, s, st, pd, op, dl, dt = c
+    dev = torch.device("cuda", 0)
+    x, dy = xq.to(dev), dyq.to(dev)
+    if tr:
+        dw = h2.conv2d_transpose_wgrad(x, dy, _w_shape(c), st, pd, op, dl)
+    else:
+        dw = h2.conv2d_dilated_wgrad(x, dy, _w_shape(c), st, pd, dl)
+    torch.cuda.synchronize()
+    return dw.cpu().double().numpy()
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: c[0])
+def test_weight_gradient(case):
+    P.say("case", case)
+    xq, dyq = _inputs(case, seed=5)
+    ref, absref = _oracle(case, xq, dyq), _oracle(case, xq, dyq, absolute=True)
+    got = _gpu(case, xq, dyq)
+    P.check(got, ref, absref, case[-1], case[0])
+
+
+@pytest.mark.parametrize("case", [CASES[0], CASES[5]], ids=lambda c: c[0])
+def test_weight_gradient_chunks(case, monkeypatch):
+    """Images split into chunks (one per image here): the fp32 gradient is
+    accumulated over the chunks in order; same bar, and deterministic."""
+    monkeypatch.setenv("HUGE2_WGRAD_CHUNK", "1")
+    P.say("case", case, "one image per chunk")
+    xq, dyq = _inputs(case, seed=6)
+    ref, absref = _oracle(case, xq, dyq), _oracle(case, xq, dyq, absolute=True)
+    got = _gpu(case, xq, dyq)
+    P.check(got, ref, absref, case[-1], case[0])
+    again = _gpu(case, xq, dyq)
+    assert np.array_equal(got, again)
+
+
+def test_weight_gradient_plan_reuse():
+    """One plan, two calls on different data: each matches the oracle."""
+    case = CASES[2]
+    name, tr, n, ci, h, w, co, r, s, st, pd, op, dl, dt = case
+    desc = h2.make_desc(n, ci, h, w, co, r, s, st, pd, op, dl, h2.HUGE2_NCHW, h2.HUGE2_BF16)
+    plan = h2.huge2_wgrad_plan_create(desc, 1)
+    dev = torch.device("cuda", 0)
+    try:
+        for seed in (7, 8):
+            xq, dyq = _inputs(case, seed)
+            x, dy = xq.to(dev), dyq.to(dev)
+            dw = torch.empty(_w_shape(case), dtype=x.dtype, device=dev)
+            h2.huge2_wgrad_execute(plan, x.data_ptr(), dy.data_ptr(), dw.data_ptr(),
+                                   torch.cuda.current_stream().cuda_stream)
+            torch.cuda.synchronize()
+            P.check(dw.cpu().double().numpy(), _oracle(case, xq, dyq),
+                    _oracle(case, xq, dyq, absolute=True), dt, name)
+    finally:
+        h2.huge2_wgrad_plan_destroy(plan)
+
+
+def test_dcgan_layer_weight_gradient_full_size():
+    """The generator's second layer (512 -> 256, 8x8 -> 16x16, batch 64) in
+    full, checked element by element against the oracle."""
+    case = ("dcgan_l2_wgrad", True, 64, 512, 8, 8, 256, 4, 4, 2, 1, 0, 1, "bf16")
+    P.say("case", case)
+    xq, dyq = _inputs(case, seed=9)
+    got = _gpu(case, xq, dyq)
+    P.check(got, _oracle(case, xq, dyq), _oracle(case, xq, dyq, absolute=True), "bf16", case[0])
+
+
+def test_data_gradients_are_the_exchanged_forward_forms():
+    """dx of the transposed conv = strided conv of dy with the same w; dx of
+    the strided conv = transposed conv of dy; both against the oracle."""
+    dev = torch.device("cuda", 0)
+    g = torch.Generator().manual_seed(10)
+    # transposed conv 64 -> 32, k4 s2 p1, 6x6 -> 12x12
+    w = (torch.randn(64, 32, 4, 4, generator=g) * 0.1).to(torch.bfloat16)
+    dy = torch.randn(2, 32, 12, 12, generator=g).to(torch.bfloat16)
+    dx = h2.conv2d_transpose_dgrad(dy.to(dev), w.to(dev), 2, 1, 1).cpu().double().numpy()
+    assert dx.shape == (2, 64, 6, 6)
+    ref = oracle.conv2d_dilated_alg2(dy.double().numpy(), w.double().numpy(), None, 2, 1, 1)
+    absref = oracle.conv2d_dilated_alg2(np.abs(dy.double().numpy()), np.abs(w.double().numpy()),
+                                        None, 2, 1, 1)
+    P.check(dx, ref, absref, "bf16", "transpose dgrad")
+    # strided conv 16 -> 24, k3 s2 p1, 11x11 -> 6x6: dx back to 11x11
+    w2 = (torch.randn(24, 16, 3, 3, generator=g) * 0.1).to(torch.bfloat16)
+    dy2 = torch.randn(2, 24, 6, 6, generator=g).to(torch.bfloat16)
+    dx2 = h2.conv2d_dilated_dgrad(dy2.to(dev), w2.to(dev), (11, 11), 2, 1, 1).cpu().double().numpy()
+    assert dx2.shape == (2, 16, 11, 11)
+    ref2 = oracle.conv2d_transpose_alg1(dy2.double().numpy(), w2.double().numpy(), None, 2, 1, 0, 1)
+    absref2 = oracle.conv2d_transpose_alg1(np.abs(dy2.double().numpy()), np.abs(w2.double().numpy()),
+                                           None, 2, 1, 0, 1)
+    P.check(dx2, ref2, absref2, "bf16", "dilated dgrad")
+    # and the adjoint relation the data gradient must satisfy, in float64
+    x2 = np.random.default_rng(3).standard_normal((2, 16, 11, 11))
+    y2 = oracle.conv2d_dilated_alg2(x2, w2.double().numpy(), None, 2, 1, 1)
+    assert abs(np.sum(y2 * dy2.double().numpy()) - np.sum(x2 * ref2)) < 1e-9 * np.sum(np.abs(y2 * dy2.double().numpy()))

@@ -888,6 +888,7 @@ struct huge2_wgrad_plan {
   int hs, ws, hb, wb;  // small / big pixel grids
   int chunk;           // images per chunk
   int kp;              // padded K of a full chunk
+  int ksplit;          // K ranges per tap (workgroups along K)
   void* st;
   void* bt;
   float* g;
@@ -934,8 +935,15 @@ huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, i
     if (forced > 0 && forced < chunk) chunk = forced;
   }
   const long long kp = (chunk * hws + 63) / 64 * 64;
+  // split K so that the GEMM has about four workgroups per compute unit,
+  // each split keeping at least 8 K stages
+  const long long tiles = taps * ((p->ms + 63) / 64) * ((p->nb + 63) / 64);
+  const long long stages = kp * esz / 128;
+  long long ksplit = std::max(1ll, (4ll * kComputeUnits + tiles - 1) / tiles);
+  ksplit = std::max(1ll, std::min(ksplit, stages / 8));
+  ksplit = std::min(ksplit, 64ll);
   const long long st_b = p->ms * kp * esz, bt_b = taps * p->nb * kp * esz;
-  const long long g_b = taps * p->ms * p->nb * 4;
+  const long long g_b = ksplit * taps * p->ms * p->nb * 4;
   const long long big_b = (long long)d.n * p->nb * p->hb * p->wb * esz;
   const long long small_b = (long long)d.n * p->ms * hws * esz;
   if (st_b >= (1ll << 31) || bt_b >= (1ll << 31) || g_b >= (1ll << 31) || big_b >= (1ll << 40) ||
@@ -945,6 +953,7 @@ huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, i
   }
   p->chunk = (int)chunk;
   p->kp = (int)kp;
+  p->ksplit = (int)ksplit;
   if (fault("alloc") || hipMalloc(&p->st, st_b) != hipSuccess || hipMalloc(&p->bt, bt_b) != hipSuccess ||
       hipMalloc((void**)&p->g, g_b) != hipSuccess) {
     (void)hipGetLastError();
@@ -973,6 +982,7 @@ huge2_status wgrad_execute(const huge2_wgrad_plan* p, const void* x, const void*
   a.r = d.r, a.s = d.s;
   a.stride_h = d.stride_h, a.stride_w = d.stride_w, a.pad_h = d.pad_h, a.pad_w = d.pad_w;
   a.dil_h = d.dil_h, a.dil_w = d.dil_w;
+  a.ksplit = p->ksplit;
   const long long hws = (long long)p->hs * p->ws;
   // chunks in order: the first writes the fp32 gradient, the rest add to it
   for (int img0 = 0; img0 < d.n; img0 += p->chunk) {

@@ -1553,39 +1553,77 @@ hipError_t launch_pack_weights(const void* w, void* wp, int dtype, bool transpos
 // grid, so that every tap's gradient is one dense GEMM over pixels with no
 // zero products; the GEMM then runs on MFMA with both operands K-contiguous.
 
-// Staging of one image chunk: St (element-wise transpose of the image and
-// channel axes) and Bt (the tap gather), zero up to kp.
+// Staging of one image chunk: St (the image and channel axes exchanged) and
+// Bt (the tap gather), zero up to kp.  A thread produces 8 consecutive k of
+// one row and writes them with one 16-byte store (kp is a multiple of 64).
+// When rows of the small grid are a multiple of 8 (the usual case), the 8 k
+// lie in one row: St takes one 16-byte load, Bt one row of the big tensor at
+// the stride; otherwise each element is located on its own.  Indices fit 32
+// bits (the staged buffers stay below 2^31 bytes).
 template <typename T>
 __global__ __launch_bounds__(256) void wgrad_stage_kernel(WgArgs a) {
-  const long long hws = (long long)a.hs * a.ws;
-  const long long kreal = (long long)a.nimg * hws;
-  const long long st_total = (long long)a.ms * a.kp;
-  const long long bt_total = (long long)a.r * a.s * a.nb * a.kp;
-  const long long stride = (long long)gridDim.x * blockDim.x;
-  for (long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x; e < st_total + bt_total; e += stride) {
-    if (e < st_total) {
-      const long long k = e % a.kp, m = e / a.kp;
-      T v = T(0);
-      if (k < kreal) {
-        const long long il = k / hws, q = k - il * hws;
-        v = ((const T*)a.sm)[((a.img0 + il) * a.ms + m) * hws + q];
+  constexpr int V = 8;
+  const uint32_t hws = (uint32_t)a.hs * (uint32_t)a.ws;
+  const uint32_t kreal = (uint32_t)a.nimg * hws;
+  const uint32_t kv = (uint32_t)a.kp / V;
+  const uint32_t st_total = (uint32_t)a.ms * kv;
+  const uint32_t total = st_total + (uint32_t)(a.r * a.s * a.nb) * kv;
+  const bool rows8 = a.ws % V == 0;
+  const T* sm = (const T*)a.sm;
+  const T* bg = (const T*)a.bg;
+  for (uint32_t e = blockIdx.x * blockDim.x + threadIdx.x; e < total; e += gridDim.x * blockDim.x) {
+    T v[V];
+    const bool is_st = e < st_total;
+    const uint32_t f = is_st ? e : e - st_total;
+    const uint32_t row = f / kv, k0 = (f - row * kv) * V;
+    T* dst = (is_st ? (T*)a.st : (T*)a.bt) + (size_t)row * a.kp + k0;
+    const uint32_t il0 = k0 / hws, q0 = k0 - il0 * hws;
+    const uint32_t qh0 = q0 / (uint32_t)a.ws, qw0 = q0 - qh0 * (uint32_t)a.ws;
+    if (is_st) {
+      const size_t base = ((size_t)(a.img0 + il0) * a.ms + row) * hws;
+      if (rows8 && k0 < kreal) {
+        __builtin_memcpy(v, sm + base + q0, sizeof(v));
+      } else {
+#pragma unroll
+        for (int t = 0; t < V; ++t) {
+          const uint32_t k = k0 + t, il = k / hws, q = k - il * hws;
+          v[t] = k < kreal ? sm[((size_t)(a.img0 + il) * a.ms + row) * hws + q] : T(0);
+        }
       }
-      ((T*)a.st)[e] = v;
     } else {
-      const long long f = e - st_total;
-      const long long k = f % a.kp, t2 = f / a.kp;
-      const int n = (int)(t2 % a.nb), tap = (int)(t2 / a.nb);
+      const int n = (int)(row % (uint32_t)a.nb), tap = (int)(row / (uint32_t)a.nb);
       const int kh = tap / a.s, kw = tap - kh * a.s;
-      T v = T(0);
-      if (k < kreal) {
-        const long long il = k / hws, q = k - il * hws;
-        const int qh = (int)(q / a.ws), qw = (int)(q - (long long)qh * a.ws);
-        const int ih = qh * a.stride_h - a.pad_h + kh * a.dil_h;
-        const int iw = qw * a.stride_w - a.pad_w + kw * a.dil_w;
-        if (ih >= 0 && ih < a.hb && iw >= 0 && iw < a.wb)
-          v = ((const T*)a.bg)[(((a.img0 + il) * a.nb + n) * (long long)a.hb + ih) * a.wb + iw];
+      if (rows8 && k0 < kreal) {
+        const int ih = (int)qh0 * a.stride_h - a.pad_h + kh * a.dil_h;
+        const int iw0 = (int)qw0 * a.stride_w - a.pad_w + kw * a.dil_w;
+        const bool row_in = ih >= 0 && ih < a.hb;
+        const T* src = bg + (((size_t)(a.img0 + il0) * a.nb + n) * a.hb + (row_in ? ih : 0)) * a.wb;
+#pragma unroll
+        for (int t = 0; t < V; ++t) {
+          const int iw = iw0 + t * a.stride_w;
+          v[t] = (row_in && iw >= 0 && iw < a.wb) ? src[iw] : T(0);
+        }
+      } else {
+#pragma unroll
+        for (int t = 0; t < V; ++t) {
+          const uint32_t k = k0 + t;
+          v[t] = T(0);
+          if (k < kreal) {
+            const uint32_t il = k / hws, q = k - il * hws;
+            const int qh = (int)(q / (uint32_t)a.ws), qw = (int)(q - (uint32_t)qh * (uint32_t)a.ws);
+            const int ih = qh * a.stride_h - a.pad_h + kh * a.dil_h;
+            const int iw = qw * a.stride_w - a.pad_w + kw * a.dil_w;
+            if (ih >= 0 && ih < a.hb && iw >= 0 && iw < a.wb)
+              v[t] = bg[(((size_t)(a.img0 + il) * a.nb + n) * a.hb + ih) * a.wb + iw];
+          }
+        }
       }
-      ((T*)a.bt)[f] = v;
+    }
+#pragma unroll
+    for (int t = 0; t < V; t += 16 / (int)sizeof(T)) {
+      uint4 u;
+      __builtin_memcpy(&u, &v[t], 16);
+      *(uint4*)(dst + t) = u;
     }
   }
 }
@@ -1604,7 +1642,9 @@ __global__ __launch_bounds__(256) void wgrad_gemm_kernel(WgArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave & 1, wn = wave >> 1;
-  const int m0 = blockIdx.x * 64, n0 = blockIdx.y * 64, tap = blockIdx.z;
+  const int taps = a.r * a.s;
+  const int m0 = blockIdx.x * 64, n0 = blockIdx.y * 64, tap = blockIdx.z % taps;
+  const int split = blockIdx.z / taps;
   // this thread's two rows of each operand (rows past the end repeat the last)
   const int chunk = tid & 7, row = tid >> 3;  // 8 chunks of 16 bytes per row
   const char* const st = (const char*)a.st;
@@ -1658,21 +1698,26 @@ __global__ __launch_bounds__(256) void wgrad_gemm_kernel(WgArgs a) {
       }
     }
   };
-  const int nk = a.kp / KC;
-  store(0, load(0));
-  __syncthreads();
-  for (int ks = 0; ks < nk; ++ks) {
-    // the next stage's loads (stage 0 again past the end: unused) overlap
-    // this stage's MFMAs
-    const Regs nx = load(ks + 1 < nk ? ks + 1 : 0);
-    compute(ks & 1);
-    if (ks + 1 < nk) store((ks + 1) & 1, nx);
+  // this split's K stages [k_lo, k_hi)
+  const int nk_all = a.kp / KC;
+  const int per = (nk_all + a.ksplit - 1) / a.ksplit;
+  const int k_lo = min(split * per, nk_all), k_hi = min(k_lo + per, nk_all);
+  if (k_hi > k_lo) {
+    store(0, load(k_lo));
     __syncthreads();
+    for (int ks = k_lo; ks < k_hi; ++ks) {
+      // the next stage's loads (the first again past the end: unused)
+      // overlap this stage's MFMAs
+      const Regs nx = load(ks + 1 < k_hi ? ks + 1 : k_lo);
+      compute((ks - k_lo) & 1);
+      if (ks + 1 < k_hi) store((ks + 1 - k_lo) & 1, nx);
+      __syncthreads();
+    }
   }
   // acc: lane holds m = m0 + wm*32 + lane%32 (MFMA column: the St operand went
   // second) and n = n0 + wn*32 + 8*(r/4) + 4*(lane/32) + r%4 (rows)
   const int m = m0 + wm * 32 + (lane & 31);
-  float* gt = a.g + ((size_t)tap * a.ms + min(m, a.ms - 1)) * a.nb;
+  float* gt = a.g + (((size_t)split * taps + tap) * a.ms + min(m, a.ms - 1)) * a.nb;
   const bool acc_in = a.accumulate != 0;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
@@ -1682,20 +1727,22 @@ __global__ __launch_bounds__(256) void wgrad_gemm_kernel(WgArgs a) {
   }
 }
 
-// dw[m][n][tap] from G[tap][m][n], rounded to the dtype.
+// dw[m][n][tap] from the splits of G[split][tap][m][n] (summed in order),
+// rounded to the dtype: a thread per (tap, m, n), (m, n) fastest so that the
+// reads of G coalesce.
 template <bool BF16>
 __global__ __launch_bounds__(256) void wgrad_store_kernel(WgArgs a) {
   const int taps = a.r * a.s;
-  const long long total = (long long)a.ms * a.nb * taps;
-  for (long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x; e < total;
-       e += (long long)gridDim.x * blockDim.x) {
-    const int tap = (int)(e % taps);
-    const long long mn = e / taps;
-    const float v = a.g[(long long)tap * a.ms * a.nb + mn];
+  const uint32_t mn_total = (uint32_t)a.ms * (uint32_t)a.nb;
+  const uint32_t total = mn_total * (uint32_t)taps;
+  for (uint32_t e = blockIdx.x * blockDim.x + threadIdx.x; e < total; e += gridDim.x * blockDim.x) {
+    const uint32_t tap = e / mn_total, mn = e - tap * mn_total;
+    float v = 0.f;
+    for (int sp = 0; sp < a.ksplit; ++sp) v += a.g[(size_t)sp * total + e];
     if constexpr (BF16)
-      ((uint16_t*)a.dw)[e] = f32_to_bf16_rne(v);
+      ((uint16_t*)a.dw)[(size_t)mn * taps + tap] = f32_to_bf16_rne(v);
     else
-      ((float*)a.dw)[e] = v;
+      ((float*)a.dw)[(size_t)mn * taps + tap] = v;
   }
 }
 
@@ -1705,7 +1752,7 @@ static dim3 grid_for(long long total) {
 }
 
 hipError_t launch_wgrad_stage(const WgArgs& a, int dtype, hipStream_t stream) {
-  const long long total = (long long)a.ms * a.kp + (long long)a.r * a.s * a.nb * a.kp;
+  const long long total = ((long long)a.ms * a.kp + (long long)a.r * a.s * a.nb * a.kp) / 8;
   if (dtype == 1)
     hipLaunchKernelGGL(wgrad_stage_kernel<uint16_t>, grid_for(total), dim3(256), 0, stream, a);
   else
@@ -1714,7 +1761,7 @@ hipError_t launch_wgrad_stage(const WgArgs& a, int dtype, hipStream_t stream) {
 }
 
 hipError_t launch_wgrad_gemm(const WgArgs& a, int dtype, hipStream_t stream) {
-  const dim3 grid((a.ms + 63) / 64, (a.nb + 63) / 64, a.r * a.s);
+  const dim3 grid((a.ms + 63) / 64, (a.nb + 63) / 64, a.r * a.s * a.ksplit);
   if (dtype == 1)
     hipLaunchKernelGGL(wgrad_gemm_kernel<true>, grid, dim3(256), 0, stream, a);
   else

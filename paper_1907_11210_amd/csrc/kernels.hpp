@@ -253,20 +253,23 @@ hipError_t launch_quad(const QArgs& a, hipStream_t stream);
 //  - wgrad_stage: St[m][k] = S[image][m][q] and Bt[tap][n][k] = B at the tap
 //    position (zero outside), k = local image * hws + q, zero up to kp (a
 //    multiple of 64): the untangled copies of the big tensor, one per tap;
-//  - wgrad_gemm: G[tap] (fp32) = (or +=) St Bt[tap]^T on MFMA;
-//  - wgrad_store: dw[(m * nb + n) * taps + tap] = G[tap][m][n] in the dtype.
+//  - wgrad_gemm: G[split][tap] (fp32) = (or +=) St Bt[tap]^T over the
+//    split's K range, on MFMA;
+//  - wgrad_store: dw[(m * nb + n) * taps + tap] = sum over the splits (in
+//    order) of G[split][tap][m][n], in the dtype.
 struct WgArgs {
   const void* sm;  // small tensor [n][ms][hs][ws] (NCHW)
   const void* bg;  // big tensor [n][nb][hb][wb]
   void* st;       // [ms][kp]
   void* bt;       // [taps][nb][kp]
-  float* g;       // [taps][ms][nb]
+  float* g;       // [ksplit][taps][ms][nb]
   void* dw;       // [ms][nb][r][s]
   int img0, nimg;  // image chunk
   int ms, nb, hs, ws, hb, wb, r, s;
   int stride_h, stride_w, pad_h, pad_w, dil_h, dil_w;
   int kp;          // padded K of the chunk (multiple of 64)
   int accumulate;  // 0: G = product, 1: G += product
+  int ksplit;      // K ranges per tap, each with its own fp32 slice of G
 };
 hipError_t launch_wgrad_stage(const WgArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_wgrad_gemm(const WgArgs& a, int dtype, hipStream_t stream);

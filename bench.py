@@ -63,7 +63,11 @@ DESCRIPTIONS = {
                     "(4->8), 512->256, 256->128, 128->3 (32->64), bf16 NCHW, batch 1",
     "table1_cgan": "the paper's Table 1 cGAN deconvolutions: ConvT k4 s2 p1 256->128 (8->16), "
                    "128->3 (16->32), bf16 NCHW, batch 1",
+    "dcgan_wgrad": "training (section 3.2.3): weight gradients of the DCGAN generator's four "
+                   "ConvT layers (k4 s2 p1, 1024->512->256->128->3, bf16 NCHW, batch 64) from "
+                   "their inputs and seeded output errors",
 }
+WGRAD_WORKLOADS = {"dcgan_wgrad": "dcgan"}
 
 
 def parse():
@@ -310,6 +314,124 @@ def summarize_profiles(d, workload):
     print(json.dumps({"layer_mean_us": avg_us}))
 
 
+def run_wgrad(args, dev):
+    """The weight-gradient workload: one step = the weight gradient of every
+    layer (huge2_wgrad_execute: staging, MFMA GEMM, store), inputs and output
+    errors resident in HBM; FLOP = 2 x the layers' structural non-zero MACs
+    (each product of the forward pass appears once in the gradient)."""
+    import numpy as np
+    import torch
+    from paper_1907_11210_amd import huge2 as h2
+    from paper_1907_11210_amd import workloads as wl
+
+    layers = wl.WORKLOADS[WGRAD_WORKLOADS[args.workload]]
+    g = torch.Generator().manual_seed(0)
+    plans, xs, dys, dws, flops = [], [], [], [], []
+    for layer in layers:
+        dt = wl.torch_dtype(layer.dtype)
+        ho, wo = layer.out_hw()
+        xs.append(torch.randn(layer.n, layer.c_in, layer.h, layer.w, generator=g).to(dt).to(dev))
+        dys.append(torch.randn(layer.n, layer.c_out, ho, wo, generator=g).to(dt).to(dev))
+        desc = h2.make_desc(layer.n, layer.c_in, layer.h, layer.w, layer.c_out, layer.r, layer.s,
+                            layer.stride, layer.pad, layer.out_pad, layer.dil, h2.HUGE2_NCHW,
+                            h2.HUGE2_BF16 if layer.dtype == "bf16" else h2.HUGE2_F32)
+        plans.append(h2.huge2_wgrad_plan_create(desc, 1 if layer.transposed else 0))
+        dws.append(torch.empty(layer.c_in, layer.c_out, layer.r, layer.s, dtype=dt, device=dev))
+        flops.append(2 * h2.huge2_plan_macs(desc, layer.transposed)[0])
+    stream = torch.cuda.current_stream(dev).cuda_stream
+
+    def run_layer(i):
+        h2.huge2_wgrad_execute(plans[i], xs[i].data_ptr(), dys[i].data_ptr(), dws[i].data_ptr(),
+                               stream)
+
+    def step():
+        for i in range(len(layers)):
+            run_layer(i)
+
+    for _ in range(args.warmup):
+        step()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = start.elapsed_time(stop) / args.steps
+    per = []
+    for i in range(len(layers)):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            run_layer(i)
+        e1.record()
+        torch.cuda.synchronize()
+        per.append(e0.elapsed_time(e1) / args.steps)
+    dom = int(np.argmax(per))
+    peak = PEAK[layers[0].dtype]
+    achieved = flops[dom] / (per[dom] * 1e-3) / 1e12
+    out = {
+        "metric": METRIC, "value": round(sum(flops) / (ms_step * 1e-3) / 1e12, 3), "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": layers[0].dtype,
+        "data": "synthetic (seeded inputs and output errors of the layers' shapes)",
+        "config": {"workload": args.workload, "description": DESCRIPTIONS[args.workload],
+                   "batch": layers[0].n, "layout": "NCHW", "launch": "eager launches"},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": None,
+                     "kernel": "wgrad_stage + wgrad_gemm + wgrad_store (%s)" % layers[dom].name,
+                     "mean_launch_ms": round(per[dom], 5), "algorithmic_flop_per_launch": flops[dom]},
+        "layers": [{"layer": l.name, "ms": round(t, 5), "eff_tflops": round(f / (t * 1e-3) / 1e12, 2),
+                    "nz_gflop": round(f / 1e9, 3)} for l, t, f in zip(layers, per, flops)],
+        "kernel_source_sha": kernel_source_sha(), "wall_s_timed": round(wall, 3),
+    }
+    for p in plans:
+        h2.huge2_wgrad_plan_destroy(p)
+    if not args.no_cpu_baseline:
+        cb = cpu_baseline_wgrad(layers, args.cpu_seconds)
+        cb["speedup_gpu_over_oracle"] = round(out["value"] / cb["value"], 1)
+        out["cpu_baseline"] = cb
+    return out
+
+
+def cpu_baseline_wgrad(layers, target_s):
+    """The oracle's weight gradients on a batch-reduced sample of the layers."""
+    import numpy as np
+
+    import oracle
+    from paper_1907_11210_amd import huge2 as h2
+
+    oracle.build()
+    threads = os.cpu_count() or 1
+    rng = np.random.default_rng(0)
+
+    def run(batch):
+        flops, t0 = 0, time.perf_counter()
+        for l in layers:
+            ho, wo = l.out_hw()
+            x = rng.standard_normal((batch, l.c_in, l.h, l.w))
+            dy = rng.standard_normal((batch, l.c_out, ho, wo))
+            oracle.conv2d_transpose_wgrad(x, dy, (l.c_in, l.c_out, l.r, l.s), l.stride, l.pad,
+                                          l.out_pad, l.dil, nthreads=threads)
+            d = h2.make_desc(batch, l.c_in, l.h, l.w, l.c_out, l.r, l.s, l.stride, l.pad, l.out_pad,
+                             l.dil, h2.HUGE2_NCHW, h2.HUGE2_F32)
+            flops += 2 * h2.huge2_plan_macs(d, 1)[0]
+        return flops, time.perf_counter() - t0
+
+    full = layers[0].n
+    flops, secs = run(1)
+    batch = 1
+    if secs < target_s and full > 1:
+        batch = int(min(full, max(1, target_s / max(secs, 1e-3))))
+        if batch > 1:
+            flops, secs = run(batch)
+    return {"value": flops / secs / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": "the %d layers' weight gradients at batch %d of %d (float64), %.1f s"
+                      % (len(layers), batch, full, secs), "seconds": secs}
+
+
 def library_reference(layer, steps, dev):
     """The vendor library's dense GEMM with the M x N x K of the layer's phase
     GEMMs: a calibration of what this GPU reaches on that contraction size."""
@@ -420,6 +542,9 @@ def main():
     dev = torch.device("cuda", 0)
     if args.copy_calibration:
         copy_calibration(dev)
+        return
+    if args.workload in WGRAD_WORKLOADS:
+        print(json.dumps(run_wgrad(args, dev)), flush=True)
         return
     items, plans, step, step_outputs, step_input = build_workload(args.workload, dev)
     flops = layer_flops(plans)

@@ -369,10 +369,14 @@ bool rowphase_shape(const huge2_conv_desc& d, bool transposed, RpArgs* z, int64_
 // with stride 2, a 4x4 kernel, padding 1, dilation 1 and no output padding
 // (so every phase has 2x2 taps at input offsets in [-1, 1] and the input's
 // pixel grid), input channels a multiple of 64, and a width of at least 4
-// that tiles 64 positions per workgroup: whole images of h*w <= 64 pixels
-// (h*w dividing 64, a multiple of 8), or 64/w full rows (w dividing 64, h a
-// multiple of 64/w).  Returns false otherwise (or with HUGE2_QUAD=0, or a
-// GEMM tile forced).
+// that tiles P = 64 (or 128) positions per workgroup: whole images of
+// h*w <= P pixels (h*w dividing P, a multiple of 8), or P/w full rows (w
+// dividing P, h a multiple of P/w).  Returns false otherwise (or with
+// HUGE2_QUAD=0, or a GEMM tile forced).
+//
+// 128 positions per workgroup (np = 4) halve the weight bytes per
+// multiply-add; they are taken when they still give every compute unit a
+// workgroup of 64 channels (DCGAN L3: 32.5 -> 29.4 us).
 bool quad_shape(const huge2_conv_desc& d, bool transposed, QArgs* q, int64_t* issued) {
   if (!transposed || d.layout != HUGE2_NCHW || d.dtype != HUGE2_BF16) return false;
   if (env_int("HUGE2_QUAD", 1) == 0 || env_int("HUGE2_TILE", -1) >= 0) return false;
@@ -380,37 +384,63 @@ bool quad_shape(const huge2_conv_desc& d, bool transposed, QArgs* q, int64_t* is
       d.pad_w != 1 || d.dil_h != 1 || d.dil_w != 1 || d.out_pad_h != 0 || d.out_pad_w != 0)
     return false;
   if (d.c_in % 64 != 0 || d.w < 4) return false;
-  int ni, qbh;
   const long long hw = (long long)d.h * d.w;
-  if (hw <= kQuadPix) {
-    if (kQuadPix % hw != 0 || hw % 8 != 0) return false;
-    ni = (int)(kQuadPix / hw);
-    qbh = d.h;
-  } else {
-    if (d.w > kQuadPix || kQuadPix % d.w != 0) return false;
-    ni = 1;
-    qbh = kQuadPix / d.w;
-    if (d.h % qbh != 0) return false;
-  }
-  if (ni * (qbh + 2) * (d.w + 2) > kQuadHaloRows) return false;
-  const int igroups = (d.n + ni - 1) / ni, hblocks = d.h / qbh;
-  // 64-channel tiles: two waves of 32 channels per phase, or (HUGE2_QUAD_WCH=2,
-  // an even number of 64-channel K blocks) two K groups of one wave of 64
-  // channels per phase; 32-channel tiles in two K groups when 64-channel
-  // tiles would leave compute units idle
   const bool keven = (d.c_in / 64) % 2 == 0;
-  int nch = 2, ks = 1;
-  const long long wg64 = (long long)igroups * hblocks * ((d.c_out + 63) / 64);
-  if (wg64 < kComputeUnits && keven) {
-    nch = 1;
-    ks = 2;
-  } else if (keven && env_int("HUGE2_QUAD_WCH", 1) == 2) {
-    ks = 2;
+  // images and rows per workgroup for pix positions; false if the shape
+  // does not tile or the halo tile or the input items per thread overflow
+  auto tiling = [&](int pix, int ks, int* ni, int* qbh) {
+    if (hw <= pix) {
+      if (pix % hw != 0 || hw % 8 != 0) return false;
+      *ni = (int)(pix / hw);
+      *qbh = d.h;
+    } else {
+      if (d.w > pix || pix % d.w != 0) return false;
+      *ni = 1;
+      *qbh = pix / d.w;
+      if (d.h % *qbh != 0) return false;
+    }
+    if (*ni * (*qbh + 2) * (d.w + 2) > kQuadHaloRows) return false;
+    // loaded rows per block: at most min(h, qbh + 2)
+    const long long items = (long long)*ni * std::min(d.h, *qbh + 2) * d.w / 2 * 8;
+    return items <= (long long)kQuadMaxPieces * (kQuadThreads / ks);
+  };
+  auto wgs_for = [&](int ni, int qbh, int nch) {
+    return (long long)((d.n + ni - 1) / ni) * (d.h / qbh) * ((d.c_out + 32 * nch - 1) / (32 * nch));
+  };
+  int ni = 0, qbh = 0, np = 0, nch = 2, ks = 1;
+  const int np_env = env_int("HUGE2_QUAD_NP", 0);  // 0: by shape; 2 or 4: forced
+  const int ks_env = env_int("HUGE2_QUAD_KS", 0);  // 128 positions: K groups forced
+  if (np_env != 2) {
+    // 128 positions: 64-channel tiles (two waves of 32 channels per phase)
+    // if every compute unit gets one.  32-channel tiles in two K groups are
+    // taken only when forced (measured slower than 64 positions on DCGAN L2)
+    for (int cand = 0; cand < 2 && np == 0; ++cand) {
+      const int cks = cand == 0 ? 1 : 2, cnch = cand == 0 ? 2 : 1;
+      if ((cks == 2 && (!keven || np_env != 4)) || (ks_env != 0 && ks_env != cks)) continue;
+      if (!tiling(128, cks, &ni, &qbh)) continue;
+      if (np_env != 4 && wgs_for(ni, qbh, cnch) < kComputeUnits) continue;
+      np = 4;
+      nch = cnch;
+      ks = cks;
+    }
+    if (np == 0 && np_env == 4) return false;
   }
-  // loaded rows per block: at most min(h, qbh + 2); input items (pixel pair x
-  // 8 channels) per thread bounded
-  const long long items = (long long)ni * std::min(d.h, qbh + 2) * d.w / 2 * 8;
-  if (items > (long long)kQuadMaxPieces * (kQuadThreads / ks)) return false;
+  if (np == 0) {
+    // 64 positions.  64-channel tiles: two waves of 32 channels per phase,
+    // or (HUGE2_QUAD_WCH=2, an even number of 64-channel K blocks) two K
+    // groups of one wave of 64 channels per phase; 32-channel tiles in two K
+    // groups when 64-channel tiles would leave compute units idle
+    np = 2;
+    if (!tiling(64, 1, &ni, &qbh)) return false;
+    if (wgs_for(ni, qbh, 2) < kComputeUnits && keven) {
+      nch = 1;
+      ks = 2;
+    } else if (keven && env_int("HUGE2_QUAD_WCH", 1) == 2) {
+      ks = 2;
+    }
+    if (!tiling(64, ks, &ni, &qbh)) return false;
+  }
+  const int igroups = (d.n + ni - 1) / ni, hblocks = d.h / qbh;
   const long long x_bytes = (long long)d.n * d.c_in * hw * 2;
   if (x_bytes >= (1ll << 31)) return false;
   std::memset(q, 0, sizeof(*q));
@@ -423,6 +453,7 @@ bool quad_shape(const huge2_conv_desc& d, bool transposed, QArgs* q, int64_t* is
   q->cout_pad = round_up(d.c_out, 32 * nch);
   q->ni = ni;
   q->qbh = qbh;
+  q->np = np;
   q->nch = nch;
   q->ks = ks;
   q->igroups = igroups;
@@ -430,7 +461,9 @@ bool quad_shape(const huge2_conv_desc& d, bool transposed, QArgs* q, int64_t* is
   q->ntiles = q->cout_pad / (32 * nch);
   const long long wgs = (long long)q->ntiles * igroups * hblocks;
   q->depth = env_int("HUGE2_QUAD_DEPTH", 2);
-  if ((q->depth != 2 && q->depth != 4 && q->depth != 8) || (nch == 2 && ks == 2)) q->depth = 2;
+  if ((q->depth != 2 && q->depth != 4 && q->depth != 8) || (nch == 2 && ks == 2) ||
+      (np == 4 && q->depth == 8))
+    q->depth = 2;
   const long long wp_bytes = 16ll * q->cout_pad * d.c_in * 2;
   if (wp_bytes >= (1ll << 31)) return false;
   q->wp_bytes = (uint32_t)wp_bytes;
@@ -445,9 +478,9 @@ bool quad_shape(const huge2_conv_desc& d, bool transposed, QArgs* q, int64_t* is
           q->dh[2 * rh + rw][2 * th + tw] = (int8_t)((rh + d.pad_h - kh) / 2);
           q->dw[2 * rh + rw][2 * th + tw] = (int8_t)((rw + d.pad_w - kw) / 2);
         }
-  // issued multiply-adds: per workgroup 4 phases x 64 positions x 32*nch
+  // issued multiply-adds: per workgroup 4 phases x 32*np positions x 32*nch
   // channels x 4 taps x c_in
-  *issued = wgs * 4 * kQuadPix * 32 * nch * 4 * (long long)d.c_in;
+  *issued = wgs * 4 * (32 * np) * 32 * nch * 4 * (long long)d.c_in;
   return true;
 }
 

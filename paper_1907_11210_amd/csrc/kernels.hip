@@ -20,6 +20,8 @@ namespace huge2 {
 typedef __attribute__((ext_vector_type(16))) float f32x16;
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+
 // Workgroups are dealt to the 8 XCDs round-robin (id mod 8).  Map them so
 // that each XCD runs one contiguous run of the work list: neighbouring
 // tiles share input rows and weight blocks, which then stay in that XCD's L2.
@@ -1209,9 +1211,11 @@ hipError_t launch_rowphase(const RpArgs& a, hipStream_t stream) {
 // Stride-2 transposed conv with a 4x4 kernel and padding 1 (NCHW, bf16), the
 // DCGAN/cGAN generator layer.  Each of its four output phases has 2x2 taps
 // whose input offsets lie in [-1, 1], and each phase's pixel grid is the
-// input grid (section 3.1).  A workgroup takes 64 input positions (ni images
-// x qbh rows x the full width) and 32*nch output channels, and computes the
-// four phases there:
+// input grid (section 3.1).  A workgroup takes 32*NP input positions (ni
+// images x qbh rows x the full width) and 32*nch output channels, and
+// computes the four phases there.  Each weight fragment a wave loads feeds
+// NP MFMAs, so NP = 4 halves the weight bytes per multiply-add that reach
+// the compute unit from L2:
 //  - per 64-channel K block, the input block plus a one-pixel halo is read
 //    straight from the NCHW planes into an LDS tile of channel-contiguous
 //    pixel rows: a thread loads one pixel pair of 8 channels (8 dword loads,
@@ -1228,7 +1232,7 @@ hipError_t launch_rowphase(const RpArgs& a, hipStream_t stream) {
 //    (the scatter of section 3.1) and written with 16-byte stores.
 // With two K groups, group 1 hands its partial sums to group 0 through LDS in
 // a fixed order (deterministic).
-template <int KS, int WCH, int DEPTH>
+template <int KS, int WCH, int DEPTH, int NP>
 __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
   constexpr int NT = kQuadThreads;
   constexpr int NTG = NT / KS;  // threads of one K group
@@ -1238,8 +1242,16 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
   constexpr uint32_t OOB = 0x80000000u;
   static_assert(DEPTH == 2 || DEPTH == 4 || DEPTH == 8, "weight stages in flight");
   static_assert(KS == 2 || WCH == 1, "one K group: two waves of 32 channels per phase");
+  static_assert(NP == 2 || (NP == 4 && WCH == 1), "32-position blocks per wave");
   constexpr int U = DEPTH > 4 ? DEPTH / 4 : 1;  // K blocks per unrolled loop step
-  __shared__ __attribute__((aligned(16))) char smem[KS * 2 * HALO_B];
+  // LDS: the K groups' double-buffered halo tiles, reused after the main loop
+  // for group 1's partial sums and then for the interleaved output block
+  // (64 channels x 4 phases x 32*NP positions, rows padded by 16 bytes)
+  constexpr int TILE_B = KS * 2 * HALO_B;
+  constexpr int RED_B = KS > 1 ? 4 * WCH * NP * 16 * 64 * 4 : 0;
+  constexpr int OUT_B = 64 * (4 * 32 * NP + 8) * 2;
+  constexpr int SMEM_B = cmax(TILE_B, cmax(RED_B, OUT_B));
+  __shared__ __attribute__((aligned(16))) char smem[SMEM_B];
   __shared__ float s_bias[64];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -1321,9 +1333,9 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
 
   // This wave's pixels: q = 32 i + lane % 32; LDS byte offset of its halo
   // pixel at tap offset (0, 0), plus the lane half's 64 bytes of K.
-  int lrow[2];
+  int lrow[NP];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < NP; ++i) {
     const int q = 32 * i + (lane & 31);
     const int per_img = a.qbh * a.w;
     const int il = q / per_img, qr = q - il * per_img;
@@ -1350,23 +1362,26 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
     }
   };
 
-  f32x16 acc[WCH][2];
+  f32x16 acc[WCH][NP];
 #pragma unroll
   for (int j = 0; j < WCH; ++j)
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < NP; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[j][i][r] = 0.f;
   auto compute = [&](const char* tile, int t, const uint4 (&W)[WCH][4]) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const bf16x8 f0 = __builtin_bit_cast(bf16x8, *(const uint4*)(tile + lrow[0] + tdelta[t] + 16 * c));
-      const bf16x8 f1 = __builtin_bit_cast(bf16x8, *(const uint4*)(tile + lrow[1] + tdelta[t] + 16 * c));
+      bf16x8 f[NP];
+#pragma unroll
+      for (int i = 0; i < NP; ++i)
+        f[i] = __builtin_bit_cast(bf16x8, *(const uint4*)(tile + lrow[i] + tdelta[t] + 16 * c));
 #pragma unroll
       for (int j = 0; j < WCH; ++j) {
         const bf16x8 wv = __builtin_bit_cast(bf16x8, W[j][c]);
-        acc[j][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv, f0, acc[j][0], 0, 0, 0);
-        acc[j][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv, f1, acc[j][1], 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < NP; ++i)
+          acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv, f[i], acc[j][i], 0, 0, 0);
       }
     }
   };
@@ -1405,23 +1420,23 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
 
   if constexpr (KS > 1) {
     // group 1's partial sums to LDS (lane-contiguous), group 0 adds them
-    float* red = (float*)smem + rho * (WCH * 2 * 16 * 64) + lane;
+    float* red = (float*)smem + rho * (WCH * NP * 16 * 64) + lane;
     if (grp == 1) {
 #pragma unroll
       for (int j = 0; j < WCH; ++j)
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < NP; ++i)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) red[((j * 2 + i) * 16 + r) * 64] = acc[j][i][r];
+          for (int r = 0; r < 16; ++r) red[((j * NP + i) * 16 + r) * 64] = acc[j][i][r];
     }
     __syncthreads();
     if (grp == 0) {
 #pragma unroll
       for (int j = 0; j < WCH; ++j)
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < NP; ++i)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) acc[j][i][r] += red[((j * 2 + i) * 16 + r) * 64];
+          for (int r = 0; r < 16; ++r) acc[j][i][r] += red[((j * NP + i) * 16 + r) * 64];
     }
     __syncthreads();
   }
@@ -1436,7 +1451,7 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
   if (grp == 0) {
     const int rho_h = rho >> 1, rho_w = rho & 1;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < NP; ++i) {
       const int q = 32 * i + (lane & 31);
       const int per_img = a.qbh * a.w;
       const int il = q / per_img, qr = q - il * per_img;
@@ -1470,18 +1485,26 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
 
 hipError_t launch_quad(const QArgs& a, hipStream_t stream) {
   const dim3 grid(a.ntiles * a.igroups * a.hblocks);
-#define HUGE2_QUAD_LAUNCH(KS_, WCH_, D_) \
-  hipLaunchKernelGGL((quad_kernel<KS_, WCH_, D_>), grid, dim3(kQuadThreads), 0, stream, a)
-  if (a.ks == 2 && a.nch == 2) {
-    HUGE2_QUAD_LAUNCH(2, 2, 2);  // both channel blocks per wave: two stages fit the registers
+#define HUGE2_QUAD_LAUNCH(KS_, WCH_, D_, NP_) \
+  hipLaunchKernelGGL((quad_kernel<KS_, WCH_, D_, NP_>), grid, dim3(kQuadThreads), 0, stream, a)
+  if (a.np == 4) {
+    if (a.ks == 2) {
+      if (a.depth == 2) HUGE2_QUAD_LAUNCH(2, 1, 2, 4);
+      else HUGE2_QUAD_LAUNCH(2, 1, 4, 4);
+    } else {
+      if (a.depth == 2) HUGE2_QUAD_LAUNCH(1, 1, 2, 4);
+      else HUGE2_QUAD_LAUNCH(1, 1, 4, 4);
+    }
+  } else if (a.ks == 2 && a.nch == 2) {
+    HUGE2_QUAD_LAUNCH(2, 2, 2, 2);  // both channel blocks per wave: two stages fit the registers
   } else if (a.ks == 2) {
-    if (a.depth == 2) HUGE2_QUAD_LAUNCH(2, 1, 2);
-    else if (a.depth == 4) HUGE2_QUAD_LAUNCH(2, 1, 4);
-    else HUGE2_QUAD_LAUNCH(2, 1, 8);
+    if (a.depth == 2) HUGE2_QUAD_LAUNCH(2, 1, 2, 2);
+    else if (a.depth == 4) HUGE2_QUAD_LAUNCH(2, 1, 4, 2);
+    else HUGE2_QUAD_LAUNCH(2, 1, 8, 2);
   } else {
-    if (a.depth == 2) HUGE2_QUAD_LAUNCH(1, 1, 2);
-    else if (a.depth == 4) HUGE2_QUAD_LAUNCH(1, 1, 4);
-    else HUGE2_QUAD_LAUNCH(1, 1, 8);
+    if (a.depth == 2) HUGE2_QUAD_LAUNCH(1, 1, 2, 2);
+    else if (a.depth == 4) HUGE2_QUAD_LAUNCH(1, 1, 4, 2);
+    else HUGE2_QUAD_LAUNCH(1, 1, 8, 2);
   }
 #undef HUGE2_QUAD_LAUNCH
   return hipGetLastError();

@@ -221,7 +221,7 @@ hipError_t launch_rowphase(const RpArgs& a, hipStream_t stream);
 // Weights in the lane order of 128-byte K stages (pack_weights_kernel with
 // lane_kb = 128).
 constexpr int kQuadThreads = 512;
-constexpr int kQuadPix = 64;         // input positions per workgroup
+constexpr int kQuadPix = 64;         // input positions per workgroup (np = 2; 128 with np = 4)
 constexpr int kQuadRowB = 144;       // LDS bytes per halo pixel: 64 channels + 16-byte pad
 constexpr int kQuadHaloRows = 200;   // halo pixels per LDS tile: ni * (qbh + 2) * (w + 2)
 constexpr int kQuadMaxPieces = 2;    // input items (pixel pair x 8 channels) per thread and K block
@@ -232,7 +232,8 @@ struct QArgs {
   void* y;           // NCHW output, 2h x 2w
   uint32_t x_bytes, wp_bytes;
   int n, cin, h, w, cout, cout_pad;
-  int ni, qbh;       // images and input rows per workgroup (ni * qbh * w = 64)
+  int ni, qbh;       // images and input rows per workgroup (ni * qbh * w = 32 * np)
+  int np;            // 32-position MFMA blocks per wave: 2, or 4 (one 32-channel block per wave)
   // 32-channel blocks and K groups per workgroup; the 8 waves are 4 phases x
   // (nch = 2, ks = 1: a 32-channel block each | nch = 1, ks = 2: a K group
   // each | nch = 2, ks = 2: a K group each, both 32-channel blocks per wave)

@@ -64,6 +64,8 @@ SMALL = [
     L("ct_quad_rows16", True, 2, 192, 16, 16, 96, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
     L("ct_quad_w32", True, 1, 64, 8, 32, 32, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
     L("ct_quad_w64", True, 1, 64, 4, 64, 32, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
+    L("ct_quad_np4_rows", True, 2, 128, 16, 16, 64, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
+    L("ct_quad_np4_ragged", True, 3, 128, 8, 8, 48, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
 ]
 
 
@@ -382,14 +384,25 @@ def test_large_stride_forms(rowphase, monkeypatch):
 QUAD = [l for l in SMALL if l.name.startswith("ct_quad")]
 
 
-@pytest.mark.parametrize("quad,wch", [(0, 1), (1, 1), (1, 2)])
+# (layer, K groups) pairs that tile 128 positions per workgroup
+QUAD_NP4 = {("ct_quad_img8", 1), ("ct_quad_two_kgroups", 1), ("ct_quad_two_kgroups", 2),
+            ("ct_quad_rows16", 1), ("ct_quad_np4_rows", 1), ("ct_quad_np4_ragged", 1),
+            ("ct_quad_np4_ragged", 2)}
+
+
+@pytest.mark.parametrize("quad,wch,np_,ks", [(0, 1, 0, 0), (1, 1, 2, 0), (1, 2, 2, 0), (1, 1, 4, 1),
+                                             (1, 1, 4, 2)])
 @pytest.mark.parametrize("layer", QUAD, ids=lambda l: l.name)
-def test_all_phase_forms(layer, quad, wch, monkeypatch):
-    """The all-phase kernel (both wave layouts) and the phase GEMM it replaces
-    all match the oracle."""
+def test_all_phase_forms(layer, quad, wch, np_, ks, monkeypatch):
+    """The all-phase kernel (64 positions per workgroup in both wave layouts,
+    128 positions in one or two K groups) and the phase GEMM it replaces all
+    match the oracle."""
     monkeypatch.setenv("HUGE2_QUAD", str(quad))
     monkeypatch.setenv("HUGE2_QUAD_WCH", str(wch))
-    P.say("case", layer, "HUGE2_QUAD", quad, "HUGE2_QUAD_WCH", wch)
+    monkeypatch.setenv("HUGE2_QUAD_NP", str(np_))
+    monkeypatch.setenv("HUGE2_QUAD_KS", str(ks))
+    P.say("case", layer, "HUGE2_QUAD", quad, "HUGE2_QUAD_WCH", wch, "HUGE2_QUAD_NP", np_,
+          "HUGE2_QUAD_KS", ks)
     xq, wq = _inputs(layer, seed=11)
     bias = torch.linspace(-1.0, 1.0, layer.c_out)
     y = P.run_gpu(layer, xq, wq, bias)
@@ -397,6 +410,10 @@ def test_all_phase_forms(layer, quad, wch, monkeypatch):
             layer.dtype, layer.name)
     plan = P.make_plan(layer, wq.contiguous().to(torch.device("cuda", 0)))
     try:
-        assert ("quad_kernel" in plan.kernel) == bool(quad), plan.kernel
+        expect = bool(quad) and (np_ != 4 or (layer.name, ks) in QUAD_NP4)
+        assert ("quad_kernel" in plan.kernel) == expect, plan.kernel
+        if expect and np_ == 4:
+            dims = plan.kernel.split()[1].split("x")
+            assert int(dims[0]) * int(dims[1]) * int(dims[2]) == 128, plan.kernel
     finally:
         plan.close()

@@ -22,6 +22,15 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte store of output data that nothing in the kernel reads back, with
+// the non-temporal (streaming) cache policy.
+__device__ __forceinline__ void store_stream16(void* p, uint4 v) {
+  const u32x4 t = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(t, (u32x4*)p);
+}
+
 // Workgroups are dealt to the 8 XCDs round-robin (id mod 8).  Map them so
 // that each XCD runs one contiguous run of the work list: neighbouring
 // tiles share input rows and weight blocks, which then stay in that XCD's L2.
@@ -32,10 +41,8 @@ __device__ __forceinline__ int xcd_remap(int b, int g) {
 }
 
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);  // quiet NaN
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+  // v_cvt_pk_bf16_f32: round to nearest even, NaN stays a (quiet) NaN
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
 // Decomposition of a segment pixel index into image, output and input coordinates.
@@ -81,7 +88,15 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, const SegDev& sg,
                                            const f32x16 (&acc)[TP][TC], int pix0, int ch0,
                                            int lane, const float* sb) {
   const int hw_o = a.ho * a.wo;
+  // the bias values are read from LDS up front: an LDS read between the
+  // global stores would wait for its own latency element by element
   if constexpr (!NCHW_OUT) {
+    float bv[TC];
+#pragma unroll
+    for (int j = 0; j < TC; ++j) {
+      const int ch = ch0 + 32 * j + (lane & 31);
+      bv[j] = ch < a.cout ? sb[ch] : 0.f;
+    }
 #pragma unroll
     for (int i = 0; i < TP; ++i) {
 #pragma unroll
@@ -94,7 +109,7 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, const SegDev& sg,
         for (int j = 0; j < TC; ++j) {
           const int ch = ch0 + 32 * j + (lane & 31);
           if (ch >= a.cout) continue;
-          const float v = acc[i][j][r] + sb[ch];
+          const float v = acc[i][j][r] + bv[j];
           const size_t off = (size_t)pix * a.cout + ch;
           if constexpr (BF16)
             ((uint16_t*)a.y)[off] = f32_to_bf16_rne(v);
@@ -104,20 +119,32 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, const SegDev& sg,
       }
     }
   } else {
+    size_t base[TP];
+    bool ok[TP];
 #pragma unroll
     for (int i = 0; i < TP; ++i) {
       const int m = pix0 + 32 * i + (lane & 31);
-      if (m >= sg.m_total) continue;
-      const PixelPos p = pixel_pos(sg, a.n, m);
-      const size_t base = (size_t)p.img * a.cout * hw_o + (size_t)p.oh * a.wo + p.ow;
+      ok[i] = m < sg.m_total;
+      const PixelPos p = pixel_pos(sg, a.n, ok[i] ? m : 0);
+      base[i] = (size_t)p.img * a.cout * hw_o + (size_t)p.oh * a.wo + p.ow;
+    }
 #pragma unroll
-      for (int j = 0; j < TC; ++j) {
+    for (int j = 0; j < TC; ++j) {
+      float bv[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int ch = ch0 + 32 * j + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        bv[r] = ch < a.cout ? sb[ch] : 0.f;
+      }
+#pragma unroll
+      for (int i = 0; i < TP; ++i) {
+        if (!ok[i]) continue;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int ch = ch0 + 32 * j + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
           if (ch >= a.cout) continue;
-          const float v = acc[i][j][r] + sb[ch];
-          const size_t off = base + (size_t)ch * hw_o;
+          const float v = acc[i][j][r] + bv[r];
+          const size_t off = base[i] + (size_t)ch * hw_o;
           if constexpr (BF16)
             ((uint16_t*)a.y)[off] = f32_to_bf16_rne(v);
           else
@@ -1196,7 +1223,7 @@ __global__ __launch_bounds__(kRpThreads) void rowphase_kernel(RpArgs a) {
           ++qw;
         }
       }
-      *(uint4*)(yrow + v * 8) = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+      store_stream16(yrow + v * 8, make_uint4(wv[0], wv[1], wv[2], wv[3]));
     }
   }
 }
@@ -1243,6 +1270,8 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
   static_assert(DEPTH == 2 || DEPTH == 4 || DEPTH == 8, "weight stages in flight");
   static_assert(KS == 2 || WCH == 1, "one K group: two waves of 32 channels per phase");
   static_assert(NP == 2 || (NP == 4 && WCH == 1), "32-position blocks per wave");
+  // pixel fragments double-buffered across taps where the registers allow
+  constexpr bool PF = NP == 2 && WCH == 1 && DEPTH == 2;
   constexpr int U = DEPTH > 4 ? DEPTH / 4 : 1;  // K blocks per unrolled loop step
   // LDS: the K groups' double-buffered halo tiles, reused after the main loop
   // for group 1's partial sums and then for the interleaved output block
@@ -1252,7 +1281,7 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
   constexpr int OUT_B = 64 * (4 * 32 * NP + 8) * 2;
   constexpr int SMEM_B = cmax(TILE_B, cmax(RED_B, OUT_B));
   __shared__ __attribute__((aligned(16))) char smem[SMEM_B];
-  __shared__ float s_bias[64];
+  __shared__ __attribute__((aligned(16))) float s_bias[64];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1369,21 +1398,24 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
     for (int i = 0; i < NP; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[j][i][r] = 0.f;
-  auto compute = [&](const char* tile, int t, const uint4 (&W)[WCH][4]) {
+  // the pixel fragments of one tap: 4 K steps of 16 channels x NP blocks
+  auto read_frags = [&](const char* tile, int t, bf16x8 (&f)[4][NP]) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      bf16x8 f[NP];
+    for (int c = 0; c < 4; ++c)
 #pragma unroll
       for (int i = 0; i < NP; ++i)
-        f[i] = __builtin_bit_cast(bf16x8, *(const uint4*)(tile + lrow[i] + tdelta[t] + 16 * c));
+        f[c][i] = __builtin_bit_cast(bf16x8, *(const uint4*)(tile + lrow[i] + tdelta[t] + 16 * c));
+  };
+  auto mfmas = [&](const bf16x8 (&f)[4][NP], const uint4 (&W)[WCH][4]) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
 #pragma unroll
       for (int j = 0; j < WCH; ++j) {
         const bf16x8 wv = __builtin_bit_cast(bf16x8, W[j][c]);
 #pragma unroll
         for (int i = 0; i < NP; ++i)
-          acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv, f[i], acc[j][i], 0, 0, 0);
+          acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv, f[c][i], acc[j][i], 0, 0, 0);
       }
-    }
   };
 
   __syncthreads();  // halo tiles zeroed
@@ -1402,15 +1434,40 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
       const int cbi = cb0 + u;
       if (U > 1 && cbi >= cbn) break;  // the same for the whole workgroup
       const char* tile = tiles + (cbi & 1) * HALO_B;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        compute(tile, t, W[(4 * u + t) % DEPTH]);
+      auto next_w = [&](int t) {
         // the stage DEPTH taps later goes into the buffer just consumed,
         // issued here (not sunk below later taps' MFMAs by the scheduler)
         const int nb = cbi + (t + DEPTH) / 4;
         __builtin_amdgcn_sched_barrier(0);
         load_w(W[(4 * u + t) % DEPTH], nb < cbn, cb_lo + min(nb, cbn - 1), (t + DEPTH) % 4);
         __builtin_amdgcn_sched_barrier(0);
+      };
+      if constexpr (PF) {
+        // Tap t's MFMAs run while tap t+1's pixel fragments are read from
+        // LDS (two register sets): the LDS latency is exposed once per K
+        // block rather than before every MFMA.
+        auto step = [&](int t, const bf16x8 (&cur)[4][NP], bf16x8 (&nxt)[4][NP]) {
+          if (t < 3) read_frags(tile, t + 1, nxt);
+          __builtin_amdgcn_sched_barrier(0);
+          mfmas(cur, W[(4 * u + t) % DEPTH]);
+          next_w(t);
+        };
+        bf16x8 fa[4][NP], fb[4][NP];
+        read_frags(tile, 0, fa);
+        step(0, fa, fb);
+        step(1, fb, fa);
+        step(2, fa, fb);
+        step(3, fb, fa);
+      } else {
+        // one register set: a tap's reads all issued before its MFMAs
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          bf16x8 f[4][NP];
+          read_frags(tile, t, f);
+          __builtin_amdgcn_sched_barrier(0);
+          mfmas(f, W[(4 * u + t) % DEPTH]);
+          next_w(t);
+        }
       }
       if (cbi + 1 < cbn) store_pieces(tiles + ((cbi + 1) & 1) * HALO_B, P);
       __syncthreads();
@@ -1450,21 +1507,36 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
   __syncthreads();
   if (grp == 0) {
     const int rho_h = rho >> 1, rho_w = rho & 1;
+    // this lane's bias values (channels 8g + 4 (lane / 32) + 0..3 of each
+    // 32-channel block) and output positions, all read before any store
+    float bv[WCH][16];
+#pragma unroll
+    for (int j = 0; j < WCH; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const float4 b4 = *(const float4*)(s_bias + (hc * WCH + j) * 32 + 8 * g + 4 * (lane >> 5));
+        bv[j][4 * g] = b4.x;
+        bv[j][4 * g + 1] = b4.y;
+        bv[j][4 * g + 2] = b4.z;
+        bv[j][4 * g + 3] = b4.w;
+      }
+    int pos[NP];
 #pragma unroll
     for (int i = 0; i < NP; ++i) {
       const int q = 32 * i + (lane & 31);
       const int per_img = a.qbh * a.w;
       const int il = q / per_img, qr = q - il * per_img;
       const int qh = qr / a.w, qw = qr - qh * a.w;
-      const int pos = (il * obh + 2 * qh + rho_h) * obw + 2 * qw + rho_w;
-#pragma unroll
-      for (int j = 0; j < WCH; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int ch = (hc * WCH + j) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-          so[ch * cpo + pos] = f32_to_bf16_rne(acc[j][i][r] + s_bias[ch]);
-        }
+      pos[i] = (il * obh + 2 * qh + rho_h) * obw + 2 * qw + rho_w;
     }
+#pragma unroll
+    for (int j = 0; j < WCH; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int ch = (hc * WCH + j) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+#pragma unroll
+        for (int i = 0; i < NP; ++i) so[ch * cpo + pos[i]] = f32_to_bf16_rne(acc[j][i][r] + bv[j][r]);
+      }
   }
   __syncthreads();
   // Whole output rows: per (channel, image) the rows [2 qh0, 2 qh0 + obh)
@@ -1479,7 +1551,7 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
     const uint4 v = *(const uint4*)(so + ch * cpo + il * obh * obw + 8 * k8);
     uint16_t* dst = (uint16_t*)a.y + ((size_t)(img0 + il) * a.cout + n0 + ch) * plane_o +
                     (size_t)(2 * qh0) * obw + 8 * k8;
-    *(uint4*)dst = v;
+    store_stream16(dst, v);
   }
 }
 
@@ -1488,13 +1560,9 @@ hipError_t launch_quad(const QArgs& a, hipStream_t stream) {
 #define HUGE2_QUAD_LAUNCH(KS_, WCH_, D_, NP_) \
   hipLaunchKernelGGL((quad_kernel<KS_, WCH_, D_, NP_>), grid, dim3(kQuadThreads), 0, stream, a)
   if (a.np == 4) {
-    if (a.ks == 2) {
-      if (a.depth == 2) HUGE2_QUAD_LAUNCH(2, 1, 2, 4);
-      else HUGE2_QUAD_LAUNCH(2, 1, 4, 4);
-    } else {
-      if (a.depth == 2) HUGE2_QUAD_LAUNCH(1, 1, 2, 4);
-      else HUGE2_QUAD_LAUNCH(1, 1, 4, 4);
-    }
+    // two weight stages in flight: the registers hold no more
+    if (a.ks == 2) HUGE2_QUAD_LAUNCH(2, 1, 2, 4);
+    else HUGE2_QUAD_LAUNCH(1, 1, 2, 4);
   } else if (a.ks == 2 && a.nch == 2) {
     HUGE2_QUAD_LAUNCH(2, 2, 2, 2);  // both channel blocks per wave: two stages fit the registers
   } else if (a.ks == 2) {

@@ -63,6 +63,10 @@ DESCRIPTIONS = {
                     "(4->8), 512->256, 256->128, 128->3 (32->64), bf16 NCHW, batch 1",
     "table1_cgan": "the paper's Table 1 cGAN deconvolutions: ConvT k4 s2 p1 256->128 (8->16), "
                    "128->3 (16->32), bf16 NCHW, batch 1",
+    "dcgan_dgrad": "training (section 3.2.3): data gradients of the DCGAN generator's four ConvT "
+                   "layers, back to front, as stride-2 convs of the output errors with the same "
+                   "weights: 3->128 (64->32), 128->256, 256->512, 512->1024 (8->4), bf16 NCHW, "
+                   "batch 64",
     "dcgan_wgrad": "training (section 3.2.3): weight gradients of the DCGAN generator's four "
                    "ConvT layers (k4 s2 p1, 1024->512->256->128->3, bf16 NCHW, batch 64) from "
                    "their inputs and seeded output errors",

@@ -29,6 +29,15 @@ Workloads (``name``: layers):
                with the phase roles mirrored).  Input N(0,1), weights N(0,0.02), chained.
   table1_cgan  the cGAN layers of Table 1: 4x4 kernels, stride 2, pad 1,
                8x8x256 -> 16x16x128 -> 32x32x3, batch 1, bf16 NCHW, chained.
+  dcgan_dgrad  training (section 3.2.3): the data gradients of the dcgan generator's
+               four ConvTranspose layers, back to front.  The gradient of a stride-2
+               transposed conv with respect to its input is the stride-2 conv of the
+               output error with the same weight array, read as [C_out_conv = C_in,
+               C_in_conv = C_out, 4, 4]: 3->128 (64x64 -> 32x32), 128->256 (32 -> 16),
+               256->512 (16 -> 8), 512->1024 (8 -> 4), batch 64, bf16 NCHW.  The
+               generator has no activations between its layers, so each layer's input
+               gradient is the previous one's output error (chained).  The first error
+               is N(0,1); the weights are the dcgan draws.
 """
 from __future__ import annotations
 
@@ -82,6 +91,13 @@ def dcgan_layers(dtype="bf16", batch=64):
     return out
 
 
+def dcgan_dgrad_layers(dtype="bf16", batch=64):
+    fwd = dcgan_layers(dtype, batch)
+    return [Layer("dcgan_dgrad_l%d" % (4 - i), False, batch, l.c_out, 2 * l.h, 2 * l.w, l.c_in,
+                  l.r, l.s, l.stride, l.pad, 0, l.dil, l.layout, dtype)
+            for i, l in enumerate(reversed(fwd))]
+
+
 def table1_layers(kind, batch=1, dtype="bf16"):
     if kind == "dcgan":
         chans, k, pad, op, hw0 = [(1024, 512), (512, 256), (256, 128), (128, 3)], 5, 2, 1, 4
@@ -106,8 +122,9 @@ WORKLOADS = {
                            "bf16")],
     "table1_dcgan": table1_layers("dcgan"),
     "table1_cgan": table1_layers("cgan"),
+    "dcgan_dgrad": dcgan_dgrad_layers("bf16"),
 }
-CHAINED = ("dcgan", "dcgan_f32", "table1_dcgan", "table1_cgan")
+CHAINED = ("dcgan", "dcgan_f32", "table1_dcgan", "table1_cgan", "dcgan_dgrad")
 
 
 def torch_dtype(name):
@@ -146,6 +163,16 @@ def generate(workload, seed=0, batch=None):
         out = [(layers[0], x1, ws[0])]
         out += [(l, None, w) for l, w in zip(layers[1:], ws[1:])]
         return out
+    if workload == "dcgan_dgrad":
+        # the dcgan draws (z, linear weight, w1..w4), then the output error
+        n = layers[0].n
+        _normal(g, (n, 100))
+        _normal(g, (1024 * 4 * 4, 100), 0.02)
+        ws = [_normal(g, l.w_shape(), 0.02) for l in dcgan_layers("bf16", n)]
+        l0 = layers[0]
+        dy = _normal(g, (n, l0.c_in, l0.h, l0.w))
+        ws = ws[::-1]  # back to front; [C_in_T, C_out_T, 4, 4] = [C_out_conv, C_in_conv, 4, 4]
+        return [(layers[0], dy, ws[0])] + [(l, None, w) for l, w in zip(layers[1:], ws[1:])]
     if workload in ("table1_dcgan", "table1_cgan"):
         l0 = layers[0]
         x1 = _normal(g, (l0.n, l0.c_in, l0.h, l0.w))

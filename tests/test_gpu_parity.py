@@ -156,7 +156,7 @@ def test_coverage_and_determinism():
 def test_dcgan_chain_reduced_batch():
     """DCGAN generator at batch 2: each layer gets the oracle's output of the
     previous layer (rounded to the dtype), so errors do not compound."""
-    for wname in ("dcgan_f32", "dcgan"):
+    for wname in ("dcgan_f32", "dcgan", "dcgan_dgrad"):
         items = wl.generate(wname, seed=0, batch=2)
         x_prev = None
         for layer, x, w in items:
@@ -220,7 +220,7 @@ def test_workload_reduced_full_check(wname, over):
         P.check(y, ref, absref, layer.dtype, layer.name)
 
 
-FULL = ["convt_small", "dcgan_f32", "dcgan", "convt_odd", "aspp", "fcn_upsample"]
+FULL = ["convt_small", "dcgan_f32", "dcgan", "convt_odd", "aspp", "fcn_upsample", "dcgan_dgrad"]
 
 
 @pytest.mark.parametrize("wname", FULL)
@@ -229,7 +229,7 @@ def test_workload_full_size_sampled(wname):
     sampled outputs that cover every phase, border and first/last channel."""
     items = wl.generate(wname, seed=0)
     for i, (layer, x, w) in enumerate(items):
-        if x is None:  # dcgan layers 2-4: standalone input of the chained shape
+        if x is None:  # chained layers 2-4: standalone input of the chained shape
             x = wl.layer_input(layer, seed=100 + i, std=0.25)
         P.say("case", wname, layer)
         xq, wq = P.quantise(x, layer.dtype), P.quantise(w, layer.dtype)

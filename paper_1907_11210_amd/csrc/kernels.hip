@@ -1267,7 +1267,10 @@ template <int KS, int WCH, int DEPTH, int NP>
 __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
   constexpr int NT = kQuadThreads;
   constexpr int NTG = NT / KS;  // threads of one K group
-  constexpr int RB = kQuadRowB;
+  // the slot swizzle (below) for 64 positions; with 128 the registers hold
+  // no more addresses, and rows padded by 16 bytes are taken instead
+  constexpr bool SWZ = NP == 2 && WCH == 1;
+  constexpr int RB = SWZ ? kQuadRowB : kQuadRowB + 16;
   constexpr int HALO_B = kQuadHaloRows * RB;
   constexpr int MAXP = kQuadMaxPieces;
   constexpr uint32_t OOB = 0x80000000u;
@@ -1321,8 +1324,16 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
   const int rows = r1 - r0;
   const int npairs = a.ni * rows * a.w / 2;
   const int itotal = npairs * 8;
+  // LDS tile layout: halo pixel (il, rl, cl) (rl, cl counting the halo row
+  // and column) is the RB-byte row p = (il * hrows + rl) * hww + cl, and its
+  // eight 16-byte groups of 8 channels sit at slots g ^ sw(pv), where
+  // sw(pv) = (pv >> 1) & 7 and pv = (il * qbh + rl - 1) * w + cl.  The 32
+  // pixels that one fragment read takes (any tap) have consecutive pv, so
+  // the XOR spreads them over all 64 banks (no padding needed; measured: two
+  // rows of 16 or four rows of 8 such 144-byte rows conflict two-way).
+  auto slot_sw = [](int pv) { return SWZ ? (pv >> 1) & 7 : 0; };
   uint32_t p_src[MAXP];
-  int p_lds[MAXP];
+  int p_lds[MAXP], p_lds_hi[MAXP];
 #pragma unroll
   for (int j = 0; j < MAXP; ++j) {
     const int it = tg + NTG * j;
@@ -1334,7 +1345,10 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
     p_src[j] = ok ? ((((uint32_t)(img0 + il) * (uint32_t)a.cin + 8u * g) * (uint32_t)a.h + (uint32_t)(r0 + pr)) *
                          (uint32_t)a.w + (uint32_t)col) * 2u
                   : OOB;
-    p_lds[j] = ok ? ((il * hrows + r0 + pr - qh0 + 1) * hww + col + 1) * RB + g * 16 : -1;
+    const int rl = r0 + pr - qh0 + 1, cl = col + 1;
+    const int prow = (il * hrows + rl) * hww + cl, pv = (il * a.qbh + rl - 1) * a.w + cl;
+    p_lds[j] = ok ? prow * RB + 16 * (g ^ slot_sw(pv)) : -1;
+    p_lds_hi[j] = (prow + 1) * RB + 16 * (g ^ slot_sw(pv + 1));
   }
   auto load_pieces = [&](int cb, uint32_t (&P)[MAXP][8]) {
     const uint32_t cbo = (uint32_t)cb * 64u * plane_b;
@@ -1360,24 +1374,30 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
         hi[e] = __builtin_amdgcn_perm(P[j][2 * e + 1], P[j][2 * e], 0x07060302u);
       }
       *(uint4*)(tile + p_lds[j]) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-      *(uint4*)(tile + p_lds[j] + RB) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+      *(uint4*)(tile + p_lds_hi[j]) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
     }
   };
 
-  // This wave's pixels: q = 32 i + lane % 32; LDS byte offset of its halo
-  // pixel at tap offset (0, 0), plus the lane half's 64 bytes of K.
-  int lrow[NP];
+  // This wave's pixels: q = 32 i + lane % 32; LDS byte offset and virtual
+  // index pv of its halo pixel at tap offset (0, 0).  The lane half h reads
+  // K groups 4h + c (c = 0..3), at slots (4h + c) ^ sw(pv + tap delta).
+  int lrow[NP], lpv[NP];
 #pragma unroll
   for (int i = 0; i < NP; ++i) {
     const int q = 32 * i + (lane & 31);
     const int per_img = a.qbh * a.w;
     const int il = q / per_img, qr = q - il * per_img;
     const int qh = qr / a.w, qw = qr - qh * a.w;
-    lrow[i] = ((il * hrows + qh + 1) * hww + qw + 1) * RB + (lane >> 5) * 64;
+    lrow[i] = ((il * hrows + qh + 1) * hww + qw + 1) * RB;
+    lpv[i] = (il * a.qbh + qh) * a.w + qw + 1;
   }
-  int tdelta[4];
+  const int hk = 4 * (lane >> 5);
+  int tdelta[4], tdv[4];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) tdelta[t] = (a.dh[rho][t] * hww + a.dw[rho][t]) * RB;
+  for (int t = 0; t < 4; ++t) {
+    tdelta[t] = (a.dh[rho][t] * hww + a.dw[rho][t]) * RB;
+    tdv[t] = a.dh[rho][t] * a.w + a.dw[rho][t];
+  }
 
   // weight stage (K block cb, tap t) of this wave's 32-channel blocks
   const int ncb = a.cin / 64;
@@ -1408,7 +1428,8 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
     for (int c = 0; c < 4; ++c)
 #pragma unroll
       for (int i = 0; i < NP; ++i)
-        f[c][i] = __builtin_bit_cast(bf16x8, *(const uint4*)(tile + lrow[i] + tdelta[t] + 16 * c));
+        f[c][i] = __builtin_bit_cast(
+            bf16x8, *(const uint4*)(tile + lrow[i] + tdelta[t] + 16 * ((hk + c) ^ slot_sw(lpv[i] + tdv[t]))));
   };
   auto mfmas = [&](const bf16x8 (&f)[4][NP], const uint4 (&W)[WCH][4]) {
 #pragma unroll

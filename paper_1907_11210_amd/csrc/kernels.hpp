@@ -222,7 +222,7 @@ hipError_t launch_rowphase(const RpArgs& a, hipStream_t stream);
 // lane_kb = 128).
 constexpr int kQuadThreads = 512;
 constexpr int kQuadPix = 64;         // input positions per workgroup (np = 2; 128 with np = 4)
-constexpr int kQuadRowB = 144;       // LDS bytes per halo pixel: 64 channels + 16-byte pad
+constexpr int kQuadRowB = 128;       // LDS bytes per halo pixel: 64 channels (slot-swizzled; + 16-byte pad unswizzled)
 constexpr int kQuadHaloRows = 200;   // halo pixels per LDS tile: ni * (qbh + 2) * (w + 2)
 constexpr int kQuadMaxPieces = 2;    // input items (pixel pair x 8 channels) per thread and K block
 struct QArgs {

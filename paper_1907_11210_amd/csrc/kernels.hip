@@ -1269,7 +1269,7 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
   constexpr int NTG = NT / KS;  // threads of one K group
   // the slot swizzle (below) for 64 positions; with 128 the registers hold
   // no more addresses, and rows padded by 16 bytes are taken instead
-  constexpr bool SWZ = NP == 2 && WCH == 1;
+  constexpr bool SWZ = WCH == 1;
   constexpr int RB = SWZ ? kQuadRowB : kQuadRowB + 16;
   constexpr int HALO_B = kQuadHaloRows * RB;
   constexpr int MAXP = kQuadMaxPieces;
@@ -1431,6 +1431,22 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
         f[c][i] = __builtin_bit_cast(
             bf16x8, *(const uint4*)(tile + lrow[i] + tdelta[t] + 16 * ((hk + c) ^ slot_sw(lpv[i] + tdv[t]))));
   };
+  // one K step (16 channels) of a tap
+  auto read_step = [&](const char* tile, int t, int c, bf16x8 (&f)[NP]) {
+#pragma unroll
+    for (int i = 0; i < NP; ++i)
+      f[i] = __builtin_bit_cast(
+          bf16x8, *(const uint4*)(tile + lrow[i] + tdelta[t] + 16 * ((hk + c) ^ slot_sw(lpv[i] + tdv[t]))));
+  };
+  auto mfma_step = [&](int c, const bf16x8 (&f)[NP], const uint4 (&W)[WCH][4]) {
+#pragma unroll
+    for (int j = 0; j < WCH; ++j) {
+      const bf16x8 wv = __builtin_bit_cast(bf16x8, W[j][c]);
+#pragma unroll
+      for (int i = 0; i < NP; ++i)
+        acc[j][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv, f[i], acc[j][i], 0, 0, 0);
+    }
+  };
   auto mfmas = [&](const bf16x8 (&f)[4][NP], const uint4 (&W)[WCH][4]) {
 #pragma unroll
     for (int c = 0; c < 4; ++c)
@@ -1459,6 +1475,12 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
       const int cbi = cb0 + u;
       if (U > 1 && cbi >= cbn) break;  // the same for the whole workgroup
       const char* tile = tiles + (cbi & 1) * HALO_B;
+      if constexpr (NP == 4) {
+        // recomputed per K block: hoisted, the 64 swizzled fragment
+        // addresses would not fit the registers
+#pragma unroll
+        for (int i = 0; i < NP; ++i) __asm__ volatile("" : "+v"(lrow[i]), "+v"(lpv[i]));
+      }
       auto next_w = [&](int t) {
         // the stage DEPTH taps later goes into the buffer just consumed,
         // issued here (not sunk below later taps' MFMAs by the scheduler)
@@ -1484,13 +1506,23 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
         step(2, fa, fb);
         step(3, fb, fa);
       } else {
-        // one register set: a tap's reads all issued before its MFMAs
+        // per tap, K step c+1's fragments are read while step c's MFMAs run
+        // (two sets of NP fragments)
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-          bf16x8 f[4][NP];
-          read_frags(tile, t, f);
+          const uint4 (&Wt)[WCH][4] = W[(4 * u + t) % DEPTH];
+          bf16x8 f0[NP], f1[NP];
+          read_step(tile, t, 0, f0);
+          read_step(tile, t, 1, f1);
           __builtin_amdgcn_sched_barrier(0);
-          mfmas(f, W[(4 * u + t) % DEPTH]);
+          mfma_step(0, f0, Wt);
+          read_step(tile, t, 2, f0);
+          __builtin_amdgcn_sched_barrier(0);
+          mfma_step(1, f1, Wt);
+          read_step(tile, t, 3, f1);
+          __builtin_amdgcn_sched_barrier(0);
+          mfma_step(2, f0, Wt);
+          mfma_step(3, f1, Wt);
           next_w(t);
         }
       }

@@ -929,16 +929,12 @@ __global__ __launch_bounds__(kZtileThreads) void ztile_kernel(ZArgs a) {
     src_off[mi] = min((wave + NW * mi) * 32 + (lane & 31), np - 1) * RB + (lane >> 5) * 64;
 
   __syncthreads();  // tiles zeroed
-  // the first two passes' loads are both in flight before the first wait
-  const int npass = a.cin_pad / 64;
   uint32_t P[MAXP][8];
-  {
-    uint32_t P0[MAXP][8];
-    load_items(0, P0);
-    if (npass > 1) load_items(64, P);
-    store_items(zsm, P0);
-  }
+  load_items(0, P);
+  store_items(zsm, P);
   __syncthreads();
+  const int npass = a.cin_pad / 64;
+  if (npass > 1) load_items(64, P);
   for (int pass = 0; pass < npass; ++pass) {
     const char* buf = zsm + (pass & 1) * BUF_B;
 #pragma unroll

@@ -1263,9 +1263,8 @@ template <int KS, int WCH, int DEPTH, int NP>
 __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
   constexpr int NT = kQuadThreads;
   constexpr int NTG = NT / KS;  // threads of one K group
-  // the slot swizzle (below) for 64 positions; with 128 the registers hold
-  // no more addresses, and rows padded by 16 bytes are taken instead
-  constexpr bool SWZ = WCH == 1;
+  // the slot swizzle (below); unswizzled rows are padded by 16 bytes
+  constexpr bool SWZ = true;
   constexpr int RB = SWZ ? kQuadRowB : kQuadRowB + 16;
   constexpr int HALO_B = kQuadHaloRows * RB;
   constexpr int MAXP = kQuadMaxPieces;
@@ -1471,7 +1470,7 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
       const int cbi = cb0 + u;
       if (U > 1 && cbi >= cbn) break;  // the same for the whole workgroup
       const char* tile = tiles + (cbi & 1) * HALO_B;
-      if constexpr (NP == 4) {
+      if constexpr (!PF) {
         // recomputed per K block: hoisted, the 64 swizzled fragment
         // addresses would not fit the registers
 #pragma unroll

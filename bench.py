@@ -63,6 +63,9 @@ DESCRIPTIONS = {
                     "(4->8), 512->256, 256->128, 128->3 (32->64), bf16 NCHW, batch 1",
     "table1_cgan": "the paper's Table 1 cGAN deconvolutions: ConvT k4 s2 p1 256->128 (8->16), "
                    "128->3 (16->32), bf16 NCHW, batch 1",
+    "dcgan_generator": "the whole DCGAN generator, bf16 NCHW, batch 64: z (100) -> ConvT k4 s1 "
+                       "p0 to 4x4x1024, then ConvT k4 s2 p1 1024->512->256->128->3 (64x64); "
+                       "ReLU fused after each layer, tanh after the last",
     "dcgan_dgrad": "training (section 3.2.3): data gradients of the DCGAN generator's four ConvT "
                    "layers, back to front, as stride-2 convs of the output errors with the same "
                    "weights: 3->128 (64->32), 128->256, 256->512, 512->1024 (8->4), bf16 NCHW, "
@@ -112,7 +115,7 @@ def build_workload(name, dev):
         x_shape = ((layer.n, layer.c_in, layer.h, layer.w) if layer.layout == "NCHW"
                    else (layer.n, layer.h, layer.w, layer.c_in))
         plans.append(h2.Plan(w_dev, x_shape, layer.transposed, layer.stride, layer.pad,
-                             layer.out_pad, layer.dil, layer.layout))
+                             layer.out_pad, layer.dil, layer.layout, layer.act))
         inputs.append(None if x is None else wl.to_layout(x.to(dt), layer.layout).to(dev))
         del w_dev
     chained = name in wl.CHAINED
@@ -498,6 +501,7 @@ def cpu_baseline(name, target_s):
             else:
                 y = oracle.conv2d_dilated_alg2(xd, wd, None, layer.stride, layer.pad, layer.dil,
                                                nthreads=threads)
+            y = oracle.activate(y, layer.act)
             prev = __import__("torch").from_numpy(y).float()
             d = h2.make_desc(layer.n, layer.c_in, layer.h, layer.w, layer.c_out, layer.r,
                              layer.s, layer.stride, layer.pad, layer.out_pad, layer.dil,

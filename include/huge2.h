@@ -62,6 +62,12 @@ typedef enum {
 
 typedef enum { HUGE2_F32 = 0, HUGE2_BF16 = 1 } huge2_dtype;
 typedef enum { HUGE2_NCHW = 0, HUGE2_NHWC = 1 } huge2_layout;
+/* Elementwise function applied by the epilogue after the bias (the
+ * generator's nonlinearities, with batch normalisation folded into w and
+ * bias): y = act(op(x) + bias).  HUGE2_ACT_RELU: max(v, 0); HUGE2_ACT_TANH:
+ * tanh(v).  Forward entry points only; the weight-gradient entry points
+ * return HUGE2_ERR_UNSUPPORTED for any activation but HUGE2_ACT_NONE. */
+typedef enum { HUGE2_ACT_NONE = 0, HUGE2_ACT_RELU = 1, HUGE2_ACT_TANH = 2 } huge2_activation;
 
 /* Problem descriptor: the paper's Conv2DTranspose(I, K, O, s_m, s_n) and
  * Conv2DDilated(I, K, O, s_m, s_n) (Algorithms 1-2), extended with batch,
@@ -75,6 +81,7 @@ typedef struct {
   int32_t dil_h, dil_w;         /* >= 1 (the paper's s_m, s_n for the dilated conv) */
   int32_t layout;               /* huge2_layout */
   int32_t dtype;                /* huge2_dtype */
+  int32_t activation;           /* huge2_activation, applied after the bias (0: none) */
 } huge2_conv_desc;
 
 typedef struct huge2_plan huge2_plan; /* opaque */

@@ -16,6 +16,9 @@ marshals numpy arrays into it:
 * ``*_points`` -- the same definitions for selected output elements only.
 * ``*_wgrad`` -- the weight gradients of both (section 3.2.3, GAN training),
   written out from the definitions by the chain rule.
+* :func:`activate` -- the generator's elementwise functions applied after the
+  bias (ReLU between deconvolution layers, tanh after the last one), by their
+  definitions, in float64 (numpy).
 
 All arrays are float64 NCHW; transposed weights are ``[C_in, C_out, R, S]`` (the
 paper's C x N x R x S of section 4.2), conv weights ``[C_out, C_in, R, S]``.
@@ -203,3 +206,17 @@ def conv2d_dilated_wgrad(x, dy, w_shape, stride=1, padding=0, dilation=1, nthrea
                                            _threads(nthreads)):
         raise ValueError("oracle_conv2d_dilated_wgrad rejected its arguments")
     return dw
+
+
+def activate(y, act):
+    """The generator's nonlinearity applied to an oracle output: "none" (or
+    None) leaves y, "relu" is max(y, 0) and "tanh" the hyperbolic tangent,
+    elementwise in float64."""
+    if act in (None, "none"):
+        return y
+    y = _f64(y)
+    if act == "relu":
+        return np.maximum(y, 0.0)
+    if act == "tanh":
+        return np.tanh(y)
+    raise ValueError("unknown activation %r" % (act,))

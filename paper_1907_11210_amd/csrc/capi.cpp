@@ -829,6 +829,7 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
     z.wp = p->wp;
     z.bias = bias;
     z.y = y;
+    z.act = d.activation;
     if (launch_ztile(z, d.dtype, stream) != hipSuccess) {
       (void)hipGetLastError();
       return HUGE2_ERR_HIP;
@@ -841,6 +842,7 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
     z.wp = p->wp;
     z.bias = bias;
     z.y = y;
+    z.act = d.activation;
     if (launch_rowphase(z, stream) != hipSuccess) {
       (void)hipGetLastError();
       return HUGE2_ERR_HIP;
@@ -853,6 +855,7 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
     z.wp = p->wp;
     z.bias = bias;
     z.y = y;
+    z.act = d.activation;
     if (launch_quad(z, stream) != hipSuccess) {
       (void)hipGetLastError();
       return HUGE2_ERR_HIP;
@@ -864,6 +867,7 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
   a.wp = p->wp;
   a.bias = bias;
   a.y = y;
+  a.act = d.activation;
   a.segs = p->d_segs;
   a.taps = p->d_taps;
   a.works = p->d_works;
@@ -946,7 +950,7 @@ huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, i
   huge2_status st = validate_desc(desc, transposed != 0);
   if (st != HUGE2_OK) return st;
   const huge2_conv_desc& d = *desc;
-  if (d.layout != HUGE2_NCHW) return HUGE2_ERR_UNSUPPORTED;
+  if (d.layout != HUGE2_NCHW || d.activation != HUGE2_ACT_NONE) return HUGE2_ERR_UNSUPPORTED;
   int ho, wo;
   if (!output_dims(d, transposed != 0, &ho, &wo)) return HUGE2_ERR_INVALID_ARG;
   huge2_wgrad_plan* p = new (std::nothrow) huge2_wgrad_plan();

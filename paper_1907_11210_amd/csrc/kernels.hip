@@ -40,6 +40,12 @@ __device__ __forceinline__ int xcd_remap(int b, int g) {
   return r * g8 + (x - r) * (g8 - 1) + y;
 }
 
+// The epilogue's elementwise function (huge2_activation): 0 none, 1 max(v, 0),
+// 2 tanh(v).  act is uniform over the launch.
+__device__ __forceinline__ float activate(float v, int act) {
+  return act == 1 ? fmaxf(v, 0.f) : act == 2 ? tanhf(v) : v;
+}
+
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   // v_cvt_pk_bf16_f32: round to nearest even, NaN stays a (quiet) NaN
   return __builtin_bit_cast(uint16_t, (__bf16)f);
@@ -109,7 +115,7 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, const SegDev& sg,
         for (int j = 0; j < TC; ++j) {
           const int ch = ch0 + 32 * j + (lane & 31);
           if (ch >= a.cout) continue;
-          const float v = acc[i][j][r] + bv[j];
+          const float v = activate(acc[i][j][r] + bv[j], a.act);
           const size_t off = (size_t)pix * a.cout + ch;
           if constexpr (BF16)
             ((uint16_t*)a.y)[off] = f32_to_bf16_rne(v);
@@ -143,7 +149,7 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, const SegDev& sg,
         for (int r = 0; r < 16; ++r) {
           const int ch = ch0 + 32 * j + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
           if (ch >= a.cout) continue;
-          const float v = acc[i][j][r] + bv[r];
+          const float v = activate(acc[i][j][r] + bv[r], a.act);
           const size_t off = base[i] + (size_t)ch * hw_o;
           if constexpr (BF16)
             ((uint16_t*)a.y)[off] = f32_to_bf16_rne(v);
@@ -1039,7 +1045,7 @@ __global__ __launch_bounds__(kZtileThreads) void ztile_kernel(ZArgs a) {
             v += use[th][tw] ? z : 0.f;
           }
         }
-        if (ow < a.wo) ((uint16_t*)a.y)[off] = f32_to_bf16_rne(v);
+        if (ow < a.wo) ((uint16_t*)a.y)[off] = f32_to_bf16_rne(activate(v, a.act));
       }
     }
   }
@@ -1136,7 +1142,7 @@ __global__ __launch_bounds__(kRpThreads) void rowphase_kernel(RpArgs a) {
   const int npair = a.cout * (cp / 2);
   for (int e = tid; e < npair; e += NT) {
     const int kk = e / (cp / 2);
-    const uint32_t bb = f32_to_bf16_rne(s_b[kk]);
+    const uint32_t bb = f32_to_bf16_rne(activate(s_b[kk], a.act));
     *(uint32_t*)(s_out + (size_t)e * 2) = bb | (bb << 16);
   }
   __syncthreads();
@@ -1181,7 +1187,7 @@ __global__ __launch_bounds__(kRpThreads) void rowphase_kernel(RpArgs a) {
           const int mm = mb * 32 + 8 * (q >> 2) + 4 * half + (q & 3);
           if (mm >= npix) continue;
           const int qr = (int)(((float)mm + 0.5f) * inv_nqw), qwv = qw_lo + mm - qr * nqw;
-          s_out[k * cp + (qr * a.stride_w + rho_w) * nq + qwv] = f32_to_bf16_rne(acc[q] + bk);
+          s_out[k * cp + (qr * a.stride_w + rho_w) * nq + qwv] = f32_to_bf16_rne(activate(acc[q] + bk, a.act));
         }
       }
     }
@@ -1587,7 +1593,8 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
       for (int r = 0; r < 16; ++r) {
         const int ch = (hc * WCH + j) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
 #pragma unroll
-        for (int i = 0; i < NP; ++i) so[ch * cpo + pos[i]] = f32_to_bf16_rne(acc[j][i][r] + bv[j][r]);
+        for (int i = 0; i < NP; ++i)
+          so[ch * cpo + pos[i]] = f32_to_bf16_rne(activate(acc[j][i][r] + bv[j][r], a.act));
       }
   }
   __syncthreads();

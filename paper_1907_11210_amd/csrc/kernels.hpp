@@ -67,6 +67,7 @@ struct GemmArgs {
   int32_t cout, cout_pad;
   int32_t ho, wo;
   int32_t ks;  // kernel width s: weight slot of tap (kh, kw) = kh * ks + kw
+  int act;           // huge2_activation, applied after the bias
 };
 
 // Tile configurations of the phase GEMM kernel: BM pixels x BN output
@@ -188,6 +189,7 @@ struct ZArgs {
   int max_th, max_tw;  // largest tap count of a phase, per axis
   int8_t tap_k[2][kZtileMaxStride][kZtileMaxTaps];
   int8_t tap_d[2][kZtileMaxStride][kZtileMaxTaps];
+  int act;           // huge2_activation, applied after the bias
 };
 hipError_t launch_ztile(const ZArgs& a, int dtype, hipStream_t stream);
 
@@ -211,6 +213,7 @@ struct RpArgs {
   int rb;       // rows of one row phase per workgroup
   int qblocks;  // row blocks per (image, row phase)
   int nq;       // q_w slots per column phase in LDS (stride_w * nq a multiple of 8)
+  int act;           // huge2_activation, applied after the bias
 };
 hipError_t launch_rowphase(const RpArgs& a, hipStream_t stream);
 
@@ -243,6 +246,7 @@ struct QArgs {
   // per phase (2 * rho_h + rho_w) and tap (2 * th + tw): weight slot kh*4+kw
   // and input offsets: output (2q_h + rho_h, 2q_w + rho_w) reads input q + (dh, dw)
   int8_t slot[4][4], dh[4][4], dw[4][4];
+  int act;           // huge2_activation, applied after the bias
 };
 hipError_t launch_quad(const QArgs& a, hipStream_t stream);
 

@@ -171,6 +171,9 @@ huge2_status validate_desc(const huge2_conv_desc* d, bool transposed) {
     return HUGE2_ERR_INVALID_ARG;
   if (d->layout != HUGE2_NCHW && d->layout != HUGE2_NHWC) return HUGE2_ERR_INVALID_ARG;
   if (d->dtype != HUGE2_F32 && d->dtype != HUGE2_BF16) return HUGE2_ERR_INVALID_ARG;
+  if (d->activation != HUGE2_ACT_NONE && d->activation != HUGE2_ACT_RELU &&
+      d->activation != HUGE2_ACT_TANH)
+    return HUGE2_ERR_INVALID_ARG;
   if (transposed) {
     if (d->out_pad_h >= std::max(d->stride_h, d->dil_h) ||
         d->out_pad_w >= std::max(d->stride_w, d->dil_w))

@@ -20,6 +20,9 @@ LIB_PATH = os.path.join(_PKG, "libhuge2.so")
 HUGE2_OK, HUGE2_ERR_INVALID_ARG, HUGE2_ERR_UNSUPPORTED, HUGE2_ERR_ALLOC, HUGE2_ERR_HIP = range(5)
 HUGE2_F32, HUGE2_BF16 = 0, 1
 HUGE2_NCHW, HUGE2_NHWC = 0, 1
+HUGE2_ACT_NONE, HUGE2_ACT_RELU, HUGE2_ACT_TANH = 0, 1, 2
+ACTIVATIONS = {None: HUGE2_ACT_NONE, "none": HUGE2_ACT_NONE, "relu": HUGE2_ACT_RELU,
+               "tanh": HUGE2_ACT_TANH}
 
 EXPORTED = (
     "huge2_status_str", "huge2_output_shape", "huge2_plan_create", "huge2_plan_execute",
@@ -41,7 +44,7 @@ class Huge2Error(RuntimeError):
 class ConvDesc(ctypes.Structure):
     _fields_ = [(f, ctypes.c_int32) for f in (
         "n", "c_in", "h", "w", "c_out", "r", "s", "stride_h", "stride_w", "pad_h", "pad_w",
-        "out_pad_h", "out_pad_w", "dil_h", "dil_w", "layout", "dtype")]
+        "out_pad_h", "out_pad_w", "dil_h", "dil_w", "layout", "dtype", "activation")]
 
 
 class Segment(ctypes.Structure):
@@ -113,12 +116,13 @@ def _pair(v):
 
 
 def make_desc(n, c_in, h, w, c_out, r, s, stride=1, padding=0, output_padding=0, dilation=1,
-              layout=HUGE2_NCHW, dtype=HUGE2_F32):
+              layout=HUGE2_NCHW, dtype=HUGE2_F32, activation=HUGE2_ACT_NONE):
     sh, sw = _pair(stride)
     ph, pw = _pair(padding)
     oph, opw = _pair(output_padding)
     dh, dw = _pair(dilation)
-    return ConvDesc(n, c_in, h, w, c_out, r, s, sh, sw, ph, pw, oph, opw, dh, dw, layout, dtype)
+    return ConvDesc(n, c_in, h, w, c_out, r, s, sh, sw, ph, pw, oph, opw, dh, dw, layout, dtype,
+                    activation)
 
 
 # ---- the C entry points ---------------------------------------------------
@@ -271,7 +275,14 @@ def _check_tensor(t, name, device=None):
         raise ValueError("%s is on %s, expected %s" % (name, t.device, device))
 
 
-def _desc_for(x, w, transposed, stride, padding, output_padding, dilation, layout):
+def _act_code(activation):
+    if activation not in ACTIVATIONS:
+        raise ValueError("unknown activation %r (none, relu, tanh)" % (activation,))
+    return ACTIVATIONS[activation]
+
+
+def _desc_for(x, w, transposed, stride, padding, output_padding, dilation, layout,
+              activation=None):
     lay = _layout_code(layout)
     if x.dim() != 4 or w.dim() != 4:
         raise ValueError("x and w must be 4-D")
@@ -288,7 +299,7 @@ def _desc_for(x, w, transposed, stride, padding, output_padding, dilation, layou
     if w.dtype != x.dtype:
         raise ValueError("x and w must share a dtype")
     return make_desc(n, c_in, h, wd, c_out, r, s, stride, padding, output_padding, dilation,
-                     lay, _dtype_code(x))
+                     lay, _dtype_code(x), _act_code(activation))
 
 
 def _out_shape(desc, transposed):
@@ -313,12 +324,13 @@ def _stream(x):
 
 
 def conv2d_transpose(x, w, bias=None, stride=1, padding=0, output_padding=0, dilation=1,
-                     layout="NCHW", out=None):
-    """Transposed conv on the GPU (w: [C_in, C_out, R, S]); returns y."""
+                     layout="NCHW", out=None, activation=None):
+    """Transposed conv on the GPU (w: [C_in, C_out, R, S]); returns
+    y = activation(op(x) + bias), activation None, "relu" or "tanh"."""
     torch = _torch()
     _check_tensor(x, "x")
     _check_tensor(w, "w", x.device)
-    desc = _desc_for(x, w, True, stride, padding, output_padding, dilation, layout)
+    desc = _desc_for(x, w, True, stride, padding, output_padding, dilation, layout, activation)
     shape = _out_shape(desc, True)
     if desc.c_out != w.shape[1] or bias is not None and bias.numel() != desc.c_out:
         raise ValueError("bias size does not match C_out")
@@ -331,12 +343,14 @@ def conv2d_transpose(x, w, bias=None, stride=1, padding=0, output_padding=0, dil
     return y
 
 
-def conv2d_dilated(x, w, bias=None, stride=1, padding=0, dilation=1, layout="NCHW", out=None):
-    """Dilated / strided conv on the GPU (w: [C_out, C_in, R, S]); returns y."""
+def conv2d_dilated(x, w, bias=None, stride=1, padding=0, dilation=1, layout="NCHW", out=None,
+                   activation=None):
+    """Dilated / strided conv on the GPU (w: [C_out, C_in, R, S]); returns
+    y = activation(op(x) + bias)."""
     torch = _torch()
     _check_tensor(x, "x")
     _check_tensor(w, "w", x.device)
-    desc = _desc_for(x, w, False, stride, padding, 0, dilation, layout)
+    desc = _desc_for(x, w, False, stride, padding, 0, dilation, layout, activation)
     shape = _out_shape(desc, False)
     if bias is not None and bias.numel() != desc.c_out:
         raise ValueError("bias size does not match C_out")
@@ -417,7 +431,7 @@ class Plan:
     :meth:`__call__` enqueues huge2_plan_execute on the current stream."""
 
     def __init__(self, w, x_shape, transposed, stride=1, padding=0, output_padding=0,
-                 dilation=1, layout="NCHW"):
+                 dilation=1, layout="NCHW", activation=None):
         torch = _torch()
         _check_tensor(w, "w")
         dummy = torch.empty(0, dtype=w.dtype)
@@ -433,7 +447,7 @@ class Plan:
         if wc_in != c_in:
             raise ValueError("weight has %d input channels, x has %d" % (wc_in, c_in))
         self.desc = make_desc(n, c_in, h, wd, c_out, r, s, stride, padding, output_padding,
-                              dilation, lay, _dtype_code(dummy))
+                              dilation, lay, _dtype_code(dummy), _act_code(activation))
         self.transposed = bool(transposed)
         self.device = w.device
         self.dtype = w.dtype

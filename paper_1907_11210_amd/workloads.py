@@ -29,6 +29,13 @@ Workloads (``name``: layers):
                with the phase roles mirrored).  Input N(0,1), weights N(0,0.02), chained.
   table1_cgan  the cGAN layers of Table 1: 4x4 kernels, stride 2, pad 1,
                8x8x256 -> 16x16x128 -> 32x32x3, batch 1, bf16 NCHW, chained.
+  dcgan_generator
+               the whole DCGAN generator on the library, bf16 NCHW, batch 64: the projection
+               of z (100-d, N(0,1)) to 4x4x1024 as a ConvTranspose k4 s1 p0 of the 1x1 input,
+               then the four dcgan layers; ReLU after every layer but the last, tanh after
+               the last, fused into the epilogues (batch normalisation, which a trained
+               generator folds into weights and bias, is left out: no bias).  Weights
+               N(0,0.02), chained.
   dcgan_dgrad  training (section 3.2.3): the data gradients of the dcgan generator's
                four ConvTranspose layers, back to front.  The gradient of a stride-2
                transposed conv with respect to its input is the stride-2 conv of the
@@ -63,6 +70,7 @@ class Layer:
     dil: int
     layout: str  # "NCHW" or "NHWC"
     dtype: str   # "f32" or "bf16"
+    act: str = "none"  # epilogue function after the bias: "none", "relu" or "tanh"
 
     def out_hw(self):
         if self.transposed:
@@ -98,6 +106,13 @@ def dcgan_dgrad_layers(dtype="bf16", batch=64):
             for i, l in enumerate(reversed(fwd))]
 
 
+def generator_layers(dtype="bf16", batch=64):
+    proj = Layer("gen_proj", True, batch, 100, 1, 1, 1024, 4, 4, 1, 0, 0, 1, "NCHW", dtype, "relu")
+    body = [l.with_(name=l.name.replace("dcgan", "gen"), act="relu" if i < 3 else "tanh")
+            for i, l in enumerate(dcgan_layers(dtype, batch))]
+    return [proj] + body
+
+
 def table1_layers(kind, batch=1, dtype="bf16"):
     if kind == "dcgan":
         chans, k, pad, op, hw0 = [(1024, 512), (512, 256), (256, 128), (128, 3)], 5, 2, 1, 4
@@ -123,8 +138,9 @@ WORKLOADS = {
     "table1_dcgan": table1_layers("dcgan"),
     "table1_cgan": table1_layers("cgan"),
     "dcgan_dgrad": dcgan_dgrad_layers("bf16"),
+    "dcgan_generator": generator_layers("bf16"),
 }
-CHAINED = ("dcgan", "dcgan_f32", "table1_dcgan", "table1_cgan", "dcgan_dgrad")
+CHAINED = ("dcgan", "dcgan_f32", "table1_dcgan", "table1_cgan", "dcgan_dgrad", "dcgan_generator")
 
 
 def torch_dtype(name):
@@ -163,6 +179,11 @@ def generate(workload, seed=0, batch=None):
         out = [(layers[0], x1, ws[0])]
         out += [(l, None, w) for l, w in zip(layers[1:], ws[1:])]
         return out
+    if workload == "dcgan_generator":
+        l0 = layers[0]
+        z = _normal(g, (l0.n, 100, 1, 1))
+        ws = [_normal(g, l.w_shape(), 0.02) for l in layers]
+        return [(layers[0], z, ws[0])] + [(l, None, w) for l, w in zip(layers[1:], ws[1:])]
     if workload == "dcgan_dgrad":
         # the dcgan draws (z, linear weight, w1..w4), then the output error
         n = layers[0].n

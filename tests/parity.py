@@ -48,9 +48,13 @@ def oracle_full(layer, xq, wq, bias=None, absolute=False):
     if absolute:
         x, w, b = np.abs(x), np.abs(w), None if b is None else np.abs(b)
     if layer.transposed:
-        return oracle.conv2d_transpose_alg1(x, w, b, layer.stride, layer.pad, layer.out_pad,
-                                            layer.dil)
-    return oracle.conv2d_dilated_alg2(x, w, b, layer.stride, layer.pad, layer.dil)
+        y = oracle.conv2d_transpose_alg1(x, w, b, layer.stride, layer.pad, layer.out_pad,
+                                         layer.dil)
+    else:
+        y = oracle.conv2d_dilated_alg2(x, w, b, layer.stride, layer.pad, layer.dil)
+    # |act(u) - act(v)| <= |u - v| for both functions: the bound of the
+    # absolute-value run still holds after the activation
+    return y if absolute else oracle.activate(y, layer.act)
 
 
 def oracle_points(layer, xq, wq, idx, bias=None, absolute=False):
@@ -60,14 +64,16 @@ def oracle_points(layer, xq, wq, idx, bias=None, absolute=False):
     if absolute:
         x, w, b = np.abs(x), np.abs(w), None if b is None else np.abs(b)
     if layer.transposed:
-        return oracle.conv2d_transpose_points(x, w, idx, b, layer.stride, layer.pad,
-                                              layer.out_pad, layer.dil)
-    return oracle.conv2d_dilated_points(x, w, idx, b, layer.stride, layer.pad, layer.dil)
+        y = oracle.conv2d_transpose_points(x, w, idx, b, layer.stride, layer.pad,
+                                           layer.out_pad, layer.dil)
+    else:
+        y = oracle.conv2d_dilated_points(x, w, idx, b, layer.stride, layer.pad, layer.dil)
+    return y if absolute else oracle.activate(y, layer.act)
 
 
 def make_plan(layer, w_dev):
     return h2.Plan(w_dev, _x_shape(layer), layer.transposed, layer.stride, layer.pad,
-                   layer.out_pad, layer.dil, layer.layout)
+                   layer.out_pad, layer.dil, layer.layout, layer.act)
 
 
 def _x_shape(layer):
@@ -85,10 +91,10 @@ def run_gpu(layer, xq, wq, bias=None, one_shot=False, plan=None):
     if one_shot:
         if layer.transposed:
             y = h2.conv2d_transpose(x_dev, w_dev, b_dev, layer.stride, layer.pad, layer.out_pad,
-                                    layer.dil, layer.layout)
+                                    layer.dil, layer.layout, activation=layer.act)
         else:
             y = h2.conv2d_dilated(x_dev, w_dev, b_dev, layer.stride, layer.pad, layer.dil,
-                                  layer.layout)
+                                  layer.layout, activation=layer.act)
     else:
         p = plan if plan is not None else make_plan(layer, w_dev)
         y = p(x_dev, b_dev)

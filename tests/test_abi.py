@@ -54,6 +54,7 @@ def _good():
 @pytest.mark.parametrize("field,value", [
     ("n", 0), ("c_in", 0), ("h", -1), ("c_out", 0), ("r", 0), ("stride_h", 0), ("dil_w", 0),
     ("pad_h", -1), ("out_pad_w", 2), ("layout", 2), ("dtype", 7), ("pad_h", 40),
+    ("activation", 3), ("activation", -1),
 ])
 def test_invalid_descriptor_rejected_without_gpu(L, field, value):
     d = _good()
@@ -158,6 +159,9 @@ def test_weight_gradient_entry_points_validate_without_gpu(L, monkeypatch):
     nhwc = _good()
     nhwc.layout = h2.HUGE2_NHWC
     assert L.huge2_wgrad_plan_create(ctypes.byref(plan), ctypes.byref(nhwc), 1) == h2.HUGE2_ERR_UNSUPPORTED
+    fused = _good()
+    fused.activation = h2.HUGE2_ACT_RELU  # the gradient of a fused activation is not built
+    assert L.huge2_wgrad_plan_create(ctypes.byref(plan), ctypes.byref(fused), 1) == h2.HUGE2_ERR_UNSUPPORTED
     assert L.huge2_wgrad_execute(None, fake, fake, other, None) == h2.HUGE2_ERR_INVALID_ARG
     assert L.huge2_wgrad_plan_destroy(None) == h2.HUGE2_OK
     # one-shot forms: NULL and aliased pointers, before any allocation

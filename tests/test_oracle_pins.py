@@ -335,3 +335,23 @@ def test_wgrad_matches_torch_autograd(oracle_mod, transposed):
         np.testing.assert_allclose(got, w.grad.numpy(), rtol=1e-10, atol=1e-10)
         checked += 1
     assert checked >= 30
+
+
+@pytest.mark.parametrize("act", ["relu", "tanh"])
+def test_activation_matches_torch(oracle_mod, act):
+    """The generator's fused activations against torch's own functions on a
+    transposed conv (bias included) in float64, and the identity for none."""
+    rng = np.random.default_rng(7)
+    x = rng.standard_normal((2, 5, 6, 7))
+    w = rng.standard_normal((5, 3, 4, 4)) * 0.3
+    b = rng.standard_normal(3)
+    y = oracle_mod.conv2d_transpose_alg1(x, w, b, 2, 1, 0, 1)
+    ref = torch.nn.functional.conv_transpose2d(torch.from_numpy(x), torch.from_numpy(w),
+                                               torch.from_numpy(b), stride=2, padding=1)
+    ref = torch.relu(ref) if act == "relu" else torch.tanh(ref)
+    got = oracle_mod.activate(y, act)
+    np.testing.assert_allclose(got, ref.numpy(), rtol=1e-12, atol=1e-12)
+    assert (got >= 0).all() if act == "relu" else (np.abs(got) < 1).all()
+    assert oracle_mod.activate(y, "none") is y
+    with pytest.raises(ValueError):
+        oracle_mod.activate(y, "gelu")

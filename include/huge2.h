@@ -16,6 +16,8 @@
  *       y[n,k,oh,ow] = bias[k] + sum_{c,m,q} x[n,c, oh*stride_h - pad_h + m*dil_h,
  *                                              ow*stride_w - pad_w + q*dil_w] * w[k,c,m,q],
  *     h_out = floor((h + 2*pad_h - dil_h*(r-1) - 1)/stride_h) + 1.
+ *   Both then apply desc->activation elementwise (none, ReLU or tanh; see
+ *   huge2_activation) before rounding to the output dtype.
  *
  * How (section 3): the kernel is decomposed into stride_h*stride_w phase
  * sub-kernels (section 3.1, Eq. 1-4); each phase is a dense convolution over

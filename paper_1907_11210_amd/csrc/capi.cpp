@@ -46,6 +46,7 @@ struct huge2_plan {
   RpArgs rpargs;
   bool quad;      // all-phase form of the stride-2, 4x4, padding-1 layer
   QArgs qargs;
+  int bias_div;   // GEMM columns per bias entry (r * s for the 1x1-input product form)
   char kernel_name[64];
 };
 
@@ -576,6 +577,7 @@ huge2_status create_direct(huge2_plan** out, const huge2_conv_desc& d, int trans
   const int esz = elem_size(d.dtype);
   p->desc = d;
   p->transposed = transposed;
+  p->bias_div = 1;
   output_dims(d, true, &p->ho, &p->wo);
   p->cfg = -1;
   p->staged = false;
@@ -631,8 +633,25 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   huge2_status st = validate_desc(desc, transposed != 0);
   if (st != HUGE2_OK) return st;
   if (!w) return HUGE2_ERR_INVALID_ARG;
-  const huge2_conv_desc& d = *desc;
   const bool tr = transposed != 0;
+  // A transposed conv of a 1x1 NCHW input with no padding and unit dilation
+  // is the plain product y[n][k*r*s + m*s + q] = sum_c x[n][c] w[c][k][m][q]
+  // (section 3.1 with a single input pixel: every tap its own phase and
+  // output pixel): one dense GEMM of n rows, on the same memory read as a
+  // 1x1 conv to c_out*r*s channels (x [n][c_in], w [c_in][c_out*r*s], y
+  // [n][c_out*r*s]).  Bias k then covers r*s consecutive GEMM columns.
+  huge2_conv_desc dd = *desc;
+  int bias_div = 1;
+  if (tr && dd.h == 1 && dd.w == 1 && dd.layout == HUGE2_NCHW && dd.pad_h == 0 && dd.pad_w == 0 &&
+      dd.out_pad_h == 0 && dd.out_pad_w == 0 && dd.dil_h == 1 && dd.dil_w == 1 &&
+      (dd.r > 1 || dd.s > 1) && (long long)dd.c_out * dd.r * dd.s <= INT32_MAX / 2) {
+    bias_div = dd.r * dd.s;
+    dd.c_out = dd.c_out * dd.r * dd.s;
+    dd.r = dd.s = 1;
+    dd.stride_h = dd.stride_w = 1;
+    dd.layout = HUGE2_NHWC;
+  }
+  const huge2_conv_desc& d = dd;
 
   {
     ZArgs z;
@@ -661,6 +680,7 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   p->transposed = transposed;
   output_dims(d, tr, &p->ho, &p->wo);
   p->cfg = cfg;
+  p->bias_div = bias_div;
   {
     const TileShape& t = kTiles[cfg];
     if (t.kind == 0)
@@ -867,6 +887,7 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
   a.wp = p->wp;
   a.bias = bias;
   a.y = y;
+  a.bias_div = p->bias_div;
   a.act = d.activation;
   a.segs = p->d_segs;
   a.taps = p->d_taps;

@@ -240,7 +240,7 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
 
   __shared__ float s_bias[BN];
   for (int t = tid; t < BN; t += NT)
-    s_bias[t] = (a.bias && wk.n0 + t < a.cout) ? a.bias[wk.n0 + t] : 0.f;
+    s_bias[t] = (a.bias && wk.n0 + t < a.cout) ? a.bias[(wk.n0 + t) / a.bias_div] : 0.f;
 
   // The segment's taps in LDS: byte delta of the tapped pixel and byte
   // offset of the tap's weight block.
@@ -554,7 +554,7 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm2_kernel(GemmArgs a) {
 
   __shared__ float s_bias[BN];
   for (int t = threadIdx.x; t < BN; t += NTA)
-    s_bias[t] = (a.bias && wk.n0 + t < a.cout) ? a.bias[wk.n0 + t] : 0.f;
+    s_bias[t] = (a.bias && wk.n0 + t < a.cout) ? a.bias[(wk.n0 + t) / a.bias_div] : 0.f;
   __shared__ int4 s_taps[kMaxLdsTaps];
   const bool lds_taps = !sg.tap_ap && ntaps <= kMaxLdsTaps;
   if (lds_taps) {

@@ -55,7 +55,7 @@ struct WorkDev {
 struct GemmArgs {
   const void* x;      // input, channel-contiguous: [n][h][w][cin]
   const void* wp;     // packed weights: [slot][cout_pad][cin_pad]
-  const float* bias;  // [cout] or null
+  const float* bias;  // [cout / bias_div] or null: output channel ch takes bias[ch / bias_div]
   void* y;            // output, NCHW or NHWC
   const SegDev* segs;
   const TapDev* taps;
@@ -67,6 +67,7 @@ struct GemmArgs {
   int32_t cout, cout_pad;
   int32_t ho, wo;
   int32_t ks;  // kernel width s: weight slot of tap (kh, kw) = kh * ks + kw
+  int32_t bias_div;
   int act;           // huge2_activation, applied after the bias
 };
 

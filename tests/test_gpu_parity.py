@@ -68,6 +68,10 @@ SMALL = [
     L("ct_quad_w64", True, 1, 64, 4, 64, 32, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
     L("ct_quad_np4_rows", True, 2, 128, 16, 16, 64, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
     L("ct_quad_np4_ragged", True, 3, 128, 8, 8, 48, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
+    # a 1x1 input (the generator's projection of z): one dense GEMM
+    L("ct_1x1_proj", True, 3, 20, 1, 1, 24, 4, 4, 1, 0, 0, 1, "NCHW", "bf16"),
+    L("ct_1x1_proj_f32", True, 2, 16, 1, 1, 8, 3, 5, 2, 0, 0, 1, "NCHW", "f32"),
+    L("ct_1x1_nhwc", True, 2, 16, 1, 1, 8, 3, 3, 1, 0, 0, 1, "NHWC", "bf16"),
 ]
 
 
@@ -426,7 +430,7 @@ def test_all_phase_forms(layer, quad, wch, np_, ks, monkeypatch):
 # phase), all-taps, row-phase and all-phase
 ACT_LAYERS = [SMALL[i] for i in range(len(SMALL)) if SMALL[i].name in (
     "ct_fewout_bf16", "ct_rowphase_zerotap", "ct_rowphase_s4", "ct_quad_img8", "ct_quad_np4_rows",
-    "dil_f32_nchw", "conv_plain", "dil_aspp_d6")]
+    "dil_f32_nchw", "conv_plain", "dil_aspp_d6", "ct_1x1_proj")]
 
 
 @pytest.mark.parametrize("act", ["relu", "tanh"])

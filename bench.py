@@ -197,7 +197,12 @@ PROFILE_COMMANDS = [
                    "python3 $R/bench.py --copy-calibration"),
     ("copy_write", "timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE -f csv -d $O -o copy_write -- "
                    "python3 $R/bench.py --copy-calibration"),
+    ("mfma", "timeout -s KILL 120 rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_VALU_MFMA_BF16 "
+             "-f csv -d $O -o mfma -- python3 $R/bench.py --workload {w} --no-cpu-baseline "
+             "--no-library-reference --steps 3 --warmup 1"),
 ]
+# one bf16 MFMA "MOP" is 512 flops (a 32x32x16 bf16 MFMA, 32768 flops, counts 64)
+MFMA_FLOPS_PER_MOP_BF16 = 512
 
 
 def _csv_rows(path):
@@ -311,6 +316,29 @@ def summarize_profiles(d, workload):
             traffic["layers"][l.name] = {"fetch_kib": round(fk, 1), "write_kib": round(wk, 1),
                                          "traffic_bytes": int(round(tb)), "algorithmic_bytes": algo}
             lines.append("| %s | %.1f | %.1f | %.2f | %.2f |" % (l.name, fk, wk, tb / 1e6, algo / 1e6))
+    mfma_csv = os.path.join(d, "mfma_counter_collection.csv")
+    if os.path.exists(mfma_csv):
+        from paper_1907_11210_amd import huge2 as h2
+        mops = _counter_per_dispatch(mfma_csv, "SQ_INSTS_VALU_MFMA_MOPS_BF16")
+        lines += ["", "## MFMA work of each layer's main kernel (SQ_INSTS_VALU_MFMA_MOPS_BF16)", "",
+                  "Counted MFMA flops = %d x MOPs per dispatch. Utilisation = counted flops / mean "
+                  "duration (kernel trace above) / %.1f TFLOP/s (the published dense bf16 peak); "
+                  "structural = the non-zero MACs of the layer, the same numerator as the "
+                  "benchmark's effective TFLOP/s." % (MFMA_FLOPS_PER_MOP_BF16, PEAK["bf16"]), "",
+                  "| layer | counted MFMA GFLOP | issued (plan) GFLOP | structural GFLOP | "
+                  "MFMA utilisation | structural / peak |", "|---|---|---|---|---|---|"]
+        for l, ids in zip(layers, _layer_dispatches(mops, nl)):
+            if l.dtype != "bf16":
+                continue
+            cf = MFMA_FLOPS_PER_MOP_BF16 * float(np.mean([mops[i][1] for i in ids]))
+            desc = h2.make_desc(l.n, l.c_in, l.h, l.w, l.c_out, l.r, l.s, l.stride, l.pad,
+                                l.out_pad, l.dil, h2.HUGE2_NCHW, h2.HUGE2_BF16)
+            nz = 2.0 * h2.huge2_plan_macs(desc, l.transposed)[0]
+            issued = 2.0 * h2.huge2_plan_macs(desc, l.transposed)[1] if l.layout == "NCHW" else float("nan")
+            t = avg_us[l.name] * 1e-6
+            lines.append("| %s | %.2f | %.2f | %.2f | %.3f | %.3f |" % (
+                l.name, cf / 1e9, issued / 1e9, nz / 1e9, cf / t / (PEAK["bf16"] * 1e12),
+                nz / t / (PEAK["bf16"] * 1e12)))
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
     with open(os.path.join(ROOT, "profiles", "layer_kernels_%s.md" % workload), "w") as f:
         f.write("\n".join(lines) + "\n")

@@ -25,7 +25,8 @@ Prints ONE JSON line.  Fields beyond the standard ones:
                 rocprofv3 counter summary when it matches the kernel source.
   cpu_baseline  the CPU oracle (Algorithm 1 zero insertion / Algorithm 2
                 gather, float64) timed on a bounded sample of the workload.
-  layers        per-layer mean time, effective TFLOP/s, issued-MAC utilisation.
+  layers        per-layer mean time, effective TFLOP/s, issued-MAC utilisation and
+                achieved algorithmic HBM GB/s (|x| + |w| + |y| per launch / time).
   library_reference
                 context for roofline.frac, not part of the path: the vendor
                 library's dense GEMM (torch.matmul -> hipBLASLt) of the same
@@ -666,6 +667,7 @@ def main():
             "mfma_issued_util": round(issued[i] / (gemm_ms[i] * 1e-3) / 1e12 / PEAK[layer.dtype], 4),
             "nz_gflop": round(flops[i] / 1e9, 3),
             "algorithmic_mb": round(nbytes / 1e6, 2),
+            "gemm_alg_gbs": round(nbytes / (gemm_ms[i] * 1e-3) / 1e9, 1),
         })
     dom = int(np.argmax(gemm_ms))
     # The dominant layer's main kernel alone: its input staged once, then

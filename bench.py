@@ -561,7 +561,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: the kernels shard by batch, output channel or "
-              "phase without communication, and no multi-GPU run is part of this build "
+              "phase without communication, and there is no multi-GPU path "
               "(asked for --gpus %d, WORLD_SIZE %d)" % (args.gpus, world), file=sys.stderr)
         sys.exit(2)
 

@@ -47,6 +47,8 @@ struct huge2_plan {
   bool quad;      // all-phase form of the stride-2, 4x4, padding-1 layer
   QArgs qargs;
   int bias_div;   // GEMM columns per bias entry (r * s for the 1x1-input product form)
+  int ksplit;     // K slices across workgroups (1: none)
+  void* part;     // their fp32 partial outputs, ksplit x |y| (or null)
   char kernel_name[64];
 };
 
@@ -128,7 +130,7 @@ void order_works_for_xcds(std::vector<WorkDev>& works, const std::vector<SegDev>
   const int b = best_b, a = 8 / best_b;
   struct Key {
     int64_t cell, pos;
-    int32_t seg, m0, n0;
+    int32_t seg, m0, n0, ks;
   };
   std::vector<Key> keys;
   keys.reserve(works.size());
@@ -150,6 +152,7 @@ void order_works_for_xcds(std::vector<WorkDev>& works, const std::vector<SegDev>
     k.seg = w.seg;
     k.m0 = w.m0;
     k.n0 = w.n0;
+    k.ks = w.ks;
     keys.push_back(k);
   }
   std::stable_sort(keys.begin(), keys.end(), [](const Key& x, const Key& y) {
@@ -157,12 +160,14 @@ void order_works_for_xcds(std::vector<WorkDev>& works, const std::vector<SegDev>
     if (x.pos != y.pos) return x.pos < y.pos;
     if (x.seg != y.seg) return x.seg < y.seg;
     if (x.m0 != y.m0) return x.m0 < y.m0;
-    return x.n0 < y.n0;
+    if (x.n0 != y.n0) return x.n0 < y.n0;
+    return x.ks < y.ks;
   });
   for (size_t i = 0; i < works.size(); ++i) {
     works[i].seg = keys[i].seg;
     works[i].m0 = keys[i].m0;
     works[i].n0 = keys[i].n0;
+    works[i].ks = keys[i].ks;
   }
 }
 
@@ -538,7 +543,7 @@ int plan_gemm_shape(const huge2_conv_desc& d, bool tr, PlanShape* shape) {
 
 
 void free_buffers(huge2_plan* p) {
-  void* bufs[3] = {p->wp, p->meta, p->xs};
+  void* bufs[4] = {p->wp, p->meta, p->xs, p->part};
   for (void* b : bufs) {
     if (!b) continue;
     if (p->stream_ordered)
@@ -546,7 +551,7 @@ void free_buffers(huge2_plan* p) {
     else
       (void)hipFree(b);
   }
-  p->wp = p->meta = p->xs = nullptr;
+  p->wp = p->meta = p->xs = p->part = nullptr;
 }
 
 huge2_status dev_alloc(huge2_plan* p, void** out, size_t bytes) {
@@ -578,6 +583,7 @@ huge2_status create_direct(huge2_plan** out, const huge2_conv_desc& d, int trans
   p->desc = d;
   p->transposed = transposed;
   p->bias_div = 1;
+  p->ksplit = 1;
   output_dims(d, true, &p->ho, &p->wo);
   p->cfg = -1;
   p->staged = false;
@@ -766,12 +772,34 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
         wd.seg = (int32_t)i;
         wd.m0 = m0;
         wd.n0 = nt * bn;
-        wd.pad = 0;
+        wd.ks = 0;
         works.push_back(wd);
         issued += (int64_t)bm * bn * s.tap_count * p->cin_pad;
       }
   }
   p->issued_macs = issued;
+  // Too few tiles to give every compute unit one: split the input channel
+  // blocks into ksplit slices, one workgroup per (tile, slice), whose fp32
+  // partials a second kernel adds in slice order (deterministic), with the
+  // bias and activation.  The partials cost 2 x 4 x ksplit bytes per output.
+  {
+    const int cblocks = p->cin_pad / bk;
+    int ks = std::min({cblocks, kComputeUnits / std::max(1, (int)works.size()), 8});
+    const int forced = env_int("HUGE2_SPLITK", -1);
+    if (forced >= 1) ks = std::min(forced, cblocks);
+    const size_t ny = (size_t)d.n * d.c_out * p->ho * p->wo;
+    while (ks > 1 && (ks * ny * 4 > ((size_t)1 << 28) || ny >= ((size_t)1 << 31))) --ks;
+    p->ksplit = std::max(1, ks);
+    if (p->ksplit > 1) {
+      const size_t nw = works.size();
+      for (int k = 1; k < p->ksplit; ++k)
+        for (size_t i = 0; i < nw; ++i) {
+          WorkDev wd = works[i];
+          wd.ks = k;
+          works.push_back(wd);
+        }
+    }
+  }
   p->n_works = (int)works.size();
   // NCHW outputs of transposed convs with few phases: the phases of a
   // region share input rows and output cache lines (measured: fewer bytes and
@@ -789,9 +817,12 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   const size_t xs_b = p->staged ? p->x_bytes : 0;
   p->wp_bytes = wp_b;
 
+  const size_t part_b =
+      p->ksplit > 1 ? (size_t)p->ksplit * d.n * d.c_out * p->ho * p->wo * sizeof(float) : 0;
   if ((st = dev_alloc(p, &p->meta, meta_b)) != HUGE2_OK ||
       (st = dev_alloc(p, &p->wp, wp_b)) != HUGE2_OK ||
-      (st = dev_alloc(p, &p->xs, xs_b)) != HUGE2_OK) {
+      (st = dev_alloc(p, &p->xs, xs_b)) != HUGE2_OK ||
+      (st = dev_alloc(p, &p->part, part_b)) != HUGE2_OK) {
     free_buffers(p);
     delete p;
     return st;
@@ -889,6 +920,14 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
   a.y = y;
   a.bias_div = p->bias_div;
   a.act = d.activation;
+  a.ksplit = p->ksplit;
+  a.part = (float*)p->part;
+  a.part_stride = (uint32_t)((size_t)d.n * d.c_out * p->ho * p->wo);
+  if (p->ksplit > 1) {
+    // the slices write partials; bias and activation come with the sum
+    a.bias = nullptr;
+    a.act = HUGE2_ACT_NONE;
+  }
   a.segs = p->d_segs;
   a.taps = p->d_taps;
   a.works = p->d_works;
@@ -908,6 +947,24 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
   if (launch_phase_gemm(a, d.dtype, p->cfg, d.layout == HUGE2_NCHW, stream) != hipSuccess) {
     (void)hipGetLastError();
     return HUGE2_ERR_HIP;
+  }
+  if (p->ksplit > 1) {
+    SplitKArgs r;
+    r.part = (const float*)p->part;
+    r.bias = bias;
+    r.y = y;
+    r.stride = a.part_stride;
+    r.total = a.part_stride;
+    r.ksplit = p->ksplit;
+    r.cout = d.c_out;
+    r.hw = p->ho * p->wo;
+    r.nchw = d.layout == HUGE2_NCHW ? 1 : 0;
+    r.bias_div = p->bias_div;
+    r.act = d.activation;
+    if (launch_splitk_reduce(r, d.dtype, stream) != hipSuccess) {
+      (void)hipGetLastError();
+      return HUGE2_ERR_HIP;
+    }
   }
   return HUGE2_OK;
 }

@@ -11,6 +11,7 @@
 //  pack_weights_kernel the per-tap sub-kernel blocks (the N x C matrix of each
 //                      kernel position, section 3.2.1), K-contiguous.
 //  stage_*_kernel      input re-layout to channel-contiguous pixels.
+#include <algorithm>
 #include <type_traits>
 
 #include "kernels.hpp"
@@ -234,7 +235,9 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
   }
   const int ntaps = sg.tap_count;
   const int cblocks = a.cin_pad / KC;
-  const int nsteps = ntaps * cblocks;
+  // this workgroup's K slice of channel blocks, [cb_w0, cb_w1)
+  const int cb_w0 = wk.ks * cblocks / a.ksplit, cb_w1 = (wk.ks + 1) * cblocks / a.ksplit;
+  const int nsteps = ntaps * (cb_w1 - cb_w0);
   // channels of the last K block that exist (a partial block needs masking)
   const int tail_c = a.cin - (cblocks - 1) * KC;
 
@@ -281,7 +284,7 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
   // past the last stage goes through the empty resources instead of
   // branching around the loads: the load sequence stays the same on every
   // path, which lets the compiler wait only for the stage it stores.
-  int ld_tap = 0, ld_cb = 0, ld_th = 0, ld_tw = 0;
+  int ld_tap = 0, ld_cb = cb_w0, ld_th = 0, ld_tw = 0;
   const uint32_t slot_bytes = (uint32_t)a.cout_pad * (uint32_t)a.cin_pad * ESZ;
   auto load_step = [&](Regs& R, bool valid) {
     const __amdgpu_buffer_rsrc_t xs = valid ? xr : xr0;
@@ -448,8 +451,15 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
     }
   }
 
-  store_tile<BF16, NCHW_OUT, TP, TC>(a, sg, acc, wk.m0 + wp_i * WP, wk.n0 + wc_i * WC, lane,
-                                     s_bias - wk.n0);
+  if (a.ksplit > 1) {
+    GemmArgs ap = a;
+    ap.y = a.part + (size_t)wk.ks * a.part_stride;
+    store_tile<false, NCHW_OUT, TP, TC>(ap, sg, acc, wk.m0 + wp_i * WP, wk.n0 + wc_i * WC, lane,
+                                        s_bias - wk.n0);
+  } else {
+    store_tile<BF16, NCHW_OUT, TP, TC>(a, sg, acc, wk.m0 + wp_i * WP, wk.n0 + wc_i * WC, lane,
+                                       s_bias - wk.n0);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -546,9 +556,12 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm2_kernel(GemmArgs a) {
 
   const int ntaps = sg.tap_count;
   const int cblocks = a.cin_pad / KC;
-  const int cb_per = (cblocks + KS - 1) / KS;                 // channel blocks per K group
-  const int cb_lo = min(grp * cb_per, cblocks);
-  const int nsteps = ntaps * (min(cb_lo + cb_per, cblocks) - cb_lo);  // this group's stages
+  // this workgroup's K slice of channel blocks [cb_w0, cb_w1), split over
+  // its K groups
+  const int cb_w0 = wk.ks * cblocks / a.ksplit, cb_w1 = (wk.ks + 1) * cblocks / a.ksplit;
+  const int cb_per = (cb_w1 - cb_w0 + KS - 1) / KS;           // channel blocks per K group
+  const int cb_lo = min(cb_w0 + grp * cb_per, cb_w1);
+  const int nsteps = ntaps * (min(cb_lo + cb_per, cb_w1) - cb_lo);  // this group's stages
   const int nsteps_all = ntaps * cb_per;                      // the loop runs this many
   const int tail_c = a.cin - (cblocks - 1) * KC;
 
@@ -756,7 +769,13 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm2_kernel(GemmArgs a) {
   }
   const int pix0 = wk.m0 + (SHARE_A ? 0 : wave * RD);
   const int ch0 = wk.n0 + (SHARE_A ? wave * RD : 0);
-  store_tile<BF16, NCHW_OUT, TP, TC>(a, sg, acc, pix0, ch0, lane, s_bias - wk.n0);
+  if (a.ksplit > 1) {
+    GemmArgs ap = a;
+    ap.y = a.part + (size_t)wk.ks * a.part_stride;
+    store_tile<false, NCHW_OUT, TP, TC>(ap, sg, acc, pix0, ch0, lane, s_bias - wk.n0);
+  } else {
+    store_tile<BF16, NCHW_OUT, TP, TC>(a, sg, acc, pix0, ch0, lane, s_bias - wk.n0);
+  }
 }
 
 template <bool BF16, bool NCHW_OUT, int CFG>
@@ -1612,6 +1631,33 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
                     (size_t)(2 * qh0) * obw + 8 * k8;
     store_stream16(dst, v);
   }
+}
+
+// ---------------------------------------------------------------------------
+// Split-K reduction: the K slices' fp32 partial outputs added in slice order
+// (deterministic), then bias, activation and the output dtype.
+template <bool BF16>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(SplitKArgs a) {
+  for (uint32_t i = blockIdx.x * 256u + threadIdx.x; i < a.total; i += gridDim.x * 256u) {
+    float v = 0.f;
+    for (int s = 0; s < a.ksplit; ++s) v += a.part[(size_t)s * a.stride + i];
+    const uint32_t ch = a.nchw ? (i / (uint32_t)a.hw) % (uint32_t)a.cout : i % (uint32_t)a.cout;
+    if (a.bias) v += a.bias[ch / (uint32_t)a.bias_div];
+    v = activate(v, a.act);
+    if constexpr (BF16)
+      ((uint16_t*)a.y)[i] = f32_to_bf16_rne(v);
+    else
+      ((float*)a.y)[i] = v;
+  }
+}
+
+hipError_t launch_splitk_reduce(const SplitKArgs& a, int dtype, hipStream_t stream) {
+  const uint32_t blocks = std::min<uint32_t>((a.total + 255u) / 256u, 4096u);
+  if (dtype == 1)
+    hipLaunchKernelGGL(splitk_reduce_kernel<true>, dim3(blocks), dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(splitk_reduce_kernel<false>, dim3(blocks), dim3(256), 0, stream, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_quad(const QArgs& a, hipStream_t stream) {

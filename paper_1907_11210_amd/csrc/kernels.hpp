@@ -47,9 +47,10 @@ struct TapDev {
 };
 constexpr int kMaxLdsTaps = 64;  // taps per segment staged in LDS (more: scalar loads)
 
-// One workgroup's job: GEMM tile (m0, n0) of segment seg.
+// One workgroup's job: GEMM tile (m0, n0) of segment seg, over the input
+// channel blocks of K slice ks (of GemmArgs::ksplit).
 struct WorkDev {
-  int32_t seg, m0, n0, pad;
+  int32_t seg, m0, n0, ks;
 };
 
 struct GemmArgs {
@@ -68,6 +69,12 @@ struct GemmArgs {
   int32_t ho, wo;
   int32_t ks;  // kernel width s: weight slot of tap (kh, kw) = kh * ks + kw
   int32_t bias_div;
+  // K split across workgroups: ksplit > 1 writes each slice's fp32 partial
+  // tile (no bias, no activation) to part + slice * part_stride, in the
+  // output's layout; splitk_reduce then sums the slices in order
+  int32_t ksplit;
+  float* part;
+  uint32_t part_stride;
   int act;           // huge2_activation, applied after the bias
 };
 
@@ -250,6 +257,18 @@ struct QArgs {
   int act;           // huge2_activation, applied after the bias
 };
 hipError_t launch_quad(const QArgs& a, hipStream_t stream);
+
+// y[i] = act(bias[ch(i) / bias_div] + sum over s < ksplit, in order, of
+// part[s * stride + i]) in the dtype; ch(i) = (i / hw) % cout for NCHW, i %
+// cout for NHWC.
+struct SplitKArgs {
+  const float* part;
+  const float* bias;
+  void* y;
+  uint32_t stride, total;
+  int ksplit, cout, hw, nchw, bias_div, act;
+};
+hipError_t launch_splitk_reduce(const SplitKArgs& a, int dtype, hipStream_t stream);
 
 // Weight gradient (training, section 3.2.3).  With the "small" tensor S on
 // the tap's pixel grid and the "big" tensor B read at position

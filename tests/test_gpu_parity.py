@@ -448,3 +448,30 @@ def test_fused_activation(layer, act):
     P.check(P.run_gpu(layer, xq, wq, bias, one_shot=True), ref, absref, layer.dtype, layer.name)
     if act == "relu":
         assert np.all(P.run_gpu(layer, xq, wq, bias) >= 0)
+
+
+# phase-GEMM layers of every output layout and dtype, with ragged channels
+SPLITK_LAYERS = [l for l in SMALL if l.name in ("ct_vecstage_bf16", "ct_ragged_bf16_nhwc")] + [
+    L("sk_conv_nchw", False, 2, 200, 9, 7, 40, 3, 3, 2, 1, 0, 1, "NCHW", "bf16"),
+    L("sk_ct_nhwc_f32", True, 1, 150, 5, 6, 24, 3, 3, 2, 1, 1, 1, "NHWC", "f32"),
+    L("sk_dgrad_nchw", False, 2, 256, 8, 8, 64, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
+    L("sk_proj_nchw", True, 2, 300, 1, 1, 16, 4, 4, 1, 0, 0, 1, "NCHW", "bf16"),
+]
+
+
+@pytest.mark.parametrize("ksplit", [2, 3])
+@pytest.mark.parametrize("layer", SPLITK_LAYERS, ids=lambda l: l.name)
+def test_split_k(layer, ksplit, monkeypatch):
+    """K split across workgroups (fp32 partials added in order by a second
+    kernel, with bias and activation) matches the oracle and is bitwise
+    reproducible."""
+    monkeypatch.setenv("HUGE2_SPLITK", str(ksplit))
+    layer = layer.with_(act="relu")
+    P.say("case", layer, "HUGE2_SPLITK", ksplit)
+    xq, wq = _inputs(layer, seed=17)
+    bias = torch.linspace(-0.5, 0.5, layer.c_out)
+    ref = P.oracle_full(layer, xq, wq, bias)
+    absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
+    y1 = P.run_gpu(layer, xq, wq, bias)
+    P.check(y1, ref, absref, layer.dtype, layer.name)
+    assert np.array_equal(y1, P.run_gpu(layer, xq, wq, bias))

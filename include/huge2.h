@@ -109,6 +109,10 @@ huge2_status huge2_output_shape(const huge2_conv_desc* desc, int32_t transposed,
  *   transposed = 0: w is [c_out][c_in][r][s] (PyTorch Conv2d order).
  * w is read only by work enqueued on hip_stream: it may be freed or changed
  * once that work has completed.  *out receives the plan (NULL on error).
+ * A layer with fewer output tiles than compute units also gets a plan-owned
+ * fp32 workspace of up to 8 x |y| elements (at most 256 MiB) for its K
+ * slices; executes of one plan therefore share it: enqueue them on one
+ * stream (or order them).
  * Errors: INVALID_ARG (descriptor, null out/w), UNSUPPORTED, ALLOC, HIP. */
 huge2_status huge2_plan_create(huge2_plan** out, const huge2_conv_desc* desc, int32_t transposed,
                                const void* w, void* hip_stream);

@@ -49,6 +49,8 @@ struct huge2_plan {
   int bias_div;   // GEMM columns per bias entry (r * s for the 1x1-input product form)
   int ksplit;     // K slices across workgroups (1: none)
   void* part;     // their fp32 partial outputs, ksplit x |y| (or null)
+  huge2_plan* inner;  // two-pass all-taps form: the per-tap pointwise GEMM (or null)
+  void* zbuf;         // its output, the per-tap products (fp32 NCHW)
   char kernel_name[64];
 };
 
@@ -543,7 +545,7 @@ int plan_gemm_shape(const huge2_conv_desc& d, bool tr, PlanShape* shape) {
 
 
 void free_buffers(huge2_plan* p) {
-  void* bufs[4] = {p->wp, p->meta, p->xs, p->part};
+  void* bufs[5] = {p->wp, p->meta, p->xs, p->part, p->zbuf};
   for (void* b : bufs) {
     if (!b) continue;
     if (p->stream_ordered)
@@ -551,7 +553,12 @@ void free_buffers(huge2_plan* p) {
     else
       (void)hipFree(b);
   }
-  p->wp = p->meta = p->xs = p->part = nullptr;
+  p->wp = p->meta = p->xs = p->part = p->zbuf = nullptr;
+  if (p->inner) {
+    free_buffers(p->inner);
+    delete p->inner;
+    p->inner = nullptr;
+  }
 }
 
 huge2_status dev_alloc(huge2_plan* p, void** out, size_t bytes) {
@@ -631,6 +638,64 @@ huge2_status create_direct(huge2_plan** out, const huge2_conv_desc& d, int trans
   return HUGE2_OK;
 }
 
+// The two-pass all-taps form applies to fp32 NCHW transposed convs whose
+// taps x output channels fit one 64-wide tile (the fp32 counterpart of the
+// all-taps kernel): pass 1 is the pointwise GEMM of every input pixel with
+// all taps, z = x . w read as [c_in][c_out*r*s] (a 1x1 transposed conv, on
+// the phase GEMM), pass 2 gathers each output's taps from z.  The phase
+// GEMM would pad the few output channels to a 32-wide MFMA tile per phase.
+bool two_pass_shape(const huge2_conv_desc& d, bool transposed, huge2_conv_desc* d1) {
+  if (!transposed || d.dtype != HUGE2_F32 || d.layout != HUGE2_NCHW) return false;
+  if (env_int("HUGE2_TWOPASS", 1) == 0 || env_int("HUGE2_TILE", -1) >= 0) return false;
+  if ((long long)d.c_out * d.r * d.s > 64 || (d.r == 1 && d.s == 1)) return false;
+  *d1 = d;
+  d1->c_out = d.c_out * d.r * d.s;
+  d1->r = d1->s = 1;
+  d1->stride_h = d1->stride_w = 1;
+  d1->pad_h = d1->pad_w = 0;
+  d1->out_pad_h = d1->out_pad_w = 0;
+  d1->dil_h = d1->dil_w = 1;
+  d1->activation = HUGE2_ACT_NONE;
+  return (long long)d.n * d1->c_out * d.h * d.w < (1ll << 31);
+}
+
+huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int transposed,
+                         const void* w, hipStream_t stream, bool stream_ordered);
+
+huge2_status create_two_pass(huge2_plan** out, const huge2_conv_desc& d, const huge2_conv_desc& d1,
+                             const void* w, hipStream_t stream, bool stream_ordered) {
+  huge2_plan* inner = nullptr;
+  huge2_status st = create_impl(&inner, &d1, 1, w, stream, stream_ordered);
+  if (st != HUGE2_OK) return st;
+  huge2_plan* p = new (std::nothrow) huge2_plan();
+  if (!p) {
+    free_buffers(inner);
+    delete inner;
+    return HUGE2_ERR_ALLOC;
+  }
+  p->desc = d;
+  p->transposed = 1;
+  p->bias_div = 1;
+  p->ksplit = 1;
+  p->stream_ordered = stream_ordered;
+  p->alloc_stream = stream;
+  output_dims(d, true, &p->ho, &p->wo);
+  p->inner = inner;
+  p->staged = inner->staged;
+  p->issued_macs = inner->issued_macs;
+  PlanShape shape;
+  p->nonzero_macs = build_shape(d, true, 2, 128, &shape) ? shape.nonzero_macs : 0;
+  std::snprintf(p->kernel_name, sizeof(p->kernel_name), "two-pass: %.40s + taps_combine",
+                inner->kernel_name);
+  if ((st = dev_alloc(p, &p->zbuf, (size_t)d.n * d1.c_out * d.h * d.w * sizeof(float))) != HUGE2_OK) {
+    free_buffers(p);
+    delete p;
+    return st;
+  }
+  *out = p;
+  return HUGE2_OK;
+}
+
 huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int transposed,
                          const void* w, hipStream_t stream, bool stream_ordered) {
   if (!out) return HUGE2_ERR_INVALID_ARG;
@@ -658,6 +723,10 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     dd.layout = HUGE2_NHWC;
   }
   const huge2_conv_desc& d = dd;
+  {
+    huge2_conv_desc d1;
+    if (two_pass_shape(d, tr, &d1)) return create_two_pass(out, d, d1, w, stream, stream_ordered);
+  }
 
   {
     ZArgs z;
@@ -782,9 +851,15 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   // blocks into ksplit slices, one workgroup per (tile, slice), whose fp32
   // partials a second kernel adds in slice order (deterministic), with the
   // bias and activation.  The partials cost 2 x 4 x ksplit bytes per output.
+  // (HUGE2_SPLITK forces a count, up to the channel blocks.)
   {
     const int cblocks = p->cin_pad / bk;
-    int ks = std::min({cblocks, kComputeUnits / std::max(1, (int)works.size()), 8});
+    int max_taps = 1;
+    for (const SegDev& sd : segs) max_taps = std::max(max_taps, (int)sd.tap_count);
+    // at least 8 K stages per slice: shorter slices lose more to the second
+    // launch than they gain (measured on a 2-block, 1-tap GEMM)
+    int ks = std::min({cblocks, kComputeUnits / std::max(1, (int)works.size()), 8,
+                       std::max(1, cblocks * max_taps / 8)});
     const int forced = env_int("HUGE2_SPLITK", -1);
     if (forced >= 1) ks = std::min(forced, cblocks);
     const size_t ny = (size_t)d.n * d.c_out * p->ho * p->wo;
@@ -857,6 +932,7 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
 
 huge2_status stage_impl(const huge2_plan* p, const void* x, hipStream_t stream) {
   if (!p) return HUGE2_ERR_INVALID_ARG;
+  if (p->inner) return stage_impl(p->inner, x, stream);
   if (!p->staged) return HUGE2_OK;
   if (!x) return HUGE2_ERR_INVALID_ARG;
   const huge2_conv_desc& d = p->desc;
@@ -874,6 +950,34 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
   if (!p || !y || (!p->staged && !x) || x == y) return HUGE2_ERR_INVALID_ARG;
   const huge2_conv_desc& d = p->desc;
   if (fault("launch")) return HUGE2_ERR_HIP;
+  if (p->inner) {
+    huge2_status st = gemm_impl(p->inner, x, nullptr, p->zbuf, stream);
+    if (st != HUGE2_OK) return st;
+    CombArgs c;
+    c.z = (const float*)p->zbuf;
+    c.bias = bias;
+    c.y = (float*)y;
+    c.n = d.n;
+    c.h = d.h;
+    c.w = d.w;
+    c.cout = d.c_out;
+    c.r = d.r;
+    c.s = d.s;
+    c.stride_h = d.stride_h;
+    c.stride_w = d.stride_w;
+    c.pad_h = d.pad_h;
+    c.pad_w = d.pad_w;
+    c.dil_h = d.dil_h;
+    c.dil_w = d.dil_w;
+    c.ho = p->ho;
+    c.wo = p->wo;
+    c.act = d.activation;
+    if (launch_taps_combine(c, stream) != hipSuccess) {
+      (void)hipGetLastError();
+      return HUGE2_ERR_HIP;
+    }
+    return HUGE2_OK;
+  }
   if (p->ztile) {
     ZArgs z = p->zargs;
     z.x = x;
@@ -1265,6 +1369,14 @@ huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, in
     int64_t z_issued = 0;
     RpArgs rp;
     QArgs q;
+    huge2_conv_desc d1;
+    if (two_pass_shape(*desc, transposed != 0, &d1)) {
+      int64_t nz1 = 0;
+      PlanShape shape;
+      if (!build_shape(*desc, true, 2, 128, &shape)) return HUGE2_ERR_INVALID_ARG;
+      *nonzero_macs = shape.nonzero_macs;
+      return huge2_plan_macs(&d1, 1, &nz1, issued_macs);
+    }
     if (ztile_shape(*desc, transposed != 0, &z, &z_issued) ||
         rowphase_shape(*desc, transposed != 0, &rp, &z_issued) ||
         quad_shape(*desc, transposed != 0, &q, &z_issued)) {

@@ -1660,6 +1660,46 @@ hipError_t launch_splitk_reduce(const SplitKArgs& a, int dtype, hipStream_t stre
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Gather of the per-tap products into the transposed-conv output (section
+// 3.1's relation read from the output side: output o takes tap m iff
+// o + pad - m*dil is a multiple of the stride, reading input (o + pad -
+// m*dil) / stride).  One thread per output element, taps in a fixed order.
+__global__ __launch_bounds__(256) void taps_combine_kernel(CombArgs a) {
+  const uint32_t total = (uint32_t)a.n * a.cout * a.ho * a.wo;
+  for (uint32_t i = blockIdx.x * 256u + threadIdx.x; i < total; i += gridDim.x * 256u) {
+    const int ow = (int)(i % (uint32_t)a.wo);
+    uint32_t t = i / (uint32_t)a.wo;
+    const int oh = (int)(t % (uint32_t)a.ho);
+    t /= (uint32_t)a.ho;
+    const int k = (int)(t % (uint32_t)a.cout);
+    const int img = (int)(t / (uint32_t)a.cout);
+    float v = a.bias ? a.bias[k] : 0.f;
+    for (int m = 0; m < a.r; ++m) {
+      const int uh = oh + a.pad_h - m * a.dil_h;
+      if (uh < 0 || uh % a.stride_h != 0) continue;
+      const int ih = uh / a.stride_h;
+      if (ih >= a.h) continue;
+      for (int q = 0; q < a.s; ++q) {
+        const int uw = ow + a.pad_w - q * a.dil_w;
+        if (uw < 0 || uw % a.stride_w != 0) continue;
+        const int iw = uw / a.stride_w;
+        if (iw >= a.w) continue;
+        const size_t zc = ((size_t)img * a.cout + k) * a.r * a.s + (size_t)m * a.s + q;
+        v += a.z[(zc * a.h + ih) * a.w + iw];
+      }
+    }
+    a.y[i] = activate(v, a.act);
+  }
+}
+
+hipError_t launch_taps_combine(const CombArgs& a, hipStream_t stream) {
+  const uint32_t total = (uint32_t)a.n * a.cout * a.ho * a.wo;
+  const uint32_t blocks = std::min<uint32_t>((total + 255u) / 256u, 8192u);
+  hipLaunchKernelGGL(taps_combine_kernel, dim3(blocks), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_quad(const QArgs& a, hipStream_t stream) {
   const dim3 grid(a.ntiles * a.igroups * a.hblocks);
 #define HUGE2_QUAD_LAUNCH(KS_, WCH_, D_, NP_) \

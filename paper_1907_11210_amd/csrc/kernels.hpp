@@ -270,6 +270,20 @@ struct SplitKArgs {
 };
 hipError_t launch_splitk_reduce(const SplitKArgs& a, int dtype, hipStream_t stream);
 
+// Second pass of the two-pass all-taps form of a transposed conv: z holds,
+// per input pixel, every kernel tap's products, z[n][(k*r + m)*s + q][ih][iw]
+// = sum_c x[n][c][ih][iw] * w[c][k][m][q] (fp32, NCHW); the output gathers
+// y[n][k][oh][ow] = act(bias[k] + sum over the taps (m, q), in order, with
+// oh + pad_h - m*dil_h = ih*stride_h and ow + pad_w - q*dil_w = iw*stride_w
+// inside the input, of z[n][(k*r + m)*s + q][ih][iw]) (fp32, NCHW).
+struct CombArgs {
+  const float* z;
+  const float* bias;
+  float* y;
+  int n, h, w, cout, r, s, stride_h, stride_w, pad_h, pad_w, dil_h, dil_w, ho, wo, act;
+};
+hipError_t launch_taps_combine(const CombArgs& a, hipStream_t stream);
+
 // Weight gradient (training, section 3.2.3).  With the "small" tensor S on
 // the tap's pixel grid and the "big" tensor B read at position
 // q*stride - pad + k*dil of that grid (transposed conv: S = x, B = dy; strided

@@ -475,3 +475,33 @@ def test_split_k(layer, ksplit, monkeypatch):
     y1 = P.run_gpu(layer, xq, wq, bias)
     P.check(y1, ref, absref, layer.dtype, layer.name)
     assert np.array_equal(y1, P.run_gpu(layer, xq, wq, bias))
+
+
+TWO_PASS_LAYERS = [l for l in SMALL if l.name in ("ct_fewout_f32_op", "ct_fewout_wide")] + [
+    L("tp_rgb_f32", True, 2, 128, 8, 8, 3, 4, 4, 2, 1, 0, 1, "NCHW", "f32"),
+    L("tp_dil_f32", True, 1, 40, 6, 7, 4, 3, 3, 3, 2, 1, 2, "NCHW", "f32"),
+]
+
+
+@pytest.mark.parametrize("two_pass", [1, 0])
+@pytest.mark.parametrize("layer", TWO_PASS_LAYERS, ids=lambda l: l.name)
+def test_two_pass_forms(layer, two_pass, monkeypatch):
+    """fp32 transposed convs with few output channels: the two-pass form
+    (pointwise GEMM to per-tap maps, then the ordered gather) and the phase
+    GEMM it replaces both match the oracle, bias and activation included."""
+    monkeypatch.setenv("HUGE2_TWOPASS", str(two_pass))
+    layer = layer.with_(act="tanh")
+    P.say("case", layer, "HUGE2_TWOPASS", two_pass)
+    xq, wq = _inputs(layer, seed=19)
+    bias = torch.linspace(-0.5, 0.5, layer.c_out)
+    ref = P.oracle_full(layer, xq, wq, bias)
+    absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
+    y = P.run_gpu(layer, xq, wq, bias)
+    P.check(y, ref, absref, layer.dtype, layer.name)
+    assert np.array_equal(y, P.run_gpu(layer, xq, wq, bias))
+    P.check(P.run_gpu(layer, xq, wq, bias, one_shot=True), ref, absref, layer.dtype, layer.name)
+    plan = P.make_plan(layer, wq.contiguous().to(torch.device("cuda", 0)))
+    try:
+        assert plan.kernel.startswith("two-pass") == bool(two_pass), plan.kernel
+    finally:
+        plan.close()

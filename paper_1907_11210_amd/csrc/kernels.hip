@@ -953,9 +953,9 @@ __global__ __launch_bounds__(kZtileThreads) void ztile_kernel(ZArgs a) {
   for (int mi = 0; mi < MB_MAX; ++mi)
     src_off[mi] = min((wave + NW * mi) * 32 + (lane & 31), np - 1) * RB + (lane >> 5) * 64;
 
-  __syncthreads();  // tiles zeroed
   uint32_t P[MAXP][8];
-  load_items(0, P);
+  load_items(0, P);  // registers only: issued before the barrier
+  __syncthreads();  // tiles zeroed
   store_items(zsm, P);
   __syncthreads();
   const int npass = a.cin_pad / 64;
@@ -1479,13 +1479,16 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
       }
   };
 
-  __syncthreads();  // halo tiles zeroed
   char* const tiles = smem + grp * 2 * HALO_B;
   uint32_t P[MAXP][8];
   uint4 W[DEPTH][WCH][4];
+  // the first K block's loads go out before the barrier (they only fill
+  // registers), so their latency overlaps the LDS clear and the launch of
+  // the workgroup's other waves
   load_pieces(cb_lo, P);
 #pragma unroll
   for (int d = 0; d < DEPTH; ++d) load_w(W[d], d / 4 < cbn, cb_lo + min(d / 4, cbn - 1), d % 4);
+  __syncthreads();  // halo tiles zeroed
   store_pieces(tiles, P);
   __syncthreads();
   if (cbn > 1) load_pieces(cb_lo + 1, P);

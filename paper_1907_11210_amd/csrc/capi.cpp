@@ -638,6 +638,26 @@ huge2_status create_direct(huge2_plan** out, const huge2_conv_desc& d, int trans
   return HUGE2_OK;
 }
 
+// A transposed conv of a 1x1 NCHW input with no padding and unit dilation
+// is the plain product y[n][k*r*s + m*s + q] = sum_c x[n][c] w[c][k][m][q]
+// (section 3.1 with a single input pixel: every tap its own phase and
+// output pixel): one dense GEMM of n rows, on the same memory read as a
+// 1x1 conv to c_out*r*s channels (x [n][c_in], w [c_in][c_out*r*s], y
+// [n][c_out*r*s]).  Writes the descriptor the plan runs to *dd and returns
+// the GEMM columns per bias entry (r * s in the product form, else 1).
+int product_form(const huge2_conv_desc& d, bool transposed, huge2_conv_desc* dd) {
+  *dd = d;
+  if (!transposed || d.h != 1 || d.w != 1 || d.layout != HUGE2_NCHW || d.pad_h != 0 ||
+      d.pad_w != 0 || d.out_pad_h != 0 || d.out_pad_w != 0 || d.dil_h != 1 || d.dil_w != 1 ||
+      (d.r == 1 && d.s == 1) || (long long)d.c_out * d.r * d.s > INT32_MAX / 2)
+    return 1;
+  dd->c_out = d.c_out * d.r * d.s;
+  dd->r = dd->s = 1;
+  dd->stride_h = dd->stride_w = 1;
+  dd->layout = HUGE2_NHWC;
+  return d.r * d.s;
+}
+
 // The two-pass all-taps form applies to fp32 NCHW transposed convs whose
 // taps x output channels fit one 64-wide tile (the fp32 counterpart of the
 // all-taps kernel): pass 1 is the pointwise GEMM of every input pixel with
@@ -705,23 +725,9 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   if (st != HUGE2_OK) return st;
   if (!w) return HUGE2_ERR_INVALID_ARG;
   const bool tr = transposed != 0;
-  // A transposed conv of a 1x1 NCHW input with no padding and unit dilation
-  // is the plain product y[n][k*r*s + m*s + q] = sum_c x[n][c] w[c][k][m][q]
-  // (section 3.1 with a single input pixel: every tap its own phase and
-  // output pixel): one dense GEMM of n rows, on the same memory read as a
-  // 1x1 conv to c_out*r*s channels (x [n][c_in], w [c_in][c_out*r*s], y
-  // [n][c_out*r*s]).  Bias k then covers r*s consecutive GEMM columns.
-  huge2_conv_desc dd = *desc;
-  int bias_div = 1;
-  if (tr && dd.h == 1 && dd.w == 1 && dd.layout == HUGE2_NCHW && dd.pad_h == 0 && dd.pad_w == 0 &&
-      dd.out_pad_h == 0 && dd.out_pad_w == 0 && dd.dil_h == 1 && dd.dil_w == 1 &&
-      (dd.r > 1 || dd.s > 1) && (long long)dd.c_out * dd.r * dd.s <= INT32_MAX / 2) {
-    bias_div = dd.r * dd.s;
-    dd.c_out = dd.c_out * dd.r * dd.s;
-    dd.r = dd.s = 1;
-    dd.stride_h = dd.stride_w = 1;
-    dd.layout = HUGE2_NHWC;
-  }
+  // the 1x1-input product form: bias k then covers r*s consecutive columns
+  huge2_conv_desc dd;
+  const int bias_div = product_form(*desc, tr, &dd);
   const huge2_conv_desc& d = dd;
   {
     huge2_conv_desc d1;
@@ -1369,17 +1375,20 @@ huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, in
     int64_t z_issued = 0;
     RpArgs rp;
     QArgs q;
+    // the same form choices, in the same order, as plan creation
+    huge2_conv_desc dd;
+    product_form(*desc, transposed != 0, &dd);
     huge2_conv_desc d1;
-    if (two_pass_shape(*desc, transposed != 0, &d1)) {
+    if (two_pass_shape(dd, transposed != 0, &d1)) {
       int64_t nz1 = 0;
       PlanShape shape;
-      if (!build_shape(*desc, true, 2, 128, &shape)) return HUGE2_ERR_INVALID_ARG;
+      if (!build_shape(dd, true, 2, 128, &shape)) return HUGE2_ERR_INVALID_ARG;
       *nonzero_macs = shape.nonzero_macs;
       return huge2_plan_macs(&d1, 1, &nz1, issued_macs);
     }
-    if (ztile_shape(*desc, transposed != 0, &z, &z_issued) ||
-        rowphase_shape(*desc, transposed != 0, &rp, &z_issued) ||
-        quad_shape(*desc, transposed != 0, &q, &z_issued)) {
+    if (ztile_shape(dd, transposed != 0, &z, &z_issued) ||
+        rowphase_shape(dd, transposed != 0, &rp, &z_issued) ||
+        quad_shape(dd, transposed != 0, &q, &z_issued)) {
       PlanShape shape;
       if (!build_shape(*desc, true, 2, 128, &shape)) return HUGE2_ERR_INVALID_ARG;
       *nonzero_macs = shape.nonzero_macs;
@@ -1387,12 +1396,12 @@ huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, in
       return HUGE2_OK;
     }
     PlanShape shape;
-    const int cfg = plan_gemm_shape(*desc, transposed != 0, &shape);
+    const int cfg = plan_gemm_shape(dd, transposed != 0, &shape);
     if (cfg < 0) return HUGE2_ERR_INVALID_ARG;
     const int bm = tile_bm(cfg), bn = tile_bn(cfg);
-    const int bk = tile_kb(cfg) / elem_size(desc->dtype);
-    const int64_t cin_pad = round_up(desc->c_in, bk);
-    const int64_t ntn = round_up(desc->c_out, bn) / bn;
+    const int bk = tile_kb(cfg) / elem_size(dd.dtype);
+    const int64_t cin_pad = round_up(dd.c_in, bk);
+    const int64_t ntn = round_up(dd.c_out, bn) / bn;
     *nonzero_macs = shape.nonzero_macs;
     *issued_macs = shape.tile_taps * bm * bn * ntn * cin_pad;
     return HUGE2_OK;

@@ -194,3 +194,21 @@ def test_aspp_phase_views(dil, monkeypatch):
     nz2, issued = h2.huge2_plan_macs(d, 0)
     assert nz2 == nz
     assert nz <= issued <= 1.10 * nz  # only the ragged ends of M tiles are padding
+
+
+def test_mac_counts_of_the_special_forms():
+    """The 1x1-input product form and the fp32 two-pass form report the
+    same structural MACs as the definition, and issue at least as many."""
+    cases = [
+        # 1x1 input (the generator's projection): n * c_in * c_out * r * s
+        (h2.make_desc(64, 100, 1, 1, 1024, 4, 4, 1, 0, 0, 1, h2.HUGE2_NCHW, h2.HUGE2_BF16),
+         64 * 100 * 1024 * 16),
+        (h2.make_desc(3, 20, 1, 1, 8, 3, 5, 2, 0, 0, 1, h2.HUGE2_NCHW, h2.HUGE2_F32), 3 * 20 * 8 * 15),
+        # fp32 RGB layer (two-pass): every (input pixel, tap) pair lands
+        (h2.make_desc(2, 128, 8, 8, 3, 4, 4, 2, 1, 0, 1, h2.HUGE2_NCHW, h2.HUGE2_F32),
+         _brute_nonzero(1, 2, 128, 3, 8, 8, 4, 4, (2, 2), (1, 1), (1, 1), 16, 16)),
+    ]
+    for d, expect in cases:
+        nz, issued = h2.huge2_plan_macs(d, 1)
+        assert nz == expect
+        assert issued >= nz

@@ -49,7 +49,9 @@ struct huge2_plan {
   int bias_div;   // GEMM columns per bias entry (r * s for the 1x1-input product form)
   int ksplit;     // K slices across workgroups (1: none)
   void* part;     // their fp32 partial outputs, ksplit x |y| (or null)
-  huge2_plan* inner;  // two-pass all-taps form: the per-tap pointwise GEMM (or null)
+  huge2_plan* inner;  // two-pass all-taps form: the per-tap pointwise GEMM; gather form: the
+                      // pointwise GEMM over the gathered receptive fields (or null)
+  bool gather;        // gather form: staging = the receptive-field gather into inner->xs
   void* zbuf;         // its output, the per-tap products (fp32 NCHW)
   char kernel_name[64];
 };
@@ -682,6 +684,64 @@ bool two_pass_shape(const huge2_conv_desc& d, bool transposed, huge2_conv_desc* 
 huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int transposed,
                          const void* w, hipStream_t stream, bool stream_ordered);
 
+// The gather form applies to NCHW convs (dilated or strided) with few input
+// channels, c_in*r*s <= 64 and r*s > 1 (a discriminator's RGB input layer,
+// the last layer of a generator's backward pass): the phase GEMM would pad
+// each tap's few channels to a 64-channel K stage.  Instead each output
+// pixel's receptive field (c_in*r*s values, Algorithm 2's gather) is gathered
+// into one GEMM row, in the staged layout of a pointwise conv whose weights
+// are w read in place as [c_out][c_in*r*s].
+bool gather_shape(const huge2_conv_desc& d, bool transposed, huge2_conv_desc* d1) {
+  if (transposed || d.layout != HUGE2_NCHW) return false;
+  if (env_int("HUGE2_GATHER", 1) == 0 || env_int("HUGE2_TILE", -1) >= 0) return false;
+  if ((long long)d.c_in * d.r * d.s > 64 || (d.r == 1 && d.s == 1)) return false;
+  int ho, wo;
+  if (!output_dims(d, false, &ho, &wo)) return false;
+  *d1 = d;
+  d1->c_in = d.c_in * d.r * d.s;
+  d1->h = ho;
+  d1->w = wo;
+  d1->r = d1->s = 1;
+  d1->stride_h = d1->stride_w = 1;
+  d1->pad_h = d1->pad_w = 0;
+  d1->dil_h = d1->dil_w = 1;
+  return true;
+}
+
+huge2_status create_gather(huge2_plan** out, const huge2_conv_desc& d, const huge2_conv_desc& d1,
+                           const void* w, hipStream_t stream, bool stream_ordered) {
+  huge2_plan* inner = nullptr;
+  huge2_status st = create_impl(&inner, &d1, 0, w, stream, stream_ordered);
+  if (st != HUGE2_OK) return st;
+  if (!inner->staged || inner->inner) {  // the pointwise GEMM must read a staged input
+    free_buffers(inner);
+    delete inner;
+    return HUGE2_ERR_UNSUPPORTED;
+  }
+  huge2_plan* p = new (std::nothrow) huge2_plan();
+  if (!p) {
+    free_buffers(inner);
+    delete inner;
+    return HUGE2_ERR_ALLOC;
+  }
+  p->desc = d;
+  p->transposed = 0;
+  p->bias_div = 1;
+  p->ksplit = 1;
+  p->stream_ordered = stream_ordered;
+  p->alloc_stream = stream;
+  output_dims(d, false, &p->ho, &p->wo);
+  p->inner = inner;
+  p->gather = true;
+  p->staged = true;
+  p->issued_macs = inner->issued_macs;
+  PlanShape shape;
+  p->nonzero_macs = build_shape(d, false, 2, 128, &shape) ? shape.nonzero_macs : 0;
+  std::snprintf(p->kernel_name, sizeof(p->kernel_name), "gather_taps + %.48s", inner->kernel_name);
+  *out = p;
+  return HUGE2_OK;
+}
+
 huge2_status create_two_pass(huge2_plan** out, const huge2_conv_desc& d, const huge2_conv_desc& d1,
                              const void* w, hipStream_t stream, bool stream_ordered) {
   huge2_plan* inner = nullptr;
@@ -732,6 +792,7 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   {
     huge2_conv_desc d1;
     if (two_pass_shape(d, tr, &d1)) return create_two_pass(out, d, d1, w, stream, stream_ordered);
+    if (gather_shape(d, tr, &d1)) return create_gather(out, d, d1, w, stream, stream_ordered);
   }
 
   {
@@ -938,6 +999,34 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
 
 huge2_status stage_impl(const huge2_plan* p, const void* x, hipStream_t stream) {
   if (!p) return HUGE2_ERR_INVALID_ARG;
+  if (p->gather) {
+    if (!x) return HUGE2_ERR_INVALID_ARG;
+    if (fault("launch")) return HUGE2_ERR_HIP;
+    const huge2_conv_desc& d = p->desc;
+    GatherArgs g;
+    g.x = x;
+    g.xs = p->inner->xs;
+    g.n = d.n;
+    g.cin = d.c_in;
+    g.h = d.h;
+    g.w = d.w;
+    g.r = d.r;
+    g.s = d.s;
+    g.stride_h = d.stride_h;
+    g.stride_w = d.stride_w;
+    g.pad_h = d.pad_h;
+    g.pad_w = d.pad_w;
+    g.dil_h = d.dil_h;
+    g.dil_w = d.dil_w;
+    g.ho = p->ho;
+    g.wo = p->wo;
+    g.c_stride = p->inner->c_stride;
+    if (launch_gather_taps(g, d.dtype, stream) != hipSuccess) {
+      (void)hipGetLastError();
+      return HUGE2_ERR_HIP;
+    }
+    return HUGE2_OK;
+  }
   if (p->inner) return stage_impl(p->inner, x, stream);
   if (!p->staged) return HUGE2_OK;
   if (!x) return HUGE2_ERR_INVALID_ARG;
@@ -956,6 +1045,7 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
   if (!p || !y || (!p->staged && !x) || x == y) return HUGE2_ERR_INVALID_ARG;
   const huge2_conv_desc& d = p->desc;
   if (fault("launch")) return HUGE2_ERR_HIP;
+  if (p->gather) return gemm_impl(p->inner, x, bias, y, stream);
   if (p->inner) {
     huge2_status st = gemm_impl(p->inner, x, nullptr, p->zbuf, stream);
     if (st != HUGE2_OK) return st;
@@ -1379,12 +1469,12 @@ huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, in
     huge2_conv_desc dd;
     product_form(*desc, transposed != 0, &dd);
     huge2_conv_desc d1;
-    if (two_pass_shape(dd, transposed != 0, &d1)) {
+    if (two_pass_shape(dd, transposed != 0, &d1) || gather_shape(dd, transposed != 0, &d1)) {
       int64_t nz1 = 0;
       PlanShape shape;
-      if (!build_shape(dd, true, 2, 128, &shape)) return HUGE2_ERR_INVALID_ARG;
+      if (!build_shape(dd, transposed != 0, 2, 128, &shape)) return HUGE2_ERR_INVALID_ARG;
       *nonzero_macs = shape.nonzero_macs;
-      return huge2_plan_macs(&d1, 1, &nz1, issued_macs);
+      return huge2_plan_macs(&d1, transposed != 0 ? 1 : 0, &nz1, issued_macs);
     }
     if (ztile_shape(dd, transposed != 0, &z, &z_issued) ||
         rowphase_shape(dd, transposed != 0, &rp, &z_issued) ||

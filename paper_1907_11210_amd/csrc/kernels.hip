@@ -1703,6 +1703,51 @@ hipError_t launch_taps_combine(const CombArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Receptive-field gather for a conv with few input channels (Algorithm 2's
+// gather, stored per output pixel as one GEMM row).  One thread per element
+// of xs, so the stores are contiguous.
+template <typename T>
+__global__ __launch_bounds__(256) void gather_taps_kernel(GatherArgs a) {
+  // 16 bytes of one pixel's row per thread (c_stride is a multiple of VEC)
+  constexpr int VEC = 16 / (int)sizeof(T);
+  const int cv = a.c_stride / VEC;
+  const uint32_t total = (uint32_t)a.n * a.ho * a.wo * cv;
+  const int rs = a.r * a.s, kk = a.cin * rs;
+  for (uint32_t i = blockIdx.x * 256u + threadIdx.x; i < total; i += gridDim.x * 256u) {
+    const int j0 = (int)(i % (uint32_t)cv) * VEC;
+    const uint32_t pix = i / (uint32_t)cv;
+    const int ow = (int)(pix % (uint32_t)a.wo);
+    const uint32_t t = pix / (uint32_t)a.wo;
+    const int oh = (int)(t % (uint32_t)a.ho), img = (int)(t / (uint32_t)a.ho);
+    T v[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      const int j = j0 + e;
+      v[e] = T(0);
+      if (j < kk) {
+        const int c = j / rs, mq = j - c * rs, m = mq / a.s, q = mq - m * a.s;
+        const int ih = oh * a.stride_h - a.pad_h + m * a.dil_h;
+        const int iw = ow * a.stride_w - a.pad_w + q * a.dil_w;
+        if (ih >= 0 && ih < a.h && iw >= 0 && iw < a.w)
+          v[e] = ((const T*)a.x)[(((size_t)img * a.cin + c) * a.h + ih) * a.w + iw];
+      }
+    }
+    *(uint4*)((T*)a.xs + (size_t)pix * a.c_stride + j0) = *(const uint4*)v;
+  }
+}
+
+hipError_t launch_gather_taps(const GatherArgs& a, int dtype, hipStream_t stream) {
+  const int vec = dtype == 1 ? 8 : 4;
+  const uint32_t total = (uint32_t)a.n * a.ho * a.wo * (uint32_t)(a.c_stride / vec);
+  const uint32_t blocks = std::min<uint32_t>((total + 255u) / 256u, 8192u);
+  if (dtype == 1)
+    hipLaunchKernelGGL(gather_taps_kernel<uint16_t>, dim3(blocks), dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(gather_taps_kernel<uint32_t>, dim3(blocks), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_quad(const QArgs& a, hipStream_t stream) {
   const dim3 grid(a.ntiles * a.igroups * a.hblocks);
 #define HUGE2_QUAD_LAUNCH(KS_, WCH_, D_, NP_) \

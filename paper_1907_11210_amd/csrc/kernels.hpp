@@ -319,4 +319,16 @@ hipError_t launch_wgrad_store(const WgArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_stage_input(const void* x, void* xs, int dtype, bool nchw, int n, int cin,
                               int hw, int c_stride, hipStream_t stream);
 
+// Gather form of a conv with few input channels: every output pixel's
+// receptive field, xs[n][oh*wo + ow][(c*r + m)*s + q] = x[n][c][oh*stride_h -
+// pad_h + m*dil_h][ow*stride_w - pad_w + q*dil_w] (NCHW x; zero outside the
+// input and for j >= cin*r*s up to c_stride), in the channel-contiguous
+// layout the phase GEMM reads.
+struct GatherArgs {
+  const void* x;
+  void* xs;
+  int n, cin, h, w, r, s, stride_h, stride_w, pad_h, pad_w, dil_h, dil_w, ho, wo, c_stride;
+};
+hipError_t launch_gather_taps(const GatherArgs& a, int dtype, hipStream_t stream);
+
 }  // namespace huge2

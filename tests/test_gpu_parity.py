@@ -505,3 +505,35 @@ def test_two_pass_forms(layer, two_pass, monkeypatch):
         assert plan.kernel.startswith("two-pass") == bool(two_pass), plan.kernel
     finally:
         plan.close()
+
+
+GATHER_LAYERS = [
+    L("ga_rgb_s2", False, 2, 3, 16, 16, 40, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
+    L("ga_rgb_f32", False, 2, 3, 11, 9, 24, 3, 3, 1, 1, 0, 1, "NCHW", "f32"),
+    L("ga_dil", False, 1, 5, 13, 12, 16, 3, 3, 1, 2, 0, 2, "NCHW", "bf16"),
+    L("ga_valid_odd", False, 3, 7, 10, 14, 8, 3, 3, 2, 0, 0, 1, "NCHW", "bf16"),
+]
+
+
+@pytest.mark.parametrize("gather", [1, 0])
+@pytest.mark.parametrize("layer", GATHER_LAYERS, ids=lambda l: l.name)
+def test_gather_forms(layer, gather, monkeypatch):
+    """Convs with few input channels: the receptive-field gather into a
+    pointwise GEMM and the phase GEMM it replaces both match the oracle."""
+    monkeypatch.setenv("HUGE2_GATHER", str(gather))
+    layer = layer.with_(act="relu")
+    P.say("case", layer, "HUGE2_GATHER", gather)
+    xq, wq = _inputs(layer, seed=23)
+    bias = torch.linspace(-0.5, 0.5, layer.c_out)
+    ref = P.oracle_full(layer, xq, wq, bias)
+    absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
+    y = P.run_gpu(layer, xq, wq, bias)
+    P.check(y, ref, absref, layer.dtype, layer.name)
+    assert np.array_equal(y, P.run_gpu(layer, xq, wq, bias))
+    P.check(P.run_gpu(layer, xq, wq, bias, one_shot=True), ref, absref, layer.dtype, layer.name)
+    plan = P.make_plan(layer, wq.contiguous().to(torch.device("cuda", 0)))
+    try:
+        assert plan.kernel.startswith("gather_taps") == bool(gather), plan.kernel
+        assert plan.stages_input
+    finally:
+        plan.close()

@@ -471,7 +471,8 @@ bool quad_shape(const huge2_conv_desc& d, bool transposed, QArgs* q, int64_t* is
   q->ntiles = q->cout_pad / (32 * nch);
   const long long wgs = (long long)q->ntiles * igroups * hblocks;
   q->depth = env_int("HUGE2_QUAD_DEPTH", 2);
-  if ((q->depth != 2 && q->depth != 4 && q->depth != 8) || (nch == 2 && ks == 2) ||
+  // (eight stages spill the registers: measured 4x slower)
+  if ((q->depth != 2 && q->depth != 4) || (nch == 2 && ks == 2) ||
       np == 4)
     q->depth = 2;
   const long long wp_bytes = 16ll * q->cout_pad * d.c_in * 2;

@@ -1294,7 +1294,7 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
   constexpr int HALO_B = kQuadHaloRows * RB;
   constexpr int MAXP = kQuadMaxPieces;
   constexpr uint32_t OOB = 0x80000000u;
-  static_assert(DEPTH == 2 || DEPTH == 4 || DEPTH == 8, "weight stages in flight");
+  static_assert(DEPTH == 2 || DEPTH == 4, "weight stages in flight");
   static_assert(KS == 2 || WCH == 1, "one K group: two waves of 32 channels per phase");
   static_assert(NP == 2 || (NP == 4 && WCH == 1), "32-position blocks per wave");
   // pixel fragments double-buffered across taps where the registers allow
@@ -1760,12 +1760,10 @@ hipError_t launch_quad(const QArgs& a, hipStream_t stream) {
     HUGE2_QUAD_LAUNCH(2, 2, 2, 2);  // both channel blocks per wave: two stages fit the registers
   } else if (a.ks == 2) {
     if (a.depth == 2) HUGE2_QUAD_LAUNCH(2, 1, 2, 2);
-    else if (a.depth == 4) HUGE2_QUAD_LAUNCH(2, 1, 4, 2);
-    else HUGE2_QUAD_LAUNCH(2, 1, 8, 2);
+    else HUGE2_QUAD_LAUNCH(2, 1, 4, 2);
   } else {
     if (a.depth == 2) HUGE2_QUAD_LAUNCH(1, 1, 2, 2);
-    else if (a.depth == 4) HUGE2_QUAD_LAUNCH(1, 1, 4, 2);
-    else HUGE2_QUAD_LAUNCH(1, 1, 8, 2);
+    else HUGE2_QUAD_LAUNCH(1, 1, 4, 2);
   }
 #undef HUGE2_QUAD_LAUNCH
   return hipGetLastError();

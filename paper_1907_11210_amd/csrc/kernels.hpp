@@ -250,7 +250,7 @@ struct QArgs {
   // each | nch = 2, ks = 2: a K group each, both 32-channel blocks per wave)
   int nch, ks;
   int igroups, hblocks, ntiles;  // grid = ntiles x igroups x hblocks
-  int depth;         // weight stages in flight (2, 4 or 8)
+  int depth;         // weight stages in flight (2 or 4)
   // per phase (2 * rho_h + rho_w) and tap (2 * th + tw): weight slot kh*4+kw
   // and input offsets: output (2q_h + rho_h, 2q_w + rho_w) reads input q + (dh, dw)
   int8_t slot[4][4], dh[4][4], dw[4][4];

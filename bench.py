@@ -233,15 +233,17 @@ def _is_main(name):
     return any(k + "<" in name or k + "(" in name for k in MAIN_KERNELS)
 
 
-def _layer_dispatches(per_dispatch, nl):
+def _layer_dispatches(per_dispatch, nl, trailing):
     """Assign each layer's main-kernel dispatches (in launch order) to it.
     bench.py launches every layer in order once per step, then the dominant
-    layer's kernel alone, back to back: that trailing run (same kernel name
-    and grid) is left out, except for the dispatches that complete the last
-    step."""
+    layer's kernel alone, back to back (`trailing` = the --steps of the
+    profiled command): that trailing run (same kernel name and grid, at most
+    `trailing` long, since several layers may share a kernel instance) is left
+    out, except for the dispatches that complete the last step."""
     ids = sorted(d for d, (name, _) in per_dispatch.items() if _is_main(name))
     run = 1
-    while run < len(ids) and per_dispatch[ids[-run - 1]][0] == per_dispatch[ids[-1]][0]:
+    while (run < min(len(ids), trailing) and
+           per_dispatch[ids[-run - 1]][0] == per_dispatch[ids[-1]][0]):
         run += 1
     if nl > 1 and run > 1:
         keep = len(ids) - run
@@ -276,7 +278,7 @@ def summarize_profiles(d, workload):
     per = {int(r["Dispatch_Id"]): ("%s grid %sx%s" % (r["Kernel_Name"], r["Grid_Size_X"], r["Grid_Size_Y"]),
                                    int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
            for r in trace}
-    by_layer = _layer_dispatches(per, nl)
+    by_layer = _layer_dispatches(per, nl, 50)
     lines += ["", "## Main kernel per layer (dispatches in launch order, layer = k mod %d)" % nl,
               "", "| layer | dispatches | mean us | min us | kernel instance |", "|---|---|---|---|---|"]
     avg_us = {}
@@ -293,7 +295,7 @@ def summarize_profiles(d, workload):
     # benchmark's roofline.mean_launch_ms times
     ids_all = sorted(i for i, (name, _) in per.items() if _is_main(name))
     run = 1
-    while run < len(ids_all) and per[ids_all[-run - 1]][0] == per[ids_all[-1]][0]:
+    while run < min(len(ids_all), 50) and per[ids_all[-run - 1]][0] == per[ids_all[-1]][0]:
         run += 1
     tail = [per[i][1] for i in ids_all[-run:]][-50:] if ids_all else []
     if tail:
@@ -322,7 +324,7 @@ def summarize_profiles(d, workload):
                   "WRITE_SIZE x %.4f of its known size." % (COPY_MIB, f_fetch, f_write), "",
                   "| layer | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled traffic MB | algorithmic MB |",
                   "|---|---|---|---|---|"]
-        for l, fids, wids in zip(layers, _layer_dispatches(fe, nl), _layer_dispatches(wr, nl)):
+        for l, fids, wids in zip(layers, _layer_dispatches(fe, nl, 3), _layer_dispatches(wr, nl, 3)):
             fk = float(np.mean([fe[i][1] for i in fids]))
             wk = float(np.mean([wr[i][1] for i in wids]))
             tb = 1024.0 * (fk * f_fetch + wk * f_write)
@@ -343,7 +345,7 @@ def summarize_profiles(d, workload):
                   "benchmark's effective TFLOP/s." % (MFMA_FLOPS_PER_MOP_BF16, PEAK["bf16"]), "",
                   "| layer | counted MFMA GFLOP | issued (plan) GFLOP | structural GFLOP | "
                   "MFMA utilisation | structural / peak |", "|---|---|---|---|---|---|"]
-        for l, ids in zip(layers, _layer_dispatches(mops, nl)):
+        for l, ids in zip(layers, _layer_dispatches(mops, nl, 3)):
             if l.dtype != "bf16":
                 continue
             cf = MFMA_FLOPS_PER_MOP_BF16 * float(np.mean([mops[i][1] for i in ids]))

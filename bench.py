@@ -350,9 +350,11 @@ def summarize_profiles(d, workload):
                 continue
             cf = MFMA_FLOPS_PER_MOP_BF16 * float(np.mean([mops[i][1] for i in ids]))
             desc = h2.make_desc(l.n, l.c_in, l.h, l.w, l.c_out, l.r, l.s, l.stride, l.pad,
-                                l.out_pad, l.dil, h2.HUGE2_NCHW, h2.HUGE2_BF16)
+                                l.out_pad, l.dil,
+                                h2.HUGE2_NCHW if l.layout == "NCHW" else h2.HUGE2_NHWC,
+                                h2.HUGE2_BF16)
             nz = 2.0 * h2.huge2_plan_macs(desc, l.transposed)[0]
-            issued = 2.0 * h2.huge2_plan_macs(desc, l.transposed)[1] if l.layout == "NCHW" else float("nan")
+            issued = 2.0 * h2.huge2_plan_macs(desc, l.transposed)[1]
             t = avg_us[l.name] * 1e-6
             lines.append("| %s | %.2f | %.2f | %.2f | %.3f | %.3f |" % (
                 l.name, cf / 1e9, issued / 1e9, nz / 1e9, cf / t / (PEAK["bf16"] * 1e12),

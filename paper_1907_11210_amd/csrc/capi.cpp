@@ -93,8 +93,10 @@ long long count_works(const huge2_conv_desc& d, bool transposed, int class_split
 // (ASPP: twice the pixels per weight fetch of 64 x 256, which its L2 traffic
 // needs), else the 64 x 256 one with plenty of its tiles; otherwise the split-wave tiles with two K groups per workgroup,
 // 128 x 128 when that still gives every CU a tile, else 64 x 128 (few
-// pixels and long K: the first DCGAN layers).  Few output channels take the
-// narrow 128 x 32 tile.  fp32 keeps the two-operand-LDS tiles.
+// pixels and long K: the first DCGAN layers).  A pointwise GEMM of at most
+// 64 pixel rows and many channels (a generator's projection of z) takes the
+// 4-wave 32 x 256 tile: two row tiles, and no second K group idling on its
+// single K stage.  Few output channels take the narrow 128 x 32 tile.  fp32 keeps the two-operand-LDS tiles.
 int choose_cfg(const huge2_conv_desc& d, bool transposed, int class_split) {
   int forced = env_int("HUGE2_TILE", -1);
   if (forced >= 0 && forced < TILE_COUNT) return forced;
@@ -102,6 +104,8 @@ int choose_cfg(const huge2_conv_desc& d, bool transposed, int class_split) {
   const bool large = count_works(d, transposed, class_split, 8) >= 512;
   if (d.dtype != HUGE2_BF16) return large ? 8 : 2;
   if (large && d.c_out <= 128) return 8;                            // 128 x 128, 8 waves
+  if (d.r == 1 && d.s == 1 && (long long)d.n * d.h * d.w <= 64 && d.c_out >= 256)
+    return 24;  // 32 x 256: a pointwise GEMM of at most 64 rows (the 1x1-input product form)
   if (d.c_out >= 256 && count_works(d, transposed, class_split, 32) >= kComputeUnits) return 32;
   if (d.c_out >= 256 && count_works(d, transposed, class_split, 23) >= 384) return 23;
   if (count_works(d, transposed, class_split, 27) >= kComputeUnits) return 27;

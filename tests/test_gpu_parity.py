@@ -72,6 +72,9 @@ SMALL = [
     L("ct_1x1_proj", True, 3, 20, 1, 1, 24, 4, 4, 1, 0, 0, 1, "NCHW", "bf16"),
     L("ct_1x1_proj_f32", True, 2, 16, 1, 1, 8, 3, 5, 2, 0, 0, 1, "NCHW", "f32"),
     L("ct_1x1_nhwc", True, 2, 16, 1, 1, 8, 3, 3, 1, 0, 0, 1, "NHWC", "bf16"),
+    # the projection on the 32 x 256 tile: two row tiles (the second ragged), a
+    # ragged last channel tile (800 GEMM columns) and a K of 100 (ragged K block)
+    L("ct_1x1_proj_rag", True, 45, 100, 1, 1, 50, 4, 4, 1, 0, 0, 1, "NCHW", "bf16"),
 ]
 
 

@@ -83,7 +83,10 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    # about 30 ms of untimed steps: a cold MI355X needs some 20 ms of load
+    # before its clocks settle (the first 200 timed DCGAN steps after 10
+    # warmup steps averaged 93 us, every later 200 averaged 85.6 us)
+    ap.add_argument("--warmup", type=int, default=300)
     ap.add_argument("--workload", default="dcgan", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-library-reference", action="store_true",

@@ -36,6 +36,8 @@ Workloads (``name``: layers):
                the last, fused into the epilogues (batch normalisation, which a trained
                generator folds into weights and bias, is left out: no bias).  Weights
                N(0,0.02), chained.
+  dcgan_generator_b1
+               the same generator at batch 1 (one image: the latency case).
   dcgan_dgrad  training (section 3.2.3): the data gradients of the dcgan generator's
                four ConvTranspose layers, back to front.  The gradient of a stride-2
                transposed conv with respect to its input is the stride-2 conv of the
@@ -139,8 +141,10 @@ WORKLOADS = {
     "table1_cgan": table1_layers("cgan"),
     "dcgan_dgrad": dcgan_dgrad_layers("bf16"),
     "dcgan_generator": generator_layers("bf16"),
+    "dcgan_generator_b1": generator_layers("bf16", batch=1),
 }
-CHAINED = ("dcgan", "dcgan_f32", "table1_dcgan", "table1_cgan", "dcgan_dgrad", "dcgan_generator")
+CHAINED = ("dcgan", "dcgan_f32", "table1_dcgan", "table1_cgan", "dcgan_dgrad", "dcgan_generator",
+           "dcgan_generator_b1")
 
 
 def torch_dtype(name):
@@ -179,7 +183,7 @@ def generate(workload, seed=0, batch=None):
         out = [(layers[0], x1, ws[0])]
         out += [(l, None, w) for l, w in zip(layers[1:], ws[1:])]
         return out
-    if workload == "dcgan_generator":
+    if workload in ("dcgan_generator", "dcgan_generator_b1"):
         l0 = layers[0]
         z = _normal(g, (l0.n, 100, 1, 1))
         ws = [_normal(g, l.w_shape(), 0.02) for l in layers]

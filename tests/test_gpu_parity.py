@@ -180,11 +180,12 @@ def test_dcgan_chain_reduced_batch():
             x_prev = torch.from_numpy(ref).to(torch.float32)
 
 
-@pytest.mark.parametrize("wname", ["table1_dcgan", "table1_cgan"])
-def test_table1_layers_full(wname):
+@pytest.mark.parametrize("wname", ["table1_dcgan", "table1_cgan", "dcgan_generator_b1"])
+def test_batch1_workloads_full(wname):
     """The paper's own Table 1 deconvolution layers (5x5 DCGAN with unequal
-    phases, 4x4 cGAN), batch 1, checked in full; each layer gets the oracle's
-    output of the previous one."""
+    phases, 4x4 cGAN) and the whole generator with its fused activations, at
+    batch 1 (the plan path the benchmark times), checked in full; each layer
+    gets the oracle's output of the previous one."""
     items = wl.generate(wname, seed=0)
     x_prev = None
     for layer, x, w in items:

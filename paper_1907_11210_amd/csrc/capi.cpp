@@ -474,6 +474,12 @@ bool quad_shape(const huge2_conv_desc& d, bool transposed, QArgs* q, int64_t* is
   q->hblocks = hblocks;
   q->ntiles = q->cout_pad / (32 * nch);
   const long long wgs = (long long)q->ntiles * igroups * hblocks;
+  // Few workgroups over a long K: each runs its K blocks one after another,
+  // where the phase GEMM splits K across workgroups.  Measured on the batch-1
+  // DCGAN L1 (16 workgroups, 8 K blocks per group): 19.8 us here, 14.7 us on
+  // the phase GEMM with an 8-way K split; with 4 K blocks per group (batch-1
+  // L2) this kernel is still the faster (12.8 against 14.5 us).
+  if (wgs < kComputeUnits / 4 && d.c_in / (64 * ks) >= 8) return false;
   q->depth = env_int("HUGE2_QUAD_DEPTH", 2);
   // (eight stages spill the registers: measured 4x slower)
   if ((q->depth != 2 && q->depth != 4) || (nch == 2 && ks == 2) ||

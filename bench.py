@@ -7,13 +7,14 @@ synthetic input already resident in HBM (default: the DCGAN generator's four
 ConvTranspose layers, bf16 NCHW, batch 64, chained on the device; the z ->
 linear layer is input generation and is not timed).  Each layer is an
 input-staging launch where the layout needs one (NCHW, or channels not a
-multiple of the vector width) followed by one GEMM launch
-(huge2_plan_stage_input + huge2_plan_run_gemm, the two halves of
-huge2_plan_execute); the plans (weight packing) are built before the timed
-region.  Kernels are launched eagerly from the host (measured faster here
+multiple of the vector width) followed by one GEMM launch (and the split-K
+reduce where the plan has one), all from one huge2_plan_execute call; the
+plans (weight packing) are built before the timed region.  Kernels are launched eagerly from the host (measured faster here
 than replaying the step as one captured HIP graph, which --launch graph
 does after checking a replay bitwise against the eager step).  Per-layer
-times come from a separate eager pass with HIP events around each kernel.
+times come from a separate eager pass with HIP events around each kernel
+(huge2_plan_stage_input and huge2_plan_run_gemm, the two halves of
+huge2_plan_execute, called separately there).
 
 Prints ONE JSON line.  Fields beyond the standard ones:
   roofline      the dominant layer's main kernel (the layer with the most

@@ -943,6 +943,17 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     const size_t ny = (size_t)d.n * d.c_out * p->ho * p->wo;
     while (ks > 1 && (ks * ny * 4 > ((size_t)1 << 28) || ny >= ((size_t)1 << 31))) --ks;
     p->ksplit = std::max(1, ks);
+    // With four or more slices per tile, the two K groups inside a workgroup
+    // of the 64 x 128 tile only halve work that is already short: its
+    // one-group form (same tile, same work list and packing, three
+    // workgroups per compute unit) measured faster on the batch-1 5x5
+    // DCGAN layers (17.3 against 20.1 us, 16.1 against 18.9 us).
+    if (p->ksplit >= 4 && p->cfg == 25 && env_int("HUGE2_TILE", -1) < 0) {
+      p->cfg = 17;
+      const TileShape& t = kTiles[17];
+      std::snprintf(p->kernel_name, sizeof(p->kernel_name), "phase_gemm2_kernel %dx%d w%d k%d",
+                    t.bm, t.bn, t.pw * t.cw, t.ksplit);
+    }
     if (p->ksplit > 1) {
       const size_t nw = works.size();
       for (int k = 1; k < p->ksplit; ++k)

@@ -463,7 +463,7 @@ SPLITK_LAYERS = [l for l in SMALL if l.name in ("ct_vecstage_bf16", "ct_ragged_b
 ]
 
 
-@pytest.mark.parametrize("ksplit", [2, 3])
+@pytest.mark.parametrize("ksplit", [2, 3, 4])
 @pytest.mark.parametrize("layer", SPLITK_LAYERS, ids=lambda l: l.name)
 def test_split_k(layer, ksplit, monkeypatch):
     """K split across workgroups (fp32 partials added in order by a second

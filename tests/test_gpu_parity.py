@@ -199,6 +199,23 @@ def test_batch1_workloads_full(wname):
         x_prev = torch.from_numpy(ref).to(torch.float32)
 
 
+def test_batch1_form_choice():
+    """At batch 1 the long-K DCGAN L1 (16 all-phase workgroups over 1024
+    channels) runs on the phase GEMM with its K split across workgroups and
+    one K group per workgroup; L2 (512 channels) keeps the all-phase kernel;
+    at batch 64 L1 keeps it too."""
+    kinds = {}
+    for l in wl.WORKLOADS["dcgan_generator_b1"][1:3] + wl.WORKLOADS["dcgan"][:1]:
+        P.say("case", l)
+        w = wl.random_weight(l, seed=3).to(torch.bfloat16).cuda()
+        p = P.make_plan(l, w)
+        kinds[(l.name, l.n)] = p.kernel
+        p.close()
+    assert kinds[("gen_l1", 1)].startswith("phase_gemm2_kernel 64x128 w4 k1"), kinds
+    assert kinds[("gen_l2", 1)].startswith("quad_kernel"), kinds
+    assert kinds[("dcgan_l1", 64)].startswith("quad_kernel"), kinds
+
+
 REDUCED = [
     ("convt_small", {}),
     ("convt_odd", dict(n=1)),

@@ -3,13 +3,18 @@
 decomposed transposed / dilated convolution on one MI355X.
 
 One step = one pass of every layer of the workload over one batch of seeded
-synthetic input already resident in HBM (default: the DCGAN generator's four
-ConvTranspose layers, bf16 NCHW, batch 64, chained on the device; the z ->
-linear layer is input generation and is not timed).  Each layer is an
-input-staging launch where the layout needs one (NCHW, or channels not a
-multiple of the vector width) followed by one GEMM launch (and the split-K
-reduce where the plan has one), all from one huge2_plan_execute call; the
-plans (weight packing) are built before the timed region.  Kernels are launched eagerly from the host (measured faster here
+synthetic input already resident in HBM.  The default workload is the
+largest single-GPU one: the atrous spatial pyramid (four 3x3 dilated convs
+2048 -> 256 channels, dilations 6/12/18/24, bf16 NHWC, batch 8, 886.6 GFLOP
+of structural work per step).  The DCGAN generator's four ConvTranspose
+layers (bf16 NCHW, batch 64, chained on the device) are timed the same way
+in the same run and reported under "also".  Each layer is an input-staging
+launch where the layout needs one (NCHW, or channels not a multiple of the
+vector width) followed by one GEMM launch (and the split-K reduce where the
+plan has one), all from one huge2_plan_execute call; the plans (weight
+packing) are built before the timed region.  Before the warmup steps,
+untimed steps run for about --settle-ms of GPU time, so that the timed steps
+see settled clocks.  Kernels are launched eagerly from the host (measured faster here
 than replaying the step as one captured HIP graph, which --launch graph
 does after checking a replay bitwise against the eager step).  Per-layer
 times come from a separate eager pass with HIP events around each kernel
@@ -37,7 +42,7 @@ Prints ONE JSON line.  Fields beyond the standard ones:
                 the same way on random operands of the layer's dtype.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                       [--no-cpu-baseline]
+                       [--also NAMES|none] [--no-cpu-baseline]
 """
 import argparse
 import json
@@ -91,7 +96,14 @@ def parse():
     # before its clocks settle (the first 200 timed DCGAN steps after 10
     # warmup steps averaged 93 us, every later 200 averaged 85.6 us)
     ap.add_argument("--warmup", type=int, default=300)
-    ap.add_argument("--workload", default="dcgan", choices=sorted(DESCRIPTIONS))
+    # the largest single-GPU workload (886.6 GFLOP of structural work per step)
+    ap.add_argument("--workload", default="aspp", choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--also", default="dcgan",
+                    help="comma-separated further forward workloads timed the same way in the "
+                         "same run and reported under 'also' (empty: none)")
+    ap.add_argument("--settle-ms", type=float, default=100.0,
+                    help="untimed load (GPU milliseconds of steps) run before the warmup steps, "
+                         "so that the timed steps see settled clocks")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-library-reference", action="store_true",
                     help="skip the dense-GEMM library timing reported as context")
@@ -195,20 +207,20 @@ def copy_calibration(dev, mib=COPY_MIB, reps=10):
 # `cd /tmp && export TMPDIR=/tmp`.
 PROFILE_COMMANDS = [
     ("trace", "rocprofv3 --kernel-trace --stats -f csv -d $O -o trace -- "
-              "python3 $R/bench.py --workload {w} --no-cpu-baseline --no-library-reference"),
+              "python3 $R/bench.py --workload {w} --also none --no-cpu-baseline --no-library-reference"),
     ("fetch", "timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE -f csv -d $O -o fetch -- "
-              "python3 $R/bench.py --workload {w} --no-cpu-baseline --no-library-reference "
-              "--steps 3 --warmup 1"),
+              "python3 $R/bench.py --workload {w} --also none --no-cpu-baseline "
+              "--no-library-reference --steps 3 --warmup 1 --settle-ms 0"),
     ("write", "timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE -f csv -d $O -o write -- "
-              "python3 $R/bench.py --workload {w} --no-cpu-baseline --no-library-reference "
-              "--steps 3 --warmup 1"),
+              "python3 $R/bench.py --workload {w} --also none --no-cpu-baseline "
+              "--no-library-reference --steps 3 --warmup 1 --settle-ms 0"),
     ("copy_fetch", "timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE -f csv -d $O -o copy_fetch -- "
                    "python3 $R/bench.py --copy-calibration"),
     ("copy_write", "timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE -f csv -d $O -o copy_write -- "
                    "python3 $R/bench.py --copy-calibration"),
     ("mfma", "timeout -s KILL 120 rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_VALU_MFMA_BF16 "
-             "-f csv -d $O -o mfma -- python3 $R/bench.py --workload {w} --no-cpu-baseline "
-             "--no-library-reference --steps 3 --warmup 1"),
+             "-f csv -d $O -o mfma -- python3 $R/bench.py --workload {w} --also none "
+             "--no-cpu-baseline --no-library-reference --steps 3 --warmup 1 --settle-ms 0"),
 ]
 # one bf16 MFMA "MOP" is 512 flops (a 32x32x16 bf16 MFMA, 32768 flops, counts 64)
 MFMA_FLOPS_PER_MOP_BF16 = 512
@@ -582,40 +594,41 @@ def cpu_baseline(name, target_s):
     }
 
 
-def main():
-    args = parse()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU only: the kernels shard by batch, output channel or "
-              "phase without communication, and there is no multi-GPU path "
-              "(asked for --gpus %d, WORLD_SIZE %d)" % (args.gpus, world), file=sys.stderr)
-        sys.exit(2)
+def settle(step, ms):
+    """Run untimed steps until about `ms` milliseconds of GPU time have passed
+    (at least one step): a cold MI355X raises its clocks over the first tens
+    of milliseconds of load.  Returns the GPU time spent."""
+    import torch
+    if ms <= 0:
+        return 0.0
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    step()
+    e1.record()
+    torch.cuda.synchronize()
+    one = max(e0.elapsed_time(e1), 1e-3)
+    reps = int(min(10000, max(0, ms / one - 1)))
+    e0.record()
+    for _ in range(reps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    return one + (e0.elapsed_time(e1) if reps else 0.0)
 
-    if args.summarize_profiles:
-        summarize_profiles(args.summarize_profiles, args.workload)
-        return
 
+def bench_forward(name, args, dev):
+    """Time one forward workload: returns its JSON record and the dominant layer."""
     import numpy as np
     import torch
-    from paper_1907_11210_amd import huge2 as h2
 
-    if not os.path.exists(h2.LIB_PATH):
-        import __graft_entry__
-        __graft_entry__.build()
-    dev = torch.device("cuda", 0)
-    if args.copy_calibration:
-        copy_calibration(dev)
-        return
-    if args.workload in WGRAD_WORKLOADS:
-        print(json.dumps(run_wgrad(args, dev)), flush=True)
-        return
-    items, plans, step, step_outputs, step_input = build_workload(args.workload, dev)
+    items, plans, step, step_outputs, step_input = build_workload(name, dev)
     flops = layer_flops(plans)
     issued = [2 * p.macs()[1] for p in plans]
     total_flops = sum(flops)
     dtype = items[0][0].dtype
     esz = 2 if dtype == "bf16" else 4
 
+    settled_ms = settle(step, args.settle_ms)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -726,7 +739,8 @@ def main():
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
         per_launch = {"algorithmic_bytes_per_launch": algo_bytes[dom]}
-    roofline["traffic"] = measured_traffic(args.workload, items[dom][0].name)
+    dom_layer = items[dom][0]
+    roofline["traffic"] = measured_traffic(name, items[dom][0].name)
     roofline.update({"kernel": "%s (%s)" % (plans[dom].kernel, items[dom][0].name),
                      "mean_launch_ms": round(dom_ms, 5),
                      "arithmetic_intensity_flop_per_byte": round(intensity, 1)})
@@ -744,18 +758,62 @@ def main():
         "vs_baseline": None,
         "dtype": dtype,
         "data": "synthetic (seeded; random-init weights of the workload's shapes)",
-        "config": {"workload": args.workload, "description": DESCRIPTIONS[args.workload],
+        "config": {"workload": name, "description": DESCRIPTIONS[name],
                    "batch": items[0][0].n, "layout": items[0][0].layout,
                    "launch": "one HIP graph per step" if graph is not None else "eager launches"},
         "roofline": roofline,
         "layers": layers,
         "kernel_source_sha": kernel_source_sha(),
         "wall_s_timed": round(wall, 3),
+        "settle_ms": round(settled_ms, 1),
     }
     for p in plans:
         p.close()
+    del plans, step, items
+    torch.cuda.synchronize()
+    return out, dom_layer
+
+
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the kernels shard by batch, output channel or "
+              "phase without communication, and there is no multi-GPU path "
+              "(asked for --gpus %d, WORLD_SIZE %d)" % (args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+
+    if args.summarize_profiles:
+        summarize_profiles(args.summarize_profiles, args.workload)
+        return
+
+    import numpy as np
+    import torch
+    from paper_1907_11210_amd import huge2 as h2
+
+    if not os.path.exists(h2.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    dev = torch.device("cuda", 0)
+    if args.copy_calibration:
+        copy_calibration(dev)
+        return
+    if args.workload in WGRAD_WORKLOADS:
+        print(json.dumps(run_wgrad(args, dev)), flush=True)
+        return
+    out, dom_layer = bench_forward(args.workload, args, dev)
     if not args.no_library_reference:
-        out["library_reference"] = library_reference(items[dom][0], args.steps, dev)
+        out["library_reference"] = library_reference(dom_layer, args.steps, dev)
+    also = [w for w in args.also.split(",") if w and w not in ("none", args.workload)]
+    if also:
+        out["also"] = {}
+    for w in also:
+        o, _ = bench_forward(w, args, dev)
+        torch.cuda.empty_cache()
+        out["also"][w] = {k: o[k] for k in ("value", "unit", "ms_per_step", "dtype", "config",
+                                             "roofline", "layers")}
     if not args.no_cpu_baseline:
         cb = cpu_baseline(args.workload, args.cpu_seconds)
         cb["speedup_gpu_over_oracle"] = round(out["value"] / cb["value"], 1)

@@ -27,18 +27,20 @@ COMMON_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I", os.path.join(ROOT, 
 
 
 def build(verbose: bool = False) -> str:
-    objs = []
     build_dir = os.path.join(PKG, "_build")
     os.makedirs(build_dir, exist_ok=True)
-    for src in SOURCES:
+    procs, objs = [], []
+    for src in SOURCES:  # the translation units compile in parallel
         path = os.path.join(CSRC, src)
         obj = os.path.join(build_dir, src + ".o")
-        lang = ["-x", "hip"]
-        cmd = [HIPCC] + COMMON_FLAGS + DEVICE_FLAGS + lang + ["-c", path, "-o", obj]
+        cmd = [HIPCC] + COMMON_FLAGS + DEVICE_FLAGS + ["-x", "hip", "-c", path, "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
-        subprocess.run(cmd, check=True)
+        procs.append((cmd, subprocess.Popen(cmd)))
         objs.append(obj)
+    failed = [cmd for cmd, p in procs if p.wait() != 0]
+    if failed:
+        raise subprocess.CalledProcessError(1, failed[0])
     tmp = LIB + ".tmp%d" % os.getpid()
     cmd = [HIPCC, "-shared", "-fPIC"] + DEVICE_FLAGS + objs + ["-o", tmp]
     if verbose:

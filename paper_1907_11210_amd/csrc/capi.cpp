@@ -100,16 +100,19 @@ long long count_works(const huge2_conv_desc& d, bool transposed, int class_split
 int choose_cfg(const huge2_conv_desc& d, bool transposed, int class_split) {
   int forced = env_int("HUGE2_TILE", -1);
   if (forced >= 0 && forced < TILE_COUNT) return forced;
-  if (d.c_out <= 32) return 10;                                     // 128 x 32, KB 64
-  const bool large = count_works(d, transposed, class_split, 8) >= 512;
-  if (d.dtype != HUGE2_BF16) return large ? 8 : 2;
-  if (large && d.c_out <= 128) return 8;                            // 128 x 128, 8 waves
+  if (d.c_out <= 32) return TILE_128x32;
+  const bool large = count_works(d, transposed, class_split, TILE_128x128) >= 512;
+  if (d.dtype != HUGE2_BF16) return large ? TILE_128x128 : TILE_64x128;
+  if (large && d.c_out <= 128) return TILE_128x128;
   if (d.r == 1 && d.s == 1 && (long long)d.n * d.h * d.w <= 64 && d.c_out >= 256)
-    return 24;  // 32 x 256: a pointwise GEMM of at most 64 rows (the 1x1-input product form)
-  if (d.c_out >= 256 && count_works(d, transposed, class_split, 32) >= kComputeUnits) return 32;
-  if (d.c_out >= 256 && count_works(d, transposed, class_split, 23) >= 384) return 23;
-  if (count_works(d, transposed, class_split, 27) >= kComputeUnits) return 27;
-  return 25;                                                        // 64 x 128, 2 K groups
+    return TILE_SW_32x256;  // a pointwise GEMM of at most 64 rows (the 1x1-input product form)
+  if (d.c_out >= 256 && count_works(d, transposed, class_split, TILE_SW_128x256) >= kComputeUnits)
+    return TILE_SW_128x256;
+  if (d.c_out >= 256 && count_works(d, transposed, class_split, TILE_SW_64x256) >= 384)
+    return TILE_SW_64x256;
+  if (count_works(d, transposed, class_split, TILE_SW_128x128_K2) >= kComputeUnits)
+    return TILE_SW_128x128_K2;
+  return TILE_SW_64x128_K2;
 }
 
 // Order the work list for the eight XCDs.  The kernel hands work index
@@ -948,9 +951,9 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     // one-group form (same tile, same work list and packing, three
     // workgroups per compute unit) measured faster on the batch-1 5x5
     // DCGAN layers (17.3 against 20.1 us, 16.1 against 18.9 us).
-    if (p->ksplit >= 4 && p->cfg == 25 && env_int("HUGE2_TILE", -1) < 0) {
-      p->cfg = 17;
-      const TileShape& t = kTiles[17];
+    if (p->ksplit >= 4 && p->cfg == TILE_SW_64x128_K2 && env_int("HUGE2_TILE", -1) < 0) {
+      p->cfg = TILE_SW_64x128;
+      const TileShape& t = kTiles[TILE_SW_64x128];
       std::snprintf(p->kernel_name, sizeof(p->kernel_name), "phase_gemm2_kernel %dx%d w%d k%d",
                     t.bm, t.bn, t.pw * t.cw, t.ksplit);
     }
@@ -1005,7 +1008,7 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     ok = hipMemcpyAsync(p->meta, host.data(), meta_b, hipMemcpyHostToDevice, stream) == hipSuccess;
   if (ok)
     ok = launch_pack_weights(w, p->wp, d.dtype, tr, d.c_in, d.c_out, d.r, d.s, p->cin_pad,
-                             p->cout_pad, kTiles[cfg].kind == 1 ? tile_kb(cfg) : 0,
+                             p->cout_pad, kTiles[p->cfg].kind == 1 ? tile_kb(p->cfg) : 0,
                              stream) == hipSuccess;
   // the host copy of the metadata must outlive the transfer
   if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;

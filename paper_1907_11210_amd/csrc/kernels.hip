@@ -425,11 +425,11 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
       __syncthreads();
       for (int s = 0; s < nsteps2; s += 2) {
         load_step(r1, s + 2 < nsteps);
-        compute(0);
+        compute(0);  // s < nsteps always
         store_stage(1, r0);
         __syncthreads();
         load_step(r0, s + 3 < nsteps);
-        compute(1);
+        if (s + 1 < nsteps) compute(1);  // the padding step of an odd count has no MFMAs
         store_stage(0, r1);
         __syncthreads();
       }
@@ -444,7 +444,7 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
         store_stage(1, r0);
         __syncthreads();
         load_step(r0, s + 2 < nsteps);
-        compute(1);
+        if (s + 1 < nsteps) compute(1);
         store_stage(0, r0);
         __syncthreads();
       }
@@ -739,7 +739,8 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm2_kernel(GemmArgs a) {
     for (int s = 0; s < nsteps_u; s += U) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        compute(u & 1, rb[u % DEPTH]);
+        // the steps that round the loop up to U hold zeros: no MFMAs for them
+        if (s + u < nsteps) compute(u & 1, rb[u % DEPTH]);
         store_shared((u + 1) & 1, rb[(u + 1) % DEPTH]);
         load_step(rb[u % DEPTH], s + u + DEPTH < nsteps);
         __syncthreads();

@@ -89,50 +89,43 @@ struct GemmArgs {
 // kind 0: both operands through LDS, PW x CW waves of (BM/PW) x (BN/CW).
 // kind 1: split-wave form, the pixel tile through LDS, CW waves each loading
 //         BN/CW weight rows itself (PW = 1) from lane-ordered packed weights.
-// kind 2: split-wave form, the weight tile through LDS, PW waves each loading
-//         BM/PW pixel rows itself (CW = 1).
 // ksplit (split-wave kinds): K groups of PW x CW waves per workgroup, each
 // over its own share of the input-channel blocks, summed in LDS at the end.
 struct TileShape {
   int bm, bn, pw, cw, kb, depth, wg_per_cu, kind, ksplit = 1;
 };
-constexpr TileShape kTiles[] = {
-    {128, 128, 2, 2, 128, 2, 2, 0},  // 0
-    {256, 32, 4, 1, 128, 2, 1, 0},   // 1  narrow: few output channels
-    {64, 128, 1, 4, 128, 2, 2, 0},   // 2
-    {256, 128, 2, 2, 128, 2, 1, 0},  // 3
-    {128, 256, 2, 2, 128, 2, 1, 0},  // 4
-    {256, 256, 2, 4, 128, 2, 1, 0},  // 5  8 waves
-    {256, 128, 4, 2, 128, 2, 1, 0},  // 6  8 waves
-    {128, 256, 2, 4, 128, 2, 1, 0},  // 7  8 waves
-    {128, 128, 4, 2, 128, 2, 2, 0},  // 8  8 waves
-    {256, 256, 2, 2, 128, 1, 1, 0},  // 9  4 waves of 128 x 128
-    {128, 32, 4, 1, 64, 2, 6, 0},    // 10 narrow, small LDS footprint
-    {256, 32, 4, 1, 64, 2, 3, 0},    // 11 narrow, small LDS footprint
-    {64, 128, 1, 4, 64, 2, 5, 0},    // 12 small LDS footprint
-    {128, 128, 2, 2, 64, 2, 3, 0},   // 13 small LDS footprint
-    {256, 128, 2, 2, 128, 1, 1, 0},  // 14 4 waves of 128 x 64, one buffer
-    {128, 256, 2, 2, 128, 1, 1, 0},  // 15 4 waves of 64 x 128, one buffer
-    {256, 128, 4, 1, 128, 3, 1, 2},  // 16 split-wave: 4 waves of 64 pixels x 128
-    {64, 128, 1, 4, 128, 4, 3, 1},   // 17 split-wave: 4 waves of 64 x 32 channels
-    {128, 128, 4, 1, 128, 3, 2, 2},  // 18 split-wave: 4 waves of 32 pixels x 128
-    {128, 128, 1, 4, 128, 3, 2, 1},  // 19 split-wave: 4 waves of 128 x 32 channels
-    {256, 64, 4, 1, 128, 3, 2, 2},   // 20 split-wave: 4 waves of 64 pixels x 64
-    {256, 128, 8, 1, 128, 2, 2, 2},  // 21 split-wave: 8 waves of 32 pixels x 128
-    {128, 256, 1, 4, 128, 3, 1, 1},  // 22 split-wave: 4 waves of 128 x 64 channels
-    {64, 256, 1, 4, 128, 3, 2, 1},   // 23 split-wave: 4 waves of 64 x 64 channels
-    {32, 256, 1, 4, 128, 4, 2, 1},   // 24 split-wave: 4 waves of 32 x 64 channels
-    {64, 128, 1, 4, 128, 4, 1, 1, 2},   // 25 as 17, two K groups (8 waves)
-    {64, 256, 1, 4, 128, 3, 1, 1, 2},   // 26 as 23, two K groups
-    {128, 128, 1, 4, 128, 3, 1, 1, 2},  // 27 as 19, two K groups
-    {64, 128, 1, 4, 256, 3, 1, 1, 2},   // 28 as 25 with 256-byte K stages
-    {128, 128, 1, 4, 256, 2, 1, 1, 2},  // 29 as 27 with 256-byte K stages
-    {64, 256, 1, 4, 256, 2, 2, 1, 1},   // 30 as 23 with 256-byte K stages
-    {128, 128, 4, 2, 256, 2, 1, 0},     // 31 as 8 with 256-byte K stages
-    {128, 256, 1, 8, 128, 3, 1, 1, 1},  // 32 split-wave: 8 waves of 128 x 32 channels
-    {128, 256, 1, 8, 128, 2, 2, 1, 1},  // 33 as 32, two stages in flight
-    {128, 128, 1, 4, 128, 4, 1, 1, 2},  // 34 as 27, four stages in flight
+// Every configuration here is one that the planner picks for some shape
+// (choose_cfg and the split-K rewrite in capi.cpp).
+enum TileCfg {
+  TILE_128x128 = 0,      // two-operand LDS, 8 waves
+  TILE_64x128 = 1,       // two-operand LDS, 4 waves
+  TILE_128x32 = 2,       // narrow: few output channels, small LDS footprint
+  TILE_SW_64x128 = 3,    // split-wave: 4 waves of 64 x 32 channels
+  TILE_SW_64x256 = 4,    // split-wave: 4 waves of 64 x 64 channels
+  TILE_SW_32x256 = 5,    // split-wave: 4 waves of 32 x 64 channels
+  TILE_SW_64x128_K2 = 6,   // as TILE_SW_64x128, two K groups (8 waves)
+  TILE_SW_128x128_K2 = 7,  // split-wave: 4 waves of 128 x 32 channels, two K groups
+  TILE_SW_128x256 = 8,   // split-wave: 8 waves of 128 x 32 channels
 };
+constexpr TileShape kTiles[] = {
+    {128, 128, 4, 2, 128, 2, 2, 0},     // TILE_128x128
+    {64, 128, 1, 4, 128, 2, 2, 0},      // TILE_64x128
+    {128, 32, 4, 1, 64, 2, 6, 0},       // TILE_128x32
+    {64, 128, 1, 4, 128, 4, 3, 1},      // TILE_SW_64x128
+    {64, 256, 1, 4, 128, 3, 2, 1},      // TILE_SW_64x256
+    {32, 256, 1, 4, 128, 4, 2, 1},      // TILE_SW_32x256
+    {64, 128, 1, 4, 128, 4, 1, 1, 2},   // TILE_SW_64x128_K2
+    {128, 128, 1, 4, 128, 3, 1, 1, 2},  // TILE_SW_128x128_K2
+    {128, 256, 1, 8, 128, 3, 1, 1, 1},  // TILE_SW_128x256
+};
+// A split-K plan may switch from the two-K-group 64 x 128 tile to its
+// one-group form after the work list and the weight packing were laid out for
+// the first: both must share the tile, the K block and the packed layout.
+static_assert(kTiles[TILE_SW_64x128].bm == kTiles[TILE_SW_64x128_K2].bm &&
+                  kTiles[TILE_SW_64x128].bn == kTiles[TILE_SW_64x128_K2].bn &&
+                  kTiles[TILE_SW_64x128].kb == kTiles[TILE_SW_64x128_K2].kb &&
+                  kTiles[TILE_SW_64x128].kind == kTiles[TILE_SW_64x128_K2].kind,
+              "the split-K tile switch keeps the work list and the packing");
 constexpr int kComputeUnits = 256;  // MI355X
 constexpr int TILE_COUNT = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 inline int tile_bm(int cfg) { return kTiles[cfg].bm; }

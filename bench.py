@@ -142,10 +142,16 @@ def build_workload(name, dev):
     chained = name in wl.CHAINED
     outs = [torch.empty(p.out_shape, dtype=wl.torch_dtype(l.dtype), device=dev)
             for p, (l, _, _) in zip(plans, items)]
+    # layers of one input (the pyramid's branches) run as one grouped launch
+    group = h2.Group(plans) if name in wl.GROUPED else None
 
     def step(events=None):
         # events[3*i]: before the layer's input staging, events[3*i+1]: before its
-        # GEMM kernel, events[3*i+2]: after it (all on the launch stream)
+        # GEMM kernel, events[3*i+2]: after it (all on the launch stream).  The
+        # per-layer pass (events given) runs a grouped workload layer by layer.
+        if group is not None and events is None:
+            group(inputs[0], outs=outs)
+            return
         for i, p in enumerate(plans):
             x = inputs[i] if (not chained or i == 0) else outs[i - 1]
             if events is None:
@@ -160,7 +166,7 @@ def build_workload(name, dev):
     def step_input(i):
         return inputs[i] if (not chained or i == 0) else outs[i - 1]
 
-    return items, plans, step, lambda: outs, step_input
+    return items, plans, step, lambda: outs, step_input, group
 
 
 def kernel_source_sha():
@@ -274,12 +280,28 @@ def _layer_dispatches(per_dispatch, nl, trailing):
     return by_layer
 
 
+def _split_group(per):
+    """Separate the grouped launches (the main-kernel dispatches with the
+    largest grid) from the per-layer ones: returns (the rest, [(name, value)]
+    of the grouped launches in dispatch order)."""
+    def grid(name):
+        return int(name[name.rfind(" grid ") + 6:].split("x")[0])
+    mains = [i for i, (name, _) in per.items() if _is_main(name)]
+    if not mains:
+        return per, []
+    top = max(grid(per[i][0]) for i in mains)
+    gids = sorted(i for i in mains if grid(per[i][0]) == top)
+    rest = {i: v for i, v in per.items() if i not in set(gids)}
+    return rest, [per[i] for i in gids]
+
+
 def summarize_profiles(d, workload):
     import numpy as np
     from paper_1907_11210_amd import workloads as wl
 
     layers = wl.WORKLOADS[workload]
     nl = len(layers)
+    grouped = workload in wl.GROUPED
     cmds = ["cd /tmp && export TMPDIR=/tmp"] + [c.format(w=workload) for _, c in PROFILE_COMMANDS]
     lines = ["# Main kernel of each layer (phase GEMM or all-taps form) on workload `%s`: "
              "rocprofv3 kernel trace" % workload, "",
@@ -297,6 +319,18 @@ def summarize_profiles(d, workload):
     per = {int(r["Dispatch_Id"]): ("%s grid %sx%s" % (r["Kernel_Name"], r["Grid_Size_X"], r["Grid_Size_Y"]),
                                    int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
            for r in trace}
+    group_ids = []
+    if grouped:
+        # the grouped launches (every layer's works: the largest grid) run the
+        # steps; the layers' own launches come from the per-layer pass
+        per, group_ids = _split_group(per)
+        gt = np.array([per_group[1] for per_group in group_ids]) / 1e3
+        lines += ["", "## Grouped launch of the %d layers (one kernel per step)" % nl, "",
+                  "| launches | mean us | min us | kernel instance |", "|---|---|---|---|",
+                  "| %d | %.2f | %.2f | %s |" % (len(gt), gt.mean(), gt.min(),
+                                               group_ids[0][0].split("(")[0].split("::")[-1] +
+                                               group_ids[0][0][group_ids[0][0].rfind(" grid "):])]
+        avg_group_us = float(gt.mean())
     by_layer = _layer_dispatches(per, nl, 50)
     lines += ["", "## Main kernel per layer (dispatches in launch order, layer = k mod %d)" % nl,
               "", "| layer | dispatches | mean us | min us | kernel instance |", "|---|---|---|---|---|"]
@@ -343,6 +377,21 @@ def summarize_profiles(d, workload):
                   "WRITE_SIZE x %.4f of its known size." % (COPY_MIB, f_fetch, f_write), "",
                   "| layer | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled traffic MB | algorithmic MB |",
                   "|---|---|---|---|---|"]
+        if grouped:
+            fe, gfe = _split_group(fe)
+            wr, gwr = _split_group(wr)
+            fk = float(np.mean([v for _, v in gfe]))
+            wk = float(np.mean([v for _, v in gwr]))
+            tb = 1024.0 * (fk * f_fetch + wk * f_write)
+            l0 = layers[0]
+            esz = 2 if l0.dtype == "bf16" else 4
+            algo = esz * l0.n * l0.c_in * l0.h * l0.w
+            for l in layers:
+                ho, wo = l.out_hw()
+                algo += esz * (l.c_in * l.c_out * l.r * l.s + l.n * l.c_out * ho * wo)
+            traffic["layers"]["group"] = {"fetch_kib": round(fk, 1), "write_kib": round(wk, 1),
+                                          "traffic_bytes": int(round(tb)), "algorithmic_bytes": algo}
+            lines.append("| grouped launch | %.1f | %.1f | %.2f | %.2f |" % (fk, wk, tb / 1e6, algo / 1e6))
         for l, fids, wids in zip(layers, _layer_dispatches(fe, nl, 3), _layer_dispatches(wr, nl, 3)):
             fk = float(np.mean([fe[i][1] for i in fids]))
             wk = float(np.mean([wr[i][1] for i in wids]))
@@ -364,6 +413,22 @@ def summarize_profiles(d, workload):
                   "benchmark's effective TFLOP/s." % (MFMA_FLOPS_PER_MOP_BF16, PEAK["bf16"]), "",
                   "| layer | counted MFMA GFLOP | issued (plan) GFLOP | structural GFLOP | "
                   "MFMA utilisation | structural / peak |", "|---|---|---|---|---|---|"]
+        if grouped:
+            mops, gm = _split_group(mops)
+            cf = MFMA_FLOPS_PER_MOP_BF16 * float(np.mean([v for _, v in gm]))
+            nz = issued = 0.0
+            for l in layers:
+                desc = h2.make_desc(l.n, l.c_in, l.h, l.w, l.c_out, l.r, l.s, l.stride, l.pad,
+                                    l.out_pad, l.dil,
+                                    h2.HUGE2_NCHW if l.layout == "NCHW" else h2.HUGE2_NHWC,
+                                    h2.HUGE2_BF16)
+                m = h2.huge2_plan_macs(desc, l.transposed)
+                nz += 2.0 * m[0]
+                issued += 2.0 * m[1]
+            t = avg_group_us * 1e-6
+            lines.append("| grouped launch | %.2f | %.2f | %.2f | %.3f | %.3f |" % (
+                cf / 1e9, issued / 1e9, nz / 1e9, cf / t / (PEAK["bf16"] * 1e12),
+                nz / t / (PEAK["bf16"] * 1e12)))
         for l, ids in zip(layers, _layer_dispatches(mops, nl, 3)):
             if l.dtype != "bf16":
                 continue
@@ -621,7 +686,7 @@ def bench_forward(name, args, dev):
     import numpy as np
     import torch
 
-    items, plans, step, step_outputs, step_input = build_workload(name, dev)
+    items, plans, step, step_outputs, step_input, group = build_workload(name, dev)
     flops = layer_flops(plans)
     issued = [2 * p.macs()[1] for p in plans]
     total_flops = sum(flops)
@@ -716,32 +781,49 @@ def bench_forward(name, args, dev):
     # `steps` back-to-back launches between two events on the launch stream
     # (the same input every time), so that per-launch event overhead does
     # not enter the mean launch duration.
+    # A grouped workload's kernel is the one launch of all its layers: its
+    # algorithmic work is every layer's FLOPs, its bytes the shared input once
+    # plus every layer's weights and output.
     x_dom = step_input(dom)
-    plans[dom].stage(x_dom)
-    torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(args.steps):
-        plans[dom].gemm(x_dom, step_outputs()[dom])
-    e1.record()
+    if group is not None:
+        l0 = items[0][0]
+        dom_flops = total_flops
+        dom_bytes = sum(algo_bytes) - (len(items) - 1) * esz * l0.n * l0.c_in * l0.h * l0.w
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(args.steps):
+            group(x_dom, outs=step_outputs())
+        e1.record()
+    else:
+        dom_flops, dom_bytes = flops[dom], algo_bytes[dom]
+        plans[dom].stage(x_dom)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(args.steps):
+            plans[dom].gemm(x_dom, step_outputs()[dom])
+        e1.record()
     torch.cuda.synchronize()
     dom_ms = e0.elapsed_time(e1) / args.steps
     dom_t = dom_ms * 1e-3
-    intensity = flops[dom] / algo_bytes[dom]
+    intensity = dom_flops / dom_bytes
     ridge = PEAK[dtype] * 1e12 / (HBM_PEAK_GBS * 1e9)
     if intensity >= ridge:
-        achieved = flops[dom] / dom_t / 1e12
+        achieved = dom_flops / dom_t / 1e12
         roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK[dtype],
                     "unit": "TFLOP/s", "frac": round(achieved / PEAK[dtype], 4)}
-        per_launch = {"algorithmic_flop_per_launch": flops[dom]}
+        per_launch = {"algorithmic_flop_per_launch": dom_flops}
     else:
-        achieved = algo_bytes[dom] / dom_t / 1e9
+        achieved = dom_bytes / dom_t / 1e9
         roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
-        per_launch = {"algorithmic_bytes_per_launch": algo_bytes[dom]}
+        per_launch = {"algorithmic_bytes_per_launch": dom_bytes}
     dom_layer = items[dom][0]
-    roofline["traffic"] = measured_traffic(name, items[dom][0].name)
-    roofline.update({"kernel": "%s (%s)" % (plans[dom].kernel, items[dom][0].name),
+    dom_name = "group" if group is not None else items[dom][0].name
+    roofline["traffic"] = measured_traffic(name, dom_name)
+    roofline.update({"kernel": ("grouped launch of %d layers: %s (%s)" % (len(plans), plans[dom].kernel, name)
+                                if group is not None else
+                                "%s (%s)" % (plans[dom].kernel, items[dom][0].name)),
                      "mean_launch_ms": round(dom_ms, 5),
                      "arithmetic_intensity_flop_per_byte": round(intensity, 1)})
     roofline.update(per_launch)
@@ -767,9 +849,11 @@ def bench_forward(name, args, dev):
         "wall_s_timed": round(wall, 3),
         "settle_ms": round(settled_ms, 1),
     }
+    if group is not None:
+        group.close()
     for p in plans:
         p.close()
-    del plans, step, items
+    del plans, step, items, group
     torch.cuda.synchronize()
     return out, dom_layer
 

@@ -165,6 +165,45 @@ huge2_status huge2_conv2d_transpose(const huge2_conv_desc* desc, const void* x, 
 huge2_status huge2_conv2d_dilated(const huge2_conv_desc* desc, const void* x, const void* w,
                                   const float* bias, void* y, void* hip_stream);
 
+/* ---- several convolutions of one input in one launch ------------------- */
+
+/* A group runs the GEMM work of several plans that read the same input as
+ * ONE kernel launch: e.g. the parallel branches of an atrous spatial
+ * pyramid, each a dilated convolution of one feature map with its own
+ * dilation (section 3.2.2 applied per branch).  The works of all plans are
+ * listed together, image by image, and inside an image the costliest first
+ * (the number of kernel taps a tile multiplies differs between border
+ * classes and between dilations): the eight XCDs of the MI355X then each
+ * work through contiguous images, whose input rows every branch shares in
+ * that XCD's L2, and the compute units finish together.  Every output
+ * element is computed exactly as by huge2_plan_execute of its own plan (the
+ * same tiles, taps and summation order: the results are bitwise equal).
+ *
+ * huge2_group_create: plans[0 .. count) (1 <= count <= 8) must be plans
+ * whose main kernel is the phase GEMM without a staging pass or a K split
+ * (huge2_plan_kernel names "phase_gemm"; huge2_plan_stages_input is 0), with
+ * equal input descriptors (n, c_in, h, w, layout, dtype), output channels,
+ * kernel size, output size, activation and tile shape; they may differ in
+ * stride, padding and dilation.  The group keeps pointers to the plans, which must
+ * outlive it, and owns a device copy of the merged work list (copied on
+ * hip_stream, which it then waits for).  Errors: INVALID_ARG (NULL out or
+ * plans, count out of range), UNSUPPORTED (plans that cannot share a
+ * launch), ALLOC, HIP. */
+typedef struct huge2_group huge2_group;
+huge2_status huge2_group_create(huge2_group** out, const huge2_plan* const* plans, int32_t count,
+                                void* hip_stream);
+
+/* Enqueue the group's launch on hip_stream: y[i] = op_i(x) (+ bias[i]) for
+ * plan i.  x is the shared input (the plans' layout); y is an array of
+ * count output pointers (none NULL or equal to x); bias is NULL or an array
+ * of count pointers, each NULL or [c_out] float.  Executes of one group may
+ * overlap (nothing is written but the outputs).  Errors: INVALID_ARG, HIP. */
+huge2_status huge2_group_execute(const huge2_group* group, const void* x, const float* const* bias,
+                                 void* const* y, void* hip_stream);
+
+/* Release a group (its plans are untouched).  NULL is accepted.  Errors: HIP. */
+huge2_status huge2_group_destroy(huge2_group* group);
+
 /* ---- training: weight gradients (section 3.2.3) ------------------------- */
 
 /* Back-propagation of a GAN updates the kernels from the output errors dy

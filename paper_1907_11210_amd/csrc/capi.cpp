@@ -37,6 +37,7 @@ struct huge2_plan {
   SegDev* d_segs;
   TapDev* d_taps;
   WorkDev* d_works;
+  const uint32_t* d_ptab;  // pixel table of a listed plan (or null)
   bool stream_ordered;  // buffers came from hipMallocAsync on alloc_stream
   hipStream_t alloc_stream;
   int64_t nonzero_macs, issued_macs;
@@ -54,6 +55,25 @@ struct huge2_plan {
   bool gather;        // gather form: staging = the receptive-field gather into inner->xs
   void* zbuf;         // its output, the per-tap products (fp32 NCHW)
   char kernel_name[64];
+  // host copies of the GEMM metadata, for grouped launches (huge2_group)
+  std::vector<SegDev> h_segs;
+  std::vector<TapDev> h_taps;
+  std::vector<WorkDev> h_works;
+  std::vector<uint32_t> h_ptab;
+};
+
+// Several GEMM plans of one input run as one launch: their segments, taps,
+// works and pixel tables concatenated (each segment naming its plan), the
+// works ordered by image and, inside an image, by decreasing cost.
+struct huge2_group {
+  int count;
+  const huge2_plan* plans[huge2::kMaxGroup];
+  void* meta;
+  huge2::SegDev* d_segs;
+  huge2::TapDev* d_taps;
+  huge2::WorkDev* d_works;
+  const uint32_t* d_ptab;
+  int n_works;
 };
 
 namespace {
@@ -141,7 +161,7 @@ void order_works_for_xcds(std::vector<WorkDev>& works, const std::vector<SegDev>
   const int b = best_b, a = 8 / best_b;
   struct Key {
     int64_t cell, pos;
-    int32_t seg, m0, n0, ks;
+    WorkDev w;
   };
   std::vector<Key> keys;
   keys.reserve(works.size());
@@ -151,7 +171,7 @@ void order_works_for_xcds(std::vector<WorkDev>& works, const std::vector<SegDev>
     j /= sg.qn_w;
     const int64_t a_h = j % sg.qn_h;
     j /= sg.qn_h;
-    const int64_t img = j % nimg;
+    const int64_t img = std::min<int64_t>(j / sg.nphase, nimg - 1);
     const int64_t qt = std::max<int64_t>(1, (ho + sg.out_step_h - 1) / sg.out_step_h);
     const int64_t qh = std::min<int64_t>(sg.q0_h + a_h, qt - 1);
     const int64_t pos = img * qt + qh;  // in [0, nimg * qt)
@@ -160,26 +180,18 @@ void order_works_for_xcds(std::vector<WorkDev>& works, const std::vector<SegDev>
     Key k;
     k.cell = row * b + col;
     k.pos = pos;
-    k.seg = w.seg;
-    k.m0 = w.m0;
-    k.n0 = w.n0;
-    k.ks = w.ks;
+    k.w = w;
     keys.push_back(k);
   }
   std::stable_sort(keys.begin(), keys.end(), [](const Key& x, const Key& y) {
     if (x.cell != y.cell) return x.cell < y.cell;
     if (x.pos != y.pos) return x.pos < y.pos;
-    if (x.seg != y.seg) return x.seg < y.seg;
-    if (x.m0 != y.m0) return x.m0 < y.m0;
-    if (x.n0 != y.n0) return x.n0 < y.n0;
-    return x.ks < y.ks;
+    if (x.w.seg != y.w.seg) return x.w.seg < y.w.seg;
+    if (x.w.m0 != y.w.m0) return x.w.m0 < y.w.m0;
+    if (x.w.n0 != y.w.n0) return x.w.n0 < y.w.n0;
+    return x.w.ks < y.w.ks;
   });
-  for (size_t i = 0; i < works.size(); ++i) {
-    works[i].seg = keys[i].seg;
-    works[i].m0 = keys[i].m0;
-    works[i].n0 = keys[i].n0;
-    works[i].ks = keys[i].ks;
-  }
+  for (size_t i = 0; i < works.size(); ++i) works[i] = keys[i].w;
 }
 
 // Schedule model: the dispatcher hands the works, in list order, to the first
@@ -187,31 +199,52 @@ void order_works_for_xcds(std::vector<WorkDev>& works, const std::vector<SegDev>
 // stages plus about two stages of prologue and epilogue.  Returns the model's
 // makespan in stages.  A work count just above the slot count doubles the
 // makespan, which a finer split into border classes can cause.
-int64_t makespan_stages(const huge2_conv_desc& d, const PlanShape& shape, int cfg) {
-  const int bm = tile_bm(cfg), bn = tile_bn(cfg);
-  const int64_t kc = tile_kb(cfg) / elem_size(d.dtype);
-  const int64_t cblocks = (d.c_in + kc - 1) / kc;
-  const int64_t ntn = (d.c_out + bn - 1) / bn;
+int64_t makespan_of(const std::vector<int64_t>& costs, int cfg) {
   const int64_t slots = (int64_t)kComputeUnits * kTiles[cfg].wg_per_cu;
   std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> free_at;
   int64_t used = 0, end = 0;
+  for (int64_t cost : costs) {
+    int64_t t = 0;
+    if (used < slots) {
+      ++used;
+    } else {
+      t = free_at.top();
+      free_at.pop();
+    }
+    free_at.push(t + cost);
+    end = std::max(end, t + cost);
+  }
+  return end;
+}
+
+int64_t cblocks_of(const huge2_conv_desc& d, int cfg) {
+  const int64_t kc = tile_kb(cfg) / elem_size(d.dtype);
+  return (d.c_in + kc - 1) / kc;
+}
+
+int64_t makespan_stages(const huge2_conv_desc& d, const PlanShape& shape, int cfg) {
+  const int bm = tile_bm(cfg), bn = tile_bn(cfg);
+  const int64_t cblocks = cblocks_of(d, cfg);
+  const int64_t ntn = (d.c_out + bn - 1) / bn;
+  std::vector<int64_t> costs;
   for (const huge2_segment& s : shape.segs) {
     const int64_t m = (int64_t)d.n * s.nphase_h * s.nphase_w * s.qn_h * s.qn_w;
     const int64_t works = (m + bm - 1) / bm * ntn;
-    const int64_t cost = (int64_t)s.tap_count * cblocks + 2;
-    for (int64_t i = 0; i < works; ++i) {
-      int64_t t = 0;
-      if (used < slots) {
-        ++used;
-      } else {
-        t = free_at.top();
-        free_at.pop();
-      }
-      free_at.push(t + cost);
-      end = std::max(end, t + cost);
-    }
+    costs.insert(costs.end(), works, (int64_t)s.tap_count * cblocks + 2);
   }
-  return end;
+  return makespan_of(costs, cfg);
+}
+
+// The same model for the listed form: per image, its tiles in list order.
+int64_t makespan_listed(const huge2_conv_desc& d, const ListedShape& ls, int cfg) {
+  const int bn = tile_bn(cfg);
+  const int64_t cblocks = cblocks_of(d, cfg);
+  const int64_t ntn = (d.c_out + bn - 1) / bn;
+  std::vector<int64_t> costs;
+  for (int img = 0; img < d.n; ++img)
+    for (const auto& taps : ls.tile_taps)
+      costs.insert(costs.end(), ntn, (int64_t)taps.size() * cblocks + 2);
+  return makespan_of(costs, cfg);
 }
 
 int floor_div_i(int a, int b) { return a >= 0 ? a / b : -((-a + b - 1) / b); }
@@ -550,12 +583,19 @@ int choose_split(const huge2_conv_desc& d, bool transposed, int cfg) {
 }
 
 // Tile configuration, border-class form and decomposition of a GEMM plan
-// (shared by plan creation and the MAC report).  Returns -1 if the shape
-// cannot be built.
-int plan_gemm_shape(const huge2_conv_desc& d, bool tr, PlanShape* shape) {
+// (shared by plan creation and the MAC report).  A stride-1 dilated conv
+// takes the listed form (*listed true, ls filled) when the schedule model
+// finishes it no later than the segment form (HUGE2_LISTED=0/1 forces the
+// choice).  Returns -1 if the shape cannot be built.
+int plan_gemm_shape(const huge2_conv_desc& d, bool tr, PlanShape* shape, bool* listed,
+                    ListedShape* ls) {
   const int cfg = choose_cfg(d, tr, 2);
   const int split = choose_split(d, tr, cfg);
   if (!build_shape(d, tr, split, tile_bm(cfg), shape)) return -1;
+  *listed = false;
+  const int force = env_int("HUGE2_LISTED", -1);
+  if (!tr && force != 0 && build_listed(d, tile_bm(cfg), ls))
+    *listed = force == 1 || makespan_listed(d, *ls, cfg) <= makespan_stages(d, *shape, cfg);
   return cfg;
 }
 
@@ -826,7 +866,9 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   }
 
   PlanShape shape;
-  const int cfg = plan_gemm_shape(d, tr, &shape);
+  ListedShape ls;
+  bool listed = false;
+  const int cfg = plan_gemm_shape(d, tr, &shape, &listed, &ls);
   if (cfg < 0) return HUGE2_ERR_INVALID_ARG;
   const int bm = tile_bm(cfg), bn = tile_bn(cfg);
 
@@ -845,6 +887,10 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     else
       std::snprintf(p->kernel_name, sizeof(p->kernel_name), "phase_gemm2_kernel %dx%d w%d k%d",
                     t.bm, t.bn, t.pw * t.cw, t.ksplit);
+    if (listed) {
+      const size_t len = std::strlen(p->kernel_name);
+      std::snprintf(p->kernel_name + len, sizeof(p->kernel_name) - len, " listed");
+    }
   }
   const int esz = elem_size(d.dtype);
   const int vec = 16 / esz;
@@ -866,7 +912,70 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   std::vector<WorkDev> works;
   const int ntiles_n = p->cout_pad / bn;
   int64_t issued = 0;
+  std::vector<uint32_t> ptab;
+  if (listed) {
+    // one segment over every image; each tile of bm listed pixels of one image
+    // runs its own tap set (the taps of equal sets are stored once)
+    SegDev sd;
+    std::memset(&sd, 0, sizeof(sd));
+    const int per_img = (int)ls.pix.size();
+    sd.nphase_w = sd.nphase = 1;
+    sd.m_total = d.n * per_img;
+    sd.out_step_h = sd.out_step_w = 1;
+    sd.in0_h = -d.pad_h;
+    sd.in0_w = -d.pad_w;
+    sd.in_step_h = sd.in_step_w = 1;
+    sd.ptab = 0;
+    sd.per_img = per_img;
+    sd.ntw = 1;
+    const uint32_t divisors[4] = {1, 1, (uint32_t)per_img, 1};
+    for (int k = 0; k < 4; ++k) division_magic(divisors[k], &sd.div_mul[k], &sd.div_shift[k]);
+    segs.push_back(sd);
+    ptab = ls.pix;
+    std::vector<std::pair<int, int>> tile_range;  // (tap_begin, tap_count) per tile
+    for (const auto& tl : ls.tile_taps) {
+      int found = -1;
+      for (size_t u = 0; u < tile_range.size() && found < 0; ++u) {
+        const auto& prev = ls.tile_taps[u];
+        if (prev.size() != tl.size()) continue;
+        bool same = true;
+        for (size_t k = 0; k < tl.size() && same; ++k)
+          same = prev[k].kh == tl[k].kh && prev[k].kw == tl[k].kw;
+        if (same) found = (int)u;
+      }
+      if (found >= 0) {
+        tile_range.push_back(tile_range[found]);
+        continue;
+      }
+      tile_range.emplace_back((int)taps.size(), (int)tl.size());
+      for (const huge2_tap& t : tl) {
+        TapDev td;
+        td.slot = t.kh * d.s + t.kw;
+        td.off_h = t.off_h;
+        td.off_w = t.off_w;
+        td.pad = 0;
+        taps.push_back(td);
+      }
+    }
+    for (int img = 0; img < d.n; ++img)
+      for (size_t t = 0; t < ls.tile_taps.size(); ++t) {
+        const int m0 = img * per_img + (int)t * bm;
+        for (int nt = 0; nt < ntiles_n; ++nt) {
+          WorkDev wd;
+          std::memset(&wd, 0, sizeof(wd));
+          wd.seg = 0;
+          wd.m0 = m0;
+          wd.m1 = std::min(m0 + bm, (img + 1) * per_img);
+          wd.n0 = nt * bn;
+          wd.tap_begin = tile_range[t].first;
+          wd.tap_count = tile_range[t].second;
+          works.push_back(wd);
+          issued += (int64_t)bm * bn * wd.tap_count * p->cin_pad;
+        }
+      }
+  }
   for (const huge2_tap& t : shape.taps) {
+    if (listed) break;
     TapDev td;
     td.slot = t.kh * d.s + t.kw;
     td.off_h = t.off_h;
@@ -874,10 +983,11 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     td.pad = 0;
     taps.push_back(td);
   }
-  for (size_t i = 0; i < shape.segs.size(); ++i) {
+  for (size_t i = 0; i < shape.segs.size() && !listed; ++i) {
     const huge2_segment& s = shape.segs[i];
     SegDev sd;
     std::memset(&sd, 0, sizeof(sd));
+    sd.ptab = -1;
     sd.phase0_h = s.phase0_h;
     sd.phase0_w = s.phase0_w;
     sd.nphase_w = s.nphase_w;
@@ -896,7 +1006,8 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     sd.in_step_w = s.in_step_w;
     sd.tap_begin = s.tap_begin;
     sd.tap_count = s.tap_count;
-    const uint32_t divisors[4] = {(uint32_t)s.qn_w, (uint32_t)s.qn_h, (uint32_t)d.n,
+    sd.nphase = s.nphase_h * s.nphase_w;
+    const uint32_t divisors[4] = {(uint32_t)s.qn_w, (uint32_t)s.qn_h, (uint32_t)sd.nphase,
                                   (uint32_t)s.nphase_w};
     for (int k = 0; k < 4; ++k) division_magic(divisors[k], &sd.div_mul[k], &sd.div_shift[k]);
     // exact: every tap's read is in range for every pixel of the segment (the
@@ -919,10 +1030,14 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     for (int m0 = 0; m0 < sd.m_total; m0 += bm)
       for (int nt = 0; nt < ntiles_n; ++nt) {
         WorkDev wd;
+        std::memset(&wd, 0, sizeof(wd));
         wd.seg = (int32_t)i;
         wd.m0 = m0;
+        wd.m1 = std::min(m0 + bm, sd.m_total);
         wd.n0 = nt * bn;
         wd.ks = 0;
+        wd.tap_begin = s.tap_begin;
+        wd.tap_count = s.tap_count;
         works.push_back(wd);
         issued += (int64_t)bm * bn * s.tap_count * p->cin_pad;
       }
@@ -979,7 +1094,8 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   const size_t seg_b = segs.size() * sizeof(SegDev);
   const size_t tap_b = taps.size() * sizeof(TapDev);
   const size_t work_b = works.size() * sizeof(WorkDev);
-  const size_t meta_b = seg_b + tap_b + work_b;
+  const size_t ptab_b = ptab.size() * sizeof(uint32_t);
+  const size_t meta_b = seg_b + tap_b + work_b + ptab_b;
   const size_t wp_b = (size_t)d.r * d.s * p->cout_pad * p->cin_pad * esz;
   const size_t xs_b = p->staged ? p->x_bytes : 0;
   p->wp_bytes = wp_b;
@@ -997,11 +1113,13 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   p->d_segs = (SegDev*)p->meta;
   p->d_taps = (TapDev*)((char*)p->meta + seg_b);
   p->d_works = (WorkDev*)((char*)p->meta + seg_b + tap_b);
+  p->d_ptab = ptab_b ? (const uint32_t*)((char*)p->meta + seg_b + tap_b + work_b) : nullptr;
 
   std::vector<char> host(meta_b);
   if (seg_b) std::memcpy(host.data(), segs.data(), seg_b);
   if (tap_b) std::memcpy(host.data() + seg_b, taps.data(), tap_b);
   if (work_b) std::memcpy(host.data() + seg_b + tap_b, works.data(), work_b);
+  if (ptab_b) std::memcpy(host.data() + seg_b + tap_b + work_b, ptab.data(), ptab_b);
 
   bool ok = !fault("launch");
   if (ok && meta_b)
@@ -1012,6 +1130,12 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
                              stream) == hipSuccess;
   // the host copy of the metadata must outlive the transfer
   if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
+  if (ok) {
+    p->h_segs = std::move(segs);
+    p->h_taps = std::move(taps);
+    p->h_works = std::move(works);
+    p->h_ptab = std::move(ptab);
+  }
   if (!ok) {
     (void)hipGetLastError();
     free_buffers(p);
@@ -1139,10 +1263,11 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
     return HUGE2_OK;
   }
   GemmArgs a;
+  std::memset(&a, 0, sizeof(a));
   a.x = p->staged ? p->xs : x;
-  a.wp = p->wp;
-  a.bias = bias;
-  a.y = y;
+  a.wp[0] = p->wp;
+  a.bias[0] = bias;
+  a.y[0] = y;
   a.bias_div = p->bias_div;
   a.act = d.activation;
   a.ksplit = p->ksplit;
@@ -1150,12 +1275,13 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
   a.part_stride = (uint32_t)((size_t)d.n * d.c_out * p->ho * p->wo);
   if (p->ksplit > 1) {
     // the slices write partials; bias and activation come with the sum
-    a.bias = nullptr;
+    a.bias[0] = nullptr;
     a.act = HUGE2_ACT_NONE;
   }
   a.segs = p->d_segs;
   a.taps = p->d_taps;
   a.works = p->d_works;
+  a.ptab = p->d_ptab;
   a.n_works = p->n_works;
   a.n = d.n;
   a.h = d.h;
@@ -1356,6 +1482,157 @@ huge2_status wgrad_one_shot(const huge2_conv_desc* desc, int transposed, const v
   return st;
 }
 
+// ---------------------------------------------------------------------------
+// Grouped launch of several GEMM plans that read one input.
+
+bool groupable(const huge2_plan* p, const huge2_plan* q) {
+  if (!p || !q || p->cfg < 0 || q->cfg < 0 || p->inner || q->inner || p->ztile || q->ztile ||
+      p->rowphase || q->rowphase || p->quad || q->quad || p->staged || q->staged ||
+      p->ksplit != 1 || q->ksplit != 1 || p->h_works.empty() || q->h_works.empty())
+    return false;
+  const huge2_conv_desc &a = p->desc, &b = q->desc;
+  return a.n == b.n && a.c_in == b.c_in && a.h == b.h && a.w == b.w && a.c_out == b.c_out &&
+         a.layout == b.layout && a.dtype == b.dtype && a.activation == b.activation &&
+         p->ho == q->ho && p->wo == q->wo && p->cfg == q->cfg && p->cin_pad == q->cin_pad &&
+         p->cout_pad == q->cout_pad && p->c_stride == q->c_stride && p->x_bytes == q->x_bytes &&
+         p->wp_bytes == q->wp_bytes && p->bias_div == q->bias_div && a.r == b.r && a.s == b.s;
+}
+
+// Image of the first pixel of a work (the segment's pixels are image-major).
+int work_image(const SegDev& sg, const WorkDev& w) {
+  if (sg.ptab >= 0) return w.m0 / std::max(1, sg.per_img);
+  const int64_t per_img = (int64_t)sg.qn_w * sg.qn_h * sg.nphase;
+  return (int)(w.m0 / std::max<int64_t>(1, per_img));
+}
+
+huge2_status group_create(huge2_group** out, const huge2_plan* const* plans, int count,
+                          hipStream_t stream) {
+  if (!out) return HUGE2_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (!plans || count < 1 || count > kMaxGroup) return HUGE2_ERR_INVALID_ARG;
+  for (int i = 0; i < count; ++i)
+    if (!plans[i]) return HUGE2_ERR_INVALID_ARG;
+  for (int i = 0; i < count; ++i)
+    if (!groupable(plans[0], plans[i])) return HUGE2_ERR_UNSUPPORTED;
+  const huge2_plan* p0 = plans[0];
+  const int64_t kc = tile_kb(p0->cfg) / elem_size(p0->desc.dtype);
+  const int64_t cblocks = (p0->cin_pad + kc - 1) / kc;
+  std::vector<SegDev> segs;
+  std::vector<TapDev> taps;
+  std::vector<uint32_t> ptab;
+  struct Item {
+    int img;
+    int64_t cost;
+    WorkDev w;
+  };
+  std::vector<Item> items;
+  for (int i = 0; i < count; ++i) {
+    const huge2_plan* p = plans[i];
+    const int s0 = (int)segs.size(), t0 = (int)taps.size(), q0 = (int)ptab.size();
+    for (SegDev sd : p->h_segs) {
+      sd.plan = i;
+      sd.tap_begin += t0;
+      if (sd.ptab >= 0) sd.ptab += q0;
+      segs.push_back(sd);
+    }
+    taps.insert(taps.end(), p->h_taps.begin(), p->h_taps.end());
+    ptab.insert(ptab.end(), p->h_ptab.begin(), p->h_ptab.end());
+    for (WorkDev w : p->h_works) {
+      const int img = work_image(p->h_segs[w.seg], w);
+      w.seg += s0;
+      w.tap_begin += t0;
+      items.push_back({img, (int64_t)w.tap_count * cblocks + 2, w});
+    }
+  }
+  // image-major: the eight XCDs take contiguous runs of the list, so the
+  // workgroups that run together on one XCD share one image's input rows in
+  // its L2; inside an image the costliest works first, so that the
+  // dispatcher's greedy placement balances the compute units
+  std::stable_sort(items.begin(), items.end(), [](const Item& a, const Item& b) {
+    if (a.img != b.img) return a.img < b.img;
+    return a.cost > b.cost;
+  });
+  std::vector<WorkDev> works;
+  works.reserve(items.size());
+  for (const Item& it : items) works.push_back(it.w);
+  huge2_group* g = new (std::nothrow) huge2_group();
+  if (!g) return HUGE2_ERR_ALLOC;
+  g->count = count;
+  for (int i = 0; i < count; ++i) g->plans[i] = plans[i];
+  g->n_works = (int)works.size();
+  const size_t seg_b = segs.size() * sizeof(SegDev), tap_b = taps.size() * sizeof(TapDev);
+  const size_t work_b = works.size() * sizeof(WorkDev), ptab_b = ptab.size() * sizeof(uint32_t);
+  const size_t meta_b = seg_b + tap_b + work_b + ptab_b;
+  if (fault("alloc") || hipMalloc(&g->meta, meta_b) != hipSuccess) {
+    (void)hipGetLastError();
+    delete g;
+    return HUGE2_ERR_ALLOC;
+  }
+  g->d_segs = (SegDev*)g->meta;
+  g->d_taps = (TapDev*)((char*)g->meta + seg_b);
+  g->d_works = (WorkDev*)((char*)g->meta + seg_b + tap_b);
+  g->d_ptab = ptab_b ? (const uint32_t*)((char*)g->meta + seg_b + tap_b + work_b) : nullptr;
+  std::vector<char> host(meta_b);
+  std::memcpy(host.data(), segs.data(), seg_b);
+  if (tap_b) std::memcpy(host.data() + seg_b, taps.data(), tap_b);
+  std::memcpy(host.data() + seg_b + tap_b, works.data(), work_b);
+  if (ptab_b) std::memcpy(host.data() + seg_b + tap_b + work_b, ptab.data(), ptab_b);
+  bool ok = !fault("launch") &&
+            hipMemcpyAsync(g->meta, host.data(), meta_b, hipMemcpyHostToDevice, stream) == hipSuccess;
+  if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
+  if (!ok) {
+    (void)hipGetLastError();
+    (void)hipFree(g->meta);
+    delete g;
+    return HUGE2_ERR_HIP;
+  }
+  *out = g;
+  return HUGE2_OK;
+}
+
+huge2_status group_execute(const huge2_group* g, const void* x, const float* const* bias,
+                           void* const* y, hipStream_t stream) {
+  if (!g || !x || !y) return HUGE2_ERR_INVALID_ARG;
+  for (int i = 0; i < g->count; ++i)
+    if (!y[i] || y[i] == x) return HUGE2_ERR_INVALID_ARG;
+  if (fault("launch")) return HUGE2_ERR_HIP;
+  const huge2_plan* p = g->plans[0];
+  const huge2_conv_desc& d = p->desc;
+  GemmArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.x = x;
+  for (int i = 0; i < g->count; ++i) {
+    a.wp[i] = g->plans[i]->wp;
+    a.bias[i] = bias ? bias[i] : nullptr;
+    a.y[i] = y[i];
+  }
+  a.bias_div = p->bias_div;
+  a.act = d.activation;
+  a.ksplit = 1;
+  a.segs = g->d_segs;
+  a.taps = g->d_taps;
+  a.works = g->d_works;
+  a.ptab = g->d_ptab;
+  a.n_works = g->n_works;
+  a.n = d.n;
+  a.h = d.h;
+  a.w = d.w;
+  a.cin = p->c_stride;
+  a.ks = d.s;
+  a.x_bytes = (uint32_t)p->x_bytes;
+  a.wp_bytes = (uint32_t)p->wp_bytes;
+  a.cin_pad = p->cin_pad;
+  a.cout = d.c_out;
+  a.cout_pad = p->cout_pad;
+  a.ho = p->ho;
+  a.wo = p->wo;
+  if (launch_phase_gemm(a, d.dtype, p->cfg, d.layout == HUGE2_NCHW, stream) != hipSuccess) {
+    (void)hipGetLastError();
+    return HUGE2_ERR_HIP;
+  }
+  return HUGE2_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1511,14 +1788,17 @@ huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, in
       return HUGE2_OK;
     }
     PlanShape shape;
-    const int cfg = plan_gemm_shape(dd, transposed != 0, &shape);
+    ListedShape ls;
+    bool listed = false;
+    const int cfg = plan_gemm_shape(dd, transposed != 0, &shape, &listed, &ls);
     if (cfg < 0) return HUGE2_ERR_INVALID_ARG;
     const int bm = tile_bm(cfg), bn = tile_bn(cfg);
     const int bk = tile_kb(cfg) / elem_size(dd.dtype);
     const int64_t cin_pad = round_up(dd.c_in, bk);
     const int64_t ntn = round_up(dd.c_out, bn) / bn;
     *nonzero_macs = shape.nonzero_macs;
-    *issued_macs = shape.tile_taps * bm * bn * ntn * cin_pad;
+    *issued_macs = listed ? ls.issued_rows_taps * bn * ntn * cin_pad
+                          : shape.tile_taps * bm * bn * ntn * cin_pad;
     return HUGE2_OK;
   } catch (...) {
     return HUGE2_ERR_ALLOC;
@@ -1566,6 +1846,31 @@ huge2_status huge2_conv2d_dilated_wgrad(const huge2_conv_desc* desc, const void*
   } catch (...) {
     return HUGE2_ERR_ALLOC;
   }
+}
+
+huge2_status huge2_group_create(huge2_group** out, const huge2_plan* const* plans, int32_t count,
+                                void* hip_stream) {
+  try {
+    return group_create(out, plans, count, (hipStream_t)hip_stream);
+  } catch (...) {
+    return HUGE2_ERR_ALLOC;
+  }
+}
+
+huge2_status huge2_group_execute(const huge2_group* group, const void* x, const float* const* bias,
+                                 void* const* y, void* hip_stream) {
+  try {
+    return group_execute(group, x, bias, y, (hipStream_t)hip_stream);
+  } catch (...) {
+    return HUGE2_ERR_HIP;
+  }
+}
+
+huge2_status huge2_group_destroy(huge2_group* group) {
+  if (!group) return HUGE2_OK;
+  const hipError_t e = hipFree(group->meta);  // waits for work that may still read it
+  delete group;
+  return e == hipSuccess ? HUGE2_OK : HUGE2_ERR_HIP;
 }
 
 }  // extern "C"

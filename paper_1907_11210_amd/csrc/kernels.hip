@@ -59,9 +59,19 @@ struct PixelPos {
 __device__ __forceinline__ uint32_t fast_div(uint32_t v, uint32_t mul, uint32_t shift) {
   return (uint32_t)(((uint64_t)v * mul) >> shift);
 }
-__device__ __forceinline__ PixelPos pixel_pos(const SegDev& sg, int nimg, int m) {
+__device__ __forceinline__ PixelPos pixel_pos(const SegDev& sg, const uint32_t* ptab, int m) {
   PixelPos p;
   uint32_t j = (uint32_t)m;
+  if (sg.ptab >= 0) {
+    const uint32_t img = fast_div(j, sg.div_mul[2], sg.div_shift[2]);
+    const uint32_t e = ptab[sg.ptab + (int)(j - img * (uint32_t)sg.per_img)];
+    p.img = (int)img;
+    p.oh = (int)(e >> 16);
+    p.ow = (int)(e & 0xffffu);
+    p.ih = sg.in0_h + p.oh;
+    p.iw = sg.in0_w + p.ow;
+    return p;
+  }
   uint32_t t = fast_div(j, sg.div_mul[0], sg.div_shift[0]);
   const int a_w = (int)(j - t * (uint32_t)sg.qn_w);
   j = t;
@@ -69,8 +79,8 @@ __device__ __forceinline__ PixelPos pixel_pos(const SegDev& sg, int nimg, int m)
   const int a_h = (int)(j - t * (uint32_t)sg.qn_h);
   j = t;
   t = fast_div(j, sg.div_mul[2], sg.div_shift[2]);
-  p.img = (int)(j - t * (uint32_t)nimg);
-  const uint32_t iph = t;
+  const uint32_t iph = j - t * (uint32_t)sg.nphase;
+  p.img = (int)t;
   const uint32_t iph_h = fast_div(iph, sg.div_mul[3], sg.div_shift[3]);
   const int iph_w = (int)(iph - iph_h * (uint32_t)sg.nphase_w);
   const int qh = sg.q0_h + a_h, qw = sg.q0_w + a_w;
@@ -91,7 +101,7 @@ __device__ __forceinline__ PixelPos pixel_pos(const SegDev& sg, int nimg, int m)
 // reading it from global memory between the stores would make every load
 // wait for the stores issued before it.
 template <bool BF16, bool NCHW_OUT, int TP, int TC>
-__device__ __forceinline__ void store_tile(const GemmArgs& a, const SegDev& sg,
+__device__ __forceinline__ void store_tile(const GemmArgs& a, const SegDev& sg, int m_end, void* y,
                                            const f32x16 (&acc)[TP][TC], int pix0, int ch0,
                                            int lane, const float* sb) {
   const int hw_o = a.ho * a.wo;
@@ -109,8 +119,8 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, const SegDev& sg,
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int m = pix0 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (m >= sg.m_total) continue;
-        const PixelPos p = pixel_pos(sg, a.n, m);
+        if (m >= m_end) continue;
+        const PixelPos p = pixel_pos(sg, a.ptab, m);
         const int pix = (p.img * a.ho + p.oh) * a.wo + p.ow;
 #pragma unroll
         for (int j = 0; j < TC; ++j) {
@@ -119,9 +129,9 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, const SegDev& sg,
           const float v = activate(acc[i][j][r] + bv[j], a.act);
           const size_t off = (size_t)pix * a.cout + ch;
           if constexpr (BF16)
-            ((uint16_t*)a.y)[off] = f32_to_bf16_rne(v);
+            ((uint16_t*)y)[off] = f32_to_bf16_rne(v);
           else
-            ((float*)a.y)[off] = v;
+            ((float*)y)[off] = v;
         }
       }
     }
@@ -131,8 +141,8 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, const SegDev& sg,
 #pragma unroll
     for (int i = 0; i < TP; ++i) {
       const int m = pix0 + 32 * i + (lane & 31);
-      ok[i] = m < sg.m_total;
-      const PixelPos p = pixel_pos(sg, a.n, ok[i] ? m : 0);
+      ok[i] = m < m_end;
+      const PixelPos p = pixel_pos(sg, a.ptab, ok[i] ? m : pix0);
       base[i] = (size_t)p.img * a.cout * hw_o + (size_t)p.oh * a.wo + p.ow;
     }
 #pragma unroll
@@ -153,9 +163,9 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, const SegDev& sg,
           const float v = activate(acc[i][j][r] + bv[r], a.act);
           const size_t off = base[i] + (size_t)ch * hw_o;
           if constexpr (BF16)
-            ((uint16_t*)a.y)[off] = f32_to_bf16_rne(v);
+            ((uint16_t*)y)[off] = f32_to_bf16_rne(v);
           else
-            ((float*)a.y)[off] = v;
+            ((float*)y)[off] = v;
         }
       }
     }
@@ -215,7 +225,7 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
   const __amdgpu_buffer_rsrc_t xr =
       __builtin_amdgcn_make_buffer_rsrc((void*)a.x, 0, a.x_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t wr =
-      __builtin_amdgcn_make_buffer_rsrc((void*)a.wp, 0, a.wp_bytes, 0x00020000);
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.wp[sg.plan], 0, a.wp_bytes, 0x00020000);
 
   // This thread's A-tile rows (pixels) and its 16-byte chunk within a row.
   // Rows past the end of the segment repeat its last pixel: they compute
@@ -225,15 +235,15 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
   uint32_t a_base[A_LD];  // byte offset of (pixel, chunk) at tap offset (0, 0)
 #pragma unroll
   for (int i = 0; i < A_LD; ++i) {
-    const int m = min(wk.m0 + tid / CPR + (NT / CPR) * i, sg.m_total - 1);
-    const PixelPos p = pixel_pos(sg, a.n, m);
+    const int m = min(wk.m0 + tid / CPR + (NT / CPR) * i, wk.m1 - 1);
+    const PixelPos p = pixel_pos(sg, a.ptab, m);
     a_ih[i] = p.ih;
     a_iw[i] = p.iw;
     // unsigned (wrapping) arithmetic: the tap offset brings it back in range
     a_base[i] = (((uint32_t)p.img * (uint32_t)a.h + (uint32_t)p.ih) * (uint32_t)a.w +
                  (uint32_t)p.iw) * (uint32_t)a.cin * ESZ + (uint32_t)(chunk * VE * ESZ);
   }
-  const int ntaps = sg.tap_count;
+  const int ntaps = wk.tap_count;
   const int cblocks = a.cin_pad / KC;
   // this workgroup's K slice of channel blocks, [cb_w0, cb_w1)
   const int cb_w0 = wk.ks * cblocks / a.ksplit, cb_w1 = (wk.ks + 1) * cblocks / a.ksplit;
@@ -242,8 +252,9 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
   const int tail_c = a.cin - (cblocks - 1) * KC;
 
   __shared__ float s_bias[BN];
+  const float* const bias = a.bias[sg.plan];
   for (int t = tid; t < BN; t += NT)
-    s_bias[t] = (a.bias && wk.n0 + t < a.cout) ? a.bias[(wk.n0 + t) / a.bias_div] : 0.f;
+    s_bias[t] = (bias && wk.n0 + t < a.cout) ? bias[(wk.n0 + t) / a.bias_div] : 0.f;
 
   // The segment's taps in LDS: byte delta of the tapped pixel and byte
   // offset of the tap's weight block.
@@ -251,7 +262,7 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
   const bool lds_taps = !sg.tap_ap && ntaps <= kMaxLdsTaps;
   if (lds_taps) {
     for (int t = tid; t < ntaps; t += NT) {
-      const TapDev tp = a.taps[sg.tap_begin + t];
+      const TapDev tp = a.taps[wk.tap_begin + t];
       s_taps[t] = make_int4((tp.off_h * a.w + tp.off_w) * a.cin * ESZ,
                             (int)((uint32_t)tp.slot * (uint32_t)a.cout_pad * (uint32_t)a.cin_pad * ESZ),
                             tp.off_h, tp.off_w);
@@ -277,7 +288,7 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
   const __amdgpu_buffer_rsrc_t xr0 =
       __builtin_amdgcn_make_buffer_rsrc((void*)a.x, 0, 0, 0x00020000);
   const __amdgpu_buffer_rsrc_t wr0 =
-      __builtin_amdgcn_make_buffer_rsrc((void*)a.wp, 0, 0, 0x00020000);
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.wp[sg.plan], 0, 0, 0x00020000);
 
   // K order: channel block outer, tap inner, so that the taps of one channel
   // block re-read the same input rows while they are still in cache.  A load
@@ -302,7 +313,7 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
       if (lds_taps) {
         ti = s_taps[valid ? ld_tap : 0];
       } else {
-        const TapDev tp = a.taps[sg.tap_begin + (valid ? ld_tap : 0)];
+        const TapDev tp = a.taps[wk.tap_begin + (valid ? ld_tap : 0)];
         ti = make_int4((tp.off_h * a.w + tp.off_w) * a.cin * ESZ, (int)((uint32_t)tp.slot * slot_bytes),
                        tp.off_h, tp.off_w);
       }
@@ -452,13 +463,11 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
   }
 
   if (a.ksplit > 1) {
-    GemmArgs ap = a;
-    ap.y = a.part + (size_t)wk.ks * a.part_stride;
-    store_tile<false, NCHW_OUT, TP, TC>(ap, sg, acc, wk.m0 + wp_i * WP, wk.n0 + wc_i * WC, lane,
-                                        s_bias - wk.n0);
+    store_tile<false, NCHW_OUT, TP, TC>(a, sg, wk.m1, a.part + (size_t)wk.ks * a.part_stride, acc,
+                                        wk.m0 + wp_i * WP, wk.n0 + wc_i * WC, lane, s_bias - wk.n0);
   } else {
-    store_tile<BF16, NCHW_OUT, TP, TC>(a, sg, acc, wk.m0 + wp_i * WP, wk.n0 + wc_i * WC, lane,
-                                       s_bias - wk.n0);
+    store_tile<BF16, NCHW_OUT, TP, TC>(a, sg, wk.m1, a.y[sg.plan], acc, wk.m0 + wp_i * WP,
+                                       wk.n0 + wc_i * WC, lane, s_bias - wk.n0);
   }
 }
 
@@ -515,11 +524,11 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm2_kernel(GemmArgs a) {
   const __amdgpu_buffer_rsrc_t xr =
       __builtin_amdgcn_make_buffer_rsrc((void*)a.x, 0, a.x_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t wr =
-      __builtin_amdgcn_make_buffer_rsrc((void*)a.wp, 0, a.wp_bytes, 0x00020000);
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.wp[sg.plan], 0, a.wp_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t xr0 =
       __builtin_amdgcn_make_buffer_rsrc((void*)a.x, 0, 0, 0x00020000);
   const __amdgpu_buffer_rsrc_t wr0 =
-      __builtin_amdgcn_make_buffer_rsrc((void*)a.wp, 0, 0, 0x00020000);
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.wp[sg.plan], 0, 0, 0x00020000);
 
   // Pixel rows this thread loads: the shared rows (SHARE_A, S_LD of them, as
   // chunk tid % CPR) or its wave's own rows (TD of them, as lane half).
@@ -530,8 +539,8 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm2_kernel(GemmArgs a) {
 #pragma unroll
   for (int i = 0; i < NPIX; ++i) {
     const int r = SHARE_A ? tid / CPR + (NT / CPR) * i : wave * RD + 32 * i + row32;
-    const int m = min(wk.m0 + r, sg.m_total - 1);
-    const PixelPos p = pixel_pos(sg, a.n, m);
+    const int m = min(wk.m0 + r, wk.m1 - 1);
+    const PixelPos p = pixel_pos(sg, a.ptab, m);
     p_ih[i] = p.ih;
     p_iw[i] = p.iw;
     const uint32_t byte_in_row = SHARE_A ? (uint32_t)(s_chunk * 16) : (uint32_t)(half * (KB / 2));
@@ -554,7 +563,7 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm2_kernel(GemmArgs a) {
     }
   }
 
-  const int ntaps = sg.tap_count;
+  const int ntaps = wk.tap_count;
   const int cblocks = a.cin_pad / KC;
   // this workgroup's K slice of channel blocks [cb_w0, cb_w1), split over
   // its K groups
@@ -566,13 +575,14 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm2_kernel(GemmArgs a) {
   const int tail_c = a.cin - (cblocks - 1) * KC;
 
   __shared__ float s_bias[BN];
+  const float* const bias = a.bias[sg.plan];
   for (int t = threadIdx.x; t < BN; t += NTA)
-    s_bias[t] = (a.bias && wk.n0 + t < a.cout) ? a.bias[(wk.n0 + t) / a.bias_div] : 0.f;
+    s_bias[t] = (bias && wk.n0 + t < a.cout) ? bias[(wk.n0 + t) / a.bias_div] : 0.f;
   __shared__ int4 s_taps[kMaxLdsTaps];
   const bool lds_taps = !sg.tap_ap && ntaps <= kMaxLdsTaps;
   if (lds_taps) {
     for (int t = threadIdx.x; t < ntaps; t += NTA) {
-      const TapDev tp = a.taps[sg.tap_begin + t];
+      const TapDev tp = a.taps[wk.tap_begin + t];
       s_taps[t] = make_int4((tp.off_h * a.w + tp.off_w) * a.cin * ESZ,
                             (int)((uint32_t)tp.slot * (uint32_t)a.cout_pad * (uint32_t)a.cin_pad * ESZ),
                             tp.off_h, tp.off_w);
@@ -603,7 +613,7 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm2_kernel(GemmArgs a) {
       if (lds_taps) {
         ti = s_taps[valid ? ld_tap : 0];
       } else {
-        const TapDev tp = a.taps[sg.tap_begin + (valid ? ld_tap : 0)];
+        const TapDev tp = a.taps[wk.tap_begin + (valid ? ld_tap : 0)];
         ti = make_int4((tp.off_h * a.w + tp.off_w) * a.cin * ESZ, (int)((uint32_t)tp.slot * slot_bytes),
                        tp.off_h, tp.off_w);
       }
@@ -771,11 +781,11 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm2_kernel(GemmArgs a) {
   const int pix0 = wk.m0 + (SHARE_A ? 0 : wave * RD);
   const int ch0 = wk.n0 + (SHARE_A ? wave * RD : 0);
   if (a.ksplit > 1) {
-    GemmArgs ap = a;
-    ap.y = a.part + (size_t)wk.ks * a.part_stride;
-    store_tile<false, NCHW_OUT, TP, TC>(ap, sg, acc, pix0, ch0, lane, s_bias - wk.n0);
+    store_tile<false, NCHW_OUT, TP, TC>(a, sg, wk.m1, a.part + (size_t)wk.ks * a.part_stride, acc,
+                                        pix0, ch0, lane, s_bias - wk.n0);
   } else {
-    store_tile<BF16, NCHW_OUT, TP, TC>(a, sg, acc, pix0, ch0, lane, s_bias - wk.n0);
+    store_tile<BF16, NCHW_OUT, TP, TC>(a, sg, wk.m1, a.y[sg.plan], acc, pix0, ch0, lane,
+                                       s_bias - wk.n0);
   }
 }
 

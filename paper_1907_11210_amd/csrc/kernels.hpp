@@ -9,9 +9,11 @@ namespace huge2 {
 // A segment as the GEMM kernel reads it (mirrors huge2_segment, plus the
 // flattened GEMM height m_total = n * nphase_h * nphase_w * qn_h * qn_w).
 // Pixel index j of the segment decomposes, fastest first, as
-// (a_w in [0,qn_w), a_h in [0,qn_h), image n, phase index in [0, nphase_h*nphase_w)).
+// (a_w in [0,qn_w), a_h in [0,qn_h), phase index in [0, nphase), image n):
+// the pixels of one image are contiguous, so that the workgroups that run at
+// the same time read a compact region of the input.
 struct SegDev {
-  int32_t phase0_h, phase0_w, nphase_w, m_total;
+  int32_t phase0_h, phase0_w, nphase_w, nphase, m_total;
   int32_t out_step_h, out_step_w, q0_h, q0_w;
   int32_t qn_h, qn_w, in0_h, in0_w;
   int32_t in_dphase_h, in_dphase_w, in_step_h, in_step_w;
@@ -24,9 +26,15 @@ struct SegDev {
   int32_t tap_ap;
   int32_t ntw, off0_h, doff_h, off0_w, doff_w, kh0, dkh, kw0, dkw;
   // floor(v / d) = (v * mul) >> shift for 0 <= v < 2^31, for the divisors
-  // qn_w, qn_h, n (images) and nphase_w of the pixel decomposition
+  // qn_w, qn_h, nphase (phases) and nphase_w of the pixel decomposition
   uint32_t div_mul[4];
   uint32_t div_shift[4];
+  // ptab >= 0: a listed segment.  Pixel m is image m / per_img (divisor 2 of
+  // the magic numbers above) and entry ptab + m mod per_img of the pixel
+  // table, (oh << 16) | ow, reading input (in0_h + oh, in0_w + ow) + tap
+  // offset (a stride-1 dilated conv with in0 = -pad).
+  int32_t ptab, per_img;
+  int32_t plan;  // entry of the per-plan pointers of GemmArgs (0 outside a group)
 };
 
 // Multiplier and shift of the division by d (1 <= d < 2^31) for dividends
@@ -47,20 +55,26 @@ struct TapDev {
 };
 constexpr int kMaxLdsTaps = 64;  // taps per segment staged in LDS (more: scalar loads)
 
-// One workgroup's job: GEMM tile (m0, n0) of segment seg, over the input
-// channel blocks of K slice ks (of GemmArgs::ksplit).
+// One workgroup's job: GEMM tile of pixels [m0, m1) (at most BM of them) and
+// output channels from n0 of segment seg, over the input channel blocks of K
+// slice ks (of GemmArgs::ksplit), with the taps [tap_begin, tap_begin +
+// tap_count) of the tap list (the segment's taps, or a listed tile's own).
 struct WorkDev {
-  int32_t seg, m0, n0, ks;
+  int32_t seg, m0, m1, n0, ks, tap_begin, tap_count, pad;
 };
 
+constexpr int kMaxGroup = 8;  // plans of one grouped launch (huge2_group)
 struct GemmArgs {
-  const void* x;      // input, channel-contiguous: [n][h][w][cin]
-  const void* wp;     // packed weights: [slot][cout_pad][cin_pad]
-  const float* bias;  // [cout / bias_div] or null: output channel ch takes bias[ch / bias_div]
-  void* y;            // output, NCHW or NHWC
+  const void* x;  // input, channel-contiguous: [n][h][w][cin]
+  // Per plan of a grouped launch (entry 0 alone for a single plan); a
+  // segment's `plan` field selects the entry.
+  const void* wp[kMaxGroup];     // packed weights: [slot][cout_pad][cin_pad]
+  const float* bias[kMaxGroup];  // [cout / bias_div] or null: channel ch takes bias[ch / bias_div]
+  void* y[kMaxGroup];            // output, NCHW or NHWC
   const SegDev* segs;
   const TapDev* taps;
   const WorkDev* works;
+  const uint32_t* ptab;        // pixel table of listed segments
   uint32_t x_bytes, wp_bytes;  // buffer extents (< 2^31)
   int32_t n_works;
   int32_t n, h, w, cin;       // cin: channels per input pixel, a multiple of 16 bytes
@@ -106,6 +120,9 @@ enum TileCfg {
   TILE_SW_64x128_K2 = 6,   // as TILE_SW_64x128, two K groups (8 waves)
   TILE_SW_128x128_K2 = 7,  // split-wave: 4 waves of 128 x 32 channels, two K groups
   TILE_SW_128x256 = 8,   // split-wave: 8 waves of 128 x 32 channels
+  TILE_SW_128x256_W4 = 9,   // split-wave: 4 waves of 128 x 64 channels
+  TILE_SW_128x256_W4D4 = 10,  // as 9, four stages in flight
+  TILE_SW_128x256_K2 = 11,  // as 9, two K groups (8 waves), two stages in flight
 };
 constexpr TileShape kTiles[] = {
     {128, 128, 4, 2, 128, 2, 2, 0},     // TILE_128x128
@@ -117,6 +134,9 @@ constexpr TileShape kTiles[] = {
     {64, 128, 1, 4, 128, 4, 1, 1, 2},   // TILE_SW_64x128_K2
     {128, 128, 1, 4, 128, 3, 1, 1, 2},  // TILE_SW_128x128_K2
     {128, 256, 1, 8, 128, 3, 1, 1, 1},  // TILE_SW_128x256
+    {128, 256, 1, 4, 128, 3, 1, 1, 1},  // TILE_SW_128x256_W4
+    {128, 256, 1, 4, 128, 4, 1, 1, 1},  // TILE_SW_128x256_W4D4
+    {128, 256, 1, 4, 128, 2, 1, 1, 2},  // TILE_SW_128x256_K2
 };
 // A split-K plan may switch from the two-K-group 64 x 128 tile to its
 // one-group form after the work list and the weight packing were laid out for

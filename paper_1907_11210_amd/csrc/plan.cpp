@@ -281,4 +281,78 @@ bool build_shape(const huge2_conv_desc& d, bool transposed, int class_split, int
   return true;
 }
 
+bool build_listed(const huge2_conv_desc& d, int bm, ListedShape* out) {
+  if (d.stride_h != 1 || d.stride_w != 1 || (d.dil_h == 1 && d.dil_w == 1)) return false;
+  if ((long long)d.r * d.s > 64 || bm < 1) return false;
+  int ho, wo;
+  if (!output_dims(d, false, &ho, &wo) || ho >= 65536 || wo >= 65536) return false;
+  // per axis: the in-range taps of each output coordinate as a bit mask, and
+  // the bands (maximal runs of equal masks)
+  auto axis = [](int out_size, int in_size, int ksize, int pad, int dil, std::vector<uint64_t>* mask,
+                 std::vector<int>* band_start) {
+    mask->assign(out_size, 0);
+    band_start->clear();
+    for (int o = 0; o < out_size; ++o) {
+      for (int k = 0; k < ksize; ++k) {
+        const long long i = (long long)o - pad + (long long)k * dil;
+        if (i >= 0 && i < in_size) (*mask)[o] |= 1ull << k;
+      }
+      if (o == 0 || (*mask)[o] != (*mask)[o - 1]) band_start->push_back(o);
+    }
+    band_start->push_back(out_size);
+  };
+  std::vector<uint64_t> mh, mw;
+  std::vector<int> bh, bw;
+  axis(ho, d.h, d.r, d.pad_h, d.dil_h, &mh, &bh);
+  axis(wo, d.w, d.s, d.pad_w, d.dil_w, &mw, &bw);
+  out->pix.clear();
+  out->tile_taps.clear();
+  out->pix.reserve((size_t)ho * wo);
+  const int nbh = (int)bh.size() - 1, nbw = (int)bw.size() - 1;
+  for (int a = 0; a < nbh; ++a) {
+    for (int bi = 0; bi < nbw; ++bi) {
+      const int b = (a % 2 == 0) ? bi : nbw - 1 - bi;  // snake order over the band grid
+      // the cell's pixels by phase view, then by position in the view
+      for (int ph = 0; ph < d.dil_h; ++ph)
+        for (int pw = 0; pw < d.dil_w; ++pw)
+          for (int oh = bh[a]; oh < bh[a + 1]; ++oh) {
+            if (oh % d.dil_h != ph) continue;
+            for (int ow = bw[b]; ow < bw[b + 1]; ++ow)
+              if (ow % d.dil_w == pw) out->pix.push_back(((uint32_t)oh << 16) | (uint32_t)ow);
+          }
+    }
+  }
+  const int per_img = (int)out->pix.size();
+  int64_t nz = 0;
+  for (int o = 0; o < ho; ++o) nz += __builtin_popcountll(mh[o]);
+  int64_t nzw = 0;
+  for (int o = 0; o < wo; ++o) nzw += __builtin_popcountll(mw[o]);
+  out->nonzero_macs = (int64_t)d.n * d.c_in * d.c_out * nz * nzw;
+  out->issued_rows_taps = 0;
+  for (int t0 = 0; t0 < per_img; t0 += bm) {
+    std::vector<uint8_t> used((size_t)d.r * d.s, 0);
+    for (int i = t0; i < std::min(per_img, t0 + bm); ++i) {
+      const uint64_t h = mh[out->pix[i] >> 16], w = mw[out->pix[i] & 0xffff];
+      for (int kh = 0; kh < d.r; ++kh)
+        if (h >> kh & 1)
+          for (int kw = 0; kw < d.s; ++kw)
+            if (w >> kw & 1) used[(size_t)kh * d.s + kw] = 1;
+    }
+    std::vector<huge2_tap> taps;
+    for (int kh = 0; kh < d.r; ++kh)
+      for (int kw = 0; kw < d.s; ++kw)
+        if (used[(size_t)kh * d.s + kw]) {
+          huge2_tap t;
+          t.kh = kh;
+          t.kw = kw;
+          t.off_h = kh * d.dil_h;
+          t.off_w = kw * d.dil_w;
+          taps.push_back(t);
+        }
+    out->issued_rows_taps += (int64_t)d.n * bm * (int64_t)taps.size();
+    out->tile_taps.push_back(std::move(taps));
+  }
+  return true;
+}
+
 }  // namespace huge2

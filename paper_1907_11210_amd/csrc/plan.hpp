@@ -66,4 +66,23 @@ huge2_status validate_desc(const huge2_conv_desc* d, bool transposed);
 bool build_shape(const huge2_conv_desc& d, bool transposed, int class_split, int bm,
                  PlanShape* out);
 
+// Listed form of a stride-1 dilated conv (section 3.2.2).  The output pixels
+// of one image are listed in this order: the 2-D border cells (products of
+// the per-axis bands on which the set of in-range taps is constant) in snake
+// order over the grid of bands, and inside a cell by phase view (oh mod
+// dil_h, ow mod dil_w), then by position in the view.  Every phase view's
+// pixels with one tap set are thus one run of the list, and each tile of bm
+// consecutive pixels uses the union of its pixels' tap sets (adjacent cells
+// in snake order have nested tap sets for three bands per axis, so that union
+// is the larger cell's set).  The same list serves every image.
+struct ListedShape {
+  std::vector<uint32_t> pix;                     // per image: (oh << 16) | ow
+  std::vector<std::vector<huge2_tap>> tile_taps; // per tile of bm pixels of one image
+  int64_t nonzero_macs = 0;
+  int64_t issued_rows_taps = 0;  // sum over tiles (all images) of bm x taps
+};
+// False when the form does not apply (transposed, a stride above 1, dilation
+// 1 on both axes, outputs of 65536 rows or columns, more than 64 taps).
+bool build_listed(const huge2_conv_desc& d, int bm, ListedShape* out);
+
 }  // namespace huge2

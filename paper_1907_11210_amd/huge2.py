@@ -32,7 +32,9 @@ EXPORTED = (
     "huge2_plan_describe", "huge2_plan_macs",
     "huge2_wgrad_plan_create", "huge2_wgrad_execute", "huge2_wgrad_plan_destroy",
     "huge2_conv2d_transpose_wgrad", "huge2_conv2d_dilated_wgrad",
+    "huge2_group_create", "huge2_group_execute", "huge2_group_destroy",
 )
+MAX_GROUP = 8
 
 
 class Huge2Error(RuntimeError):
@@ -93,6 +95,9 @@ def lib():
         L.huge2_wgrad_plan_destroy.argtypes = [vp]
         L.huge2_conv2d_transpose_wgrad.argtypes = [dp, vp, vp, vp, vp]
         L.huge2_conv2d_dilated_wgrad.argtypes = [dp, vp, vp, vp, vp]
+        L.huge2_group_create.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, vp]
+        L.huge2_group_execute.argtypes = [vp, vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp]
+        L.huge2_group_destroy.argtypes = [vp]
         for name in EXPORTED[1:]:
             getattr(L, name).restype = ctypes.c_int
         L.huge2_plan_kernel.restype = ctypes.c_char_p
@@ -240,6 +245,24 @@ def huge2_conv2d_dilated_wgrad(desc, x_ptr, dy_ptr, dw_ptr, stream=0):
 
 
 # ---- torch conveniences -----------------------------------------------------
+
+def huge2_group_create(plans, stream=0):
+    arr = (ctypes.c_void_p * len(plans))(*plans)
+    out = ctypes.c_void_p()
+    _check(lib().huge2_group_create(ctypes.byref(out), arr, len(plans), stream),
+           "huge2_group_create")
+    return out.value
+
+
+def huge2_group_execute(group, x_ptr, bias_ptrs, y_ptrs, stream=0):
+    ys = (ctypes.c_void_p * len(y_ptrs))(*y_ptrs)
+    bs = None if bias_ptrs is None else (ctypes.c_void_p * len(bias_ptrs))(*bias_ptrs)
+    _check(lib().huge2_group_execute(group, x_ptr, bs, ys, stream), "huge2_group_execute")
+
+
+def huge2_group_destroy(group):
+    _check(lib().huge2_group_destroy(group), "huge2_group_destroy")
+
 
 def _torch():
     import torch
@@ -506,6 +529,49 @@ class Plan:
         if self._plan is not None:
             huge2_plan_destroy(self._plan)
             self._plan = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Group:
+    """Several :class:`Plan` objects of one input run as one launch
+    (huge2_group_create); :meth:`__call__` enqueues huge2_group_execute on the
+    current stream.  The plans must stay open while the group is used."""
+
+    def __init__(self, plans):
+        torch = _torch()
+        self.plans = list(plans)
+        self._group = None
+        self._group = huge2_group_create([p._plan for p in self.plans],
+                                         torch.cuda.current_stream(self.plans[0].device).cuda_stream)
+
+    def __call__(self, x, biases=None, outs=None):
+        torch = _torch()
+        p0 = self.plans[0]
+        _check_tensor(x, "x", p0.device)
+        if tuple(x.shape) != p0.x_shape or x.dtype != p0.dtype:
+            raise ValueError("x does not match the plans")
+        if outs is None:
+            outs = [torch.empty(p.out_shape, dtype=x.dtype, device=x.device) for p in self.plans]
+        for p, y in zip(self.plans, outs):
+            _check_tensor(y, "out", p0.device)
+            if tuple(y.shape) != p.out_shape or y.dtype != p.dtype:
+                raise ValueError("out does not match its plan")
+        bias_ptrs = None
+        if biases is not None:
+            bias_ptrs = [_bias_ptr(b, x) for b in biases]
+        huge2_group_execute(self._group, x.data_ptr(), bias_ptrs, [y.data_ptr() for y in outs],
+                            _stream(x))
+        return outs
+
+    def close(self):
+        if self._group is not None:
+            huge2_group_destroy(self._group)
+            self._group = None
 
     def __del__(self):
         try:

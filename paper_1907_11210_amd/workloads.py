@@ -143,6 +143,8 @@ WORKLOADS = {
     "dcgan_generator": generator_layers("bf16"),
     "dcgan_generator_b1": generator_layers("bf16", batch=1),
 }
+# layers that read one input and run as one grouped launch (huge2_group)
+GROUPED = ("aspp",)
 CHAINED = ("dcgan", "dcgan_f32", "table1_dcgan", "table1_cgan", "dcgan_dgrad", "dcgan_generator",
            "dcgan_generator_b1")
 

@@ -82,12 +82,23 @@ def _x_shape(layer):
     return (layer.n, layer.h, layer.w, layer.c_in)
 
 
-def run_gpu(layer, xq, wq, bias=None, one_shot=False, plan=None):
-    """Run the layer on the GPU; returns the output as a float64 NCHW array."""
+def run_gpu(layer, xq, wq, bias=None, one_shot=False, plan=None, prefill_nan=False):
+    """Run the layer on the GPU; returns the output as a float64 NCHW array.
+    prefill_nan: the plan path writes into an output filled with NaN first, so
+    that an element the kernels never write stays NaN."""
     dev = torch.device("cuda", 0)
     x_dev = wl.to_layout(xq, layer.layout).to(dev)
     w_dev = wq.contiguous().to(dev)
     b_dev = None if bias is None else bias.to(torch.float32).to(dev)
+    if prefill_nan and not one_shot:
+        p = plan if plan is not None else make_plan(layer, w_dev)
+        y = torch.full(p.out_shape, float("nan"), dtype=xq.dtype, device=dev)
+        p(x_dev, b_dev, out=y)
+        if plan is None:
+            torch.cuda.synchronize()
+            p.close()
+        torch.cuda.synchronize()
+        return wl.from_layout(y.cpu(), layer.layout).double().numpy()
     if one_shot:
         if layer.transposed:
             y = h2.conv2d_transpose(x_dev, w_dev, b_dev, layer.stride, layer.pad, layer.out_pad,

@@ -171,3 +171,18 @@ def test_weight_gradient_entry_points_validate_without_gpu(L, monkeypatch):
     monkeypatch.setenv("HUGE2_FAULT", "alloc")
     assert L.huge2_wgrad_plan_create(ctypes.byref(plan), ctypes.byref(d), 1) == h2.HUGE2_ERR_ALLOC
     assert plan.value is None
+
+
+def test_group_entry_points_validate_without_gpu(L):
+    """Grouped launches reject NULL and out-of-range arguments before any HIP call."""
+    import ctypes
+    out = ctypes.c_void_p()
+    assert L.huge2_group_create(None, None, 1, None) == h2.HUGE2_ERR_INVALID_ARG
+    assert L.huge2_group_create(ctypes.byref(out), None, 1, None) == h2.HUGE2_ERR_INVALID_ARG
+    arr = (ctypes.c_void_p * 1)(None)
+    assert L.huge2_group_create(ctypes.byref(out), arr, 1, None) == h2.HUGE2_ERR_INVALID_ARG
+    assert L.huge2_group_create(ctypes.byref(out), arr, 0, None) == h2.HUGE2_ERR_INVALID_ARG
+    assert L.huge2_group_create(ctypes.byref(out), arr, 9, None) == h2.HUGE2_ERR_INVALID_ARG
+    assert out.value is None
+    assert L.huge2_group_execute(None, None, None, None, None) == h2.HUGE2_ERR_INVALID_ARG
+    assert L.huge2_group_destroy(None) == h2.HUGE2_OK

@@ -254,14 +254,16 @@ FULL = ["convt_small", "dcgan_f32", "dcgan", "convt_odd", "aspp", "fcn_upsample"
 @pytest.mark.parametrize("wname", FULL)
 def test_workload_full_size_sampled(wname):
     """Full-size workloads, plan path (as timed by the benchmark), checked on
-    sampled outputs that cover every phase, border and first/last channel."""
+    sampled outputs that cover every phase, border and first/last channel;
+    the output starts as NaN, so the finiteness check over the whole tensor
+    shows that every element was written."""
     items = wl.generate(wname, seed=0)
     for i, (layer, x, w) in enumerate(items):
         if x is None:  # chained layers 2-4: standalone input of the chained shape
             x = wl.layer_input(layer, seed=100 + i, std=0.25)
         P.say("case", wname, layer)
         xq, wq = P.quantise(x, layer.dtype), P.quantise(w, layer.dtype)
-        y = P.run_gpu(layer, xq, wq)
+        y = P.run_gpu(layer, xq, wq, prefill_nan=True)
         idx = P.sample_indices(layer, 3000, seed=i)
         ref = P.oracle_points(layer, xq, wq, idx)
         absref = P.oracle_points(layer, xq, wq, idx, absolute=True)
@@ -558,3 +560,100 @@ def test_gather_forms(layer, gather, monkeypatch):
         assert plan.stages_input
     finally:
         plan.close()
+
+
+LISTED_LAYERS = [
+    L("li_aspp_d6", False, 2, 64, 64, 64, 48, 3, 3, 1, 6, 0, 6, "NHWC", "bf16"),
+    L("li_aspp_d24", False, 1, 64, 64, 64, 48, 3, 3, 1, 24, 0, 24, "NHWC", "bf16"),
+    # an image whose pixel count is no multiple of the tile height: the last
+    # tile of each image is partial and must not touch the next image
+    L("li_ragged_img", False, 3, 40, 13, 11, 72, 3, 3, 1, 3, 0, 3, "NHWC", "bf16"),
+    # dilation larger than half the image: a band with only the centre tap
+    L("li_wide_dil", False, 2, 24, 9, 10, 40, 3, 3, 1, 7, 0, 7, "NHWC", "bf16"),
+    L("li_aniso_5x3", False, 2, 16, 12, 17, 36, 5, 3, 1, 2, 0, 2, "NCHW", "f32"),
+    L("li_valid_pad0", False, 1, 32, 15, 15, 64, 3, 3, 1, 0, 0, 3, "NHWC", "f32"),
+    L("li_c300", False, 1, 300, 20, 20, 260, 3, 3, 1, 4, 0, 4, "NHWC", "bf16"),
+]
+
+
+@pytest.mark.parametrize("listed", [0, 1])
+@pytest.mark.parametrize("layer", LISTED_LAYERS, ids=lambda l: l.name)
+def test_listed_form(layer, listed, monkeypatch):
+    """Stride-1 dilated convs through the listed form (per-image pixel list in
+    border-cell and phase-view order, each tile with the union of its pixels'
+    taps) and through the phase-view segments: both match the oracle and write
+    every output element."""
+    monkeypatch.setenv("HUGE2_LISTED", str(listed))
+    layer = layer.with_(act="relu")
+    P.say("case", layer, "HUGE2_LISTED", listed)
+    xq, wq = _inputs(layer, seed=29)
+    bias = torch.linspace(-0.5, 0.5, layer.c_out)
+    ref = P.oracle_full(layer, xq, wq, bias)
+    absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
+    y = P.run_gpu(layer, xq, wq, bias, prefill_nan=True)
+    P.check(y, ref, absref, layer.dtype, layer.name)
+    plan = P.make_plan(layer, wq.contiguous().to(torch.device("cuda", 0)))
+    try:
+        assert plan.kernel.endswith("listed") == bool(listed), plan.kernel
+    finally:
+        plan.close()
+
+
+GROUP_SETS = [
+    # the pyramid's four branches at reduced size (listed form)
+    [L("gr_d%d" % d, False, 2, 96, 24, 24, 64, 3, 3, 1, d, 0, d, "NHWC", "bf16") for d in (2, 3, 5, 8)],
+    # branches of different kinds and paddings on one input, fp32
+    [L("gr_f32_a", False, 1, 24, 13, 11, 40, 3, 3, 1, 1, 0, 1, "NHWC", "f32"),
+     L("gr_f32_b", False, 1, 24, 13, 11, 40, 3, 3, 1, 2, 0, 2, "NHWC", "f32"),
+     L("gr_f32_c", False, 1, 24, 13, 11, 40, 3, 3, 1, 3, 0, 3, "NHWC", "f32")],
+]
+
+
+@pytest.mark.parametrize("layers", GROUP_SETS, ids=["aspp_reduced", "mixed_f32"])
+def test_grouped_launch(layers):
+    """Several plans of one input in one launch (huge2_group): every output
+    matches the oracle, equals its own plan's output bitwise, and is written
+    in full (NaN-prefilled outputs keep no NaN)."""
+    dev = torch.device("cuda", 0)
+    x = P.quantise(wl.layer_input(layers[0], seed=41), layers[0].dtype)
+    x_dev = wl.to_layout(x, layers[0].layout).to(dev)
+    plans, ws, biases = [], [], []
+    for i, layer in enumerate(layers):
+        P.say("case group", layer)
+        wq = P.quantise(wl.random_weight(layer, seed=42 + i, std=0.05), layer.dtype)
+        ws.append(wq)
+        plans.append(P.make_plan(layer, wq.contiguous().to(dev)))
+        biases.append(torch.linspace(-0.5, 0.5 + i, layer.c_out).to(dev))
+    group = h2.Group(plans)
+    try:
+        outs = [torch.full(p.out_shape, float("nan"), dtype=x.dtype, device=dev) for p in plans]
+        group(x_dev, biases, outs)
+        single = [p(x_dev, b) for p, b in zip(plans, biases)]
+        torch.cuda.synchronize()
+        for layer, wq, b, y, y1 in zip(layers, ws, biases, outs, single):
+            iv = torch.int16 if y.dtype == torch.bfloat16 else torch.int32
+            assert torch.equal(y.view(iv), y1.view(iv)), layer.name
+            yn = wl.from_layout(y.cpu(), layer.layout).double().numpy()
+            ref = P.oracle_full(layer, x, wq, b.cpu())
+            absref = P.oracle_full(layer, x, wq, b.cpu(), absolute=True)
+            P.check(yn, ref, absref, layer.dtype, layer.name + " grouped")
+    finally:
+        group.close()
+        for p in plans:
+            p.close()
+
+
+def test_group_rejects_unlike_plans():
+    """Plans of different input shapes cannot share a launch."""
+    dev = torch.device("cuda", 0)
+    a = L("ga", False, 1, 16, 8, 8, 32, 3, 3, 1, 1, 0, 1, "NHWC", "bf16")
+    b = a.with_(name="gb", h=9)
+    pa = P.make_plan(a, P.quantise(wl.random_weight(a, seed=1), "bf16").to(dev))
+    pb = P.make_plan(b, P.quantise(wl.random_weight(b, seed=2), "bf16").to(dev))
+    try:
+        with pytest.raises(h2.Huge2Error) as e:
+            h2.Group([pa, pb])
+        assert e.value.status == h2.HUGE2_ERR_UNSUPPORTED
+    finally:
+        pa.close()
+        pb.close()

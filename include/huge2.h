@@ -159,6 +159,24 @@ huge2_status huge2_plan_destroy(huge2_plan* plan);
 huge2_status huge2_conv2d_transpose(const huge2_conv_desc* desc, const void* x, const void* w,
                                     const float* bias, void* y, void* hip_stream);
 
+/* The one-shot transposed convolution for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the same computation and arguments as
+ * huge2_conv2d_transpose, but every device buffer the call needs (the packed
+ * sub-kernel weights, the work list, the input staging and the K-slice
+ * partials) is carved from a static device array of 64 MiB that the library
+ * holds on each GPU it runs on until the process ends; no hipMalloc,
+ * hipFree or other allocating routine is called (host memory holds the
+ * plan's description during the call, which waits for hip_stream as plan
+ * creation does).  Every call on one GPU uses that GPU's same array: calls
+ * that overlap on one GPU (other streams, other host threads) race and must
+ * be ordered by the caller; calls on one stream are ordered already.  A
+ * layer whose buffers exceed the 64 MiB returns HUGE2_ERR_UNSUPPORTED with y
+ * untouched.  Errors otherwise as huge2_conv2d_transpose. */
+huge2_status huge2_conv2d_transpose_noalloc(const huge2_conv_desc* desc, const void* x,
+                                            const void* w, const float* bias, void* y,
+                                            void* hip_stream);
+
 /* One-shot dilated convolution (Algorithm 2 semantics; stride 1 is computed
  * by dil_h x dil_w phase views, stride > 1 by the same GEMM core over a
  * direct gather).  w is [c_out][c_in][r][s]; desc->out_pad_* must be 0. */

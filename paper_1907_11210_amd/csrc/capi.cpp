@@ -11,6 +11,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <queue>
 #include <vector>
@@ -20,6 +21,19 @@
 #include "plan.hpp"
 
 using namespace huge2;
+
+// Where a plan's device buffers come from: hipMalloc, hipMallocAsync on the
+// plan's stream (stream_ordered, the one-shot entry points), or a bump
+// allocation from a caller-provided region (arena, the no-allocation entry
+// point), which the plan never frees.
+struct Arena {
+  char* base;
+  size_t cap, used;
+};
+struct Mem {
+  bool stream_ordered = false;
+  Arena* arena = nullptr;
+};
 
 struct huge2_plan {
   huge2_conv_desc desc;
@@ -38,7 +52,7 @@ struct huge2_plan {
   TapDev* d_taps;
   WorkDev* d_works;
   const uint32_t* d_ptab;  // pixel table of a listed plan (or null)
-  bool stream_ordered;  // buffers came from hipMallocAsync on alloc_stream
+  Mem mem;  // where the buffers came from (see Mem)
   hipStream_t alloc_stream;
   int64_t nonzero_macs, issued_macs;
   bool ztile;   // all-taps form for few output channels (no GEMM work list)
@@ -604,7 +618,9 @@ void free_buffers(huge2_plan* p) {
   void* bufs[5] = {p->wp, p->meta, p->xs, p->part, p->zbuf};
   for (void* b : bufs) {
     if (!b) continue;
-    if (p->stream_ordered)
+    if (p->mem.arena)
+      continue;  // a region the plan does not own
+    if (p->mem.stream_ordered)
       (void)hipFreeAsync(b, p->alloc_stream);
     else
       (void)hipFree(b);
@@ -620,8 +636,16 @@ void free_buffers(huge2_plan* p) {
 huge2_status dev_alloc(huge2_plan* p, void** out, size_t bytes) {
   *out = nullptr;
   if (bytes == 0) return HUGE2_OK;
+  if (p->mem.arena) {
+    Arena& a = *p->mem.arena;
+    const size_t at = (a.used + 255) / 256 * 256;
+    if (at > a.cap || bytes > a.cap - at) return HUGE2_ERR_UNSUPPORTED;
+    *out = a.base + at;
+    a.used = at + bytes;
+    return HUGE2_OK;
+  }
   if (fault("alloc")) return HUGE2_ERR_ALLOC;
-  hipError_t e = p->stream_ordered ? hipMallocAsync(out, bytes, p->alloc_stream)
+  hipError_t e = p->mem.stream_ordered ? hipMallocAsync(out, bytes, p->alloc_stream)
                                    : hipMalloc(out, bytes);
   if (e != hipSuccess) {
     *out = nullptr;
@@ -636,7 +660,7 @@ huge2_status dev_alloc(huge2_plan* p, void** out, size_t bytes) {
 // of 128-byte K stages for qp); the three kernels read the NCHW input
 // directly, so nothing is staged.
 huge2_status create_direct(huge2_plan** out, const huge2_conv_desc& d, int transposed,
-                          const void* w, hipStream_t stream, bool stream_ordered, const ZArgs* zp,
+                          const void* w, hipStream_t stream, Mem mem, const ZArgs* zp,
                           const RpArgs* rp, const QArgs* qp, int64_t issued) {
   PlanShape shape;
   if (!build_shape(d, true, 2, 128, &shape)) return HUGE2_ERR_INVALID_ARG;
@@ -655,7 +679,7 @@ huge2_status create_direct(huge2_plan** out, const huge2_conv_desc& d, int trans
   p->cout_pad = zp ? zp->cout_pad : qp ? qp->cout_pad : kRpCh;
   p->x_bytes = (size_t)d.n * d.c_in * d.h * d.w * esz;
   p->wp_bytes = (size_t)d.r * d.s * p->cout_pad * p->cin_pad * esz;
-  p->stream_ordered = stream_ordered;
+  p->mem = mem;
   p->alloc_stream = stream;
   p->nonzero_macs = shape.nonzero_macs;
   p->issued_macs = issued;
@@ -736,7 +760,7 @@ bool two_pass_shape(const huge2_conv_desc& d, bool transposed, huge2_conv_desc* 
 }
 
 huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int transposed,
-                         const void* w, hipStream_t stream, bool stream_ordered);
+                         const void* w, hipStream_t stream, Mem mem);
 
 // The gather form applies to NCHW convs (dilated or strided) with few input
 // channels, c_in*r*s <= 64 and r*s > 1 (a discriminator's RGB input layer,
@@ -763,9 +787,9 @@ bool gather_shape(const huge2_conv_desc& d, bool transposed, huge2_conv_desc* d1
 }
 
 huge2_status create_gather(huge2_plan** out, const huge2_conv_desc& d, const huge2_conv_desc& d1,
-                           const void* w, hipStream_t stream, bool stream_ordered) {
+                           const void* w, hipStream_t stream, Mem mem) {
   huge2_plan* inner = nullptr;
-  huge2_status st = create_impl(&inner, &d1, 0, w, stream, stream_ordered);
+  huge2_status st = create_impl(&inner, &d1, 0, w, stream, mem);
   if (st != HUGE2_OK) return st;
   if (!inner->staged || inner->inner) {  // the pointwise GEMM must read a staged input
     free_buffers(inner);
@@ -782,7 +806,7 @@ huge2_status create_gather(huge2_plan** out, const huge2_conv_desc& d, const hug
   p->transposed = 0;
   p->bias_div = 1;
   p->ksplit = 1;
-  p->stream_ordered = stream_ordered;
+  p->mem = mem;
   p->alloc_stream = stream;
   output_dims(d, false, &p->ho, &p->wo);
   p->inner = inner;
@@ -797,9 +821,9 @@ huge2_status create_gather(huge2_plan** out, const huge2_conv_desc& d, const hug
 }
 
 huge2_status create_two_pass(huge2_plan** out, const huge2_conv_desc& d, const huge2_conv_desc& d1,
-                             const void* w, hipStream_t stream, bool stream_ordered) {
+                             const void* w, hipStream_t stream, Mem mem) {
   huge2_plan* inner = nullptr;
-  huge2_status st = create_impl(&inner, &d1, 1, w, stream, stream_ordered);
+  huge2_status st = create_impl(&inner, &d1, 1, w, stream, mem);
   if (st != HUGE2_OK) return st;
   huge2_plan* p = new (std::nothrow) huge2_plan();
   if (!p) {
@@ -811,7 +835,7 @@ huge2_status create_two_pass(huge2_plan** out, const huge2_conv_desc& d, const h
   p->transposed = 1;
   p->bias_div = 1;
   p->ksplit = 1;
-  p->stream_ordered = stream_ordered;
+  p->mem = mem;
   p->alloc_stream = stream;
   output_dims(d, true, &p->ho, &p->wo);
   p->inner = inner;
@@ -831,7 +855,7 @@ huge2_status create_two_pass(huge2_plan** out, const huge2_conv_desc& d, const h
 }
 
 huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int transposed,
-                         const void* w, hipStream_t stream, bool stream_ordered) {
+                         const void* w, hipStream_t stream, Mem mem) {
   if (!out) return HUGE2_ERR_INVALID_ARG;
   *out = nullptr;
   if (transposed != 0 && transposed != 1) return HUGE2_ERR_INVALID_ARG;
@@ -845,23 +869,23 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   const huge2_conv_desc& d = dd;
   {
     huge2_conv_desc d1;
-    if (two_pass_shape(d, tr, &d1)) return create_two_pass(out, d, d1, w, stream, stream_ordered);
-    if (gather_shape(d, tr, &d1)) return create_gather(out, d, d1, w, stream, stream_ordered);
+    if (two_pass_shape(d, tr, &d1)) return create_two_pass(out, d, d1, w, stream, mem);
+    if (gather_shape(d, tr, &d1)) return create_gather(out, d, d1, w, stream, mem);
   }
 
   {
     ZArgs z;
     int64_t z_issued = 0;
     if (ztile_shape(d, tr, &z, &z_issued))
-      return create_direct(out, d, transposed, w, stream, stream_ordered, &z, nullptr, nullptr,
+      return create_direct(out, d, transposed, w, stream, mem, &z, nullptr, nullptr,
                            z_issued);
     RpArgs rp;
     if (rowphase_shape(d, tr, &rp, &z_issued))
-      return create_direct(out, d, transposed, w, stream, stream_ordered, nullptr, &rp, nullptr,
+      return create_direct(out, d, transposed, w, stream, mem, nullptr, &rp, nullptr,
                            z_issued);
     QArgs q;
     if (quad_shape(d, tr, &q, &z_issued))
-      return create_direct(out, d, transposed, w, stream, stream_ordered, nullptr, nullptr, &q,
+      return create_direct(out, d, transposed, w, stream, mem, nullptr, nullptr, &q,
                            z_issued);
   }
 
@@ -902,7 +926,7 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   p->x_bytes = (size_t)d.n * d.h * d.w * p->c_stride * esz;
   p->cin_pad = round_up(d.c_in, bk);
   p->cout_pad = round_up(d.c_out, bn);
-  p->stream_ordered = stream_ordered;
+  p->mem = mem;
   p->alloc_stream = stream;
   p->nonzero_macs = shape.nonzero_macs;
 
@@ -1334,10 +1358,64 @@ huge2_status one_shot(const huge2_conv_desc* desc, int transposed, const void* x
   if (st != HUGE2_OK) return st;
   if (!x || !w || !y || x == y) return HUGE2_ERR_INVALID_ARG;
   huge2_plan* p = nullptr;
-  st = create_impl(&p, desc, transposed, w, stream, true);
+  Mem mem;
+  mem.stream_ordered = true;
+  st = create_impl(&p, desc, transposed, w, stream, mem);
   if (st != HUGE2_OK) return st;
   st = execute_impl(p, x, bias, y, stream);
   free_buffers(p);  // stream-ordered: released after the enqueued work
+  delete p;
+  return st;
+}
+
+// The no-allocation form of the one-shot transposed conv: every device
+// buffer the plan needs (packed weights, work list, staging, K-slice
+// partials) is carved from this device's copy of `scratch`, whose device
+// address hipGetSymbolAddress gives once per device (in host code the
+// array's name is not a device address).
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+constexpr int kMaxDevices = 64;
+std::once_flag g_scratch_once[kMaxDevices];
+void* g_scratch_ptr[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+huge2_status scratch_region(void** ptr) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return HUGE2_ERR_HIP;
+  }
+  std::call_once(g_scratch_once[dev], [dev] {
+    void* p = nullptr;
+    g_scratch_err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    g_scratch_ptr[dev] = g_scratch_err[dev] == hipSuccess ? p : nullptr;
+  });
+  if (g_scratch_err[dev] != hipSuccess || !g_scratch_ptr[dev]) return HUGE2_ERR_HIP;
+  *ptr = g_scratch_ptr[dev];
+  return HUGE2_OK;
+}
+
+huge2_status one_shot_noalloc(const huge2_conv_desc* desc, const void* x, const void* w,
+                              const float* bias, void* y, hipStream_t stream) {
+  huge2_status st = validate_desc(desc, true);
+  if (st != HUGE2_OK) return st;
+  if (!x || !w || !y || x == y) return HUGE2_ERR_INVALID_ARG;
+  void* base = nullptr;
+  if ((st = scratch_region(&base)) != HUGE2_OK) return st;
+  Arena arena{(char*)base, kScratchBytes, 0};
+  Mem mem;
+  mem.arena = &arena;
+  huge2_plan* p = nullptr;
+  st = create_impl(&p, desc, 1, w, stream, mem);
+  if (st != HUGE2_OK) return st;
+  st = execute_impl(p, x, bias, y, stream);
+  free_buffers(p);  // nothing to release: the buffers lie in the scratch region
   delete p;
   return st;
 }
@@ -1664,7 +1742,7 @@ huge2_status huge2_output_shape(const huge2_conv_desc* desc, int32_t transposed,
 huge2_status huge2_plan_create(huge2_plan** out, const huge2_conv_desc* desc, int32_t transposed,
                                const void* w, void* hip_stream) {
   try {
-    return create_impl(out, desc, transposed, w, (hipStream_t)hip_stream, false);
+    return create_impl(out, desc, transposed, w, (hipStream_t)hip_stream, Mem());
   } catch (...) {
     return HUGE2_ERR_ALLOC;
   }
@@ -1719,6 +1797,16 @@ huge2_status huge2_conv2d_transpose(const huge2_conv_desc* desc, const void* x, 
     return one_shot(desc, 1, x, w, bias, y, (hipStream_t)hip_stream);
   } catch (...) {
     return HUGE2_ERR_ALLOC;
+  }
+}
+
+huge2_status huge2_conv2d_transpose_noalloc(const huge2_conv_desc* desc, const void* x,
+                                            const void* w, const float* bias, void* y,
+                                            void* hip_stream) {
+  try {
+    return one_shot_noalloc(desc, x, w, bias, y, (hipStream_t)hip_stream);
+  } catch (...) {
+    return HUGE2_ERR_HIP;
   }
 }
 

@@ -33,6 +33,7 @@ EXPORTED = (
     "huge2_wgrad_plan_create", "huge2_wgrad_execute", "huge2_wgrad_plan_destroy",
     "huge2_conv2d_transpose_wgrad", "huge2_conv2d_dilated_wgrad",
     "huge2_group_create", "huge2_group_execute", "huge2_group_destroy",
+    "huge2_conv2d_transpose_noalloc",
 )
 MAX_GROUP = 8
 
@@ -98,6 +99,7 @@ def lib():
         L.huge2_group_create.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, vp]
         L.huge2_group_execute.argtypes = [vp, vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp]
         L.huge2_group_destroy.argtypes = [vp]
+        L.huge2_conv2d_transpose_noalloc.argtypes = [dp, vp, vp, vp, vp, vp]
         for name in EXPORTED[1:]:
             getattr(L, name).restype = ctypes.c_int
         L.huge2_plan_kernel.restype = ctypes.c_char_p
@@ -181,6 +183,13 @@ def huge2_conv2d_transpose(desc, x_ptr, w_ptr, bias_ptr, y_ptr, stream=0):
                                         ctypes.c_void_p(w_ptr), ctypes.c_void_p(bias_ptr),
                                         ctypes.c_void_p(y_ptr), ctypes.c_void_p(stream)),
            "huge2_conv2d_transpose")
+
+
+def huge2_conv2d_transpose_noalloc(desc, x_ptr, w_ptr, bias_ptr, y_ptr, stream=0):
+    _check(lib().huge2_conv2d_transpose_noalloc(ctypes.byref(desc), ctypes.c_void_p(x_ptr),
+                                                ctypes.c_void_p(w_ptr), ctypes.c_void_p(bias_ptr),
+                                                ctypes.c_void_p(y_ptr), ctypes.c_void_p(stream)),
+           "huge2_conv2d_transpose_noalloc")
 
 
 def huge2_conv2d_dilated(desc, x_ptr, w_ptr, bias_ptr, y_ptr, stream=0):

@@ -50,7 +50,7 @@ def build(force: bool = False) -> str:
 class _Conv(ctypes.Structure):
     _fields_ = [(name, ctypes.c_int) for name in (
         "n", "c_in", "h", "w", "c_out", "r", "s", "stride_h", "stride_w", "pad_h", "pad_w",
-        "out_pad_h", "out_pad_w", "dil_h", "dil_w")]
+        "out_pad_h", "out_pad_w", "dil_h", "dil_w", "groups")]
 
 
 _lib = None
@@ -80,19 +80,22 @@ def _pair(v):
     return (int(v), int(v)) if np.isscalar(v) else (int(v[0]), int(v[1]))
 
 
-def _desc(x_shape, w_shape, transposed, stride, padding, output_padding, dilation):
+def _desc(x_shape, w_shape, transposed, stride, padding, output_padding, dilation, groups=1):
     n, c_in, h, w = x_shape
+    g = int(groups)
     if transposed:
-        wc_in, c_out, r, s = w_shape
+        wc_in, cog, r, s = w_shape
+        c_out = cog * g
     else:
-        c_out, wc_in, r, s = w_shape
+        c_out, cig, r, s = w_shape
+        wc_in = cig * g
     if wc_in != c_in:
         raise ValueError("weight C_in %d does not match input C_in %d" % (wc_in, c_in))
     sh, sw = _pair(stride)
     ph, pw = _pair(padding)
     oph, opw = _pair(output_padding)
     dh, dw = _pair(dilation)
-    return _Conv(n, c_in, h, w, c_out, r, s, sh, sw, ph, pw, oph, opw, dh, dw)
+    return _Conv(n, c_in, h, w, c_out, r, s, sh, sw, ph, pw, oph, opw, dh, dw, g)
 
 
 def _ptr(a):
@@ -107,16 +110,16 @@ def _threads(nthreads):
     return int(nthreads) if nthreads else (os.cpu_count() or 1)
 
 
-def transpose_out_dims(x_shape, w_shape, stride, padding, output_padding=0, dilation=1):
-    d = _desc(x_shape, w_shape, True, stride, padding, output_padding, dilation)
+def transpose_out_dims(x_shape, w_shape, stride, padding, output_padding=0, dilation=1, groups=1):
+    d = _desc(x_shape, w_shape, True, stride, padding, output_padding, dilation, groups)
     ho, wo = ctypes.c_int(), ctypes.c_int()
     if _load().oracle_transpose_out_dims(ctypes.byref(d), ctypes.byref(ho), ctypes.byref(wo)):
         raise ValueError("invalid transposed-conv descriptor")
     return ho.value, wo.value
 
 
-def conv_out_dims(x_shape, w_shape, stride, padding, dilation=1):
-    d = _desc(x_shape, w_shape, False, stride, padding, 0, dilation)
+def conv_out_dims(x_shape, w_shape, stride, padding, dilation=1, groups=1):
+    d = _desc(x_shape, w_shape, False, stride, padding, 0, dilation, groups)
     ho, wo = ctypes.c_int(), ctypes.c_int()
     if _load().oracle_conv_out_dims(ctypes.byref(d), ctypes.byref(ho), ctypes.byref(wo)):
         raise ValueError("invalid conv descriptor")
@@ -124,11 +127,13 @@ def conv_out_dims(x_shape, w_shape, stride, padding, dilation=1):
 
 
 def conv2d_transpose_alg1(x, w, bias=None, stride=1, padding=0, output_padding=0, dilation=1,
-                          nthreads=None):
-    """Transposed conv by zero insertion (Algorithm 1); float64 NCHW in and out."""
+                          nthreads=None, groups=1):
+    """Transposed conv by zero insertion (Algorithm 1); float64 NCHW in and out.
+    groups > 1: w is [C_in, C_out/groups, R, S] and each output channel sums
+    over its group's input channels only."""
     x, w, bias = _f64(x), _f64(w), _f64(bias)
-    d = _desc(x.shape, w.shape, True, stride, padding, output_padding, dilation)
-    ho, wo = transpose_out_dims(x.shape, w.shape, stride, padding, output_padding, dilation)
+    d = _desc(x.shape, w.shape, True, stride, padding, output_padding, dilation, groups)
+    ho, wo = transpose_out_dims(x.shape, w.shape, stride, padding, output_padding, dilation, groups)
     y = np.empty((d.n, d.c_out, ho, wo), dtype=np.float64)
     rc = _load().oracle_conv2d_transpose_alg1(ctypes.byref(d), _ptr(x), _ptr(w), _ptr(bias),
                                               _ptr(y), _threads(nthreads))
@@ -137,11 +142,13 @@ def conv2d_transpose_alg1(x, w, bias=None, stride=1, padding=0, output_padding=0
     return y
 
 
-def conv2d_dilated_alg2(x, w, bias=None, stride=1, padding=0, dilation=1, nthreads=None):
-    """Dilated / strided conv by direct gather (Algorithm 2); float64 NCHW in and out."""
+def conv2d_dilated_alg2(x, w, bias=None, stride=1, padding=0, dilation=1, nthreads=None,
+                        groups=1):
+    """Dilated / strided conv by direct gather (Algorithm 2); float64 NCHW in and out.
+    groups > 1: w is [C_out, C_in/groups, R, S]."""
     x, w, bias = _f64(x), _f64(w), _f64(bias)
-    d = _desc(x.shape, w.shape, False, stride, padding, 0, dilation)
-    ho, wo = conv_out_dims(x.shape, w.shape, stride, padding, dilation)
+    d = _desc(x.shape, w.shape, False, stride, padding, 0, dilation, groups)
+    ho, wo = conv_out_dims(x.shape, w.shape, stride, padding, dilation, groups)
     y = np.empty((d.n, d.c_out, ho, wo), dtype=np.float64)
     rc = _load().oracle_conv2d_dilated_alg2(ctypes.byref(d), _ptr(x), _ptr(w), _ptr(bias),
                                             _ptr(y), _threads(nthreads))
@@ -162,18 +169,18 @@ def _points(fn, d, x, w, bias, flat_idx, nthreads):
 
 
 def conv2d_transpose_points(x, w, flat_idx, bias=None, stride=1, padding=0, output_padding=0,
-                            dilation=1, nthreads=None):
+                            dilation=1, nthreads=None, groups=1):
     """Algorithm 1 evaluated at flat NCHW output indices ``flat_idx``."""
     x, w, bias = _f64(x), _f64(w), _f64(bias)
-    d = _desc(x.shape, w.shape, True, stride, padding, output_padding, dilation)
+    d = _desc(x.shape, w.shape, True, stride, padding, output_padding, dilation, groups)
     return _points(_load().oracle_conv2d_transpose_points, d, x, w, bias, flat_idx, nthreads)
 
 
 def conv2d_dilated_points(x, w, flat_idx, bias=None, stride=1, padding=0, dilation=1,
-                          nthreads=None):
+                          nthreads=None, groups=1):
     """Algorithm 2 evaluated at flat NCHW output indices ``flat_idx``."""
     x, w, bias = _f64(x), _f64(w), _f64(bias)
-    d = _desc(x.shape, w.shape, False, stride, padding, 0, dilation)
+    d = _desc(x.shape, w.shape, False, stride, padding, 0, dilation, groups)
     return _points(_load().oracle_conv2d_dilated_points, d, x, w, bias, flat_idx, nthreads)
 
 

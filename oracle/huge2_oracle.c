@@ -25,8 +25,11 @@
 #include <stdlib.h>
 #include <string.h>
 
+static int ngroups(const oracle_conv* d) { return d->groups > 1 ? d->groups : 1; }
+
 static int valid_common(const oracle_conv* d) {
   if (!d) return 0;
+  if (d->groups < 0 || d->c_in % ngroups(d) != 0 || d->c_out % ngroups(d) != 0) return 0;
   if (d->n < 1 || d->c_in < 1 || d->h < 1 || d->w < 1) return 0;
   if (d->c_out < 1 || d->r < 1 || d->s < 1) return 0;
   if (d->stride_h < 1 || d->stride_w < 1 || d->dil_h < 1 || d->dil_w < 1) return 0;
@@ -124,15 +127,28 @@ static double xhat_padded(const alg1_ctx* a, int n, int c, int ph, int pw) {
   return a->xhat[(((long)n * a->d->c_in + c) * a->hh + jh) * a->wh + jw];
 }
 
+/* The input channels output channel k sums over: its group's [*c0, *c1), and
+ * k's index inside the group (the weight array holds c_out/groups of them
+ * for the transposed conv, c_in/groups for the conv). */
+static void group_of(const oracle_conv* d, int k, int* c0, int* c1, int* k_in_group) {
+  const int g = ngroups(d), cig = d->c_in / g, cog = d->c_out / g;
+  *c0 = (k / cog) * cig;
+  *c1 = *c0 + cig;
+  *k_in_group = k % cog;
+}
+
 static double alg1_output(const alg1_ctx* a, int n, int k, int oh, int ow) {
   const oracle_conv* d = a->d;
+  const int cog = d->c_out / ngroups(d);
+  int c0, c1, kg;
+  group_of(d, k, &c0, &c1, &kg);
   double acc = 0.0;
-  for (int c = 0; c < d->c_in; ++c)
+  for (int c = c0; c < c1; ++c)
     for (int m = 0; m < d->r; ++m)
       for (int q = 0; q < d->s; ++q) {
         /* the transposed kernel: rotated by 180 degrees, w[c][k] used as the
          * (k <- c) filter of the stride-1 convolution */
-        double wv = a->w[(((long)c * d->c_out + k) * d->r + (d->r - 1 - m)) * d->s + (d->s - 1 - q)];
+        double wv = a->w[(((long)c * cog + kg) * d->r + (d->r - 1 - m)) * d->s + (d->s - 1 - q)];
         acc += xhat_padded(a, n, c, oh + m * d->dil_h, ow + q * d->dil_w) * wv;
       }
   if (a->bias) acc += a->bias[k];
@@ -210,11 +226,14 @@ static void alg1_point(void* ctx, long i) {
   f /= p->a.ho;
   int k = (int)(f % d->c_out);
   int n = (int)(f / d->c_out);
+  const int cog = d->c_out / ngroups(d);
+  int c0, c1, kg;
+  group_of(d, k, &c0, &c1, &kg);
   double acc = 0.0;
-  for (int c = 0; c < d->c_in; ++c)
+  for (int c = c0; c < c1; ++c)
     for (int m = 0; m < d->r; ++m)
       for (int q = 0; q < d->s; ++q) {
-        double wv = p->a.w[(((long)c * d->c_out + k) * d->r + (d->r - 1 - m)) * d->s + (d->s - 1 - q)];
+        double wv = p->a.w[(((long)c * cog + kg) * d->r + (d->r - 1 - m)) * d->s + (d->s - 1 - q)];
         acc += xhat_defined(p, n, c, oh + m * d->dil_h, ow + q * d->dil_w) * wv;
       }
   if (p->a.bias) acc += p->a.bias[k];
@@ -256,15 +275,18 @@ typedef struct {
 
 static double alg2_output(const alg2_ctx* a, int n, int k, int oh, int ow) {
   const oracle_conv* d = a->d;
+  const int cig = d->c_in / ngroups(d);
+  int c0, c1, kg;
+  group_of(d, k, &c0, &c1, &kg);
   double acc = 0.0;
-  for (int c = 0; c < d->c_in; ++c)
+  for (int c = c0; c < c1; ++c)
     for (int m = 0; m < d->r; ++m)
       for (int q = 0; q < d->s; ++q) {
         int ih = oh * d->stride_h - d->pad_h + m * d->dil_h;
         int iw = ow * d->stride_w - d->pad_w + q * d->dil_w;
         if (ih < 0 || ih >= d->h || iw < 0 || iw >= d->w) continue; /* zero padding */
         acc += a->x[(((long)n * d->c_in + c) * d->h + ih) * d->w + iw] *
-               a->w[(((long)k * d->c_in + c) * d->r + m) * d->s + q];
+               a->w[(((long)k * cig + (c - c0)) * d->r + m) * d->s + q];
       }
   if (a->bias) acc += a->bias[k];
   return acc;
@@ -379,7 +401,8 @@ static void wgrad_plane(void* p, long plane) {
 int oracle_conv2d_transpose_wgrad(const oracle_conv* d, const double* x, const double* dy,
                                   double* dw, int nthreads) {
   wgrad_ctx a;
-  if (!x || !dy || !dw || oracle_transpose_out_dims(d, &a.ho, &a.wo) != 0) return -1;
+  if (!x || !dy || !dw || oracle_transpose_out_dims(d, &a.ho, &a.wo) != 0 || ngroups(d) != 1)
+    return -1;
   a.d = d;
   a.x = x;
   a.dy = dy;
@@ -392,7 +415,8 @@ int oracle_conv2d_transpose_wgrad(const oracle_conv* d, const double* x, const d
 int oracle_conv2d_dilated_wgrad(const oracle_conv* d, const double* x, const double* dy,
                                 double* dw, int nthreads) {
   wgrad_ctx a;
-  if (!x || !dy || !dw || oracle_conv_out_dims(d, &a.ho, &a.wo) != 0) return -1;
+  if (!x || !dy || !dw || oracle_conv_out_dims(d, &a.ho, &a.wo) != 0 || ngroups(d) != 1)
+    return -1;
   a.d = d;
   a.x = x;
   a.dy = dy;

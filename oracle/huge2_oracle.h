@@ -8,9 +8,9 @@
  *
  * Everything is float64, NCHW, contiguous:
  *   x  [n][c_in][h][w]
- *   w  transposed conv: [c_in][c_out][r][s]   (the paper's C x N x R x S,
- *                                              section 4.2)
- *      dilated / strided conv: [c_out][c_in][r][s]
+ *   w  transposed conv: [c_in][c_out/groups][r][s]   (the paper's C x N x R x
+ *                                              S of section 4.2 when groups = 1)
+ *      dilated / strided conv: [c_out][c_in/groups][r][s]
  *   y  [n][c_out][h_out][w_out]
  *   bias  [c_out] or NULL
  *
@@ -32,6 +32,11 @@ typedef struct {
   int pad_h, pad_w;
   int out_pad_h, out_pad_w;
   int dil_h, dil_w;
+  /* Grouped convolution (0 or 1: none): the channels split into `groups`
+   * equal groups, and output channel k of group k / (c_out/groups) sums only
+   * over the input channels of the same group (PyTorch's groups).  The
+   * weight gradients take groups <= 1 only. */
+  int groups;
 } oracle_conv;
 
 /* Output size of the transposed conv: (h-1)*stride - 2*pad + dil*(r-1) + out_pad + 1. */

@@ -33,8 +33,10 @@ def _golden_of(kind):
     out = []
     for path in _golden_cases():
         with open(path) as f:
-            if json.load(f)["op"].endswith("_wgrad") == (kind == "wgrad"):
-                out.append(path)
+            op = json.load(f)["op"]
+        k = "wgrad" if op.endswith("_wgrad") else "grouped" if op.endswith("_grouped") else "forward"
+        if k == kind:
+            out.append(path)
     return out
 
 
@@ -54,6 +56,99 @@ def test_golden_examples(oracle_mod, path):
                                            nthreads=1)
     assert y.shape[2:] == exp.shape
     np.testing.assert_array_equal(y[0, 0], exp)
+
+
+@pytest.mark.parametrize("path", _golden_of("grouped"), ids=lambda p: os.path.basename(p)[:-5])
+def test_golden_grouped(oracle_mod, path):
+    """Hand-worked grouped and depthwise cases: multi-channel fixtures whose
+    expected outputs fail if a group reads another group's channels or the
+    weight of the wrong in-group channel."""
+    with open(path) as f:
+        g = json.load(f)
+    assert g["citation"]
+    x = np.array(g["x"], dtype=np.float64)[None]
+    w = np.array(g["w"], dtype=np.float64)
+    exp = np.array(g["expected"], dtype=np.float64)
+    if g["op"] == "transpose_grouped":
+        y = oracle_mod.conv2d_transpose_alg1(x, w, None, g["stride"], g["padding"],
+                                             g["output_padding"], g["dilation"], nthreads=1,
+                                             groups=g["groups"])
+    else:
+        y = oracle_mod.conv2d_dilated_alg2(x, w, None, g["stride"], g["padding"], g["dilation"],
+                                           nthreads=1, groups=g["groups"])
+    np.testing.assert_array_equal(y[0], exp)
+
+
+def _block_diagonal(w, groups, transposed):
+    """The ungrouped weight array equal to a grouped one: zero wherever the
+    input and output channel lie in different groups."""
+    if transposed:
+        c_in, cog = w.shape[:2]
+        full = np.zeros((c_in, cog * groups) + w.shape[2:])
+        cig = c_in // groups
+        for c in range(c_in):
+            g = c // cig
+            full[c, g * cog:(g + 1) * cog] = w[c]
+    else:
+        c_out, cig = w.shape[:2]
+        full = np.zeros((c_out, cig * groups) + w.shape[2:])
+        cog = c_out // groups
+        for k in range(c_out):
+            g = k // cog
+            full[k, g * cig:(g + 1) * cig] = w[k]
+    return full
+
+
+@pytest.mark.parametrize("transposed", [True, False])
+def test_grouped_equals_block_diagonal(oracle_mod, transposed):
+    """A grouped conv is the ungrouped conv whose weight is block diagonal
+    over the groups (the ungrouped loops check the grouped indexing), over
+    random shapes, strides, paddings and dilations, depthwise included."""
+    rng = np.random.default_rng(7 if transposed else 8)
+    for _ in range(12):
+        groups = int(rng.choice([2, 3, 4]))
+        cig, cog = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+        n, h, w = int(rng.integers(1, 3)), int(rng.integers(2, 7)), int(rng.integers(2, 7))
+        r = int(rng.integers(1, 5))
+        st, dl = int(rng.integers(1, 4)), int(rng.integers(1, 3))
+        pd = int(rng.integers(0, dl * (r - 1) + 1))
+        x = rng.standard_normal((n, cig * groups, h, w))
+        b = rng.standard_normal(cog * groups)
+        if transposed:
+            op = int(rng.integers(0, max(st, dl)))
+            wt = rng.standard_normal((cig * groups, cog, r, r))
+            y = oracle_mod.conv2d_transpose_alg1(x, wt, b, st, pd, op, dl, groups=groups)
+            y0 = oracle_mod.conv2d_transpose_alg1(x, _block_diagonal(wt, groups, True), b, st, pd,
+                                                  op, dl)
+        else:
+            if h + 2 * pd - dl * (r - 1) - 1 < 0 or w + 2 * pd - dl * (r - 1) - 1 < 0:
+                continue
+            wt = rng.standard_normal((cog * groups, cig, r, r))
+            y = oracle_mod.conv2d_dilated_alg2(x, wt, b, st, pd, dl, groups=groups)
+            y0 = oracle_mod.conv2d_dilated_alg2(x, _block_diagonal(wt, groups, False), b, st, pd, dl)
+        np.testing.assert_allclose(y, y0, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("transposed", [True, False])
+def test_grouped_matches_torch(oracle_mod, transposed):
+    """torch.nn.functional.conv_transpose2d / conv2d with groups=, float64 on
+    the CPU, over a sweep that includes depthwise layers with multipliers."""
+    rng = np.random.default_rng(9 if transposed else 10)
+    cases = [(2, 3, 2), (4, 1, 1), (3, 2, 4), (6, 1, 3)]  # (groups, C_in/groups, C_out/groups)
+    for groups, cig, cog in cases:
+        x = rng.standard_normal((2, cig * groups, 6, 5))
+        if transposed:
+            w = rng.standard_normal((cig * groups, cog, 3, 4))
+            y = oracle_mod.conv2d_transpose_alg1(x, w, None, (2, 3), (1, 2), (1, 0), (1, 1),
+                                                 groups=groups)
+            t = torch.nn.functional.conv_transpose2d(torch.from_numpy(x), torch.from_numpy(w), None,
+                                                     (2, 3), (1, 2), (1, 0), groups, (1, 1))
+        else:
+            w = rng.standard_normal((cog * groups, cig, 3, 3))
+            y = oracle_mod.conv2d_dilated_alg2(x, w, None, (1, 2), (2, 1), (2, 1), groups=groups)
+            t = torch.nn.functional.conv2d(torch.from_numpy(x), torch.from_numpy(w), None, (1, 2),
+                                           (2, 1), (2, 1), groups)
+        np.testing.assert_allclose(y, t.numpy(), rtol=1e-11, atol=1e-11)
 
 
 @pytest.mark.parametrize("path", _golden_of("wgrad"), ids=lambda p: os.path.basename(p)[:-5])

@@ -84,6 +84,16 @@ typedef struct {
   int32_t layout;               /* huge2_layout */
   int32_t dtype;                /* huge2_dtype */
   int32_t activation;           /* huge2_activation, applied after the bias (0: none) */
+  /* Grouped convolution (0 or 1: none; PyTorch's groups): c_in and c_out
+   * split into `groups` equal groups, output channel k (of group k /
+   * (c_out/groups)) sums only over its group's input channels, and w holds
+   * c_out/groups (transposed) or c_in/groups (dilated) channels on its
+   * second axis.  groups = c_in is the depthwise convolution (a channel
+   * multiplier c_out/c_in).  Grouped layers run on a direct kernel that
+   * forms each output from its phase's taps (section 3.1) and its group's
+   * channels; the weight-gradient entry points and grouped launches
+   * (huge2_group) take groups <= 1 only. */
+  int32_t groups;
 } huge2_conv_desc;
 
 typedef struct huge2_plan huge2_plan; /* opaque */
@@ -104,9 +114,9 @@ huge2_status huge2_output_shape(const huge2_conv_desc* desc, int32_t transposed,
  * list), copies the work list and runs on hip_stream the kernel that gathers
  * w into per-tap, K-contiguous sub-kernel blocks (section 3.2.1: the N x C
  * matrix for each kernel position), then waits for hip_stream.
- *   transposed = 1: w is [c_in][c_out][r][s] (the paper's C x N x R x S,
+ *   transposed = 1: w is [c_in][c_out/groups][r][s] (the paper's C x N x R x S,
  *                   section 4.2; PyTorch ConvTranspose2d order).
- *   transposed = 0: w is [c_out][c_in][r][s] (PyTorch Conv2d order).
+ *   transposed = 0: w is [c_out][c_in/groups][r][s] (PyTorch Conv2d order).
  * w is read only by work enqueued on hip_stream: it may be freed or changed
  * once that work has completed.  *out receives the plan (NULL on error).
  * A layer with fewer output tiles than compute units also gets a plan-owned

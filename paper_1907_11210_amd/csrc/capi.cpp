@@ -59,6 +59,10 @@ struct huge2_plan {
   ZArgs zargs;  // its launch shape (pointers filled per call)
   bool rowphase;  // output-stationary form for large strides
   RpArgs rpargs;
+  bool colphase;  // column-phase form for a column stride of 32
+  CpArgs cpargs;
+  bool grouped;   // grouped / depthwise: the direct kernel over a copy of w
+  GrArgs grargs;
   bool quad;      // all-phase form of the stride-2, 4x4, padding-1 layer
   QArgs qargs;
   int bias_div;   // GEMM columns per bias entry (r * s for the 1x1-input product form)
@@ -123,14 +127,17 @@ long long count_works(const huge2_conv_desc& d, bool transposed, int class_split
 
 // Tile choice, from measurements on MI355X.  bf16: many pixels and at most
 // 128 output channels take the 8-wave 128 x 128 tile; 256 or more output
-// channels take the 8-wave split-wave 128 x 256 tile when every CU gets one
-// (ASPP: twice the pixels per weight fetch of 64 x 256, which its L2 traffic
-// needs), else the 64 x 256 one with plenty of its tiles; otherwise the split-wave tiles with two K groups per workgroup,
-// 128 x 128 when that still gives every CU a tile, else 64 x 128 (few
-// pixels and long K: the first DCGAN layers).  A pointwise GEMM of at most
-// 64 pixel rows and many channels (a generator's projection of z) takes the
-// 4-wave 32 x 256 tile: two row tiles, and no second K group idling on its
-// single K stage.  Few output channels take the narrow 128 x 32 tile.  fp32 keeps the two-operand-LDS tiles.
+// channels take the pipelined 8-wave 128 x 256 tile when every CU gets one
+// (the atrous pyramid: twice the pixels per weight fetch of 64 x 256, which
+// its L2 traffic needs; its three-buffer pipeline measured 1090 against 955
+// TFLOP/s for the split-wave kernel of the same tile on the grouped pyramid),
+// else the 64 x 256 one with plenty of its tiles; otherwise the split-wave
+// tiles with two K groups per workgroup, 128 x 128 when that still gives
+// every CU a tile, else 64 x 128 (few pixels and long K: the first DCGAN
+// layers).  A pointwise GEMM of at most 64 pixel rows and many channels (a
+// generator's projection of z) takes the 4-wave 32 x 256 tile: two row tiles,
+// and no second K group idling on its single K stage.  Few output channels
+// take the narrow 128 x 32 tile.  fp32 keeps the two-operand-LDS tiles.
 int choose_cfg(const huge2_conv_desc& d, bool transposed, int class_split) {
   int forced = env_int("HUGE2_TILE", -1);
   if (forced >= 0 && forced < TILE_COUNT) return forced;
@@ -140,8 +147,8 @@ int choose_cfg(const huge2_conv_desc& d, bool transposed, int class_split) {
   if (large && d.c_out <= 128) return TILE_128x128;
   if (d.r == 1 && d.s == 1 && (long long)d.n * d.h * d.w <= 64 && d.c_out >= 256)
     return TILE_SW_32x256;  // a pointwise GEMM of at most 64 rows (the 1x1-input product form)
-  if (d.c_out >= 256 && count_works(d, transposed, class_split, TILE_SW_128x256) >= kComputeUnits)
-    return TILE_SW_128x256;
+  if (d.c_out >= 256 && count_works(d, transposed, class_split, TILE_P3_128x256) >= kComputeUnits)
+    return TILE_P3_128x256;
   if (d.c_out >= 256 && count_works(d, transposed, class_split, TILE_SW_64x256) >= 384)
     return TILE_SW_64x256;
   if (count_works(d, transposed, class_split, TILE_SW_128x128_K2) >= kComputeUnits)
@@ -429,6 +436,59 @@ bool rowphase_shape(const huge2_conv_desc& d, bool transposed, RpArgs* z, int64_
   return true;
 }
 
+// The column-phase form (colphase_kernel) applies to NCHW bf16 transposed
+// convs with column stride 32, dilation 1, at most 32 input channels, kernel
+// width at most 64 and height at most twice the row stride, output padding
+// and width multiples of 8 (16-byte output pieces), every output row and
+// column reaching back into the input or its one-pixel border, and the
+// staged input within 64 KiB of LDS.  Returns false otherwise (or with
+// HUGE2_COLPHASE=0, or a GEMM tile forced).
+bool colphase_shape(const huge2_conv_desc& d, bool transposed, CpArgs* z, int64_t* issued) {
+  if (!transposed || d.layout != HUGE2_NCHW || d.dtype != HUGE2_BF16) return false;
+  if (env_int("HUGE2_COLPHASE", 1) == 0 || env_int("HUGE2_TILE", -1) >= 0) return false;
+  if (d.stride_w != 32 || d.dil_h != 1 || d.dil_w != 1 || d.c_in > 32 || d.s > 64 ||
+      d.r > 2 * d.stride_h || d.pad_w % 8 != 0)
+    return false;
+  int ho, wo;
+  if (!output_dims(d, true, &ho, &wo) || wo % 8 != 0) return false;
+  const int cp = round_up(d.c_in, 8);
+  if (((long long)(d.h + 2) * (d.w + 2) * cp + (long long)kCpWaves * kCpRows * wo) * 2 > kCpMaxLds)
+    return false;
+  const int qw_lo = ceil_div_i(d.pad_w - 31, 32), qw_hi = floor_div_i(wo - 1 + d.pad_w, 32);
+  if (qw_lo < 0 || qw_hi > d.w || qw_hi < qw_lo) return false;
+  int64_t cols = 0;
+  for (int rho = 0; rho < d.stride_h; ++rho) {
+    const int q_lo = ceil_div_i(d.pad_h - rho, d.stride_h);
+    const int q_hi = floor_div_i(ho - 1 + d.pad_h - rho, d.stride_h);
+    if (q_hi < q_lo) continue;
+    if (q_lo < 0 || q_hi > d.h) return false;
+    cols += ((int64_t)(q_hi - q_lo + 1) * (qw_hi - qw_lo + 1) + 31) / 32 * 32;
+  }
+  std::memset(z, 0, sizeof(*z));
+  z->n = d.n;
+  z->cin = d.c_in;
+  z->h = d.h;
+  z->w = d.w;
+  z->cout = d.c_out;
+  z->r = d.r;
+  z->s = d.s;
+  z->stride_h = d.stride_h;
+  z->pad_h = d.pad_h;
+  z->pad_w = d.pad_w;
+  z->ho = ho;
+  z->wo = wo;
+  z->cp = cp;
+  z->qw_lo = qw_lo;
+  z->nqw = qw_hi - qw_lo + 1;
+  const uint32_t dv[4] = {(uint32_t)(d.w + 2), (uint32_t)(d.h + 2), (uint32_t)z->nqw,
+                          (uint32_t)(cp / 8)};
+  for (int k = 0; k < 4; ++k) division_magic(dv[k], &z->dv_mul[k], &z->dv_shift[k]);
+  // per (image, output channel) and row phase: 32 column phases x the
+  // padded columns x K = 4 taps x cp
+  *issued = (int64_t)d.n * d.c_out * cols * 32 * 4 * cp;
+  return true;
+}
+
 // The all-phase form (quad_kernel) applies to NCHW bf16 transposed convs
 // with stride 2, a 4x4 kernel, padding 1, dilation 1 and no output padding
 // (so every phase has 2x2 taps at input offsets in [-1, 1] and the input's
@@ -582,6 +642,32 @@ bool tap_progressions(const huge2_tap* tl, int count, SegDev* sd) {
   return true;
 }
 
+// The same check for a work's own tap list, into the work's progression
+// fields (ap_ntw = 0 when the taps are no such product).
+void work_progressions(const TapDev* tl, int count, int s_width, WorkDev* w) {
+  w->ap_ntw = 0;
+  if (count <= 0) return;
+  std::vector<huge2_tap> t(count);
+  for (int i = 0; i < count; ++i) {
+    t[i].kh = tl[i].slot / s_width;
+    t[i].kw = tl[i].slot % s_width;
+    t[i].off_h = tl[i].off_h;
+    t[i].off_w = tl[i].off_w;
+  }
+  SegDev sd;
+  std::memset(&sd, 0, sizeof(sd));
+  if (!tap_progressions(t.data(), count, &sd)) return;
+  w->ap_ntw = sd.ntw;
+  w->ap_kh0 = sd.kh0;
+  w->ap_dkh = sd.dkh;
+  w->ap_kw0 = sd.kw0;
+  w->ap_dkw = sd.dkw;
+  w->ap_off0_h = sd.off0_h;
+  w->ap_doff_h = sd.doff_h;
+  w->ap_off0_w = sd.off0_w;
+  w->ap_doff_w = sd.doff_w;
+}
+
 // Border-class splitting of a plan: HUGE2_CLASS_SPLIT (0, 1, 2) forces it;
 // otherwise 0 (one segment per phase group, out-of-range taps read zeros) or
 // 2 (per group, the form that issues fewer tile-taps), whichever the schedule
@@ -661,7 +747,8 @@ huge2_status dev_alloc(huge2_plan* p, void** out, size_t bytes) {
 // directly, so nothing is staged.
 huge2_status create_direct(huge2_plan** out, const huge2_conv_desc& d, int transposed,
                           const void* w, hipStream_t stream, Mem mem, const ZArgs* zp,
-                          const RpArgs* rp, const QArgs* qp, int64_t issued) {
+                          const RpArgs* rp, const QArgs* qp, int64_t issued,
+                          const CpArgs* cpa = nullptr) {
   PlanShape shape;
   if (!build_shape(d, true, 2, 128, &shape)) return HUGE2_ERR_INVALID_ARG;
   huge2_plan* p = new (std::nothrow) huge2_plan();
@@ -679,11 +766,20 @@ huge2_status create_direct(huge2_plan** out, const huge2_conv_desc& d, int trans
   p->cout_pad = zp ? zp->cout_pad : qp ? qp->cout_pad : kRpCh;
   p->x_bytes = (size_t)d.n * d.c_in * d.h * d.w * esz;
   p->wp_bytes = (size_t)d.r * d.s * p->cout_pad * p->cin_pad * esz;
+  if (cpa) {
+    p->cin_pad = cpa->cp;
+    p->cout_pad = d.c_out;
+    p->wp_bytes = (size_t)d.c_out * d.stride_h * (cpa->cp / 4) * 64 * 8 * esz;
+  }
   p->mem = mem;
   p->alloc_stream = stream;
   p->nonzero_macs = shape.nonzero_macs;
   p->issued_macs = issued;
-  if (zp) {
+  if (cpa) {
+    p->colphase = true;
+    p->cpargs = *cpa;
+    std::snprintf(p->kernel_name, sizeof(p->kernel_name), "colphase_kernel cp%d", cpa->cp);
+  } else if (zp) {
     p->ztile = true;
     p->zargs = *zp;
     std::snprintf(p->kernel_name, sizeof(p->kernel_name), "ztile_kernel ob%d", zp->ob);
@@ -704,7 +800,10 @@ huge2_status create_direct(huge2_plan** out, const huge2_conv_desc& d, int trans
     return st;
   }
   bool ok = !fault("launch");
-  if (ok)
+  if (ok && cpa)
+    ok = launch_pack_colphase(w, p->wp, d.c_in, d.c_out, d.r, d.s, d.stride_h, cpa->cp, stream) ==
+         hipSuccess;
+  else if (ok)
     ok = launch_pack_weights(w, p->wp, d.dtype, true, d.c_in, d.c_out, d.r, d.s, p->cin_pad,
                              p->cout_pad, qp ? 128 : 0, stream) == hipSuccess;
   if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
@@ -854,6 +953,69 @@ huge2_status create_two_pass(huge2_plan** out, const huge2_conv_desc& d, const h
   return HUGE2_OK;
 }
 
+// A grouped (or depthwise) layer: the weight copied into the plan (the caller
+// may free w after plan creation), the direct kernel at execute.
+huge2_status create_grouped(huge2_plan** out, const huge2_conv_desc& d, int transposed,
+                            const void* w, hipStream_t stream, Mem mem) {
+  huge2_plan* p = new (std::nothrow) huge2_plan();
+  if (!p) return HUGE2_ERR_ALLOC;
+  const bool tr = transposed != 0;
+  const int esz = elem_size(d.dtype);
+  p->desc = d;
+  p->transposed = transposed;
+  p->bias_div = 1;
+  p->ksplit = 1;
+  p->cfg = -1;
+  p->staged = false;
+  output_dims(d, tr, &p->ho, &p->wo);
+  p->mem = mem;
+  p->alloc_stream = stream;
+  p->grouped = true;
+  p->wp_bytes = (size_t)d.c_in * (d.c_out / d.groups) * d.r * d.s * esz;
+  PlanShape shape;
+  p->nonzero_macs = build_shape(d, tr, 2, 128, &shape) ? shape.nonzero_macs / d.groups : 0;
+  p->issued_macs = p->nonzero_macs;
+  GrArgs& g = p->grargs;
+  std::memset(&g, 0, sizeof(g));
+  g.n = d.n;
+  g.cin = d.c_in;
+  g.h = d.h;
+  g.w_ = d.w;
+  g.cout = d.c_out;
+  g.r = d.r;
+  g.s = d.s;
+  g.stride_h = d.stride_h;
+  g.stride_w = d.stride_w;
+  g.pad_h = d.pad_h;
+  g.pad_w = d.pad_w;
+  g.dil_h = d.dil_h;
+  g.dil_w = d.dil_w;
+  g.ho = p->ho;
+  g.wo = p->wo;
+  g.groups = d.groups;
+  g.transposed = transposed;
+  g.nhwc = d.layout == HUGE2_NHWC;
+  g.act = d.activation;
+  std::snprintf(p->kernel_name, sizeof(p->kernel_name), "grouped_kernel g%d", d.groups);
+  huge2_status st = dev_alloc(p, &p->wp, p->wp_bytes);
+  if (st != HUGE2_OK) {
+    free_buffers(p);
+    delete p;
+    return st;
+  }
+  bool ok = !fault("launch") &&
+            hipMemcpyAsync(p->wp, w, p->wp_bytes, hipMemcpyDeviceToDevice, stream) == hipSuccess;
+  if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
+  if (!ok) {
+    (void)hipGetLastError();
+    free_buffers(p);
+    delete p;
+    return HUGE2_ERR_HIP;
+  }
+  *out = p;
+  return HUGE2_OK;
+}
+
 huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int transposed,
                          const void* w, hipStream_t stream, Mem mem) {
   if (!out) return HUGE2_ERR_INVALID_ARG;
@@ -863,6 +1025,7 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   if (st != HUGE2_OK) return st;
   if (!w) return HUGE2_ERR_INVALID_ARG;
   const bool tr = transposed != 0;
+  if (desc->groups > 1) return create_grouped(out, *desc, transposed, w, stream, mem);
   // the 1x1-input product form: bias k then covers r*s consecutive columns
   huge2_conv_desc dd;
   const int bias_div = product_form(*desc, tr, &dd);
@@ -879,6 +1042,10 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     if (ztile_shape(d, tr, &z, &z_issued))
       return create_direct(out, d, transposed, w, stream, mem, &z, nullptr, nullptr,
                            z_issued);
+    CpArgs cpa;
+    if (colphase_shape(d, tr, &cpa, &z_issued))
+      return create_direct(out, d, transposed, w, stream, mem, nullptr, nullptr, nullptr,
+                           z_issued, &cpa);
     RpArgs rp;
     if (rowphase_shape(d, tr, &rp, &z_issued))
       return create_direct(out, d, transposed, w, stream, mem, nullptr, &rp, nullptr,
@@ -909,8 +1076,8 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
       std::snprintf(p->kernel_name, sizeof(p->kernel_name), "phase_gemm_kernel %dx%d w%dx%d",
                     t.bm, t.bn, t.pw, t.cw);
     else
-      std::snprintf(p->kernel_name, sizeof(p->kernel_name), "phase_gemm2_kernel %dx%d w%d k%d",
-                    t.bm, t.bn, t.pw * t.cw, t.ksplit);
+      std::snprintf(p->kernel_name, sizeof(p->kernel_name), "phase_gemm%d_kernel %dx%d w%d k%d",
+                    t.kind == 3 ? 3 : 2, t.bm, t.bn, t.pw * t.cw, t.ksplit);
     if (listed) {
       const size_t len = std::strlen(p->kernel_name);
       std::snprintf(p->kernel_name + len, sizeof(p->kernel_name) - len, " listed");
@@ -1067,6 +1234,31 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
       }
   }
   p->issued_macs = issued;
+  bool all_ap = true;
+  for (WorkDev& wd : works) {
+    work_progressions(taps.data() + wd.tap_begin, wd.tap_count, d.s, &wd);
+    all_ap = all_ap && wd.ap_ntw > 0;
+  }
+  if (kTiles[p->cfg].kind == 3 && !all_ap) {
+    // the pipelined kernel steps through progressions only: the split-wave
+    // kernel of the same tile and packing takes tap lists
+    for (int c = 0; c < TILE_COUNT; ++c) {
+      const TileShape &t = kTiles[c], &u = kTiles[p->cfg];
+      if (t.kind == 1 && t.bm == u.bm && t.bn == u.bn && t.kb == u.kb && t.pw * t.cw == u.pw * u.cw &&
+          t.ksplit == u.ksplit) {
+        p->cfg = c;
+        break;
+      }
+    }
+    if (kTiles[p->cfg].kind == 3) {
+      free_buffers(p);
+      delete p;
+      return HUGE2_ERR_UNSUPPORTED;
+    }
+    const TileShape& t = kTiles[p->cfg];
+    std::snprintf(p->kernel_name, sizeof(p->kernel_name), "phase_gemm2_kernel %dx%d w%d k%d%s",
+                  t.bm, t.bn, t.pw * t.cw, t.ksplit, listed ? " listed" : "");
+  }
   // Too few tiles to give every compute unit one: split the input channel
   // blocks into ksplit slices, one workgroup per (tile, slice), whose fp32
   // partials a second kernel adds in slice order (deterministic), with the
@@ -1150,7 +1342,7 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     ok = hipMemcpyAsync(p->meta, host.data(), meta_b, hipMemcpyHostToDevice, stream) == hipSuccess;
   if (ok)
     ok = launch_pack_weights(w, p->wp, d.dtype, tr, d.c_in, d.c_out, d.r, d.s, p->cin_pad,
-                             p->cout_pad, kTiles[p->cfg].kind == 1 ? tile_kb(p->cfg) : 0,
+                             p->cout_pad, kTiles[p->cfg].kind != 0 ? tile_kb(p->cfg) : 0,
                              stream) == hipSuccess;
   // the host copy of the metadata must outlive the transfer
   if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
@@ -1255,6 +1447,31 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
     z.y = y;
     z.act = d.activation;
     if (launch_ztile(z, d.dtype, stream) != hipSuccess) {
+      (void)hipGetLastError();
+      return HUGE2_ERR_HIP;
+    }
+    return HUGE2_OK;
+  }
+  if (p->grouped) {
+    GrArgs g = p->grargs;
+    g.x = x;
+    g.w = p->wp;
+    g.bias = bias;
+    g.y = y;
+    if (launch_grouped(g, d.dtype, stream) != hipSuccess) {
+      (void)hipGetLastError();
+      return HUGE2_ERR_HIP;
+    }
+    return HUGE2_OK;
+  }
+  if (p->colphase) {
+    CpArgs z = p->cpargs;
+    z.x = x;
+    z.wp = p->wp;
+    z.bias = bias;
+    z.y = y;
+    z.act = d.activation;
+    if (launch_colphase(z, stream) != hipSuccess) {
       (void)hipGetLastError();
       return HUGE2_ERR_HIP;
     }
@@ -1457,7 +1674,8 @@ huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, i
   huge2_status st = validate_desc(desc, transposed != 0);
   if (st != HUGE2_OK) return st;
   const huge2_conv_desc& d = *desc;
-  if (d.layout != HUGE2_NCHW || d.activation != HUGE2_ACT_NONE) return HUGE2_ERR_UNSUPPORTED;
+  if (d.layout != HUGE2_NCHW || d.activation != HUGE2_ACT_NONE || d.groups > 1)
+    return HUGE2_ERR_UNSUPPORTED;
   int ho, wo;
   if (!output_dims(d, transposed != 0, &ho, &wo)) return HUGE2_ERR_INVALID_ARG;
   huge2_wgrad_plan* p = new (std::nothrow) huge2_wgrad_plan();
@@ -1565,7 +1783,8 @@ huge2_status wgrad_one_shot(const huge2_conv_desc* desc, int transposed, const v
 
 bool groupable(const huge2_plan* p, const huge2_plan* q) {
   if (!p || !q || p->cfg < 0 || q->cfg < 0 || p->inner || q->inner || p->ztile || q->ztile ||
-      p->rowphase || q->rowphase || p->quad || q->quad || p->staged || q->staged ||
+      p->rowphase || q->rowphase || p->quad || q->quad || p->colphase || q->colphase ||
+      p->staged || q->staged ||
       p->ksplit != 1 || q->ksplit != 1 || p->h_works.empty() || q->h_works.empty())
     return false;
   const huge2_conv_desc &a = p->desc, &b = q->desc;
@@ -1851,6 +2070,12 @@ huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, in
   huge2_status st = validate_desc(desc, transposed != 0);
   if (st != HUGE2_OK) return st;
   try {
+    if (desc->groups > 1) {
+      PlanShape shape;
+      if (!build_shape(*desc, transposed != 0, 2, 128, &shape)) return HUGE2_ERR_INVALID_ARG;
+      *nonzero_macs = *issued_macs = shape.nonzero_macs / desc->groups;
+      return HUGE2_OK;
+    }
     ZArgs z;
     int64_t z_issued = 0;
     RpArgs rp;
@@ -1866,7 +2091,9 @@ huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, in
       *nonzero_macs = shape.nonzero_macs;
       return huge2_plan_macs(&d1, transposed != 0 ? 1 : 0, &nz1, issued_macs);
     }
+    CpArgs cpa;
     if (ztile_shape(dd, transposed != 0, &z, &z_issued) ||
+        colphase_shape(dd, transposed != 0, &cpa, &z_issued) ||
         rowphase_shape(dd, transposed != 0, &rp, &z_issued) ||
         quad_shape(dd, transposed != 0, &q, &z_issued)) {
       PlanShape shape;

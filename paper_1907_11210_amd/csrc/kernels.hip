@@ -22,6 +22,18 @@ typedef __attribute__((ext_vector_type(16))) float f32x16;
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
+constexpr int gcd_c(int a, int b) { return b == 0 ? a : gcd_c(b, a % b); }
+constexpr int lcm3(int a, int b, int c) {
+  return (a / gcd_c(a, b) * b) / gcd_c(a / gcd_c(a, b) * b, c) * c;
+}
+// f(integral_constant<int, u>) for u = 0 .. N-1, unrolled at compile time.
+template <int N, int I = 0, typename F>
+__device__ __forceinline__ void unroll_stages(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>());
+    unroll_stages<N, I + 1>(f);
+  }
+}
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
@@ -789,12 +801,321 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm2_kernel(GemmArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Phase GEMM, pipelined split-wave form.  The same tile as phase_gemm2_kernel
+// (BM pixel rows through LDS, each of the W waves of a K group loading its
+// BN/W weight rows straight into registers in the MFMA lane layout), with
+// the stage order rearranged so that LDS latency hides behind the MFMAs:
+//  - three LDS stage buffers: stage s is written two stages ahead of its use
+//    (while stage s-1's buffer may still be read), so one barrier per stage
+//    separates every write from the reads it must not overtake;
+//  - the 16-byte pixel fragments of K chunk c+1 are read while the MFMAs of
+//    chunk c run, and the first chunk of stage s+1 while stage s finishes;
+//  - pixel chunks are loaded DA = 2 stages before they are written to LDS,
+//    weight fragments DB stages before their MFMAs, each with its own tap
+//    and channel-block counter (a work's taps are a product of two
+//    arithmetic progressions, read from the work item: no memory lookup per
+//    stage; plans whose works have other tap lists take the unpipelined
+//    kernel).
+// The loop is unrolled by U = 6 (a multiple of the 3 LDS buffers and of DA
+// and DB), so every buffer index is a compile-time constant.
+template <bool BF16, int BM, int BN, int W, int KB, int DA, int DB, int KS, bool NCHW_OUT>
+__global__ __launch_bounds__(W * 64 * KS) void phase_gemm3_kernel(GemmArgs a) {
+  constexpr int NTA = W * 64 * KS, NT = W * 64;
+  constexpr int ESZ = BF16 ? 2 : 4;
+  constexpr int KC = KB / ESZ;   // K elements per stage
+  constexpr int VE = 16 / ESZ;   // elements per 16-byte chunk
+  constexpr int CPR = KB / 16;   // 16-byte chunks per row and stage
+  constexpr int HC = CPR / 2;    // K chunks per stage (one per lane half)
+  constexpr int ROWB = KB + 16;  // LDS row pitch (16-byte pad: distinct banks)
+  constexpr int RD = BN / W;     // weight rows (output channels) per wave
+  constexpr int TP = BM / 32, TC = RD / 32;
+  constexpr int S_LD = (BM * CPR + NT - 1) / NT;  // pixel chunks per thread and stage
+  constexpr int NB = 3;
+  constexpr int U = lcm3(NB, DA, DB);
+  static_assert(RD % 32 == 0 && BM % 32 == 0 && HC >= 2 && HC % 2 == 0, "tile shape");
+  static_assert(DA >= 2 && DA <= 4 && DB >= 2 && DB <= 4, "two to four stages in flight");
+  constexpr int STAGE_B = BM * ROWB;
+  constexpr uint32_t OOB = 0x80000000u;
+  constexpr int ACC_B = KS > 1 ? W * 64 * TP * TC * 16 * 4 : 0;
+  constexpr int SMEM_B = KS * NB * STAGE_B > ACC_B ? KS * NB * STAGE_B : ACC_B;
+  __shared__ __attribute__((aligned(16))) char smem_all[SMEM_B];
+  __shared__ float s_bias[BN];
+
+  const int wave_all = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int lane = threadIdx.x & 63, grp = KS > 1 ? wave_all / W : 0;
+  const int wave = wave_all - grp * W;
+  const int tid = (int)threadIdx.x - grp * NT;
+  char* const smem = smem_all + grp * NB * STAGE_B;
+  const int half = lane >> 5, row32 = lane & 31;
+  const int work = xcd_remap(blockIdx.x, gridDim.x);
+  const WorkDev wk = a.works[work];
+  const SegDev sg = a.segs[wk.seg];
+  const __amdgpu_buffer_rsrc_t xr =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.x, 0, a.x_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t wr =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.wp[sg.plan], 0, a.wp_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t xr0 = __builtin_amdgcn_make_buffer_rsrc((void*)a.x, 0, 0, 0x00020000);
+  const __amdgpu_buffer_rsrc_t wr0 =
+      __builtin_amdgcn_make_buffer_rsrc((void*)a.wp[sg.plan], 0, 0, 0x00020000);
+
+  // this thread's pixel rows (chunk s_chunk of rows tid / CPR + (NT / CPR) * i)
+  int p_ih[S_LD], p_iw[S_LD];
+  uint32_t p_base[S_LD];
+  const int s_chunk = tid % CPR;
+#pragma unroll
+  for (int i = 0; i < S_LD; ++i) {
+    const int r = tid / CPR + (NT / CPR) * i;
+    const int m = min(wk.m0 + r, wk.m1 - 1);
+    const PixelPos p = pixel_pos(sg, a.ptab, m);
+    p_ih[i] = p.ih;
+    p_iw[i] = p.iw;
+    p_base[i] = (((uint32_t)p.img * (uint32_t)a.h + (uint32_t)p.ih) * (uint32_t)a.w +
+                 (uint32_t)p.iw) * (uint32_t)a.cin * ESZ + (uint32_t)(s_chunk * 16);
+  }
+  // lane-ordered weights: 32-channel block (n0 + wave * RD) / 32 + i
+  uint32_t w_off[TC];
+#pragma unroll
+  for (int i = 0; i < TC; ++i)
+    w_off[i] = (uint32_t)(((wk.n0 + wave * RD) / 32 + i) * 32 * a.cin_pad * ESZ + lane * 16);
+
+  const int ntaps = wk.tap_count;
+  const int cblocks = a.cin_pad / KC;
+  const int cb_w0 = wk.ks * cblocks / a.ksplit, cb_w1 = (wk.ks + 1) * cblocks / a.ksplit;
+  const int cb_per = (cb_w1 - cb_w0 + KS - 1) / KS;
+  const int cb_lo = min(cb_w0 + grp * cb_per, cb_w1);
+  const int nsteps = ntaps * (min(cb_lo + cb_per, cb_w1) - cb_lo);  // this group's stages
+  const int nsteps_all = ntaps * cb_per;  // both groups run this many (shared barriers)
+  const int tail_c = a.cin - (cblocks - 1) * KC;
+  const uint32_t slot_bytes = (uint32_t)a.cout_pad * (uint32_t)a.cin_pad * ESZ;
+
+  const float* const bias = a.bias[sg.plan];
+  for (int t = threadIdx.x; t < BN; t += NTA)
+    s_bias[t] = (bias && wk.n0 + t < a.cout) ? bias[(wk.n0 + t) / a.bias_div] : 0.f;
+
+  // Stage counters: tap (th, tw) inner, channel block outer.
+  struct Iter {
+    int th, tw, t, cb;
+  };
+  auto advance = [&](Iter& it) {
+    if (++it.tw == wk.ap_ntw) {
+      it.tw = 0;
+      ++it.th;
+    }
+    if (++it.t == ntaps) {
+      it.t = it.th = it.tw = 0;
+      ++it.cb;
+    }
+  };
+  // (the plan gives this kernel only works whose taps are progressions)
+  auto tap_of = [&](const Iter& it, int* off_h, int* off_w, uint32_t* slot_b) {
+    *off_h = wk.ap_off0_h + it.th * wk.ap_doff_h;
+    *off_w = wk.ap_off0_w + it.tw * wk.ap_doff_w;
+    *slot_b = (uint32_t)((wk.ap_kh0 + it.th * wk.ap_dkh) * a.ks + wk.ap_kw0 + it.tw * wk.ap_dkw) *
+              slot_bytes;
+  };
+  Iter ia{0, 0, 0, cb_lo}, ib{0, 0, 0, cb_lo};
+
+  struct RegA {
+    uint4 v[S_LD];
+  };
+  struct RegB {
+    uint4 v[TC][HC];
+  };
+  RegA ra[DA];
+  RegB rb[DB];
+
+  // Both loads are branch-free: a stage past the end reads through a
+  // zero-size buffer (zeros), and a read outside the input gets an
+  // out-of-range offset (zeros); the counters run on regardless.
+  auto load_a = [&](RegA& R, bool valid) {
+    const __amdgpu_buffer_rsrc_t xs = valid ? xr : xr0;
+    int off_h, off_w;
+    uint32_t slot_b;
+    tap_of(ia, &off_h, &off_w, &slot_b);
+    const int delta = (off_h * a.w + off_w) * a.cin * ESZ;
+    const uint32_t kb = (uint32_t)ia.cb * KB;
+    const bool tail = ia.cb == cblocks - 1 && tail_c < KC && s_chunk * VE >= tail_c;
+#pragma unroll
+    for (int i = 0; i < S_LD; ++i) {
+      const int ih = p_ih[i] + off_h, iw = p_iw[i] + off_w;
+      const bool in = ((unsigned)ih < (unsigned)a.h) & ((unsigned)iw < (unsigned)a.w) & !tail;
+      const uint32_t v = in ? p_base[i] + (uint32_t)delta : OOB;
+      R.v[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xs, v, kb, 0));
+    }
+    advance(ia);
+  };
+  auto load_b = [&](RegB& R, bool valid) {
+    const __amdgpu_buffer_rsrc_t ws = valid ? wr : wr0;
+    int off_h, off_w;
+    uint32_t slot_b;
+    tap_of(ib, &off_h, &off_w, &slot_b);
+    const uint32_t kb = (uint32_t)ib.cb * KB;
+#pragma unroll
+    for (int i = 0; i < TC; ++i)
+#pragma unroll
+      for (int c = 0; c < HC; ++c)
+        R.v[i][c] = __builtin_bit_cast(
+            uint4, __builtin_amdgcn_raw_buffer_load_b128(ws, w_off[i], slot_b + 32 * kb + 1024 * c, 0));
+    advance(ib);
+  };
+  auto store_a = [&](int buf, const RegA& R) {
+    char* ss = smem + buf * STAGE_B;
+#pragma unroll
+    for (int i = 0; i < S_LD; ++i)
+      if (BM * CPR % NT == 0 || tid + NT * i < BM * CPR)
+        *(uint4*)(ss + (tid / CPR + (NT / CPR) * i) * ROWB + s_chunk * 16) = R.v[i];
+  };
+  auto read_f = [&](int buf, int c, uint4 (&f)[TP]) {
+    const char* ss = smem + buf * STAGE_B + row32 * ROWB + half * (KB / 2) + 16 * c;
+#pragma unroll
+    for (int i = 0; i < TP; ++i) f[i] = *(const uint4*)(ss + 32 * i * ROWB);
+  };
+
+  f32x16 acc[TP][TC];
+#pragma unroll
+  for (int i = 0; i < TP; ++i)
+#pragma unroll
+    for (int j = 0; j < TC; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  auto mfma_chunk = [&](const uint4 (&fp)[TP], const RegB& R, int c) {
+    if constexpr (BF16) {
+#pragma unroll
+      for (int i = 0; i < TP; ++i)
+#pragma unroll
+        for (int j = 0; j < TC; ++j) {
+          const bf16x8 vp = __builtin_bit_cast(bf16x8, fp[i]);
+          const bf16x8 vc = __builtin_bit_cast(bf16x8, R.v[j][c]);
+          if constexpr (NCHW_OUT)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vc, vp, acc[i][j], 0, 0, 0);
+          else
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vp, vc, acc[i][j], 0, 0, 0);
+        }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int i = 0; i < TP; ++i)
+#pragma unroll
+          for (int j = 0; j < TC; ++j) {
+            const uint4 x4 = fp[i], w4 = R.v[j][c];
+            const uint32_t bp = e == 0 ? x4.x : e == 1 ? x4.y : e == 2 ? x4.z : x4.w;
+            const uint32_t bc = e == 0 ? w4.x : e == 1 ? w4.y : e == 2 ? w4.z : w4.w;
+            const float vp = __uint_as_float(bp), vc = __uint_as_float(bc);
+            if constexpr (NCHW_OUT)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(vc, vp, acc[i][j], 0, 0, 0);
+            else
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(vp, vc, acc[i][j], 0, 0, 0);
+          }
+    }
+  };
+
+  // Prologue: stages 0 and 1 in LDS buffers 0 and 1, stages 2 and 3 in the
+  // pixel registers, weight stages 0 .. DB-1 in flight, the first K chunk of
+  // stage 0 being read.
+  uint4 fr[2][TP];
+  // One stage of the loop (u = stage mod U, a compile-time constant).  With
+  // `checked`, the MFMAs of stages past this group's end are skipped (the
+  // last, partial block of U stages); the full blocks run branch-free.
+  auto stage = [&](auto u_c, auto checked, int st) {
+    constexpr int u = decltype(u_c)::value;
+#pragma unroll
+    for (int c = 0; c < HC; ++c) {
+      if (c + 1 < HC)
+        read_f(u % NB, c + 1, fr[(c + 1) & 1]);
+      else
+        read_f((u + 1) % NB, 0, fr[(c + 1) & 1]);
+      if constexpr (decltype(checked)::value) {
+        if (st < nsteps) mfma_chunk(fr[c & 1], rb[u % DB], c);
+      } else {
+        mfma_chunk(fr[c & 1], rb[u % DB], c);
+      }
+      if (c == 0) {
+        // stage st + 2 to LDS (its buffer last held stage st - 1, which
+        // every wave finished reading before the previous barrier), and the
+        // pixel loads of stage st + 2 + DA into the freed registers
+        store_a((u + 2) % NB, ra[(u + 2) % DA]);
+        load_a(ra[(u + 2) % DA], st + 2 + DA < nsteps);
+      }
+    }
+    load_b(rb[u % DB], st + DB < nsteps);
+    __syncthreads();
+  };
+  auto block = [&](auto checked, int s0) {
+    unroll_stages<U>([&](auto u_c) { stage(u_c, checked, s0 + decltype(u_c)::value); });
+  };
+  if (nsteps_all > 0) {
+    // stages 0, 1 through registers 0, 1 to LDS; then stages 2 .. DA+1 into
+    // registers (stage j in register j mod DA: the loop stores stage st + 2
+    // from register st mod DA and reloads it with stage st + 2 + DA)
+    load_a(ra[0], 0 < nsteps);
+    load_a(ra[1 % DA], 1 < nsteps);
+    if constexpr (DA == 2) {
+#pragma unroll
+      for (int d = 0; d < DB; ++d) load_b(rb[d], d < nsteps);
+      store_a(0, ra[0]);
+      store_a(1, ra[1]);
+    } else {
+      store_a(0, ra[0]);
+      store_a(1, ra[1]);
+#pragma unroll
+      for (int d = 0; d < DB; ++d) load_b(rb[d], d < nsteps);
+    }
+#pragma unroll
+    for (int j = 2; j < 2 + DA; ++j) load_a(ra[j % DA], j < nsteps);
+    __syncthreads();
+    read_f(0, 0, fr[0]);
+    // full blocks: every group has all of their stages when KS = 1 or the
+    // groups' channel blocks split evenly; otherwise the shorter group's
+    // extra stages multiply the zeros its loads returned
+    const int nfull = (KS == 1 || nsteps == nsteps_all) ? nsteps_all / U * U : 0;
+    for (int s = 0; s < nfull; s += U) block(std::false_type(), s);
+    for (int s = nfull; s < nsteps_all; s += U) block(std::true_type(), s);
+  } else {
+    __syncthreads();
+  }
+
+  if constexpr (KS > 1) {
+    float* red = (float*)smem_all + wave * (TP * TC * 16 * 64) + lane;
+    if (grp == 1) {
+#pragma unroll
+      for (int i = 0; i < TP; ++i)
+#pragma unroll
+        for (int j = 0; j < TC; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) red[((i * TC + j) * 16 + r) * 64] = acc[i][j][r];
+    }
+    __syncthreads();
+    if (grp != 0) return;
+#pragma unroll
+    for (int i = 0; i < TP; ++i)
+#pragma unroll
+      for (int j = 0; j < TC; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] += red[((i * TC + j) * 16 + r) * 64];
+  }
+  const int ch0 = wk.n0 + wave * RD;
+  if (a.ksplit > 1) {
+    store_tile<false, NCHW_OUT, TP, TC>(a, sg, wk.m1, a.part + (size_t)wk.ks * a.part_stride, acc,
+                                        wk.m0, ch0, lane, s_bias - wk.n0);
+  } else {
+    store_tile<BF16, NCHW_OUT, TP, TC>(a, sg, wk.m1, a.y[sg.plan], acc, wk.m0, ch0, lane,
+                                       s_bias - wk.n0);
+  }
+}
+
 template <bool BF16, bool NCHW_OUT, int CFG>
 static void launch_one(const GemmArgs& a, hipStream_t stream) {
   constexpr TileShape t = kTiles[CFG];
   if constexpr (t.kind == 0)
     hipLaunchKernelGGL((phase_gemm_kernel<BF16, t.bm, t.bn, t.pw, t.cw, t.kb, t.depth, NCHW_OUT>),
                        dim3(a.n_works), dim3(t.pw * t.cw * 64), 0, stream, a);
+  else if constexpr (t.kind == 3)
+    hipLaunchKernelGGL((phase_gemm3_kernel<BF16, t.bm, t.bn, t.pw * t.cw, t.kb, t.depth % 10,
+                                           t.depth / 10, t.ksplit, NCHW_OUT>),
+                       dim3(a.n_works), dim3(t.pw * t.cw * t.ksplit * 64), 0, stream, a);
   else
     hipLaunchKernelGGL((phase_gemm2_kernel<BF16, t.bm, t.bn, t.pw * t.cw, t.kb, t.depth,
                                            t.kind == 1, t.ksplit, NCHW_OUT>),
@@ -1262,6 +1583,181 @@ __global__ __launch_bounds__(kRpThreads) void rowphase_kernel(RpArgs a) {
       store_stream16(yrow + v * 8, make_uint4(wv[0], wv[1], wv[2], wv[3]));
     }
   }
+}
+
+// ---------------------------------------------------------------------------
+// Column-phase form of a transposed conv with column stride 32 (the FCN-32s
+// upsampling shape).  Output column o with o + pad_w = 32*Q_w + rho_w takes
+// kernel columns rho_w + 32*tw from input column Q_w - tw (tw = 0, 1); row
+// phase rho_h likewise takes kernel rows rho_h + s_h*th from input row Q - th.
+// For one (k, rho_h) the 32 column phases share the input fragments, so they
+// are the 32 rows of an MFMA tile whose columns are input positions (Q, Q_w):
+// each result column is then 32 consecutive elements of one output row,
+// which after one exchange between the wave halves go out as 16-byte pieces.
+
+template <int KBLK, int ACT>
+__global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t s_x[];  // [(h+2)*(w+2)][cp]
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int rblocks = (a.stride_h + kCpWaves - 1) / kCpWaves;
+  int b = blockIdx.x;
+  const int rb = b % rblocks;
+  b /= rblocks;
+  const int img = b % a.n, k = b / a.n;
+  const int rho_h = rb * kCpWaves + wave;
+  constexpr int kblk = KBLK;  // K blocks of 16: 4 taps x cp channels (cp = 4 * KBLK)
+  const int wp2 = a.w + 2;
+
+  // this wave's weight fragments (row rho_w = lane % 32, K run 2*kb + lane/32)
+  uint4 wa[KBLK];
+  const bool live = rho_h < a.stride_h;
+  {
+    const uint4* src = (const uint4*)a.wp + ((size_t)(k * a.stride_h + (live ? rho_h : 0)) * kblk) * 64 + lane;
+#pragma unroll
+    for (int kb = 0; kb < kblk; ++kb) wa[kb] = src[kb * 64];
+  }
+  // image img's input, channel-contiguous, with a border of zeros; the
+  // elements go 16 per thread at a time, all loads before the LDS stores,
+  // so that their latencies overlap
+  const int npix = (a.h + 2) * wp2;
+  const int total = npix * a.cp;
+  const uint16_t* xin = (const uint16_t*)a.x + (size_t)img * a.cin * a.h * a.w;
+  constexpr int SU = 16;
+  for (int e0 = tid; e0 < total; e0 += SU * kCpWaves * 64) {
+    uint16_t v[SU];
+    int dst[SU];
+#pragma unroll
+    for (int u = 0; u < SU; ++u) {
+      const int e = e0 + u * kCpWaves * 64;
+      const int t = (int)fast_div((uint32_t)e, a.dv_mul[0], a.dv_shift[0]);
+      const int pj = e - t * wp2;
+      const int c = (int)fast_div((uint32_t)t, a.dv_mul[1], a.dv_shift[1]);
+      const int pi = t - c * (a.h + 2);
+      const int i = pi - 1, j = pj - 1;
+      const bool in = e < total && c < a.cin && i >= 0 && i < a.h && j >= 0 && j < a.w;
+      // branch-free: an element outside the input reads x[0] and keeps 0
+      const uint16_t xv = xin[in ? ((size_t)c * a.h + i) * a.w + j : 0];
+      v[u] = in ? xv : (uint16_t)0;
+      dst[u] = e < total ? (pi * wp2 + pj) * a.cp + c : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < SU; ++u)
+      if (dst[u] >= 0) s_x[dst[u]] = v[u];
+  }
+  const float bk = a.bias ? a.bias[k] : 0.f;
+  __syncthreads();
+  if (!live) return;
+
+  const int q_lo = -floor_div_d(-(a.pad_h - rho_h), a.stride_h);
+  const int q_hi = floor_div_d(a.ho - 1 + a.pad_h - rho_h, a.stride_h);
+  const int nq = q_hi - q_lo + 1;
+  if (nq <= 0) return;
+  const int half = lane >> 5, col32 = lane & 31;
+  const int rpt = a.cp / 8;  // 8-channel runs per tap
+  uint16_t* yk = (uint16_t*)a.y + ((size_t)img * a.cout + k) * a.ho * a.wo;
+  // this wave's output rows, kCpRows at a time, assembled in LDS and then
+  // written whole (16 bytes per lane, consecutive lanes consecutive pieces)
+  uint16_t* s_o = s_x + (size_t)(a.h + 2) * wp2 * a.cp + (size_t)wave * kCpRows * a.wo;
+  const int vpr = a.wo / 8;  // 16-byte pieces per output row
+  for (int q0 = 0; q0 < nq; q0 += kCpRows) {
+    const int nr = min(kCpRows, nq - q0);
+    const int ncol = nr * a.nqw;
+    for (int c0 = 0; c0 < ncol; c0 += 32) {
+      const int col = min(c0 + col32, ncol - 1);
+      const int qi = (int)fast_div((uint32_t)col, a.dv_mul[2], a.dv_shift[2]);
+      const int Q = q_lo + q0 + qi, Qw = a.qw_lo + col - qi * a.nqw;
+      f32x16 acc;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < kblk; ++kb) {
+        const int run = 2 * kb + half;
+        const int t = (int)fast_div((uint32_t)run, a.dv_mul[3], a.dv_shift[3]);
+        const int cc = (run - t * rpt) * 8;
+        const int pi = Q - (t >> 1) + 1, pj = Qw - (t & 1) + 1;
+        const uint4 xv = *(const uint4*)(s_x + (pi * wp2 + pj) * a.cp + cc);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, wa[kb]),
+                                                      __builtin_bit_cast(bf16x8, xv), acc, 0, 0, 0);
+      }
+      // rows 8g + 4*half + (0..3) of this column are four consecutive output
+      // elements of row qi: one 8-byte LDS write each
+      if (c0 + col32 < ncol) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int ow0 = 32 * Qw + 8 * g + 4 * half - a.pad_w;
+          if (ow0 < 0 || ow0 >= a.wo) continue;
+          uint32_t pk[2];
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            const uint32_t lo = f32_to_bf16_rne(activate(acc[4 * g + 2 * e] + bk, ACT));
+            const uint32_t hi = f32_to_bf16_rne(activate(acc[4 * g + 2 * e + 1] + bk, ACT));
+            pk[e] = lo | (hi << 16);
+          }
+          *(uint2*)(s_o + qi * a.wo + ow0) = make_uint2(pk[0], pk[1]);
+        }
+      }
+    }
+    // the rows out: piece v of row qi from LDS to the output
+    for (int qi = 0; qi < nr; ++qi) {
+      const int oh = a.stride_h * (q_lo + q0 + qi) + rho_h - a.pad_h;
+      for (int v = lane; v < vpr; v += 64)
+        *(uint4*)(yk + (size_t)oh * a.wo + 8 * v) = *(const uint4*)(s_o + qi * a.wo + 8 * v);
+    }
+  }
+}
+
+hipError_t launch_colphase(const CpArgs& a, hipStream_t stream) {
+  const int rblocks = (a.stride_h + kCpWaves - 1) / kCpWaves;
+  const dim3 grid(a.cout * a.n * rblocks);
+  const size_t lds = ((size_t)(a.h + 2) * (a.w + 2) * a.cp + (size_t)kCpWaves * kCpRows * a.wo) * 2;
+  const int kblk = a.cp / 4;
+#define HUGE2_CP_LAUNCH(KB, ACT)                                                            \
+  if (kblk == KB && a.act == ACT)                                                           \
+    hipLaunchKernelGGL((colphase_kernel<KB, ACT>), grid, dim3(kCpWaves * 64), lds, stream, a);
+  HUGE2_CP_LAUNCH(2, 0) HUGE2_CP_LAUNCH(2, 1) HUGE2_CP_LAUNCH(2, 2)
+  HUGE2_CP_LAUNCH(4, 0) HUGE2_CP_LAUNCH(4, 1) HUGE2_CP_LAUNCH(4, 2)
+  HUGE2_CP_LAUNCH(6, 0) HUGE2_CP_LAUNCH(6, 1) HUGE2_CP_LAUNCH(6, 2)
+  HUGE2_CP_LAUNCH(8, 0) HUGE2_CP_LAUNCH(8, 1) HUGE2_CP_LAUNCH(8, 2)
+#undef HUGE2_CP_LAUNCH
+  return hipGetLastError();
+}
+
+// Weights of the column-phase form: per (k, rho_h), K block kb and lane l the
+// 8 values w[c, k, rho_h + s_h*th, rho_w + 32*tw] for c in [c0, c0 + 8), with
+// rho_w = l % 32, K run 2*kb + l/32 = tap * (cp/8) + c0/8, tap = 2*th + tw
+// (zero for c >= c_in or a kernel index past the kernel).
+__global__ void pack_colphase_kernel(const uint16_t* __restrict__ w, uint16_t* __restrict__ wp,
+                                     int cin, int cout, int r, int s, int stride_h, int cp,
+                                     long long total) {
+  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const int e = (int)(idx % 8);
+    long long t = idx / 8;
+    const int lane = (int)(t % 64);
+    t /= 64;
+    const int kblk = cp / 4;
+    const int kb = (int)(t % kblk);
+    t /= kblk;
+    const int rho_h = (int)(t % stride_h);
+    const int k = (int)(t / stride_h);
+    const int rho_w = lane % 32, run = 2 * kb + lane / 32, rpt = cp / 8;
+    const int tap = run / rpt, c = (run - tap * rpt) * 8 + e;
+    const int kh = rho_h + stride_h * (tap >> 1), kw = rho_w + 32 * (tap & 1);
+    uint16_t v = 0;
+    if (c < cin && kh < r && kw < s) v = w[(((long long)c * cout + k) * r + kh) * s + kw];
+    wp[idx] = v;
+  }
+}
+
+hipError_t launch_pack_colphase(const void* w, void* wp, int cin, int cout, int r, int s,
+                                int stride_h, int cp, hipStream_t stream) {
+  const long long total = (long long)cout * stride_h * (cp / 4) * 64 * 8;
+  const long long want = (total + 255) / 256;
+  const int grid = (int)(want < 65536 ? want : 65536);
+  hipLaunchKernelGGL(pack_colphase_kernel, dim3(grid), dim3(256), 0, stream, (const uint16_t*)w,
+                     (uint16_t*)wp, cin, cout, r, s, stride_h, cp, total);
+  return hipGetLastError();
 }
 
 hipError_t launch_rowphase(const RpArgs& a, hipStream_t stream) {
@@ -1756,6 +2252,92 @@ hipError_t launch_gather_taps(const GatherArgs& a, int dtype, hipStream_t stream
     hipLaunchKernelGGL(gather_taps_kernel<uint16_t>, dim3(blocks), dim3(256), 0, stream, a);
   else
     hipLaunchKernelGGL(gather_taps_kernel<uint32_t>, dim3(blocks), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Grouped and depthwise convolutions (see GrArgs).
+template <typename T>
+__device__ __forceinline__ float to_f32(T v) {
+  if constexpr (std::is_same<T, uint16_t>::value)
+    return __uint_as_float((uint32_t)v << 16);
+  else
+    return __uint_as_float(v);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void grouped_kernel(GrArgs a, long long total) {
+  const T* __restrict__ x = (const T*)a.x;
+  const T* __restrict__ w = (const T*)a.w;
+  const int cig = a.cin / a.groups, cog = a.cout / a.groups;
+  for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (long long)gridDim.x * blockDim.x) {
+    long long t = idx;
+    int k, oh, ow, n;
+    if (a.nhwc) {
+      k = (int)(t % a.cout);
+      t /= a.cout;
+      ow = (int)(t % a.wo);
+      t /= a.wo;
+      oh = (int)(t % a.ho);
+      n = (int)(t / a.ho);
+    } else {
+      ow = (int)(t % a.wo);
+      t /= a.wo;
+      oh = (int)(t % a.ho);
+      t /= a.ho;
+      k = (int)(t % a.cout);
+      n = (int)(t / a.cout);
+    }
+    const int g = k / cog, kg = k - g * cog, c0 = g * cig;
+    float acc = 0.f;
+    for (int m = 0; m < a.r; ++m) {
+      int ih;
+      if (a.transposed) {
+        const int num = oh + a.pad_h - m * a.dil_h;  // = ih * stride_h on the phase's taps
+        if (num < 0 || num % a.stride_h != 0) continue;
+        ih = num / a.stride_h;
+      } else {
+        ih = oh * a.stride_h - a.pad_h + m * a.dil_h;
+      }
+      if (ih < 0 || ih >= a.h) continue;
+      for (int q = 0; q < a.s; ++q) {
+        int iw;
+        if (a.transposed) {
+          const int num = ow + a.pad_w - q * a.dil_w;
+          if (num < 0 || num % a.stride_w != 0) continue;
+          iw = num / a.stride_w;
+        } else {
+          iw = ow * a.stride_w - a.pad_w + q * a.dil_w;
+        }
+        if (iw < 0 || iw >= a.w_) continue;
+        for (int ci = 0; ci < cig; ++ci) {
+          const int c = c0 + ci;
+          const size_t xi = a.nhwc ? (((size_t)n * a.h + ih) * a.w_ + iw) * a.cin + c
+                                   : (((size_t)n * a.cin + c) * a.h + ih) * a.w_ + iw;
+          const size_t wi = a.transposed ? (((size_t)c * cog + kg) * a.r + m) * a.s + q
+                                         : (((size_t)k * cig + ci) * a.r + m) * a.s + q;
+          acc = fmaf(to_f32(x[xi]), to_f32(w[wi]), acc);
+        }
+      }
+    }
+    const float v = activate(acc + (a.bias ? a.bias[k] : 0.f), a.act);
+    if constexpr (std::is_same<T, uint16_t>::value)
+      ((uint16_t*)a.y)[idx] = f32_to_bf16_rne(v);
+    else
+      ((float*)a.y)[idx] = v;
+  }
+}
+
+hipError_t launch_grouped(const GrArgs& a, int dtype, hipStream_t stream) {
+  const long long total = (long long)a.n * a.cout * a.ho * a.wo;
+  const long long want = (total + 255) / 256;
+  const int grid = (int)(want < 1048576 ? want : 1048576);
+  if (total == 0) return hipSuccess;
+  if (dtype == 1)
+    hipLaunchKernelGGL(grouped_kernel<uint16_t>, dim3(grid), dim3(256), 0, stream, a, total);
+  else
+    hipLaunchKernelGGL(grouped_kernel<uint32_t>, dim3(grid), dim3(256), 0, stream, a, total);
   return hipGetLastError();
 }
 

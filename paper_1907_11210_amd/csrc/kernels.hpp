@@ -59,8 +59,14 @@ constexpr int kMaxLdsTaps = 64;  // taps per segment staged in LDS (more: scalar
 // output channels from n0 of segment seg, over the input channel blocks of K
 // slice ks (of GemmArgs::ksplit), with the taps [tap_begin, tap_begin +
 // tap_count) of the tap list (the segment's taps, or a listed tile's own).
+// When those taps are the product of two arithmetic progressions (ap_ntw >
+// 0), tap t = (th, tw) = (t / ap_ntw, t % ap_ntw) is kernel tap (ap_kh0 +
+// th*ap_dkh, ap_kw0 + tw*ap_dkw) at input offset (ap_off0_h + th*ap_doff_h,
+// ap_off0_w + tw*ap_doff_w), so that a kernel can step through them with two
+// counters and no memory reads.
 struct WorkDev {
-  int32_t seg, m0, m1, n0, ks, tap_begin, tap_count, pad;
+  int32_t seg, m0, m1, n0, ks, tap_begin, tap_count;
+  int32_t ap_ntw, ap_kh0, ap_dkh, ap_kw0, ap_dkw, ap_off0_h, ap_doff_h, ap_off0_w, ap_doff_w;
 };
 
 constexpr int kMaxGroup = 8;  // plans of one grouped launch (huge2_group)
@@ -103,6 +109,9 @@ struct GemmArgs {
 // kind 0: both operands through LDS, PW x CW waves of (BM/PW) x (BN/CW).
 // kind 1: split-wave form, the pixel tile through LDS, CW waves each loading
 //         BN/CW weight rows itself (PW = 1) from lane-ordered packed weights.
+// kind 3: the same tile and packing, pipelined over three LDS stage buffers
+//         (phase_gemm3_kernel; depth = 10 x weight stages in flight + pixel
+//         stages held in registers).
 // ksplit (split-wave kinds): K groups of PW x CW waves per workgroup, each
 // over its own share of the input-channel blocks, summed in LDS at the end.
 struct TileShape {
@@ -120,9 +129,7 @@ enum TileCfg {
   TILE_SW_64x128_K2 = 6,   // as TILE_SW_64x128, two K groups (8 waves)
   TILE_SW_128x128_K2 = 7,  // split-wave: 4 waves of 128 x 32 channels, two K groups
   TILE_SW_128x256 = 8,   // split-wave: 8 waves of 128 x 32 channels
-  TILE_SW_128x256_W4 = 9,   // split-wave: 4 waves of 128 x 64 channels
-  TILE_SW_128x256_W4D4 = 10,  // as 9, four stages in flight
-  TILE_SW_128x256_K2 = 11,  // as 9, two K groups (8 waves), two stages in flight
+  TILE_P3_128x256 = 9,   // pipelined split-wave: 8 waves of 128 x 32 channels
 };
 constexpr TileShape kTiles[] = {
     {128, 128, 4, 2, 128, 2, 2, 0},     // TILE_128x128
@@ -134,9 +141,7 @@ constexpr TileShape kTiles[] = {
     {64, 128, 1, 4, 128, 4, 1, 1, 2},   // TILE_SW_64x128_K2
     {128, 128, 1, 4, 128, 3, 1, 1, 2},  // TILE_SW_128x128_K2
     {128, 256, 1, 8, 128, 3, 1, 1, 1},  // TILE_SW_128x256
-    {128, 256, 1, 4, 128, 3, 1, 1, 1},  // TILE_SW_128x256_W4
-    {128, 256, 1, 4, 128, 4, 1, 1, 1},  // TILE_SW_128x256_W4D4
-    {128, 256, 1, 4, 128, 2, 1, 1, 2},  // TILE_SW_128x256_K2
+    {128, 256, 1, 8, 128, 32, 1, 3, 1},  // TILE_P3_128x256
 };
 // A split-K plan may switch from the two-K-group 64 x 128 tile to its
 // one-group form after the work list and the weight packing were laid out for
@@ -158,8 +163,8 @@ inline int tile_kb(int cfg) { return kTiles[cfg].kb; }
 // 16-byte row pad)
 inline int tile_lds(int cfg) {
   const TileShape& t = kTiles[cfg];
-  const int rows = t.kind == 0 ? t.bm + t.bn : (t.kind == 1 ? t.bm : t.bn);
-  return 2 * rows * (t.kb + 16);
+  const int rows = t.kind == 0 ? t.bm + t.bn : t.bm;
+  return (t.kind == 3 ? 3 : 2) * rows * (t.kb + 16);
 }
 constexpr int kMaxBlockK_bytes = 256;  // largest K block per stage: 128 bf16 or 64 fp32
 
@@ -238,6 +243,39 @@ struct RpArgs {
 };
 hipError_t launch_rowphase(const RpArgs& a, hipStream_t stream);
 
+// Column-phase form for a column stride of 32 (NCHW, bf16, dilation 1, at
+// most 32 input channels, kernel width <= 64, kernel height <= 2 * row
+// stride): the 32 column phases rho_w of an output block are the 32 rows of
+// one MFMA tile, so that its results are 32 consecutive output elements of
+// one output row.  Wave (output channel k, image n, row phase rho_h) runs
+//   C[rho_w][(Q, Q_w)] = sum over (th, tw, c) of
+//       Wp[k][rho_h][rho_w][(th, tw, c)] * X[n][c][Q - th][Q_w - tw]
+// (K = 4 taps x cp channels, cp = c_in padded to 8) with the input of image
+// n staged in LDS (channel-contiguous, one pixel of zeros around it).  Each
+// column's 32 results are output row rho_h + s_h*Q - pad_h, columns 32*Q_w -
+// pad_w + [0, 32): they go to an LDS copy of kCpRows output rows, which are
+// then written whole, 16 bytes per lane.
+constexpr int kCpWaves = 4;              // row phases per workgroup
+constexpr int kCpRows = 8;               // output rows per wave assembled in LDS at a time
+constexpr int kCpMaxLds = 64 * 1024;     // LDS bytes of the staged input and the output rows
+struct CpArgs {
+  const void* x;
+  const void* wp;  // [c_out][s_h][kblk][64 lanes][8 bf16] (pack_colphase_kernel)
+  const float* bias;
+  void* y;
+  int n, cin, h, w, cout, r, s;
+  int stride_h, pad_h, pad_w, ho, wo;
+  int cp;        // c_in padded to 8
+  int qw_lo, nqw;  // Q_w range of every row phase
+  int act;
+  // floor(v / d) = (v * mul) >> shift (division_magic) for d = w + 2, h + 2,
+  // nqw and cp / 8: the kernel's index arithmetic has no integer division
+  uint32_t dv_mul[4], dv_shift[4];
+};
+hipError_t launch_colphase(const CpArgs& a, hipStream_t stream);
+hipError_t launch_pack_colphase(const void* w, void* wp, int cin, int cout, int r, int s,
+                                int stride_h, int cp, hipStream_t stream);
+
 // All four phases per workgroup for the stride-2, 4x4, padding-1 transposed
 // conv (NCHW, bf16): every phase has 2 x 2 taps with input offsets in
 // [-1, 1] and the input's pixel grid.  Workgroup: 64 input positions (ni
@@ -270,6 +308,22 @@ struct QArgs {
   int act;           // huge2_activation, applied after the bias
 };
 hipError_t launch_quad(const QArgs& a, hipStream_t stream);
+
+// Grouped (and depthwise) convolution, direct: one thread per output
+// element, in the output's layout order.  Transposed (transposed = 1): output
+// o with o + pad = i*stride + m*dil takes input i through kernel tap m (the
+// taps of o's phase, section 3.1); dilated / strided: input o*stride - pad +
+// m*dil.  The sum runs over the taps and the input channels of the output
+// channel's group, in fp32, then bias, activation and rounding.
+struct GrArgs {
+  const void* x;
+  const void* w;   // the plan's copy of the weight, the caller's layout
+  const float* bias;
+  void* y;
+  int n, cin, h, w_, cout, r, s, stride_h, stride_w, pad_h, pad_w, dil_h, dil_w, ho, wo;
+  int groups, transposed, nhwc, act;
+};
+hipError_t launch_grouped(const GrArgs& a, int dtype, hipStream_t stream);
 
 // y[i] = act(bias[ch(i) / bias_div] + sum over s < ksplit, in order, of
 // part[s * stride + i]) in the dtype; ch(i) = (i / hw) % cout for NCHW, i %

@@ -174,6 +174,8 @@ huge2_status validate_desc(const huge2_conv_desc* d, bool transposed) {
   if (d->activation != HUGE2_ACT_NONE && d->activation != HUGE2_ACT_RELU &&
       d->activation != HUGE2_ACT_TANH)
     return HUGE2_ERR_INVALID_ARG;
+  if (d->groups < 0 || (d->groups > 1 && (d->c_in % d->groups != 0 || d->c_out % d->groups != 0)))
+    return HUGE2_ERR_INVALID_ARG;
   if (transposed) {
     if (d->out_pad_h >= std::max(d->stride_h, d->dil_h) ||
         d->out_pad_w >= std::max(d->stride_w, d->dil_w))

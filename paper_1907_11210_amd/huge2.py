@@ -47,7 +47,7 @@ class Huge2Error(RuntimeError):
 class ConvDesc(ctypes.Structure):
     _fields_ = [(f, ctypes.c_int32) for f in (
         "n", "c_in", "h", "w", "c_out", "r", "s", "stride_h", "stride_w", "pad_h", "pad_w",
-        "out_pad_h", "out_pad_w", "dil_h", "dil_w", "layout", "dtype", "activation")]
+        "out_pad_h", "out_pad_w", "dil_h", "dil_w", "layout", "dtype", "activation", "groups")]
 
 
 class Segment(ctypes.Structure):
@@ -123,13 +123,13 @@ def _pair(v):
 
 
 def make_desc(n, c_in, h, w, c_out, r, s, stride=1, padding=0, output_padding=0, dilation=1,
-              layout=HUGE2_NCHW, dtype=HUGE2_F32, activation=HUGE2_ACT_NONE):
+              layout=HUGE2_NCHW, dtype=HUGE2_F32, activation=HUGE2_ACT_NONE, groups=1):
     sh, sw = _pair(stride)
     ph, pw = _pair(padding)
     oph, opw = _pair(output_padding)
     dh, dw = _pair(dilation)
     return ConvDesc(n, c_in, h, w, c_out, r, s, sh, sw, ph, pw, oph, opw, dh, dw, layout, dtype,
-                    activation)
+                    activation, groups)
 
 
 # ---- the C entry points ---------------------------------------------------
@@ -314,7 +314,7 @@ def _act_code(activation):
 
 
 def _desc_for(x, w, transposed, stride, padding, output_padding, dilation, layout,
-              activation=None):
+              activation=None, groups=1):
     lay = _layout_code(layout)
     if x.dim() != 4 or w.dim() != 4:
         raise ValueError("x and w must be 4-D")
@@ -322,16 +322,19 @@ def _desc_for(x, w, transposed, stride, padding, output_padding, dilation, layou
         n, c_in, h, wd = x.shape
     else:
         n, h, wd, c_in = x.shape
+    g = int(groups)
     if transposed:
-        wc_in, c_out, r, s = w.shape
+        wc_in, cog, r, s = w.shape
+        c_out = cog * g
     else:
-        c_out, wc_in, r, s = w.shape
+        c_out, cig, r, s = w.shape
+        wc_in = cig * g
     if wc_in != c_in:
         raise ValueError("weight has %d input channels, x has %d" % (wc_in, c_in))
     if w.dtype != x.dtype:
         raise ValueError("x and w must share a dtype")
     return make_desc(n, c_in, h, wd, c_out, r, s, stride, padding, output_padding, dilation,
-                     lay, _dtype_code(x), _act_code(activation))
+                     lay, _dtype_code(x), _act_code(activation), g)
 
 
 def _out_shape(desc, transposed):
@@ -356,15 +359,16 @@ def _stream(x):
 
 
 def conv2d_transpose(x, w, bias=None, stride=1, padding=0, output_padding=0, dilation=1,
-                     layout="NCHW", out=None, activation=None):
-    """Transposed conv on the GPU (w: [C_in, C_out, R, S]); returns
+                     layout="NCHW", out=None, activation=None, groups=1):
+    """Transposed conv on the GPU (w: [C_in, C_out/groups, R, S]); returns
     y = activation(op(x) + bias), activation None, "relu" or "tanh"."""
     torch = _torch()
     _check_tensor(x, "x")
     _check_tensor(w, "w", x.device)
-    desc = _desc_for(x, w, True, stride, padding, output_padding, dilation, layout, activation)
+    desc = _desc_for(x, w, True, stride, padding, output_padding, dilation, layout, activation,
+                     groups)
     shape = _out_shape(desc, True)
-    if desc.c_out != w.shape[1] or bias is not None and bias.numel() != desc.c_out:
+    if bias is not None and bias.numel() != desc.c_out:
         raise ValueError("bias size does not match C_out")
     y = out if out is not None else torch.empty(shape, dtype=x.dtype, device=x.device)
     _check_tensor(y, "out", x.device)
@@ -376,13 +380,13 @@ def conv2d_transpose(x, w, bias=None, stride=1, padding=0, output_padding=0, dil
 
 
 def conv2d_dilated(x, w, bias=None, stride=1, padding=0, dilation=1, layout="NCHW", out=None,
-                   activation=None):
-    """Dilated / strided conv on the GPU (w: [C_out, C_in, R, S]); returns
+                   activation=None, groups=1):
+    """Dilated / strided conv on the GPU (w: [C_out, C_in/groups, R, S]); returns
     y = activation(op(x) + bias)."""
     torch = _torch()
     _check_tensor(x, "x")
     _check_tensor(w, "w", x.device)
-    desc = _desc_for(x, w, False, stride, padding, 0, dilation, layout, activation)
+    desc = _desc_for(x, w, False, stride, padding, 0, dilation, layout, activation, groups)
     shape = _out_shape(desc, False)
     if bias is not None and bias.numel() != desc.c_out:
         raise ValueError("bias size does not match C_out")
@@ -463,7 +467,7 @@ class Plan:
     :meth:`__call__` enqueues huge2_plan_execute on the current stream."""
 
     def __init__(self, w, x_shape, transposed, stride=1, padding=0, output_padding=0,
-                 dilation=1, layout="NCHW", activation=None):
+                 dilation=1, layout="NCHW", activation=None, groups=1):
         torch = _torch()
         _check_tensor(w, "w")
         dummy = torch.empty(0, dtype=w.dtype)
@@ -472,14 +476,17 @@ class Plan:
             n, c_in, h, wd = x_shape
         else:
             n, h, wd, c_in = x_shape
+        g = int(groups)
         if transposed:
-            wc_in, c_out, r, s = w.shape
+            wc_in, cog, r, s = w.shape
+            c_out = cog * g
         else:
-            c_out, wc_in, r, s = w.shape
+            c_out, cig, r, s = w.shape
+            wc_in = cig * g
         if wc_in != c_in:
             raise ValueError("weight has %d input channels, x has %d" % (wc_in, c_in))
         self.desc = make_desc(n, c_in, h, wd, c_out, r, s, stride, padding, output_padding,
-                              dilation, lay, _dtype_code(dummy), _act_code(activation))
+                              dilation, lay, _dtype_code(dummy), _act_code(activation), g)
         self.transposed = bool(transposed)
         self.device = w.device
         self.dtype = w.dtype

@@ -73,6 +73,7 @@ class Layer:
     layout: str  # "NCHW" or "NHWC"
     dtype: str   # "f32" or "bf16"
     act: str = "none"  # epilogue function after the bias: "none", "relu" or "tanh"
+    groups: int = 1    # grouped convolution (groups = c_in: depthwise)
 
     def out_hw(self):
         if self.transposed:
@@ -84,8 +85,8 @@ class Layer:
         return ho, wo
 
     def w_shape(self):
-        return ((self.c_in, self.c_out, self.r, self.s) if self.transposed
-                else (self.c_out, self.c_in, self.r, self.s))
+        return ((self.c_in, self.c_out // self.groups, self.r, self.s) if self.transposed
+                else (self.c_out, self.c_in // self.groups, self.r, self.s))
 
     def with_(self, **kw):
         return dataclasses.replace(self, **kw)

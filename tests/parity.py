@@ -49,9 +49,10 @@ def oracle_full(layer, xq, wq, bias=None, absolute=False):
         x, w, b = np.abs(x), np.abs(w), None if b is None else np.abs(b)
     if layer.transposed:
         y = oracle.conv2d_transpose_alg1(x, w, b, layer.stride, layer.pad, layer.out_pad,
-                                         layer.dil)
+                                         layer.dil, groups=layer.groups)
     else:
-        y = oracle.conv2d_dilated_alg2(x, w, b, layer.stride, layer.pad, layer.dil)
+        y = oracle.conv2d_dilated_alg2(x, w, b, layer.stride, layer.pad, layer.dil,
+                                       groups=layer.groups)
     # |act(u) - act(v)| <= |u - v| for both functions: the bound of the
     # absolute-value run still holds after the activation
     return y if absolute else oracle.activate(y, layer.act)
@@ -65,15 +66,16 @@ def oracle_points(layer, xq, wq, idx, bias=None, absolute=False):
         x, w, b = np.abs(x), np.abs(w), None if b is None else np.abs(b)
     if layer.transposed:
         y = oracle.conv2d_transpose_points(x, w, idx, b, layer.stride, layer.pad,
-                                           layer.out_pad, layer.dil)
+                                           layer.out_pad, layer.dil, groups=layer.groups)
     else:
-        y = oracle.conv2d_dilated_points(x, w, idx, b, layer.stride, layer.pad, layer.dil)
+        y = oracle.conv2d_dilated_points(x, w, idx, b, layer.stride, layer.pad, layer.dil,
+                                         groups=layer.groups)
     return y if absolute else oracle.activate(y, layer.act)
 
 
 def make_plan(layer, w_dev):
     return h2.Plan(w_dev, _x_shape(layer), layer.transposed, layer.stride, layer.pad,
-                   layer.out_pad, layer.dil, layer.layout, layer.act)
+                   layer.out_pad, layer.dil, layer.layout, layer.act, layer.groups)
 
 
 def _x_shape(layer):
@@ -102,10 +104,11 @@ def run_gpu(layer, xq, wq, bias=None, one_shot=False, plan=None, prefill_nan=Fal
     if one_shot:
         if layer.transposed:
             y = h2.conv2d_transpose(x_dev, w_dev, b_dev, layer.stride, layer.pad, layer.out_pad,
-                                    layer.dil, layer.layout, activation=layer.act)
+                                    layer.dil, layer.layout, activation=layer.act,
+                                    groups=layer.groups)
         else:
             y = h2.conv2d_dilated(x_dev, w_dev, b_dev, layer.stride, layer.pad, layer.dil,
-                                  layer.layout, activation=layer.act)
+                                  layer.layout, activation=layer.act, groups=layer.groups)
     else:
         p = plan if plan is not None else make_plan(layer, w_dev)
         y = p(x_dev, b_dev)

@@ -186,3 +186,22 @@ def test_group_entry_points_validate_without_gpu(L):
     assert out.value is None
     assert L.huge2_group_execute(None, None, None, None, None) == h2.HUGE2_ERR_INVALID_ARG
     assert L.huge2_group_destroy(None) == h2.HUGE2_OK
+
+
+def test_groups_validated_without_gpu(L):
+    """groups must divide both channel counts; grouped layers have no weight
+    gradient and their MAC count is the ungrouped one over groups."""
+    import ctypes
+    d = h2.make_desc(1, 6, 5, 5, 4, 3, 3, 2, 1, 0, 1, h2.HUGE2_NHWC, h2.HUGE2_BF16)
+    full = h2.huge2_plan_macs(d, 1)[0]
+    d.groups = 2
+    assert h2.huge2_plan_macs(d, 1) == (full // 2, full // 2)
+    for bad in (4, -1):
+        d.groups = bad
+        nz, iss = ctypes.c_int64(), ctypes.c_int64()
+        assert L.huge2_plan_macs(ctypes.byref(d), 1, ctypes.byref(nz), ctypes.byref(iss)) == \
+            h2.HUGE2_ERR_INVALID_ARG
+    d.groups = 2
+    p = ctypes.c_void_p()
+    assert L.huge2_wgrad_plan_create(ctypes.byref(p), ctypes.byref(d), 1) in (
+        h2.HUGE2_ERR_UNSUPPORTED, h2.HUGE2_ERR_INVALID_ARG)

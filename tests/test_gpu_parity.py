@@ -657,3 +657,73 @@ def test_group_rejects_unlike_plans():
     finally:
         pa.close()
         pb.close()
+
+
+COLPHASE_LAYERS = [
+    L("cp_fcn_reduced", True, 2, 21, 5, 6, 21, 64, 64, 32, 16, 0, 1, "NCHW", "bf16"),
+    # 32 input channels, a short kernel (phases with one tap or none per axis)
+    L("cp_c32_short", True, 1, 32, 3, 4, 8, 36, 40, 32, 8, 0, 1, "NCHW", "bf16"),
+    # output padding, a kernel shorter than two row strides
+    L("cp_outpad", True, 3, 5, 4, 3, 6, 30, 64, 32, 8, 8, 1, "NCHW", "bf16"),
+    # no padding: the first and last column blocks are whole
+    L("cp_pad0", True, 1, 12, 2, 2, 33, 64, 64, 32, 0, 0, 1, "NCHW", "bf16"),
+]
+
+
+@pytest.mark.parametrize("colphase", [1, 0])
+@pytest.mark.parametrize("layer", COLPHASE_LAYERS, ids=lambda l: l.name)
+def test_colphase_form(layer, colphase, monkeypatch):
+    """Column stride 32: the column-phase form (the 32 column phases as MFMA
+    rows, 16-byte row pieces) and, with it switched off, the other forms all
+    match the oracle and write every output element."""
+    monkeypatch.setenv("HUGE2_COLPHASE", str(colphase))
+    layer = layer.with_(act="relu")
+    P.say("case", layer, "HUGE2_COLPHASE", colphase)
+    xq, wq = _inputs(layer, seed=37)
+    bias = torch.linspace(-0.5, 0.5, layer.c_out)
+    ref = P.oracle_full(layer, xq, wq, bias)
+    absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
+    y = P.run_gpu(layer, xq, wq, bias, prefill_nan=True)
+    P.check(y, ref, absref, layer.dtype, layer.name)
+    plan = P.make_plan(layer, wq.contiguous().to(torch.device("cuda", 0)))
+    try:
+        assert plan.kernel.startswith("colphase_kernel") == bool(colphase), plan.kernel
+    finally:
+        plan.close()
+
+
+def LG(name, tr, n, ci, h, w, co, r, s, st, pd, op, dl, layout, dtype, groups):
+    return Layer(name, tr, n, ci, h, w, co, r, s, st, pd, op, dl, layout, dtype, "none", groups)
+
+
+GROUPED_LAYERS = [
+    # depthwise transposed upsampling (groups = C_in = C_out)
+    LG("gp_dw_ct_nhwc", True, 2, 64, 8, 8, 64, 4, 4, 2, 1, 0, 1, "NHWC", "bf16", 64),
+    # depthwise with channel multiplier 2 and output padding
+    LG("gp_dw_mult2_f32", True, 2, 8, 5, 6, 16, 3, 3, 2, 1, 1, 1, "NCHW", "f32", 8),
+    LG("gp_ct_g4", True, 1, 32, 6, 5, 48, 3, 3, 2, 1, 0, 1, "NHWC", "bf16", 4),
+    LG("gp_dil_g3", False, 2, 24, 9, 10, 36, 3, 3, 1, 2, 0, 2, "NCHW", "bf16", 3),
+    LG("gp_dw_strided_dil", False, 1, 16, 11, 9, 16, 3, 3, 2, 2, 0, 2, "NHWC", "f32", 16),
+]
+
+
+@pytest.mark.parametrize("layer", GROUPED_LAYERS, ids=lambda l: l.name)
+def test_grouped_and_depthwise(layer):
+    """Grouped and depthwise transposed / dilated convs (the descriptor's
+    groups) against the grouped oracle, plan and one-shot entry points, every
+    output element written."""
+    layer = layer.with_(act="relu")
+    P.say("case", layer)
+    xq, wq = _inputs(layer, seed=43)
+    bias = torch.linspace(-0.5, 0.5, layer.c_out)
+    ref = P.oracle_full(layer, xq, wq, bias)
+    absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
+    P.check(P.run_gpu(layer, xq, wq, bias, prefill_nan=True), ref, absref, layer.dtype, layer.name)
+    P.check(P.run_gpu(layer, xq, wq, bias, one_shot=True), ref, absref, layer.dtype, layer.name)
+    plan = P.make_plan(layer, wq.contiguous().to(torch.device("cuda", 0)))
+    try:
+        assert plan.kernel.startswith("grouped_kernel"), plan.kernel
+        nz, issued = plan.macs()
+        assert nz == issued
+    finally:
+        plan.close()

@@ -101,12 +101,26 @@ typedef struct huge2_plan huge2_plan; /* opaque */
 /* Human-readable name of a status code (static storage; never NULL). */
 const char* huge2_status_str(huge2_status status);
 
-/* Output height/width of the operation described by desc.
- * transposed = 1: the transposed conv; 0: the dilated/strided conv.
+/* Output height/width of the operation described by desc: the loop bounds
+ * of Algorithm 1 (transposed = 1: h_out = (h-1)*stride - 2*pad +
+ * dil*(r-1) + out_pad + 1) and Algorithm 2 (transposed = 0: h_out =
+ * floor((h + 2*pad - dil*(r-1) - 1)/stride) + 1), section 2.1.1, read as
+ * the output range those definitions cover (the printed bounds are garbled).
  * Host only, no HIP call.  INVALID_ARG if the descriptor is invalid or the
  * output would be empty. */
 huge2_status huge2_output_shape(const huge2_conv_desc* desc, int32_t transposed, int32_t* h_out,
                                 int32_t* w_out);
+
+/* The data gradient of a strided / dilated conv (section 3.2.3: the error
+ * maps are carried back through the same kernel) is the transposed conv of
+ * dy with the same weight array, stride, padding and dilation; several input
+ * sizes h give one output size, and the output padding of that transposed
+ * conv picks the right one.  For the strided conv described by conv_desc
+ * (input h x w), writes the output padding (*op_h, *op_w) that makes the
+ * transposed conv of its h_out x w_out output return exactly h x w.
+ * Host only.  INVALID_ARG for an invalid descriptor or NULL outputs. */
+huge2_status huge2_dgrad_output_padding(const huge2_conv_desc* conv_desc, int32_t* op_h,
+                                        int32_t* op_w);
 
 /* Build a reusable plan (the decomposition of section 3.1 done once per
  * layer): enumerates the phases, their kernel taps and border classes on the
@@ -127,11 +141,14 @@ huge2_status huge2_output_shape(const huge2_conv_desc* desc, int32_t transposed,
 huge2_status huge2_plan_create(huge2_plan** out, const huge2_conv_desc* desc, int32_t transposed,
                                const void* w, void* hip_stream);
 
-/* Run a plan: y = op(x) (+ bias).  x and y are laid out per the plan's
- * descriptor; bias is NULL or [c_out] float.  Enqueues on hip_stream the
- * phase GEMM kernel, preceded, when x is NCHW or its channel count is not a
- * multiple of 16 bytes, by a kernel that re-lays x out into the plan's
- * channel-contiguous staging buffer.  A plan is immutable once created; two
+/* Run a plan: y = op(x) (+ bias) -- Algorithm 1 or 2 (section 2.1.1)
+ * computed by the phase decomposition of section 3.1-3.2.  x and y are laid
+ * out per the plan's descriptor; bias is NULL or [c_out] float.  Enqueues on
+ * hip_stream the plan's main kernel (the phase GEMM or one of its direct
+ * forms, huge2_plan_kernel names it), preceded, when x is NCHW or its
+ * channel count is not a multiple of 16 bytes and the main kernel reads a
+ * channel-contiguous input, by a kernel that re-lays x out into the plan's
+ * staging buffer.  A plan is immutable once created; two
  * executes of one plan that needs staging must not overlap (they share the
  * staging buffer).  Errors: INVALID_ARG (null plan/x/y, x == y), HIP (launch
  * failure). */

@@ -1958,6 +1958,21 @@ huge2_status huge2_output_shape(const huge2_conv_desc* desc, int32_t transposed,
   return HUGE2_OK;
 }
 
+huge2_status huge2_dgrad_output_padding(const huge2_conv_desc* conv_desc, int32_t* op_h,
+                                        int32_t* op_w) {
+  if (!op_h || !op_w) return HUGE2_ERR_INVALID_ARG;
+  huge2_status st = validate_desc(conv_desc, false);
+  if (st == HUGE2_ERR_UNSUPPORTED) st = HUGE2_OK;  // the shape itself is well defined
+  if (st != HUGE2_OK) return st;
+  const huge2_conv_desc& d = *conv_desc;
+  int ho, wo;
+  if (!output_dims(d, false, &ho, &wo)) return HUGE2_ERR_INVALID_ARG;
+  // the transposed conv of an ho x wo input reaches (ho-1)*s - 2p + d(r-1) + 1
+  *op_h = d.h - ((ho - 1) * d.stride_h - 2 * d.pad_h + d.dil_h * (d.r - 1) + 1);
+  *op_w = d.w - ((wo - 1) * d.stride_w - 2 * d.pad_w + d.dil_w * (d.s - 1) + 1);
+  return HUGE2_OK;
+}
+
 huge2_status huge2_plan_create(huge2_plan** out, const huge2_conv_desc* desc, int32_t transposed,
                                const void* w, void* hip_stream) {
   try {

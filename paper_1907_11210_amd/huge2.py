@@ -33,7 +33,7 @@ EXPORTED = (
     "huge2_wgrad_plan_create", "huge2_wgrad_execute", "huge2_wgrad_plan_destroy",
     "huge2_conv2d_transpose_wgrad", "huge2_conv2d_dilated_wgrad",
     "huge2_group_create", "huge2_group_execute", "huge2_group_destroy",
-    "huge2_conv2d_transpose_noalloc",
+    "huge2_conv2d_transpose_noalloc", "huge2_dgrad_output_padding",
 )
 MAX_GROUP = 8
 
@@ -100,6 +100,7 @@ def lib():
         L.huge2_group_execute.argtypes = [vp, vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp]
         L.huge2_group_destroy.argtypes = [vp]
         L.huge2_conv2d_transpose_noalloc.argtypes = [dp, vp, vp, vp, vp, vp]
+        L.huge2_dgrad_output_padding.argtypes = [dp, i32p, i32p]
         for name in EXPORTED[1:]:
             getattr(L, name).restype = ctypes.c_int
         L.huge2_plan_kernel.restype = ctypes.c_char_p
@@ -139,6 +140,13 @@ def huge2_output_shape(desc, transposed):
     _check(lib().huge2_output_shape(ctypes.byref(desc), int(transposed), ctypes.byref(ho),
                                     ctypes.byref(wo)), "huge2_output_shape")
     return ho.value, wo.value
+
+
+def huge2_dgrad_output_padding(conv_desc):
+    oph, opw = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib().huge2_dgrad_output_padding(ctypes.byref(conv_desc), ctypes.byref(oph),
+                                            ctypes.byref(opw)), "huge2_dgrad_output_padding")
+    return oph.value, opw.value
 
 
 def huge2_plan_create(desc, transposed, w_ptr, stream=0):
@@ -451,15 +459,13 @@ def conv2d_transpose_dgrad(dy, w, stride=1, padding=0, dilation=1, layout="NCHW"
 def conv2d_dilated_dgrad(dy, w, x_hw, stride=1, padding=0, dilation=1, layout="NCHW"):
     """Data gradient of the dilated / strided conv: the transposed conv of dy
     with the same w, output padding chosen so that the result is x_hw."""
-    sh, sw = _pair(stride)
-    ph, pw = _pair(padding)
-    dh, dw = _pair(dilation)
     lay = _layout_code(layout)
-    ho, wo = (dy.shape[2], dy.shape[3]) if lay == HUGE2_NCHW else (dy.shape[1], dy.shape[2])
-    r, s = w.shape[2], w.shape[3]
-    oph = x_hw[0] - ((ho - 1) * sh - 2 * ph + dh * (r - 1) + 1)
-    opw = x_hw[1] - ((wo - 1) * sw - 2 * pw + dw * (s - 1) + 1)
-    return conv2d_transpose(dy, w, None, stride, padding, (oph, opw), dilation, layout)
+    n, c_y = (dy.shape[0], dy.shape[1]) if lay == HUGE2_NCHW else (dy.shape[0], dy.shape[3])
+    # the forward strided conv: input x_hw with w.shape[1] channels, c_y outputs
+    fwd = make_desc(n, w.shape[1], x_hw[0], x_hw[1], c_y, w.shape[2], w.shape[3], stride,
+                    padding, 0, dilation, lay, _dtype_code(dy))
+    op = huge2_dgrad_output_padding(fwd)
+    return conv2d_transpose(dy, w, None, stride, padding, op, dilation, layout)
 
 
 class Plan:

@@ -205,3 +205,38 @@ def test_groups_validated_without_gpu(L):
     p = ctypes.c_void_p()
     assert L.huge2_wgrad_plan_create(ctypes.byref(p), ctypes.byref(d), 1) in (
         h2.HUGE2_ERR_UNSUPPORTED, h2.HUGE2_ERR_INVALID_ARG)
+
+
+def test_dgrad_output_padding_without_gpu(L):
+    """The output padding that carries a strided conv's output size back to
+    its input size: the transposed conv with it has exactly the input's size,
+    and it is a valid output padding, over a sweep of shapes."""
+    import numpy as np
+    rng = np.random.default_rng(3)
+    checked = 0
+    for _ in range(300):
+        h, w = int(rng.integers(1, 40)), int(rng.integers(1, 40))
+        r, s = int(rng.integers(1, 6)), int(rng.integers(1, 6))
+        st, dl = int(rng.integers(1, 5)), int(rng.integers(1, 4))
+        pd = int(rng.integers(0, dl * (r - 1) + 1))
+        conv = h2.make_desc(2, 8, h, w, 4, r, s, st, pd, 0, dl)
+        try:
+            ho, wo = h2.huge2_output_shape(conv, 0)
+        except h2.Huge2Error:
+            continue
+        oph, opw = h2.huge2_dgrad_output_padding(conv)
+        assert 0 <= oph < max(st, dl) and 0 <= opw < max(st, dl), (h, w, r, s, st, pd, dl)
+        tr = h2.make_desc(2, 4, ho, wo, 8, r, s, st, pd, (oph, opw), dl)
+        assert h2.huge2_output_shape(tr, 1) == (h, w)
+        checked += 1
+    assert checked > 100
+
+
+def test_pyramid_plans_take_the_listed_form(L):
+    """The atrous pyramid's four branches plan the listed form: the tiles'
+    issued multiply-adds stay within 6% of the structural ones (the masked
+    phase views issue 14% / 30% / 51% / 78% more for d = 6 / 12 / 18 / 24)."""
+    for d in (6, 12, 18, 24):
+        desc = h2.make_desc(8, 2048, 64, 64, 256, 3, 3, 1, d, 0, d, h2.HUGE2_NHWC, h2.HUGE2_BF16)
+        nz, issued = h2.huge2_plan_macs(desc, 0)
+        assert nz <= issued <= 1.06 * nz, (d, nz, issued)

@@ -727,3 +727,28 @@ def test_grouped_and_depthwise(layer):
         assert nz == issued
     finally:
         plan.close()
+
+
+def test_launch_fault_is_reported(monkeypatch):
+    """HUGE2_FAULT=launch (set from the host) makes every enqueueing entry
+    point report HUGE2_ERR_HIP without touching its output."""
+    dev = torch.device("cuda", 0)
+    layer = SMALL[1]  # NHWC bf16 phase GEMM
+    xq, wq = _inputs(layer, seed=5)
+    x_dev = wl.to_layout(xq, layer.layout).to(dev)
+    w_dev = wq.contiguous().to(dev)
+    plan = P.make_plan(layer, w_dev)
+    try:
+        y = torch.full(plan.out_shape, 3.0, dtype=xq.dtype, device=dev)
+        monkeypatch.setenv("HUGE2_FAULT", "launch")
+        for call in (lambda: plan(x_dev, out=y), lambda: plan.gemm(x_dev, y),
+                     lambda: h2.conv2d_transpose(x_dev, w_dev, None, layer.stride, layer.pad,
+                                                 layer.out_pad, layer.dil, layer.layout, out=y)):
+            with pytest.raises(h2.Huge2Error) as e:
+                call()
+            assert e.value.status == h2.HUGE2_ERR_HIP
+        monkeypatch.delenv("HUGE2_FAULT")
+        torch.cuda.synchronize()
+        assert bool((y == 3.0).all())
+    finally:
+        plan.close()

@@ -821,7 +821,7 @@ def bench_forward(name, args, dev):
     dom_layer = items[dom][0]
     dom_name = "group" if group is not None else items[dom][0].name
     roofline["traffic"] = measured_traffic(name, dom_name)
-    roofline.update({"kernel": ("grouped launch of %d layers: %s (%s)" % (len(plans), plans[dom].kernel, name)
+    roofline.update({"kernel": ("grouped launch of %d layers: %s (%s)" % (len(plans), group.kernel, name)
                                 if group is not None else
                                 "%s (%s)" % (plans[dom].kernel, items[dom][0].name)),
                      "mean_launch_ms": round(dom_ms, 5),

@@ -221,8 +221,12 @@ huge2_status huge2_conv2d_dilated(const huge2_conv_desc* desc, const void* x, co
  * classes and between dilations): the eight XCDs of the MI355X then each
  * work through contiguous images, whose input rows every branch shares in
  * that XCD's L2, and the compute units finish together.  Every output
- * element is computed exactly as by huge2_plan_execute of its own plan (the
- * same tiles, taps and summation order: the results are bitwise equal).
+ * element is computed as by huge2_plan_execute of its own plan: the same
+ * tiles and taps, and with the plans' own kernel the same summation order
+ * (bitwise equal results).  A list long enough for two workgroups on every
+ * compute unit may run the 4-wave form of the pipelined 128 x 256 tile
+ * instead (huge2_group_kernel names it), whose 64-byte K blocks sum the
+ * products in another order: equal to rounding.
  *
  * huge2_group_create: plans[0 .. count) (1 <= count <= 8) must be plans
  * whose main kernel is the phase GEMM without a staging pass or a K split
@@ -245,6 +249,10 @@ huge2_status huge2_group_create(huge2_group** out, const huge2_plan* const* plan
  * overlap (nothing is written but the outputs).  Errors: INVALID_ARG, HIP. */
 huge2_status huge2_group_execute(const huge2_group* group, const void* x, const float* const* bias,
                                  void* const* y, void* hip_stream);
+
+/* Name and tile shape of the kernel the group launches (owned by the group;
+ * "" for NULL). */
+const char* huge2_group_kernel(const huge2_group* group);
 
 /* Release a group (its plans are untouched).  NULL is accepted.  Errors: HIP. */
 huge2_status huge2_group_destroy(huge2_group* group);

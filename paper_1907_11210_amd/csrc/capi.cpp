@@ -92,6 +92,8 @@ struct huge2_group {
   huge2::WorkDev* d_works;
   const uint32_t* d_ptab;
   int n_works;
+  int cfg;  // launch tile: the plans' own, or its two-per-CU form for long lists
+  char kernel_name[64];
 };
 
 namespace {
@@ -147,8 +149,14 @@ int choose_cfg(const huge2_conv_desc& d, bool transposed, int class_split) {
   if (large && d.c_out <= 128) return TILE_128x128;
   if (d.r == 1 && d.s == 1 && (long long)d.n * d.h * d.w <= 64 && d.c_out >= 256)
     return TILE_SW_32x256;  // a pointwise GEMM of at most 64 rows (the 1x1-input product form)
-  if (d.c_out >= 256 && count_works(d, transposed, class_split, TILE_P3_128x256) >= kComputeUnits)
-    return TILE_P3_128x256;
+  if (d.c_out >= 256) {
+    const long long w3 = count_works(d, transposed, class_split, TILE_P3_128x256);
+    // two workgroups per CU (its fallback for tap lists, the 128 x 256
+    // split-wave tile, takes 128-byte K blocks)
+    if (w3 >= 2 * kComputeUnits && d.c_in % (tile_kb(TILE_SW_128x256) / elem_size(d.dtype)) == 0)
+      return TILE_P3_128x256_W4;
+    if (w3 >= kComputeUnits) return TILE_P3_128x256;
+  }
   if (d.c_out >= 256 && count_works(d, transposed, class_split, TILE_SW_64x256) >= 384)
     return TILE_SW_64x256;
   if (count_works(d, transposed, class_split, TILE_SW_128x128_K2) >= kComputeUnits)
@@ -1242,10 +1250,12 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   if (kTiles[p->cfg].kind == 3 && !all_ap) {
     // the pipelined kernel steps through progressions only: the split-wave
     // kernel of the same tile and packing takes tap lists
+    // (the same works and lane-ordered packing; its K block must divide the
+    // padded channel count)
     for (int c = 0; c < TILE_COUNT; ++c) {
       const TileShape &t = kTiles[c], &u = kTiles[p->cfg];
-      if (t.kind == 1 && t.bm == u.bm && t.bn == u.bn && t.kb == u.kb && t.pw * t.cw == u.pw * u.cw &&
-          t.ksplit == u.ksplit) {
+      if (t.kind == 1 && t.bm == u.bm && t.bn == u.bn && t.ksplit == u.ksplit &&
+          p->cin_pad % (t.kb / esz) == 0) {
         p->cfg = c;
         break;
       }
@@ -1342,7 +1352,7 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     ok = hipMemcpyAsync(p->meta, host.data(), meta_b, hipMemcpyHostToDevice, stream) == hipSuccess;
   if (ok)
     ok = launch_pack_weights(w, p->wp, d.dtype, tr, d.c_in, d.c_out, d.r, d.s, p->cin_pad,
-                             p->cout_pad, kTiles[p->cfg].kind != 0 ? tile_kb(p->cfg) : 0,
+                             p->cout_pad, kTiles[p->cfg].kind != 0 ? kPackKB : 0,
                              stream) == hipSuccess;
   // the host copy of the metadata must outlive the transfer
   if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
@@ -1857,6 +1867,22 @@ huge2_status group_create(huge2_group** out, const huge2_plan* const* plans, int
   g->count = count;
   for (int i = 0; i < count; ++i) g->plans[i] = plans[i];
   g->n_works = (int)works.size();
+  // Enough works for two workgroups on every compute unit: the 4-wave form of
+  // the pipelined tile (the same 128 x 256 works and packed weights, a K
+  // block of 64 bytes), two of which share a compute unit and hide each
+  // other's barriers and epilogues.
+  g->cfg = p0->cfg;
+  const int64_t kc4 = tile_kb(TILE_P3_128x256_W4) / elem_size(p0->desc.dtype);
+  if (p0->cfg == TILE_P3_128x256 && env_int("HUGE2_TILE", -1) < 0 &&
+      g->n_works >= 2 * kComputeUnits && p0->cin_pad % kc4 == 0)
+    g->cfg = TILE_P3_128x256_W4;
+  if (g->cfg == p0->cfg) {
+    std::snprintf(g->kernel_name, sizeof(g->kernel_name), "%s", p0->kernel_name);
+  } else {
+    const TileShape& t = kTiles[g->cfg];
+    std::snprintf(g->kernel_name, sizeof(g->kernel_name), "phase_gemm3_kernel %dx%d w%d k%d%s", t.bm,
+                  t.bn, t.pw * t.cw, t.ksplit, std::strstr(p0->kernel_name, " listed") ? " listed" : "");
+  }
   const size_t seg_b = segs.size() * sizeof(SegDev), tap_b = taps.size() * sizeof(TapDev);
   const size_t work_b = works.size() * sizeof(WorkDev), ptab_b = ptab.size() * sizeof(uint32_t);
   const size_t meta_b = seg_b + tap_b + work_b + ptab_b;
@@ -1923,7 +1949,7 @@ huge2_status group_execute(const huge2_group* g, const void* x, const float* con
   a.cout_pad = p->cout_pad;
   a.ho = p->ho;
   a.wo = p->wo;
-  if (launch_phase_gemm(a, d.dtype, p->cfg, d.layout == HUGE2_NCHW, stream) != hipSuccess) {
+  if (launch_phase_gemm(a, d.dtype, g->cfg, d.layout == HUGE2_NCHW, stream) != hipSuccess) {
     (void)hipGetLastError();
     return HUGE2_ERR_HIP;
   }
@@ -2185,6 +2211,10 @@ huge2_status huge2_group_create(huge2_group** out, const huge2_plan* const* plan
   } catch (...) {
     return HUGE2_ERR_ALLOC;
   }
+}
+
+const char* huge2_group_kernel(const huge2_group* group) {
+  return group ? group->kernel_name : "";
 }
 
 huge2_status huge2_group_execute(const huge2_group* group, const void* x, const float* const* bias,

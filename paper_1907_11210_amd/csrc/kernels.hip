@@ -128,12 +128,19 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, const SegDev& sg, 
     }
 #pragma unroll
     for (int i = 0; i < TP; ++i) {
+      // the 16 rows' positions before their stores: a table lookup issued
+      // behind stores would wait for them (the memory counter is in order)
+      int pixr[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int m = pix0 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (m >= m_end) continue;
-        const PixelPos p = pixel_pos(sg, a.ptab, m);
-        const int pix = (p.img * a.ho + p.oh) * a.wo + p.ow;
+        const PixelPos p = pixel_pos(sg, a.ptab, m < m_end ? m : pix0);
+        pixr[r] = m < m_end ? (p.img * a.ho + p.oh) * a.wo + p.ow : -1;
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int pix = pixr[r];
+        if (pix < 0) continue;
 #pragma unroll
         for (int j = 0; j < TC; ++j) {
           const int ch = ch0 + 32 * j + (lane & 31);
@@ -181,6 +188,56 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, const SegDev& sg, 
         }
       }
     }
+  }
+}
+
+// NHWC bf16 epilogue through LDS, for tiles whose output rows are whole
+// 16-byte pieces (C_out a multiple of 8, a 16-byte aligned output).  The
+// waves write their results (bias, activation, rounding) into a [BM][BN]
+// tile in LDS; then every thread stores 16-byte pieces of output pixel
+// rows: in NHWC a pixel's channels are contiguous, so each row of the tile
+// is one run of BN * 2 bytes.  lds: at least BM * (2 * BN + 16) bytes, free
+// once every wave passed the barrier at the start; row_off: each tile row's
+// output pixel index (-1: past the end of the work), in LDS; sb: the tile's
+// BN bias values (zeros without bias); wch0: the wave's first channel within
+// the tile.
+template <int TP, int TC, int BM, int BN, int NT, int ACT>
+__device__ __forceinline__ void store_rows_nhwc(const GemmArgs& a, int n0, void* y,
+                                                const f32x16 (&acc)[TP][TC], int wch0, int lane,
+                                                int tid, char* lds, const int* row_off,
+                                                const float* sb) {
+  constexpr int PITCH = 2 * BN + 16;  // 16-byte pad: rows 4 apart on other banks
+  constexpr int PIECES = 2 * BN / 16;
+  constexpr int RSTEP = NT / PIECES;
+  constexpr int PASSES = BM / RSTEP;
+  static_assert(NT % PIECES == 0 && BM % RSTEP == 0, "epilogue shape");
+  float bv[TC];
+#pragma unroll
+  for (int j = 0; j < TC; ++j) bv[j] = sb[wch0 + 32 * j + (lane & 31)];
+  __syncthreads();  // every wave has finished with the stage buffers
+#pragma unroll
+  for (int i = 0; i < TP; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int px = 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+#pragma unroll
+      for (int j = 0; j < TC; ++j) {
+        float v = acc[i][j][r] + bv[j];
+        if constexpr (ACT == 1) v = fmaxf(v, 0.f);
+        if constexpr (ACT == 2) v = tanhf(v);
+        *(uint16_t*)(lds + px * PITCH + 2 * (wch0 + 32 * j + (lane & 31))) = f32_to_bf16_rne(v);
+      }
+    }
+  __syncthreads();
+  const int piece = tid % PIECES, row0 = tid / PIECES;
+  if (n0 + 8 * piece >= a.cout) return;
+  uint16_t* const yb = (uint16_t*)y + n0 + 8 * piece;
+#pragma unroll
+  for (int k = 0; k < PASSES; ++k) {
+    const int row = row0 + RSTEP * k;
+    const int off = row_off[row];
+    if (off >= 0)
+      *(uint4*)(yb + (size_t)off * a.cout) = *(const uint4*)(lds + row * PITCH + 16 * piece);
   }
 }
 
@@ -512,6 +569,7 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm2_kernel(GemmArgs a) {
   constexpr int S_LD = (RS * CPR + NT - 1) / NT;  // shared-operand loads per thread
   constexpr int U = DEPTH == 3 ? 6 : (DEPTH == 1 ? 2 : DEPTH);
   static_assert(RD % 32 == 0 && RS % 32 == 0 && HC >= 1, "32-row blocks, whole lane halves");
+  static_assert(!SHARE_A || KB % kPackKB == 0, "K stages of whole packing blocks");
   static_assert(DEPTH >= 2 && DEPTH <= 4, "two to four stages in flight");
   constexpr int STAGE_B = RS * ROWB;
   constexpr uint32_t OOB = 0x80000000u;
@@ -706,12 +764,14 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm2_kernel(GemmArgs a) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   auto compute = [&](int buf, const Regs& R) {
-    const char* ss = smem + buf * STAGE_B + row32 * ROWB + half * (KB / 2);
+    const char* ss = smem + buf * STAGE_B + row32 * ROWB;
 #pragma unroll
     for (int c = 0; c < HC; ++c) {
       uint4 fs[TS];
 #pragma unroll
-      for (int i = 0; i < TS; ++i) fs[i] = *(const uint4*)(ss + 32 * i * ROWB + 16 * c);
+      for (int i = 0; i < TS; ++i)
+        fs[i] = *(const uint4*)(ss + 32 * i * ROWB +
+                                (SHARE_A ? pack_chunk_byte(c, half) : half * (KB / 2) + 16 * c));
       uint4 fp[TP], fc[TC];
 #pragma unroll
       for (int i = 0; i < TP; ++i) fp[i] = SHARE_A ? fs[i] : R.d[i][c];
@@ -820,7 +880,7 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm2_kernel(GemmArgs a) {
 // The loop is unrolled by U = 6 (a multiple of the 3 LDS buffers and of DA
 // and DB), so every buffer index is a compile-time constant.
 template <bool BF16, int BM, int BN, int W, int KB, int DA, int DB, int KS, bool NCHW_OUT>
-__global__ __launch_bounds__(W * 64 * KS) void phase_gemm3_kernel(GemmArgs a) {
+__global__ __launch_bounds__(W * 64 * KS, 2) void phase_gemm3_kernel(GemmArgs a) {
   constexpr int NTA = W * 64 * KS, NT = W * 64;
   constexpr int ESZ = BF16 ? 2 : 4;
   constexpr int KC = KB / ESZ;   // K elements per stage
@@ -834,13 +894,18 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm3_kernel(GemmArgs a) {
   constexpr int NB = 3;
   constexpr int U = lcm3(NB, DA, DB);
   static_assert(RD % 32 == 0 && BM % 32 == 0 && HC >= 2 && HC % 2 == 0, "tile shape");
+  static_assert(KB % kPackKB == 0, "K stages of whole packing blocks");
   static_assert(DA >= 2 && DA <= 4 && DB >= 2 && DB <= 4, "two to four stages in flight");
   constexpr int STAGE_B = BM * ROWB;
   constexpr uint32_t OOB = 0x80000000u;
   constexpr int ACC_B = KS > 1 ? W * 64 * TP * TC * 16 * 4 : 0;
-  constexpr int SMEM_B = KS * NB * STAGE_B > ACC_B ? KS * NB * STAGE_B : ACC_B;
+  constexpr bool ROWS_OUT = BF16 && !NCHW_OUT && KS == 1;  // row epilogue through LDS
+  constexpr int EPI_B = ROWS_OUT ? BM * (2 * BN + 16) : 0;
+  constexpr int SMEM_B0 = KS * NB * STAGE_B > ACC_B ? KS * NB * STAGE_B : ACC_B;
+  constexpr int SMEM_B = SMEM_B0 > EPI_B ? SMEM_B0 : EPI_B;
   __shared__ __attribute__((aligned(16))) char smem_all[SMEM_B];
   __shared__ float s_bias[BN];
+  __shared__ int s_rowoff[ROWS_OUT ? BM : 1];  // output pixel index of each tile row
 
   const int wave_all = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
   const int lane = threadIdx.x & 63, grp = KS > 1 ? wave_all / W : 0;
@@ -872,6 +937,8 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm3_kernel(GemmArgs a) {
     p_iw[i] = p.iw;
     p_base[i] = (((uint32_t)p.img * (uint32_t)a.h + (uint32_t)p.ih) * (uint32_t)a.w +
                  (uint32_t)p.iw) * (uint32_t)a.cin * ESZ + (uint32_t)(s_chunk * 16);
+    if (ROWS_OUT && s_chunk == 0 && r < BM)
+      s_rowoff[r] = wk.m0 + r < wk.m1 ? (p.img * a.ho + p.oh) * a.wo + p.ow : -1;
   }
   // lane-ordered weights: 32-channel block (n0 + wave * RD) / 32 + i
   uint32_t w_off[TC];
@@ -967,7 +1034,7 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm3_kernel(GemmArgs a) {
         *(uint4*)(ss + (tid / CPR + (NT / CPR) * i) * ROWB + s_chunk * 16) = R.v[i];
   };
   auto read_f = [&](int buf, int c, uint4 (&f)[TP]) {
-    const char* ss = smem + buf * STAGE_B + row32 * ROWB + half * (KB / 2) + 16 * c;
+    const char* ss = smem + buf * STAGE_B + row32 * ROWB + pack_chunk_byte(c, half);
 #pragma unroll
     for (int i = 0; i < TP; ++i) f[i] = *(const uint4*)(ss + 32 * i * ROWB);
   };
@@ -1097,6 +1164,21 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm3_kernel(GemmArgs a) {
         for (int r = 0; r < 16; ++r) acc[i][j][r] += red[((i * TC + j) * 16 + r) * 64];
   }
   const int ch0 = wk.n0 + wave * RD;
+  if constexpr (ROWS_OUT) {
+    void* const yp = a.y[sg.plan];
+    if (a.ksplit == 1 && (a.cout & 7) == 0 && ((uintptr_t)yp & 15) == 0) {
+      if (a.act == 1)
+        store_rows_nhwc<TP, TC, BM, BN, NT, 1>(a, wk.n0, yp, acc, wave * RD, lane, tid,
+                                               smem_all, s_rowoff, s_bias);
+      else if (a.act == 2)
+        store_rows_nhwc<TP, TC, BM, BN, NT, 2>(a, wk.n0, yp, acc, wave * RD, lane, tid,
+                                               smem_all, s_rowoff, s_bias);
+      else
+        store_rows_nhwc<TP, TC, BM, BN, NT, 0>(a, wk.n0, yp, acc, wave * RD, lane, tid,
+                                               smem_all, s_rowoff, s_bias);
+      return;
+    }
+  }
   if (a.ksplit > 1) {
     store_tile<false, NCHW_OUT, TP, TC>(a, sg, wk.m1, a.part + (size_t)wk.ks * a.part_stride, acc,
                                         wk.m0, ch0, lane, s_bias - wk.n0);
@@ -2366,11 +2448,12 @@ hipError_t launch_quad(const QArgs& a, hipStream_t stream) {
 // Weight packing: element (slot, k, c) = w at kernel tap slot = (kh, kw),
 // output channel k, input channel c.
 //   lane_kb = 0: K-contiguous rows, wp[slot][k][c].
-//   lane_kb = KB: the lane order of the split-wave GEMM's own-operand loads
-//     for KB-byte stages: per (slot, 32-channel block, K stage) a block of
-//     32 rows x KB bytes stored as [chunk c16 < KB/32][lane < 64][16 bytes],
-//     lane = 32 * (byte / (KB/2)) + row, so that one 16-byte load per lane
-//     reads 1 KB contiguous.
+//   lane_kb = kPackKB (or the all-phase kernel's 128): the lane order of the
+//     split-wave GEMM's own-operand loads: per (slot, 32-channel block, K
+//     block of lane_kb bytes) a block of 32 rows x lane_kb bytes stored as
+//     [chunk c16 < lane_kb/32][lane < 64][16 bytes], lane = 32 * (byte /
+//     (lane_kb/2)) + row, so that one 16-byte load per lane reads 1 KB
+//     contiguous.
 
 template <typename T>
 __global__ void pack_weights_kernel(const T* __restrict__ w, T* __restrict__ wp, bool transposed,

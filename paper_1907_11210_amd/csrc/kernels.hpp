@@ -130,6 +130,7 @@ enum TileCfg {
   TILE_SW_128x128_K2 = 7,  // split-wave: 4 waves of 128 x 32 channels, two K groups
   TILE_SW_128x256 = 8,   // split-wave: 8 waves of 128 x 32 channels
   TILE_P3_128x256 = 9,   // pipelined split-wave: 8 waves of 128 x 32 channels
+  TILE_P3_128x256_W4 = 10,  // pipelined split-wave: 4 waves of 128 x 64 channels, 64-byte K
 };
 constexpr TileShape kTiles[] = {
     {128, 128, 4, 2, 128, 2, 2, 0},     // TILE_128x128
@@ -142,6 +143,7 @@ constexpr TileShape kTiles[] = {
     {128, 128, 1, 4, 128, 3, 1, 1, 2},  // TILE_SW_128x128_K2
     {128, 256, 1, 8, 128, 3, 1, 1, 1},  // TILE_SW_128x256
     {128, 256, 1, 8, 128, 32, 1, 3, 1},  // TILE_P3_128x256
+    {128, 256, 1, 4, 64, 32, 2, 3, 1},   // TILE_P3_128x256_W4
 };
 // A split-K plan may switch from the two-K-group 64 x 128 tile to its
 // one-group form after the work list and the weight packing were laid out for
@@ -153,6 +155,16 @@ static_assert(kTiles[TILE_SW_64x128].bm == kTiles[TILE_SW_64x128_K2].bm &&
               "the split-K tile switch keeps the work list and the packing");
 constexpr int kComputeUnits = 256;  // MI355X
 constexpr int TILE_COUNT = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
+// K bytes of one block of the lane-ordered weight packing (split-wave and
+// pipelined kinds).  Inside a block, MFMA K chunk c takes bytes
+// [16c, 16c + 16) of the block's first half in lanes 0-31 and of its second
+// half in lanes 32-63; a K stage of KB bytes is KB / kPackKB such blocks.  One
+// packing for every K block size, so that plans of different tiles share it.
+constexpr int kPackKB = 64;
+// Byte offset, inside a K stage, of MFMA K chunk c for lane half `half`.
+__host__ __device__ constexpr int pack_chunk_byte(int c, int half) {
+  return (c / (kPackKB / 32)) * kPackKB + half * (kPackKB / 2) + (c % (kPackKB / 32)) * 16;
+}
 inline int tile_bm(int cfg) { return kTiles[cfg].bm; }
 inline int tile_bn(int cfg) { return kTiles[cfg].bn; }
 inline int tile_threads(int cfg) {

@@ -32,7 +32,7 @@ EXPORTED = (
     "huge2_plan_describe", "huge2_plan_macs",
     "huge2_wgrad_plan_create", "huge2_wgrad_execute", "huge2_wgrad_plan_destroy",
     "huge2_conv2d_transpose_wgrad", "huge2_conv2d_dilated_wgrad",
-    "huge2_group_create", "huge2_group_execute", "huge2_group_destroy",
+    "huge2_group_create", "huge2_group_execute", "huge2_group_destroy", "huge2_group_kernel",
     "huge2_conv2d_transpose_noalloc", "huge2_dgrad_output_padding",
 )
 MAX_GROUP = 8
@@ -99,11 +99,13 @@ def lib():
         L.huge2_group_create.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(vp), i32, vp]
         L.huge2_group_execute.argtypes = [vp, vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp]
         L.huge2_group_destroy.argtypes = [vp]
+        L.huge2_group_kernel.argtypes = [vp]
         L.huge2_conv2d_transpose_noalloc.argtypes = [dp, vp, vp, vp, vp, vp]
         L.huge2_dgrad_output_padding.argtypes = [dp, i32p, i32p]
         for name in EXPORTED[1:]:
             getattr(L, name).restype = ctypes.c_int
         L.huge2_plan_kernel.restype = ctypes.c_char_p
+        L.huge2_group_kernel.restype = ctypes.c_char_p
         _lib = L
     return _lib
 
@@ -275,6 +277,10 @@ def huge2_group_execute(group, x_ptr, bias_ptrs, y_ptrs, stream=0):
     ys = (ctypes.c_void_p * len(y_ptrs))(*y_ptrs)
     bs = None if bias_ptrs is None else (ctypes.c_void_p * len(bias_ptrs))(*bias_ptrs)
     _check(lib().huge2_group_execute(group, x_ptr, bs, ys, stream), "huge2_group_execute")
+
+
+def huge2_group_kernel(group):
+    return lib().huge2_group_kernel(group).decode()
 
 
 def huge2_group_destroy(group):
@@ -589,6 +595,11 @@ class Group:
         huge2_group_execute(self._group, x.data_ptr(), bias_ptrs, [y.data_ptr() for y in outs],
                             _stream(x))
         return outs
+
+    @property
+    def kernel(self):
+        """Name and tile shape of the kernel the group launches."""
+        return huge2_group_kernel(self._group)
 
     def close(self):
         if self._group is not None:

@@ -186,6 +186,7 @@ def test_group_entry_points_validate_without_gpu(L):
     assert out.value is None
     assert L.huge2_group_execute(None, None, None, None, None) == h2.HUGE2_ERR_INVALID_ARG
     assert L.huge2_group_destroy(None) == h2.HUGE2_OK
+    assert h2.huge2_group_kernel(None) == ""
 
 
 def test_groups_validated_without_gpu(L):

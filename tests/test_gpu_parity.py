@@ -609,6 +609,50 @@ GROUP_SETS = [
 ]
 
 
+# four branches of 256 works each (the single plans take the 8-wave
+# pipelined tile) whose 1024 works make the group run the 4-wave form
+GROUP_UPGRADE = [L("gu_d%d" % d, False, 2, 64, 128, 128, 256, 3, 3, 1, d, 0, d, "NHWC", "bf16")
+                 for d in (2, 6, 12, 24)]
+
+
+def test_grouped_launch_two_per_cu():
+    """A group long enough for two workgroups per compute unit runs the
+    4-wave pipelined tile: its outputs match the oracle on sampled points,
+    are written in full, and equal each plan's own output to rounding."""
+    dev = torch.device("cuda", 0)
+    layers = GROUP_UPGRADE
+    x = P.quantise(wl.layer_input(layers[0], seed=43), "bf16")
+    x_dev = wl.to_layout(x, "NHWC").to(dev)
+    plans, ws = [], []
+    for i, layer in enumerate(layers):
+        P.say("case group", layer)
+        wq = P.quantise(wl.random_weight(layer, seed=44 + i, std=0.05), "bf16")
+        ws.append(wq)
+        plans.append(P.make_plan(layer, wq.contiguous().to(dev)))
+        assert "w8" in plans[-1].kernel, plans[-1].kernel
+    group = h2.Group(plans)
+    try:
+        assert "phase_gemm3_kernel 128x256 w4" in group.kernel, group.kernel
+        outs = [torch.full(p.out_shape, float("nan"), dtype=x.dtype, device=dev) for p in plans]
+        group(x_dev, None, outs)
+        single = [p(x_dev) for p in plans]
+        torch.cuda.synchronize()
+        for k, (layer, wq, y, y1) in enumerate(zip(layers, ws, outs, single)):
+            yf, y1f = y.float(), y1.float()
+            assert bool(torch.isfinite(yf).all()), layer.name
+            scale = float(y1f.abs().max())
+            assert float((yf - y1f).abs().max()) <= 2e-2 * scale, layer.name
+            idx = P.sample_indices(layer, 3000, seed=50 + k)
+            yn = wl.from_layout(y.cpu(), "NHWC").double().numpy().reshape(-1)[idx]
+            ref = P.oracle_points(layer, x, wq, idx)
+            absref = P.oracle_points(layer, x, wq, idx, absolute=True)
+            P.check(yn, ref, absref, "bf16", layer.name + " grouped w4")
+    finally:
+        group.close()
+        for p in plans:
+            p.close()
+
+
 @pytest.mark.parametrize("layers", GROUP_SETS, ids=["aspp_reduced", "mixed_f32"])
 def test_grouped_launch(layers):
     """Several plans of one input in one launch (huge2_group): every output

@@ -1705,6 +1705,42 @@ __global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
   const int npix = (a.h + 2) * wp2;
   const int total = npix * a.cp;
   const uint16_t* xin = (const uint16_t*)a.x + (size_t)img * a.cin * a.h * a.w;
+  constexpr int NT = kCpWaves * 64;
+  if ((a.w & 7) == 0 && ((uintptr_t)a.x & 15) == 0) {
+    // 16-byte pieces of input rows (8 pixels of one channel), four per
+    // thread in flight, then spread to the pixels' channel slots over a
+    // zeroed area (border and padding channels stay 0).  Piece q is channel
+    // q mod C_in of pixel piece q div C_in: neighbouring lanes write
+    // neighbouring channel slots (few LDS bank conflicts).
+    const int wv = a.w / 8, nv = a.cin * a.h * wv;
+    uint4 v[4];
+    int dst[4];
+    auto fetch = [&](int q0) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int q = q0 + u * NT;
+        const int c = q % a.cin, rest = q / a.cin;
+        const int piece = rest % wv, i = rest / wv;
+        v[u] = q < nv ? *(const uint4*)(xin + ((size_t)c * a.h + i) * a.w + 8 * piece)
+                      : make_uint4(0, 0, 0, 0);
+        dst[u] = ((i + 1) * wp2 + 8 * piece + 1) * a.cp + c;
+      }
+    };
+    fetch(tid);  // the first pieces in flight during the zeroing pass
+    for (int e = 8 * tid; e < total; e += 8 * NT) *(uint4*)(s_x + e) = make_uint4(0, 0, 0, 0);
+    __syncthreads();
+    for (int q0 = tid; q0 < nv; q0 += 4 * NT) {
+      if (q0 != tid) fetch(q0);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (q0 + u * NT >= nv) break;
+        uint16_t* d = s_x + dst[u];
+        const uint32_t w4[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+        for (int t = 0; t < 8; ++t) d[t * a.cp] = (uint16_t)(w4[t >> 1] >> (16 * (t & 1)));
+      }
+    }
+  } else {
   constexpr int SU = 16;
   for (int e0 = tid; e0 < total; e0 += SU * kCpWaves * 64) {
     uint16_t v[SU];
@@ -1726,6 +1762,7 @@ __global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
 #pragma unroll
     for (int u = 0; u < SU; ++u)
       if (dst[u] >= 0) s_x[dst[u]] = v[u];
+  }
   }
   const float bk = a.bias ? a.bias[k] : 0.f;
   __syncthreads();

@@ -711,7 +711,24 @@ COLPHASE_LAYERS = [
     L("cp_outpad", True, 3, 5, 4, 3, 6, 30, 64, 32, 8, 8, 1, "NCHW", "bf16"),
     # no padding: the first and last column blocks are whole
     L("cp_pad0", True, 1, 12, 2, 2, 33, 64, 64, 32, 0, 0, 1, "NCHW", "bf16"),
+    # input rows of 8 and 16 pixels: the 16-byte staging pieces, fewer pieces
+    # than threads (15) and more than four rounds of them (1056)
+    L("cp_w8_few", True, 1, 5, 3, 8, 7, 64, 64, 32, 16, 0, 1, "NCHW", "bf16"),
+    L("cp_w8_many", True, 1, 32, 33, 8, 2, 32, 32, 32, 0, 0, 1, "NCHW", "bf16"),
 ]
+
+
+_COLPHASE_REF = {}
+
+
+def _colphase_reference(layer):
+    # the oracle's result for a layer, computed once for both forms
+    if layer.name not in _COLPHASE_REF:
+        xq, wq = _inputs(layer, seed=37)
+        bias = torch.linspace(-0.5, 0.5, layer.c_out)
+        _COLPHASE_REF[layer.name] = (xq, wq, bias, P.oracle_full(layer, xq, wq, bias),
+                                     P.oracle_full(layer, xq, wq, bias, absolute=True))
+    return _COLPHASE_REF[layer.name]
 
 
 @pytest.mark.parametrize("colphase", [1, 0])
@@ -723,10 +740,7 @@ def test_colphase_form(layer, colphase, monkeypatch):
     monkeypatch.setenv("HUGE2_COLPHASE", str(colphase))
     layer = layer.with_(act="relu")
     P.say("case", layer, "HUGE2_COLPHASE", colphase)
-    xq, wq = _inputs(layer, seed=37)
-    bias = torch.linspace(-0.5, 0.5, layer.c_out)
-    ref = P.oracle_full(layer, xq, wq, bias)
-    absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
+    xq, wq, bias, ref, absref = _colphase_reference(layer)
     y = P.run_gpu(layer, xq, wq, bias, prefill_nan=True)
     P.check(y, ref, absref, layer.dtype, layer.name)
     plan = P.make_plan(layer, wq.contiguous().to(torch.device("cuda", 0)))

@@ -77,6 +77,14 @@ DESCRIPTIONS = {
     "dcgan_generator_b1": "the whole DCGAN generator at batch 1 (latency): z (100) -> ConvT k4 "
                           "s1 p0 to 4x4x1024, then ConvT k4 s2 p1 1024->512->256->128->3 "
                           "(64x64), bf16 NCHW; ReLU fused after each layer, tanh after the last",
+    "dcgan_generator_nhwc": "the whole DCGAN generator in NHWC (channel-contiguous from z to "
+                            "the image), bf16, batch 64: z (100) -> ConvT k4 s1 p0 to 4x4x1024, "
+                            "then ConvT k4 s2 p1 1024->512->256->128->3 (64x64); ReLU fused "
+                            "after each layer, tanh after the last",
+    "dcgan_generator_nhwc_b1": "the whole DCGAN generator in NHWC at batch 1 (latency): z (100) "
+                               "-> ConvT k4 s1 p0 to 4x4x1024, then ConvT k4 s2 p1 "
+                               "1024->512->256->128->3 (64x64), bf16; ReLU fused after each "
+                               "layer, tanh after the last",
     "dcgan_dgrad": "training (section 3.2.3): data gradients of the DCGAN generator's four ConvT "
                    "layers, back to front, as stride-2 convs of the output errors with the same "
                    "weights: 3->128 (64->32), 128->256, 256->512, 512->1024 (8->4), bf16 NCHW, "

@@ -38,6 +38,9 @@ Workloads (``name``: layers):
                N(0,0.02), chained.
   dcgan_generator_b1
                the same generator at batch 1 (one image: the latency case).
+  dcgan_generator_nhwc, dcgan_generator_nhwc_b1
+               the same generator with every activation in NHWC (channel-contiguous
+               pixels from z to the image), batch 64 and batch 1; the same draws.
   dcgan_dgrad  training (section 3.2.3): the data gradients of the dcgan generator's
                four ConvTranspose layers, back to front.  The gradient of a stride-2
                transposed conv with respect to its input is the stride-2 conv of the
@@ -109,9 +112,10 @@ def dcgan_dgrad_layers(dtype="bf16", batch=64):
             for i, l in enumerate(reversed(fwd))]
 
 
-def generator_layers(dtype="bf16", batch=64):
-    proj = Layer("gen_proj", True, batch, 100, 1, 1, 1024, 4, 4, 1, 0, 0, 1, "NCHW", dtype, "relu")
-    body = [l.with_(name=l.name.replace("dcgan", "gen"), act="relu" if i < 3 else "tanh")
+def generator_layers(dtype="bf16", batch=64, layout="NCHW"):
+    proj = Layer("gen_proj", True, batch, 100, 1, 1, 1024, 4, 4, 1, 0, 0, 1, layout, dtype, "relu")
+    body = [l.with_(name=l.name.replace("dcgan", "gen"), act="relu" if i < 3 else "tanh",
+                    layout=layout)
             for i, l in enumerate(dcgan_layers(dtype, batch))]
     return [proj] + body
 
@@ -143,11 +147,14 @@ WORKLOADS = {
     "dcgan_dgrad": dcgan_dgrad_layers("bf16"),
     "dcgan_generator": generator_layers("bf16"),
     "dcgan_generator_b1": generator_layers("bf16", batch=1),
+    "dcgan_generator_nhwc": generator_layers("bf16", layout="NHWC"),
+    "dcgan_generator_nhwc_b1": generator_layers("bf16", batch=1, layout="NHWC"),
 }
+GENERATORS = ("dcgan_generator", "dcgan_generator_b1", "dcgan_generator_nhwc",
+              "dcgan_generator_nhwc_b1")
 # layers that read one input and run as one grouped launch (huge2_group)
 GROUPED = ("aspp",)
-CHAINED = ("dcgan", "dcgan_f32", "table1_dcgan", "table1_cgan", "dcgan_dgrad", "dcgan_generator",
-           "dcgan_generator_b1")
+CHAINED = ("dcgan", "dcgan_f32", "table1_dcgan", "table1_cgan", "dcgan_dgrad") + GENERATORS
 
 
 def torch_dtype(name):
@@ -186,7 +193,7 @@ def generate(workload, seed=0, batch=None):
         out = [(layers[0], x1, ws[0])]
         out += [(l, None, w) for l, w in zip(layers[1:], ws[1:])]
         return out
-    if workload in ("dcgan_generator", "dcgan_generator_b1"):
+    if workload in GENERATORS:
         l0 = layers[0]
         z = _normal(g, (l0.n, 100, 1, 1))
         ws = [_normal(g, l.w_shape(), 0.02) for l in layers]

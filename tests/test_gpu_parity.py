@@ -180,7 +180,8 @@ def test_dcgan_chain_reduced_batch():
             x_prev = torch.from_numpy(ref).to(torch.float32)
 
 
-@pytest.mark.parametrize("wname", ["table1_dcgan", "table1_cgan", "dcgan_generator_b1"])
+@pytest.mark.parametrize("wname", ["table1_dcgan", "table1_cgan", "dcgan_generator_b1",
+                                   "dcgan_generator_nhwc_b1"])
 def test_batch1_workloads_full(wname):
     """The paper's own Table 1 deconvolution layers (5x5 DCGAN with unequal
     phases, 4x4 cGAN) and the whole generator with its fused activations, at
@@ -216,6 +217,39 @@ def test_batch1_form_choice():
     assert kinds[("dcgan_l1", 64)].startswith("quad_kernel"), kinds
 
 
+@pytest.mark.parametrize("wname", ["dcgan_generator_nhwc_b1", "dcgan_generator_b1"])
+def test_generator_end_to_end(wname):
+    """The whole generator as the benchmark runs it: each layer reads the
+    previous layer's output where it lies on the device, in the workload's
+    layout (no host round trip).  Every layer's output matches the oracle
+    applied to that same device input, and the image is written in full."""
+    dev = torch.device("cuda", 0)
+    items = wl.generate(wname, seed=0)
+    layout = items[0][0].layout
+    x_dev = None
+    plans = []
+    try:
+        for i, (layer, x, w) in enumerate(items):
+            P.say("case", wname, layer)
+            if x_dev is None:
+                x_dev = wl.to_layout(P.quantise(x, layer.dtype), layout).to(dev)
+            wq = P.quantise(w, layer.dtype)
+            plans.append(P.make_plan(layer, wq.contiguous().to(dev)))
+            y_dev = torch.full(plans[-1].out_shape, float("nan"), dtype=x_dev.dtype, device=dev)
+            plans[-1](x_dev, out=y_dev)
+            torch.cuda.synchronize()
+            xin = wl.from_layout(x_dev.cpu(), layout).float()
+            ref = P.oracle_full(layer, xin, wq)
+            absref = P.oracle_full(layer, xin, wq, absolute=True)
+            y = wl.from_layout(y_dev.cpu(), layout).double().numpy()
+            P.check(y, ref, absref, layer.dtype, layer.name)
+            x_dev = y_dev
+        assert tuple(x_dev.shape) == ((1, 3, 64, 64) if layout == "NCHW" else (1, 64, 64, 3))
+    finally:
+        for p in plans:
+            p.close()
+
+
 REDUCED = [
     ("convt_small", {}),
     ("convt_odd", dict(n=1)),
@@ -248,7 +282,7 @@ def test_workload_reduced_full_check(wname, over):
 
 
 FULL = ["convt_small", "dcgan_f32", "dcgan", "convt_odd", "aspp", "fcn_upsample", "dcgan_dgrad",
-        "dcgan_generator"]
+        "dcgan_generator", "dcgan_generator_nhwc"]
 
 
 @pytest.mark.parametrize("wname", FULL)

@@ -1707,12 +1707,18 @@ huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, i
     if (forced > 0 && forced < chunk) chunk = forced;
   }
   const long long kp = (chunk * hws + 63) / 64 * 64;
-  // split K so that the GEMM has about four workgroups per compute unit,
+  // split K so that the GEMM has about two workgroups per compute unit
+  // (the 128 x 128 tiles run two per compute unit; the 64 x 64 ones four),
   // each split keeping at least 8 K stages
-  const long long tiles = taps * ((p->ms + 63) / 64) * ((p->nb + 63) / 64);
+  const long long wt = wgrad_tile(p->ms, p->nb);
+  const long long tiles = taps * ((p->ms + wt - 1) / wt) * ((p->nb + wt - 1) / wt);
   const long long stages = kp * esz / 128;
-  long long ksplit = std::max(1ll, (4ll * kComputeUnits + tiles - 1) / tiles);
+  const long long per_cu = wt == 128 ? 2 : 4;
+  long long ksplit = std::max(1ll, (per_cu * kComputeUnits + tiles - 1) / tiles);
   ksplit = std::max(1ll, std::min(ksplit, stages / 8));
+  // each slice's fp32 gradient is read back by the store: at most 16 MiB of them
+  const long long g_slice = taps * p->ms * p->nb * 4;
+  ksplit = std::min(ksplit, std::max(1ll, (16ll << 20) / g_slice));
   ksplit = std::min(ksplit, 64ll);
   const long long st_b = p->ms * kp * esz, bt_b = taps * p->nb * kp * esz;
   const long long g_b = ksplit * taps * p->ms * p->nb * 4;

@@ -2564,6 +2564,12 @@ __global__ __launch_bounds__(256) void wgrad_stage_kernel(WgArgs a) {
   const uint32_t st_total = (uint32_t)a.ms * kv;
   const uint32_t total = st_total + (uint32_t)(a.r * a.s * a.nb) * kv;
   const bool rows8 = a.ws % V == 0;
+  // the 8 k of a piece lie in one image (hws % 8 == 0): contiguous in the
+  // small tensor; rows of 1, 2 or 4 pixels (8 % ws == 0) are whole rows of
+  // the big tensor's gather
+  const bool img8 = hws % V == 0;
+  const bool short_rows = img8 && !rows8 && V % a.ws == 0;
+  const int lg_ws = a.ws == 1 ? 0 : a.ws == 2 ? 1 : 2;
   const T* sm = (const T*)a.sm;
   const T* bg = (const T*)a.bg;
   for (uint32_t e = blockIdx.x * blockDim.x + threadIdx.x; e < total; e += gridDim.x * blockDim.x) {
@@ -2576,7 +2582,7 @@ __global__ __launch_bounds__(256) void wgrad_stage_kernel(WgArgs a) {
     const uint32_t qh0 = q0 / (uint32_t)a.ws, qw0 = q0 - qh0 * (uint32_t)a.ws;
     if (is_st) {
       const size_t base = ((size_t)(a.img0 + il0) * a.ms + row) * hws;
-      if (rows8 && k0 < kreal) {
+      if (img8 && k0 < kreal) {
         __builtin_memcpy(v, sm + base + q0, sizeof(v));
       } else {
 #pragma unroll
@@ -2597,6 +2603,16 @@ __global__ __launch_bounds__(256) void wgrad_stage_kernel(WgArgs a) {
         for (int t = 0; t < V; ++t) {
           const int iw = iw0 + t * a.stride_w;
           v[t] = (row_in && iw >= 0 && iw < a.wb) ? src[iw] : T(0);
+        }
+      } else if (short_rows && k0 < kreal) {
+        const T* src = bg + ((size_t)(a.img0 + il0) * a.nb + n) * a.hb * a.wb;
+#pragma unroll
+        for (int t = 0; t < V; ++t) {
+          const int qh = (int)qh0 + (t >> lg_ws), qw = t & (a.ws - 1);
+          const int ih = qh * a.stride_h - a.pad_h + kh * a.dil_h;
+          const int iw = qw * a.stride_w - a.pad_w + kw * a.dil_w;
+          const bool in = ih >= 0 && ih < a.hb && iw >= 0 && iw < a.wb;
+          v[t] = in ? src[in ? ih * a.wb + iw : 0] : T(0);
         }
       } else {
 #pragma unroll
@@ -2722,6 +2738,134 @@ __global__ __launch_bounds__(256) void wgrad_gemm_kernel(WgArgs a) {
   }
 }
 
+// The same product on 128 x 128 tiles: 4 waves of 64 x 64 (four
+// accumulators each, so consecutive MFMAs do not wait for each other, and
+// each fragment read from LDS feeds two MFMAs), two workgroups per compute
+// unit.  The St fragments go first: a lane holds one output channel n of
+// each 32 x 32 block, so the fp32 partial rows of G are written 128 bytes at
+// a time.
+template <bool BF16>
+__global__ __launch_bounds__(256, 2) void wgrad_gemm2_kernel(WgArgs a) {
+  constexpr int ESZ = BF16 ? 2 : 4;
+  constexpr int KB = 128, KC = KB / ESZ, ROWB = KB + 16;
+  constexpr int TM = 128, TN = 128;
+  constexpr int STAGE_B = (TM + TN) * ROWB;
+  __shared__ __attribute__((aligned(16))) char smem[2 * STAGE_B];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave & 1, wn = wave >> 1;
+  const int taps = a.r * a.s;
+  const int m0 = blockIdx.x * TM, n0 = blockIdx.y * TN, tap = blockIdx.z % taps;
+  const int split = blockIdx.z / taps;
+  const int chunk = tid & 7, row = tid >> 3;  // 8 chunks of 16 bytes per row, 32 rows per pass
+  const char* const st = (const char*)a.st;
+  const char* const bt = (const char*)a.bt;
+  // this thread's rows (rows past the end repeat the last: their products
+  // are never stored)
+  size_t ao[4], bo[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    ao[j] = (size_t)min(m0 + row + 32 * j, a.ms - 1) * a.kp * ESZ + chunk * 16;
+    bo[j] = ((size_t)tap * a.nb + min(n0 + row + 32 * j, a.nb - 1)) * a.kp * ESZ + chunk * 16;
+  }
+  struct Regs {
+    uint4 a[4], b[4];
+  };
+  auto load = [&](int ks, Regs& r) {
+    const size_t off = (size_t)ks * KB;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      r.a[j] = *(const uint4*)(st + ao[j] + off);
+      r.b[j] = *(const uint4*)(bt + bo[j] + off);
+    }
+  };
+  auto store = [&](int buf, const Regs& r) {
+    char* as = smem + buf * STAGE_B;
+    char* bs = as + TM * ROWB;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      *(uint4*)(as + (row + 32 * j) * ROWB + chunk * 16) = r.a[j];
+      *(uint4*)(bs + (row + 32 * j) * ROWB + chunk * 16) = r.b[j];
+    }
+  };
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  auto compute = [&](int buf) {
+    const char* as = smem + buf * STAGE_B + (wm * 64 + (lane & 31)) * ROWB + (lane >> 5) * (KB / 2);
+    const char* bs =
+        smem + buf * STAGE_B + (TM + wn * 64 + (lane & 31)) * ROWB + (lane >> 5) * (KB / 2);
+#pragma unroll
+    for (int t = 0; t < KB / 32; ++t) {
+      uint4 fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        fa[i] = *(const uint4*)(as + 32 * i * ROWB + 16 * t);
+        fb[i] = *(const uint4*)(bs + 32 * i * ROWB + 16 * t);
+      }
+      if constexpr (BF16) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8, fa[i]), __builtin_bit_cast(bf16x8, fb[j]), acc[i][j], 0, 0,
+                0);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+              const uint32_t ea = e == 0 ? fa[i].x : e == 1 ? fa[i].y : e == 2 ? fa[i].z : fa[i].w;
+              const uint32_t eb = e == 0 ? fb[j].x : e == 1 ? fb[j].y : e == 2 ? fb[j].z : fb[j].w;
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(ea), __uint_as_float(eb),
+                                                               acc[i][j], 0, 0, 0);
+            }
+      }
+    }
+  };
+  const int nk_all = a.kp / KC;
+  const int per = (nk_all + a.ksplit - 1) / a.ksplit;
+  const int k_lo = min(split * per, nk_all), k_hi = min(k_lo + per, nk_all);
+  if (k_hi > k_lo) {
+    Regs cur, nx;
+    load(k_lo, cur);
+    store(0, cur);
+    __syncthreads();
+    for (int ks = k_lo; ks < k_hi; ++ks) {
+      // the next stage's loads (the first again past the end: unused)
+      // overlap this stage's MFMAs
+      load(ks + 1 < k_hi ? ks + 1 : k_lo, nx);
+      compute((ks - k_lo) & 1);
+      if (ks + 1 < k_hi) store((ks + 1 - k_lo) & 1, nx);
+      __syncthreads();
+    }
+  }
+  // lane: n = n0 + wn*64 + 32 j + lane % 32; m = m0 + wm*64 + 32 i + 8 (r/4) + 4 (lane/32) + r%4
+  const bool acc_in = a.accumulate != 0;
+  const int n = n0 + wn * 64 + (lane & 31);
+  float* const gt = a.g + ((size_t)split * taps + tap) * a.ms * a.nb;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int m = m0 + wm * 64 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      if (m >= a.ms) continue;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        if (n + 32 * j >= a.nb) continue;
+        float* gp = gt + (size_t)m * a.nb + n + 32 * j;
+        *gp = acc_in ? *gp + acc[i][j][r] : acc[i][j][r];
+      }
+    }
+}
+
 // dw[m][n][tap] from the splits of G[split][tap][m][n] (summed in order),
 // rounded to the dtype: a thread per (tap, m, n), (m, n) fastest so that the
 // reads of G coalesce.
@@ -2756,20 +2900,78 @@ hipError_t launch_wgrad_stage(const WgArgs& a, int dtype, hipStream_t stream) {
 }
 
 hipError_t launch_wgrad_gemm(const WgArgs& a, int dtype, hipStream_t stream) {
-  const dim3 grid((a.ms + 63) / 64, (a.nb + 63) / 64, a.r * a.s * a.ksplit);
-  if (dtype == 1)
+  const int t = wgrad_tile(a.ms, a.nb);
+  const dim3 grid((a.ms + t - 1) / t, (a.nb + t - 1) / t, a.r * a.s * a.ksplit);
+  if (t == 128 && dtype == 1)
+    hipLaunchKernelGGL(wgrad_gemm2_kernel<true>, grid, dim3(256), 0, stream, a);
+  else if (t == 128)
+    hipLaunchKernelGGL(wgrad_gemm2_kernel<false>, grid, dim3(256), 0, stream, a);
+  else if (dtype == 1)
     hipLaunchKernelGGL(wgrad_gemm_kernel<true>, grid, dim3(256), 0, stream, a);
   else
     hipLaunchKernelGGL(wgrad_gemm_kernel<false>, grid, dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 
+// The same for kernels of at most kWgTapsMax taps, a thread per (m, n): it
+// reads every tap's splits (each read coalesced across the threads) and
+// writes the pair's run of taps in dw, which is contiguous, with 16-byte
+// stores where the run allows.
+constexpr int kWgTapsMax = 32;
+template <bool BF16>
+__global__ __launch_bounds__(256) void wgrad_store2_kernel(WgArgs a) {
+  const int taps = a.r * a.s;
+  const uint32_t mn_total = (uint32_t)a.ms * (uint32_t)a.nb;
+  const uint32_t total = mn_total * (uint32_t)taps;
+  for (uint32_t mn = blockIdx.x * blockDim.x + threadIdx.x; mn < mn_total; mn += gridDim.x * blockDim.x) {
+    float v[kWgTapsMax];
+#pragma unroll
+    for (int t = 0; t < kWgTapsMax; ++t) {
+      v[t] = 0.f;
+      if (t < taps)
+        for (int sp = 0; sp < a.ksplit; ++sp) v[t] += a.g[(size_t)sp * total + (size_t)t * mn_total + mn];
+    }
+    if constexpr (BF16) {
+      uint16_t* d = (uint16_t*)a.dw + (size_t)mn * taps;
+      if (taps % 8 == 0 && ((uintptr_t)a.dw & 15) == 0) {
+#pragma unroll
+        for (int t = 0; t < kWgTapsMax; t += 8) {
+          if (t >= taps) break;
+          uint32_t w4[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            w4[e] = (uint32_t)f32_to_bf16_rne(v[t + 2 * e]) |
+                    ((uint32_t)f32_to_bf16_rne(v[t + 2 * e + 1]) << 16);
+          *(uint4*)(d + t) = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+        }
+      } else {
+#pragma unroll
+        for (int t = 0; t < kWgTapsMax; ++t)
+          if (t < taps) d[t] = f32_to_bf16_rne(v[t]);
+      }
+    } else {
+      float* d = (float*)a.dw + (size_t)mn * taps;
+#pragma unroll
+      for (int t = 0; t < kWgTapsMax; ++t)
+        if (t < taps) d[t] = v[t];
+    }
+  }
+}
+
 hipError_t launch_wgrad_store(const WgArgs& a, int dtype, hipStream_t stream) {
   const long long total = (long long)a.ms * a.nb * a.r * a.s;
-  if (dtype == 1)
+  // (one thread per pair serialises taps x splits reads: only for many pairs)
+  if (a.r * a.s <= kWgTapsMax && (long long)a.ms * a.nb >= (1ll << 18)) {
+    const long long pairs = (long long)a.ms * a.nb;
+    if (dtype == 1)
+      hipLaunchKernelGGL(wgrad_store2_kernel<true>, grid_for(pairs), dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL(wgrad_store2_kernel<false>, grid_for(pairs), dim3(256), 0, stream, a);
+  } else if (dtype == 1) {
     hipLaunchKernelGGL(wgrad_store_kernel<true>, grid_for(total), dim3(256), 0, stream, a);
-  else
+  } else {
     hipLaunchKernelGGL(wgrad_store_kernel<false>, grid_for(total), dim3(256), 0, stream, a);
+  }
   return hipGetLastError();
 }
 

@@ -389,6 +389,9 @@ struct WgArgs {
   int accumulate;  // 0: G = product, 1: G += product
   int ksplit;      // K ranges per tap, each with its own fp32 slice of G
 };
+// Output tile of the weight-gradient GEMM (square, channels of the small x
+// the large tensor): 128 x 128 when both channel counts reach 128, else 64.
+inline int wgrad_tile(int ms, int nb) { return ms >= 128 && nb >= 128 ? 128 : 64; }
 hipError_t launch_wgrad_stage(const WgArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_wgrad_gemm(const WgArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_wgrad_store(const WgArgs& a, int dtype, hipStream_t stream);

@@ -26,6 +26,12 @@ CASES = [
     ("conv_dilated_f32", False, 2, 16, 12, 12, 20, 3, 3, 1, 2, 0, 2, "f32"),
     ("conv_1x1", False, 2, 33, 5, 7, 17, 1, 1, 1, 0, 0, 1, "bf16"),
     ("conv_aspp_like", False, 1, 64, 24, 24, 32, 3, 3, 1, 6, 0, 6, "bf16"),
+    # 128 x 128 GEMM tiles (both channel counts >= 128), ragged in both
+    ("ct_tile128_ragged", True, 2, 130, 4, 4, 200, 4, 4, 2, 1, 0, 1, "bf16"),
+    ("conv_tile128_f32", False, 2, 136, 8, 8, 144, 3, 3, 2, 1, 0, 1, "f32"),
+    # small grids with rows of 2 and 1 pixels (staging pieces of whole rows)
+    ("ct_rows2", True, 2, 16, 4, 2, 24, 4, 4, 2, 1, 0, 1, "f32"),
+    ("ct_rows1", True, 1, 8, 8, 1, 8, 3, 3, 2, 1, 1, 1, "bf16"),
 ]
 
 
@@ -80,7 +86,7 @@ def test_weight_gradient(case):
     P.check(got, ref, absref, case[-1], case[0])
 
 
-@pytest.mark.parametrize("case", [CASES[0], CASES[5]], ids=lambda c: c[0])
+@pytest.mark.parametrize("case", [CASES[0], CASES[5], CASES[9]], ids=lambda c: c[0])
 def test_weight_gradient_chunks(case, monkeypatch):
     """Images split into chunks (one per image here): the fp32 gradient is
     accumulated over the chunks in order; same bar, and deterministic."""

@@ -32,6 +32,12 @@ CASES = [
     # small grids with rows of 2 and 1 pixels (staging pieces of whole rows)
     ("ct_rows2", True, 2, 16, 4, 2, 24, 4, 4, 2, 1, 0, 1, "f32"),
     ("ct_rows1", True, 1, 8, 8, 1, 8, 3, 3, 2, 1, 1, 1, "bf16"),
+    # 128 x 128 tiles on wider grids: ragged channels, dilation with output
+    # padding, and strided convs (small grid = their output)
+    ("ct_wide_ragged", True, 3, 136, 8, 16, 130, 4, 4, 2, 1, 0, 1, "bf16"),
+    ("ct_wide_dil_op", True, 2, 128, 8, 8, 128, 3, 3, 2, 2, 1, 2, "bf16"),
+    ("conv_wide", False, 2, 144, 16, 16, 136, 4, 4, 2, 1, 0, 1, "bf16"),
+    ("conv_wide_pad0", False, 1, 128, 18, 34, 128, 3, 3, 2, 0, 0, 1, "bf16"),
 ]
 
 

@@ -258,12 +258,12 @@ def _counter_per_dispatch(path, counter):
     return out
 
 
-MAIN_KERNELS = ("phase_gemm_kernel", "phase_gemm2_kernel", "ztile_kernel", "rowphase_kernel",
-                "quad_kernel")
+MAIN_KERNELS = ("phase_gemm_kernel", "phase_gemm2_kernel", "phase_gemm3_kernel", "ztile_kernel",
+                "rowphase_kernel", "colphase_kernel", "quad_kernel", "grouped_kernel")
 
 
 def _is_main(name):
-    return any(k + "<" in name or k + "(" in name for k in MAIN_KERNELS)
+    return any("::" + k + "<" in name or "::" + k + "(" in name for k in MAIN_KERNELS)
 
 
 def _layer_dispatches(per_dispatch, nl, trailing):

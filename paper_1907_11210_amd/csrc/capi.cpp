@@ -128,7 +128,12 @@ long long count_works(const huge2_conv_desc& d, bool transposed, int class_split
 }
 
 // Tile choice, from measurements on MI355X.  bf16: many pixels and at most
-// 128 output channels take the 8-wave 128 x 128 tile; 256 or more output
+// 128 output channels take the pipelined 4-wave 128 x 128 tile for
+// transposed convs (the odd-kernel layer 20.4 against 23.0 us, the NHWC
+// generator's third layer 33.4 against 37.9 us) and the two-operand 8-wave
+// tile of that shape for convs (the gathered data gradient of the
+// generator's last layer, one short K stage: 25.8 against 33.1 us); 256 or
+// more output
 // channels take the pipelined 8-wave 128 x 256 tile when every CU gets one
 // (the atrous pyramid: twice the pixels per weight fetch of 64 x 256, which
 // its L2 traffic needs; its three-buffer pipeline measured 1090 against 955
@@ -146,7 +151,7 @@ int choose_cfg(const huge2_conv_desc& d, bool transposed, int class_split) {
   if (d.c_out <= 32) return TILE_128x32;
   const bool large = count_works(d, transposed, class_split, TILE_128x128) >= 512;
   if (d.dtype != HUGE2_BF16) return large ? TILE_128x128 : TILE_64x128;
-  if (large && d.c_out <= 128) return TILE_128x128;
+  if (large && d.c_out <= 128) return transposed ? TILE_P3_128x128 : TILE_128x128;
   if (d.r == 1 && d.s == 1 && (long long)d.n * d.h * d.w <= 64 && d.c_out >= 256)
     return TILE_SW_32x256;  // a pointwise GEMM of at most 64 rows (the 1x1-input product form)
   if (d.c_out >= 256) {
@@ -221,6 +226,60 @@ void order_works_for_xcds(std::vector<WorkDev>& works, const std::vector<SegDev>
     return x.w.ks < y.w.ks;
   });
   for (size_t i = 0; i < works.size(); ++i) works[i] = keys[i].w;
+}
+
+// Works that are all resident at once (at most 32 x wg_per_cu per XCD).  The
+// y-th workgroup of an XCD's run then lands on compute unit y mod 32 of that
+// XCD (measured: workgroups y and y + 32 of a run share a unit), and
+// co-resident workgroups share the unit's MFMA, LDS and load pipes, so a unit
+// finishes after about the sum of its works' stages.  Inside each XCD's run
+// (the contiguous chunk of the list that xcd_remap gives it), the works are
+// dealt longest first to the least loaded unit with a free slot, and placed
+// so that unit k's works sit at run positions k, k + 32, ...  Works beyond
+// the resident slots (a few, from ragged segments) go last, shortest first:
+// they start on the units that free first.  Only the placement inside a run
+// changes, so an XCD keeps its share of the input and weights.
+void order_works_resident(std::vector<WorkDev>& works, int cblocks, int ksplit, int wg_per_cu) {
+  const int g = (int)works.size();
+  if (g < 16) return;
+  const int g8 = (g + 7) / 8, r = g % 8;
+  constexpr int kUnits = kComputeUnits / 8;
+  if (g8 > kUnits * wg_per_cu + kUnits) return;  // several rounds: the dispatcher balances
+  auto cost = [&](const WorkDev& w) {
+    const int cb = (w.ks + 1) * cblocks / ksplit - w.ks * cblocks / ksplit;
+    return (int64_t)w.tap_count * cb + 2;
+  };
+  std::vector<WorkDev> out(works.size());
+  for (int x = 0; x < 8; ++x) {
+    const int start = (r == 0 || x < r) ? x * g8 : r * g8 + (x - r) * (g8 - 1);
+    const int len = (r == 0 || x < r) ? g8 : g8 - 1;
+    std::vector<int> idx(len);
+    for (int i = 0; i < len; ++i) idx[i] = start + i;
+    std::stable_sort(idx.begin(), idx.end(),
+                     [&](int a, int b) { return cost(works[a]) > cost(works[b]); });
+    const int resident = std::min(len, kUnits * wg_per_cu);
+    const int units = std::min(len, kUnits);
+    std::vector<int64_t> load(units, 0);
+    std::vector<std::vector<int>> held(units);
+    for (int i = 0; i < resident; ++i) {
+      int best = -1;
+      for (int u = 0; u < units; ++u)
+        if ((int)held[u].size() < wg_per_cu && (best < 0 || load[u] < load[best])) best = u;
+      held[best].push_back(idx[i]);
+      load[best] += cost(works[idx[i]]);
+    }
+    // units holding more works first, so that every level is a prefix
+    std::stable_sort(held.begin(), held.end(), [](const std::vector<int>& a,
+                                                  const std::vector<int>& b) {
+      return a.size() > b.size();
+    });
+    int pos = start;
+    for (int level = 0; level < wg_per_cu; ++level)
+      for (int u = 0; u < units; ++u)
+        if ((int)held[u].size() > level) out[pos++] = works[held[u][level]];
+    for (int i = len - 1; i >= resident; --i) out[pos++] = works[idx[i]];
+  }
+  works.swap(out);
 }
 
 // Schedule model: the dispatcher hands the works, in list order, to the first
@@ -679,7 +738,11 @@ void work_progressions(const TapDev* tl, int count, int s_width, WorkDev* w) {
 // Border-class splitting of a plan: HUGE2_CLASS_SPLIT (0, 1, 2) forces it;
 // otherwise 0 (one segment per phase group, out-of-range taps read zeros) or
 // 2 (per group, the form that issues fewer tile-taps), whichever the schedule
-// model finishes first (ties: 2).
+// model finishes first (ties: 2).  When the works of form 0 are all resident
+// at once and the split's ragged segments add works beyond the resident
+// slots, form 0 wins: such a straggler starts only when a unit frees and
+// adds its whole latency (measured on the odd-kernel layer, 512 against 514
+// works: 21.3 against 25.1 us).
 int choose_split(const huge2_conv_desc& d, bool transposed, int cfg) {
   const int forced = env_int("HUGE2_CLASS_SPLIT", -1);
   if (forced >= 0 && forced <= 2) return forced;
@@ -687,6 +750,9 @@ int choose_split(const huge2_conv_desc& d, bool transposed, int cfg) {
   if (!build_shape(d, transposed, 0, tile_bm(cfg), &s0) ||
       !build_shape(d, transposed, 2, tile_bm(cfg), &s2))
     return 2;
+  const long long slots = (long long)kComputeUnits * kTiles[cfg].wg_per_cu;
+  const long long w0 = count_works(d, transposed, 0, cfg), w2 = count_works(d, transposed, 2, cfg);
+  if (w0 <= slots && w2 > slots) return 0;
   return makespan_stages(d, s0, cfg) < makespan_stages(d, s2, cfg) ? 0 : 2;
 }
 
@@ -1251,15 +1317,17 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     // the pipelined kernel steps through progressions only: the split-wave
     // kernel of the same tile and packing takes tap lists
     // (the same works and lane-ordered packing; its K block must divide the
-    // padded channel count)
-    for (int c = 0; c < TILE_COUNT; ++c) {
-      const TileShape &t = kTiles[c], &u = kTiles[p->cfg];
-      if (t.kind == 1 && t.bm == u.bm && t.bn == u.bn && t.ksplit == u.ksplit &&
-          p->cin_pad % (t.kb / esz) == 0) {
-        p->cfg = c;
-        break;
+    // padded channel count; one with the same K groups first)
+    const int from = p->cfg;
+    for (int pass = 0; pass < 2 && kTiles[p->cfg].kind == 3; ++pass)
+      for (int c = 0; c < TILE_COUNT; ++c) {
+        const TileShape &t = kTiles[c], &u = kTiles[from];
+        if (t.kind == 1 && t.bm == u.bm && t.bn == u.bn && (pass == 1 || t.ksplit == u.ksplit) &&
+            p->cin_pad % (t.kb / esz) == 0) {
+          p->cfg = c;
+          break;
+        }
       }
-    }
     if (kTiles[p->cfg].kind == 3) {
       free_buffers(p);
       delete p;
@@ -1311,11 +1379,20 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   p->n_works = (int)works.size();
   // NCHW outputs of transposed convs with few phases: the phases of a
   // region share input rows and output cache lines (measured: fewer bytes and
-  // faster); elsewhere the segment-major order measured as fast or faster.
+  // faster); elsewhere the segment-major order measured as fast or faster,
+  // except for works that are all resident at once: their XCDs then finish
+  // when their own works do, so every XCD takes a cell of every phase, and
+  // inside the cell long works share compute units with short ones.
+  // (HUGE2_WORK_ORDER=0 forces segment-major order, 1 the cells alone.)
   const int order = env_int("HUGE2_WORK_ORDER", -1);
-  if (order == 1 || (order < 0 && tr && d.layout == HUGE2_NCHW && d.stride_h * d.stride_w <= 16))
+  const bool resident =
+      (int64_t)works.size() <= (int64_t)kComputeUnits * kTiles[p->cfg].wg_per_cu + 8;
+  if (order == 1 || (order < 0 && tr && (d.layout == HUGE2_NCHW || resident) &&
+                     d.stride_h * d.stride_w <= 16))
     order_works_for_xcds(works, segs, d.n, p->ho, bn, ntiles_n, (double)p->x_bytes,
                          (double)d.r * d.s * p->cout_pad * p->cin_pad * esz);
+  if (order != 0 && order != 1 && resident)
+    order_works_resident(works, p->cin_pad / bk, p->ksplit, kTiles[p->cfg].wg_per_cu);
 
   const size_t seg_b = segs.size() * sizeof(SegDev);
   const size_t tap_b = taps.size() * sizeof(TapDev);

@@ -131,6 +131,7 @@ enum TileCfg {
   TILE_SW_128x256 = 8,   // split-wave: 8 waves of 128 x 32 channels
   TILE_P3_128x256 = 9,   // pipelined split-wave: 8 waves of 128 x 32 channels
   TILE_P3_128x256_W4 = 10,  // pipelined split-wave: 4 waves of 128 x 64 channels, 64-byte K
+  TILE_P3_128x128 = 11,  // pipelined split-wave: 4 waves of 128 x 32 channels
 };
 constexpr TileShape kTiles[] = {
     {128, 128, 4, 2, 128, 2, 2, 0},     // TILE_128x128
@@ -144,6 +145,7 @@ constexpr TileShape kTiles[] = {
     {128, 256, 1, 8, 128, 3, 1, 1, 1},  // TILE_SW_128x256
     {128, 256, 1, 8, 128, 32, 1, 3, 1},  // TILE_P3_128x256
     {128, 256, 1, 4, 64, 32, 2, 3, 1},   // TILE_P3_128x256_W4
+    {128, 128, 1, 4, 128, 32, 2, 3, 1},  // TILE_P3_128x128
 };
 // A split-K plan may switch from the two-K-group 64 x 128 tile to its
 // one-group form after the work list and the weight packing were laid out for

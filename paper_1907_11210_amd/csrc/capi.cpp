@@ -523,13 +523,17 @@ bool colphase_shape(const huge2_conv_desc& d, bool transposed, CpArgs* z, int64_
     return false;
   const int qw_lo = ceil_div_i(d.pad_w - 31, 32), qw_hi = floor_div_i(wo - 1 + d.pad_w, 32);
   if (qw_lo < 0 || qw_hi > d.w || qw_hi < qw_lo) return false;
+  // issued: the kernel's column tiles, kCpRows rows of a row phase at a time
   int64_t cols = 0;
   for (int rho = 0; rho < d.stride_h; ++rho) {
     const int q_lo = ceil_div_i(d.pad_h - rho, d.stride_h);
     const int q_hi = floor_div_i(ho - 1 + d.pad_h - rho, d.stride_h);
     if (q_hi < q_lo) continue;
     if (q_lo < 0 || q_hi > d.h) return false;
-    cols += ((int64_t)(q_hi - q_lo + 1) * (qw_hi - qw_lo + 1) + 31) / 32 * 32;
+    for (int q0 = 0; q0 < q_hi - q_lo + 1; q0 += kCpRows) {
+      const int nr = std::min(kCpRows, q_hi - q_lo + 1 - q0);
+      cols += ((int64_t)nr * (qw_hi - qw_lo + 1) + 31) / 32 * 32;
+    }
   }
   std::memset(z, 0, sizeof(*z));
   z->n = d.n;

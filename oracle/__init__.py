@@ -185,12 +185,13 @@ def conv2d_dilated_points(x, w, flat_idx, bias=None, stride=1, padding=0, dilati
 
 
 def conv2d_transpose_wgrad(x, dy, w_shape, stride=1, padding=0, output_padding=0, dilation=1,
-                           nthreads=None):
-    """Weight gradient of the transposed conv: dw [C_in, C_out, R, S] from the
-    input x and the output error dy; float64."""
+                           nthreads=None, groups=1):
+    """Weight gradient of the transposed conv: dw [C_in, C_out/groups, R, S]
+    from the input x and the output error dy; float64."""
     x, dy = _f64(x), _f64(dy)
-    d = _desc(x.shape, tuple(w_shape), True, stride, padding, output_padding, dilation)
-    ho, wo = transpose_out_dims(x.shape, w_shape, stride, padding, output_padding, dilation)
+    d = _desc(x.shape, tuple(w_shape), True, stride, padding, output_padding, dilation, groups)
+    ho, wo = transpose_out_dims(x.shape, w_shape, stride, padding, output_padding, dilation,
+                                groups)
     if dy.shape != (d.n, d.c_out, ho, wo):
         raise ValueError("dy shape %s does not match the output %s" % (dy.shape, (d.n, d.c_out, ho, wo)))
     dw = np.empty(tuple(w_shape), dtype=np.float64)
@@ -200,12 +201,13 @@ def conv2d_transpose_wgrad(x, dy, w_shape, stride=1, padding=0, output_padding=0
     return dw
 
 
-def conv2d_dilated_wgrad(x, dy, w_shape, stride=1, padding=0, dilation=1, nthreads=None):
-    """Weight gradient of the dilated / strided conv: dw [C_out, C_in, R, S]
-    from the input x and the output error dy; float64."""
+def conv2d_dilated_wgrad(x, dy, w_shape, stride=1, padding=0, dilation=1, nthreads=None,
+                         groups=1):
+    """Weight gradient of the dilated / strided conv: dw [C_out, C_in/groups,
+    R, S] from the input x and the output error dy; float64."""
     x, dy = _f64(x), _f64(dy)
-    d = _desc(x.shape, tuple(w_shape), False, stride, padding, 0, dilation)
-    ho, wo = conv_out_dims(x.shape, w_shape, stride, padding, dilation)
+    d = _desc(x.shape, tuple(w_shape), False, stride, padding, 0, dilation, groups)
+    ho, wo = conv_out_dims(x.shape, w_shape, stride, padding, dilation, groups)
     if dy.shape != (d.n, d.c_out, ho, wo):
         raise ValueError("dy shape %s does not match the output %s" % (dy.shape, (d.n, d.c_out, ho, wo)))
     dw = np.empty(tuple(w_shape), dtype=np.float64)

@@ -347,7 +347,10 @@ int oracle_conv2d_dilated_points(const oracle_conv* d, const double* x, const do
 
 /* ------------------------------------------------------------------ */
 /* Weight gradients (section 3.2.3): the chain rule applied to the two  */
-/* definitions above, one weight element at a time.                     */
+/* definitions above, one weight element at a time.  With groups, a     */
+/* weight element joins input channel c only to the output channels of  */
+/* c's group, so its gradient sums over that pair alone (groups = c_in  */
+/* is the depthwise case: one input and one output map per element).    */
 
 typedef struct {
   const oracle_conv* d;
@@ -358,11 +361,21 @@ typedef struct {
   int transposed;
 } wgrad_ctx;
 
-/* dw for weight plane (c, k): all r x s taps. */
+/* dw for one weight plane (all r x s taps): transposed, plane (c, k - first
+ * output channel of c's group) of w [c_in][c_out/groups]; otherwise plane
+ * (k, c - first input channel of k's group) of w [c_out][c_in/groups]. */
 static void wgrad_plane(void* p, long plane) {
   wgrad_ctx* a = (wgrad_ctx*)p;
   const oracle_conv* d = a->d;
-  const int c = (int)(plane / d->c_out), k = (int)(plane % d->c_out);
+  const int g = ngroups(d), cig = d->c_in / g, cog = d->c_out / g;
+  int c, k;
+  if (a->transposed) {
+    c = (int)(plane / cog);
+    k = (c / cig) * cog + (int)(plane % cog);
+  } else {
+    k = (int)(plane / cig);
+    c = (k / cog) * cig + (int)(plane % cig);
+  }
   for (int m = 0; m < d->r; ++m)
     for (int q = 0; q < d->s; ++q) {
       double acc = 0.0;
@@ -379,7 +392,7 @@ static void wgrad_plane(void* p, long plane) {
                      a->dy[(((long)n * d->c_out + k) * a->ho + oh) * a->wo + ow];
             }
           }
-        a->dw[(((long)c * d->c_out + k) * d->r + m) * d->s + q] = acc;
+        a->dw[(((long)c * cog + k % cog) * d->r + m) * d->s + q] = acc;
       } else {
         /* every output pixel (oh, ow) and the input it reads through tap (m, q) */
         for (int n = 0; n < d->n; ++n)
@@ -393,7 +406,7 @@ static void wgrad_plane(void* p, long plane) {
                      a->x[(((long)n * d->c_in + c) * d->h + ih) * d->w + iw];
             }
           }
-        a->dw[(((long)k * d->c_in + c) * d->r + m) * d->s + q] = acc;
+        a->dw[(((long)k * cig + c % cig) * d->r + m) * d->s + q] = acc;
       }
     }
 }
@@ -401,27 +414,25 @@ static void wgrad_plane(void* p, long plane) {
 int oracle_conv2d_transpose_wgrad(const oracle_conv* d, const double* x, const double* dy,
                                   double* dw, int nthreads) {
   wgrad_ctx a;
-  if (!x || !dy || !dw || oracle_transpose_out_dims(d, &a.ho, &a.wo) != 0 || ngroups(d) != 1)
-    return -1;
+  if (!x || !dy || !dw || oracle_transpose_out_dims(d, &a.ho, &a.wo) != 0) return -1;
   a.d = d;
   a.x = x;
   a.dy = dy;
   a.dw = dw;
   a.transposed = 1;
-  run_parallel(wgrad_plane, &a, (long)d->c_in * d->c_out, nthreads);
+  run_parallel(wgrad_plane, &a, (long)d->c_in * (d->c_out / ngroups(d)), nthreads);
   return 0;
 }
 
 int oracle_conv2d_dilated_wgrad(const oracle_conv* d, const double* x, const double* dy,
                                 double* dw, int nthreads) {
   wgrad_ctx a;
-  if (!x || !dy || !dw || oracle_conv_out_dims(d, &a.ho, &a.wo) != 0 || ngroups(d) != 1)
-    return -1;
+  if (!x || !dy || !dw || oracle_conv_out_dims(d, &a.ho, &a.wo) != 0) return -1;
   a.d = d;
   a.x = x;
   a.dy = dy;
   a.dw = dw;
   a.transposed = 0;
-  run_parallel(wgrad_plane, &a, (long)d->c_in * d->c_out, nthreads);
+  run_parallel(wgrad_plane, &a, (long)d->c_out * (d->c_in / ngroups(d)), nthreads);
   return 0;
 }

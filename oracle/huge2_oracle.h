@@ -34,8 +34,9 @@ typedef struct {
   int dil_h, dil_w;
   /* Grouped convolution (0 or 1: none): the channels split into `groups`
    * equal groups, and output channel k of group k / (c_out/groups) sums only
-   * over the input channels of the same group (PyTorch's groups).  The
-   * weight gradients take groups <= 1 only. */
+   * over the input channels of the same group (PyTorch's groups); the
+   * weight gradients then join each weight element's input channel to the
+   * output channels of its own group only. */
   int groups;
 } oracle_conv;
 

@@ -156,15 +156,22 @@ def test_golden_weight_gradients(oracle_mod, path):
     with open(path) as f:
         g = json.load(f)
     assert g["citation"]
-    x = np.array(g["x"], dtype=np.float64)[None, None]
-    dy = np.array(g["dy"], dtype=np.float64)[None, None]
-    if g["op"] == "transpose_wgrad":
+    groups = g.get("groups", 1)
+    if groups > 1:  # multi-channel fixtures: [C][H][W] maps, the whole gradient
+        x = np.array(g["x"], dtype=np.float64)[None]
+        dy = np.array(g["dy"], dtype=np.float64)[None]
+    else:
+        x = np.array(g["x"], dtype=np.float64)[None, None]
+        dy = np.array(g["dy"], dtype=np.float64)[None, None]
+    if g["op"].startswith("transpose"):
         dw = oracle_mod.conv2d_transpose_wgrad(x, dy, g["w_shape"], g["stride"], g["padding"],
-                                               g["output_padding"], g["dilation"], nthreads=1)
+                                               g["output_padding"], g["dilation"], nthreads=1,
+                                               groups=groups)
     else:
         dw = oracle_mod.conv2d_dilated_wgrad(x, dy, g["w_shape"], g["stride"], g["padding"],
-                                             g["dilation"], nthreads=1)
-    np.testing.assert_array_equal(dw[0, 0], np.array(g["expected"], dtype=np.float64))
+                                             g["dilation"], nthreads=1, groups=groups)
+    exp = np.array(g["expected"], dtype=np.float64)
+    np.testing.assert_array_equal(dw if groups > 1 else dw[0, 0], exp)
 
 
 def _random_case(rng, transposed):
@@ -430,6 +437,56 @@ def test_wgrad_matches_torch_autograd(oracle_mod, transposed):
         np.testing.assert_allclose(got, w.grad.numpy(), rtol=1e-10, atol=1e-10)
         checked += 1
     assert checked >= 30
+
+
+@pytest.mark.parametrize("transposed", [True, False])
+def test_grouped_wgrad_matches_torch_autograd(oracle_mod, transposed):
+    """Grouped and depthwise weight gradients against torch CPU autograd in
+    float64 (an independent routine), and the inner-product identity with
+    the separately pinned grouped forward definitions."""
+    rng = np.random.default_rng(93 if transposed else 94)
+    checked = depthwise = 0
+    for _ in range(80):
+        c = _random_case(rng, transposed)
+        g = int(rng.integers(2, 5))
+        cig, cog = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+        if rng.random() < 0.4:
+            cig = 1  # depthwise (with a channel multiplier cog)
+        ci, co = g * cig, g * cog
+        x = rng.standard_normal((c["n"], ci, c["h"], c["w"]))
+        wshape = (ci, cog, c["r"], c["s"]) if transposed else (co, cig, c["r"], c["s"])
+        w = torch.tensor(rng.standard_normal(wshape), requires_grad=True)
+        try:
+            if transposed:
+                y = torch.nn.functional.conv_transpose2d(torch.from_numpy(x), w, stride=c["stride"],
+                                                         padding=c["pad"], output_padding=c["op"],
+                                                         dilation=c["dil"], groups=g)
+            else:
+                y = torch.nn.functional.conv2d(torch.from_numpy(x), w, stride=c["stride"],
+                                               padding=c["pad"], dilation=c["dil"], groups=g)
+        except RuntimeError:
+            continue
+        if y.numel() == 0:
+            continue
+        dy = rng.standard_normal(tuple(y.shape))
+        (y * torch.from_numpy(dy)).sum().backward()
+        v = rng.standard_normal(wshape)
+        if transposed:
+            got = oracle_mod.conv2d_transpose_wgrad(x, dy, wshape, c["stride"], c["pad"], c["op"],
+                                                    c["dil"], nthreads=2, groups=g)
+            yv = oracle_mod.conv2d_transpose_alg1(x, v, None, c["stride"], c["pad"], c["op"],
+                                                  c["dil"], nthreads=2, groups=g)
+        else:
+            got = oracle_mod.conv2d_dilated_wgrad(x, dy, wshape, c["stride"], c["pad"], c["dil"],
+                                                  nthreads=2, groups=g)
+            yv = oracle_mod.conv2d_dilated_alg2(x, v, None, c["stride"], c["pad"], c["dil"],
+                                                nthreads=2, groups=g)
+        np.testing.assert_allclose(got, w.grad.numpy(), rtol=1e-10, atol=1e-10)
+        lhs, rhs = float(np.sum(got * v)), float(np.sum(dy * yv))
+        assert abs(lhs - rhs) <= 1e-12 * max(1.0, np.sum(np.abs(got * v)), np.sum(np.abs(dy * yv)))
+        checked += 1
+        depthwise += cig == 1
+    assert checked >= 30 and depthwise >= 8
 
 
 @pytest.mark.parametrize("act", ["relu", "tanh"])

@@ -91,8 +91,9 @@ typedef struct {
    * second axis.  groups = c_in is the depthwise convolution (a channel
    * multiplier c_out/c_in).  Grouped layers run on a direct kernel that
    * forms each output from its phase's taps (section 3.1) and its group's
-   * channels; the weight-gradient entry points and grouped launches
-   * (huge2_group) take groups <= 1 only. */
+   * channels, and their weight gradients on a direct per-plane kernel (see
+   * the training section); grouped launches (huge2_group) take groups <= 1
+   * only. */
   int32_t groups;
 } huge2_conv_desc;
 
@@ -280,14 +281,21 @@ huge2_status huge2_group_destroy(huge2_group* group);
  * and every tap's gradient is then one dense MFMA GEMM over pixels with no
  * zero products, accumulated in fp32 over chunks of images in a fixed order
  * and rounded once to the dtype.
+ * Grouped layers (groups > 1; dw is [c_in][c_out/groups][r][s] or
+ * [c_out][c_in/groups][r][s]): the sums above run only over channel pairs of
+ * one group.  Each weight plane then joins one input map to one error map --
+ * the depthwise form of section 3.2.3, an outer product of two maps summed
+ * over the pixels -- and is summed directly in fp32 (one workgroup per plane
+ * and run of 16 taps, a fixed reduction order), with no workspace.
  * Layout: NCHW only (HUGE2_NHWC returns HUGE2_ERR_UNSUPPORTED).  dtype as
  * above: x, dy and dw share it; accumulation is fp32 for both dtypes. */
 typedef struct huge2_wgrad_plan huge2_wgrad_plan;
 
 /* Build a weight-gradient plan for desc (the forward layer's descriptor;
- * transposed selects the layer type).  Allocates the per-plan workspace:
- * the staged operands of one chunk of images (the chunk is sized so they
- * stay under 256 MiB; at least one image) and the fp32 gradient.  No HIP
+ * transposed selects the layer type).  Allocates the per-plan workspace
+ * (none for grouped layers): the staged operands of one chunk of images
+ * (the chunk is sized so they stay under 256 MiB; at least one image) and
+ * the fp32 gradient.  No HIP
  * work is enqueued.  Errors: INVALID_ARG (NULL out/desc, invalid
  * descriptor), UNSUPPORTED (NHWC; byte extents of 2^31 or more), ALLOC. */
 huge2_status huge2_wgrad_plan_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc,

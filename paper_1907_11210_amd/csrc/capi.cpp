@@ -1741,6 +1741,7 @@ struct huge2_wgrad_plan {
   int chunk;           // images per chunk
   int kp;              // padded K of a full chunk
   int ksplit;          // K ranges per tap (workgroups along K)
+  int groups;          // > 1: grouped conv (direct per-plane sums, no workspace)
   void* st;
   void* bt;
   float* g;
@@ -1765,8 +1766,7 @@ huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, i
   huge2_status st = validate_desc(desc, transposed != 0);
   if (st != HUGE2_OK) return st;
   const huge2_conv_desc& d = *desc;
-  if (d.layout != HUGE2_NCHW || d.activation != HUGE2_ACT_NONE || d.groups > 1)
-    return HUGE2_ERR_UNSUPPORTED;
+  if (d.layout != HUGE2_NCHW || d.activation != HUGE2_ACT_NONE) return HUGE2_ERR_UNSUPPORTED;
   int ho, wo;
   if (!output_dims(d, transposed != 0, &ho, &wo)) return HUGE2_ERR_INVALID_ARG;
   huge2_wgrad_plan* p = new (std::nothrow) huge2_wgrad_plan();
@@ -1779,6 +1779,22 @@ huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, i
     p->ms = d.c_out, p->nb = d.c_in, p->hs = ho, p->ws = wo, p->hb = d.h, p->wb = d.w;
   }
   const long long esz = elem_size(d.dtype), taps = (long long)d.r * d.s;
+  if (d.groups > 1) {
+    // grouped: one plane per (small channel, big channel of its group), no
+    // staged operands and no fp32 gradient (wgrad_grouped_kernel)
+    const long long big_b = (long long)d.n * p->nb * p->hb * p->wb * esz;
+    const long long small_b = (long long)d.n * p->ms * p->hs * p->ws * esz;
+    if (big_b >= (1ll << 40) || small_b >= (1ll << 40) || taps > 65535 ||
+        (long long)p->ms * (p->nb / d.groups) >= (1ll << 31)) {
+      delete p;
+      return HUGE2_ERR_UNSUPPORTED;
+    }
+    p->groups = d.groups;
+    p->chunk = d.n;
+    p->ksplit = 1;
+    *out = p;
+    return HUGE2_OK;
+  }
   const long long hws = (long long)p->hs * p->ws;
   const long long per_img = esz * (p->ms + taps * p->nb) * hws;
   long long chunk = std::max(1ll, std::min<long long>(d.n, kWgradStageBudget / std::max(1ll, per_img)));
@@ -1842,6 +1858,16 @@ huge2_status wgrad_execute(const huge2_wgrad_plan* p, const void* x, const void*
   a.stride_h = d.stride_h, a.stride_w = d.stride_w, a.pad_h = d.pad_h, a.pad_w = d.pad_w;
   a.dil_h = d.dil_h, a.dil_w = d.dil_w;
   a.ksplit = p->ksplit;
+  if (p->groups > 1) {
+    a.groups = p->groups;
+    a.img0 = 0;
+    a.nimg = d.n;
+    if (launch_wgrad_grouped(a, d.dtype, stream) != hipSuccess) {
+      (void)hipGetLastError();
+      return HUGE2_ERR_HIP;
+    }
+    return HUGE2_OK;
+  }
   const long long hws = (long long)p->hs * p->ws;
   // chunks in order: the first writes the fp32 gradient, the rest add to it
   for (int img0 = 0; img0 < d.n; img0 += p->chunk) {

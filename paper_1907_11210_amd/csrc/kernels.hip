@@ -2976,6 +2976,90 @@ hipError_t launch_wgrad_store(const WgArgs& a, int dtype, hipStream_t stream) {
 }
 
 // ---------------------------------------------------------------------------
+// Weight gradient of a grouped conv (groups > 1; groups = channels is the
+// depthwise conv).  Weight plane (cs, bl) joins small-tensor channel cs to
+// big-tensor channel cb = (cs / (ms/groups)) * (nb/groups) + bl, and
+//   dw[cs][bl][m][q] = sum over images n and small pixels (i, j) of
+//     small[n][cs][i][j] * big[n][cb][i*stride_h - pad_h + m*dil_h]
+//                                    [j*stride_w - pad_w + q*dil_w]
+// (out-of-range big pixels omitted): per plane the depthwise form of section
+// 3.2.3, the outer product of two maps summed over the pixels.  No GEMM is
+// left to tile (one channel on each side of a plane), so the sums run on the
+// vector units in fp32: one workgroup per (plane, run of kWgGTaps taps), each
+// thread summing a fixed stride of the pixels for every tap of the run, then
+// the workgroup adds the threads' sums in a fixed tree order
+// (deterministic) and rounds once to the dtype.
+constexpr int kWgGTaps = 16;
+
+template <typename T>
+__global__ __launch_bounds__(256) void wgrad_grouped_kernel(WgArgs a) {
+  __shared__ float red[kWgGTaps][257];
+  const T* __restrict__ sm = (const T*)a.sm;
+  const T* __restrict__ bg = (const T*)a.bg;
+  const int tid = threadIdx.x;
+  const int sgc = a.ms / a.groups, bgc = a.nb / a.groups;
+  const int plane = blockIdx.x;
+  const int cs = plane / bgc, bl = plane - cs * bgc;
+  const int cb = (cs / sgc) * bgc + bl;
+  const int taps = a.r * a.s, t0 = blockIdx.y * kWgGTaps;
+  int dh[kWgGTaps], dwo[kWgGTaps];
+#pragma unroll
+  for (int u = 0; u < kWgGTaps; ++u) {
+    const int t = min(t0 + u, taps - 1), m = t / a.s, q = t - m * a.s;
+    dh[u] = m * a.dil_h - a.pad_h;
+    dwo[u] = q * a.dil_w - a.pad_w;
+  }
+  float acc[kWgGTaps];
+#pragma unroll
+  for (int u = 0; u < kWgGTaps; ++u) acc[u] = 0.f;
+  const int hws = a.hs * a.ws;
+  for (int n = 0; n < a.nimg; ++n) {
+    const T* sp = sm + ((size_t)n * a.ms + cs) * hws;
+    const T* bp = bg + ((size_t)n * a.nb + cb) * ((size_t)a.hb * a.wb);
+    for (int p = tid; p < hws; p += 256) {
+      const int i = p / a.ws, j = p - i * a.ws;
+      const float v = to_f32(sp[p]);
+      const int bi = i * a.stride_h, bj = j * a.stride_w;
+#pragma unroll
+      for (int u = 0; u < kWgGTaps; ++u) {
+        const int y = bi + dh[u], x = bj + dwo[u];
+        if (t0 + u < taps && (unsigned)y < (unsigned)a.hb && (unsigned)x < (unsigned)a.wb)
+          acc[u] = fmaf(v, to_f32(bp[(size_t)y * a.wb + x]), acc[u]);
+      }
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kWgGTaps; ++u) red[u][tid] = acc[u];
+  __syncthreads();
+  for (int st = 128; st > 0; st >>= 1) {
+    if (tid < st)
+#pragma unroll
+      for (int u = 0; u < kWgGTaps; ++u) red[u][tid] += red[u][tid + st];
+    __syncthreads();
+  }
+  if (tid < kWgGTaps && t0 + tid < taps) {
+    const float v = red[tid][0];
+    const size_t o = (size_t)plane * taps + t0 + tid;
+    if constexpr (std::is_same<T, uint16_t>::value)
+      ((uint16_t*)a.dw)[o] = f32_to_bf16_rne(v);
+    else
+      ((float*)a.dw)[o] = v;
+  }
+}
+
+hipError_t launch_wgrad_grouped(const WgArgs& a, int dtype, hipStream_t stream) {
+  const long long planes = (long long)a.ms * (a.nb / a.groups);
+  const int taps = a.r * a.s;
+  if (planes <= 0 || planes >= (1ll << 31) || a.groups < 2) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)planes, (unsigned)((taps + kWgGTaps - 1) / kWgGTaps));
+  if (dtype == 1)
+    hipLaunchKernelGGL(wgrad_grouped_kernel<uint16_t>, grid, dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(wgrad_grouped_kernel<uint32_t>, grid, dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // Input staging: channel-contiguous pixels [n][h*w][c_stride], zero padded
 // channels, for NCHW inputs and for NHWC inputs whose channel count is not a
 // multiple of 16 bytes.

@@ -390,6 +390,7 @@ struct WgArgs {
   int kp;          // padded K of the chunk (multiple of 64)
   int accumulate;  // 0: G = product, 1: G += product
   int ksplit;      // K ranges per tap, each with its own fp32 slice of G
+  int groups;      // > 1: grouped conv (wgrad_grouped_kernel; st, bt and g unused)
 };
 // Output tile of the weight-gradient GEMM (square, channels of the small x
 // the large tensor): 128 x 128 when both channel counts reach 128, else 64.
@@ -397,6 +398,7 @@ inline int wgrad_tile(int ms, int nb) { return ms >= 128 && nb >= 128 ? 128 : 64
 hipError_t launch_wgrad_stage(const WgArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_wgrad_gemm(const WgArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_wgrad_store(const WgArgs& a, int dtype, hipStream_t stream);
+hipError_t launch_wgrad_grouped(const WgArgs& a, int dtype, hipStream_t stream);
 
 // Re-layout the input into [n][h*w][c_stride] with zero channel padding.
 // nchw: source is NCHW; otherwise NHWC with cin channels per pixel.

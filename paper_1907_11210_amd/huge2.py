@@ -413,7 +413,8 @@ def conv2d_dilated(x, w, bias=None, stride=1, padding=0, dilation=1, layout="NCH
     return y
 
 
-def _wgrad(x, dy, w_shape, transposed, stride, padding, output_padding, dilation, out):
+def _wgrad(x, dy, w_shape, transposed, stride, padding, output_padding, dilation, out,
+           groups=1):
     torch = _torch()
     _check_tensor(x, "x")
     _check_tensor(dy, "dy", x.device)
@@ -423,14 +424,17 @@ def _wgrad(x, dy, w_shape, transposed, stride, padding, output_padding, dilation
     if x.dim() != 4 or len(w_shape) != 4:
         raise ValueError("x and the weight shape must be 4-D")
     n, c_in, h, wd = x.shape
+    g = int(groups)
     if transposed:
-        wc_in, c_out, r, s = w_shape
+        wc_in, cog, r, s = w_shape
+        c_out = cog * g
     else:
-        c_out, wc_in, r, s = w_shape
+        c_out, cig, r, s = w_shape
+        wc_in = cig * g
     if wc_in != c_in:
         raise ValueError("weight has %d input channels, x has %d" % (wc_in, c_in))
     desc = make_desc(n, c_in, h, wd, c_out, r, s, stride, padding, output_padding, dilation,
-                     HUGE2_NCHW, _dtype_code(x))
+                     HUGE2_NCHW, _dtype_code(x), groups=g)
     if tuple(dy.shape) != _out_shape(desc, transposed):
         raise ValueError("dy has shape %s, the layer's output is %s"
                          % (tuple(dy.shape), _out_shape(desc, transposed)))
@@ -444,16 +448,16 @@ def _wgrad(x, dy, w_shape, transposed, stride, padding, output_padding, dilation
 
 
 def conv2d_transpose_wgrad(x, dy, w_shape, stride=1, padding=0, output_padding=0, dilation=1,
-                           out=None):
-    """Weight gradient of the transposed conv (NCHW): dw [C_in, C_out, R, S]
-    from the input x and the output error dy."""
-    return _wgrad(x, dy, w_shape, True, stride, padding, output_padding, dilation, out)
-
-
-def conv2d_dilated_wgrad(x, dy, w_shape, stride=1, padding=0, dilation=1, out=None):
-    """Weight gradient of the dilated / strided conv (NCHW): dw [C_out, C_in,
+                           out=None, groups=1):
+    """Weight gradient of the transposed conv (NCHW): dw [C_in, C_out/groups,
     R, S] from the input x and the output error dy."""
-    return _wgrad(x, dy, w_shape, False, stride, padding, 0, dilation, out)
+    return _wgrad(x, dy, w_shape, True, stride, padding, output_padding, dilation, out, groups)
+
+
+def conv2d_dilated_wgrad(x, dy, w_shape, stride=1, padding=0, dilation=1, out=None, groups=1):
+    """Weight gradient of the dilated / strided conv (NCHW): dw [C_out,
+    C_in/groups, R, S] from the input x and the output error dy."""
+    return _wgrad(x, dy, w_shape, False, stride, padding, 0, dilation, out, groups)
 
 
 def conv2d_transpose_dgrad(dy, w, stride=1, padding=0, dilation=1, layout="NCHW"):

@@ -164,3 +164,68 @@ def test_data_gradients_are_the_exchanged_forward_forms():
     x2 = np.random.default_rng(3).standard_normal((2, 16, 11, 11))
     y2 = oracle.conv2d_dilated_alg2(x2, w2.double().numpy(), None, 2, 1, 1)
     assert abs(np.sum(y2 * dy2.double().numpy()) - np.sum(x2 * ref2)) < 1e-9 * np.sum(np.abs(y2 * dy2.double().numpy()))
+
+
+# grouped and depthwise layers: (name, transposed, n, c_in, h, w, c_out, r, s,
+# stride, pad, out_pad, dil, dtype, groups)
+GROUPED_CASES = [
+    # depthwise transposed upsampling (the generator-side depthwise layer)
+    ("ct_depthwise", True, 3, 32, 8, 8, 32, 4, 4, 2, 1, 0, 1, "bf16", 32),
+    # channel multiplier 2, output padding and dilation, fp32
+    ("ct_dw_mult2_f32", True, 2, 6, 5, 7, 12, 3, 3, 2, 1, 1, 2, "f32", 6),
+    # four groups of 8 -> 6 channels, a 5x5 kernel (two runs of 16 taps)
+    ("ct_groups4_k5", True, 2, 32, 6, 5, 24, 5, 5, 2, 2, 1, 1, "bf16", 4),
+    # the discriminator's depthwise strided conv (section 3.2.3's C = 1 case)
+    ("conv_depthwise", False, 4, 24, 16, 16, 24, 4, 4, 2, 1, 0, 1, "bf16", 24),
+    # dilated grouped conv, 3 groups of 4 -> 5 channels
+    ("conv_groups3_dil", False, 2, 12, 13, 11, 15, 3, 3, 1, 2, 0, 2, "f32", 3),
+    # many pixels per plane (more than one pass of the workgroup's threads)
+    ("conv_dw_large", False, 2, 8, 40, 36, 8, 3, 3, 1, 1, 0, 1, "bf16", 8),
+]
+
+
+def _g_w_shape(c):
+    _, tr, n, ci, h, w, co, r, s = c[:9]
+    g = c[14]
+    return (ci, co // g, r, s) if tr else (co, ci // g, r, s)
+
+
+def _g_oracle(c, xq, dyq, absolute=False):
+    name, tr, n, ci, h, w, co, r, s, st, pd, op, dl, dt, g = c
+    x, dy = xq.double().numpy(), dyq.double().numpy()
+    if absolute:
+        x, dy = np.abs(x), np.abs(dy)
+    if tr:
+        return oracle.conv2d_transpose_wgrad(x, dy, _g_w_shape(c), st, pd, op, dl, groups=g)
+    return oracle.conv2d_dilated_wgrad(x, dy, _g_w_shape(c), st, pd, dl, groups=g)
+
+
+@pytest.mark.parametrize("case", GROUPED_CASES, ids=lambda c: c[0])
+def test_grouped_weight_gradient(case):
+    """Grouped and depthwise weight gradients (each weight plane joins one
+    input map to one error map) against the grouped oracle, element by
+    element, deterministic across calls, through the plan entry points too."""
+    P.say("case", case)
+    name, tr, n, ci, h, w, co, r, s, st, pd, op, dl, dt, g = case
+    xq, dyq = _inputs(case[:14], seed=11)
+    ref, absref = _g_oracle(case, xq, dyq), _g_oracle(case, xq, dyq, absolute=True)
+    dev = torch.device("cuda", 0)
+    x, dy = xq.to(dev), dyq.to(dev)
+    if tr:
+        got = h2.conv2d_transpose_wgrad(x, dy, _g_w_shape(case), st, pd, op, dl, groups=g)
+    else:
+        got = h2.conv2d_dilated_wgrad(x, dy, _g_w_shape(case), st, pd, dl, groups=g)
+    torch.cuda.synchronize()
+    got = got.cpu().double().numpy()
+    P.check(got, ref, absref, dt, name)
+    desc = h2.make_desc(n, ci, h, w, co, r, s, st, pd, op, dl, h2.HUGE2_NCHW,
+                        h2.HUGE2_BF16 if dt == "bf16" else h2.HUGE2_F32, groups=g)
+    plan = h2.huge2_wgrad_plan_create(desc, int(tr))
+    try:
+        dw = torch.full(_g_w_shape(case), float("nan"), dtype=x.dtype, device=dev)
+        h2.huge2_wgrad_execute(plan, x.data_ptr(), dy.data_ptr(), dw.data_ptr(),
+                               torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        assert np.array_equal(dw.cpu().double().numpy(), got)
+    finally:
+        h2.huge2_wgrad_plan_destroy(plan)

@@ -19,9 +19,13 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SOURCES = ["plan.cpp", "capi.cpp", "kernels.hip"]
 
 # Packed-FP32 VALU ops are disabled for all device code; the host pass only
-# warns that it does not know the feature.
+# warns that it does not know the feature.  MFMA accumulators live in
+# ordinary VGPRs (-amdgpu-mfma-vgpr-form): kernels whose accumulators the
+# compiler would place in AGPRs then skip the copies to and from them in
+# every epilogue (the column-phase kernel's tile epilogues spent 32 of their
+# VALU instructions on those copies), and no kernel needs more registers.
 DEVICE_FLAGS = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang",
-                "-packed-fp32-ops"]
+                "-packed-fp32-ops", "-mllvm", "-amdgpu-mfma-vgpr-form"]
 COMMON_FLAGS = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I", os.path.join(ROOT, "include"),
                 "-I", CSRC]
 

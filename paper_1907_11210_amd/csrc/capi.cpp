@@ -519,7 +519,8 @@ bool colphase_shape(const huge2_conv_desc& d, bool transposed, CpArgs* z, int64_
   int ho, wo;
   if (!output_dims(d, true, &ho, &wo) || wo % 8 != 0) return false;
   const int cp = round_up(d.c_in, 8);
-  if (((long long)(d.h + 2) * (d.w + 2) * cp + (long long)kCpWaves * kCpRows * wo) * 2 > kCpMaxLds)
+  if (((long long)(d.h + 2) * (d.w + 2) * cp + (long long)kCpWaves * kCpRows * round_up(wo, 32)) *
+          2 > kCpMaxLds)
     return false;
   const int qw_lo = ceil_div_i(d.pad_w - 31, 32), qw_hi = floor_div_i(wo - 1 + d.pad_w, 32);
   if (qw_lo < 0 || qw_hi > d.w || qw_hi < qw_lo) return false;
@@ -551,9 +552,9 @@ bool colphase_shape(const huge2_conv_desc& d, bool transposed, CpArgs* z, int64_
   z->cp = cp;
   z->qw_lo = qw_lo;
   z->nqw = qw_hi - qw_lo + 1;
-  const uint32_t dv[4] = {(uint32_t)(d.w + 2), (uint32_t)(d.h + 2), (uint32_t)z->nqw,
-                          (uint32_t)(cp / 8)};
-  for (int k = 0; k < 4; ++k) division_magic(dv[k], &z->dv_mul[k], &z->dv_shift[k]);
+  const uint32_t dv[6] = {(uint32_t)(d.w + 2), (uint32_t)(d.h + 2), (uint32_t)z->nqw,
+                          (uint32_t)(cp / 8), (uint32_t)d.c_in, (uint32_t)std::max(1, d.w / 8)};
+  for (int k = 0; k < 6; ++k) division_magic(dv[k], &z->dv_mul[k], &z->dv_shift[k]);
   // per (image, output channel) and row phase: 32 column phases x the
   // padded columns x K = 4 taps x cp
   *issued = (int64_t)d.n * d.c_out * cols * 32 * 4 * cp;

@@ -1719,8 +1719,10 @@ __global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int q = q0 + u * NT;
-        const int c = q % a.cin, rest = q / a.cin;
-        const int piece = rest % wv, i = rest / wv;
+        const int rest = (int)fast_div((uint32_t)q, a.dv_mul[4], a.dv_shift[4]);
+        const int c = q - rest * a.cin;
+        const int i = (int)fast_div((uint32_t)rest, a.dv_mul[5], a.dv_shift[5]);
+        const int piece = rest - i * wv;
         v[u] = q < nv ? *(const uint4*)(xin + ((size_t)c * a.h + i) * a.w + 8 * piece)
                       : make_uint4(0, 0, 0, 0);
         dst[u] = ((i + 1) * wp2 + 8 * piece + 1) * a.cp + c;
@@ -1777,51 +1779,77 @@ __global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
   uint16_t* yk = (uint16_t*)a.y + ((size_t)img * a.cout + k) * a.ho * a.wo;
   // this wave's output rows, kCpRows at a time, assembled in LDS and then
   // written whole (16 bytes per lane, consecutive lanes consecutive pieces)
-  uint16_t* s_o = s_x + (size_t)(a.h + 2) * wp2 * a.cp + (size_t)wave * kCpRows * a.wo;
+  // Row qi of the buffer holds 16-byte piece p of the output row at piece
+  // p ^ ((p >> 4) & 3) (rows padded to whole groups of four pieces): the
+  // lanes of one LDS write hold neighbouring 64-byte column blocks, which
+  // unswizzled fall on four bank groups (8-way conflicts), swizzled on 16.
+  const int wo_lds = (a.wo + 31) & ~31;
+  uint16_t* s_o = s_x + (size_t)(a.h + 2) * wp2 * a.cp + (size_t)wave * kCpRows * wo_lds;
+  auto swz = [](int piece) { return piece ^ ((piece >> 4) & 3); };
   const int vpr = a.wo / 8;  // 16-byte pieces per output row
   for (int q0 = 0; q0 < nq; q0 += kCpRows) {
     const int nr = min(kCpRows, nq - q0);
     const int ncol = nr * a.nqw;
-    for (int c0 = 0; c0 < ncol; c0 += 32) {
-      const int col = min(c0 + col32, ncol - 1);
-      const int qi = (int)fast_div((uint32_t)col, a.dv_mul[2], a.dv_shift[2]);
-      const int Q = q_lo + q0 + qi, Qw = a.qw_lo + col - qi * a.nqw;
-      f32x16 acc;
+    // column tiles two at a time (independent accumulators: their MFMA
+    // chains and LDS reads interleave), then the odd one
+    auto tiles = [&](int c0, auto two_c) {
+      constexpr int NTL = decltype(two_c)::value ? 2 : 1;
+      int qi[NTL], Qw[NTL], base[NTL];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+      for (int u = 0; u < NTL; ++u) {
+        const int col = min(c0 + 32 * u + col32, ncol - 1);
+        qi[u] = (int)fast_div((uint32_t)col, a.dv_mul[2], a.dv_shift[2]);
+        Qw[u] = a.qw_lo + col - qi[u] * a.nqw;
+        base[u] = ((q_lo + q0 + qi[u] + 1) * wp2 + Qw[u] + 1) * a.cp;
+      }
+      f32x16 acc[NTL];  // the bias is the sums' starting value
+#pragma unroll
+      for (int u = 0; u < NTL; ++u)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[u][r] = bk;
 #pragma unroll
       for (int kb = 0; kb < kblk; ++kb) {
         const int run = 2 * kb + half;
         const int t = (int)fast_div((uint32_t)run, a.dv_mul[3], a.dv_shift[3]);
-        const int cc = (run - t * rpt) * 8;
-        const int pi = Q - (t >> 1) + 1, pj = Qw - (t & 1) + 1;
-        const uint4 xv = *(const uint4*)(s_x + (pi * wp2 + pj) * a.cp + cc);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, wa[kb]),
-                                                      __builtin_bit_cast(bf16x8, xv), acc, 0, 0, 0);
+        const int off = (-(t >> 1) * wp2 - (t & 1)) * a.cp + (run - t * rpt) * 8;
+        uint4 xv[NTL];
+#pragma unroll
+        for (int u = 0; u < NTL; ++u) xv[u] = *(const uint4*)(s_x + base[u] + off);
+#pragma unroll
+        for (int u = 0; u < NTL; ++u)
+          acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, wa[kb]),
+                                                           __builtin_bit_cast(bf16x8, xv[u]), acc[u],
+                                                           0, 0, 0);
       }
-      // rows 8g + 4*half + (0..3) of this column are four consecutive output
+      // rows 8g + 4*half + (0..3) of a column are four consecutive output
       // elements of row qi: one 8-byte LDS write each
-      if (c0 + col32 < ncol) {
+#pragma unroll
+      for (int u = 0; u < NTL; ++u) {
+        if (c0 + 32 * u + col32 >= ncol) continue;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int ow0 = 32 * Qw + 8 * g + 4 * half - a.pad_w;
+          const int ow0 = 32 * Qw[u] + 8 * g + 4 * half - a.pad_w;
           if (ow0 < 0 || ow0 >= a.wo) continue;
           uint32_t pk[2];
 #pragma unroll
           for (int e = 0; e < 2; ++e) {
-            const uint32_t lo = f32_to_bf16_rne(activate(acc[4 * g + 2 * e] + bk, ACT));
-            const uint32_t hi = f32_to_bf16_rne(activate(acc[4 * g + 2 * e + 1] + bk, ACT));
+            const uint32_t lo = f32_to_bf16_rne(activate(acc[u][4 * g + 2 * e], ACT));
+            const uint32_t hi = f32_to_bf16_rne(activate(acc[u][4 * g + 2 * e + 1], ACT));
             pk[e] = lo | (hi << 16);
           }
-          *(uint2*)(s_o + qi * a.wo + ow0) = make_uint2(pk[0], pk[1]);
+          *(uint2*)(s_o + qi[u] * wo_lds + 8 * swz(ow0 >> 3) + (ow0 & 7)) =
+              make_uint2(pk[0], pk[1]);
         }
       }
-    }
+    };
+    int c0 = 0;
+    for (; c0 + 32 < ncol; c0 += 64) tiles(c0, std::true_type());
+    if (c0 < ncol) tiles(c0, std::false_type());
     // the rows out: piece v of row qi from LDS to the output
     for (int qi = 0; qi < nr; ++qi) {
       const int oh = a.stride_h * (q_lo + q0 + qi) + rho_h - a.pad_h;
       for (int v = lane; v < vpr; v += 64)
-        *(uint4*)(yk + (size_t)oh * a.wo + 8 * v) = *(const uint4*)(s_o + qi * a.wo + 8 * v);
+        *(uint4*)(yk + (size_t)oh * a.wo + 8 * v) = *(const uint4*)(s_o + qi * wo_lds + 8 * swz(v));
     }
   }
 }
@@ -1829,7 +1857,8 @@ __global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
 hipError_t launch_colphase(const CpArgs& a, hipStream_t stream) {
   const int rblocks = (a.stride_h + kCpWaves - 1) / kCpWaves;
   const dim3 grid(a.cout * a.n * rblocks);
-  const size_t lds = ((size_t)(a.h + 2) * (a.w + 2) * a.cp + (size_t)kCpWaves * kCpRows * a.wo) * 2;
+  const size_t lds =
+      ((size_t)(a.h + 2) * (a.w + 2) * a.cp + (size_t)kCpWaves * kCpRows * ((a.wo + 31) & ~31)) * 2;
   const int kblk = a.cp / 4;
 #define HUGE2_CP_LAUNCH(KB, ACT)                                                            \
   if (kblk == KB && a.act == ACT)                                                           \

@@ -283,8 +283,9 @@ struct CpArgs {
   int qw_lo, nqw;  // Q_w range of every row phase
   int act;
   // floor(v / d) = (v * mul) >> shift (division_magic) for d = w + 2, h + 2,
-  // nqw and cp / 8: the kernel's index arithmetic has no integer division
-  uint32_t dv_mul[4], dv_shift[4];
+  // nqw, cp / 8, cin and w / 8: the kernel's index arithmetic has no integer
+  // division
+  uint32_t dv_mul[6], dv_shift[6];
 };
 hipError_t launch_colphase(const CpArgs& a, hipStream_t stream);
 hipError_t launch_pack_colphase(const void* w, void* wp, int cin, int cout, int r, int s,

@@ -1870,6 +1870,12 @@ huge2_status wgrad_execute(const huge2_wgrad_plan* p, const void* x, const void*
     return HUGE2_OK;
   }
   const long long hws = (long long)p->hs * p->ws;
+  // Bt through LDS where the planes fit (HUGE2_WGRAD_GATHER=0: the plain
+  // staging kernel gathers it)
+  if (env_int("HUGE2_WGRAD_GATHER", 1) != 0)
+    a.gather_ib =
+        wgrad_gather_images(p->hs, p->ws, p->hb, p->wb, elem_size(d.dtype), p->chunk, p->nb);
+  division_magic((uint32_t)p->ws, &a.ws_mul, &a.ws_shift);
   // chunks in order: the first writes the fp32 gradient, the rest add to it
   for (int img0 = 0; img0 < d.n; img0 += p->chunk) {
     a.img0 = img0;

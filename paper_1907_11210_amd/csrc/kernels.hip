@@ -2591,7 +2591,8 @@ __global__ __launch_bounds__(256) void wgrad_stage_kernel(WgArgs a) {
   const uint32_t kreal = (uint32_t)a.nimg * hws;
   const uint32_t kv = (uint32_t)a.kp / V;
   const uint32_t st_total = (uint32_t)a.ms * kv;
-  const uint32_t total = st_total + (uint32_t)(a.r * a.s * a.nb) * kv;
+  // (with the LDS gather, Bt is wgrad_gather_kernel's)
+  const uint32_t total = st_total + (a.gather_ib > 0 ? 0u : (uint32_t)(a.r * a.s * a.nb) * kv);
   const bool rows8 = a.ws % V == 0;
   // the 8 k of a piece lie in one image (hws % 8 == 0): contiguous in the
   // small tensor; rows of 1, 2 or 4 pixels (8 % ws == 0) are whole rows of
@@ -2919,12 +2920,101 @@ static dim3 grid_for(long long total) {
   return dim3((unsigned)(want < 65536 ? (want > 0 ? want : 1) : 65536));
 }
 
+// Bt through LDS (hs*ws a multiple of 8, a big-tensor plane within
+// kWgGatherLds): workgroup (n, block of gather_ib images of the chunk) reads
+// the block's planes big[img][n] whole and coalesced, then writes for every
+// tap the block's run of row (tap, n), 8 consecutive k per thread and 16-byte
+// store (the run starts at a multiple of 8: hs*ws is one), the last block
+// also the zero padding up to kp.  The strided gather then reads LDS, where
+// the plain staging kernel's reads of the big tensor were scattered 2-byte
+// loads across planes.
+template <typename T>
+__global__ __launch_bounds__(256) void wgrad_gather_kernel(WgArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char s_raw[];
+  T* const s_pl = (T*)s_raw;
+  const int n = (int)(blockIdx.x % (unsigned)a.nb);
+  const int il0 = (int)(blockIdx.x / (unsigned)a.nb) * a.gather_ib;
+  const int nim = min(a.gather_ib, a.nimg - il0);
+  const int plane = a.hb * a.wb, hws = a.hs * a.ws;
+  const T* bg = (const T*)a.bg;
+  constexpr int VE = 16 / (int)sizeof(T);
+  // the block's planes, all images in one loop (independent loads in flight)
+  const T* src0 = bg + ((size_t)(a.img0 + il0) * a.nb + n) * plane;
+  const size_t img_stride = (size_t)a.nb * plane;
+  if (plane % VE == 0 && ((uintptr_t)bg & 15) == 0) {
+    const int per = plane / VE;
+#pragma unroll 4
+    for (int e = threadIdx.x; e < nim * per; e += 256) {
+      const int il = e / per, r = e - il * per;
+      ((uint4*)s_pl)[e] = ((const uint4*)(src0 + il * img_stride))[r];
+    }
+  } else {
+#pragma unroll 4
+    for (int e = threadIdx.x; e < nim * plane; e += 256) {
+      const int il = e / plane, r = e - il * plane;
+      s_pl[e] = src0[il * img_stride + r];
+    }
+  }
+  __syncthreads();
+  // each thread takes 4-byte runs of k (EPT elements of one image: the run
+  // starts at a multiple of 8), finds their pixels once, then writes them to
+  // every tap's row: consecutive lanes hold consecutive k, so both the LDS
+  // reads (stride-apart pixels of one row) and the row stores coalesce
+  constexpr int EPT = 4 / (int)sizeof(T);
+  const int kbeg = il0 * hws, kreal = a.nimg * hws;
+  const int kend = il0 + nim >= a.nimg ? a.kp : kbeg + nim * hws;
+  const size_t row_stride = (size_t)a.nb * a.kp;
+  T* const bt0 = (T*)a.bt + (size_t)n * a.kp;
+  for (int k0 = kbeg + EPT * (int)threadIdx.x; k0 < kend; k0 += EPT * 256) {
+    int base[EPT], bh[EPT], bw[EPT];
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      const int k = k0 + e;
+      if (k < kreal) {
+        const int il = k / hws, q = k - il * hws;
+        const int qh = (int)(((uint64_t)(uint32_t)q * a.ws_mul) >> a.ws_shift), qw = q - qh * a.ws;
+        bh[e] = qh * a.stride_h - a.pad_h;
+        bw[e] = qw * a.stride_w - a.pad_w;
+        base[e] = (il - il0) * plane;
+      } else {
+        bh[e] = -(1 << 29);  // no tap reaches the zero padding
+        bw[e] = 0;
+        base[e] = 0;
+      }
+    }
+    T* dst = bt0 + k0;
+    for (int kh = 0; kh < a.r; ++kh)
+      for (int kw = 0; kw < a.s; ++kw, dst += row_stride) {
+        T v[EPT];
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+          const int ih = bh[e] + kh * a.dil_h, iw = bw[e] + kw * a.dil_w;
+          const bool in = (unsigned)ih < (unsigned)a.hb && (unsigned)iw < (unsigned)a.wb;
+          v[e] = in ? s_pl[base[e] + ih * a.wb + iw] : T(0);
+        }
+        uint32_t u;
+        __builtin_memcpy(&u, v, 4);
+        *(uint32_t*)dst = u;
+      }
+  }
+}
+
 hipError_t launch_wgrad_stage(const WgArgs& a, int dtype, hipStream_t stream) {
-  const long long total = ((long long)a.ms * a.kp + (long long)a.r * a.s * a.nb * a.kp) / 8;
+  const long long bt = a.gather_ib > 0 ? 0 : (long long)a.r * a.s * a.nb * a.kp;
+  const long long total = ((long long)a.ms * a.kp + bt) / 8;
   if (dtype == 1)
     hipLaunchKernelGGL(wgrad_stage_kernel<uint16_t>, grid_for(total), dim3(256), 0, stream, a);
   else
     hipLaunchKernelGGL(wgrad_stage_kernel<uint32_t>, grid_for(total), dim3(256), 0, stream, a);
+  if (a.gather_ib > 0) {
+    const int blocks = (a.nimg + a.gather_ib - 1) / a.gather_ib;
+    const size_t lds = (size_t)a.gather_ib * a.hb * a.wb * (dtype == 1 ? 2 : 4);
+    const dim3 grid((unsigned)((long long)a.nb * blocks));
+    if (dtype == 1)
+      hipLaunchKernelGGL(wgrad_gather_kernel<uint16_t>, grid, dim3(256), lds, stream, a);
+    else
+      hipLaunchKernelGGL(wgrad_gather_kernel<uint32_t>, grid, dim3(256), lds, stream, a);
+  }
   return hipGetLastError();
 }
 

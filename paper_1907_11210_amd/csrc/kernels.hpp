@@ -392,6 +392,8 @@ struct WgArgs {
   int accumulate;  // 0: G = product, 1: G += product
   int ksplit;      // K ranges per tap, each with its own fp32 slice of G
   int groups;      // > 1: grouped conv (wgrad_grouped_kernel; st, bt and g unused)
+  int gather_ib;   // > 0: Bt through LDS, workgroups of gather_ib images (wgrad_gather_kernel)
+  uint32_t ws_mul, ws_shift;  // floor(v / ws) = (v * ws_mul) >> ws_shift (division_magic)
 };
 // Output tile of the weight-gradient GEMM (square, channels of the small x
 // the large tensor): 128 x 128 when both channel counts reach 128, else 64.
@@ -400,6 +402,18 @@ hipError_t launch_wgrad_stage(const WgArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_wgrad_gemm(const WgArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_wgrad_store(const WgArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_wgrad_grouped(const WgArgs& a, int dtype, hipStream_t stream);
+// Images per workgroup of the LDS gather for a chunk (0: the plain staging
+// kernel gathers Bt): each workgroup holds that many big-tensor planes, as
+// many as fit and still leave about four workgroups per compute unit.
+constexpr int kWgGatherLds = 32 * 1024;
+inline int wgrad_gather_images(int hs, int ws, int hb, int wb, int esz, int nimg, int nb) {
+  const long long plane = (long long)hb * wb * esz;
+  if ((hs * ws) % 8 != 0 || plane > kWgGatherLds) return 0;
+  long long ib = (long long)nimg * nb / 1024;
+  if (ib > kWgGatherLds / plane) ib = kWgGatherLds / plane;
+  if (ib > nimg) ib = nimg;
+  return (int)(ib < 1 ? 1 : ib);
+}
 
 // Re-layout the input into [n][h*w][c_stride] with zero channel padding.
 // nchw: source is NCHW; otherwise NHWC with cin channels per pixel.

@@ -106,6 +106,21 @@ def test_weight_gradient_chunks(case, monkeypatch):
     assert np.array_equal(got, again)
 
 
+@pytest.mark.parametrize("case", [CASES[0], CASES[5], CASES[9], CASES[12]], ids=lambda c: c[0])
+def test_weight_gradient_gather_forms(case, monkeypatch):
+    """The per-tap copies of the large tensor built through LDS (whole planes
+    per workgroup) and by the plain staging kernel (HUGE2_WGRAD_GATHER=0):
+    both match the oracle, and bitwise each other (the same copies)."""
+    P.say("case", case, "LDS gather and plain staging")
+    xq, dyq = _inputs(case, seed=12)
+    ref, absref = _oracle(case, xq, dyq), _oracle(case, xq, dyq, absolute=True)
+    got = _gpu(case, xq, dyq)
+    P.check(got, ref, absref, case[-1], case[0])
+    monkeypatch.setenv("HUGE2_WGRAD_GATHER", "0")
+    plain = _gpu(case, xq, dyq)
+    assert np.array_equal(got, plain)
+
+
 def test_weight_gradient_plan_reuse():
     """One plan, two calls on different data: each matches the oracle."""
     case = CASES[2]

@@ -66,6 +66,8 @@ struct huge2_plan {
   bool quad;      // all-phase form of the stride-2, 4x4, padding-1 layer
   QArgs qargs;
   int bias_div;   // GEMM columns per bias entry (r * s for the 1x1-input product form)
+  int bias_mod;   // > 0: bias entries repeat every bias_mod columns (its NHWC form)
+  int prod_rs;    // > 0: the NHWC product form's weights are packed tap-major
   int ksplit;     // K slices across workgroups (1: none)
   void* part;     // their fp32 partial outputs, ksplit x |y| (or null)
   huge2_plan* inner;  // two-pass all-taps form: the per-tap pointwise GEMM; gather form: the
@@ -896,24 +898,37 @@ huge2_status create_direct(huge2_plan** out, const huge2_conv_desc& d, int trans
   return HUGE2_OK;
 }
 
-// A transposed conv of a 1x1 NCHW input with no padding and unit dilation
-// is the plain product y[n][k*r*s + m*s + q] = sum_c x[n][c] w[c][k][m][q]
-// (section 3.1 with a single input pixel: every tap its own phase and
-// output pixel): one dense GEMM of n rows, on the same memory read as a
-// 1x1 conv to c_out*r*s channels (x [n][c_in], w [c_in][c_out*r*s], y
-// [n][c_out*r*s]).  Writes the descriptor the plan runs to *dd and returns
-// the GEMM columns per bias entry (r * s in the product form, else 1).
-int product_form(const huge2_conv_desc& d, bool transposed, huge2_conv_desc* dd) {
+// A transposed conv of a 1x1 input with no padding and unit dilation is the
+// plain product y[n][k][m][q] = sum_c x[n][c] w[c][k][m][q] (section 3.1
+// with a single input pixel: every tap its own phase and output pixel): one
+// dense GEMM of n rows, run as a 1x1 conv to c_out*r*s channels on the same
+// memory.  NCHW: y is [n][c_out*r*s] with column k*r*s + m*s + q, w read
+// as it lies ([c_in][c_out*r*s]), bias k over r*s consecutive columns.  NHWC:
+// y is [n][r*s*c_out] with column (m*s + q)*c_out + k, the weights packed
+// tap-major, bias k repeating every c_out columns.  Writes the descriptor
+// the plan runs to *dd and the GEMM's bias mapping and packing to the
+// outputs (1, 0, 0 when the form does not apply).
+void product_form(const huge2_conv_desc& d, bool transposed, huge2_conv_desc* dd, int* bias_div,
+                  int* bias_mod, int* prod_rs) {
   *dd = d;
-  if (!transposed || d.h != 1 || d.w != 1 || d.layout != HUGE2_NCHW || d.pad_h != 0 ||
-      d.pad_w != 0 || d.out_pad_h != 0 || d.out_pad_w != 0 || d.dil_h != 1 || d.dil_w != 1 ||
+  *bias_div = 1;
+  *bias_mod = 0;
+  *prod_rs = 0;
+  if (!transposed || d.h != 1 || d.w != 1 || d.pad_h != 0 || d.pad_w != 0 ||
+      d.out_pad_h != 0 || d.out_pad_w != 0 || d.dil_h != 1 || d.dil_w != 1 ||
       (d.r == 1 && d.s == 1) || (long long)d.c_out * d.r * d.s > INT32_MAX / 2)
-    return 1;
+    return;
+  if (d.layout == HUGE2_NHWC && env_int("HUGE2_PRODUCT_NHWC", 1) == 0) return;
   dd->c_out = d.c_out * d.r * d.s;
   dd->r = dd->s = 1;
   dd->stride_h = dd->stride_w = 1;
   dd->layout = HUGE2_NHWC;
-  return d.r * d.s;
+  if (d.layout == HUGE2_NCHW) {
+    *bias_div = d.r * d.s;
+  } else {
+    *bias_mod = d.c_out;
+    *prod_rs = d.r * d.s;
+  }
 }
 
 // The two-pass all-taps form applies to fp32 NCHW transposed convs whose
@@ -1107,7 +1122,8 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   if (desc->groups > 1) return create_grouped(out, *desc, transposed, w, stream, mem);
   // the 1x1-input product form: bias k then covers r*s consecutive columns
   huge2_conv_desc dd;
-  const int bias_div = product_form(*desc, tr, &dd);
+  int bias_div, bias_mod, prod_rs;
+  product_form(*desc, tr, &dd, &bias_div, &bias_mod, &prod_rs);
   const huge2_conv_desc& d = dd;
   {
     huge2_conv_desc d1;
@@ -1149,6 +1165,8 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
   output_dims(d, tr, &p->ho, &p->wo);
   p->cfg = cfg;
   p->bias_div = bias_div;
+  p->bias_mod = bias_mod;
+  p->prod_rs = prod_rs;
   {
     const TileShape& t = kTiles[cfg];
     if (t.kind == 0)
@@ -1434,8 +1452,8 @@ huge2_status create_impl(huge2_plan** out, const huge2_conv_desc* desc, int tran
     ok = hipMemcpyAsync(p->meta, host.data(), meta_b, hipMemcpyHostToDevice, stream) == hipSuccess;
   if (ok)
     ok = launch_pack_weights(w, p->wp, d.dtype, tr, d.c_in, d.c_out, d.r, d.s, p->cin_pad,
-                             p->cout_pad, kTiles[p->cfg].kind != 0 ? kPackKB : 0,
-                             stream) == hipSuccess;
+                             p->cout_pad, kTiles[p->cfg].kind != 0 ? kPackKB : 0, stream,
+                             p->prod_rs) == hipSuccess;
   // the host copy of the metadata must outlive the transfer
   if (ok) ok = hipStreamSynchronize(stream) == hipSuccess;
   if (ok) {
@@ -1602,6 +1620,7 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
   a.bias[0] = bias;
   a.y[0] = y;
   a.bias_div = p->bias_div;
+  a.bias_mod = p->bias_mod;
   a.act = d.activation;
   a.ksplit = p->ksplit;
   a.part = (float*)p->part;
@@ -1644,6 +1663,7 @@ huge2_status gemm_impl(const huge2_plan* p, const void* x, const float* bias, vo
     r.hw = p->ho * p->wo;
     r.nchw = d.layout == HUGE2_NCHW ? 1 : 0;
     r.bias_div = p->bias_div;
+    r.bias_mod = p->bias_mod;
     r.act = d.activation;
     if (launch_splitk_reduce(r, d.dtype, stream) != hipSuccess) {
       (void)hipGetLastError();
@@ -1922,7 +1942,8 @@ bool groupable(const huge2_plan* p, const huge2_plan* q) {
          a.layout == b.layout && a.dtype == b.dtype && a.activation == b.activation &&
          p->ho == q->ho && p->wo == q->wo && p->cfg == q->cfg && p->cin_pad == q->cin_pad &&
          p->cout_pad == q->cout_pad && p->c_stride == q->c_stride && p->x_bytes == q->x_bytes &&
-         p->wp_bytes == q->wp_bytes && p->bias_div == q->bias_div && a.r == b.r && a.s == b.s;
+         p->wp_bytes == q->wp_bytes && p->bias_div == q->bias_div &&
+         p->bias_mod == q->bias_mod && a.r == b.r && a.s == b.s;
 }
 
 // Image of the first pixel of a work (the segment's pixels are image-major).
@@ -2050,6 +2071,7 @@ huge2_status group_execute(const huge2_group* g, const void* x, const float* con
     a.y[i] = y[i];
   }
   a.bias_div = p->bias_div;
+  a.bias_mod = p->bias_mod;
   a.act = d.activation;
   a.ksplit = 1;
   a.segs = g->d_segs;
@@ -2243,7 +2265,8 @@ huge2_status huge2_plan_macs(const huge2_conv_desc* desc, int32_t transposed, in
     QArgs q;
     // the same form choices, in the same order, as plan creation
     huge2_conv_desc dd;
-    product_form(*desc, transposed != 0, &dd);
+    int bias_div, bias_mod, prod_rs;
+    product_form(*desc, transposed != 0, &dd, &bias_div, &bias_mod, &prod_rs);
     huge2_conv_desc d1;
     if (two_pass_shape(dd, transposed != 0, &d1) || gather_shape(dd, transposed != 0, &d1)) {
       int64_t nz1 = 0;

@@ -68,6 +68,12 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
 struct PixelPos {
   int img, oh, ow, ih, iw;
 };
+// Bias entry of GEMM column ch (the 1x1-input product forms: bias_div
+// columns per entry, or entries repeating every bias_mod columns).
+__device__ __forceinline__ int bias_index(const GemmArgs& a, int ch) {
+  const int bc = ch / a.bias_div;
+  return a.bias_mod > 0 ? bc % a.bias_mod : bc;
+}
 __device__ __forceinline__ uint32_t fast_div(uint32_t v, uint32_t mul, uint32_t shift) {
   return (uint32_t)(((uint64_t)v * mul) >> shift);
 }
@@ -323,7 +329,7 @@ __global__ __launch_bounds__(PWAVES * CWAVES * 64) void phase_gemm_kernel(GemmAr
   __shared__ float s_bias[BN];
   const float* const bias = a.bias[sg.plan];
   for (int t = tid; t < BN; t += NT)
-    s_bias[t] = (bias && wk.n0 + t < a.cout) ? bias[(wk.n0 + t) / a.bias_div] : 0.f;
+    s_bias[t] = (bias && wk.n0 + t < a.cout) ? bias[bias_index(a, wk.n0 + t)] : 0.f;
 
   // The segment's taps in LDS: byte delta of the tapped pixel and byte
   // offset of the tap's weight block.
@@ -647,7 +653,7 @@ __global__ __launch_bounds__(W * 64 * KS) void phase_gemm2_kernel(GemmArgs a) {
   __shared__ float s_bias[BN];
   const float* const bias = a.bias[sg.plan];
   for (int t = threadIdx.x; t < BN; t += NTA)
-    s_bias[t] = (bias && wk.n0 + t < a.cout) ? bias[(wk.n0 + t) / a.bias_div] : 0.f;
+    s_bias[t] = (bias && wk.n0 + t < a.cout) ? bias[bias_index(a, wk.n0 + t)] : 0.f;
   __shared__ int4 s_taps[kMaxLdsTaps];
   const bool lds_taps = !sg.tap_ap && ntaps <= kMaxLdsTaps;
   if (lds_taps) {
@@ -958,7 +964,7 @@ __global__ __launch_bounds__(W * 64 * KS, 2) void phase_gemm3_kernel(GemmArgs a)
 
   const float* const bias = a.bias[sg.plan];
   for (int t = threadIdx.x; t < BN; t += NTA)
-    s_bias[t] = (bias && wk.n0 + t < a.cout) ? bias[(wk.n0 + t) / a.bias_div] : 0.f;
+    s_bias[t] = (bias && wk.n0 + t < a.cout) ? bias[bias_index(a, wk.n0 + t)] : 0.f;
 
   // Stage counters: tap (th, tw) inner, channel block outer.
   struct Iter {
@@ -2300,7 +2306,10 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(SplitKArgs a) {
     float v = 0.f;
     for (int s = 0; s < a.ksplit; ++s) v += a.part[(size_t)s * a.stride + i];
     const uint32_t ch = a.nchw ? (i / (uint32_t)a.hw) % (uint32_t)a.cout : i % (uint32_t)a.cout;
-    if (a.bias) v += a.bias[ch / (uint32_t)a.bias_div];
+    if (a.bias) {
+      const uint32_t bc = ch / (uint32_t)a.bias_div;
+      v += a.bias[a.bias_mod > 0 ? bc % (uint32_t)a.bias_mod : bc];
+    }
     v = activate(v, a.act);
     if constexpr (BF16)
       ((uint16_t*)a.y)[i] = f32_to_bf16_rne(v);
@@ -2524,7 +2533,7 @@ hipError_t launch_quad(const QArgs& a, hipStream_t stream) {
 template <typename T>
 __global__ void pack_weights_kernel(const T* __restrict__ w, T* __restrict__ wp, bool transposed,
                                     int cin, int cout, int r, int s, int cin_pad, int cout_pad,
-                                    int lane_kb, long long total) {
+                                    int lane_kb, long long total, int prod_rs) {
   for (long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
        idx += (long long)gridDim.x * blockDim.x) {
     const int c = (int)(idx % cin_pad);
@@ -2534,8 +2543,14 @@ __global__ void pack_weights_kernel(const T* __restrict__ w, T* __restrict__ wp,
     const int kh = slot / s, kw = slot - kh * s;
     T v = T(0);
     if (c < cin && k < cout) {
-      const long long src = transposed ? (((long long)c * cout + k) * r + kh) * s + kw
-                                       : (((long long)k * cin + c) * r + kh) * s + kw;
+      long long src;
+      if (prod_rs > 0) {  // column k = tap * (cout / prod_rs) + channel
+        const int co = cout / prod_rs, tap = k / co;
+        src = ((long long)c * co + (k - tap * co)) * prod_rs + tap;
+      } else {
+        src = transposed ? (((long long)c * cout + k) * r + kh) * s + kw
+                         : (((long long)k * cin + c) * r + kh) * s + kw;
+      }
       v = w[src];
     }
     long long dst = idx;
@@ -2554,7 +2569,7 @@ __global__ void pack_weights_kernel(const T* __restrict__ w, T* __restrict__ wp,
 
 hipError_t launch_pack_weights(const void* w, void* wp, int dtype, bool transposed, int cin,
                                int cout, int r, int s, int cin_pad, int cout_pad, int lane_kb,
-                               hipStream_t stream) {
+                               hipStream_t stream, int prod_rs) {
   const long long total = (long long)r * s * cout_pad * cin_pad;
   const int block = 256;
   const long long want = (total + block - 1) / block;
@@ -2563,11 +2578,11 @@ hipError_t launch_pack_weights(const void* w, void* wp, int dtype, bool transpos
   if (dtype == 1)
     hipLaunchKernelGGL(pack_weights_kernel<uint16_t>, dim3(grid), dim3(block), 0, stream,
                        (const uint16_t*)w, (uint16_t*)wp, transposed, cin, cout, r, s, cin_pad,
-                       cout_pad, lane_kb, total);
+                       cout_pad, lane_kb, total, prod_rs);
   else
     hipLaunchKernelGGL(pack_weights_kernel<uint32_t>, dim3(grid), dim3(block), 0, stream,
                        (const uint32_t*)w, (uint32_t*)wp, transposed, cin, cout, r, s, cin_pad,
-                       cout_pad, lane_kb, total);
+                       cout_pad, lane_kb, total, prod_rs);
   return hipGetLastError();
 }
 

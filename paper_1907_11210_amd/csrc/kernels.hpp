@@ -75,7 +75,9 @@ struct GemmArgs {
   // Per plan of a grouped launch (entry 0 alone for a single plan); a
   // segment's `plan` field selects the entry.
   const void* wp[kMaxGroup];     // packed weights: [slot][cout_pad][cin_pad]
-  const float* bias[kMaxGroup];  // [cout / bias_div] or null: channel ch takes bias[ch / bias_div]
+  // [cout / bias_div] or null: column ch takes bias[ch / bias_div], or with
+  // bias_mod > 0 bias[(ch / bias_div) % bias_mod]
+  const float* bias[kMaxGroup];
   void* y[kMaxGroup];            // output, NCHW or NHWC
   const SegDev* segs;
   const TapDev* taps;
@@ -88,7 +90,7 @@ struct GemmArgs {
   int32_t cout, cout_pad;
   int32_t ho, wo;
   int32_t ks;  // kernel width s: weight slot of tap (kh, kw) = kh * ks + kw
-  int32_t bias_div;
+  int32_t bias_div, bias_mod;
   // K split across workgroups: ksplit > 1 writes each slice's fp32 partial
   // tile (no bias, no activation) to part + slice * part_stride, in the
   // output's layout; splitk_reduce then sums the slices in order
@@ -191,9 +193,12 @@ hipError_t launch_phase_gemm(const GemmArgs& a, int dtype, int cfg, bool nchw_ou
 // transposed: w is [cin][cout][r][s]; otherwise [cout][cin][r][s].
 // lane_kb: 0 for the K-contiguous layout; the stage size KB of a kind-1 tile
 // for its lane-ordered layout (see pack_weights_kernel).
+// prod_rs > 0: w is a transposed conv's [cin][cout / prod_rs][prod_rs] (its
+// taps last) packed as a 1x1 conv to cout columns ordered tap-major (column
+// t * (cout / prod_rs) + k): the NHWC form of the 1x1-input product.
 hipError_t launch_pack_weights(const void* w, void* wp, int dtype, bool transposed, int cin,
                                int cout, int r, int s, int cin_pad, int cout_pad, int lane_kb,
-                               hipStream_t stream);
+                               hipStream_t stream, int prod_rs = 0);
 
 // All-taps form of a transposed conv with few output channels (NCHW, bf16,
 // c_out * r * s <= 64): workgroup (image, block of `ob` output rows) holds
@@ -348,7 +353,7 @@ struct SplitKArgs {
   const float* bias;
   void* y;
   uint32_t stride, total;
-  int ksplit, cout, hw, nchw, bias_div, act;
+  int ksplit, cout, hw, nchw, bias_div, bias_mod, act;
 };
 hipError_t launch_splitk_reduce(const SplitKArgs& a, int dtype, hipStream_t stream);
 

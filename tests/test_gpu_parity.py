@@ -513,6 +513,7 @@ SPLITK_LAYERS = [l for l in SMALL if l.name in ("ct_vecstage_bf16", "ct_ragged_b
     L("sk_ct_nhwc_f32", True, 1, 150, 5, 6, 24, 3, 3, 2, 1, 1, 1, "NHWC", "f32"),
     L("sk_dgrad_nchw", False, 2, 256, 8, 8, 64, 4, 4, 2, 1, 0, 1, "NCHW", "bf16"),
     L("sk_proj_nchw", True, 2, 300, 1, 1, 16, 4, 4, 1, 0, 0, 1, "NCHW", "bf16"),
+    L("sk_proj_nhwc", True, 2, 300, 1, 1, 24, 3, 4, 1, 0, 0, 1, "NHWC", "bf16"),
 ]
 
 
@@ -532,6 +533,34 @@ def test_split_k(layer, ksplit, monkeypatch):
     y1 = P.run_gpu(layer, xq, wq, bias)
     P.check(y1, ref, absref, layer.dtype, layer.name)
     assert np.array_equal(y1, P.run_gpu(layer, xq, wq, bias))
+
+
+PRODUCT_NHWC_LAYERS = [
+    # the generator's projection of z in NHWC: ragged row tile and channels
+    L("pn_proj_rag", True, 45, 100, 1, 1, 50, 4, 4, 1, 0, 0, 1, "NHWC", "bf16"),
+    # fp32, a 3 x 5 kernel, a stride (irrelevant for one input pixel)
+    L("pn_f32_3x5", True, 2, 16, 1, 1, 8, 3, 5, 2, 0, 0, 1, "NHWC", "f32"),
+    # many columns (the generator's 1024 channels x 16 taps) at batch 1
+    L("pn_wide_b1", True, 1, 100, 1, 1, 1024, 4, 4, 1, 0, 0, 1, "NHWC", "bf16"),
+]
+
+
+@pytest.mark.parametrize("product", [1, 0])
+@pytest.mark.parametrize("layer", PRODUCT_NHWC_LAYERS, ids=lambda l: l.name)
+def test_product_form_nhwc(layer, product, monkeypatch):
+    """A 1x1 NHWC input as one dense GEMM whose columns are the output's own
+    order (tap-major weight packing, bias repeating every C_out columns),
+    and with the form switched off the phase GEMM: both match the oracle,
+    with bias and ReLU, and write every output element."""
+    monkeypatch.setenv("HUGE2_PRODUCT_NHWC", str(product))
+    layer = layer.with_(act="relu")
+    P.say("case", layer, "HUGE2_PRODUCT_NHWC", product)
+    xq, wq = _inputs(layer, seed=23)
+    bias = torch.linspace(-0.5, 0.5, layer.c_out)
+    ref = P.oracle_full(layer, xq, wq, bias)
+    absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
+    y = P.run_gpu(layer, xq, wq, bias, prefill_nan=True)
+    P.check(y, ref, absref, layer.dtype, layer.name)
 
 
 TWO_PASS_LAYERS = [l for l in SMALL if l.name in ("ct_fewout_f32_op", "ct_fewout_wide")] + [

@@ -340,10 +340,11 @@ int64_t makespan_listed(const huge2_conv_desc& d, const ListedShape& ls, int cfg
 int floor_div_i(int a, int b) { return a >= 0 ? a / b : -((-a + b - 1) / b); }
 int ceil_div_i(int a, int b) { return -floor_div_i(-a, b); }
 
-// The all-taps form (ztile_kernel) applies to NCHW bf16 transposed convs
-// whose taps x output channels fit one 64-column MFMA tile, with an even input
-// width, strides up to 4, at most 4 taps of an axis reaching one output phase
-// and output rows of at most 256 columns.
+// The all-taps form (ztile_kernel) applies to bf16 transposed convs whose
+// taps x output channels fit one 64-column MFMA tile, NCHW with an even input
+// width or NHWC with a multiple of 8 input channels, strides up to 4, at
+// most 4 taps of an axis reaching one output phase and output rows of at most
+// 256 columns.
 // The block of output rows per workgroup is the largest multiple of the
 // stride whose input tile fits the LDS budget while the grid still has two
 // workgroups per CU (else one); small problems take the largest block that
@@ -351,10 +352,13 @@ int ceil_div_i(int a, int b) { return -floor_div_i(-a, b); }
 // Returns false when the form does not apply (or HUGE2_ZTILE=0, or a GEMM
 // tile is forced through HUGE2_TILE).
 bool ztile_shape(const huge2_conv_desc& d, bool transposed, ZArgs* z, int64_t* issued) {
-  // bf16 only: in fp32 the phase GEMM measured faster
-  if (!transposed || d.layout != HUGE2_NCHW || d.dtype != HUGE2_BF16) return false;
+  // bf16 only: in fp32 the phase GEMM measured faster.  NHWC reads each
+  // pixel's channels as 16-byte groups (c_in a multiple of 8)
+  if (!transposed || d.dtype != HUGE2_BF16) return false;
+  const bool nhwc = d.layout == HUGE2_NHWC;
+  if (nhwc ? d.c_in % 8 != 0 : d.w % 2 != 0) return false;
   if (env_int("HUGE2_ZTILE", 1) == 0 || env_int("HUGE2_TILE", -1) >= 0) return false;
-  if ((long long)d.c_out * d.r * d.s > 64 || d.w % 2 != 0) return false;
+  if ((long long)d.c_out * d.r * d.s > 64) return false;
   if (d.stride_h > kZtileMaxStride || d.stride_w > kZtileMaxStride || d.r > kZtileMaxTaps ||
       d.s > kZtileMaxTaps || d.dil_h > 16 || d.dil_w > 16)
     return false;
@@ -411,6 +415,7 @@ bool ztile_shape(const huge2_conv_desc& d, bool transposed, ZArgs* z, int64_t* i
   z->tcw = tcw;
   z->j_lo = j_lo;
   z->cchunk = 64;
+  z->nhwc = nhwc ? 1 : 0;
   // per-phase tap tables: output o with o + pad = stride*Q + rho reads input
   // Q + delta through kernel tap k when rho - k*dil = stride*delta
   const int strides[2] = {d.stride_h, d.stride_w}, ks[2] = {d.r, d.s}, dils[2] = {d.dil_h, d.dil_w};

@@ -1249,11 +1249,14 @@ hipError_t launch_phase_gemm(const GemmArgs& a, int dtype, int cfg, bool nchw_ou
 // each pixel's 8 channels with one 16-byte store.
 __device__ __forceinline__ int floor_div_d(int a, int b) { return a >= 0 ? a / b : -((-a + b - 1) / b); }
 
+template <bool NHWC>
 __global__ __launch_bounds__(kZtileThreads) void ztile_kernel(ZArgs a) {
   constexpr int NT = kZtileThreads, NW = NT / 64;
   constexpr int RB = kZtileRowB;
   constexpr int BUF_B = kZtileMaxPixels * RB;
-  constexpr int MAXP = kZtileMaxItems;
+  // input items per thread and pass: NCHW (pixel pair, 8 channels) as 8
+  // dword loads; NHWC (pixel, 8 channels) as one 16-byte load
+  constexpr int MAXP = NHWC ? 2 * kZtileMaxItems : kZtileMaxItems;
   constexpr int MB_MAX = (kZtileMaxPixels / 32 + NW - 1) / NW;  // M blocks per wave
   constexpr uint32_t OOB = 0x80000000u;
   __shared__ __attribute__((aligned(16))) char zsm[kZtileLds];
@@ -1316,30 +1319,56 @@ __global__ __launch_bounds__(kZtileThreads) void ztile_kernel(ZArgs a) {
   // (w is even, so a pair never straddles a row).
   const int ir0 = max(0, i_lo), ir1 = min(a.h, i_lo + a.tr);
   const int npairs = max(0, ir1 - ir0) * a.w / 2;
-  const int itotal = npairs * 8;
+  const int itotal = NHWC ? max(0, ir1 - ir0) * a.w * 8 : npairs * 8;
   uint32_t p_src[MAXP];
-  int p_lds[MAXP];
+  int p_lds[MAXP], p_grp[MAXP];
 #pragma unroll
   for (int j = 0; j < MAXP; ++j) {
     const int it = tid + NT * j;
-    const int g = it / max(npairs, 1), pp = it - g * npairs;
-    const int rr = (2 * pp) / a.w, col = 2 * pp - rr * a.w;
     const bool ok = it < itotal;
-    p_src[j] = ok ? ((((uint32_t)img * (uint32_t)a.cin + 8u * g) * (uint32_t)a.h + (uint32_t)(ir0 + rr)) *
-                         (uint32_t)a.w + (uint32_t)col) * 2u
-                  : OOB;
-    p_lds[j] = ok ? ((ir0 + rr - i_lo) * a.tcw + col - a.j_lo) * RB + 16 * g : -1;
+    if constexpr (NHWC) {
+      // the 8 channel groups of a pixel on neighbouring threads: each
+      // pixel's 128 bytes of a pass are one run
+      const int g = it & 7, px = it >> 3;
+      const int rr = px / a.w, col = px - rr * a.w;
+      p_grp[j] = g;
+      p_src[j] = ok ? ((((uint32_t)img * (uint32_t)a.h + (uint32_t)(ir0 + rr)) * (uint32_t)a.w +
+                        (uint32_t)col) * (uint32_t)a.cin + 8u * g) * 2u
+                    : OOB;
+      p_lds[j] = ok ? ((ir0 + rr - i_lo) * a.tcw + col - a.j_lo) * RB + 16 * g : -1;
+    } else {
+      const int g = it / max(npairs, 1), pp = it - g * npairs;
+      const int rr = (2 * pp) / a.w, col = 2 * pp - rr * a.w;
+      p_grp[j] = g;
+      p_src[j] = ok ? ((((uint32_t)img * (uint32_t)a.cin + 8u * g) * (uint32_t)a.h + (uint32_t)(ir0 + rr)) *
+                           (uint32_t)a.w + (uint32_t)col) * 2u
+                    : OOB;
+      p_lds[j] = ok ? ((ir0 + rr - i_lo) * a.tcw + col - a.j_lo) * RB + 16 * g : -1;
+    }
   }
+  // NCHW: P[j][k] is channel 8g + k of a pixel pair (two bf16); NHWC:
+  // P[j][0..3] are the 8 channels of one pixel (c_in a multiple of 8)
   auto load_items = [&](int c0, uint32_t (&P)[MAXP][8]) {
-    const uint32_t cbo = (uint32_t)c0 * plane_b;
+    const uint32_t cbo = NHWC ? (uint32_t)c0 * 2u : (uint32_t)c0 * plane_b;
 #pragma unroll
     for (int j = 0; j < MAXP; ++j) {
       if (j * NT >= itotal) break;  // the same for the whole workgroup
+      // channels past c_in read zeros (out-of-range offset)
+      if constexpr (NHWC) {
+        const bool in = c0 + 8 * p_grp[j] < a.cin;
+        const uint4 v = __builtin_bit_cast(
+            uint4, __builtin_amdgcn_raw_buffer_load_b128(xr, in ? p_src[j] : OOB, cbo, 0));
+        P[j][0] = v.x;
+        P[j][1] = v.y;
+        P[j][2] = v.z;
+        P[j][3] = v.w;
+      } else {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        // channels past c_in read zeros (out-of-range offset)
-        const bool in = c0 + 8 * ((tid + NT * j) / max(npairs, 1)) + k < a.cin;
-        P[j][k] = __builtin_amdgcn_raw_buffer_load_b32(xr, in ? p_src[j] : OOB, cbo + (uint32_t)k * plane_b, 0);
+        for (int k = 0; k < 8; ++k) {
+          const bool in = c0 + 8 * p_grp[j] + k < a.cin;
+          P[j][k] = __builtin_amdgcn_raw_buffer_load_b32(xr, in ? p_src[j] : OOB,
+                                                         cbo + (uint32_t)k * plane_b, 0);
+        }
       }
     }
   };
@@ -1348,14 +1377,18 @@ __global__ __launch_bounds__(kZtileThreads) void ztile_kernel(ZArgs a) {
     for (int j = 0; j < MAXP; ++j) {
       if (j * NT >= itotal) break;
       if (p_lds[j] < 0) continue;
-      uint32_t lo[4], hi[4];
+      if constexpr (NHWC) {
+        *(uint4*)(buf + p_lds[j]) = make_uint4(P[j][0], P[j][1], P[j][2], P[j][3]);
+      } else {
+        uint32_t lo[4], hi[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        lo[e] = __builtin_amdgcn_perm(P[j][2 * e + 1], P[j][2 * e], 0x05040100u);
-        hi[e] = __builtin_amdgcn_perm(P[j][2 * e + 1], P[j][2 * e], 0x07060302u);
+        for (int e = 0; e < 4; ++e) {
+          lo[e] = __builtin_amdgcn_perm(P[j][2 * e + 1], P[j][2 * e], 0x05040100u);
+          hi[e] = __builtin_amdgcn_perm(P[j][2 * e + 1], P[j][2 * e], 0x07060302u);
+        }
+        *(uint4*)(buf + p_lds[j]) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+        *(uint4*)(buf + p_lds[j] + RB) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
       }
-      *(uint4*)(buf + p_lds[j]) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-      *(uint4*)(buf + p_lds[j] + RB) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
     }
   };
 
@@ -1471,8 +1504,11 @@ __global__ __launch_bounds__(kZtileThreads) void ztile_kernel(ZArgs a) {
           addr[th][tw] = min(max(hpart[th] + wpart[c][tw], 0), zmax - a.cout + 1);
           use[th][tw] = th < nth && tw < ntw[c];
         }
-      size_t off = (((size_t)img * a.cout) * a.ho + oh) * a.wo + ow;
-      for (int k = 0; k < a.cout; ++k, off += (size_t)a.ho * a.wo) {
+      // NCHW: channel k's plane; NHWC: the pixel's c_out consecutive channels
+      size_t off = NHWC ? (((size_t)img * a.ho + oh) * a.wo + ow) * a.cout
+                        : (((size_t)img * a.cout) * a.ho + oh) * a.wo + ow;
+      const size_t kstep = NHWC ? 1 : (size_t)a.ho * a.wo;
+      for (int k = 0; k < a.cout; ++k, off += kstep) {
         float v = s_zb[k];
 #pragma unroll
         for (int th = 0; th < PT; ++th) {
@@ -1493,7 +1529,10 @@ __global__ __launch_bounds__(kZtileThreads) void ztile_kernel(ZArgs a) {
 hipError_t launch_ztile(const ZArgs& a, int dtype, hipStream_t stream) {
   if (dtype != 1) return hipErrorInvalidValue;  // the planner selects this form for bf16 only
   const dim3 grid((a.ho + a.ob - 1) / a.ob, a.n);
-  hipLaunchKernelGGL(ztile_kernel, grid, dim3(kZtileThreads), 0, stream, a);
+  if (a.nhwc)
+    hipLaunchKernelGGL(ztile_kernel<true>, grid, dim3(kZtileThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL(ztile_kernel<false>, grid, dim3(kZtileThreads), 0, stream, a);
   return hipGetLastError();
 }
 

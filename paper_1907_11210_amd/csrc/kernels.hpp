@@ -235,6 +235,7 @@ struct ZArgs {
   int8_t tap_k[2][kZtileMaxStride][kZtileMaxTaps];
   int8_t tap_d[2][kZtileMaxStride][kZtileMaxTaps];
   int act;           // huge2_activation, applied after the bias
+  int nhwc;          // 1: x and y NHWC (c_in a multiple of 8), else NCHW
 };
 hipError_t launch_ztile(const ZArgs& a, int dtype, hipStream_t stream);
 

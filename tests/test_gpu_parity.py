@@ -396,19 +396,36 @@ def test_plan_execute_in_hip_graph():
     plan.close()
 
 
+FEWOUT_NHWC = [
+    # NHWC input and output (16-byte channel groups per pixel)
+    L("ct_fewout_nhwc", True, 2, 40, 6, 8, 3, 4, 4, 2, 1, 0, 1, "NHWC", "bf16"),
+    # stride 3, dilation 2: phases with different tap counts
+    L("ct_fewout_nhwc_s3d2", True, 1, 16, 5, 6, 4, 3, 3, 3, 2, 0, 2, "NHWC", "bf16"),
+    # three 64-channel passes, the last one ragged (136 channels)
+    L("ct_fewout_nhwc_tall", True, 1, 136, 4, 4, 1, 4, 4, 2, 1, 0, 1, "NHWC", "bf16"),
+]
+
+
 @pytest.mark.parametrize("ztile", [0, 1])
 def test_few_output_channel_forms(ztile, monkeypatch):
-    """Few-output-channel NCHW transposed convs through the all-taps form and,
-    with it switched off, through the phase GEMM: both match the oracle."""
+    """Few-output-channel transposed convs (NCHW, and NHWC with 8-channel
+    groups) through the all-taps form and, with it switched off, through the
+    phase GEMM: both match the oracle."""
     monkeypatch.setenv("HUGE2_ZTILE", str(ztile))
-    for layer in [l for l in SMALL if l.name.startswith("ct_fewout")] + [SMALL[12]]:
+    for layer in [l for l in SMALL if l.name.startswith("ct_fewout")] + [SMALL[12]] + FEWOUT_NHWC:
         P.say("case ztile", ztile, layer)
         xq, wq = _inputs(layer, seed=70 + ztile)
         bias = torch.linspace(-0.3, 0.6, layer.c_out)
         ref = P.oracle_full(layer, xq, wq, bias)
         absref = P.oracle_full(layer, xq, wq, bias, absolute=True)
-        y = P.run_gpu(layer, xq, wq, bias)
+        y = P.run_gpu(layer, xq, wq, bias, prefill_nan=True)
         P.check(y, ref, absref, layer.dtype, "%s ztile %d" % (layer.name, ztile))
+        if layer in FEWOUT_NHWC:
+            plan = P.make_plan(layer, wq.contiguous().to(torch.device("cuda", 0)))
+            try:
+                assert plan.kernel.startswith("ztile_kernel") == bool(ztile), plan.kernel
+            finally:
+                plan.close()
 
 
 def test_plan_reports_its_kernel():

@@ -568,8 +568,9 @@ bool colphase_shape(const huge2_conv_desc& d, bool transposed, CpArgs* z, int64_
   return true;
 }
 
-// The all-phase form (quad_kernel) applies to NCHW bf16 transposed convs
-// with stride 2, a 4x4 kernel, padding 1, dilation 1 and no output padding
+// The all-phase form (quad_kernel) applies to bf16 transposed convs, NCHW
+// or NHWC (then with output channels a multiple of 8), with stride 2, a 4x4
+// kernel, padding 1, dilation 1 and no output padding
 // (so every phase has 2x2 taps at input offsets in [-1, 1] and the input's
 // pixel grid), input channels a multiple of 64, and a width of at least 4
 // that tiles P = 64 (or 128) positions per workgroup: whole images of
@@ -581,7 +582,9 @@ bool colphase_shape(const huge2_conv_desc& d, bool transposed, CpArgs* z, int64_
 // multiply-add; they are taken when they still give every compute unit a
 // workgroup of 64 channels (DCGAN L3: 32.5 -> 29.4 us).
 bool quad_shape(const huge2_conv_desc& d, bool transposed, QArgs* q, int64_t* issued) {
-  if (!transposed || d.layout != HUGE2_NCHW || d.dtype != HUGE2_BF16) return false;
+  if (!transposed || d.dtype != HUGE2_BF16) return false;
+  const bool nhwc = d.layout == HUGE2_NHWC;
+  if (nhwc && (d.c_out % 8 != 0 || env_int("HUGE2_QUAD_NHWC", 1) == 0)) return false;
   if (env_int("HUGE2_QUAD", 1) == 0 || env_int("HUGE2_TILE", -1) >= 0) return false;
   if (d.stride_h != 2 || d.stride_w != 2 || d.r != 4 || d.s != 4 || d.pad_h != 1 ||
       d.pad_w != 1 || d.dil_h != 1 || d.dil_w != 1 || d.out_pad_h != 0 || d.out_pad_w != 0)
@@ -648,6 +651,7 @@ bool quad_shape(const huge2_conv_desc& d, bool transposed, QArgs* q, int64_t* is
   if (x_bytes >= (1ll << 31)) return false;
   std::memset(q, 0, sizeof(*q));
   q->x_bytes = (uint32_t)x_bytes;
+  q->nhwc = nhwc ? 1 : 0;
   q->n = d.n;
   q->cin = d.c_in;
   q->h = d.h;

@@ -1984,7 +1984,7 @@ hipError_t launch_rowphase(const RpArgs& a, hipStream_t stream) {
 //    (the scatter of section 3.1) and written with 16-byte stores.
 // With two K groups, group 1 hands its partial sums to group 0 through LDS in
 // a fixed order (deterministic).
-template <int KS, int WCH, int DEPTH, int NP>
+template <int KS, int WCH, int DEPTH, int NP, bool NHWC>
 __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
   constexpr int NT = kQuadThreads;
   constexpr int NTG = NT / KS;  // threads of one K group
@@ -1992,7 +1992,9 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
   constexpr bool SWZ = true;
   constexpr int RB = SWZ ? kQuadRowB : kQuadRowB + 16;
   constexpr int HALO_B = kQuadHaloRows * RB;
-  constexpr int MAXP = kQuadMaxPieces;
+  // input items per thread and K block: NCHW (pixel pair, 8 channels) as 8
+  // dword loads; NHWC (pixel, 8 channels) as one 16-byte load
+  constexpr int MAXP = NHWC ? 2 * kQuadMaxPieces : kQuadMaxPieces;
   constexpr uint32_t OOB = 0x80000000u;
   static_assert(DEPTH == 2 || DEPTH == 4, "weight stages in flight");
   static_assert(KS == 2 || WCH == 1, "one K group: two waves of 32 channels per phase");
@@ -2005,7 +2007,8 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
   // (64 channels x 4 phases x 32*NP positions, rows padded by 16 bytes)
   constexpr int TILE_B = KS * 2 * HALO_B;
   constexpr int RED_B = KS > 1 ? 4 * WCH * NP * 16 * 64 * 4 : 0;
-  constexpr int OUT_B = 64 * (4 * 32 * NP + 8) * 2;
+  // NCHW: [channel][4 * 32 * NP positions + 8]; NHWC: [pixel][64 + 8 channels]
+  constexpr int OUT_B = NHWC ? 4 * 32 * NP * (64 + 8) * 2 : 64 * (4 * 32 * NP + 8) * 2;
   constexpr int SMEM_B = cmax(TILE_B, cmax(RED_B, OUT_B));
   __shared__ __attribute__((aligned(16))) char smem[SMEM_B];
   __shared__ __attribute__((aligned(16))) float s_bias[64];
@@ -2043,7 +2046,7 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
   const int r0 = max(0, qh0 - 1), r1 = min(a.h, qh0 + a.qbh + 1);
   const int rows = r1 - r0;
   const int npairs = a.ni * rows * a.w / 2;
-  const int itotal = npairs * 8;
+  const int itotal = NHWC ? a.ni * rows * a.w * 8 : npairs * 8;
   // LDS tile layout: halo pixel (il, rl, cl) (rl, cl counting the halo row
   // and column) is the RB-byte row p = (il * hrows + rl) * hww + cl, and its
   // eight 16-byte groups of 8 channels sit at slots g ^ sw(pv), where
@@ -2057,27 +2060,44 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
 #pragma unroll
   for (int j = 0; j < MAXP; ++j) {
     const int it = tg + NTG * j;
-    const int g = it / max(npairs, 1), pp = it - g * npairs;
-    const int px = 2 * pp, per_img = rows * a.w;
+    // NHWC: the 8 channel groups of a pixel on neighbouring threads (one
+    // 128-byte run per pixel and K block); NCHW: pixel pairs fastest
+    const int g = NHWC ? (it & 7) : it / max(npairs, 1);
+    const int px = NHWC ? (it >> 3) : 2 * (it - g * npairs), per_img = rows * a.w;
     const int il = px / per_img, rem = px - il * per_img;
     const int pr = rem / a.w, col = rem - pr * a.w;
     const bool ok = it < itotal && img0 + il < a.n;
-    p_src[j] = ok ? ((((uint32_t)(img0 + il) * (uint32_t)a.cin + 8u * g) * (uint32_t)a.h + (uint32_t)(r0 + pr)) *
-                         (uint32_t)a.w + (uint32_t)col) * 2u
-                  : OOB;
+    if constexpr (NHWC)
+      p_src[j] = ok ? ((((uint32_t)(img0 + il) * (uint32_t)a.h + (uint32_t)(r0 + pr)) * (uint32_t)a.w +
+                        (uint32_t)col) * (uint32_t)a.cin + 8u * g) * 2u
+                    : OOB;
+    else
+      p_src[j] = ok ? ((((uint32_t)(img0 + il) * (uint32_t)a.cin + 8u * g) * (uint32_t)a.h + (uint32_t)(r0 + pr)) *
+                           (uint32_t)a.w + (uint32_t)col) * 2u
+                    : OOB;
     const int rl = r0 + pr - qh0 + 1, cl = col + 1;
     const int prow = (il * hrows + rl) * hww + cl, pv = (il * a.qbh + rl - 1) * a.w + cl;
     p_lds[j] = ok ? prow * RB + 16 * (g ^ slot_sw(pv)) : -1;
     p_lds_hi[j] = (prow + 1) * RB + 16 * (g ^ slot_sw(pv + 1));
   }
+  // NCHW: P[j][k] is channel 8g + k of a pixel pair; NHWC: P[j][0..3] the 8
+  // channels of one pixel
   auto load_pieces = [&](int cb, uint32_t (&P)[MAXP][8]) {
-    const uint32_t cbo = (uint32_t)cb * 64u * plane_b;
+    const uint32_t cbo = NHWC ? (uint32_t)cb * 128u : (uint32_t)cb * 64u * plane_b;
 #pragma unroll
     for (int j = 0; j < MAXP; ++j) {
       if (j * NTG >= itotal) break;  // the same for the whole group
+      if constexpr (NHWC) {
+        const uint4 v = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xr, p_src[j], cbo, 0));
+        P[j][0] = v.x;
+        P[j][1] = v.y;
+        P[j][2] = v.z;
+        P[j][3] = v.w;
+      } else {
 #pragma unroll
-      for (int k = 0; k < 8; ++k)
-        P[j][k] = __builtin_amdgcn_raw_buffer_load_b32(xr, p_src[j], cbo + (uint32_t)k * plane_b, 0);
+        for (int k = 0; k < 8; ++k)
+          P[j][k] = __builtin_amdgcn_raw_buffer_load_b32(xr, p_src[j], cbo + (uint32_t)k * plane_b, 0);
+      }
     }
   };
   auto store_pieces = [&](char* tile, const uint32_t (&P)[MAXP][8]) {
@@ -2085,6 +2105,10 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
     for (int j = 0; j < MAXP; ++j) {
       if (j * NTG >= itotal) break;
       if (p_lds[j] < 0) continue;
+      if constexpr (NHWC) {
+        *(uint4*)(tile + p_lds[j]) = make_uint4(P[j][0], P[j][1], P[j][2], P[j][3]);
+        continue;
+      }
       // P[j][k] holds channel 8g + k of the pixel pair: low half the first
       // pixel, high half the second
       uint32_t lo[4], hi[4];
@@ -2281,7 +2305,10 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
   // Interleave the phases in LDS: [channel][image][output row][output column]
   // of the workgroup's output block (2 qbh rows x 2w columns per image).
   const int obw = 2 * a.w, obh = 2 * a.qbh;
-  const int cpo = a.ni * obh * obw + 8;  // elements per channel, 16-byte pad
+  // NCHW: [channel][position], cpo elements per channel (16-byte pad); NHWC:
+  // [position][channel], 64 + 8 elements per position
+  const int cpo = a.ni * obh * obw + 8;
+  constexpr int PPITCH = 64 + 8;
   uint16_t* so = (uint16_t*)smem;
   if (tid < 64) s_bias[tid] = bias_r;
   __syncthreads();
@@ -2316,12 +2343,29 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
         const int ch = (hc * WCH + j) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
 #pragma unroll
         for (int i = 0; i < NP; ++i)
-          so[ch * cpo + pos[i]] = f32_to_bf16_rne(activate(acc[j][i][r] + bv[j][r], a.act));
+          so[NHWC ? pos[i] * PPITCH + ch : ch * cpo + pos[i]] =
+              f32_to_bf16_rne(activate(acc[j][i][r] + bv[j][r], a.act));
       }
   }
   __syncthreads();
   // Whole output rows: per (channel, image) the rows [2 qh0, 2 qh0 + obh)
   // are one contiguous run of obh * obw elements in y.
+  if constexpr (NHWC) {
+    // each output pixel's bn channels are one run of y: 16-byte pieces,
+    // the pieces of a pixel on neighbouring threads
+    const int pieces = bn / 8, npx = a.ni * obh * obw;
+    for (int e = tid; e < npx * pieces; e += NT) {
+      const int pc = e % pieces, px = e / pieces;
+      const int il = px / (obh * obw), rem = px - il * (obh * obw);
+      const int oy = rem / obw, ox = rem - oy * obw;
+      if (n0 + 8 * pc >= a.cout || img0 + il >= a.n) continue;
+      const uint4 v = *(const uint4*)(so + px * PPITCH + 8 * pc);
+      uint16_t* dst = (uint16_t*)a.y +
+                      (((size_t)(img0 + il) * (2 * a.h) + 2 * qh0 + oy) * obw + ox) * a.cout + n0 + 8 * pc;
+      store_stream16(dst, v);
+    }
+    return;
+  }
   const int run8 = obh * obw / 8;
   const int total = bn * a.ni * run8;
   const size_t plane_o = (size_t)(2 * a.h) * (size_t)obw;
@@ -2539,8 +2583,15 @@ hipError_t launch_grouped(const GrArgs& a, int dtype, hipStream_t stream) {
 
 hipError_t launch_quad(const QArgs& a, hipStream_t stream) {
   const dim3 grid(a.ntiles * a.igroups * a.hblocks);
-#define HUGE2_QUAD_LAUNCH(KS_, WCH_, D_, NP_) \
-  hipLaunchKernelGGL((quad_kernel<KS_, WCH_, D_, NP_>), grid, dim3(kQuadThreads), 0, stream, a)
+#define HUGE2_QUAD_LAUNCH(KS_, WCH_, D_, NP_)                                                  \
+  do {                                                                                        \
+    if (a.nhwc)                                                                               \
+      hipLaunchKernelGGL((quad_kernel<KS_, WCH_, D_, NP_, true>), grid, dim3(kQuadThreads), 0, \
+                         stream, a);                                                          \
+    else                                                                                      \
+      hipLaunchKernelGGL((quad_kernel<KS_, WCH_, D_, NP_, false>), grid, dim3(kQuadThreads), 0, \
+                         stream, a);                                                          \
+  } while (0)
   if (a.np == 4) {
     // two weight stages in flight: the registers hold no more
     if (a.ks == 2) HUGE2_QUAD_LAUNCH(2, 1, 2, 4);

@@ -309,10 +309,10 @@ constexpr int kQuadRowB = 128;       // LDS bytes per halo pixel: 64 channels (s
 constexpr int kQuadHaloRows = 200;   // halo pixels per LDS tile: ni * (qbh + 2) * (w + 2)
 constexpr int kQuadMaxPieces = 2;    // input items (pixel pair x 8 channels) per thread and K block
 struct QArgs {
-  const void* x;     // NCHW input
+  const void* x;     // input, NCHW or (nhwc) NHWC
   const void* wp;    // packed weights [slot][cout_pad/32][cin/64][4][64 lanes][16 bytes]
   const float* bias;
-  void* y;           // NCHW output, 2h x 2w
+  void* y;           // output, 2h x 2w, the input's layout
   uint32_t x_bytes, wp_bytes;
   int n, cin, h, w, cout, cout_pad;
   int ni, qbh;       // images and input rows per workgroup (ni * qbh * w = 32 * np)
@@ -327,6 +327,7 @@ struct QArgs {
   // and input offsets: output (2q_h + rho_h, 2q_w + rho_w) reads input q + (dh, dw)
   int8_t slot[4][4], dh[4][4], dw[4][4];
   int act;           // huge2_activation, applied after the bias
+  int nhwc;          // 1: NHWC (c_out a multiple of 8: 16-byte output pieces)
 };
 hipError_t launch_quad(const QArgs& a, hipStream_t stream);
 

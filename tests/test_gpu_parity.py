@@ -463,6 +463,8 @@ def test_large_stride_forms(rowphase, monkeypatch):
 
 
 QUAD = [l for l in SMALL if l.name.startswith("ct_quad")]
+# the same layers in NHWC (16-byte channel groups in, pixel runs of channels out)
+QUAD += [l.with_(name=l.name + "_nhwc", layout="NHWC") for l in QUAD]
 
 
 # (layer, K groups) pairs that tile 128 positions per workgroup
@@ -486,12 +488,12 @@ def test_all_phase_forms(layer, quad, wch, np_, ks, monkeypatch):
           "HUGE2_QUAD_KS", ks)
     xq, wq = _inputs(layer, seed=11)
     bias = torch.linspace(-1.0, 1.0, layer.c_out)
-    y = P.run_gpu(layer, xq, wq, bias)
+    y = P.run_gpu(layer, xq, wq, bias, prefill_nan=True)
     P.check(y, P.oracle_full(layer, xq, wq, bias), P.oracle_full(layer, xq, wq, bias, absolute=True),
             layer.dtype, layer.name)
     plan = P.make_plan(layer, wq.contiguous().to(torch.device("cuda", 0)))
     try:
-        expect = bool(quad) and (np_ != 4 or (layer.name, ks) in QUAD_NP4)
+        expect = bool(quad) and (np_ != 4 or (layer.name.replace("_nhwc", ""), ks) in QUAD_NP4)
         assert ("quad_kernel" in plan.kernel) == expect, plan.kernel
         if expect and np_ == 4:
             dims = plan.kernel.split()[1].split("x")

@@ -1772,6 +1772,8 @@ struct huge2_wgrad_plan {
   int kp;              // padded K of a full chunk
   int ksplit;          // K ranges per tap (workgroups along K)
   int groups;          // > 1: grouped conv (direct per-plane sums, no workspace)
+  int fold;            // taps folded into the GEMM's N (WgArgs::fold)
+  int direct;          // St read in place from the small tensor (WgArgs::direct)
   void* st;
   void* bt;
   float* g;
@@ -1834,11 +1836,25 @@ huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, i
     if (forced > 0 && forced < chunk) chunk = forced;
   }
   const long long kp = (chunk * hws + 63) / 64 * 64;
+  // St read in place where every 64-pixel K run lies in one channel plane
+  // (HUGE2_WGRAD_DIRECT=0: always staged)
+  p->direct = hws % 64 == 0 && env_int("HUGE2_WGRAD_DIRECT", 1) != 0;
+  // the taps folded into N where that issues fewer tile products (a big
+  // tensor with few channels, padded per tap otherwise; HUGE2_WGRAD_FOLD=0:
+  // never)
+  {
+    const long long t0 = wgrad_tile(p->ms, p->nb), nbf = taps * p->nb;
+    const long long t1 = wgrad_tile(p->ms, (int)std::min<long long>(nbf, 1 << 30));
+    const long long issued0 = taps * ((p->ms + t0 - 1) / t0) * ((p->nb + t0 - 1) / t0) * t0 * t0;
+    const long long issued1 = ((p->ms + t1 - 1) / t1) * ((nbf + t1 - 1) / t1) * t1 * t1;
+    p->fold = issued1 < issued0 && nbf < (1ll << 31) && env_int("HUGE2_WGRAD_FOLD", 1) != 0;
+  }
   // split K so that the GEMM has about two workgroups per compute unit
   // (the 128 x 128 tiles run two per compute unit; the 64 x 64 ones four),
   // each split keeping at least 8 K stages
-  const long long wt = wgrad_tile(p->ms, p->nb);
-  const long long tiles = taps * ((p->ms + wt - 1) / wt) * ((p->nb + wt - 1) / wt);
+  const long long nb_g = p->fold ? taps * p->nb : p->nb, taps_g = p->fold ? 1 : taps;
+  const long long wt = wgrad_tile(p->ms, (int)nb_g);
+  const long long tiles = taps_g * ((p->ms + wt - 1) / wt) * ((nb_g + wt - 1) / wt);
   const long long stages = kp * esz / 128;
   const long long per_cu = wt == 128 ? 2 : 4;
   long long ksplit = std::max(1ll, (per_cu * kComputeUnits + tiles - 1) / tiles);
@@ -1846,8 +1862,8 @@ huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, i
   // each slice's fp32 gradient is read back by the store: at most 16 MiB of them
   const long long g_slice = taps * p->ms * p->nb * 4;
   ksplit = std::min(ksplit, std::max(1ll, (16ll << 20) / g_slice));
-  ksplit = std::min(ksplit, 64ll);
-  const long long st_b = p->ms * kp * esz, bt_b = taps * p->nb * kp * esz;
+  ksplit = std::min(ksplit, 256ll);
+  const long long st_b = p->direct ? 0 : p->ms * kp * esz, bt_b = taps * p->nb * kp * esz;
   const long long g_b = ksplit * taps * p->ms * p->nb * 4;
   const long long big_b = (long long)d.n * p->nb * p->hb * p->wb * esz;
   const long long small_b = (long long)d.n * p->ms * hws * esz;
@@ -1859,7 +1875,8 @@ huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, i
   p->chunk = (int)chunk;
   p->kp = (int)kp;
   p->ksplit = (int)ksplit;
-  if (fault("alloc") || hipMalloc(&p->st, st_b) != hipSuccess || hipMalloc(&p->bt, bt_b) != hipSuccess ||
+  if (fault("alloc") || (st_b > 0 && hipMalloc(&p->st, st_b) != hipSuccess) ||
+      hipMalloc(&p->bt, bt_b) != hipSuccess ||
       hipMalloc((void**)&p->g, g_b) != hipSuccess) {
     (void)hipGetLastError();
     wgrad_free(p);
@@ -1905,6 +1922,9 @@ huge2_status wgrad_execute(const huge2_wgrad_plan* p, const void* x, const void*
     a.gather_ib =
         wgrad_gather_images(p->hs, p->ws, p->hb, p->wb, elem_size(d.dtype), p->chunk, p->nb);
   division_magic((uint32_t)p->ws, &a.ws_mul, &a.ws_shift);
+  division_magic((uint32_t)hws, &a.hws_mul, &a.hws_shift);
+  a.fold = p->fold;
+  a.direct = p->direct;
   // chunks in order: the first writes the fp32 gradient, the rest add to it
   for (int img0 = 0; img0 < d.n; img0 += p->chunk) {
     a.img0 = img0;

@@ -2695,7 +2695,7 @@ __global__ __launch_bounds__(256) void wgrad_stage_kernel(WgArgs a) {
   const uint32_t hws = (uint32_t)a.hs * (uint32_t)a.ws;
   const uint32_t kreal = (uint32_t)a.nimg * hws;
   const uint32_t kv = (uint32_t)a.kp / V;
-  const uint32_t st_total = (uint32_t)a.ms * kv;
+  const uint32_t st_total = a.direct ? 0u : (uint32_t)a.ms * kv;  // (read in place: no St)
   // (with the LDS gather, Bt is wgrad_gather_kernel's)
   const uint32_t total = st_total + (a.gather_ib > 0 ? 0u : (uint32_t)(a.r * a.s * a.nb) * kv);
   const bool rows8 = a.ws % V == 0;
@@ -2774,6 +2774,21 @@ __global__ __launch_bounds__(256) void wgrad_stage_kernel(WgArgs a) {
   }
 }
 
+// Byte offsets of the GEMM's St operand: row m, and K stage ks of KC
+// elements.  Staged, St is [ms][kp]; read in place (a.direct: hs*ws a
+// multiple of 64, so a stage lies in one image) stage ks is image
+// k / (hs*ws) of the chunk at pixel k mod (hs*ws) of channel m's plane.
+__device__ __forceinline__ size_t wgrad_a_row(const WgArgs& a, int m, int esz) {
+  const size_t hws = (size_t)a.hs * a.ws;
+  return a.direct ? ((size_t)a.img0 * a.ms + m) * hws * esz : (size_t)m * a.kp * esz;
+}
+__device__ __forceinline__ size_t wgrad_a_stage(const WgArgs& a, int ks, int kc, int esz) {
+  if (!a.direct) return (size_t)ks * kc * esz;
+  const uint32_t k = (uint32_t)ks * kc, hws = (uint32_t)a.hs * a.ws;
+  const uint32_t il = fast_div(k, a.hws_mul, a.hws_shift);
+  return ((size_t)il * a.ms * hws + (k - il * hws)) * esz;
+}
+
 // G[tap][m][n] (+)= sum_k St[m][k] * Bt[tap][n][k]: a 64 x 64 tile per
 // workgroup of 4 waves (32 x 32 each), K in 128-byte stages through LDS,
 // double buffered, the next stage's loads in registers while this one
@@ -2793,20 +2808,20 @@ __global__ __launch_bounds__(256) void wgrad_gemm_kernel(WgArgs a) {
   const int split = blockIdx.z / taps;
   // this thread's two rows of each operand (rows past the end repeat the last)
   const int chunk = tid & 7, row = tid >> 3;  // 8 chunks of 16 bytes per row
-  const char* const st = (const char*)a.st;
+  const char* const st = (const char*)(a.direct ? a.sm : a.st);
   const char* const bt = (const char*)a.bt;
-  const size_t a0 = (size_t)min(m0 + row, a.ms - 1) * a.kp * ESZ + chunk * 16;
-  const size_t a1 = (size_t)min(m0 + row + 32, a.ms - 1) * a.kp * ESZ + chunk * 16;
+  const size_t a0 = wgrad_a_row(a, min(m0 + row, a.ms - 1), ESZ) + chunk * 16;
+  const size_t a1 = wgrad_a_row(a, min(m0 + row + 32, a.ms - 1), ESZ) + chunk * 16;
   const size_t b0 = ((size_t)tap * a.nb + min(n0 + row, a.nb - 1)) * a.kp * ESZ + chunk * 16;
   const size_t b1 = ((size_t)tap * a.nb + min(n0 + row + 32, a.nb - 1)) * a.kp * ESZ + chunk * 16;
   struct Regs {
     uint4 a0, a1, b0, b1;
   };
   auto load = [&](int ks) {
-    const size_t off = (size_t)ks * KB;
+    const size_t off = (size_t)ks * KB, aoff = wgrad_a_stage(a, ks, KC, ESZ);
     Regs r;
-    r.a0 = *(const uint4*)(st + a0 + off);
-    r.a1 = *(const uint4*)(st + a1 + off);
+    r.a0 = *(const uint4*)(st + a0 + aoff);
+    r.a1 = *(const uint4*)(st + a1 + aoff);
     r.b0 = *(const uint4*)(bt + b0 + off);
     r.b1 = *(const uint4*)(bt + b1 + off);
     return r;
@@ -2893,24 +2908,24 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm2_kernel(WgArgs a) {
   const int m0 = blockIdx.x * TM, n0 = blockIdx.y * TN, tap = blockIdx.z % taps;
   const int split = blockIdx.z / taps;
   const int chunk = tid & 7, row = tid >> 3;  // 8 chunks of 16 bytes per row, 32 rows per pass
-  const char* const st = (const char*)a.st;
+  const char* const st = (const char*)(a.direct ? a.sm : a.st);
   const char* const bt = (const char*)a.bt;
   // this thread's rows (rows past the end repeat the last: their products
   // are never stored)
   size_t ao[4], bo[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    ao[j] = (size_t)min(m0 + row + 32 * j, a.ms - 1) * a.kp * ESZ + chunk * 16;
+    ao[j] = wgrad_a_row(a, min(m0 + row + 32 * j, a.ms - 1), ESZ) + chunk * 16;
     bo[j] = ((size_t)tap * a.nb + min(n0 + row + 32 * j, a.nb - 1)) * a.kp * ESZ + chunk * 16;
   }
   struct Regs {
     uint4 a[4], b[4];
   };
   auto load = [&](int ks, Regs& r) {
-    const size_t off = (size_t)ks * KB;
+    const size_t off = (size_t)ks * KB, aoff = wgrad_a_stage(a, ks, KC, ESZ);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      r.a[j] = *(const uint4*)(st + ao[j] + off);
+      r.a[j] = *(const uint4*)(st + ao[j] + aoff);
       r.b[j] = *(const uint4*)(bt + bo[j] + off);
     }
   };
@@ -3004,20 +3019,57 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm2_kernel(WgArgs a) {
 // dw[m][n][tap] from the splits of G[split][tap][m][n] (summed in order),
 // rounded to the dtype: a thread per (tap, m, n), (m, n) fastest so that the
 // reads of G coalesce.
+// Index in dw of entry e of a slice of G (slices hold [taps][ms][nb], or
+// [ms][taps][nb] when the taps are folded into the GEMM's N).
+__device__ __forceinline__ uint32_t wgrad_dw_index(const WgArgs& a, uint32_t e) {
+  const uint32_t taps = (uint32_t)(a.r * a.s), nb = (uint32_t)a.nb;
+  if (a.fold) {
+    const uint32_t m = e / (taps * nb), rest = e - m * taps * nb;
+    const uint32_t tap = rest / nb, n = rest - tap * nb;
+    return (m * nb + n) * taps + tap;
+  }
+  const uint32_t mn_total = (uint32_t)a.ms * nb;
+  const uint32_t tap = e / mn_total, mn = e - tap * mn_total;
+  return mn * taps + tap;
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(256) void wgrad_store_kernel(WgArgs a) {
-  const int taps = a.r * a.s;
-  const uint32_t mn_total = (uint32_t)a.ms * (uint32_t)a.nb;
-  const uint32_t total = mn_total * (uint32_t)taps;
+  const uint32_t total = (uint32_t)a.ms * (uint32_t)a.nb * (uint32_t)(a.r * a.s);
   for (uint32_t e = blockIdx.x * blockDim.x + threadIdx.x; e < total; e += gridDim.x * blockDim.x) {
-    const uint32_t tap = e / mn_total, mn = e - tap * mn_total;
     float v = 0.f;
     for (int sp = 0; sp < a.ksplit; ++sp) v += a.g[(size_t)sp * total + e];
+    const uint32_t d = wgrad_dw_index(a, e);
     if constexpr (BF16)
-      ((uint16_t*)a.dw)[(size_t)mn * taps + tap] = f32_to_bf16_rne(v);
+      ((uint16_t*)a.dw)[d] = f32_to_bf16_rne(v);
     else
-      ((float*)a.dw)[(size_t)mn * taps + tap] = v;
+      ((float*)a.dw)[d] = v;
   }
+}
+
+// The same for many K slices: a workgroup per 64 consecutive entries, wave w
+// adding the slices w, w + 4, w + 8, ... in order (several loads in flight),
+// then the four waves' sums added in wave order.
+template <bool BF16>
+__global__ __launch_bounds__(256) void wgrad_store_split_kernel(WgArgs a) {
+  __shared__ float part[4][64];
+  const uint32_t total = (uint32_t)a.ms * (uint32_t)a.nb * (uint32_t)(a.r * a.s);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t e = blockIdx.x * 64u + (uint32_t)lane;
+  float v = 0.f;
+  if (e < total) {
+#pragma unroll 4
+    for (int sp = wave; sp < a.ksplit; sp += 4) v += a.g[(size_t)sp * total + e];
+  }
+  part[wave][lane] = v;
+  __syncthreads();
+  if (wave != 0 || e >= total) return;
+  const float sum = ((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane];
+  const uint32_t d = wgrad_dw_index(a, e);
+  if constexpr (BF16)
+    ((uint16_t*)a.dw)[d] = f32_to_bf16_rne(sum);
+  else
+    ((float*)a.dw)[d] = sum;
 }
 
 static dim3 grid_for(long long total) {
@@ -3106,10 +3158,10 @@ __global__ __launch_bounds__(256) void wgrad_gather_kernel(WgArgs a) {
 
 hipError_t launch_wgrad_stage(const WgArgs& a, int dtype, hipStream_t stream) {
   const long long bt = a.gather_ib > 0 ? 0 : (long long)a.r * a.s * a.nb * a.kp;
-  const long long total = ((long long)a.ms * a.kp + bt) / 8;
-  if (dtype == 1)
+  const long long total = ((a.direct ? 0 : (long long)a.ms * a.kp) + bt) / 8;
+  if (total > 0 && dtype == 1)
     hipLaunchKernelGGL(wgrad_stage_kernel<uint16_t>, grid_for(total), dim3(256), 0, stream, a);
-  else
+  else if (total > 0)
     hipLaunchKernelGGL(wgrad_stage_kernel<uint32_t>, grid_for(total), dim3(256), 0, stream, a);
   if (a.gather_ib > 0) {
     const int blocks = (a.nimg + a.gather_ib - 1) / a.gather_ib;
@@ -3123,7 +3175,12 @@ hipError_t launch_wgrad_stage(const WgArgs& a, int dtype, hipStream_t stream) {
   return hipGetLastError();
 }
 
-hipError_t launch_wgrad_gemm(const WgArgs& a, int dtype, hipStream_t stream) {
+hipError_t launch_wgrad_gemm(const WgArgs& a0, int dtype, hipStream_t stream) {
+  WgArgs a = a0;
+  if (a.fold) {  // one GEMM of N = taps * nb (Bt's rows (tap, n) in order)
+    a.nb *= a.r * a.s;
+    a.r = a.s = 1;
+  }
   const int t = wgrad_tile(a.ms, a.nb);
   const dim3 grid((a.ms + t - 1) / t, (a.nb + t - 1) / t, a.r * a.s * a.ksplit);
   if (t == 128 && dtype == 1)
@@ -3148,12 +3205,17 @@ __global__ __launch_bounds__(256) void wgrad_store2_kernel(WgArgs a) {
   const uint32_t mn_total = (uint32_t)a.ms * (uint32_t)a.nb;
   const uint32_t total = mn_total * (uint32_t)taps;
   for (uint32_t mn = blockIdx.x * blockDim.x + threadIdx.x; mn < mn_total; mn += gridDim.x * blockDim.x) {
+    // entry of (tap t, pair mn) in a slice of G: [taps][ms][nb], or folded
+    // [ms][taps][nb]
+    const uint32_t m = mn / (uint32_t)a.nb;
+    const size_t g0 = a.fold ? (size_t)mn + (size_t)m * (taps - 1) * a.nb : mn;
+    const size_t gt = a.fold ? (size_t)a.nb : mn_total;
     float v[kWgTapsMax];
 #pragma unroll
     for (int t = 0; t < kWgTapsMax; ++t) {
       v[t] = 0.f;
       if (t < taps)
-        for (int sp = 0; sp < a.ksplit; ++sp) v[t] += a.g[(size_t)sp * total + (size_t)t * mn_total + mn];
+        for (int sp = 0; sp < a.ksplit; ++sp) v[t] += a.g[(size_t)sp * total + g0 + t * gt];
     }
     if constexpr (BF16) {
       uint16_t* d = (uint16_t*)a.dw + (size_t)mn * taps;
@@ -3191,6 +3253,12 @@ hipError_t launch_wgrad_store(const WgArgs& a, int dtype, hipStream_t stream) {
       hipLaunchKernelGGL(wgrad_store2_kernel<true>, grid_for(pairs), dim3(256), 0, stream, a);
     else
       hipLaunchKernelGGL(wgrad_store2_kernel<false>, grid_for(pairs), dim3(256), 0, stream, a);
+  } else if (a.ksplit >= kWgSplitStore) {
+    const dim3 grid((unsigned)((total + 63) / 64));
+    if (dtype == 1)
+      hipLaunchKernelGGL(wgrad_store_split_kernel<true>, grid, dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL(wgrad_store_split_kernel<false>, grid, dim3(256), 0, stream, a);
   } else if (dtype == 1) {
     hipLaunchKernelGGL(wgrad_store_kernel<true>, grid_for(total), dim3(256), 0, stream, a);
   } else {

@@ -390,7 +390,7 @@ struct WgArgs {
   const void* bg;  // big tensor [n][nb][hb][wb]
   void* st;       // [ms][kp]
   void* bt;       // [taps][nb][kp]
-  float* g;       // [ksplit][taps][ms][nb]
+  float* g;       // [ksplit][taps][ms][nb], folded: [ksplit][ms][taps][nb]
   void* dw;       // [ms][nb][r][s]
   int img0, nimg;  // image chunk
   int ms, nb, hs, ws, hb, wb, r, s;
@@ -401,6 +401,14 @@ struct WgArgs {
   int groups;      // > 1: grouped conv (wgrad_grouped_kernel; st, bt and g unused)
   int gather_ib;   // > 0: Bt through LDS, workgroups of gather_ib images (wgrad_gather_kernel)
   uint32_t ws_mul, ws_shift;  // floor(v / ws) = (v * ws_mul) >> ws_shift (division_magic)
+  // the taps folded into the GEMM's N (one GEMM of N = taps * nb: Bt's rows
+  // (tap, n) are already consecutive), so that a small nb is not padded per tap
+  int fold;
+  // the GEMM reads its St operand in place from the small tensor (hs*ws a
+  // multiple of 64: every K stage lies in one image's channel plane) and St
+  // is not staged
+  int direct;
+  uint32_t hws_mul, hws_shift;  // floor(v / (hs*ws)) (division_magic)
 };
 // Output tile of the weight-gradient GEMM (square, channels of the small x
 // the large tensor): 128 x 128 when both channel counts reach 128, else 64.
@@ -408,6 +416,9 @@ inline int wgrad_tile(int ms, int nb) { return ms >= 128 && nb >= 128 ? 128 : 64
 hipError_t launch_wgrad_stage(const WgArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_wgrad_gemm(const WgArgs& a, int dtype, hipStream_t stream);
 hipError_t launch_wgrad_store(const WgArgs& a, int dtype, hipStream_t stream);
+// K slices from which the store adds them with a workgroup per 64 entries
+// (four waves over the slices) rather than a thread per entry
+constexpr int kWgSplitStore = 16;
 hipError_t launch_wgrad_grouped(const WgArgs& a, int dtype, hipStream_t stream);
 // Images per workgroup of the LDS gather for a chunk (0: the plain staging
 // kernel gathers Bt): each workgroup holds that many big-tensor planes, as

@@ -2789,6 +2789,19 @@ __device__ __forceinline__ size_t wgrad_a_stage(const WgArgs& a, int ks, int kc,
   return ((size_t)il * a.ms * hws + (k - il * hws)) * esz;
 }
 
+// Tile of a weight-gradient GEMM workgroup: the grid's (m block, n block,
+// tap + taps * split) in that order of the linear workgroup index, each XCD
+// taking a contiguous run of it (xcd_remap), so that the m blocks that read
+// one Bt tile, and the taps that read one St tile, share an L2.
+__device__ __forceinline__ void wgrad_block(int& bx, int& by, int& bz) {
+  const int nx = gridDim.x, ny = gridDim.y;
+  int b = xcd_remap(blockIdx.x + nx * (blockIdx.y + ny * blockIdx.z), nx * ny * gridDim.z);
+  bx = b % nx;
+  b /= nx;
+  by = b % ny;
+  bz = b / ny;
+}
+
 // G[tap][m][n] (+)= sum_k St[m][k] * Bt[tap][n][k]: a 64 x 64 tile per
 // workgroup of 4 waves (32 x 32 each), K in 128-byte stages through LDS,
 // double buffered, the next stage's loads in registers while this one
@@ -2804,8 +2817,10 @@ __global__ __launch_bounds__(256) void wgrad_gemm_kernel(WgArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave & 1, wn = wave >> 1;
   const int taps = a.r * a.s;
-  const int m0 = blockIdx.x * 64, n0 = blockIdx.y * 64, tap = blockIdx.z % taps;
-  const int split = blockIdx.z / taps;
+  int bx, by, bz;
+  wgrad_block(bx, by, bz);
+  const int m0 = bx * 64, n0 = by * 64, tap = bz % taps;
+  const int split = bz / taps;
   // this thread's two rows of each operand (rows past the end repeat the last)
   const int chunk = tid & 7, row = tid >> 3;  // 8 chunks of 16 bytes per row
   const char* const st = (const char*)(a.direct ? a.sm : a.st);
@@ -2905,8 +2920,10 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm2_kernel(WgArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave & 1, wn = wave >> 1;
   const int taps = a.r * a.s;
-  const int m0 = blockIdx.x * TM, n0 = blockIdx.y * TN, tap = blockIdx.z % taps;
-  const int split = blockIdx.z / taps;
+  int bx, by, bz;
+  wgrad_block(bx, by, bz);
+  const int m0 = bx * TM, n0 = by * TN, tap = bz % taps;
+  const int split = bz / taps;
   const int chunk = tid & 7, row = tid >> 3;  // 8 chunks of 16 bytes per row, 32 rows per pass
   const char* const st = (const char*)(a.direct ? a.sm : a.st);
   const char* const bt = (const char*)a.bt;
@@ -2984,16 +3001,25 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm2_kernel(WgArgs a) {
   const int per = (nk_all + a.ksplit - 1) / a.ksplit;
   const int k_lo = min(split * per, nk_all), k_hi = min(k_lo + per, nk_all);
   if (k_hi > k_lo) {
+    // the split's stages from a start rotated by (tap, split):
+    // the workgroups of one XCD do not stream the same power-of-two strided
+    // rows at the same offsets in lockstep (the m blocks that share a Bt
+    // tile keep the same order)
+    const int nst = k_hi - k_lo, rot = (bz * 5) % nst;
+    auto stage_of = [&](int i) {
+      const int j = i + rot;
+      return k_lo + (j >= nst ? j - nst : j);
+    };
     Regs cur, nx;
-    load(k_lo, cur);
+    load(stage_of(0), cur);
     store(0, cur);
     __syncthreads();
-    for (int ks = k_lo; ks < k_hi; ++ks) {
+    for (int i = 0; i < nst; ++i) {
       // the next stage's loads (the first again past the end: unused)
       // overlap this stage's MFMAs
-      load(ks + 1 < k_hi ? ks + 1 : k_lo, nx);
-      compute((ks - k_lo) & 1);
-      if (ks + 1 < k_hi) store((ks + 1 - k_lo) & 1, nx);
+      load(stage_of(i + 1 < nst ? i + 1 : 0), nx);
+      compute(i & 1);
+      if (i + 1 < nst) store((i + 1) & 1, nx);
       __syncthreads();
     }
   }

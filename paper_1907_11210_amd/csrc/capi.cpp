@@ -1772,7 +1772,7 @@ struct huge2_wgrad_plan {
   int kp;              // padded K of a full chunk
   int ksplit;          // K ranges per tap (workgroups along K)
   int groups;          // > 1: grouped conv (direct per-plane sums, no workspace)
-  int fold;            // taps folded into the GEMM's N (WgArgs::fold)
+  int direct_out;      // the GEMM writes dw (WgArgs::direct_out)
   int direct;          // St read in place from the small tensor (WgArgs::direct)
   void* st;
   void* bt;
@@ -1839,22 +1839,17 @@ huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, i
   // St read in place where every 64-pixel K run lies in one channel plane
   // (HUGE2_WGRAD_DIRECT=0: always staged)
   p->direct = hws % 64 == 0 && env_int("HUGE2_WGRAD_DIRECT", 1) != 0;
-  // the taps folded into N where that issues fewer tile products (a big
-  // tensor with few channels, padded per tap otherwise; HUGE2_WGRAD_FOLD=0:
-  // never)
-  {
-    const long long t0 = wgrad_tile(p->ms, p->nb), nbf = taps * p->nb;
-    const long long t1 = wgrad_tile(p->ms, (int)std::min<long long>(nbf, 1 << 30));
-    const long long issued0 = taps * ((p->ms + t0 - 1) / t0) * ((p->nb + t0 - 1) / t0) * t0 * t0;
-    const long long issued1 = ((p->ms + t1 - 1) / t1) * ((nbf + t1 - 1) / t1) * t1 * t1;
-    p->fold = issued1 < issued0 && nbf < (1ll << 31) && env_int("HUGE2_WGRAD_FOLD", 1) != 0;
+  // one GEMM of all taps: N = nb * taps columns (n, tap), dw's own order
+  const long long nb_g = taps * p->nb;
+  if (nb_g >= (1ll << 30)) {
+    delete p;
+    return HUGE2_ERR_UNSUPPORTED;
   }
   // split K so that the GEMM has about two workgroups per compute unit
   // (the 128 x 128 tiles run two per compute unit; the 64 x 64 ones four),
   // each split keeping at least 8 K stages
-  const long long nb_g = p->fold ? taps * p->nb : p->nb, taps_g = p->fold ? 1 : taps;
   const long long wt = wgrad_tile(p->ms, (int)nb_g);
-  const long long tiles = taps_g * ((p->ms + wt - 1) / wt) * ((nb_g + wt - 1) / wt);
+  const long long tiles = ((p->ms + wt - 1) / wt) * ((nb_g + wt - 1) / wt);
   const long long stages = kp * esz / 128;
   const long long per_cu = wt == 128 ? 2 : 4;
   long long ksplit = std::max(1ll, (per_cu * kComputeUnits + tiles - 1) / tiles);
@@ -1863,12 +1858,16 @@ huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, i
   const long long g_slice = taps * p->ms * p->nb * 4;
   ksplit = std::min(ksplit, std::max(1ll, (16ll << 20) / g_slice));
   ksplit = std::min(ksplit, 256ll);
+  // one K slice over the whole batch: the GEMM writes dw itself, rounded
+  // once, and there is no fp32 gradient (HUGE2_WGRAD_DIRECT_OUT=0: never)
+  p->direct_out = ksplit == 1 && chunk >= d.n && env_int("HUGE2_WGRAD_DIRECT_OUT", 1) != 0;
   const long long st_b = p->direct ? 0 : p->ms * kp * esz, bt_b = taps * p->nb * kp * esz;
-  const long long g_b = ksplit * taps * p->ms * p->nb * 4;
+  const long long g_b = p->direct_out ? 0 : ksplit * taps * p->ms * p->nb * 4;
   const long long big_b = (long long)d.n * p->nb * p->hb * p->wb * esz;
   const long long small_b = (long long)d.n * p->ms * hws * esz;
   if (st_b >= (1ll << 31) || bt_b >= (1ll << 31) || g_b >= (1ll << 31) || big_b >= (1ll << 40) ||
-      small_b >= (1ll << 40) || taps > 65535) {
+      small_b >= (1ll << 40) || taps > 65535 || (p->ms + wt - 1) / wt > 65535 ||
+      (nb_g + wt - 1) / wt > 65535) {
     delete p;
     return HUGE2_ERR_UNSUPPORTED;
   }
@@ -1877,7 +1876,7 @@ huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, i
   p->ksplit = (int)ksplit;
   if (fault("alloc") || (st_b > 0 && hipMalloc(&p->st, st_b) != hipSuccess) ||
       hipMalloc(&p->bt, bt_b) != hipSuccess ||
-      hipMalloc((void**)&p->g, g_b) != hipSuccess) {
+      (g_b > 0 && hipMalloc((void**)&p->g, g_b) != hipSuccess)) {
     (void)hipGetLastError();
     wgrad_free(p);
     delete p;
@@ -1923,7 +1922,7 @@ huge2_status wgrad_execute(const huge2_wgrad_plan* p, const void* x, const void*
         wgrad_gather_images(p->hs, p->ws, p->hb, p->wb, elem_size(d.dtype), p->chunk, p->nb);
   division_magic((uint32_t)p->ws, &a.ws_mul, &a.ws_shift);
   division_magic((uint32_t)hws, &a.hws_mul, &a.hws_shift);
-  a.fold = p->fold;
+  a.direct_out = p->direct_out;
   a.direct = p->direct;
   // chunks in order: the first writes the fp32 gradient, the rest add to it
   for (int img0 = 0; img0 < d.n; img0 += p->chunk) {
@@ -1937,7 +1936,7 @@ huge2_status wgrad_execute(const huge2_wgrad_plan* p, const void* x, const void*
       return HUGE2_ERR_HIP;
     }
   }
-  if (launch_wgrad_store(a, d.dtype, stream) != hipSuccess) {
+  if (!p->direct_out && launch_wgrad_store(a, d.dtype, stream) != hipSuccess) {
     (void)hipGetLastError();
     return HUGE2_ERR_HIP;
   }

@@ -2727,7 +2727,7 @@ __global__ __launch_bounds__(256) void wgrad_stage_kernel(WgArgs a) {
         }
       }
     } else {
-      const int n = (int)(row % (uint32_t)a.nb), tap = (int)(row / (uint32_t)a.nb);
+      const int tap = (int)(row % (uint32_t)(a.r * a.s)), n = (int)(row / (uint32_t)(a.r * a.s));
       const int kh = tap / a.s, kw = tap - kh * a.s;
       if (rows8 && k0 < kreal) {
         const int ih = (int)qh0 * a.stride_h - a.pad_h + kh * a.dil_h;
@@ -2802,7 +2802,10 @@ __device__ __forceinline__ void wgrad_block(int& bx, int& by, int& bz) {
   bz = b / ny;
 }
 
-// G[tap][m][n] (+)= sum_k St[m][k] * Bt[tap][n][k]: a 64 x 64 tile per
+// The GEMM of all taps at once: column c = n * taps + tap of G is Bt's row
+// (n, tap), so that G[m][c] is dw's element (m, n, tap) and a big tensor
+// with few channels is not padded to a tile per tap.
+// G[m][c] (+)= sum_k St[m][k] * Bt[c][k]: a 64 x 64 tile per
 // workgroup of 4 waves (32 x 32 each), K in 128-byte stages through LDS,
 // double buffered, the next stage's loads in registers while this one
 // multiplies.  K order inside a stage is permuted identically for both
@@ -2893,6 +2896,19 @@ __global__ __launch_bounds__(256) void wgrad_gemm_kernel(WgArgs a) {
   // acc: lane holds m = m0 + wm*32 + lane%32 (MFMA column: the St operand went
   // second) and n = n0 + wn*32 + 8*(r/4) + 4*(lane/32) + r%4 (rows)
   const int m = m0 + wm * 32 + (lane & 31);
+  if (a.direct_out) {  // one K slice and one chunk: the gradient itself
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int n = n0 + wn * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      if (m >= a.ms || n >= a.nb) continue;
+      const size_t d = (size_t)m * a.nb + n;
+      if constexpr (BF16)
+        ((uint16_t*)a.dw)[d] = f32_to_bf16_rne(acc[r]);
+      else
+        ((float*)a.dw)[d] = acc[r];
+    }
+    return;
+  }
   float* gt = a.g + (((size_t)split * taps + tap) * a.ms + min(m, a.ms - 1)) * a.nb;
   const bool acc_in = a.accumulate != 0;
 #pragma unroll
@@ -3001,11 +3017,11 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm2_kernel(WgArgs a) {
   const int per = (nk_all + a.ksplit - 1) / a.ksplit;
   const int k_lo = min(split * per, nk_all), k_hi = min(k_lo + per, nk_all);
   if (k_hi > k_lo) {
-    // the split's stages from a start rotated by (tap, split):
+    // the split's stages from a start rotated by (column block, split):
     // the workgroups of one XCD do not stream the same power-of-two strided
     // rows at the same offsets in lockstep (the m blocks that share a Bt
     // tile keep the same order)
-    const int nst = k_hi - k_lo, rot = (bz * 5) % nst;
+    const int nst = k_hi - k_lo, rot = ((bz * (int)gridDim.y + by) * 5) % nst;
     auto stage_of = [&](int i) {
       const int j = i + rot;
       return k_lo + (j >= nst ? j - nst : j);
@@ -3026,6 +3042,25 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm2_kernel(WgArgs a) {
   // lane: n = n0 + wn*64 + 32 j + lane % 32; m = m0 + wm*64 + 32 i + 8 (r/4) + 4 (lane/32) + r%4
   const bool acc_in = a.accumulate != 0;
   const int n = n0 + wn * 64 + (lane & 31);
+  if (a.direct_out) {  // one K slice and one chunk: the gradient itself
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wm * 64 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (m >= a.ms) continue;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          if (n + 32 * j >= a.nb) continue;
+          const size_t d = (size_t)m * a.nb + n + 32 * j;
+          if constexpr (BF16)
+            ((uint16_t*)a.dw)[d] = f32_to_bf16_rne(acc[i][j][r]);
+          else
+            ((float*)a.dw)[d] = acc[i][j][r];
+        }
+      }
+    return;
+  }
   float* const gt = a.g + ((size_t)split * taps + tap) * a.ms * a.nb;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -3042,34 +3077,18 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm2_kernel(WgArgs a) {
     }
 }
 
-// dw[m][n][tap] from the splits of G[split][tap][m][n] (summed in order),
-// rounded to the dtype: a thread per (tap, m, n), (m, n) fastest so that the
-// reads of G coalesce.
-// Index in dw of entry e of a slice of G (slices hold [taps][ms][nb], or
-// [ms][taps][nb] when the taps are folded into the GEMM's N).
-__device__ __forceinline__ uint32_t wgrad_dw_index(const WgArgs& a, uint32_t e) {
-  const uint32_t taps = (uint32_t)(a.r * a.s), nb = (uint32_t)a.nb;
-  if (a.fold) {
-    const uint32_t m = e / (taps * nb), rest = e - m * taps * nb;
-    const uint32_t tap = rest / nb, n = rest - tap * nb;
-    return (m * nb + n) * taps + tap;
-  }
-  const uint32_t mn_total = (uint32_t)a.ms * nb;
-  const uint32_t tap = e / mn_total, mn = e - tap * mn_total;
-  return mn * taps + tap;
-}
-
+// dw from the K slices of G (each in dw's layout), added in slice order and
+// rounded to the dtype: a thread per element, reads and writes coalesced.
 template <bool BF16>
 __global__ __launch_bounds__(256) void wgrad_store_kernel(WgArgs a) {
   const uint32_t total = (uint32_t)a.ms * (uint32_t)a.nb * (uint32_t)(a.r * a.s);
   for (uint32_t e = blockIdx.x * blockDim.x + threadIdx.x; e < total; e += gridDim.x * blockDim.x) {
     float v = 0.f;
     for (int sp = 0; sp < a.ksplit; ++sp) v += a.g[(size_t)sp * total + e];
-    const uint32_t d = wgrad_dw_index(a, e);
     if constexpr (BF16)
-      ((uint16_t*)a.dw)[d] = f32_to_bf16_rne(v);
+      ((uint16_t*)a.dw)[e] = f32_to_bf16_rne(v);
     else
-      ((float*)a.dw)[d] = v;
+      ((float*)a.dw)[e] = v;
   }
 }
 
@@ -3091,11 +3110,10 @@ __global__ __launch_bounds__(256) void wgrad_store_split_kernel(WgArgs a) {
   __syncthreads();
   if (wave != 0 || e >= total) return;
   const float sum = ((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane];
-  const uint32_t d = wgrad_dw_index(a, e);
   if constexpr (BF16)
-    ((uint16_t*)a.dw)[d] = f32_to_bf16_rne(sum);
+    ((uint16_t*)a.dw)[e] = f32_to_bf16_rne(sum);
   else
-    ((float*)a.dw)[d] = sum;
+    ((float*)a.dw)[e] = sum;
 }
 
 static dim3 grid_for(long long total) {
@@ -3106,9 +3124,9 @@ static dim3 grid_for(long long total) {
 // Bt through LDS (hs*ws a multiple of 8, a big-tensor plane within
 // kWgGatherLds): workgroup (n, block of gather_ib images of the chunk) reads
 // the block's planes big[img][n] whole and coalesced, then writes for every
-// tap the block's run of row (tap, n), 8 consecutive k per thread and 16-byte
-// store (the run starts at a multiple of 8: hs*ws is one), the last block
-// also the zero padding up to kp.  The strided gather then reads LDS, where
+// tap the block's run of row (n, tap), runs of 4 bytes of consecutive k per
+// thread (coalesced across the lanes), the last block also the zero padding
+// up to kp.  The strided gather then reads LDS, where
 // the plain staging kernel's reads of the big tensor were scattered 2-byte
 // loads across planes.
 template <typename T>
@@ -3146,8 +3164,8 @@ __global__ __launch_bounds__(256) void wgrad_gather_kernel(WgArgs a) {
   constexpr int EPT = 4 / (int)sizeof(T);
   const int kbeg = il0 * hws, kreal = a.nimg * hws;
   const int kend = il0 + nim >= a.nimg ? a.kp : kbeg + nim * hws;
-  const size_t row_stride = (size_t)a.nb * a.kp;
-  T* const bt0 = (T*)a.bt + (size_t)n * a.kp;
+  const size_t row_stride = (size_t)a.kp;  // rows (n, tap): the taps of n in order
+  T* const bt0 = (T*)a.bt + (size_t)n * (a.r * a.s) * a.kp;
   for (int k0 = kbeg + EPT * (int)threadIdx.x; k0 < kend; k0 += EPT * 256) {
     int base[EPT], bh[EPT], bw[EPT];
 #pragma unroll
@@ -3202,11 +3220,9 @@ hipError_t launch_wgrad_stage(const WgArgs& a, int dtype, hipStream_t stream) {
 }
 
 hipError_t launch_wgrad_gemm(const WgArgs& a0, int dtype, hipStream_t stream) {
-  WgArgs a = a0;
-  if (a.fold) {  // one GEMM of N = taps * nb (Bt's rows (tap, n) in order)
-    a.nb *= a.r * a.s;
-    a.r = a.s = 1;
-  }
+  WgArgs a = a0;  // one GEMM of N = nb * taps (Bt's rows (n, tap) in order)
+  a.nb *= a.r * a.s;
+  a.r = a.s = 1;
   const int t = wgrad_tile(a.ms, a.nb);
   const dim3 grid((a.ms + t - 1) / t, (a.nb + t - 1) / t, a.r * a.s * a.ksplit);
   if (t == 128 && dtype == 1)
@@ -3220,66 +3236,9 @@ hipError_t launch_wgrad_gemm(const WgArgs& a0, int dtype, hipStream_t stream) {
   return hipGetLastError();
 }
 
-// The same for kernels of at most kWgTapsMax taps, a thread per (m, n): it
-// reads every tap's splits (each read coalesced across the threads) and
-// writes the pair's run of taps in dw, which is contiguous, with 16-byte
-// stores where the run allows.
-constexpr int kWgTapsMax = 32;
-template <bool BF16>
-__global__ __launch_bounds__(256) void wgrad_store2_kernel(WgArgs a) {
-  const int taps = a.r * a.s;
-  const uint32_t mn_total = (uint32_t)a.ms * (uint32_t)a.nb;
-  const uint32_t total = mn_total * (uint32_t)taps;
-  for (uint32_t mn = blockIdx.x * blockDim.x + threadIdx.x; mn < mn_total; mn += gridDim.x * blockDim.x) {
-    // entry of (tap t, pair mn) in a slice of G: [taps][ms][nb], or folded
-    // [ms][taps][nb]
-    const uint32_t m = mn / (uint32_t)a.nb;
-    const size_t g0 = a.fold ? (size_t)mn + (size_t)m * (taps - 1) * a.nb : mn;
-    const size_t gt = a.fold ? (size_t)a.nb : mn_total;
-    float v[kWgTapsMax];
-#pragma unroll
-    for (int t = 0; t < kWgTapsMax; ++t) {
-      v[t] = 0.f;
-      if (t < taps)
-        for (int sp = 0; sp < a.ksplit; ++sp) v[t] += a.g[(size_t)sp * total + g0 + t * gt];
-    }
-    if constexpr (BF16) {
-      uint16_t* d = (uint16_t*)a.dw + (size_t)mn * taps;
-      if (taps % 8 == 0 && ((uintptr_t)a.dw & 15) == 0) {
-#pragma unroll
-        for (int t = 0; t < kWgTapsMax; t += 8) {
-          if (t >= taps) break;
-          uint32_t w4[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            w4[e] = (uint32_t)f32_to_bf16_rne(v[t + 2 * e]) |
-                    ((uint32_t)f32_to_bf16_rne(v[t + 2 * e + 1]) << 16);
-          *(uint4*)(d + t) = make_uint4(w4[0], w4[1], w4[2], w4[3]);
-        }
-      } else {
-#pragma unroll
-        for (int t = 0; t < kWgTapsMax; ++t)
-          if (t < taps) d[t] = f32_to_bf16_rne(v[t]);
-      }
-    } else {
-      float* d = (float*)a.dw + (size_t)mn * taps;
-#pragma unroll
-      for (int t = 0; t < kWgTapsMax; ++t)
-        if (t < taps) d[t] = v[t];
-    }
-  }
-}
-
 hipError_t launch_wgrad_store(const WgArgs& a, int dtype, hipStream_t stream) {
   const long long total = (long long)a.ms * a.nb * a.r * a.s;
-  // (one thread per pair serialises taps x splits reads: only for many pairs)
-  if (a.r * a.s <= kWgTapsMax && (long long)a.ms * a.nb >= (1ll << 18)) {
-    const long long pairs = (long long)a.ms * a.nb;
-    if (dtype == 1)
-      hipLaunchKernelGGL(wgrad_store2_kernel<true>, grid_for(pairs), dim3(256), 0, stream, a);
-    else
-      hipLaunchKernelGGL(wgrad_store2_kernel<false>, grid_for(pairs), dim3(256), 0, stream, a);
-  } else if (a.ksplit >= kWgSplitStore) {
+  if (a.ksplit >= kWgSplitStore) {
     const dim3 grid((unsigned)((total + 63) / 64));
     if (dtype == 1)
       hipLaunchKernelGGL(wgrad_store_split_kernel<true>, grid, dim3(256), 0, stream, a);

@@ -389,8 +389,8 @@ struct WgArgs {
   const void* sm;  // small tensor [n][ms][hs][ws] (NCHW)
   const void* bg;  // big tensor [n][nb][hb][wb]
   void* st;       // [ms][kp]
-  void* bt;       // [taps][nb][kp]
-  float* g;       // [ksplit][taps][ms][nb], folded: [ksplit][ms][taps][nb]
+  void* bt;       // [nb][taps][kp]: row (n, tap)
+  float* g;       // [ksplit][ms][nb][taps]: each K slice in dw's own layout
   void* dw;       // [ms][nb][r][s]
   int img0, nimg;  // image chunk
   int ms, nb, hs, ws, hb, wb, r, s;
@@ -401,9 +401,9 @@ struct WgArgs {
   int groups;      // > 1: grouped conv (wgrad_grouped_kernel; st, bt and g unused)
   int gather_ib;   // > 0: Bt through LDS, workgroups of gather_ib images (wgrad_gather_kernel)
   uint32_t ws_mul, ws_shift;  // floor(v / ws) = (v * ws_mul) >> ws_shift (division_magic)
-  // the taps folded into the GEMM's N (one GEMM of N = taps * nb: Bt's rows
-  // (tap, n) are already consecutive), so that a small nb is not padded per tap
-  int fold;
+  // the GEMM writes dw itself, rounded once (one K slice and one image
+  // chunk: no fp32 gradient and no store)
+  int direct_out;
   // the GEMM reads its St operand in place from the small tensor (hs*ws a
   // multiple of 64: every K stage lies in one image's channel plane) and St
   // is not staged

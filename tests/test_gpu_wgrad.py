@@ -123,25 +123,26 @@ def test_weight_gradient_gather_forms(case, monkeypatch):
 
 @pytest.mark.parametrize("case", [CASES[0], CASES[5], CASES[8], CASES[13], CASES[1]],
                          ids=lambda c: c[0])
-def test_weight_gradient_fold_and_direct_forms(case, monkeypatch):
-    """The taps folded into the GEMM's N (a big tensor with few channels) or
-    one GEMM per tap (HUGE2_WGRAD_FOLD=0), and the small tensor read in place
-    (channel planes of a multiple of 64 pixels) or staged first
-    (HUGE2_WGRAD_DIRECT=0): every form matches the oracle, and the in-place
-    and staged reads give the same bits (same products, same order)."""
-    P.say("case", case, "fold / direct forms")
+def test_weight_gradient_in_place_and_direct_out_forms(case, monkeypatch):
+    """The small tensor read in place (channel planes of a multiple of 64
+    pixels) or staged first (HUGE2_WGRAD_DIRECT=0), and, with one K slice,
+    the GEMM writing the gradient itself or through the fp32 slices and the
+    store (HUGE2_WGRAD_DIRECT_OUT=0): every form matches the oracle, and all
+    give the same values (same products, same order, one rounding)."""
+    P.say("case", case, "in-place / direct-out forms")
     xq, dyq = _inputs(case, seed=13)
     ref, absref = _oracle(case, xq, dyq), _oracle(case, xq, dyq, absolute=True)
-    outs = {}
-    for fold in ("1", "0"):
-        for direct in ("1", "0"):
-            monkeypatch.setenv("HUGE2_WGRAD_FOLD", fold)
+    outs = []
+    for direct in ("1", "0"):
+        for direct_out in ("1", "0"):
             monkeypatch.setenv("HUGE2_WGRAD_DIRECT", direct)
+            monkeypatch.setenv("HUGE2_WGRAD_DIRECT_OUT", direct_out)
             got = _gpu(case, xq, dyq)
-            P.check(got, ref, absref, case[-1], "%s fold=%s direct=%s" % (case[0], fold, direct))
-            outs[fold, direct] = got
-    for fold in ("1", "0"):
-        assert np.array_equal(outs[fold, "1"], outs[fold, "0"])
+            P.check(got, ref, absref, case[-1],
+                    "%s direct=%s direct_out=%s" % (case[0], direct, direct_out))
+            outs.append(got)
+    for o in outs[1:]:
+        assert np.array_equal(outs[0], o)
 
 
 def test_weight_gradient_plan_reuse():
@@ -177,9 +178,9 @@ def test_dcgan_layer_weight_gradient_full_size():
 
 def test_dcgan_last_layer_weight_gradient_full_size():
     """The generator's last layer (128 -> 3, 32x32 -> 64x64, batch 64) in
-    full: three big-tensor channels (the taps folded into N), the small
-    tensor read in place, and more than a hundred K slices added by the
-    split store."""
+    full: three big-tensor channels (48 GEMM columns with the taps), the
+    small tensor read in place, and more than a hundred K slices added by
+    the split store."""
     case = ("dcgan_l4_wgrad", True, 64, 128, 32, 32, 3, 4, 4, 2, 1, 0, 1, "bf16")
     P.say("case", case)
     xq, dyq = _inputs(case, seed=14)

@@ -1854,10 +1854,17 @@ huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, i
   const long long per_cu = wt == 128 ? 2 : 4;
   long long ksplit = std::max(1ll, (per_cu * kComputeUnits + tiles - 1) / tiles);
   ksplit = std::max(1ll, std::min(ksplit, stages / 8));
-  // each slice's fp32 gradient is read back by the store: at most 16 MiB of them
+  // each slice's fp32 gradient is read back by the store: at most 32 MiB of
+  // them (DCGAN's 512 -> 256 and 256 -> 128 layers measured fastest at 4 and
+  // 16 slices, two workgroups per compute unit, despite the larger store)
   const long long g_slice = taps * p->ms * p->nb * 4;
-  ksplit = std::min(ksplit, std::max(1ll, (16ll << 20) / g_slice));
+  ksplit = std::min(ksplit, std::max(1ll, (32ll << 20) / g_slice));
   ksplit = std::min(ksplit, 256ll);
+  {
+    // HUGE2_WGRAD_KSPLIT: a given number of K slices (tests and tuning)
+    const int forced = env_int("HUGE2_WGRAD_KSPLIT", 0);
+    if (forced > 0) ksplit = std::min<long long>(forced, std::max(1ll, stages));
+  }
   // one K slice over the whole batch: the GEMM writes dw itself, rounded
   // once, and there is no fp32 gradient (HUGE2_WGRAD_DIRECT_OUT=0: never)
   p->direct_out = ksplit == 1 && chunk >= d.n && env_int("HUGE2_WGRAD_DIRECT_OUT", 1) != 0;

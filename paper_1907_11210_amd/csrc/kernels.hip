@@ -64,6 +64,15 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   return __builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
+// Two floats to bf16 (round to nearest even) in one 32-bit word, lo in the
+// low half: one v_cvt_pk_bf16_f32 with both sources.
+__device__ __forceinline__ uint32_t pack_bf16x2_rne(float lo, float hi) {
+  typedef float f2_t __attribute__((ext_vector_type(2)));
+  typedef __bf16 b2_t __attribute__((ext_vector_type(2)));
+  const f2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, b2_t));
+}
+
 // Decomposition of a segment pixel index into image, output and input coordinates.
 struct PixelPos {
   int img, oh, ow, ih, iw;
@@ -1733,7 +1742,8 @@ __global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
   b /= rblocks;
   const int img = b % a.n, k = b / a.n;
   const int rho_h = rb * kCpWaves + wave;
-  constexpr int kblk = KBLK;  // K blocks of 16: 4 taps x cp channels (cp = 4 * KBLK)
+  constexpr int kblk = KBLK;  // K blocks of 16: 4 taps x CP channels
+  constexpr int CP = 4 * KBLK;  // channel slots per staged pixel (CpArgs::cp)
   const int wp2 = a.w + 2;
 
   // this wave's weight fragments (row rho_w = lane % 32, K run 2*kb + lane/32)
@@ -1748,7 +1758,7 @@ __global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
   // elements go 16 per thread at a time, all loads before the LDS stores,
   // so that their latencies overlap
   const int npix = (a.h + 2) * wp2;
-  const int total = npix * a.cp;
+  const int total = npix * CP;
   const uint16_t* xin = (const uint16_t*)a.x + (size_t)img * a.cin * a.h * a.w;
   constexpr int NT = kCpWaves * 64;
   if ((a.w & 7) == 0 && ((uintptr_t)a.x & 15) == 0) {
@@ -1770,7 +1780,7 @@ __global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
         const int piece = rest - i * wv;
         v[u] = q < nv ? *(const uint4*)(xin + ((size_t)c * a.h + i) * a.w + 8 * piece)
                       : make_uint4(0, 0, 0, 0);
-        dst[u] = ((i + 1) * wp2 + 8 * piece + 1) * a.cp + c;
+        dst[u] = ((i + 1) * wp2 + 8 * piece + 1) * CP + c;
       }
     };
     fetch(tid);  // the first pieces in flight during the zeroing pass
@@ -1784,7 +1794,7 @@ __global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
         uint16_t* d = s_x + dst[u];
         const uint32_t w4[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
 #pragma unroll
-        for (int t = 0; t < 8; ++t) d[t * a.cp] = (uint16_t)(w4[t >> 1] >> (16 * (t & 1)));
+        for (int t = 0; t < 8; ++t) d[t * CP] = (uint16_t)(w4[t >> 1] >> (16 * (t & 1)));
       }
     }
   } else {
@@ -1804,7 +1814,7 @@ __global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
       // branch-free: an element outside the input reads x[0] and keeps 0
       const uint16_t xv = xin[in ? ((size_t)c * a.h + i) * a.w + j : 0];
       v[u] = in ? xv : (uint16_t)0;
-      dst[u] = e < total ? (pi * wp2 + pj) * a.cp + c : -1;
+      dst[u] = e < total ? (pi * wp2 + pj) * CP + c : -1;
     }
 #pragma unroll
     for (int u = 0; u < SU; ++u)
@@ -1820,7 +1830,7 @@ __global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
   const int nq = q_hi - q_lo + 1;
   if (nq <= 0) return;
   const int half = lane >> 5, col32 = lane & 31;
-  const int rpt = a.cp / 8;  // 8-channel runs per tap
+  const int rpt = CP / 8;  // 8-channel runs per tap
   uint16_t* yk = (uint16_t*)a.y + ((size_t)img * a.cout + k) * a.ho * a.wo;
   // this wave's output rows, kCpRows at a time, assembled in LDS and then
   // written whole (16 bytes per lane, consecutive lanes consecutive pieces)
@@ -1829,7 +1839,7 @@ __global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
   // lanes of one LDS write hold neighbouring 64-byte column blocks, which
   // unswizzled fall on four bank groups (8-way conflicts), swizzled on 16.
   const int wo_lds = (a.wo + 31) & ~31;
-  uint16_t* s_o = s_x + (size_t)(a.h + 2) * wp2 * a.cp + (size_t)wave * kCpRows * wo_lds;
+  uint16_t* s_o = s_x + (size_t)(a.h + 2) * wp2 * CP + (size_t)wave * kCpRows * wo_lds;
   auto swz = [](int piece) { return piece ^ ((piece >> 4) & 3); };
   const int vpr = a.wo / 8;  // 16-byte pieces per output row
   for (int q0 = 0; q0 < nq; q0 += kCpRows) {
@@ -1845,7 +1855,7 @@ __global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
         const int col = min(c0 + 32 * u + col32, ncol - 1);
         qi[u] = (int)fast_div((uint32_t)col, a.dv_mul[2], a.dv_shift[2]);
         Qw[u] = a.qw_lo + col - qi[u] * a.nqw;
-        base[u] = ((q_lo + q0 + qi[u] + 1) * wp2 + Qw[u] + 1) * a.cp;
+        base[u] = ((q_lo + q0 + qi[u] + 1) * wp2 + Qw[u] + 1) * CP;
       }
       f32x16 acc[NTL];  // the bias is the sums' starting value
 #pragma unroll
@@ -1856,7 +1866,7 @@ __global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
       for (int kb = 0; kb < kblk; ++kb) {
         const int run = 2 * kb + half;
         const int t = (int)fast_div((uint32_t)run, a.dv_mul[3], a.dv_shift[3]);
-        const int off = (-(t >> 1) * wp2 - (t & 1)) * a.cp + (run - t * rpt) * 8;
+        const int off = (-(t >> 1) * wp2 - (t & 1)) * CP + (run - t * rpt) * 8;
         uint4 xv[NTL];
 #pragma unroll
         for (int u = 0; u < NTL; ++u) xv[u] = *(const uint4*)(s_x + base[u] + off);
@@ -1867,23 +1877,28 @@ __global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
                                                            0, 0, 0);
       }
       // rows 8g + 4*half + (0..3) of a column are four consecutive output
-      // elements of row qi: one 8-byte LDS write each
+      // elements of row qi: one 8-byte LDS write each (all four groups
+      // without checks where the column's 32 outputs lie inside the row)
 #pragma unroll
       for (int u = 0; u < NTL; ++u) {
         if (c0 + 32 * u + col32 >= ncol) continue;
+        const int ow_b = 32 * Qw[u] + 4 * half - a.pad_w;
+        uint16_t* const orow = s_o + qi[u] * wo_lds;
+        auto put = [&](int g) {
+          const int ow0 = ow_b + 8 * g;
+          const uint32_t p0 = pack_bf16x2_rne(activate(acc[u][4 * g], ACT),
+                                              activate(acc[u][4 * g + 1], ACT));
+          const uint32_t p1 = pack_bf16x2_rne(activate(acc[u][4 * g + 2], ACT),
+                                              activate(acc[u][4 * g + 3], ACT));
+          *(uint2*)(orow + 8 * swz(ow0 >> 3) + (ow0 & 7)) = make_uint2(p0, p1);
+        };
+        if (ow_b >= 0 && ow_b + 24 < a.wo) {
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int ow0 = 32 * Qw[u] + 8 * g + 4 * half - a.pad_w;
-          if (ow0 < 0 || ow0 >= a.wo) continue;
-          uint32_t pk[2];
+          for (int g = 0; g < 4; ++g) put(g);
+        } else {
 #pragma unroll
-          for (int e = 0; e < 2; ++e) {
-            const uint32_t lo = f32_to_bf16_rne(activate(acc[u][4 * g + 2 * e], ACT));
-            const uint32_t hi = f32_to_bf16_rne(activate(acc[u][4 * g + 2 * e + 1], ACT));
-            pk[e] = lo | (hi << 16);
-          }
-          *(uint2*)(s_o + qi[u] * wo_lds + 8 * swz(ow0 >> 3) + (ow0 & 7)) =
-              make_uint2(pk[0], pk[1]);
+          for (int g = 0; g < 4; ++g)
+            if (ow_b + 8 * g >= 0 && ow_b + 8 * g < a.wo) put(g);
         }
       }
     };

@@ -1905,11 +1905,12 @@ __global__ __launch_bounds__(kCpWaves * 64) void colphase_kernel(CpArgs a) {
     int c0 = 0;
     for (; c0 + 32 < ncol; c0 += 64) tiles(c0, std::true_type());
     if (c0 < ncol) tiles(c0, std::false_type());
-    // the rows out: piece v of row qi from LDS to the output
+    // the rows out: piece v of row qi from LDS to the output (streaming
+    // stores: the output is written once and not read back here)
     for (int qi = 0; qi < nr; ++qi) {
       const int oh = a.stride_h * (q_lo + q0 + qi) + rho_h - a.pad_h;
       for (int v = lane; v < vpr; v += 64)
-        *(uint4*)(yk + (size_t)oh * a.wo + 8 * v) = *(const uint4*)(s_o + qi * wo_lds + 8 * swz(v));
+        store_stream16(yk + (size_t)oh * a.wo + 8 * v, *(const uint4*)(s_o + qi * wo_lds + 8 * swz(v)));
     }
   }
 }

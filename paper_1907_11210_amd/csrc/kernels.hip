@@ -244,6 +244,7 @@ __device__ __forceinline__ void store_rows_nhwc(const GemmArgs& a, int n0, void*
       }
     }
   __syncthreads();
+  // (streaming stores: the output is not read back by this launch)
   const int piece = tid % PIECES, row0 = tid / PIECES;
   if (n0 + 8 * piece >= a.cout) return;
   uint16_t* const yb = (uint16_t*)y + n0 + 8 * piece;
@@ -252,7 +253,7 @@ __device__ __forceinline__ void store_rows_nhwc(const GemmArgs& a, int n0, void*
     const int row = row0 + RSTEP * k;
     const int off = row_off[row];
     if (off >= 0)
-      *(uint4*)(yb + (size_t)off * a.cout) = *(const uint4*)(lds + row * PITCH + 16 * piece);
+      store_stream16(yb + (size_t)off * a.cout, *(const uint4*)(lds + row * PITCH + 16 * piece));
   }
 }
 

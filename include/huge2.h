@@ -278,9 +278,10 @@ huge2_status huge2_group_destroy(huge2_group* group);
  * How: per kernel tap, the large tensor (dy for the transposed conv, x for
  * the strided conv) is gathered onto the small tensor's pixel grid -- one
  * untangled copy per tap, as the paper's C copies of each derivative map --
- * and every tap's gradient is then one dense MFMA GEMM over pixels with no
- * zero products, accumulated in fp32 over chunks of images in a fixed order
- * and rounded once to the dtype.
+ * and the gradient of all taps is then one dense MFMA GEMM over pixels with
+ * no zero products (its columns are the (channel, tap) pairs, dw's own
+ * order), accumulated in fp32 over K slices and chunks of images in a fixed
+ * order and rounded once to the dtype.
  * Grouped layers (groups > 1; dw is [c_in][c_out/groups][r][s] or
  * [c_out][c_in/groups][r][s]): the sums above run only over channel pairs of
  * one group.  Each weight plane then joins one input map to one error map --
@@ -294,8 +295,9 @@ typedef struct huge2_wgrad_plan huge2_wgrad_plan;
 /* Build a weight-gradient plan for desc (the forward layer's descriptor;
  * transposed selects the layer type).  Allocates the per-plan workspace
  * (none for grouped layers): the staged operands of one chunk of images
- * (the chunk is sized so they stay under 256 MiB; at least one image) and
- * the fp32 gradient.  No HIP
+ * (the chunk is sized so they stay under 256 MiB; at least one image) and,
+ * unless one K slice covers the whole batch, the fp32 gradient slices (at
+ * most 32 MiB).  No HIP
  * work is enqueued.  Errors: INVALID_ARG (NULL out/desc, invalid
  * descriptor), UNSUPPORTED (NHWC; byte extents of 2^31 or more), ALLOC. */
 huge2_status huge2_wgrad_plan_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc,

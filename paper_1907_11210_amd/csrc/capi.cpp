@@ -1773,6 +1773,9 @@ struct huge2_wgrad_plan {
   int ksplit;          // K ranges per tap (workgroups along K)
   int groups;          // > 1: grouped conv (direct per-plane sums, no workspace)
   int direct_out;      // the GEMM writes dw (WgArgs::direct_out)
+  int gather_ib;       // images per LDS-gather workgroup (0: the staging kernel gathers)
+  int bt_phase;        // Bt in phase planes (WgArgs::bt_phase)
+  int hr, sh_min;
   int direct;          // St read in place from the small tensor (WgArgs::direct)
   void* st;
   void* bt;
@@ -1839,6 +1842,23 @@ huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, i
   // St read in place where every 64-pixel K run lies in one channel plane
   // (HUGE2_WGRAD_DIRECT=0: always staged)
   p->direct = hws % 64 == 0 && env_int("HUGE2_WGRAD_DIRECT", 1) != 0;
+  // the large tensor's copies through LDS where its planes fit
+  // (HUGE2_WGRAD_GATHER=0: the plain staging kernel gathers them)
+  p->gather_ib = env_int("HUGE2_WGRAD_GATHER", 1) != 0
+                     ? wgrad_gather_images(p->hs, p->ws, p->hb, p->wb, (int)esz, (int)chunk, p->nb)
+                     : 0;
+  // phase planes instead of per-tap copies where a K stage lies in one image
+  // and the planes (hr rows each) are smaller than the taps' copies
+  // (HUGE2_WGRAD_PHASE=0: per-tap copies)
+  {
+    const int sh_lo = floor_div_i(-d.pad_h, d.stride_h);
+    const int sh_hi = floor_div_i((d.r - 1) * d.dil_h - d.pad_h, d.stride_h);
+    p->sh_min = sh_lo;
+    p->hr = p->hs + sh_hi - sh_lo;
+    p->bt_phase = p->gather_ib > 0 && hws % 64 == 0 && p->ws % 8 == 0 &&
+                  (long long)d.stride_h * p->hr < (long long)d.r * p->hs &&
+                  env_int("HUGE2_WGRAD_PHASE", 1) != 0;
+  }
   // one GEMM of all taps: N = nb * taps columns (n, tap), dw's own order
   const long long nb_g = taps * p->nb;
   if (nb_g >= (1ll << 30)) {
@@ -1868,7 +1888,10 @@ huge2_status wgrad_create(huge2_wgrad_plan** out, const huge2_conv_desc* desc, i
   // one K slice over the whole batch: the GEMM writes dw itself, rounded
   // once, and there is no fp32 gradient (HUGE2_WGRAD_DIRECT_OUT=0: never)
   p->direct_out = ksplit == 1 && chunk >= d.n && env_int("HUGE2_WGRAD_DIRECT_OUT", 1) != 0;
-  const long long st_b = p->direct ? 0 : p->ms * kp * esz, bt_b = taps * p->nb * kp * esz;
+  const long long st_b = p->direct ? 0 : p->ms * kp * esz;
+  const long long bt_b = p->bt_phase
+                             ? (long long)p->nb * d.stride_h * d.s * chunk * p->hr * p->ws * esz
+                             : taps * p->nb * kp * esz;
   const long long g_b = p->direct_out ? 0 : ksplit * taps * p->ms * p->nb * 4;
   const long long big_b = (long long)d.n * p->nb * p->hb * p->wb * esz;
   const long long small_b = (long long)d.n * p->ms * hws * esz;
@@ -1922,13 +1945,13 @@ huge2_status wgrad_execute(const huge2_wgrad_plan* p, const void* x, const void*
     return HUGE2_OK;
   }
   const long long hws = (long long)p->hs * p->ws;
-  // Bt through LDS where the planes fit (HUGE2_WGRAD_GATHER=0: the plain
-  // staging kernel gathers it)
-  if (env_int("HUGE2_WGRAD_GATHER", 1) != 0)
-    a.gather_ib =
-        wgrad_gather_images(p->hs, p->ws, p->hb, p->wb, elem_size(d.dtype), p->chunk, p->nb);
+  a.gather_ib = p->gather_ib;
+  a.bt_phase = p->bt_phase;
+  a.hr = p->hr;
+  a.sh_min = p->sh_min;
   division_magic((uint32_t)p->ws, &a.ws_mul, &a.ws_shift);
   division_magic((uint32_t)hws, &a.hws_mul, &a.hws_shift);
+  division_magic((uint32_t)(p->hr * p->ws), &a.hrws_mul, &a.hrws_shift);
   a.direct_out = p->direct_out;
   a.direct = p->direct;
   // chunks in order: the first writes the fp32 gradient, the rest add to it

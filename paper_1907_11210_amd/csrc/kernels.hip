@@ -2806,6 +2806,26 @@ __device__ __forceinline__ size_t wgrad_a_stage(const WgArgs& a, int ks, int kc,
   return ((size_t)il * a.ms * hws + (k - il * hws)) * esz;
 }
 
+// Byte offsets of the GEMM's Bt operand: column c = (n, tap), and K stage
+// ks.  Per-tap rows: row c of kp elements.  Phase planes (a.bt_phase, hs*ws
+// a multiple of 64 so that a stage lies in one image): tap (kh, kw) of n
+// reads plane (ph, kw) of n from row sh - sh_min of each image's hr rows.
+__device__ __forceinline__ size_t wgrad_b_row(const WgArgs& a, int c, int esz) {
+  if (!a.bt_phase) return (size_t)c * a.kp * esz;
+  const int n = c / a.g_taps, tap = c - n * a.g_taps, kh = tap / a.g_s, kw = tap - kh * a.g_s;
+  const int rs = kh * a.dil_h - a.pad_h;
+  const int sh = floor_div_d(rs, a.stride_h), ph = rs - sh * a.stride_h;
+  const size_t rowlen = (size_t)a.nimg * a.hr * a.ws;
+  return (((size_t)n * a.stride_h * a.g_s + ph * a.g_s + kw) * rowlen + (size_t)(sh - a.sh_min) * a.ws) *
+         esz;
+}
+__device__ __forceinline__ size_t wgrad_b_stage(const WgArgs& a, int ks, int kc, int esz) {
+  if (!a.bt_phase) return (size_t)ks * kc * esz;
+  const uint32_t k = (uint32_t)ks * kc, hws = (uint32_t)a.hs * a.ws;
+  const uint32_t il = fast_div(k, a.hws_mul, a.hws_shift);
+  return ((size_t)il * a.hr * a.ws + (k - il * hws)) * esz;
+}
+
 // Tile of a weight-gradient GEMM workgroup: the grid's (m block, n block,
 // tap + taps * split) in that order of the linear workgroup index, each XCD
 // taking a contiguous run of it (xcd_remap), so that the m blocks that read
@@ -2847,13 +2867,13 @@ __global__ __launch_bounds__(256) void wgrad_gemm_kernel(WgArgs a) {
   const char* const bt = (const char*)a.bt;
   const size_t a0 = wgrad_a_row(a, min(m0 + row, a.ms - 1), ESZ) + chunk * 16;
   const size_t a1 = wgrad_a_row(a, min(m0 + row + 32, a.ms - 1), ESZ) + chunk * 16;
-  const size_t b0 = ((size_t)tap * a.nb + min(n0 + row, a.nb - 1)) * a.kp * ESZ + chunk * 16;
-  const size_t b1 = ((size_t)tap * a.nb + min(n0 + row + 32, a.nb - 1)) * a.kp * ESZ + chunk * 16;
+  const size_t b0 = wgrad_b_row(a, tap * a.nb + min(n0 + row, a.nb - 1), ESZ) + chunk * 16;
+  const size_t b1 = wgrad_b_row(a, tap * a.nb + min(n0 + row + 32, a.nb - 1), ESZ) + chunk * 16;
   struct Regs {
     uint4 a0, a1, b0, b1;
   };
   auto load = [&](int ks) {
-    const size_t off = (size_t)ks * KB, aoff = wgrad_a_stage(a, ks, KC, ESZ);
+    const size_t off = wgrad_b_stage(a, ks, KC, ESZ), aoff = wgrad_a_stage(a, ks, KC, ESZ);
     Regs r;
     r.a0 = *(const uint4*)(st + a0 + aoff);
     r.a1 = *(const uint4*)(st + a1 + aoff);
@@ -2966,13 +2986,13 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm2_kernel(WgArgs a) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     ao[j] = wgrad_a_row(a, min(m0 + row + 32 * j, a.ms - 1), ESZ) + chunk * 16;
-    bo[j] = ((size_t)tap * a.nb + min(n0 + row + 32 * j, a.nb - 1)) * a.kp * ESZ + chunk * 16;
+    bo[j] = wgrad_b_row(a, tap * a.nb + min(n0 + row + 32 * j, a.nb - 1), ESZ) + chunk * 16;
   }
   struct Regs {
     uint4 a[4], b[4];
   };
   auto load = [&](int ks, Regs& r) {
-    const size_t off = (size_t)ks * KB, aoff = wgrad_a_stage(a, ks, KC, ESZ);
+    const size_t off = wgrad_b_stage(a, ks, KC, ESZ), aoff = wgrad_a_stage(a, ks, KC, ESZ);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       r.a[j] = *(const uint4*)(st + ao[j] + aoff);
@@ -3179,6 +3199,41 @@ __global__ __launch_bounds__(256) void wgrad_gather_kernel(WgArgs a) {
   // every tap's row: consecutive lanes hold consecutive k, so both the LDS
   // reads (stride-apart pixels of one row) and the row stores coalesce
   constexpr int EPT = 4 / (int)sizeof(T);
+  if (a.bt_phase) {
+    // phase planes: rows (n, ph * s + kw), each image hr rows of ws (the
+    // block's images are a contiguous run of each row; ws is a multiple of 8)
+    const int hrws = a.hr * a.ws, np = a.stride_h * a.s;
+    const int kb0 = il0 * hrws, kb1 = (il0 + nim) * hrws;
+    const size_t rowlen = (size_t)a.nimg * hrws;
+    T* const bp0 = (T*)a.bt + (size_t)n * np * rowlen;
+    for (int k0 = kb0 + EPT * (int)threadIdx.x; k0 < kb1; k0 += EPT * 256) {
+      int base[EPT], rh[EPT], bw[EPT];
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) {
+        const int k = k0 + e;
+        const int il = (int)fast_div((uint32_t)k, a.hrws_mul, a.hrws_shift), q = k - il * hrws;
+        const int qh = (int)fast_div((uint32_t)q, a.ws_mul, a.ws_shift), qw = q - qh * a.ws;
+        rh[e] = (qh + a.sh_min) * a.stride_h;
+        bw[e] = qw * a.stride_w - a.pad_w;
+        base[e] = (il - il0) * plane;
+      }
+      T* dst = bp0 + k0;
+      for (int ph = 0; ph < a.stride_h; ++ph)
+        for (int kw = 0; kw < a.s; ++kw, dst += rowlen) {
+          T v[EPT];
+#pragma unroll
+          for (int e = 0; e < EPT; ++e) {
+            const int ih = rh[e] + ph, iw = bw[e] + kw * a.dil_w;
+            const bool in = (unsigned)ih < (unsigned)a.hb && (unsigned)iw < (unsigned)a.wb;
+            v[e] = in ? s_pl[base[e] + ih * a.wb + iw] : T(0);
+          }
+          uint32_t u;
+          __builtin_memcpy(&u, v, 4);
+          *(uint32_t*)dst = u;
+        }
+    }
+    return;
+  }
   const int kbeg = il0 * hws, kreal = a.nimg * hws;
   const int kend = il0 + nim >= a.nimg ? a.kp : kbeg + nim * hws;
   const size_t row_stride = (size_t)a.kp;  // rows (n, tap): the taps of n in order
@@ -3238,6 +3293,8 @@ hipError_t launch_wgrad_stage(const WgArgs& a, int dtype, hipStream_t stream) {
 
 hipError_t launch_wgrad_gemm(const WgArgs& a0, int dtype, hipStream_t stream) {
   WgArgs a = a0;  // one GEMM of N = nb * taps (Bt's rows (n, tap) in order)
+  a.g_taps = a.r * a.s;
+  a.g_s = a.s;
   a.nb *= a.r * a.s;
   a.r = a.s = 1;
   const int t = wgrad_tile(a.ms, a.nb);

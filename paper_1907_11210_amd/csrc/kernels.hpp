@@ -409,6 +409,18 @@ struct WgArgs {
   // is not staged
   int direct;
   uint32_t hws_mul, hws_shift;  // floor(v / (hs*ws)) (division_magic)
+  // Bt in phase planes (bt_phase): row (n, plane = ph * s + kw) holds, per
+  // image of the chunk, hr rows of ws elements, element (i', j) = big[n][(i'
+  // + sh_min) * stride_h + ph][j * stride_w + kw * dil_w - pad_w] (zero
+  // outside).  Tap (kh, kw), whose big row for small row i is (i + sh) *
+  // stride_h + ph with kh * dil_h - pad_h = sh * stride_h + ph, reads plane
+  // (ph, kw) from row i + sh - sh_min: the taps that differ only in their row
+  // shift share one copy, and a row shift is a whole-row offset in K.
+  int bt_phase;
+  int hr, sh_min;
+  uint32_t hrws_mul, hrws_shift;  // floor(v / (hr*ws)) (division_magic)
+  int g_taps, g_s;                // the layer's taps and kernel width (the
+                                  // GEMM launch folds r, s into nb)
 };
 // Output tile of the weight-gradient GEMM (square, channels of the small x
 // the large tensor): 128 x 128 when both channel counts reach 128, else 64.

@@ -145,6 +145,24 @@ def test_weight_gradient_in_place_and_direct_out_forms(case, monkeypatch):
         assert np.array_equal(outs[0], o)
 
 
+@pytest.mark.parametrize("case", [CASES[0], CASES[5], CASES[8], CASES[13], CASES[14], CASES[15]],
+                         ids=lambda c: c[0])
+def test_weight_gradient_phase_planes(case, monkeypatch):
+    """The large tensor's copies as phase planes with halo rows (the taps
+    that differ only in their row shift read one plane at different row
+    offsets) or one copy per tap (HUGE2_WGRAD_PHASE=0): both match the
+    oracle and give the same bits (the same values in the same K order)."""
+    P.say("case", case, "phase planes / per-tap copies")
+    xq, dyq = _inputs(case, seed=15)
+    ref, absref = _oracle(case, xq, dyq), _oracle(case, xq, dyq, absolute=True)
+    got = _gpu(case, xq, dyq)
+    P.check(got, ref, absref, case[-1], case[0] + " phase planes")
+    monkeypatch.setenv("HUGE2_WGRAD_PHASE", "0")
+    per_tap = _gpu(case, xq, dyq)
+    P.check(per_tap, ref, absref, case[-1], case[0] + " per-tap copies")
+    assert np.array_equal(got, per_tap)
+
+
 def test_weight_gradient_plan_reuse():
     """One plan, two calls on different data: each matches the oracle."""
     case = CASES[2]

@@ -275,10 +275,12 @@ huge2_status huge2_group_destroy(huge2_group* group);
  * (The data gradients are the other form: dx of a transposed conv is the
  * strided conv of dy with the same w, and dx of a strided conv is the
  * transposed conv of dy; both are the entry points above.)
- * How: per kernel tap, the large tensor (dy for the transposed conv, x for
- * the strided conv) is gathered onto the small tensor's pixel grid -- one
- * untangled copy per tap, as the paper's C copies of each derivative map --
- * and the gradient of all taps is then one dense MFMA GEMM over pixels with
+ * How: the large tensor (dy for the transposed conv, x for the strided
+ * conv) is gathered onto the small tensor's pixel grid -- untangled copies,
+ * as the paper's C copies of each derivative map: one per tap, or one per
+ * (row phase, kernel column) with halo rows, shared by the taps that differ
+ * only in their row shift -- and the gradient of all taps is then one dense
+ * MFMA GEMM over pixels with
  * no zero products (its columns are the (channel, tap) pairs, dw's own
  * order), accumulated in fp32 over K slices and chunks of images in a fixed
  * order and rounded once to the dtype.

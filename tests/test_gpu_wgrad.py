@@ -38,6 +38,9 @@ CASES = [
     ("ct_wide_dil_op", True, 2, 128, 8, 8, 128, 3, 3, 2, 2, 1, 2, "bf16"),
     ("conv_wide", False, 2, 144, 16, 16, 136, 4, 4, 2, 1, 0, 1, "bf16"),
     ("conv_wide_pad0", False, 1, 128, 18, 34, 128, 3, 3, 2, 0, 0, 1, "bf16"),
+    # fp32 on the phase planes (8x8 small grid, planes of 10 rows) with the
+    # GEMM writing dw itself
+    ("ct_f32_phase", True, 2, 32, 8, 8, 24, 4, 4, 2, 1, 0, 1, "f32"),
 ]
 
 
@@ -145,8 +148,8 @@ def test_weight_gradient_in_place_and_direct_out_forms(case, monkeypatch):
         assert np.array_equal(outs[0], o)
 
 
-@pytest.mark.parametrize("case", [CASES[0], CASES[5], CASES[8], CASES[13], CASES[14], CASES[15]],
-                         ids=lambda c: c[0])
+@pytest.mark.parametrize("case", [CASES[0], CASES[5], CASES[8], CASES[13], CASES[14], CASES[15],
+                                  CASES[17]], ids=lambda c: c[0])
 def test_weight_gradient_phase_planes(case, monkeypatch):
     """The large tensor's copies as phase planes with halo rows (the taps
     that differ only in their row shift read one plane at different row

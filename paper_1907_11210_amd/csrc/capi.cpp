@@ -1770,7 +1770,7 @@ struct huge2_wgrad_plan {
   int hs, ws, hb, wb;  // small / big pixel grids
   int chunk;           // images per chunk
   int kp;              // padded K of a full chunk
-  int ksplit;          // K ranges per tap (workgroups along K)
+  int ksplit;          // K slices of the GEMM (workgroups along K)
   int groups;          // > 1: grouped conv (direct per-plane sums, no workspace)
   int direct_out;      // the GEMM writes dw (WgArgs::direct_out)
   int gather_ib;       // images per LDS-gather workgroup (0: the staging kernel gathers)

@@ -2695,9 +2695,9 @@ hipError_t launch_pack_weights(const void* w, void* wp, int dtype, bool transpos
 
 // ---------------------------------------------------------------------------
 // Weight gradient (section 3.2.3).  The error maps (or, for a strided conv,
-// the input) are untangled per tap into copies on the small tensor's pixel
-// grid, so that every tap's gradient is one dense GEMM over pixels with no
-// zero products; the GEMM then runs on MFMA with both operands K-contiguous.
+// the input) are untangled into copies on the small tensor's pixel grid, so
+// that every tap's gradient is a dense product over pixels with no zero
+// products; all taps run as one GEMM on MFMA with both operands K-contiguous.
 
 // Staging of one image chunk: St (the image and channel axes exchanged) and
 // Bt (the tap gather), zero up to kp.  A thread produces 8 consecutive k of

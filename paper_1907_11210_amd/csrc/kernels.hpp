@@ -376,15 +376,19 @@ hipError_t launch_taps_combine(const CombArgs& a, hipStream_t stream);
 // Weight gradient (training, section 3.2.3).  With the "small" tensor S on
 // the tap's pixel grid and the "big" tensor B read at position
 // q*stride - pad + k*dil of that grid (transposed conv: S = x, B = dy; strided
-// or dilated conv: S = dy, B = x), G[tap][m][n] = sum over (image, q) of
-// S[m][q] * B[n][tap position of q].  For one chunk of images:
-//  - wgrad_stage: St[m][k] = S[image][m][q] and Bt[tap][n][k] = B at the tap
-//    position (zero outside), k = local image * hws + q, zero up to kp (a
-//    multiple of 64): the untangled copies of the big tensor, one per tap;
-//  - wgrad_gemm: G[split][tap] (fp32) = (or +=) St Bt[tap]^T over the
-//    split's K range, on MFMA;
-//  - wgrad_store: dw[(m * nb + n) * taps + tap] = sum over the splits (in
-//    order) of G[split][tap][m][n], in the dtype.
+// or dilated conv: S = dy, B = x), dw[m][n][tap] = sum over (image, q) of
+// S[m][q] * B[n][tap position of q].  For one chunk of images, with
+// k = local image * hws + q (zero up to kp, a multiple of 64):
+//  - St[m][k] = S[image][m][q], read in place by the GEMM (direct) or
+//    staged by wgrad_stage;
+//  - Bt, the untangled copies of the big tensor (zero outside): one row per
+//    (n, tap) (wgrad_stage or wgrad_gather), or phase planes that the taps of
+//    one kernel column and row phase share (bt_phase, wgrad_gather);
+//  - wgrad_gemm: G[split][m][n * taps + tap] (fp32) = (or +=) St Bt^T over
+//    the split's K range, all taps in one GEMM on MFMA (or, direct_out, dw
+//    itself);
+//  - wgrad_store: dw = the sum over the splits (in a fixed order), in the
+//    dtype.
 struct WgArgs {
   const void* sm;  // small tensor [n][ms][hs][ws] (NCHW)
   const void* bg;  // big tensor [n][nb][hb][wb]
@@ -397,7 +401,7 @@ struct WgArgs {
   int stride_h, stride_w, pad_h, pad_w, dil_h, dil_w;
   int kp;          // padded K of the chunk (multiple of 64)
   int accumulate;  // 0: G = product, 1: G += product
-  int ksplit;      // K ranges per tap, each with its own fp32 slice of G
+  int ksplit;      // K slices of the GEMM, each with its own fp32 slice of G
   int groups;      // > 1: grouped conv (wgrad_grouped_kernel; st, bt and g unused)
   int gather_ib;   // > 0: Bt through LDS, workgroups of gather_ib images (wgrad_gather_kernel)
   uint32_t ws_mul, ws_shift;  // floor(v / ws) = (v * ws_mul) >> ws_shift (division_magic)

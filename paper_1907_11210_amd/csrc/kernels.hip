@@ -2353,16 +2353,34 @@ __global__ __launch_bounds__(kQuadThreads) void quad_kernel(QArgs a) {
       const int qh = qr / a.w, qw = qr - qh * a.w;
       pos[i] = (il * obh + 2 * qh + rho_h) * obw + 2 * qw + rho_w;
     }
+    if constexpr (NHWC) {
+      // rows 4g .. 4g + 3 of a lane are four consecutive channels of one
+      // output position: one 8-byte write of the packed pairs
 #pragma unroll
-    for (int j = 0; j < WCH; ++j)
+      for (int j = 0; j < WCH; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int ch = (hc * WCH + j) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        for (int g = 0; g < 4; ++g) {
+          const int ch = (hc * WCH + j) * 32 + 8 * g + 4 * (lane >> 5);
 #pragma unroll
-        for (int i = 0; i < NP; ++i)
-          so[NHWC ? pos[i] * PPITCH + ch : ch * cpo + pos[i]] =
-              f32_to_bf16_rne(activate(acc[j][i][r] + bv[j][r], a.act));
-      }
+          for (int i = 0; i < NP; ++i) {
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = activate(acc[j][i][4 * g + e] + bv[j][4 * g + e], a.act);
+            *(uint2*)(so + pos[i] * PPITCH + ch) =
+                make_uint2(pack_bf16x2_rne(v[0], v[1]), pack_bf16x2_rne(v[2], v[3]));
+          }
+        }
+    } else {
+#pragma unroll
+      for (int j = 0; j < WCH; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int ch = (hc * WCH + j) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+#pragma unroll
+          for (int i = 0; i < NP; ++i)
+            so[ch * cpo + pos[i]] = f32_to_bf16_rne(activate(acc[j][i][r] + bv[j][r], a.act));
+        }
+    }
   }
   __syncthreads();
   // Whole output rows: per (channel, image) the rows [2 qh0, 2 qh0 + obh)
